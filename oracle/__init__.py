@@ -1,0 +1,24 @@
+"""fp64 CPU oracle for the read-sparse readout and store-sparse commit.
+
+TEST INFRASTRUCTURE ONLY.  This package is the slow, plain definition of what
+the HIP path computes; it is imported only by the tests, by the smoke check
+and by the benchmark's CPU-baseline leg.  The product path never calls it and
+shares no code with it (neither imports the other).  Inputs come from the
+seeded generator in ``workloads``; every floating-point step runs in float64
+on values widened exactly from their stored bfloat16/float32 bits.
+
+Modules:
+  geometry  down-sampling, bounding boxes, Chebyshev dilation, tracker state
+            (Sec. 3.1, Eqs. 1, 2 and 5; Algorithm 1)
+  select    token energy and the read keep-set (Sec. 3.1, Eq. 4)
+  readout   the sparse memory readout with scatter (Sec. 3.1, Eq. 6)
+  bank      write compaction and the ring memory bank (Sec. 3.2, Eq. 8)
+
+Parity unpinned: absolute readout values at the workload sizes (the paper
+prints no tensors and its weights are not available); every other function is
+pinned by the tests in tests/test_oracle_*.py.
+"""
+from .geometry import Track, bbox, down_s, down_s_box, fill_box, dilate, prior_object  # noqa: F401
+from .select import energy, topk_keep, select_queries  # noqa: F401
+from .readout import project_bank, attention_weights, readout, readout_dense, attend  # noqa: F401
+from .bank import compact, RingBank, FrameListBank, RS3_OK, RS3_E_CAPACITY  # noqa: F401
