@@ -1,0 +1,202 @@
+/*
+ * rs3.h -- C ABI of the read-sparse memory readout and store-sparse commit
+ * (RS^3-Prune, Sec. 3.1 and Sec. 3.2) on AMD Instinct MI355X (gfx950).
+ *
+ * Three calls make up one frame of the method's hot path:
+ *   rs3_select_queries : per-object spatial prior from the previous masks
+ *                        (Eqs. 1, 2, 5) and the energy top-k keep-set inside
+ *                        it (Eq. 4)  -> ascending selected-query lists;
+ *   rs3_readout        : gather the selected query tokens, cross-attend them
+ *                        to the object's memory bank (Eq. 6) and scatter the
+ *                        result back; unselected rows pass through unchanged;
+ *   rs3_commit         : compact the memory-encoder tokens inside the mask
+ *                        (Eq. 8) into the object's ring memory bank.
+ *
+ * Conventions (every call):
+ *  - Tensor pointers are DEVICE pointers unless marked [host].  The caller
+ *    owns every tensor it passes and the stream; the library owns the memory
+ *    behind its handles (weights copy, banks, tracker state).
+ *  - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL = the
+ *    null stream).  Only the *_export, *_import and rs3_bank_error calls
+ *    synchronise.  Nothing is allocated inside select/readout/commit.
+ *  - Grids are m x n token cells, cell index i = y*n + x.  Per-object masks
+ *    are uint8 [(m*s) x (n*s)] pixel grids; cell (y, x) samples pixel
+ *    (y*s, x*s).  Any nonzero byte counts as set.
+ *  - Float tensors are bf16 (stored as 16-bit patterns) or fp32, one dtype per
+ *    layer: query tokens X, outputs Y, weights and the bank share it.  All
+ *    accumulation is fp32; token energies are fp64.
+ *  - Errors are return codes, never exceptions.  Problems visible on the host
+ *    (null pointers, bad sizes, dtype mismatches, pin misuse, workspace too
+ *    small) return RS3_E_INVALID before any device work and change no state.
+ *    Problems only the device can see (a bank frame that does not fit, a
+ *    selection list that is out of range or not ascending) set a sticky error
+ *    word in the affected bank; the failing operation leaves that bank
+ *    unchanged (commit) or skips the offending rows (readout).  The word keeps
+ *    the first error; rs3_bank_error reads it.  HIP failures map to
+ *    RS3_E_DEVICE (launch/copy) or RS3_E_OOM (allocation).
+ *  - A handle must not be used from two streams at once.
+ */
+#ifndef RS3_H
+#define RS3_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  RS3_OK = 0,
+  RS3_E_INVALID = 1,
+  RS3_E_CAPACITY = 2,
+  RS3_E_DEVICE = 3,
+  RS3_E_OOM = 4
+} rs3_status;
+
+typedef enum { RS3_F32 = 0, RS3_BF16 = 1 } rs3_dtype;
+
+/* Token grid m x n; masks are (m*s) x (n*s) pixels (s = encoder stride). */
+typedef struct {
+  int32_t m, n, s;
+} rs3_grid;
+
+/* Prior parameters (Sec. 3.1, Algorithm 1 hyper-parameters):
+ *   r_s            dilation radius in cells of the previous-mask prior (Eq. 2)
+ *   c              cap on the extra radius of the lost-object box fallback (Eq. 5)
+ *   seed_box       1: a non-empty mask contributes its dilated filled bounding
+ *                  box (the frame-0 seed prior, Eq. 1); 0: the dilated mask
+ *   union_objects  1: one keep-set for the union of all objects' priors (as in
+ *                  the paper); 0: one keep-set per object */
+typedef struct {
+  int32_t r_s, c, seed_box, union_objects;
+} rs3_select_params;
+
+#define RS3_MAX_OBJ 64          /* objects per call */
+#define RS3_MAX_MN 32768        /* token cells per grid */
+#define RS3_TRACK_WORDS 6       /* y0, x0, y1, x1, streak, has_box (pixels) */
+#define RS3_BANK_HDR_WORDS 8    /* exported header: n_frames, pin_end, err, ... */
+
+typedef struct rs3_track rs3_track; /* per-object tracker state, device resident */
+typedef struct rs3_layer rs3_layer; /* cross-attention weights and shape */
+typedef struct rs3_bank rs3_bank;   /* one object's ring memory bank */
+
+const char* rs3_status_str(rs3_status s);
+
+/* ---- tracker state (Sec. 3.1, streak-counted box fallback, Eq. 5) --------
+ * Holds, per object, the last non-empty bounding box in pixel coordinates
+ * (inclusive), the count of consecutive empty frames and whether a box was
+ * ever seen.  Created zeroed (no box).  export/import copy
+ * int32 [n_obj][RS3_TRACK_WORDS] host arrays and synchronise the device. */
+rs3_status rs3_track_create(int32_t n_obj, rs3_track** out);
+void rs3_track_destroy(rs3_track* t);
+rs3_status rs3_track_export(const rs3_track* t, int32_t* state /*[host]*/);
+rs3_status rs3_track_import(rs3_track* t, const int32_t* state /*[host]*/);
+
+/* ---- layer (one cross-attention of the memory readout, Eq. 6) -------------
+ * C: query token width; H heads of width d_h with D = H*d_h = C; d_kv: width
+ * of the bank's raw key/value tokens.  Weights are [host] row-major arrays in
+ * dtype `dt`: Wq [C][D], Wk [d_kv][D], Wv [d_kv][D], Wo [D][C]; the library
+ * copies them (into its own device layouts).  d_h must be 32, 64, 128 or 256
+ * for bf16 and at most 256 for fp32; C <= 1024; d_kv <= 256, multiple of 16. */
+rs3_status rs3_layer_create(int32_t C, int32_t H, int32_t d_kv, rs3_dtype dt,
+                            const void* Wq, const void* Wk, const void* Wv,
+                            const void* Wo, rs3_layer** out);
+void rs3_layer_destroy(rs3_layer* L);
+
+/* ---- bank (Sec. 3.2; placement rule below) --------------------------------
+ * A ring of `cap` token rows holding at most `f_max` frames, of which the
+ * first commits (at most n_pin, all before any unpinned commit) may be pinned.
+ * Pinned frames are laid out from row 0 and never evicted.  An unpinned frame
+ * of L kept tokens: (1) L > cap - pin_end -> RS3_E_CAPACITY, bank unchanged;
+ * (2) while f_max frames are resident evict the oldest unpinned frame;
+ * (3) start = end of the newest unpinned frame (pin_end if none), or pin_end
+ * if start + L > cap; (4) evict unpinned frames oldest first until none
+ * overlaps [start, start+L); (5) store rows and record (start, L, t, pinned).
+ * Zero-length frames are recorded.  The bank stores the raw K/V rows, the
+ * kept cell index (`pos`) per row, and the rows projected by W_k / W_v of
+ * the layer it was created for (which must outlive it).
+ * Requires 0 <= n_pin < f_max <= 256, 1 <= cap <= 2^26. */
+rs3_status rs3_bank_create(const rs3_layer* L, int32_t cap, int32_t f_max,
+                           int32_t n_pin, rs3_bank** out);
+void rs3_bank_destroy(rs3_bank* b);
+
+/* Bank snapshot in key order (pinned frames, then unpinned oldest->newest).
+ * hdr [host, RS3_BANK_HDR_WORDS]: n_frames, pin_end, err, n_keys, rest 0.
+ * frames [host, f_max][4]: start, length, t, pinned (first n_frames rows).
+ * K, V [host, cap][d_kv] (dtype bytes) and pos [host, cap]: resident rows
+ * concatenated in key order (first n_keys rows); any may be NULL.
+ * Synchronises the device. */
+rs3_status rs3_bank_export(const rs3_bank* b, int32_t* hdr, int32_t* frames,
+                           void* K, void* V, int32_t* pos);
+/* Read (and optionally clear) the sticky device error word.  Synchronises. */
+rs3_status rs3_bank_error(rs3_bank* b, int32_t* err /*[host]*/, int32_t clear);
+
+/* ---- select_queries (Sec. 3.1: Eqs. 1, 2, 4, 5; Algorithm 1) --------------
+ * masks  : uint8 [n_obj][m*s][n*s], each object's previous-frame mask
+ * tr     : tracker state for n_obj objects, updated in place (box, streak)
+ * X      : [n_x][m*n][C] query tokens in `dt`; x_obj_stride (elements) = 0
+ *          when all objects share one grid, else the per-object stride (then
+ *          p->union_objects must be 0 or n_obj 1)
+ * k      : [host][n_groups] keep budgets floor(rho*mn), computed exactly by
+ *          the caller; n_groups = 1 if union_objects else n_obj
+ * ws     : device workspace of at least rs3_select_workspace_size() bytes
+ * sel_idx: out int32 [n_groups][m*n]; the first sel_count[g] entries of row g
+ *          are the kept cells in ascending order: all of the prior P_g if
+ *          |P_g| <= k[g], otherwise the k[g] cells of P_g with the largest
+ *          energy sum_c x_{i,c}^2 (fp64, channels added in ascending order),
+ *          ties to the lower cell index
+ * sel_count : out int32 [n_groups]
+ * prior_out : optional out uint8 [n_groups][m*n], the prior bitmap P_g */
+rs3_status rs3_select_workspace_size(const rs3_grid* g, int32_t n_obj,
+                                     int64_t x_obj_stride, size_t* bytes);
+rs3_status rs3_select_queries(const rs3_grid* g, int32_t n_obj, const uint8_t* masks,
+                              rs3_track* tr, const void* X, int64_t x_obj_stride,
+                              int32_t C, rs3_dtype dt, const int32_t* k,
+                              const rs3_select_params* p, void* ws, size_t ws_bytes,
+                              int32_t* sel_idx, int32_t* sel_count, uint8_t* prior_out,
+                              void* stream);
+
+/* ---- readout (Sec. 3.1, Eq. 6 with the residual reading) -------------------
+ * For object o with selection list sel (row o of sel_idx, or row 0 when
+ * sel_stride == 0) and bank banks[o] of N resident keys:
+ *   y_i = x_i + [softmax(q_h K^_h^T / sqrt(d_h)) V^_h]_h W_o,  q = x_i W_q,
+ *         for every selected cell i;
+ *   y_i = x_i bit for bit for every other cell, and for all cells if N = 0.
+ * X      : [n_x][m*n][C] (x_obj_stride as in select)
+ * sel_idx/sel_count : as produced by rs3_select_queries; sel_stride = m*n
+ *          for per-object lists or 0 for one shared list
+ * max_sel: upper bound on every sel_count used (host grid size), <= m*n
+ * n_splits: key splits per query tile (0 = automatic)
+ * Y      : [n_obj][m*n][C] with stride y_obj_stride (elements); may equal X
+ *          (in place) only when n_obj == 1 or X is per object with the same
+ *          stride.  y_fp32 = 1 writes Y as fp32 for diagnostics (never in
+ *          place), otherwise Y has the layer dtype.
+ * ws     : device workspace of at least rs3_readout_workspace_size() bytes */
+rs3_status rs3_readout_workspace_size(const rs3_layer* L, int32_t n_obj, int32_t max_sel,
+                                      int32_t n_splits, size_t* bytes);
+rs3_status rs3_readout(const rs3_layer* L, const rs3_grid* g, int32_t n_obj,
+                       const void* X, int64_t x_obj_stride, rs3_bank* const* banks /*[host]*/,
+                       const int32_t* sel_idx, const int32_t* sel_count, int32_t sel_stride,
+                       int32_t max_sel, int32_t n_splits, void* Y, int64_t y_obj_stride,
+                       int32_t y_fp32, void* ws, size_t ws_bytes, void* stream);
+
+/* ---- commit (Sec. 3.2, Eq. 8 and the sparse write of Algorithm 1) ----------
+ * For each object o: kept = ascending cells set in masks[o] (sampled at
+ * stride s); if kept_count < fall_min or > fall_max all m*n cells are kept
+ * (the dense fall-through; pass 0 and m*n to disable).  The kept rows of
+ * Kmem[o], Vmem[o] ([m*n][d_kv] each, object stride kv_obj_stride elements)
+ * are appended to banks[o] as frame t by the placement rule of
+ * rs3_bank_create, together with their projections by W_k and W_v.
+ * pin = 1 marks a pinned frame (host-checked: only before any unpinned commit
+ * and at most n_pin times per bank).  kept_count: optional device out
+ * int32 [n_obj]. */
+rs3_status rs3_commit(rs3_bank* const* banks /*[host]*/, int32_t n_obj, const rs3_grid* g,
+                      const void* Kmem, const void* Vmem, int64_t kv_obj_stride,
+                      const uint8_t* masks, int32_t t, int32_t pin, int32_t fall_min,
+                      int32_t fall_max, int32_t* kept_count, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* RS3_H */

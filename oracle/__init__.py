@@ -21,4 +21,4 @@ pinned by the tests in tests/test_oracle_*.py.
 from .geometry import Track, bbox, down_s, down_s_box, fill_box, dilate, prior_object  # noqa: F401
 from .select import energy, topk_keep, select_queries  # noqa: F401
 from .readout import project_bank, attention_weights, readout, readout_dense, attend  # noqa: F401
-from .bank import compact, RingBank, FrameListBank, RS3_OK, RS3_E_CAPACITY  # noqa: F401
+from .bank import compact, RingBank, FrameListBank, RS3_OK, RS3_E_INVALID, RS3_E_CAPACITY  # noqa: F401

@@ -1,0 +1,14 @@
+"""MI355X (gfx950) read-sparse memory readout and store-sparse commit.
+
+Python binding of the rs3 C ABI (include/rs3.h).  Every step of the path runs
+in the HIP kernels of librs3.so; this package only marshals arguments.  It
+fails loudly when the library is missing: there is no fallback.
+"""
+from ._binding import (  # noqa: F401
+    RS3_OK, RS3_E_INVALID, RS3_E_CAPACITY, RS3_E_DEVICE, RS3_E_OOM,
+    RS3_F32, RS3_BF16, RS3_MAX_OBJ, RS3_MAX_MN, RS3_TRACK_WORDS, RS3_BANK_HDR_WORDS,
+    Rs3Error, lib, lib_path, exported_symbols, Grid, SelectParams,
+    Track, Layer, Bank,
+    select_workspace_size, select_queries,
+    readout_workspace_size, readout, commit,
+)

@@ -1,0 +1,233 @@
+"""ctypes binding of librs3.so (argument marshalling only).
+
+Tensors are torch tensors on the GPU (their data_ptr() is passed); host-side
+arrays are numpy.  `stream=None` means torch's current stream.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+RS3_OK, RS3_E_INVALID, RS3_E_CAPACITY, RS3_E_DEVICE, RS3_E_OOM = 0, 1, 2, 3, 4
+RS3_F32, RS3_BF16 = 0, 1
+RS3_MAX_OBJ = 64
+RS3_MAX_MN = 32768
+RS3_TRACK_WORDS = 6
+RS3_BANK_HDR_WORDS = 8
+
+lib_path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librs3.so")
+
+c_i32, c_i64, c_sz, c_vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_void_p
+P_i32 = ctypes.POINTER(ctypes.c_int32)
+
+
+class Grid(ctypes.Structure):
+    _fields_ = [("m", c_i32), ("n", c_i32), ("s", c_i32)]
+
+
+class SelectParams(ctypes.Structure):
+    _fields_ = [("r_s", c_i32), ("c", c_i32), ("seed_box", c_i32), ("union_objects", c_i32)]
+
+
+class Rs3Error(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__("%s failed: %s (%d)" % (what, _status_str(status), status))
+
+
+_SIGS = {
+    "rs3_status_str": (ctypes.c_char_p, [c_i32]),
+    "rs3_track_create": (c_i32, [c_i32, ctypes.POINTER(c_vp)]),
+    "rs3_track_destroy": (None, [c_vp]),
+    "rs3_track_export": (c_i32, [c_vp, c_vp]),
+    "rs3_track_import": (c_i32, [c_vp, c_vp]),
+    "rs3_layer_create": (c_i32, [c_i32, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp, c_vp, ctypes.POINTER(c_vp)]),
+    "rs3_layer_destroy": (None, [c_vp]),
+    "rs3_bank_create": (c_i32, [c_vp, c_i32, c_i32, c_i32, ctypes.POINTER(c_vp)]),
+    "rs3_bank_destroy": (None, [c_vp]),
+    "rs3_bank_export": (c_i32, [c_vp, c_vp, c_vp, c_vp, c_vp, c_vp]),
+    "rs3_bank_error": (c_i32, [c_vp, c_vp, c_i32]),
+    "rs3_select_workspace_size": (c_i32, [ctypes.POINTER(Grid), c_i32, c_i64, ctypes.POINTER(c_sz)]),
+    "rs3_select_queries": (c_i32, [ctypes.POINTER(Grid), c_i32, c_vp, c_vp, c_vp, c_i64, c_i32, c_i32, c_vp,
+                                   ctypes.POINTER(SelectParams), c_vp, c_sz, c_vp, c_vp, c_vp, c_vp]),
+    "rs3_readout_workspace_size": (c_i32, [c_vp, c_i32, c_i32, c_i32, ctypes.POINTER(c_sz)]),
+    "rs3_readout": (c_i32, [c_vp, ctypes.POINTER(Grid), c_i32, c_vp, c_i64, c_vp, c_vp, c_vp, c_i32, c_i32,
+                            c_i32, c_vp, c_i64, c_i32, c_vp, c_sz, c_vp]),
+    "rs3_commit": (c_i32, [c_vp, c_i32, ctypes.POINTER(Grid), c_vp, c_vp, c_i64, c_vp, c_i32, c_i32, c_i32,
+                           c_i32, c_vp, c_vp]),
+}
+
+_lib = None
+
+
+def lib():
+    """Load librs3.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(lib_path):
+            raise RuntimeError("librs3.so is not built; run `python -m paper_2608_22526_amd.build`")
+        L = ctypes.CDLL(lib_path)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def exported_symbols():
+    return list(_SIGS)
+
+
+def _status_str(s: int) -> str:
+    try:
+        return lib().rs3_status_str(int(s)).decode()
+    except Exception:  # library not loadable
+        return "status"
+
+
+def _check(status: int, what: str):
+    if status != RS3_OK:
+        raise Rs3Error(status, what)
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, np.ndarray):
+        return t.ctypes.data
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is not None:
+        return stream
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+# ---------------------------------------------------------------------------
+class Track:
+    """rs3_track: per-object (box, streak, has_box) state."""
+
+    def __init__(self, n_obj: int):
+        h = c_vp()
+        _check(lib().rs3_track_create(n_obj, ctypes.byref(h)), "rs3_track_create")
+        self.h, self.n_obj = h, n_obj
+
+    def export(self) -> np.ndarray:
+        out = np.zeros((self.n_obj, RS3_TRACK_WORDS), np.int32)
+        _check(lib().rs3_track_export(self.h, out.ctypes.data), "rs3_track_export")
+        return out
+
+    def import_(self, state: np.ndarray):
+        st = np.ascontiguousarray(state, dtype=np.int32)
+        _check(lib().rs3_track_import(self.h, st.ctypes.data), "rs3_track_import")
+
+    def __del__(self):
+        if getattr(self, "h", None) and _lib is not None:
+            _lib.rs3_track_destroy(self.h)
+            self.h = None
+
+
+class Layer:
+    """rs3_layer: W_q [C][D], W_k/W_v [d_kv][D], W_o [D][C] host arrays
+    (uint16 bf16 bits or float32)."""
+
+    def __init__(self, C: int, H: int, d_kv: int, dtype: int, Wq, Wk, Wv, Wo):
+        arrs = [np.ascontiguousarray(w) for w in (Wq, Wk, Wv, Wo)]
+        h = c_vp()
+        _check(lib().rs3_layer_create(C, H, d_kv, dtype, *(a.ctypes.data for a in arrs), ctypes.byref(h)),
+               "rs3_layer_create")
+        self.h, self.C, self.H, self.d_kv, self.dtype = h, C, H, d_kv, dtype
+
+    def __del__(self):
+        if getattr(self, "h", None) and _lib is not None:
+            _lib.rs3_layer_destroy(self.h)
+            self.h = None
+
+
+class Bank:
+    """rs3_bank: one object's ring bank for `layer`."""
+
+    def __init__(self, layer: Layer, cap: int, f_max: int, n_pin: int):
+        h = c_vp()
+        _check(lib().rs3_bank_create(layer.h, cap, f_max, n_pin, ctypes.byref(h)), "rs3_bank_create")
+        self.h, self.layer, self.cap, self.f_max, self.n_pin = h, layer, cap, f_max, n_pin
+
+    def export(self):
+        es = 2 if self.layer.dtype == RS3_BF16 else 4
+        npdt = np.uint16 if es == 2 else np.float32
+        hdr = np.zeros(RS3_BANK_HDR_WORDS, np.int32)
+        frames = np.zeros((self.f_max, 4), np.int32)
+        K = np.zeros((self.cap, self.layer.d_kv), npdt)
+        V = np.zeros((self.cap, self.layer.d_kv), npdt)
+        pos = np.zeros(self.cap, np.int32)
+        _check(lib().rs3_bank_export(self.h, hdr.ctypes.data, frames.ctypes.data, K.ctypes.data,
+                                     V.ctypes.data, pos.ctypes.data), "rs3_bank_export")
+        nf, nk = int(hdr[0]), int(hdr[3])
+        return dict(hdr=hdr, n_frames=nf, pin_end=int(hdr[1]), err=int(hdr[2]), n_keys=nk,
+                    frames=frames[:nf].copy(), K=K[:nk].copy(), V=V[:nk].copy(), pos=pos[:nk].copy())
+
+    def error(self, clear: bool = False) -> int:
+        e = np.zeros(1, np.int32)
+        _check(lib().rs3_bank_error(self.h, e.ctypes.data, int(clear)), "rs3_bank_error")
+        return int(e[0])
+
+    def __del__(self):
+        if getattr(self, "h", None) and _lib is not None:
+            _lib.rs3_bank_destroy(self.h)
+            self.h = None
+
+
+def _grid(g) -> Grid:
+    if isinstance(g, Grid):
+        return g
+    m, n, s = g
+    return Grid(m, n, s)
+
+
+def select_workspace_size(grid, n_obj: int, x_obj_stride: int) -> int:
+    out = c_sz()
+    _check(lib().rs3_select_workspace_size(ctypes.byref(_grid(grid)), n_obj, x_obj_stride, ctypes.byref(out)),
+           "rs3_select_workspace_size")
+    return out.value
+
+
+def select_queries(grid, n_obj: int, masks, track: Track, X, x_obj_stride: int, C: int, dtype: int,
+                   k: Sequence[int], params: SelectParams, ws, sel_idx, sel_count, prior_out=None,
+                   stream=None):
+    karr = np.ascontiguousarray(np.asarray(k, dtype=np.int32))
+    _check(lib().rs3_select_queries(ctypes.byref(_grid(grid)), n_obj, _ptr(masks), track.h, _ptr(X),
+                                    x_obj_stride, C, dtype, karr.ctypes.data, ctypes.byref(params), _ptr(ws),
+                                    ws.numel() * ws.element_size(), _ptr(sel_idx), _ptr(sel_count),
+                                    _ptr(prior_out), _stream(stream)), "rs3_select_queries")
+
+
+def readout_workspace_size(layer: Layer, n_obj: int, max_sel: int, n_splits: int = 0) -> int:
+    out = c_sz()
+    _check(lib().rs3_readout_workspace_size(layer.h, n_obj, max_sel, n_splits, ctypes.byref(out)),
+           "rs3_readout_workspace_size")
+    return out.value
+
+
+def readout(layer: Layer, grid, n_obj: int, X, x_obj_stride: int, banks: Sequence[Bank], sel_idx, sel_count,
+            sel_stride: int, max_sel: int, n_splits: int, Y, y_obj_stride: int, y_fp32: int = 0, ws=None,
+            stream=None):
+    harr = (c_vp * len(banks))(*[b.h for b in banks])
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(lib().rs3_readout(layer.h, ctypes.byref(_grid(grid)), n_obj, _ptr(X), x_obj_stride,
+                             ctypes.cast(harr, c_vp), _ptr(sel_idx), _ptr(sel_count), sel_stride, max_sel,
+                             n_splits, _ptr(Y), y_obj_stride, y_fp32, _ptr(ws), ws_bytes, _stream(stream)),
+           "rs3_readout")
+
+
+def commit(banks: Sequence[Bank], grid, Kmem, Vmem, kv_obj_stride: int, masks, t: int, pin: int,
+           fall_min: int, fall_max: int, kept_count=None, stream=None):
+    harr = (c_vp * len(banks))(*[b.h for b in banks])
+    _check(lib().rs3_commit(ctypes.cast(harr, c_vp), len(banks), ctypes.byref(_grid(grid)), _ptr(Kmem),
+                            _ptr(Vmem), kv_obj_stride, _ptr(masks), t, pin, fall_min, fall_max,
+                            _ptr(kept_count), _stream(stream)), "rs3_commit")

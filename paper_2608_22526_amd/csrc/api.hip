@@ -1,0 +1,496 @@
+// Host side of the rs3 C ABI: handle management, argument validation and
+// kernel launches.  Every check that can be made on the host runs before any
+// HIP call, so a rejected call leaves all state untouched.
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <vector>
+
+#include "rs3_internal.h"
+
+using namespace rs3;
+
+struct rs3_track {
+  int32_t n_obj;
+  int32_t* d_state;  // [n_obj][RS3_TRACK_WORDS]
+};
+
+struct rs3_layer {
+  LayerDev dev;  // host copy holding device pointers
+};
+
+struct rs3_bank {
+  const rs3_layer* L;
+  BankDev host;     // host copy holding device pointers
+  BankDev* d_desc;  // device copy of `host`
+  int32_t pin_calls;
+  int32_t unpinned_seen;
+};
+
+namespace {
+
+size_t dtype_size(int dt) { return dt == RS3_BF16 ? 2 : 4; }
+
+rs3_status map_err(hipError_t e) {
+  if (e == hipSuccess) return RS3_OK;
+  if (e == hipErrorOutOfMemory) return RS3_E_OOM;
+  return RS3_E_DEVICE;
+}
+
+bool setup_done = false;
+
+rs3_status ensure_setup() {
+  if (setup_done) return RS3_OK;
+  hipError_t e = rs3_readout_setup();
+  if (e == hipSuccess) e = rs3_select_setup();
+  if (e != hipSuccess) return RS3_E_DEVICE;
+  setup_done = true;
+  return RS3_OK;
+}
+
+bool grid_ok(const rs3_grid* g) {
+  if (!g || g->m <= 0 || g->n <= 0 || g->s <= 0) return false;
+  int64_t mn = (int64_t)g->m * g->n;
+  if (mn > RS3_MAX_MN) return false;
+  if ((int64_t)g->m * g->s * g->n * g->s > (1ll << 30)) return false;
+  return true;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Transpose a row-major [rows][cols] host matrix of `es`-byte elements.
+std::vector<uint8_t> transpose(const void* src, int rows, int cols, size_t es) {
+  std::vector<uint8_t> out((size_t)rows * cols * es);
+  const uint8_t* s = (const uint8_t*)src;
+  for (int r = 0; r < rows; ++r)
+    for (int c = 0; c < cols; ++c) memcpy(&out[((size_t)c * rows + r) * es], &s[((size_t)r * cols + c) * es], es);
+  return out;
+}
+
+int auto_splits(int n_obj, int H, int n_qt, int n_tiles_cap) {
+  const int base = n_obj * H * n_qt;
+  int S = (512 + base - 1) / base;
+  if (S > 64) S = 64;
+  int max_by_tiles = n_tiles_cap / 2;
+  if (max_by_tiles < 1) max_by_tiles = 1;
+  if (S > max_by_tiles) S = max_by_tiles;
+  if (S < 1) S = 1;
+  return S;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* rs3_status_str(rs3_status s) {
+  switch (s) {
+    case RS3_OK: return "ok";
+    case RS3_E_INVALID: return "invalid argument";
+    case RS3_E_CAPACITY: return "bank capacity exceeded";
+    case RS3_E_DEVICE: return "device error";
+    case RS3_E_OOM: return "out of device memory";
+  }
+  return "unknown status";
+}
+
+// ---- tracker ---------------------------------------------------------------
+rs3_status rs3_track_create(int32_t n_obj, rs3_track** out) {
+  if (!out || n_obj <= 0 || n_obj > RS3_MAX_OBJ) return RS3_E_INVALID;
+  *out = nullptr;
+  rs3_track* t = new rs3_track();
+  t->n_obj = n_obj;
+  size_t bytes = (size_t)n_obj * RS3_TRACK_WORDS * 4;
+  hipError_t e = hipMalloc((void**)&t->d_state, bytes);
+  if (e == hipSuccess) e = hipMemset(t->d_state, 0, bytes);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) {
+    if (t->d_state) (void)hipFree(t->d_state);
+    delete t;
+    return map_err(e);
+  }
+  *out = t;
+  return RS3_OK;
+}
+
+void rs3_track_destroy(rs3_track* t) {
+  if (!t) return;
+  (void)hipFree(t->d_state);
+  delete t;
+}
+
+rs3_status rs3_track_export(const rs3_track* t, int32_t* state) {
+  if (!t || !state) return RS3_E_INVALID;
+  hipError_t e = hipDeviceSynchronize();
+  if (e == hipSuccess)
+    e = hipMemcpy(state, t->d_state, (size_t)t->n_obj * RS3_TRACK_WORDS * 4, hipMemcpyDeviceToHost);
+  return map_err(e);
+}
+
+rs3_status rs3_track_import(rs3_track* t, const int32_t* state) {
+  if (!t || !state) return RS3_E_INVALID;
+  hipError_t e = hipDeviceSynchronize();
+  if (e == hipSuccess)
+    e = hipMemcpy(t->d_state, state, (size_t)t->n_obj * RS3_TRACK_WORDS * 4, hipMemcpyHostToDevice);
+  return map_err(e);
+}
+
+// ---- layer -----------------------------------------------------------------
+rs3_status rs3_layer_create(int32_t C, int32_t H, int32_t d_kv, rs3_dtype dt, const void* Wq,
+                            const void* Wk, const void* Wv, const void* Wo, rs3_layer** out) {
+  if (!out || !Wq || !Wk || !Wv || !Wo) return RS3_E_INVALID;
+  if (dt != RS3_BF16 && dt != RS3_F32) return RS3_E_INVALID;
+  if (C <= 0 || C > 1024 || H <= 0 || C % H != 0) return RS3_E_INVALID;
+  const int d_h = C / H;
+  if (d_kv <= 0 || d_kv > 256 || d_kv % 16 != 0) return RS3_E_INVALID;
+  if (dt == RS3_BF16) {
+    if (d_h != 32 && d_h != 64 && d_h != 128 && d_h != 256) return RS3_E_INVALID;
+    if (C % 64 != 0) return RS3_E_INVALID;
+  } else {
+    if (d_h > 256 || C % 8 != 0) return RS3_E_INVALID;
+  }
+  *out = nullptr;
+  const size_t es = dtype_size(dt);
+  const int D = C;
+  rs3_layer* L = new rs3_layer();
+  L->dev.C = C;
+  L->dev.H = H;
+  L->dev.d_h = d_h;
+  L->dev.D = D;
+  L->dev.d_kv = d_kv;
+  L->dev.dtype = dt;
+  std::vector<uint8_t> wq = transpose(Wq, C, D, es), wk = transpose(Wk, d_kv, D, es);
+  std::vector<uint8_t> wv = transpose(Wv, d_kv, D, es), wo = transpose(Wo, D, C, es);
+  void** dst[4] = {&L->dev.WqT, &L->dev.WkT, &L->dev.WvT, &L->dev.WoT};
+  std::vector<uint8_t>* src[4] = {&wq, &wk, &wv, &wo};
+  hipError_t e = hipSuccess;
+  for (int i = 0; i < 4 && e == hipSuccess; ++i) {
+    e = hipMalloc(dst[i], src[i]->size());
+    if (e == hipSuccess) e = hipMemcpy(*dst[i], src[i]->data(), src[i]->size(), hipMemcpyHostToDevice);
+  }
+  if (e != hipSuccess) {
+    for (int i = 0; i < 4; ++i)
+      if (*dst[i]) (void)hipFree(*dst[i]);
+    delete L;
+    return map_err(e);
+  }
+  *out = L;
+  return RS3_OK;
+}
+
+void rs3_layer_destroy(rs3_layer* L) {
+  if (!L) return;
+  (void)hipFree(L->dev.WqT);
+  (void)hipFree(L->dev.WkT);
+  (void)hipFree(L->dev.WvT);
+  (void)hipFree(L->dev.WoT);
+  delete L;
+}
+
+// ---- bank ------------------------------------------------------------------
+rs3_status rs3_bank_create(const rs3_layer* L, int32_t cap, int32_t f_max, int32_t n_pin,
+                           rs3_bank** out) {
+  if (!out || !L) return RS3_E_INVALID;
+  if (cap < 1 || cap > (1 << 26) || f_max < 1 || f_max > 256 || n_pin < 0 || n_pin >= f_max)
+    return RS3_E_INVALID;
+  *out = nullptr;
+  rs3_status st = ensure_setup();
+  if (st != RS3_OK) return st;
+  const LayerDev& ld = L->dev;
+  const size_t es = dtype_size(ld.dtype);
+  rs3_bank* b = new rs3_bank();
+  b->L = L;
+  b->pin_calls = 0;
+  b->unpinned_seen = 0;
+  BankDev& h = b->host;
+  memset(&h, 0, sizeof(h));
+  h.cap = cap;
+  h.f_max = f_max;
+  h.n_pin = n_pin;
+  h.d_kv = ld.d_kv;
+  h.H = ld.H;
+  h.d_h = ld.d_h;
+  h.dtype = ld.dtype;
+  h.n_tiles_cap = (cap + KT - 1) / KT;
+  const size_t raw = (size_t)cap * ld.d_kv * es;
+  const size_t proj = (size_t)h.n_tiles_cap * KT * ld.D * es;
+  struct Alloc {
+    void** p;
+    size_t bytes;
+  } allocs[] = {
+      {&h.Kraw, raw},
+      {&h.Vraw, raw},
+      {(void**)&h.pos, (size_t)cap * 4},
+      {&h.Khat, proj},
+      {&h.Vhat, proj},
+      {(void**)&h.hdr, HDR_WORDS * 4},
+      {(void**)&h.frames, (size_t)f_max * 16},
+      {(void**)&h.tiles, (size_t)h.n_tiles_cap * sizeof(TileEnt)},
+      {(void**)&b->d_desc, sizeof(BankDev)},
+  };
+  hipError_t e = hipSuccess;
+  for (auto& a : allocs) {
+    if (e != hipSuccess) break;
+    e = hipMalloc(a.p, a.bytes);
+    // zero fill: padding rows of the projected tiles must hold finite values
+    if (e == hipSuccess) e = hipMemset(*a.p, 0, a.bytes);
+  }
+  if (e == hipSuccess) e = hipMemcpy(b->d_desc, &h, sizeof(BankDev), hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) {
+    for (auto& a : allocs)
+      if (*a.p) (void)hipFree(*a.p);
+    delete b;
+    return map_err(e);
+  }
+  *out = b;
+  return RS3_OK;
+}
+
+void rs3_bank_destroy(rs3_bank* b) {
+  if (!b) return;
+  BankDev& h = b->host;
+  void* ptrs[] = {h.Kraw, h.Vraw, h.pos, h.Khat, h.Vhat, h.hdr, h.frames, h.tiles, b->d_desc};
+  for (void* p : ptrs)
+    if (p) (void)hipFree(p);
+  delete b;
+}
+
+rs3_status rs3_bank_export(const rs3_bank* b, int32_t* hdr, int32_t* frames, void* K, void* V,
+                           int32_t* pos) {
+  if (!b || !hdr) return RS3_E_INVALID;
+  const BankDev& h = b->host;
+  hipError_t e = hipDeviceSynchronize();
+  int32_t dh[HDR_WORDS];
+  if (e == hipSuccess) e = hipMemcpy(dh, h.hdr, sizeof(dh), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return map_err(e);
+  const int nf = dh[HDR_NFRAMES];
+  std::vector<int32_t> fr((size_t)h.f_max * 4, 0);
+  e = hipMemcpy(fr.data(), h.frames, fr.size() * 4, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return map_err(e);
+  int keys = 0;
+  for (int f = 0; f < nf; ++f) keys += fr[4 * f + 1];
+  memset(hdr, 0, RS3_BANK_HDR_WORDS * 4);
+  hdr[0] = nf;
+  hdr[1] = dh[HDR_PINEND];
+  hdr[2] = dh[HDR_ERR];
+  hdr[3] = keys;
+  if (frames) memcpy(frames, fr.data(), (size_t)nf * 16);
+  const size_t es = dtype_size(h.dtype);
+  const size_t row = (size_t)h.d_kv * es;
+  size_t off = 0;
+  for (int f = 0; f < nf && e == hipSuccess; ++f) {
+    const int s = fr[4 * f], l = fr[4 * f + 1];
+    if (l == 0) continue;
+    if (K) e = hipMemcpy((uint8_t*)K + off * row, (uint8_t*)h.Kraw + (size_t)s * row, l * row, hipMemcpyDeviceToHost);
+    if (V && e == hipSuccess)
+      e = hipMemcpy((uint8_t*)V + off * row, (uint8_t*)h.Vraw + (size_t)s * row, l * row, hipMemcpyDeviceToHost);
+    if (pos && e == hipSuccess)
+      e = hipMemcpy(pos + off, h.pos + s, (size_t)l * 4, hipMemcpyDeviceToHost);
+    off += l;
+  }
+  return map_err(e);
+}
+
+rs3_status rs3_bank_error(rs3_bank* b, int32_t* err, int32_t clear) {
+  if (!b || !err) return RS3_E_INVALID;
+  hipError_t e = hipDeviceSynchronize();
+  if (e == hipSuccess) e = hipMemcpy(err, b->host.hdr + HDR_ERR, 4, hipMemcpyDeviceToHost);
+  if (e == hipSuccess && clear) e = hipMemset(b->host.hdr + HDR_ERR, 0, 4);
+  if (e == hipSuccess && clear) e = hipDeviceSynchronize();
+  return map_err(e);
+}
+
+// ---- select ----------------------------------------------------------------
+rs3_status rs3_select_workspace_size(const rs3_grid* g, int32_t n_obj, int64_t x_obj_stride,
+                                     size_t* bytes) {
+  if (!bytes || !grid_ok(g) || n_obj <= 0 || n_obj > RS3_MAX_OBJ || x_obj_stride < 0) return RS3_E_INVALID;
+  const int64_t mn = (int64_t)g->m * g->n;
+  const int n_x = x_obj_stride ? n_obj : 1;
+  *bytes = (size_t)n_x * mn * 8;
+  return RS3_OK;
+}
+
+rs3_status rs3_select_queries(const rs3_grid* g, int32_t n_obj, const uint8_t* masks, rs3_track* tr,
+                              const void* X, int64_t x_obj_stride, int32_t C, rs3_dtype dt,
+                              const int32_t* k, const rs3_select_params* p, void* ws, size_t ws_bytes,
+                              int32_t* sel_idx, int32_t* sel_count, uint8_t* prior_out, void* stream) {
+  if (!grid_ok(g) || !masks || !tr || !X || !k || !p || !ws || !sel_idx || !sel_count) return RS3_E_INVALID;
+  if (n_obj <= 0 || n_obj > RS3_MAX_OBJ || tr->n_obj != n_obj) return RS3_E_INVALID;
+  if (dt != RS3_BF16 && dt != RS3_F32) return RS3_E_INVALID;
+  if (C <= 0 || C % 8 != 0) return RS3_E_INVALID;
+  const int mn = g->m * g->n;
+  if (x_obj_stride < 0 || (x_obj_stride != 0 && x_obj_stride < (int64_t)mn * C)) return RS3_E_INVALID;
+  if (x_obj_stride != 0 && p->union_objects && n_obj > 1) return RS3_E_INVALID;
+  if (p->r_s < 0 || p->c < 0) return RS3_E_INVALID;
+  const int n_groups = p->union_objects ? 1 : n_obj;
+  for (int i = 0; i < n_groups; ++i)
+    if (k[i] < 0 || k[i] > mn) return RS3_E_INVALID;
+  size_t need;
+  rs3_select_workspace_size(g, n_obj, x_obj_stride, &need);
+  if (ws_bytes < need) return RS3_E_INVALID;
+  rs3_status st0 = ensure_setup();
+  if (st0 != RS3_OK) return st0;
+  hipStream_t st = (hipStream_t)stream;
+  const int n_x = x_obj_stride ? n_obj : 1;
+  double* e = (double*)ws;
+  hipError_t he = rs3_launch_energy(X, x_obj_stride, n_x, mn, C, dt, e, st);
+  if (he != hipSuccess) return map_err(he);
+  Rs3SelectArgs a;
+  memset(&a, 0, sizeof(a));
+  a.masks = masks;
+  a.track = tr->d_state;
+  a.e = e;
+  a.sel_idx = sel_idx;
+  a.sel_count = sel_count;
+  a.prior_out = prior_out;
+  a.m = g->m;
+  a.n = g->n;
+  a.s = g->s;
+  a.n_obj = n_obj;
+  a.union_objects = p->union_objects ? 1 : 0;
+  a.seed_box = p->seed_box ? 1 : 0;
+  a.r_s = p->r_s;
+  a.c = p->c;
+  a.x_per_obj = n_x > 1;
+  for (int i = 0; i < n_groups; ++i) a.k[i] = k[i];
+  return map_err(rs3_launch_select(a, n_groups, st));
+}
+
+// ---- readout ---------------------------------------------------------------
+static void readout_shape(const rs3_layer* L, int32_t n_obj, int32_t max_sel, int32_t S, size_t* q_bytes,
+                          size_t* o_bytes, size_t* ml_bytes) {
+  const LayerDev& ld = L->dev;
+  *q_bytes = align256((size_t)n_obj * max_sel * ld.D * 2);
+  *o_bytes = align256((size_t)n_obj * S * max_sel * ld.D * 2);
+  *ml_bytes = align256((size_t)n_obj * S * max_sel * ld.H * 8);
+}
+
+static int splits_for(const rs3_layer* L, int32_t n_obj, int32_t max_sel, int32_t n_splits) {
+  if (n_splits > 0) return n_splits;
+  const int n_qt = (max_sel + 127) / 128;
+  return auto_splits(n_obj, L->dev.H, n_qt > 0 ? n_qt : 1, 1 << 20);
+}
+
+rs3_status rs3_readout_workspace_size(const rs3_layer* L, int32_t n_obj, int32_t max_sel, int32_t n_splits,
+                                      size_t* bytes) {
+  if (!L || !bytes || n_obj <= 0 || n_obj > RS3_MAX_OBJ || max_sel < 0 || n_splits < 0 || n_splits > 256)
+    return RS3_E_INVALID;
+  if (L->dev.dtype == RS3_F32) {
+    *bytes = 0;
+    return RS3_OK;
+  }
+  const int S = splits_for(L, n_obj, max_sel, n_splits);
+  size_t q, o, ml;
+  readout_shape(L, n_obj, max_sel, S, &q, &o, &ml);
+  *bytes = q + o + ml;
+  return RS3_OK;
+}
+
+rs3_status rs3_readout(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, const void* X, int64_t x_obj_stride,
+                       rs3_bank* const* banks, const int32_t* sel_idx, const int32_t* sel_count, int32_t sel_stride,
+                       int32_t max_sel, int32_t n_splits, void* Y, int64_t y_obj_stride, int32_t y_fp32, void* ws,
+                       size_t ws_bytes, void* stream) {
+  if (!L || !grid_ok(g) || !X || !banks || !sel_idx || !sel_count || !Y) return RS3_E_INVALID;
+  if (n_obj <= 0 || n_obj > RS3_MAX_OBJ) return RS3_E_INVALID;
+  const LayerDev& ld = L->dev;
+  const int mn = g->m * g->n;
+  if (max_sel < 0 || max_sel > mn || n_splits < 0 || n_splits > 256) return RS3_E_INVALID;
+  if (sel_stride != 0 && sel_stride != mn) return RS3_E_INVALID;
+  const int64_t grid_elems = (int64_t)mn * ld.C;
+  if (x_obj_stride < 0 || (x_obj_stride != 0 && x_obj_stride < grid_elems)) return RS3_E_INVALID;
+  if (n_obj > 1 && y_obj_stride < grid_elems) return RS3_E_INVALID;
+  if (y_obj_stride < 0) return RS3_E_INVALID;
+  for (int o = 0; o < n_obj; ++o) {
+    if (!banks[o] || banks[o]->L != L) return RS3_E_INVALID;
+    for (int p = 0; p < o; ++p)
+      if (banks[p] == banks[o]) return RS3_E_INVALID;
+  }
+  if (Y == X) {
+    if (y_fp32) return RS3_E_INVALID;
+    if (n_obj > 1 && x_obj_stride != y_obj_stride) return RS3_E_INVALID;
+  }
+  if (ld.dtype == RS3_F32) y_fp32 = 0;
+  const int S = splits_for(L, n_obj, max_sel, n_splits);
+  size_t q, o_b, ml;
+  readout_shape(L, n_obj, max_sel, S, &q, &o_b, &ml);
+  if (ld.dtype == RS3_BF16 && (!ws || ws_bytes < q + o_b + ml)) return RS3_E_INVALID;
+  rs3_status st0 = ensure_setup();
+  if (st0 != RS3_OK) return st0;
+  Rs3ReadoutArgs a;
+  memset(&a, 0, sizeof(a));
+  for (int o = 0; o < n_obj; ++o) a.banks[o] = banks[o]->d_desc;
+  a.X = X;
+  a.x_stride = x_obj_stride;
+  a.Y = Y;
+  a.y_stride = y_obj_stride;
+  a.sel_idx = sel_idx;
+  a.sel_count = sel_count;
+  a.sel_stride = sel_stride;
+  a.WqT = ld.WqT;
+  a.WoT = ld.WoT;
+  a.Q = ws;
+  a.Opart = ws ? (uint8_t*)ws + q : nullptr;
+  a.ML = ws ? (float*)((uint8_t*)ws + q + o_b) : nullptr;
+  a.qscale = (float)(1.4426950408889634 / sqrt((double)ld.d_h));
+  a.mn = mn;
+  a.C = ld.C;
+  a.H = ld.H;
+  a.d_h = ld.d_h;
+  a.D = ld.D;
+  a.n_obj = n_obj;
+  a.max_sel = max_sel;
+  a.S = S;
+  a.n_qt = (max_sel + 127) / 128;
+  a.y_fp32 = y_fp32 ? 1 : 0;
+  return map_err(rs3_launch_readout(a, ld.dtype, (hipStream_t)stream));
+}
+
+// ---- commit ----------------------------------------------------------------
+rs3_status rs3_commit(rs3_bank* const* banks, int32_t n_obj, const rs3_grid* g, const void* Kmem,
+                      const void* Vmem, int64_t kv_obj_stride, const uint8_t* masks, int32_t t, int32_t pin,
+                      int32_t fall_min, int32_t fall_max, int32_t* kept_count, void* stream) {
+  if (!banks || !grid_ok(g) || !Kmem || !Vmem || !masks) return RS3_E_INVALID;
+  if (n_obj <= 0 || n_obj > RS3_MAX_OBJ) return RS3_E_INVALID;
+  const int mn = g->m * g->n;
+  const rs3_layer* L = banks[0] ? banks[0]->L : nullptr;
+  if (!L) return RS3_E_INVALID;
+  const LayerDev& ld = L->dev;
+  if (n_obj > 1 && kv_obj_stride < (int64_t)mn * ld.d_kv) return RS3_E_INVALID;
+  if (kv_obj_stride < 0) return RS3_E_INVALID;
+  for (int o = 0; o < n_obj; ++o) {
+    if (!banks[o] || banks[o]->L != L) return RS3_E_INVALID;
+    for (int p = 0; p < o; ++p)
+      if (banks[p] == banks[o]) return RS3_E_INVALID;
+    if (pin && (banks[o]->unpinned_seen || banks[o]->pin_calls >= banks[o]->host.n_pin)) return RS3_E_INVALID;
+  }
+  Rs3CommitArgs a;
+  memset(&a, 0, sizeof(a));
+  for (int o = 0; o < n_obj; ++o) a.banks[o] = banks[o]->d_desc;
+  a.masks = masks;
+  a.Kmem = Kmem;
+  a.Vmem = Vmem;
+  a.kv_stride = kv_obj_stride;
+  a.kept_count = kept_count;
+  a.WkT = ld.WkT;
+  a.WvT = ld.WvT;
+  a.m = g->m;
+  a.n = g->n;
+  a.s = g->s;
+  a.t = t;
+  a.pin = pin ? 1 : 0;
+  a.fall_min = fall_min;
+  a.fall_max = fall_max;
+  a.n_obj = n_obj;
+  hipError_t e = rs3_launch_commit(a, ld.dtype, ld.d_kv, ld.D, ld.H, ld.d_h, (hipStream_t)stream);
+  if (e != hipSuccess) return map_err(e);
+  for (int o = 0; o < n_obj; ++o) {
+    if (pin)
+      banks[o]->pin_calls++;
+    else
+      banks[o]->unpinned_seen = 1;
+  }
+  return RS3_OK;
+}
+
+}  // extern "C"

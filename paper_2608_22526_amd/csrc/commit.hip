@@ -1,0 +1,342 @@
+// Store-sparse commit (Sec. 3.2, Eq. 8; sparse write of Algorithm 1).
+//
+// k_commit_place  : one 1024-thread workgroup per object.  Compacts the mask
+//                   to the ascending kept list (ordered block scan), applies
+//                   the dense fall-through, places the frame in the ring
+//                   (single lane; the rule is documented in rs3.h), writes
+//                   the kept cell of every new row to `pos`, and rebuilds the
+//                   list of resident 64-row tiles with their row masks.
+// k_commit_append : 64 kept rows per workgroup.  Copies the raw K/V rows into
+//                   the ring and writes their projections K^ = K W_k and
+//                   V^ = V W_v into the tile-blocked attention layouts
+//                   (bf16 MFMA with fp32 accumulation, or fp32 FMA loops).
+#include "rs3_internal.h"
+
+namespace rs3 {
+
+constexpr int CP_THREADS = 1024;
+constexpr int CP_WAVES = CP_THREADS / 64;
+constexpr int CP_MAX_CPT = RS3_MAX_MN / CP_THREADS;
+
+struct CpShared {
+  int red[CP_WAVES];
+  int ok, start, len;
+};
+
+__device__ __forceinline__ int cp_wave_incl_scan(int v, int lane) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    int t = __shfl_up(v, off, 64);
+    if (lane >= off) v += t;
+  }
+  return v;
+}
+
+__device__ int cp_block_excl_scan(int v, CpShared& sh, int* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int inc = cp_wave_incl_scan(v, lane);
+  if (lane == 63) sh.red[wave] = inc;
+  __syncthreads();
+  int wsum = 0, tot = 0;
+  for (int w = 0; w < CP_WAVES; ++w) {
+    int s = sh.red[w];
+    if (w < wave) wsum += s;
+    tot += s;
+  }
+  __syncthreads();
+  *total = tot;
+  return wsum + inc - v;
+}
+
+// Removes frame `idx` from the key-ordered frame table.
+__device__ void erase_frame(int32_t* fr, int& nf, int idx) {
+  for (int f = idx; f + 1 < nf; ++f)
+    for (int w = 0; w < 4; ++w) fr[4 * f + w] = fr[4 * (f + 1) + w];
+  --nf;
+}
+
+// Returns false when no unpinned frame is resident.
+__device__ bool evict_oldest_unpinned(int32_t* fr, int& nf) {
+  for (int f = 0; f < nf; ++f)
+    if (!fr[4 * f + 3]) {
+      erase_frame(fr, nf, f);
+      return true;
+    }
+  return false;
+}
+
+// Ring placement of a frame of L rows (single lane) on the LDS copy `fr` of
+// the frame table.  Returns the start row, or -1 on a capacity error (table
+// unchanged).
+__device__ int place_frame(const BankDev& b, int32_t* fr, int& nf, int& pin_end, int L, int t,
+                           int pin) {
+  int start;
+  if (pin) {
+    if ((int64_t)pin_end + L > b.cap || nf >= b.f_max) return -1;
+    start = pin_end;
+    pin_end += L;
+  } else {
+    if (L > b.cap - pin_end) return -1;
+    while (nf >= b.f_max)
+      if (!evict_oldest_unpinned(fr, nf)) return -1;  // unreachable while n_pin < f_max
+    start = (nf > 0 && !fr[4 * (nf - 1) + 3]) ? fr[4 * (nf - 1)] + fr[4 * (nf - 1) + 1] : pin_end;
+    if ((int64_t)start + L > b.cap) start = pin_end;
+    for (;;) {
+      bool hit = false;
+      if (L > 0)
+        for (int f = 0; f < nf && !hit; ++f) {
+          int fs = fr[4 * f], fl = fr[4 * f + 1];
+          hit = !fr[4 * f + 3] && fl > 0 && fs < start + L && start < fs + fl;
+        }
+      if (!hit) break;
+      if (!evict_oldest_unpinned(fr, nf)) return -1;  // unreachable: a hit is unpinned
+    }
+  }
+  fr[4 * nf + 0] = start;
+  fr[4 * nf + 1] = L;
+  fr[4 * nf + 2] = t;
+  fr[4 * nf + 3] = pin ? 1 : 0;
+  ++nf;
+  return start;
+}
+
+__device__ __forceinline__ uint64_t tile_mask(const int32_t* fr, int nf, int tile) {
+  const int64_t t0 = (int64_t)tile * KT, t1 = t0 + KT;
+  uint64_t msk = 0;
+  for (int f = 0; f < nf; ++f) {
+    int64_t fs = fr[4 * f], fe = fs + fr[4 * f + 1];
+    int64_t a = fs > t0 ? fs : t0, e = fe < t1 ? fe : t1;
+    if (a < e) {
+      int lo = (int)(a - t0), hi = (int)(e - t0);
+      uint64_t bits = (hi - lo == 64) ? ~0ull : (((1ull << (hi - lo)) - 1ull) << lo);
+      msk |= bits;
+    }
+  }
+  return msk;
+}
+
+// grid n_obj, block 1024, dynamic LDS f_max*16 bytes.
+__global__ __launch_bounds__(CP_THREADS) void k_commit_place(Rs3CommitArgs a) {
+  extern __shared__ int32_t sfr[];
+  __shared__ CpShared sh;
+  const int o = blockIdx.x, tid = threadIdx.x;
+  BankDev& b = *a.banks[o];
+  const int m = a.m, n = a.n, s = a.s, mn = m * n, W = n * s;
+  const uint8_t* M = a.masks + (int64_t)o * (m * s) * W;
+  const int cpt = (mn + CP_THREADS - 1) / CP_THREADS;
+  const int c0 = tid * cpt;
+  uint32_t bits = 0;
+  for (int j = 0; j < cpt; ++j) {
+    int i = c0 + j;
+    if (i < mn) {
+      int y = i / n, x = i - y * n;
+      if (M[(int64_t)(y * s) * W + x * s]) bits |= 1u << j;
+    }
+  }
+  int total;
+  cp_block_excl_scan(__popc(bits), sh, &total);
+  if (total < a.fall_min || total > a.fall_max) {
+    bits = 0;
+    for (int j = 0; j < cpt; ++j)
+      if (c0 + j < mn) bits |= 1u << j;
+  }
+  int before = cp_block_excl_scan(__popc(bits), sh, &total);
+  const int nf0 = b.hdr[HDR_NFRAMES];
+  for (int i = tid; i < 4 * nf0; i += CP_THREADS) sfr[i] = b.frames[i];
+  __syncthreads();
+  if (tid == 0) {
+    if (a.kept_count) a.kept_count[o] = total;
+    int nf = nf0, pin_end = b.hdr[HDR_PINEND];
+    int start = place_frame(b, sfr, nf, pin_end, total, a.t, a.pin);
+    sh.ok = start >= 0;
+    sh.start = start;
+    sh.len = nf;
+    if (start >= 0) {
+      b.hdr[HDR_NFRAMES] = nf;
+      b.hdr[HDR_PINEND] = pin_end;
+      b.hdr[HDR_PSTART] = start;
+      b.hdr[HDR_PLEN] = total;
+    } else {
+      b.hdr[HDR_PLEN] = -1;
+      set_err(b.hdr, RS3_E_CAPACITY);
+    }
+  }
+  __syncthreads();
+  if (!sh.ok) return;
+  const int start = sh.start;
+  const int nf = sh.len;
+  for (int i = tid; i < 4 * nf; i += CP_THREADS) b.frames[i] = sfr[i];
+  for (int j = 0; j < cpt; ++j)
+    if (bits >> j & 1) b.pos[start + before++] = c0 + j;
+
+  // rebuild the resident tile list from the LDS frame table
+  const int nt = b.n_tiles_cap;
+  const int tpt = (nt + CP_THREADS - 1) / CP_THREADS;
+  const int t0 = tid * tpt;
+  int cnt = 0;
+  for (int j = 0; j < tpt; ++j)
+    if (t0 + j < nt && tile_mask(sfr, nf, t0 + j)) ++cnt;
+  int ntot;
+  int pos = cp_block_excl_scan(cnt, sh, &ntot);
+  for (int j = 0; j < tpt; ++j) {
+    if (t0 + j >= nt) break;
+    uint64_t msk = tile_mask(sfr, nf, t0 + j);
+    if (msk) {
+      TileEnt te;
+      te.tile = t0 + j;
+      te.pad = 0;
+      te.mask = msk;
+      b.tiles[pos++] = te;
+    }
+  }
+  if (tid == 0) {
+    int keys = 0;
+    for (int f = 0; f < nf; ++f) keys += sfr[4 * f + 1];
+    b.hdr[HDR_NTILES] = ntot;
+    b.hdr[HDR_NKEYS] = keys;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// append: bf16, 256 threads, 64 rows per workgroup.
+//   K^ tile rows: C = A B, A = kept K rows (64 x d_kv), B = W_k (d_kv x D):
+//     lane holds column d, rows = keys  -> Khat[tile][h][key][d%d_h]
+//   V^ as its transpose: C = W_v^T (D x d_kv) V^T (d_kv x 64):
+//     lane holds column = key, rows = d -> Vhat[tile][h][d%d_h][vslot(key)]
+__global__ __launch_bounds__(256) void k_commit_append_bf16(Rs3CommitArgs a) {
+  const int o = blockIdx.x;
+  BankDev& b = *a.banks[o];
+  const int L = b.hdr[HDR_PLEN];
+  const int r0 = blockIdx.y * 64;
+  if (L < 0 || r0 >= L) return;
+  const int start = b.hdr[HDR_PSTART];
+  const int rows = min(64, L - r0);
+  const int d_kv = b.d_kv, d_h = b.d_h, H = b.H, D = H * d_h;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5;
+  const bf16_t* Km = (const bf16_t*)a.Kmem + (int64_t)o * a.kv_stride;
+  const bf16_t* Vm = (const bf16_t*)a.Vmem + (int64_t)o * a.kv_stride;
+  bf16_t* Kr = (bf16_t*)b.Kraw;
+  bf16_t* Vr = (bf16_t*)b.Vraw;
+  // raw row copy, 16 bytes per lane step
+  const int cpr = d_kv / 8;
+  for (int q = tid; q < rows * cpr; q += 256) {
+    int r = q / cpr, c = q - r * cpr;
+    int j = start + r0 + r;
+    int src = b.pos[j];
+    *(u32x4*)(Kr + (int64_t)j * d_kv + 8 * c) = *(const u32x4*)(Km + (int64_t)src * d_kv + 8 * c);
+    *(u32x4*)(Vr + (int64_t)j * d_kv + 8 * c) = *(const u32x4*)(Vm + (int64_t)src * d_kv + 8 * c);
+  }
+  // projections: 2 row blocks x D/32 column blocks, spread over 4 waves
+  const bf16_t* WkT = (const bf16_t*)a.WkT;
+  const bf16_t* WvT = (const bf16_t*)a.WvT;
+  bf16_t* Kh = (bf16_t*)b.Khat;
+  bf16_t* Vh = (bf16_t*)b.Vhat;
+  const int nblk = 2 * (D / 32);
+  for (int blk = wave; blk < nblk; blk += 4) {
+    const int mb = blk & 1, nb = blk >> 1;
+    // key row fed by this lane (A row for K^, B column for V^)
+    const int rr = 32 * mb + (lane & 31);
+    const bool rvalid = rr < rows;
+    const int src = rvalid ? b.pos[start + r0 + rr] : 0;
+    const bf16_t* krow = Km + (int64_t)src * d_kv;
+    const bf16_t* vrow = Vm + (int64_t)src * d_kv;
+    const int dcol = 32 * nb + (lane & 31);
+    const bf16_t* wk = WkT + (int64_t)dcol * d_kv;
+    const bf16_t* wv = WvT + (int64_t)dcol * d_kv;
+    f32x16 ck = {}, cv = {};
+    for (int ks = 0; ks < d_kv; ks += 16) {
+      u32x4 ka = rvalid ? *(const u32x4*)(krow + ks + 8 * g) : u32x4{0, 0, 0, 0};
+      u32x4 va = rvalid ? *(const u32x4*)(vrow + ks + 8 * g) : u32x4{0, 0, 0, 0};
+      u32x4 wkb = *(const u32x4*)(wk + ks + 8 * g);
+      u32x4 wva = *(const u32x4*)(wv + ks + 8 * g);
+      ck = mfma32(ka, wkb, ck);   // rows = keys, cols = d
+      cv = mfma32(wva, va, cv);   // rows = d, cols = keys
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      // K^: row = key (32mb + c_row), column = d (dcol)
+      int kr = 32 * mb + c_row(r, lane);
+      if (kr < rows) {
+        int j = start + r0 + kr;
+        int tile = j >> 6, kk = j & 63, h = dcol / d_h, dd = dcol - h * d_h;
+        Kh[(((int64_t)tile * H + h) * KT + kk) * d_h + dd] = f2bf(ck[r]);
+      }
+      // V^: row = d (32nb + c_row), column = key (32mb + lane%32)
+      if (rvalid) {
+        int d = 32 * nb + c_row(r, lane);
+        int j = start + r0 + rr;
+        int tile = j >> 6, kk = j & 63, h = d / d_h, dd = d - h * d_h;
+        Vh[(((int64_t)tile * H + h) * d_h + dd) * KT + vslot(kk)] = f2bf(cv[r]);
+      }
+    }
+  }
+}
+
+// append: fp32, 256 threads, 64 rows per workgroup, FMA loops.
+__global__ __launch_bounds__(256) void k_commit_append_f32(Rs3CommitArgs a) {
+  const int o = blockIdx.x;
+  BankDev& b = *a.banks[o];
+  const int L = b.hdr[HDR_PLEN];
+  const int r0 = blockIdx.y * 64;
+  if (L < 0 || r0 >= L) return;
+  const int start = b.hdr[HDR_PSTART];
+  const int rows = min(64, L - r0);
+  const int d_kv = b.d_kv, d_h = b.d_h, H = b.H, D = H * d_h;
+  const float* Km = (const float*)a.Kmem + (int64_t)o * a.kv_stride;
+  const float* Vm = (const float*)a.Vmem + (int64_t)o * a.kv_stride;
+  float* Kr = (float*)b.Kraw;
+  float* Vr = (float*)b.Vraw;
+  for (int q = threadIdx.x; q < rows * d_kv; q += 256) {
+    int r = q / d_kv, c = q - r * d_kv;
+    int j = start + r0 + r;
+    int src = b.pos[j];
+    Kr[(int64_t)j * d_kv + c] = Km[(int64_t)src * d_kv + c];
+    Vr[(int64_t)j * d_kv + c] = Vm[(int64_t)src * d_kv + c];
+  }
+  const float* WkT = (const float*)a.WkT;
+  const float* WvT = (const float*)a.WvT;
+  float* Kh = (float*)b.Khat;
+  float* Vh = (float*)b.Vhat;
+  for (int q = threadIdx.x; q < rows * D; q += 256) {
+    int r = q / D, d = q - r * D;
+    int j = start + r0 + r;
+    int src = b.pos[j];
+    const float* kr = Km + (int64_t)src * d_kv;
+    const float* vr = Vm + (int64_t)src * d_kv;
+    const float* wk = WkT + (int64_t)d * d_kv;
+    const float* wv = WvT + (int64_t)d * d_kv;
+    float sk = 0.f, sv = 0.f;
+    for (int c = 0; c < d_kv; ++c) {
+      sk = fmaf(kr[c], wk[c], sk);
+      sv = fmaf(vr[c], wv[c], sv);
+    }
+    int tile = j >> 6, kk = j & 63, h = d / d_h, dd = d - h * d_h;
+    Kh[(((int64_t)tile * H + h) * KT + kk) * d_h + dd] = sk;
+    Vh[(((int64_t)tile * H + h) * d_h + dd) * KT + vslot(kk)] = sv;
+  }
+}
+
+}  // namespace rs3
+
+using namespace rs3;
+
+hipError_t rs3_launch_commit(const Rs3CommitArgs& a, int dtype, int d_kv, int D, int H, int d_h,
+                             hipStream_t st) {
+  (void)d_kv;
+  (void)D;
+  (void)H;
+  (void)d_h;
+  const int mn = a.m * a.n;
+  int f_max = 0;
+  // the frame table of every bank fits the largest f_max (checked on the host)
+  f_max = 256;
+  hipLaunchKernelGGL(k_commit_place, dim3(a.n_obj), dim3(CP_THREADS), f_max * 16, st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  dim3 grid(a.n_obj, (mn + 63) / 64);
+  if (dtype == RS3_BF16)
+    hipLaunchKernelGGL(k_commit_append_bf16, grid, dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL(k_commit_append_f32, grid, dim3(256), 0, st, a);
+  return hipGetLastError();
+}

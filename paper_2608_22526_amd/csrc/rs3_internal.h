@@ -1,0 +1,168 @@
+// Internal definitions shared by the HIP kernels and the host side of the
+// rs3 library (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "rs3.h"
+
+namespace rs3 {
+
+// ---- bank layout -----------------------------------------------------------
+// Device header words of a bank.
+enum : int {
+  HDR_NFRAMES = 0,   // resident frames
+  HDR_PINEND = 1,    // rows occupied by pinned frames
+  HDR_ERR = 2,       // sticky error word (first error wins)
+  HDR_PSTART = 3,    // row where the pending append starts
+  HDR_PLEN = 4,      // rows of the pending append, -1 when none
+  HDR_NTILES = 5,    // entries in the resident tile list
+  HDR_NKEYS = 6,     // resident rows (N)
+  HDR_WORDS = 8
+};
+
+constexpr int KT = 64;  // keys per bank tile
+
+// Resident tile: ring rows [64*tile, 64*tile+64), bit j set iff row 64*tile+j
+// belongs to a resident frame.
+struct TileEnt {
+  int32_t tile;
+  int32_t pad;
+  uint64_t mask;
+};
+
+// Device-resident descriptor of one bank.
+//  Kraw, Vraw : [cap][d_kv] (dtype), raw rows as committed
+//  pos        : [cap] int32, kept cell index of each row
+//  Khat       : [n_tiles_cap][H][64][d_h]   rows = keys, d contiguous
+//  Vhat       : [n_tiles_cap][H][d_h][64]   keys contiguous in the slot
+//               order of vslot() (see below)
+//  hdr        : [HDR_WORDS] int32
+//  frames     : [f_max][4] int32 {start, len, t, pinned} in key order
+//  tiles      : [n_tiles_cap] TileEnt, ascending tile index
+struct BankDev {
+  int32_t cap, f_max, n_pin, d_kv, H, d_h, dtype, n_tiles_cap;
+  void* Kraw;
+  void* Vraw;
+  int32_t* pos;
+  void* Khat;
+  void* Vhat;
+  int32_t* hdr;
+  int32_t* frames;
+  TileEnt* tiles;
+};
+
+// Slot of key j (0..63) inside a V^ tile.  Within each 16-key group the two
+// middle quads swap places ([0-3, 8-11, 4-7, 12-15]), so the eight keys that
+// one lane feeds to a 16-deep bf16 MFMA step after the key-major logits are
+// contiguous (see the attention kernel).
+__host__ __device__ inline int vslot(int j) {
+  int w = j & 15;
+  return (j & ~15) | (((w >> 2) & 1) << 3) | ((w >> 3) << 2) | (w & 3);
+}
+
+// ---- layer -----------------------------------------------------------------
+// Device weights, transposed so that every MFMA operand reads contiguous
+// 16-byte runs along the contraction dimension.
+struct LayerDev {
+  int32_t C, H, d_h, D, d_kv, dtype;
+  void* WqT;  // [D][C]
+  void* WkT;  // [D][d_kv]
+  void* WvT;  // [D][d_kv]
+  void* WoT;  // [C][D]
+};
+
+struct Launch {
+  hipStream_t stream;
+};
+
+// ---- bf16 helpers ----------------------------------------------------------
+typedef uint16_t bf16_t;
+
+__device__ __forceinline__ float bf2f(bf16_t b) {
+  return __uint_as_float(((uint32_t)b) << 16);
+}
+
+// fp32 -> bf16, round to nearest even (NaN stays NaN).
+__device__ __forceinline__ bf16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+// D = A(32x16) * B(16x32) + C.  Lane l supplies A row l%32 and B column l%32,
+// each with the eight k values 8*(l/32) .. 8*(l/32)+7.  The 16 results of lane
+// l are column l%32, rows 8*(r/4) + 4*(l/32) + (r%4) for r = 0..15.
+__device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
+}
+
+__device__ __forceinline__ int c_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
+
+__device__ __forceinline__ void set_err(int32_t* hdr, int code) {
+  atomicCAS(&hdr[HDR_ERR], 0, code);
+}
+
+}  // namespace rs3
+
+// ---- kernel argument blocks (passed by value) ------------------------------
+struct Rs3SelectArgs {
+  const uint8_t* masks;   // [n_obj][m*s][n*s]
+  int32_t* track;         // [n_obj][RS3_TRACK_WORDS]
+  const double* e;        // [n_x][mn] energies
+  int32_t* sel_idx;       // [n_groups][mn]
+  int32_t* sel_count;     // [n_groups]
+  uint8_t* prior_out;     // [n_groups][mn] or null
+  int m, n, s, n_obj, union_objects, seed_box, r_s, c, x_per_obj;
+  int k[RS3_MAX_OBJ];
+};
+
+struct Rs3CommitArgs {
+  rs3::BankDev* banks[RS3_MAX_OBJ];
+  const uint8_t* masks;   // [n_obj][m*s][n*s]
+  const void* Kmem;       // [n_obj][mn][d_kv]
+  const void* Vmem;
+  int64_t kv_stride;      // elements between objects
+  int32_t* kept_count;    // [n_obj] or null
+  const void* WkT;        // [D][d_kv]
+  const void* WvT;
+  int m, n, s, t, pin, fall_min, fall_max, n_obj;
+};
+
+struct Rs3ReadoutArgs {
+  rs3::BankDev* banks[RS3_MAX_OBJ];
+  const void* X;
+  int64_t x_stride;       // elements between objects' grids (0 = shared)
+  void* Y;
+  int64_t y_stride;
+  const int32_t* sel_idx;
+  const int32_t* sel_count;
+  int sel_stride;         // elements between objects' lists (0 = shared)
+  const void* WqT;        // [D][C]
+  const void* WoT;        // [C][D]
+  void* Q;                // [n_obj][max_sel][D] bf16 workspace
+  void* Opart;            // [n_obj][S][max_sel][D] bf16 workspace
+  float* ML;              // [n_obj][S][max_sel][H][2] workspace
+  float qscale;           // log2(e) / sqrt(d_h)
+  int mn, C, H, d_h, D, n_obj, max_sel, S, n_qt, y_fp32;
+};
+
+// Launchers (all enqueue on `st` and return the launch status).
+hipError_t rs3_launch_energy(const void* X, int64_t x_stride, int n_x, int mn, int C, int dtype,
+                             double* e, hipStream_t st);
+hipError_t rs3_launch_select(const Rs3SelectArgs& a, int n_groups, hipStream_t st);
+hipError_t rs3_launch_commit(const Rs3CommitArgs& a, int dtype, int d_kv, int D, int H, int d_h,
+                             hipStream_t st);
+hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st);
+hipError_t rs3_readout_setup();
+hipError_t rs3_select_setup();

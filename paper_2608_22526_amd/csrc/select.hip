@@ -1,0 +1,390 @@
+// Read-side keep-set: spatial prior (Sec. 3.1, Eqs. 1, 2, 5; tracker update
+// of Algorithm 1) and the energy top-k inside it (Eq. 4).
+//
+// k_energy : e_i = sum_c x_{i,c}^2 in fp64, channels added in ascending
+//            order, one lane per token row (the squares of bf16/fp32 values
+//            are exact in fp64, so the sums are reproducible bit for bit).
+// k_select : one 1024-thread workgroup per group.  Builds the group's prior
+//            bitmap in LDS (per-object bbox, streak update, separable
+//            Chebyshev dilation), then finds the k-th largest energy with an
+//            MSB-first radix select over the fp64 bit patterns (energies are
+//            >= 0, so unsigned order is numeric order) and emits the kept
+//            cells in ascending order with two ordered block scans.
+#include "rs3_internal.h"
+
+namespace rs3 {
+
+constexpr int SEL_THREADS = 1024;
+constexpr int SEL_WAVES = SEL_THREADS / 64;
+
+// ---------------------------------------------------------------------------
+template <typename T>
+__device__ __forceinline__ void load_row_chunk(const T* p, double* v);
+
+template <>
+__device__ __forceinline__ void load_row_chunk<bf16_t>(const bf16_t* p, double* v) {
+  u32x4 w = *reinterpret_cast<const u32x4*>(p);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    v[2 * j] = (double)__uint_as_float(w[j] << 16);
+    v[2 * j + 1] = (double)__uint_as_float(w[j] & 0xffff0000u);
+  }
+}
+
+template <>
+__device__ __forceinline__ void load_row_chunk<float>(const float* p, double* v) {
+  const f32x4* q = reinterpret_cast<const f32x4*>(p);
+  f32x4 a = q[0], b = q[1];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    v[j] = (double)a[j];
+    v[4 + j] = (double)b[j];
+  }
+}
+
+// grid (ceil(mn/64), n_x), block 64.  C is a multiple of 8.
+template <typename T>
+__global__ __launch_bounds__(64) void k_energy(const T* __restrict__ X, int64_t x_stride, int mn,
+                                                int C, double* __restrict__ e) {
+  const int xi = blockIdx.y;
+  const int i = blockIdx.x * 64 + threadIdx.x;
+  if (i >= mn) return;
+  const T* row = X + (int64_t)xi * x_stride + (int64_t)i * C;
+  double acc = 0.0;
+  for (int c = 0; c < C; c += 8) {
+    double v[8];
+    load_row_chunk<T>(row + c, v);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc = acc + v[j] * v[j];
+  }
+  e[(int64_t)xi * mn + i] = acc;
+}
+
+// ---------------------------------------------------------------------------
+// block-wide helpers for a 1024-thread workgroup
+struct SelShared {
+  int red[SEL_WAVES];
+  unsigned long long redu[SEL_WAVES];
+  int bb[4];
+  int mode, r, gy0, gx0, gy1, gx1;
+  int hist[256];
+  int digit, remaining;
+};
+
+__device__ __forceinline__ int wave_incl_scan(int v, int lane) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    int t = __shfl_up(v, off, 64);
+    if (lane >= off) v += t;
+  }
+  return v;
+}
+
+// Exclusive prefix over the workgroup in thread order; returns the prefix
+// and writes the total to *total.
+__device__ int block_excl_scan(int v, SelShared& sh, int* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int inc = wave_incl_scan(v, lane);
+  if (lane == 63) sh.red[wave] = inc;
+  __syncthreads();
+  int wsum = 0, tot = 0;
+  for (int w = 0; w < SEL_WAVES; ++w) {
+    int s = sh.red[w];
+    if (w < wave) wsum += s;
+    tot += s;
+  }
+  __syncthreads();
+  *total = tot;
+  return wsum + inc - v;
+}
+
+__device__ int block_sum(int v, SelShared& sh) {
+  int tot;
+  block_excl_scan(v, sh, &tot);
+  return tot;
+}
+
+__device__ unsigned long long block_minmax_u64(unsigned long long v, bool want_max, SelShared& sh) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    unsigned long long o = __shfl_xor(v, off, 64);
+    v = want_max ? (o > v ? o : v) : (o < v ? o : v);
+  }
+  if (lane == 0) sh.redu[wave] = v;
+  __syncthreads();
+  unsigned long long r = sh.redu[0];
+  for (int w = 1; w < SEL_WAVES; ++w) {
+    unsigned long long o = sh.redu[w];
+    r = want_max ? (o > r ? o : r) : (o < r ? o : r);
+  }
+  __syncthreads();
+  return r;
+}
+
+// ---------------------------------------------------------------------------
+enum { MODE_NONE = 0, MODE_MASK = 1, MODE_BOX = 2 };
+
+// Adds one object's prior into U (LDS bitmap of the group).
+__device__ void add_object_prior(const Rs3SelectArgs& a, int o, uint8_t* U, uint8_t* base,
+                                 uint8_t* tmp, SelShared& sh) {
+  const int tid = threadIdx.x;
+  const int m = a.m, n = a.n, s = a.s, mn = m * n;
+  const int W = n * s, Hpx = m * s;
+  const uint8_t* M = a.masks + (int64_t)o * Hpx * W;
+  if (tid == 0) {
+    sh.bb[0] = 0x7fffffff;
+    sh.bb[1] = 0x7fffffff;
+    sh.bb[2] = -1;
+    sh.bb[3] = -1;
+  }
+  __syncthreads();
+  int y0 = 0x7fffffff, x0 = 0x7fffffff, y1 = -1, x1 = -1;
+  const int npx = Hpx * W;
+  for (int p = tid; p < npx; p += SEL_THREADS) {
+    if (M[p]) {
+      int y = p / W, x = p - y * W;
+      y0 = min(y0, y);
+      y1 = max(y1, y);
+      x0 = min(x0, x);
+      x1 = max(x1, x);
+    }
+  }
+  if (y1 >= 0) {
+    atomicMin(&sh.bb[0], y0);
+    atomicMin(&sh.bb[1], x0);
+    atomicMax(&sh.bb[2], y1);
+    atomicMax(&sh.bb[3], x1);
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int32_t* tr = a.track + o * RS3_TRACK_WORDS;
+    const bool nonempty = sh.bb[2] >= 0;
+    int mode = MODE_NONE, r = a.r_s;
+    int by0 = 0, bx0 = 0, by1 = 0, bx1 = 0;
+    if (nonempty) {
+      by0 = sh.bb[0];
+      bx0 = sh.bb[1];
+      by1 = sh.bb[2];
+      bx1 = sh.bb[3];
+      mode = a.seed_box ? MODE_BOX : MODE_MASK;
+      tr[0] = by0;
+      tr[1] = bx0;
+      tr[2] = by1;
+      tr[3] = bx1;
+      tr[4] = 0;
+      tr[5] = 1;
+    } else {
+      int d = tr[4] + 1;
+      tr[4] = d;
+      if (tr[5]) {
+        mode = MODE_BOX;
+        by0 = tr[0];
+        bx0 = tr[1];
+        by1 = tr[2];
+        bx1 = tr[3];
+        r = a.r_s + min(d, a.c);
+      }
+    }
+    sh.mode = mode;
+    sh.r = r;
+    sh.gy0 = by0 / s;
+    sh.gx0 = bx0 / s;
+    sh.gy1 = by1 / s;
+    sh.gx1 = bx1 / s;
+  }
+  __syncthreads();
+  const int mode = sh.mode, r = sh.r;
+  if (mode == MODE_BOX) {
+    const int ya = max(0, sh.gy0 - r), yb = min(m - 1, sh.gy1 + r);
+    const int xa = max(0, sh.gx0 - r), xb = min(n - 1, sh.gx1 + r);
+    for (int i = tid; i < mn; i += SEL_THREADS) {
+      int y = i / n, x = i - y * n;
+      if (y >= ya && y <= yb && x >= xa && x <= xb) U[i] = 1;
+    }
+  } else if (mode == MODE_MASK) {
+    for (int i = tid; i < mn; i += SEL_THREADS) {
+      int y = i / n, x = i - y * n;
+      base[i] = M[(int64_t)(y * s) * W + x * s] != 0;
+    }
+    __syncthreads();
+    for (int i = tid; i < mn; i += SEL_THREADS) {
+      int y = i / n, x = i - y * n;
+      const uint8_t* row = base + y * n;
+      int xa = max(0, x - r), xb = min(n - 1, x + r);
+      uint8_t v = 0;
+      for (int xx = xa; xx <= xb && !v; ++xx) v = row[xx];
+      tmp[i] = v;
+    }
+    __syncthreads();
+    for (int i = tid; i < mn; i += SEL_THREADS) {
+      int y = i / n, x = i - y * n;
+      int ya = max(0, y - r), yb = min(m - 1, y + r);
+      uint8_t v = 0;
+      for (int yy = ya; yy <= yb && !v; ++yy) v = tmp[yy * n + x];
+      if (v) U[i] = 1;
+    }
+  }
+  __syncthreads();
+}
+
+// grid n_groups, block 1024, dynamic LDS 3*mn bytes.
+__global__ __launch_bounds__(SEL_THREADS) void k_select(Rs3SelectArgs a) {
+  extern __shared__ uint8_t lds[];
+  __shared__ SelShared sh;
+  const int g = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int mn = a.m * a.n;
+  uint8_t* U = lds;
+  uint8_t* base = lds + mn;
+  uint8_t* tmp = lds + 2 * mn;
+
+  for (int i = tid; i < mn; i += SEL_THREADS) U[i] = 0;
+  __syncthreads();
+  if (a.union_objects) {
+    for (int o = 0; o < a.n_obj; ++o) add_object_prior(a, o, U, base, tmp, sh);
+  } else {
+    add_object_prior(a, g, U, base, tmp, sh);
+  }
+  if (a.prior_out) {
+    for (int i = tid; i < mn; i += SEL_THREADS) a.prior_out[(int64_t)g * mn + i] = U[i];
+  }
+
+  // Contiguous cells per thread so that block scans follow cell order.
+  const int cpt = (mn + SEL_THREADS - 1) / SEL_THREADS;
+  const int c0 = tid * cpt;
+  // Energies are re-read from global memory (L2-resident) in every pass
+  // rather than held in registers.
+  const unsigned long long* ebits =
+      reinterpret_cast<const unsigned long long*>(a.e + (a.x_per_obj ? (int64_t)g * mn : 0)) + c0;
+  uint32_t inP = 0;
+  for (int j = 0; j < cpt; ++j) {
+    int i = c0 + j;
+    if (i < mn && U[i]) inP |= 1u << j;
+  }
+  const int k = a.k[g];
+  const int countP = block_sum(__popc(inP), sh);
+  uint32_t keep = inP;
+  if (countP > k) {
+    unsigned long long lo = ~0ull, hi = 0;
+    for (int j = 0; j < cpt; ++j)
+      if (inP >> j & 1) {
+        const unsigned long long key = ebits[j];
+        lo = key < lo ? key : lo;
+        hi = key > hi ? key : hi;
+      }
+    const unsigned long long kmin = block_minmax_u64(lo, false, sh);
+    const unsigned long long kmax = block_minmax_u64(hi, true, sh);
+    unsigned long long T;
+    int need_eq;
+    if (k == 0) {
+      T = ~0ull;  // nothing kept
+      need_eq = 0;
+    } else if (kmin == kmax) {
+      T = kmin;
+      need_eq = k;
+    } else {
+      const int h = 63 - __clzll(kmin ^ kmax);
+      unsigned long long prefix = (h == 63) ? 0ull : (kmin & ~((2ull << h) - 1ull));
+      int remaining = k;
+      int top = h;
+      while (top >= 0) {
+        const int width = top + 1 < 8 ? top + 1 : 8;
+        const int shift = top - width + 1;
+        const unsigned dmask = (1u << width) - 1u;
+        for (int b = tid; b < 256; b += SEL_THREADS) sh.hist[b] = 0;
+        __syncthreads();
+        for (int j = 0; j < cpt; ++j) {
+          if (inP >> j & 1) {
+            const unsigned long long key = ebits[j];
+            bool match = (top >= 63) || (((key ^ prefix) >> (top + 1)) == 0ull);
+            if (match) atomicAdd(&sh.hist[(unsigned)(key >> shift) & dmask], 1);
+          }
+        }
+        __syncthreads();
+        if (tid < 64) {
+          // lane owns bins 4*lane .. 4*lane+3; find the digit holding the
+          // remaining-th largest candidate
+          int h0 = sh.hist[4 * lane], h1 = sh.hist[4 * lane + 1];
+          int h2 = sh.hist[4 * lane + 2], h3 = sh.hist[4 * lane + 3];
+          int mine = h0 + h1 + h2 + h3;
+          int suf = mine;  // inclusive suffix sum over lanes >= lane
+#pragma unroll
+          for (int off = 1; off < 64; off <<= 1) {
+            int t = __shfl_down(suf, off, 64);
+            if (lane + off < 64) suf += t;
+          }
+          int above = suf - mine;  // candidates in bins of higher lanes
+          int want = remaining;
+          if (above < want && want <= suf) {
+            int hb[4] = {h0, h1, h2, h3};
+            int cum = above;
+            for (int b = 3; b >= 0; --b) {
+              if (cum + hb[b] >= want) {
+                sh.digit = 4 * lane + b;
+                sh.remaining = want - cum;
+                break;
+              }
+              cum += hb[b];
+            }
+          }
+        }
+        __syncthreads();
+        prefix |= (unsigned long long)sh.digit << shift;
+        remaining = sh.remaining;
+        __syncthreads();
+        top = shift - 1;
+      }
+      T = prefix;
+      need_eq = remaining;
+    }
+    // rank of each candidate equal to T among equals, in cell order
+    uint32_t eq = 0, gt = 0;
+    for (int j = 0; j < cpt; ++j)
+      if (inP >> j & 1) {
+        const unsigned long long key = ebits[j];
+        if (key == T) eq |= 1u << j;
+        if (key > T && T != ~0ull) gt |= 1u << j;
+      }
+    int eqTot;
+    int eqBefore = block_excl_scan(__popc(eq), sh, &eqTot);
+    keep = gt;
+    for (int j = 0; j < cpt; ++j) {
+      if (eq >> j & 1) {
+        if (eqBefore < need_eq) keep |= 1u << j;
+        ++eqBefore;
+      }
+    }
+  }
+  int total;
+  int before = block_excl_scan(__popc(keep), sh, &total);
+  int32_t* out = a.sel_idx + (int64_t)g * mn;
+  for (int j = 0; j < cpt; ++j)
+    if (keep >> j & 1) out[before++] = c0 + j;
+  if (tid == 0) a.sel_count[g] = total;
+}
+
+}  // namespace rs3
+
+using namespace rs3;
+
+hipError_t rs3_launch_energy(const void* X, int64_t x_stride, int n_x, int mn, int C, int dtype,
+                             double* e, hipStream_t st) {
+  dim3 grid((mn + 63) / 64, n_x);
+  if (dtype == RS3_BF16)
+    hipLaunchKernelGGL(k_energy<bf16_t>, grid, dim3(64), 0, st, (const bf16_t*)X, x_stride, mn, C, e);
+  else
+    hipLaunchKernelGGL(k_energy<float>, grid, dim3(64), 0, st, (const float*)X, x_stride, mn, C, e);
+  return hipGetLastError();
+}
+
+hipError_t rs3_select_setup() {
+  return hipFuncSetAttribute((const void*)k_select, hipFuncAttributeMaxDynamicSharedMemorySize,
+                             3 * RS3_MAX_MN);
+}
+
+hipError_t rs3_launch_select(const Rs3SelectArgs& a, int n_groups, hipStream_t st) {
+  const int mn = a.m * a.n;
+  hipLaunchKernelGGL(k_select, dim3(n_groups), dim3(SEL_THREADS), 3 * mn, st, a);
+  return hipGetLastError();
+}

@@ -1,0 +1,84 @@
+"""Test-side drivers: the fp64 oracle pipeline and the HIP session run on the
+same seeded inputs (test infrastructure)."""
+from __future__ import annotations
+
+import math
+from typing import List
+
+import numpy as np
+
+import oracle
+from workloads import Config, storage_to_f64
+
+TOL = {"bf16": 2e-2, "f32": 1e-4}
+
+
+def grid_masks(cfg: Config, masks_px: np.ndarray) -> np.ndarray:
+    """Pixel masks [n_obj][m*s][n*s] -> token-grid masks [n_obj][mn] (down_s)."""
+    return np.stack([oracle.down_s(masks_px[o], cfg.s).reshape(-1).astype(np.uint8)
+                     for o in range(masks_px.shape[0])])
+
+
+class OraclePipeline:
+    def __init__(self, cfg: Config, W):
+        self.cfg = cfg
+        self.W = {k: storage_to_f64(getattr(W, k), cfg.dtype) for k in ("Wq", "Wk", "Wv", "Wo")}
+        npdt = np.uint16 if cfg.dtype == "bf16" else np.float32
+        self.tracks: List[oracle.Track] = [oracle.Track() for _ in range(cfg.n_obj)]
+        self.banks = [oracle.RingBank(cfg.cap, cfg.f_max, cfg.n_pin, cfg.d_kv, npdt) for _ in range(cfg.n_obj)]
+
+    def select(self, masks_px, X_store, k, seed_box=False):
+        cfg = self.cfg
+        X = storage_to_f64(X_store, cfg.dtype)
+        sel, priors, self.tracks = oracle.select_queries(masks_px, cfg.s, cfg.m, cfg.n, self.tracks, X, k,
+                                                         cfg.r_s, cfg.c, seed_box, cfg.union_objects)
+        return sel, priors
+
+    def commit(self, K_store, V_store, masks_px, t, pin, fall_min=0, fall_max=None):
+        gm = grid_masks(self.cfg, masks_px)
+        return [self.banks[o].commit(K_store[o], V_store[o], gm[o], t, pin, fall_min, fall_max)
+                for o in range(self.cfg.n_obj)]
+
+    def readout_rows(self, X_store, o, rows):
+        """Oracle y for cell indices `rows` of object o (float64 [len][C])."""
+        cfg = self.cfg
+        xi = 0 if X_store.shape[0] == 1 else o
+        X = storage_to_f64(X_store[xi], cfg.dtype)
+        K, V, _ = self.banks[o].key_rows()
+        Kf, Vf = storage_to_f64(K, cfg.dtype), storage_to_f64(V, cfg.dtype)
+        Y = oracle.readout(X, rows, Kf, Vf, self.W["Wq"], self.W["Wk"], self.W["Wv"], self.W["Wo"], cfg.H)
+        return Y[np.asarray(rows, dtype=np.int64)]
+
+    def readout_dense_rows(self, X_store, o, rows):
+        cfg = self.cfg
+        xi = 0 if X_store.shape[0] == 1 else o
+        X = storage_to_f64(X_store[xi], cfg.dtype)[np.asarray(rows, dtype=np.int64)]
+        K, V, _ = self.banks[o].key_rows()
+        Kf, Vf = storage_to_f64(K, cfg.dtype), storage_to_f64(V, cfg.dtype)
+        return oracle.readout_dense(X, Kf, Vf, self.W["Wq"], self.W["Wk"], self.W["Wv"], self.W["Wo"], cfg.H)
+
+
+def compare_bank(gpu_export: dict, ring: oracle.RingBank):
+    ft = ring.frame_table()
+    assert gpu_export["n_frames"] == len(ring.frames), (gpu_export["n_frames"], len(ring.frames))
+    assert gpu_export["pin_end"] == ring.pin_end
+    assert gpu_export["err"] == ring.err
+    assert np.array_equal(gpu_export["frames"], ft), (gpu_export["frames"], ft)
+    K, V, pos = ring.key_rows()
+    assert gpu_export["n_keys"] == K.shape[0]
+    assert np.array_equal(gpu_export["pos"], pos)
+    assert np.array_equal(gpu_export["K"].view(np.uint8), np.ascontiguousarray(K).view(np.uint8))
+    assert np.array_equal(gpu_export["V"].view(np.uint8), np.ascontiguousarray(V).view(np.uint8))
+
+
+def sample_rows(sel: np.ndarray, n: int, seed: int) -> np.ndarray:
+    if len(sel) <= n:
+        return np.asarray(sel)
+    rng = np.random.default_rng(seed)
+    return np.sort(rng.choice(np.asarray(sel), n, replace=False))
+
+
+def max_abs(a, b) -> float:
+    if a.size == 0:
+        return 0.0
+    return float(np.max(np.abs(np.asarray(a, np.float64) - np.asarray(b, np.float64))))

@@ -1,0 +1,166 @@
+"""Edge cases of the HIP path against the oracle: empty and full masks, the
+lost-object streak, k = 0 and k = mn, tied energies, stride-2 masks, the
+write fall-through, capacity errors, zero-length frames and invalid
+selection lists."""
+from dataclasses import replace
+
+import numpy as np
+import pytest
+
+from harness import OraclePipeline, compare_bank
+from workloads import CONFIGS, make_weights, to_storage
+import oracle
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+
+def _dev(a):
+    from paper_2608_22526_amd.session import to_device
+    return to_device(a)
+
+
+def _host(t):
+    from paper_2608_22526_amd.session import to_host
+    return to_host(t)
+
+
+def _session(cfg, W, **kw):
+    from paper_2608_22526_amd.session import Session
+    return Session(m=cfg.m, n=cfg.n, s=cfg.s, C=cfg.C, H=cfg.H, d_kv=cfg.d_kv, dtype=cfg.dtype,
+                   n_obj=cfg.n_obj, shared_x=cfg.shared_x, union_objects=cfg.union_objects, cap=cfg.cap,
+                   f_max=cfg.f_max, n_pin=cfg.n_pin, weights=W, r_s=cfg.r_s, c=cfg.c, **kw)
+
+
+SMALL = replace(CONFIGS["sam2_single"], m=24, n=20, C=64, H=1, d_h=64, d_kv=16, f_max=4, cap_frames=3)
+
+
+def _check_select(sess, orc, masks, X, k, seed_box=False):
+    prior = torch.zeros((sess.n_groups, sess.mn), dtype=torch.uint8, device="cuda")
+    sess.select(_dev(masks), _dev(X), k, seed_box=seed_box, prior_out=prior)
+    sel, pri = orc.select(masks, X, k, seed_box=seed_box)
+    torch.cuda.synchronize()
+    cnt, idx = _host(sess.sel_count), _host(sess.sel_idx)
+    for g in range(sess.n_groups):
+        assert cnt[g] == len(sel[g])
+        assert np.array_equal(idx[g, :cnt[g]], sel[g])
+    assert np.array_equal(_host(prior).astype(bool), pri)
+    exp_tracks = np.array([t.as_list() for t in orc.tracks], dtype=np.int32)
+    assert np.array_equal(sess.track.export(), exp_tracks)
+    return sel
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_streak_empty_full_and_k_extremes(dtype):
+    cfg = replace(SMALL, dtype=dtype)
+    W = make_weights(cfg)
+    sess, orc = _session(cfg, W), OraclePipeline(cfg, W)
+    rng = np.random.default_rng(0)
+    X = to_storage(rng.standard_normal((1, cfg.mn, cfg.C)).astype(np.float32), dtype)
+    m0 = np.zeros((1, cfg.m, cfg.n), np.uint8)
+    m0[0, 5:9, 3:12] = 1
+    empty = np.zeros_like(m0)
+    full = np.ones_like(m0)
+    _check_select(sess, orc, m0, X, [50])
+    for t in range(20):                   # streak grows to the cap and stays
+        _check_select(sess, orc, empty, X, [cfg.mn])
+    _check_select(sess, orc, full, X, [0])          # k = 0
+    _check_select(sess, orc, full, X, [cfg.mn])     # keep everything
+    _check_select(sess, orc, m0, X, [7], seed_box=True)
+    one = np.zeros_like(m0)
+    one[0, 0, cfg.n - 1] = 1
+    _check_select(sess, orc, one, X, [3])
+
+
+def test_tied_energies():
+    cfg = SMALL
+    W = make_weights(cfg)
+    sess, orc = _session(cfg, W), OraclePipeline(cfg, W)
+    rng = np.random.default_rng(1)
+    base = rng.standard_normal((4, cfg.C)).astype(np.float32)
+    X = to_storage(base[rng.integers(0, 4, size=cfg.mn)][None], "bf16")   # four distinct energies
+    full = np.ones((1, cfg.m, cfg.n), np.uint8)
+    for k in (1, 13, 100, 333, cfg.mn - 1):
+        _check_select(sess, orc, full, X, [k])
+
+
+def test_stride2_masks_and_groups():
+    cfg = replace(SMALL, s=2, n_obj=3, union_objects=False)
+    W = make_weights(cfg)
+    sess, orc = _session(cfg, W), OraclePipeline(cfg, W)
+    rng = np.random.default_rng(2)
+    X = to_storage(rng.standard_normal((1, cfg.mn, cfg.C)).astype(np.float32), "bf16")
+    masks = (rng.random((3, cfg.m * 2, cfg.n * 2)) < 0.05).astype(np.uint8)
+    masks[1] = 0
+    for t in range(3):
+        _check_select(sess, orc, masks, X, [40, 60, 80])
+        masks = np.roll(masks, 1, axis=0)
+    cfgu = replace(cfg, union_objects=True)
+    sess2, orc2 = _session(cfgu, W), OraclePipeline(cfgu, W)
+    _check_select(sess2, orc2, masks, X, [90])
+
+
+def test_commit_ring_rules_fall_through_and_capacity():
+    cfg = replace(SMALL, m=8, n=8, cap_frames=2, f_max=4)   # cap = 128 rows
+    W = make_weights(cfg)
+    sess, orc = _session(cfg, W), OraclePipeline(cfg, W)
+    rng = np.random.default_rng(3)
+    npdt = np.uint16
+    sizes = [10, 30, 0, 64, 25, 40, 64, 64, 3, 0, 50]
+    for t, L in enumerate(sizes):
+        K = to_storage(rng.standard_normal((1, cfg.mn, cfg.d_kv)).astype(np.float32), "bf16")
+        V = to_storage(rng.standard_normal((1, cfg.mn, cfg.d_kv)).astype(np.float32), "bf16")
+        mask = np.zeros((1, cfg.m, cfg.n), np.uint8)
+        mask.reshape(-1)[rng.choice(cfg.mn, L, replace=False)] = 1
+        fmin, fmax = (4, 60) if t % 3 == 2 else (0, cfg.mn)
+        pin = t == 0
+        sess.commit(_dev(K), _dev(V), _dev(mask), t, pin, fmin, fmax)
+        counts = orc.commit(K, V, mask, t, pin, fmin, fmax)
+        torch.cuda.synchronize()
+        assert _host(sess.kept_count).tolist() == counts
+        compare_bank(sess.banks[0].export(), orc.banks[0])
+    # a frame longer than cap - pin_end is a capacity error; the bank stays
+    cfg2 = replace(cfg, cap_frames=1)
+    sess2, orc2 = _session(cfg2, W), OraclePipeline(cfg2, W)
+    K = to_storage(rng.standard_normal((1, cfg.mn, cfg.d_kv)).astype(np.float32), "bf16")
+    m_half = np.zeros((1, cfg.m, cfg.n), np.uint8)
+    m_half[0, :2] = 1
+    full = np.ones_like(m_half)
+    for t, (mk, pin) in enumerate([(m_half, True), (full, False), (m_half, False)]):
+        sess2.commit(_dev(K), _dev(K), _dev(mk), t, pin)
+        orc2.commit(K, K, mk, t, pin)
+        torch.cuda.synchronize()
+        compare_bank(sess2.banks[0].export(), orc2.banks[0])
+    assert sess2.banks[0].error() == oracle.RS3_E_CAPACITY
+
+
+def test_pin_misuse_rejected_on_host():
+    from paper_2608_22526_amd import Rs3Error
+    cfg = replace(SMALL, m=8, n=8)
+    W = make_weights(cfg)
+    sess = _session(cfg, W)
+    K = _dev(np.zeros((1, cfg.mn, cfg.d_kv), np.uint16))
+    mask = _dev(np.ones((1, cfg.m, cfg.n), np.uint8))
+    sess.commit(K, K, mask, 0, False)
+    with pytest.raises(Rs3Error):
+        sess.commit(K, K, mask, 1, True)
+
+
+def test_invalid_selection_sets_error_and_skips_rows():
+    cfg = SMALL
+    W = make_weights(cfg)
+    sess = _session(cfg, W)
+    rng = np.random.default_rng(4)
+    K = to_storage(rng.standard_normal((1, cfg.mn, cfg.d_kv)).astype(np.float32), "bf16")
+    sess.commit(_dev(K), _dev(K), _dev(np.ones((1, cfg.m, cfg.n), np.uint8)), 0, True)
+    X = _dev(to_storage(rng.standard_normal((1, cfg.mn, cfg.C)).astype(np.float32), "bf16"))
+    sess.sel_idx[0, :4] = torch.tensor([3, 2, 7, cfg.mn + 5], dtype=torch.int32)   # not ascending, out of range
+    sess.sel_count[0] = 4
+    Y = X.clone()
+    sess.readout(Y, Y)
+    torch.cuda.synchronize()
+    assert sess.banks[0].error(clear=True) == oracle.RS3_E_INVALID
+    assert sess.banks[0].error() == 0
+    Yh, Xh = _host(Y), _host(X)
+    # rows 2 (non-ascending) and the out-of-range entry are skipped
+    assert np.array_equal(Yh[0, 2], Xh[0, 2])
