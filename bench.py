@@ -1,0 +1,269 @@
+#!/usr/bin/env python3
+"""Benchmark of one frame of the read-sparse readout + store-sparse commit.
+
+One step = select_queries + readout + commit for every object of one frame,
+on synthetic inputs already resident in HBM, against a bank in steady state.
+Default workload: 64x64 token grid, d_model 256, one head of 256, bank k/v
+width 64, bf16, bank of 1 pinned conditioning frame + 6 recent frames pruned
+to in-mask tokens, read keep ratio rho ~ U[0.15, 0.30] per frame.
+
+Prints ONE JSON line (rank 0) with frames/s, the attention kernel's roofline
+fraction (kernel durations from HIP events around its launches, live) and the
+fp64 oracle's frames/s on this host as a reported CPU baseline.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import subprocess
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "readout+commit frames/s at 64x64 grid, 7-frame bank; MFMA util %, HBM GB/s"
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+N_DISTINCT = 40   # distinct resident input frames cycled through by the steps
+
+
+def _describe(cfg) -> str:
+    obj = "1 object" if cfg.n_obj == 1 else "%d objects on one shared grid" % cfg.n_obj
+    rho = ("rho %.2f" % cfg.rho) if cfg.rho is not None else ("rho ~ U[%.2f, %.2f]" % (cfg.rho_lo, cfg.rho_hi))
+    return ("%s: %dx%d grid, %s, d_model %d, %d head(s) x %d, k/v %d, %s, bank %d pinned + %d recent frames "
+            "(mask area %.2f-%.2f), %s" % (cfg.name, cfg.m, cfg.n, obj, cfg.C, cfg.H, cfg.d_h, cfg.d_kv, cfg.dtype,
+                                           cfg.n_pin, cfg.f_max - cfg.n_pin, cfg.area_lo, cfg.area_hi, rho))
+
+
+# ---------------------------------------------------------------------------
+# CPU baseline (child process, fp64 oracle, one thread)
+# ---------------------------------------------------------------------------
+def cpu_child(workload: str, frames: int):
+    import numpy as np  # noqa: F401  (threads pinned by the parent's env)
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from harness import OraclePipeline
+    from workloads import CONFIGS, make_frame, make_sequence, make_weights
+    cfg = CONFIGS[workload]
+    n_pre = cfg.f_max
+    seq = make_sequence(cfg, n_frames=n_pre + frames + 1)
+    W = make_weights(cfg)
+    orc = OraclePipeline(cfg, W)
+    for t in range(n_pre):
+        fr = make_frame(cfg, t)
+        orc.commit(fr.Kmem, fr.Vmem, seq.masks[t], t, t < cfg.n_pin)
+    t0 = time.perf_counter()
+    for t in range(n_pre, n_pre + frames):
+        fr = make_frame(cfg, t)
+        sel, _ = orc.select(seq.read_mask(cfg, t), fr.X, seq.k[t])
+        for o in range(cfg.n_obj):
+            g = 0 if cfg.union_objects else o
+            orc.readout_rows(fr.X, o, sel[g])
+        orc.commit(fr.Kmem, fr.Vmem, seq.masks[t], t, False)
+    dt = time.perf_counter() - t0
+    print(json.dumps({"seconds": dt, "frames": frames, "prefill": n_pre}))
+
+
+def cpu_baseline(workload: str, frames: int):
+    env = dict(os.environ)
+    for v in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS", "NUMEXPR_NUM_THREADS"):
+        env[v] = "1"
+    env["HIP_VISIBLE_DEVICES"] = ""
+    p = subprocess.run([sys.executable, os.path.abspath(__file__), "--cpu-child", "--workload", workload,
+                        "--cpu-frames", str(frames)], stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True,
+                       env=env, timeout=600)
+    if p.returncode != 0:
+        return {"value": None, "unit": "frames/s", "cores": 1, "kind": "oracle", "error": p.stderr[-500:]}
+    r = json.loads(p.stdout.strip().splitlines()[-1])
+    cpu = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"value": r["frames"] / r["seconds"], "unit": "frames/s", "cores": 1, "kind": "oracle",
+            "sample": "%d frames (select + readout of every selected row + commit) after a %d-frame prefill, "
+                      "fp64 NumPy, 1 thread; host %s with %d cores available"
+                      % (r["frames"], r.get("prefill", 0), cpu, len(os.sched_getaffinity(0))),
+            "seconds": r["seconds"]}
+
+
+# ---------------------------------------------------------------------------
+# GPU run
+# ---------------------------------------------------------------------------
+def _kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("readout.hip", "rs3_internal.h"):
+        h.update(open(os.path.join(ROOT, "paper_2608_22526_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def _traffic(kernel: str):
+    """HBM bytes per launch from the committed counter summary, if it was
+    taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", "traffic_%s.json" % kernel)
+    try:
+        d = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    if d.get("source_hash") != _kernel_source_hash():
+        return None
+    return d.get("bytes_per_launch")
+
+
+def gpu_run(args):
+    import numpy as np
+    import torch
+    import paper_2608_22526_amd as rs3
+    from paper_2608_22526_amd.session import Session, to_device
+    from workloads import CONFIGS, make_frame, make_sequence, make_weights
+
+    cfg = CONFIGS[args.workload]
+    dev = "cuda"
+    n_pre = cfg.f_max
+    seq = make_sequence(cfg, n_frames=n_pre + N_DISTINCT)
+    W = make_weights(cfg)
+    k_all = [max(ks) for ks in seq.k]
+    sess = Session(m=cfg.m, n=cfg.n, s=cfg.s, C=cfg.C, H=cfg.H, d_kv=cfg.d_kv, dtype=cfg.dtype,
+                   n_obj=cfg.n_obj, shared_x=cfg.shared_x, union_objects=cfg.union_objects, cap=cfg.cap,
+                   f_max=cfg.f_max, n_pin=cfg.n_pin, weights=W, r_s=cfg.r_s, c=cfg.c, max_sel=max(k_all),
+                   n_splits=args.splits)
+    # resident inputs
+    frames = []
+    for t in range(n_pre + N_DISTINCT):
+        fr = make_frame(cfg, t)
+        frames.append(dict(X=to_device(fr.X), K=to_device(fr.Kmem), V=to_device(fr.Vmem),
+                           mask=to_device(seq.masks[t]), rmask=to_device(seq.read_mask(cfg, t)), k=seq.k[t],
+                           max_sel=max(seq.k[t])))
+    in_place = cfg.n_obj == 1
+    Y = None if in_place else torch.empty((cfg.n_obj, cfg.mn, cfg.C), dtype=frames[0]["X"].dtype, device=dev)
+    for t in range(n_pre):
+        f = frames[t]
+        sess.commit(f["K"], f["V"], f["mask"], t, t < cfg.n_pin)
+
+    step_t = [n_pre]
+
+    def step(record=None):
+        t = step_t[0]
+        f = frames[n_pre + (t - n_pre) % N_DISTINCT]
+        sess.select(f["rmask"], f["X"], f["k"])
+        if record is not None:
+            cnt = sess.sel_count.cpu().numpy()
+            nk = [b.info()["n_keys"] for b in sess.banks]
+            g = [0 if cfg.union_objects else o for o in range(cfg.n_obj)]
+            record.append(dict(sel=[int(cnt[g[o]]) for o in range(cfg.n_obj)], n_keys=nk))
+        if in_place:
+            sess.readout(f["X"], f["X"], max_sel=f["max_sel"])
+        else:
+            sess.readout(f["X"], Y, max_sel=f["max_sel"])
+        sess.commit(f["K"], f["V"], f["mask"], t, False)
+        step_t[0] += 1
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    # pass A: frames/s, no instrumentation
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record()
+    for _ in range(args.steps):
+        step()
+    ev1.record()
+    torch.cuda.synchronize()
+    ms_total = ev0.elapsed_time(ev1)
+    ms_step = ms_total / args.steps
+    fps = 1000.0 / ms_step
+    # pass B: per-kernel durations from HIP events around each launch
+    rs3.profile_enable(True, 16 * args.steps + 64)
+    rs3.profile_reset()
+    recs = []
+    for _ in range(args.steps):
+        step(record=recs)
+    torch.cuda.synchronize()
+    rep = rs3.profile_report()
+    rs3.profile_enable(False)
+    errs = [b.error() for b in sess.banks]
+
+    D = cfg.D
+    attn_ms, attn_n = rep["attn"]
+    flops = sum(4.0 * r["sel"][o] * r["n_keys"][o] * D for r in recs for o in range(cfg.n_obj))
+    sel_tot = sum(sum(r["sel"]) for r in recs)
+    per_launch_flops = flops / max(attn_n, 1)
+    avg_attn_s = attn_ms / 1000.0 / max(attn_n, 1)
+    achieved_tflops = per_launch_flops / avg_attn_s / 1e12 if attn_n else 0.0
+    kernels = {}
+    for name, (ms, n) in rep.items():
+        if n and not name.startswith("_"):
+            kernels[name] = {"launches": n, "avg_us": 1000.0 * ms / n, "us_per_step": 1000.0 * ms / args.steps}
+    kernel_sum_us = sum(v["us_per_step"] for v in kernels.values())
+    traffic = _traffic("attn_" + cfg.name)
+    out = {
+        "metric": METRIC,
+        "value": fps,
+        "unit": "frames/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {"workload": _describe(cfg), "grid": "%dx%d" % (cfg.m, cfg.n), "n_obj": cfg.n_obj,
+                   "bank_frames": cfg.f_max, "d_model": cfg.C, "heads": cfg.H, "d_head": cfg.d_h,
+                   "d_kv": cfg.d_kv, "eager_launches": True, "readout": "in place" if in_place else "out of place"},
+        "roofline": {"bound": "mfma", "achieved": achieved_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved_tflops / PEAK_BF16_TFLOPS,
+                     "traffic": traffic,
+                     "kernel": "k_attn (split-KV attention)",
+                     "algorithmic_flops_per_launch": per_launch_flops,
+                     "avg_launch_us": avg_attn_s * 1e6},
+        "extra": {
+            "query_tokens_per_s": sel_tot / args.steps * fps,
+            "grid_tokens_per_s": cfg.n_obj * cfg.mn * fps,
+            "mean_selected_per_frame": sel_tot / args.steps,
+            "mean_bank_keys": sum(sum(r["n_keys"]) for r in recs) / len(recs) / cfg.n_obj,
+            "kernels": kernels,
+            "kernel_sum_us_per_step": kernel_sum_us,
+            "bank_errors": errs,
+            "splits": sess.n_splits,
+        },
+    }
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="sam2_single")
+    ap.add_argument("--splits", type=int, default=0)
+    ap.add_argument("--cpu-frames", type=int, default=12)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-child", action="store_true")
+    args = ap.parse_args()
+    if args.cpu_child:
+        cpu_child(args.workload, args.cpu_frames)
+        return
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one MI355X: the path runs on a single GPU (objects or bank frames would be "
+              "sharded across GPUs with no exchange, which this benchmark does not launch). Use --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+    out = gpu_run(args)
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_frames)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -167,12 +167,13 @@ rs3_status rs3_select_queries(const rs3_grid* g, int32_t n_obj, const uint8_t* m
  * sel_idx/sel_count : as produced by rs3_select_queries; sel_stride = m*n
  *          for per-object lists or 0 for one shared list
  * max_sel: upper bound on every sel_count used (host grid size), <= m*n
- * n_splits: key splits per query tile (0 = automatic)
+ * n_splits: key splits per query tile (0 = automatic); n_splits*H <= 512
  * Y      : [n_obj][m*n][C] with stride y_obj_stride (elements); may equal X
  *          (in place) only when n_obj == 1 or X is per object with the same
  *          stride.  y_fp32 = 1 writes Y as fp32 for diagnostics (never in
  *          place), otherwise Y has the layer dtype.
- * ws     : device workspace of at least rs3_readout_workspace_size() bytes */
+ * ws     : device workspace of at least rs3_readout_workspace_size() bytes (a
+ *          size queried for max_sel also serves every smaller max_sel) */
 rs3_status rs3_readout_workspace_size(const rs3_layer* L, int32_t n_obj, int32_t max_sel,
                                       int32_t n_splits, size_t* bytes);
 rs3_status rs3_readout(const rs3_layer* L, const rs3_grid* g, int32_t n_obj,
@@ -195,6 +196,30 @@ rs3_status rs3_commit(rs3_bank* const* banks /*[host]*/, int32_t n_obj, const rs
                       const void* Kmem, const void* Vmem, int64_t kv_obj_stride,
                       const uint8_t* masks, int32_t t, int32_t pin, int32_t fall_min,
                       int32_t fall_max, int32_t* kept_count, void* stream);
+
+/* ---- per-kernel timing (diagnostics) ---------------------------------------
+ * rs3_profile_enable(1, max_launches) creates a pool of HIP events; while
+ * enabled, each kernel launched by the library is bracketed by two events on
+ * its stream (event records only: nothing is allocated or synchronised in the
+ * timed calls; launches beyond the pool are not timed and are counted as
+ * dropped).  rs3_profile_report waits for the recorded events and fills
+ * total_ms[RS3_K_COUNT] and launches[RS3_K_COUNT] (host arrays) with the
+ * accumulated kernel durations per kernel id; rs3_profile_reset clears them. */
+enum {
+  RS3_K_ENERGY = 0,        /* token energies */
+  RS3_K_SELECT = 1,        /* prior + top-k + compaction */
+  RS3_K_COMMIT_PLACE = 2,  /* mask compaction + ring placement + tile list */
+  RS3_K_COMMIT_APPEND = 3, /* row copy + K/V projection */
+  RS3_K_COPY = 4,          /* X -> Y copy for out-of-place readout */
+  RS3_K_QPROJ = 5,         /* gather + query projection */
+  RS3_K_ATTN = 6,          /* split-KV attention */
+  RS3_K_COMBINE = 7,       /* split merge + W_o + residual + scatter */
+  RS3_K_READOUT_F32 = 8,   /* fp32 readout */
+  RS3_K_COUNT = 9
+};
+rs3_status rs3_profile_enable(int32_t on, int32_t max_launches);
+rs3_status rs3_profile_report(double* total_ms, int64_t* launches, int64_t* dropped);
+rs3_status rs3_profile_reset(void);
 
 #ifdef __cplusplus
 }

@@ -11,4 +11,5 @@ from ._binding import (  # noqa: F401
     Track, Layer, Bank,
     select_workspace_size, select_queries,
     readout_workspace_size, readout, commit,
+    KERNEL_NAMES, profile_enable, profile_reset, profile_report,
 )

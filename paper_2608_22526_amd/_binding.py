@@ -58,7 +58,13 @@ _SIGS = {
                             c_i32, c_vp, c_i64, c_i32, c_vp, c_sz, c_vp]),
     "rs3_commit": (c_i32, [c_vp, c_i32, ctypes.POINTER(Grid), c_vp, c_vp, c_i64, c_vp, c_i32, c_i32, c_i32,
                            c_i32, c_vp, c_vp]),
+    "rs3_profile_enable": (c_i32, [c_i32, c_i32]),
+    "rs3_profile_report": (c_i32, [c_vp, c_vp, c_vp]),
+    "rs3_profile_reset": (c_i32, []),
 }
+
+KERNEL_NAMES = ["energy", "select", "commit_place", "commit_append", "copy", "qproj", "attn", "combine",
+                "readout_f32"]
 
 _lib = None
 
@@ -172,6 +178,12 @@ class Bank:
         return dict(hdr=hdr, n_frames=nf, pin_end=int(hdr[1]), err=int(hdr[2]), n_keys=nk,
                     frames=frames[:nf].copy(), K=K[:nk].copy(), V=V[:nk].copy(), pos=pos[:nk].copy())
 
+    def info(self) -> dict:
+        """Header only (n_frames, pin_end, err, n_keys); synchronises."""
+        hdr = np.zeros(RS3_BANK_HDR_WORDS, np.int32)
+        _check(lib().rs3_bank_export(self.h, hdr.ctypes.data, None, None, None, None), "rs3_bank_export")
+        return dict(n_frames=int(hdr[0]), pin_end=int(hdr[1]), err=int(hdr[2]), n_keys=int(hdr[3]))
+
     def error(self, clear: bool = False) -> int:
         e = np.zeros(1, np.int32)
         _check(lib().rs3_bank_error(self.h, e.ctypes.data, int(clear)), "rs3_bank_error")
@@ -231,3 +243,23 @@ def commit(banks: Sequence[Bank], grid, Kmem, Vmem, kv_obj_stride: int, masks, t
     _check(lib().rs3_commit(ctypes.cast(harr, c_vp), len(banks), ctypes.byref(_grid(grid)), _ptr(Kmem),
                             _ptr(Vmem), kv_obj_stride, _ptr(masks), t, pin, fall_min, fall_max,
                             _ptr(kept_count), _stream(stream)), "rs3_commit")
+
+
+def profile_enable(on: bool, max_launches: int = 65536):
+    _check(lib().rs3_profile_enable(int(on), max_launches), "rs3_profile_enable")
+
+
+def profile_reset():
+    _check(lib().rs3_profile_reset(), "rs3_profile_reset")
+
+
+def profile_report() -> dict:
+    """{kernel name: (total ms, launches)} accumulated since the last reset."""
+    n = len(KERNEL_NAMES)
+    ms = np.zeros(n, np.float64)
+    cnt = np.zeros(n, np.int64)
+    dropped = np.zeros(1, np.int64)
+    _check(lib().rs3_profile_report(ms.ctypes.data, cnt.ctypes.data, dropped.ctypes.data), "rs3_profile_report")
+    out = {KERNEL_NAMES[i]: (float(ms[i]), int(cnt[i])) for i in range(n)}
+    out["_dropped"] = (0.0, int(dropped[0]))
+    return out

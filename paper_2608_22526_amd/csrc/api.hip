@@ -44,6 +44,7 @@ rs3_status ensure_setup() {
   if (setup_done) return RS3_OK;
   hipError_t e = rs3_readout_setup();
   if (e == hipSuccess) e = rs3_select_setup();
+  if (e == hipSuccess) e = rs3_commit_setup();
   if (e != hipSuccess) return RS3_E_DEVICE;
   setup_done = true;
   return RS3_OK;
@@ -68,13 +69,13 @@ std::vector<uint8_t> transpose(const void* src, int rows, int cols, size_t es) {
   return out;
 }
 
-int auto_splits(int n_obj, int H, int n_qt, int n_tiles_cap) {
+// Key splits per query tile: enough attention workgroups to cover the 256
+// CUs once (each workgroup holds 128 KB of LDS, so one fits per CU).
+int auto_splits(int n_obj, int H, int n_qt) {
   const int base = n_obj * H * n_qt;
-  int S = (512 + base - 1) / base;
+  int S = (256 + base - 1) / base;
   if (S > 64) S = 64;
-  int max_by_tiles = n_tiles_cap / 2;
-  if (max_by_tiles < 1) max_by_tiles = 1;
-  if (S > max_by_tiles) S = max_by_tiles;
+  if (S * H > RS3_MAX_SPLITS_X_HEADS) S = RS3_MAX_SPLITS_X_HEADS / H;
   if (S < 1) S = 1;
   return S;
 }
@@ -369,21 +370,32 @@ static void readout_shape(const rs3_layer* L, int32_t n_obj, int32_t max_sel, in
 static int splits_for(const rs3_layer* L, int32_t n_obj, int32_t max_sel, int32_t n_splits) {
   if (n_splits > 0) return n_splits;
   const int n_qt = (max_sel + 127) / 128;
-  return auto_splits(n_obj, L->dev.H, n_qt > 0 ? n_qt : 1, 1 << 20);
+  return auto_splits(n_obj, L->dev.H, n_qt > 0 ? n_qt : 1);
 }
 
 rs3_status rs3_readout_workspace_size(const rs3_layer* L, int32_t n_obj, int32_t max_sel, int32_t n_splits,
                                       size_t* bytes) {
-  if (!L || !bytes || n_obj <= 0 || n_obj > RS3_MAX_OBJ || max_sel < 0 || n_splits < 0 || n_splits > 256)
+  if (!L || !bytes || n_obj <= 0 || n_obj > RS3_MAX_OBJ || max_sel < 0 || n_splits < 0 ||
+      n_splits * L->dev.H > RS3_MAX_SPLITS_X_HEADS)
     return RS3_E_INVALID;
   if (L->dev.dtype == RS3_F32) {
     *bytes = 0;
     return RS3_OK;
   }
-  const int S = splits_for(L, n_obj, max_sel, n_splits);
-  size_t q, o, ml;
-  readout_shape(L, n_obj, max_sel, S, &q, &o, &ml);
-  *bytes = q + o + ml;
+  // The split count depends on max_sel, so take the largest layout over every
+  // max_sel' <= max_sel (within a 128-row tile count the largest max_sel'
+  // needs the most).
+  size_t best = 0;
+  const int n_qt_max = (max_sel + 127) / 128;
+  for (int qt = 0; qt <= n_qt_max; ++qt) {
+    const int ms = qt == n_qt_max ? max_sel : qt * 128;
+    if (ms > max_sel) continue;
+    const int S = splits_for(L, n_obj, ms, n_splits);
+    size_t q, o, ml;
+    readout_shape(L, n_obj, ms, S, &q, &o, &ml);
+    if (q + o + ml > best) best = q + o + ml;
+  }
+  *bytes = best;
   return RS3_OK;
 }
 
@@ -395,7 +407,8 @@ rs3_status rs3_readout(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, con
   if (n_obj <= 0 || n_obj > RS3_MAX_OBJ) return RS3_E_INVALID;
   const LayerDev& ld = L->dev;
   const int mn = g->m * g->n;
-  if (max_sel < 0 || max_sel > mn || n_splits < 0 || n_splits > 256) return RS3_E_INVALID;
+  if (max_sel < 0 || max_sel > mn || n_splits < 0 || n_splits * ld.H > RS3_MAX_SPLITS_X_HEADS)
+    return RS3_E_INVALID;
   if (sel_stride != 0 && sel_stride != mn) return RS3_E_INVALID;
   const int64_t grid_elems = (int64_t)mn * ld.C;
   if (x_obj_stride < 0 || (x_obj_stride != 0 && x_obj_stride < grid_elems)) return RS3_E_INVALID;
@@ -464,6 +477,8 @@ rs3_status rs3_commit(rs3_bank* const* banks, int32_t n_obj, const rs3_grid* g, 
       if (banks[p] == banks[o]) return RS3_E_INVALID;
     if (pin && (banks[o]->unpinned_seen || banks[o]->pin_calls >= banks[o]->host.n_pin)) return RS3_E_INVALID;
   }
+  rs3_status st0 = ensure_setup();
+  if (st0 != RS3_OK) return st0;
   Rs3CommitArgs a;
   memset(&a, 0, sizeof(a));
   for (int o = 0; o < n_obj; ++o) a.banks[o] = banks[o]->d_desc;

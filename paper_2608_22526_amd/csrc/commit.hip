@@ -198,12 +198,17 @@ __global__ __launch_bounds__(CP_THREADS) void k_commit_place(Rs3CommitArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// append: bf16, 256 threads, 64 rows per workgroup.
-//   K^ tile rows: C = A B, A = kept K rows (64 x d_kv), B = W_k (d_kv x D):
+// append: bf16, 256 threads, 64 rows per workgroup.  The kept rows are read
+// once (16-byte loads) into LDS and written to the raw ring from the same
+// registers; the projections then read their row operands from LDS:
+//   K^ rows: C = A B, A = kept K rows (64 x d_kv), B = W_k (d_kv x D):
 //     lane holds column d, rows = keys  -> Khat[tile][h][key][d%d_h]
 //   V^ as its transpose: C = W_v^T (D x d_kv) V^T (d_kv x 64):
 //     lane holds column = key, rows = d -> Vhat[tile][h][d%d_h][vslot(key)]
+// Dynamic LDS: 2 * 64 * (d_kv + 8) bf16.
 __global__ __launch_bounds__(256) void k_commit_append_bf16(Rs3CommitArgs a) {
+  extern __shared__ __attribute__((aligned(16))) bf16_t rows_lds[];
+  __shared__ int spos[64];
   const int o = blockIdx.x;
   BankDev& b = *a.banks[o];
   const int L = b.hdr[HDR_PLEN];
@@ -212,21 +217,33 @@ __global__ __launch_bounds__(256) void k_commit_append_bf16(Rs3CommitArgs a) {
   const int start = b.hdr[HDR_PSTART];
   const int rows = min(64, L - r0);
   const int d_kv = b.d_kv, d_h = b.d_h, H = b.H, D = H * d_h;
+  const int lg_dh = 31 - __clz(d_h);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5;
+  const int RS = d_kv + 8;  // padded LDS row
+  bf16_t* sK = rows_lds;
+  bf16_t* sV = rows_lds + 64 * RS;
   const bf16_t* Km = (const bf16_t*)a.Kmem + (int64_t)o * a.kv_stride;
   const bf16_t* Vm = (const bf16_t*)a.Vmem + (int64_t)o * a.kv_stride;
   bf16_t* Kr = (bf16_t*)b.Kraw;
   bf16_t* Vr = (bf16_t*)b.Vraw;
-  // raw row copy, 16 bytes per lane step
+  if (tid < 64) spos[tid] = tid < rows ? b.pos[start + r0 + tid] : 0;
+  __syncthreads();
   const int cpr = d_kv / 8;
-  for (int q = tid; q < rows * cpr; q += 256) {
-    int r = q / cpr, c = q - r * cpr;
-    int j = start + r0 + r;
-    int src = b.pos[j];
-    *(u32x4*)(Kr + (int64_t)j * d_kv + 8 * c) = *(const u32x4*)(Km + (int64_t)src * d_kv + 8 * c);
-    *(u32x4*)(Vr + (int64_t)j * d_kv + 8 * c) = *(const u32x4*)(Vm + (int64_t)src * d_kv + 8 * c);
+  for (int q = tid; q < 64 * cpr; q += 256) {
+    const int r = q / cpr, c = q - r * cpr;
+    u32x4 kv = {0, 0, 0, 0}, vv = {0, 0, 0, 0};
+    if (r < rows) {
+      const int src = spos[r];
+      kv = *(const u32x4*)(Km + (int64_t)src * d_kv + 8 * c);
+      vv = *(const u32x4*)(Vm + (int64_t)src * d_kv + 8 * c);
+      const int64_t j = start + r0 + r;
+      *(u32x4*)(Kr + j * d_kv + 8 * c) = kv;
+      *(u32x4*)(Vr + j * d_kv + 8 * c) = vv;
+    }
+    *(u32x4*)(sK + r * RS + 8 * c) = kv;
+    *(u32x4*)(sV + r * RS + 8 * c) = vv;
   }
-  // projections: 2 row blocks x D/32 column blocks, spread over 4 waves
+  __syncthreads();
   const bf16_t* WkT = (const bf16_t*)a.WkT;
   const bf16_t* WvT = (const bf16_t*)a.WvT;
   bf16_t* Kh = (bf16_t*)b.Khat;
@@ -234,39 +251,39 @@ __global__ __launch_bounds__(256) void k_commit_append_bf16(Rs3CommitArgs a) {
   const int nblk = 2 * (D / 32);
   for (int blk = wave; blk < nblk; blk += 4) {
     const int mb = blk & 1, nb = blk >> 1;
-    // key row fed by this lane (A row for K^, B column for V^)
-    const int rr = 32 * mb + (lane & 31);
-    const bool rvalid = rr < rows;
-    const int src = rvalid ? b.pos[start + r0 + rr] : 0;
-    const bf16_t* krow = Km + (int64_t)src * d_kv;
-    const bf16_t* vrow = Vm + (int64_t)src * d_kv;
+    const int rr = 32 * mb + (lane & 31);   // key row fed by this lane
     const int dcol = 32 * nb + (lane & 31);
-    const bf16_t* wk = WkT + (int64_t)dcol * d_kv;
-    const bf16_t* wv = WvT + (int64_t)dcol * d_kv;
+    const bf16_t* krow = sK + rr * RS + 8 * g;
+    const bf16_t* vrow = sV + rr * RS + 8 * g;
+    const bf16_t* wk = WkT + (int64_t)dcol * d_kv + 8 * g;
+    const bf16_t* wv = WvT + (int64_t)dcol * d_kv + 8 * g;
     f32x16 ck = {}, cv = {};
     for (int ks = 0; ks < d_kv; ks += 16) {
-      u32x4 ka = rvalid ? *(const u32x4*)(krow + ks + 8 * g) : u32x4{0, 0, 0, 0};
-      u32x4 va = rvalid ? *(const u32x4*)(vrow + ks + 8 * g) : u32x4{0, 0, 0, 0};
-      u32x4 wkb = *(const u32x4*)(wk + ks + 8 * g);
-      u32x4 wva = *(const u32x4*)(wv + ks + 8 * g);
-      ck = mfma32(ka, wkb, ck);   // rows = keys, cols = d
-      cv = mfma32(wva, va, cv);   // rows = d, cols = keys
+      ck = mfma32(*(const u32x4*)(krow + ks), *(const u32x4*)(wk + ks), ck);   // rows = keys, cols = d
+      cv = mfma32(*(const u32x4*)(wv + ks), *(const u32x4*)(vrow + ks), cv);   // rows = d, cols = keys
     }
+    // K^: row = key (32mb + c_row), column = d (dcol)
+    {
+      const int h = dcol >> lg_dh, dd = dcol & (d_h - 1);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      // K^: row = key (32mb + c_row), column = d (dcol)
-      int kr = 32 * mb + c_row(r, lane);
-      if (kr < rows) {
-        int j = start + r0 + kr;
-        int tile = j >> 6, kk = j & 63, h = dcol / d_h, dd = dcol - h * d_h;
-        Kh[(((int64_t)tile * H + h) * KT + kk) * d_h + dd] = f2bf(ck[r]);
+      for (int r = 0; r < 16; ++r) {
+        const int kr = 32 * mb + c_row(r, lane);
+        if (kr < rows) {
+          const int j = start + r0 + kr;
+          Kh[(((int64_t)(j >> 6) * H + h) * KT + (j & 63)) * d_h + dd] = __builtin_bit_cast(bf16_t, (__bf16)ck[r]);
+        }
       }
-      // V^: row = d (32nb + c_row), column = key (32mb + lane%32)
-      if (rvalid) {
-        int d = 32 * nb + c_row(r, lane);
-        int j = start + r0 + rr;
-        int tile = j >> 6, kk = j & 63, h = d / d_h, dd = d - h * d_h;
-        Vh[(((int64_t)tile * H + h) * d_h + dd) * KT + vslot(kk)] = f2bf(cv[r]);
+    }
+    // V^: row = d (32nb + c_row), column = key (rr)
+    if (rr < rows) {
+      const int j = start + r0 + rr;
+      const int64_t tb = (int64_t)(j >> 6) * H;
+      const int slot = vslot(j & 63);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int d = 32 * nb + c_row(r, lane);
+        const int h = d >> lg_dh, dd = d & (d_h - 1);
+        Vh[((tb + h) * d_h + dd) * KT + slot] = __builtin_bit_cast(bf16_t, (__bf16)cv[r]);
       }
     }
   }
@@ -320,9 +337,13 @@ __global__ __launch_bounds__(256) void k_commit_append_f32(Rs3CommitArgs a) {
 
 using namespace rs3;
 
+hipError_t rs3_commit_setup() {
+  return hipFuncSetAttribute((const void*)k_commit_append_bf16, hipFuncAttributeMaxDynamicSharedMemorySize,
+                             2 * 64 * (256 + 8) * 2);
+}
+
 hipError_t rs3_launch_commit(const Rs3CommitArgs& a, int dtype, int d_kv, int D, int H, int d_h,
                              hipStream_t st) {
-  (void)d_kv;
   (void)D;
   (void)H;
   (void)d_h;
@@ -330,13 +351,14 @@ hipError_t rs3_launch_commit(const Rs3CommitArgs& a, int dtype, int d_kv, int D,
   int f_max = 0;
   // the frame table of every bank fits the largest f_max (checked on the host)
   f_max = 256;
-  hipLaunchKernelGGL(k_commit_place, dim3(a.n_obj), dim3(CP_THREADS), f_max * 16, st, a);
+  RS3_LAUNCH(RS3_K_COMMIT_PLACE, st, k_commit_place, dim3(a.n_obj), dim3(CP_THREADS), f_max * 16, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 grid(a.n_obj, (mn + 63) / 64);
   if (dtype == RS3_BF16)
-    hipLaunchKernelGGL(k_commit_append_bf16, grid, dim3(256), 0, st, a);
+    RS3_LAUNCH(RS3_K_COMMIT_APPEND, st, k_commit_append_bf16, grid, dim3(256), (size_t)2 * 64 * (d_kv + 8) * 2,
+               st, a);
   else
-    hipLaunchKernelGGL(k_commit_append_f32, grid, dim3(256), 0, st, a);
+    RS3_LAUNCH(RS3_K_COMMIT_APPEND, st, k_commit_append_f32, grid, dim3(256), 0, st, a);
   return hipGetLastError();
 }

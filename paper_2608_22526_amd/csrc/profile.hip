@@ -1,0 +1,107 @@
+// Optional per-kernel timing with HIP events.  When enabled, every kernel the
+// library launches is bracketed by a pair of events recorded on the stream it
+// runs on; rs3_profile_report() waits for them and returns per-kernel totals.
+// The event pool is created at enable time, so timed calls allocate nothing.
+#include <vector>
+
+#include "rs3_internal.h"
+
+namespace {
+
+struct Rec {
+  int id;
+  int ev;  // index of the start event; ev+1 is the stop event
+};
+
+struct ProfState {
+  bool on = false;
+  std::vector<hipEvent_t> ev;
+  std::vector<Rec> recs;
+  int next = 0;
+  int open_id = -1;
+  double total_ms[RS3_K_COUNT] = {};
+  int64_t count[RS3_K_COUNT] = {};
+  int64_t dropped = 0;
+};
+
+ProfState P;
+
+hipError_t fold() {
+  for (const Rec& r : P.recs) {
+    hipError_t e = hipEventSynchronize(P.ev[r.ev + 1]);
+    if (e != hipSuccess) return e;
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, P.ev[r.ev], P.ev[r.ev + 1]);
+    if (e != hipSuccess) return e;
+    P.total_ms[r.id] += ms;
+    P.count[r.id] += 1;
+  }
+  P.recs.clear();
+  P.next = 0;
+  return hipSuccess;
+}
+
+}  // namespace
+
+void rs3_prof_begin(int id, hipStream_t st) {
+  if (!P.on) return;
+  if (P.next + 2 > (int)P.ev.size()) {
+    ++P.dropped;
+    P.open_id = -1;
+    return;
+  }
+  if (hipEventRecord(P.ev[P.next], st) != hipSuccess) {
+    P.open_id = -1;
+    return;
+  }
+  P.open_id = id;
+}
+
+void rs3_prof_end(int id, hipStream_t st) {
+  if (!P.on || P.open_id != id) return;
+  if (hipEventRecord(P.ev[P.next + 1], st) == hipSuccess) {
+    P.recs.push_back(Rec{id, P.next});
+    P.next += 2;
+  }
+  P.open_id = -1;
+}
+
+extern "C" {
+
+rs3_status rs3_profile_enable(int32_t on, int32_t max_launches) {
+  if (on) {
+    if (max_launches <= 0 || max_launches > (1 << 20)) return RS3_E_INVALID;
+    if ((int)P.ev.size() < 2 * max_launches) {
+      for (hipEvent_t e : P.ev) (void)hipEventDestroy(e);
+      P.ev.assign(2 * max_launches, nullptr);
+      for (auto& e : P.ev)
+        if (hipEventCreate(&e) != hipSuccess) return RS3_E_DEVICE;
+    }
+    P.recs.reserve(max_launches);
+  }
+  P.on = on != 0;
+  return RS3_OK;
+}
+
+rs3_status rs3_profile_report(double* total_ms, int64_t* launches, int64_t* dropped) {
+  if (!total_ms || !launches) return RS3_E_INVALID;
+  if (fold() != hipSuccess) return RS3_E_DEVICE;
+  for (int i = 0; i < RS3_K_COUNT; ++i) {
+    total_ms[i] = P.total_ms[i];
+    launches[i] = P.count[i];
+  }
+  if (dropped) *dropped = P.dropped;
+  return RS3_OK;
+}
+
+rs3_status rs3_profile_reset(void) {
+  if (fold() != hipSuccess) return RS3_E_DEVICE;
+  for (int i = 0; i < RS3_K_COUNT; ++i) {
+    P.total_ms[i] = 0.0;
+    P.count[i] = 0;
+  }
+  P.dropped = 0;
+  return RS3_OK;
+}
+
+}  // extern "C"

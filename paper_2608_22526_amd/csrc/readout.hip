@@ -73,15 +73,47 @@ __global__ __launch_bounds__(256) void k_qproj(Rs3ReadoutArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// LDS tiles are stored without padding; the 16-byte chunks of each row are
+// permuted by an XOR with a few row bits so that the 32 (or 8) rows read by
+// one MFMA operand load land in distinct LDS banks.
+template <int CPR>
+__device__ __forceinline__ int chunk_swz(int r) {
+  return CPR >= 8 ? (r & 7) : ((r >> 1) & (CPR - 1));
+}
+
+// Direct-to-LDS loads of resident tile t (K^ then V^ of head h) into a stage.
+template <int DH>
+__device__ __forceinline__ void attn_issue(const bf16_t* Kh, const bf16_t* Vh, const TileEnt* tiles, int t,
+                                           int h, int H, uint8_t* lds, int stage, int wave, const int* koff,
+                                           const int* voff) {
+  constexpr int KB = KT * DH * 2;
+  constexpr int NI = DH / 32;
+  const int tile = tiles[t].tile;
+  const bf16_t* kg = Kh + ((int64_t)tile * H + h) * (KT * DH);
+  const bf16_t* vg = Vh + ((int64_t)tile * H + h) * (DH * KT);
+  uint8_t* kd = lds + stage * 2 * KB;
+  uint8_t* vd = kd + KB;
+#pragma unroll
+  for (int j = 0; j < NI; ++j) {
+    const int i = wave + 4 * j;
+    __builtin_amdgcn_global_load_lds(kg + koff[j], kd + i * 1024, 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(vg + voff[j], vd + i * 1024, 16, 0, 0);
+  }
+}
+
 // grid 8*n_qt*ceil(G/8) with G = n_obj*H*S key groups, block 256 (4 waves x
 // 32 queries).  Block b -> key group 8*((b>>3)/n_qt) + (b&7), query tile
 // (b>>3) % n_qt, so all query tiles of one key group share an XCD (and its L2).
+// K^/V^ tiles are streamed into two LDS stages with direct-to-LDS loads
+// (global_load_lds_dwordx4): the next tile is in flight while the current one
+// is multiplied.
 template <int DH>
 __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
-  constexpr int KS = DH + 8;   // padded LDS row of the K tile (elements)
-  constexpr int VS = KT + 8;   // padded LDS row of the V tile
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[KT * KS];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[DH * VS];
+  constexpr int CPRK = DH / 8;            // 16-byte chunks per K row
+  constexpr int KB = KT * DH * 2;         // bytes of one K (or V) tile
+  constexpr int STAGE = 2 * KB;
+  constexpr int NI = DH / 32;             // DMA instructions per wave per tensor
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * STAGE];
   const int bid = blockIdx.x;
   const int rest = bid >> 3;
   const int qt = rest % a.n_qt;
@@ -93,10 +125,28 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
   const int row0 = qt * 128;
   if (row0 >= cnt) return;
   const int ntiles = b.hdr[HDR_NTILES];
-  const int tb = (int)((int64_t)s * ntiles / a.S), te = (int)((int64_t)(s + 1) * ntiles / a.S);
+  const int tps = split_tiles(ntiles, a.S);
+  const int tb = min(s * tps, ntiles), te = min(tb + tps, ntiles);
   if (tb >= te) return;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5;
+  const bf16_t* Kh = (const bf16_t*)b.Khat;
+  const bf16_t* Vh = (const bf16_t*)b.Vhat;
+  const TileEnt* tiles = b.tiles;
+  const int H = a.H;
+
+  // per-lane DMA source offsets inside a tile (elements), fixed for all tiles
+  int koff[NI], voff[NI];
+#pragma unroll
+  for (int j = 0; j < NI; ++j) {
+    const int p = (wave + 4 * j) * 64 + lane;          // LDS chunk written by this lane
+    const int r = p / CPRK, pc = p % CPRK;
+    koff[j] = (r * CPRK + (pc ^ chunk_swz<CPRK>(r))) * 8;
+    const int rv = p >> 3, pcv = p & 7;
+    voff[j] = (rv * 8 + (pcv ^ (rv & 7))) * 8;
+  }
+  attn_issue<DH>(Kh, Vh, tiles, tb, h, H, lds, 0, wave, koff, voff);
+
   const int qrow = row0 + 32 * wave + (lane & 31);
   const bool qv = qrow < cnt;
   const bf16_t* Qp = (const bf16_t*)a.Q + ((int64_t)o * a.max_sel + (qv ? qrow : 0)) * a.D + h * DH;
@@ -109,35 +159,39 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
 #pragma unroll
   for (int dt = 0; dt < DH / 32; ++dt) acc[dt] = f32x16{};
   float m_run = -INFINITY, l_run = 0.f;
-  const bf16_t* Kh = (const bf16_t*)b.Khat;
-  const bf16_t* Vh = (const bf16_t*)b.Vhat;
+  // LDS read offsets of this lane's operand rows
+  int kro[2], ksw[2];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    const int r = 32 * kb + (lane & 31);
+    kro[kb] = r * CPRK * 16;
+    ksw[kb] = chunk_swz<CPRK>(r);
+  }
+  const int vsw = lane & 7;
+  uint64_t msk = tiles[tb].mask;
 
   for (int t = tb; t < te; ++t) {
-    const TileEnt ent = b.tiles[t];
+    const int st = (t - tb) & 1;
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    const bf16_t* kg = Kh + ((int64_t)ent.tile * a.H + h) * (KT * DH);
-    const bf16_t* vg = Vh + ((int64_t)ent.tile * a.H + h) * (DH * KT);
-#pragma unroll
-    for (int c = tid; c < KT * DH / 8; c += 256) {
-      const int rr = c / (DH / 8), cc = c % (DH / 8);
-      *(u32x4*)&Ks[rr * KS + 8 * cc] = *(const u32x4*)(kg + 8 * c);
+    uint64_t msk_next = 0;
+    if (t + 1 < te) {
+      attn_issue<DH>(Kh, Vh, tiles, t + 1, h, H, lds, st ^ 1, wave, koff, voff);
+      msk_next = tiles[t + 1].mask;
     }
-#pragma unroll
-    for (int c = tid; c < DH * KT / 8; c += 256) {
-      const int rr = c >> 3, cc = c & 7;
-      *(u32x4*)&Vs[rr * VS + 8 * cc] = *(const u32x4*)(vg + 8 * c);
-    }
-    __syncthreads();
+    const uint8_t* Kl = lds + st * STAGE;
+    const uint8_t* Vl = Kl + KB;
 
     f32x16 sc[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       sc[kb] = f32x16{};
-      const bf16_t* kr = &Ks[(32 * kb + (lane & 31)) * KS + 8 * g];
 #pragma unroll
-      for (int ks = 0; ks < DH / 16; ++ks) sc[kb] = mfma32(*(const u32x4*)(kr + 16 * ks), qreg[ks], sc[kb]);
+      for (int ks = 0; ks < DH / 16; ++ks) {
+        const int c = (2 * ks + g) ^ ksw[kb];
+        sc[kb] = mfma32(*(const u32x4*)(Kl + kro[kb] + c * 16), qreg[ks], sc[kb]);
+      }
     }
-    const uint64_t msk = ent.mask;
     float mx = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -151,7 +205,7 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     const float m_new = fmaxf(m_run, mx);
     const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    const float alpha = exp2f(m_run - m_use);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
     float psum = 0.f;
     u32x4 pk[2][2];
 #pragma unroll
@@ -160,23 +214,26 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
       for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const float p0 = exp2f(sc[kb][8 * hf + 2 * j] - m_use);
-          const float p1 = exp2f(sc[kb][8 * hf + 2 * j + 1] - m_use);
+          const float p0 = __builtin_amdgcn_exp2f(sc[kb][8 * hf + 2 * j] - m_use);
+          const float p1 = __builtin_amdgcn_exp2f(sc[kb][8 * hf + 2 * j + 1] - m_use);
           psum += p0 + p1;
-          pk[kb][hf][j] = (uint32_t)f2bf(p0) | ((uint32_t)f2bf(p1) << 16);
+          pk[kb][hf][j] = pack_bf16x2(p0, p1);
         }
     l_run = l_run * alpha + psum;
     m_run = m_new;
 #pragma unroll
     for (int dt = 0; dt < DH / 32; ++dt) {
       acc[dt] *= alpha;
-      const bf16_t* vr = &Vs[(32 * dt + (lane & 31)) * VS + 8 * g];
+      const uint8_t* vrow = Vl + (32 * dt + (lane & 31)) * 128;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int hf = 0; hf < 2; ++hf)
-          acc[dt] = mfma32(*(const u32x4*)(vr + 32 * kb + 16 * hf), pk[kb][hf], acc[dt]);
+        for (int hf = 0; hf < 2; ++hf) {
+          const int c = (4 * kb + 2 * hf + g) ^ vsw;
+          acc[dt] = mfma32(*(const u32x4*)(vrow + c * 16), pk[kb][hf], acc[dt]);
+        }
     }
+    msk = msk_next;
   }
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   if (!qv) return;
@@ -189,8 +246,8 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
     for (int q4 = 0; q4 < 4; ++q4) {
       const int d = 32 * dt + 8 * q4 + 4 * g;
       u32x2 w;
-      w[0] = (uint32_t)f2bf(acc[dt][4 * q4] * inv) | ((uint32_t)f2bf(acc[dt][4 * q4 + 1] * inv) << 16);
-      w[1] = (uint32_t)f2bf(acc[dt][4 * q4 + 2] * inv) | ((uint32_t)f2bf(acc[dt][4 * q4 + 3] * inv) << 16);
+      w[0] = pack_bf16x2(acc[dt][4 * q4] * inv, acc[dt][4 * q4 + 1] * inv);
+      w[1] = pack_bf16x2(acc[dt][4 * q4 + 2] * inv, acc[dt][4 * q4 + 3] * inv);
       *(u32x2*)(op + d) = w;
     }
   if (g == 0) {
@@ -215,85 +272,102 @@ __device__ __forceinline__ void copy_out<bf16_t>(bf16_t* p, bf16_t x) { *p = x; 
 template <>
 __device__ __forceinline__ void copy_out<float>(float* p, bf16_t x) { *p = bf2f(x); }
 
-// grid (n_obj, ceil(max_sel/32)), block 256, dynamic LDS 32*(D+8)*2 bytes.
+// grid (n_obj, ceil(max_sel/16)), block 512.  Dynamic LDS: merged O rows
+// (16 x (D+8) bf16) then the per-(row, head, split) weights (16*H*S floats).
+// 1. every (row, head, split) triple loads its (m, l) pair; per (row, head)
+//    the merge weights w_s = 2^(m_s - M) l_s / sum are formed in LDS;
+// 2. each thread merges one 8-column chunk over all active splits;
+// 3. y = x + O W_o on a 32x32x16 MFMA whose rows 16..31 are zero.
+constexpr int CB_ROWS = 16;
+constexpr int CB_THREADS = 512;
 template <typename OutT>
-__global__ __launch_bounds__(256) void k_combine(Rs3ReadoutArgs a) {
-  extern __shared__ __attribute__((aligned(16))) bf16_t Os[];
-  __shared__ float Mx[32 * 32], Wi[32 * 32];  // H <= 32 (C <= 1024, d_h >= 32)
-  const int o = blockIdx.x, r0 = blockIdx.y * 32;
+__global__ __launch_bounds__(CB_THREADS) void k_combine(Rs3ReadoutArgs a) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t cl[];
+  const int o = blockIdx.x, r0 = blockIdx.y * CB_ROWS;
   BankDev& b = *a.banks[o];
   const int cnt = sel_count_of(a, o, b, false);
   if (r0 >= cnt) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5;
   const int D = a.D, C = a.C, H = a.H, d_h = a.d_h, S = a.S, OS = D + 8;
+  bf16_t* Os = (bf16_t*)cl;
+  float* wts = (float*)(cl + ((CB_ROWS * OS * 2 + 15) & ~15));
   const int ntiles = b.hdr[HDR_NTILES];
+  const int SA = ntiles > 0 ? active_splits(ntiles, S) : 0;
   const int32_t* sel = a.sel_idx + (int64_t)o * a.sel_stride;
   const int64_t base = (int64_t)o * S * a.max_sel;
 
-  // 1. per (row, head): max of the split maxima and the merged denominator
-  for (int q = tid; q < 32 * H; q += 256) {
-    const int rr = q / H, h = q - rr * H, row = r0 + rr;
-    float M = -INFINITY;
-    if (row < cnt)
-      for (int s = 0; s < S; ++s) {
-        const int tb = (int)((int64_t)s * ntiles / S), te = (int)((int64_t)(s + 1) * ntiles / S);
-        if (tb < te) M = fmaxf(M, a.ML[((base + (int64_t)s * a.max_sel + row) * H + h) * 2]);
-      }
-    float W = 0.f;
-    if (M != -INFINITY)
-      for (int s = 0; s < S; ++s) {
-        const int tb = (int)((int64_t)s * ntiles / S), te = (int)((int64_t)(s + 1) * ntiles / S);
-        if (tb < te) {
-          const float* ml = a.ML + ((base + (int64_t)s * a.max_sel + row) * H + h) * 2;
-          W += exp2f(ml[0] - M) * ml[1];
-        }
-      }
-    Mx[q] = M;
-    Wi[q] = W > 0.f ? 1.f / W : 0.f;
+  // 1a. (m, l) of every active split: wts[(rr*H + h)*SA + s] = m, then l after
+  for (int q = tid; q < CB_ROWS * H * SA; q += CB_THREADS) {
+    const int s = q % SA, rh = q / SA, h = rh % H, rr = rh / H, row = r0 + rr;
+    float m = -INFINITY, l = 0.f;
+    if (row < cnt) {
+      const float* ml = a.ML + ((base + (int64_t)s * a.max_sel + row) * H + h) * 2;
+      m = ml[0];
+      l = ml[1];
+    }
+    wts[q] = m;
+    wts[CB_ROWS * H * SA + q] = l;
   }
   __syncthreads();
-  // 2. merged O rows (bf16) into LDS, 8 columns per step
+  // 1b. weights per (row, head)
+  for (int rh = tid; rh < CB_ROWS * H; rh += CB_THREADS) {
+    float* mv = wts + rh * SA;
+    const float* lv = wts + CB_ROWS * H * SA + rh * SA;
+    float M = -INFINITY;
+    for (int s = 0; s < SA; ++s) M = fmaxf(M, mv[s]);
+    float W = 0.f;
+    if (M != -INFINITY)
+      for (int s = 0; s < SA; ++s) W += __builtin_amdgcn_exp2f(mv[s] - M) * lv[s];
+    const float iw = W > 0.f ? 1.f / W : 0.f;
+    for (int s = 0; s < SA; ++s) mv[s] = (M != -INFINITY) ? __builtin_amdgcn_exp2f(mv[s] - M) * lv[s] * iw : 0.f;
+  }
+  __syncthreads();
+  // 2. merged O rows into LDS
   const bf16_t* Op = (const bf16_t*)a.Opart;
-  for (int q = tid; q < 32 * (D / 8); q += 256) {
-    const int rr = q / (D / 8), d0 = 8 * (q - rr * (D / 8)), h = d0 / d_h, row = r0 + rr;
+  const int cpr = D / 8;
+  for (int q = tid; q < CB_ROWS * cpr; q += CB_THREADS) {
+    const int rr = q / cpr, d0 = 8 * (q - rr * cpr), h = d0 / d_h, row = r0 + rr;
     float acc8[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    const float M = Mx[rr * H + h], wi = Wi[rr * H + h];
-    if (row < cnt && wi > 0.f)
-      for (int s = 0; s < S; ++s) {
-        const int tb = (int)((int64_t)s * ntiles / S), te = (int)((int64_t)(s + 1) * ntiles / S);
-        if (tb >= te) continue;
-        const int64_t prow = base + (int64_t)s * a.max_sel + row;
-        const float* ml = a.ML + (prow * H + h) * 2;
-        const float w = exp2f(ml[0] - M) * ml[1] * wi;
-        const u32x4 v = *(const u32x4*)(Op + prow * D + d0);
+    if (row < cnt) {
+      const float* w = wts + (rr * H + h) * SA;
+      const bf16_t* src = Op + (base + row) * D + d0;
+      const int64_t sstride = (int64_t)a.max_sel * D;
+#pragma unroll 8
+      for (int s = 0; s < SA; ++s) {
+        const float ws = w[s];
+        const u32x4 v = *(const u32x4*)(src + s * sstride);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          acc8[2 * j] += w * __uint_as_float(v[j] << 16);
-          acc8[2 * j + 1] += w * __uint_as_float(v[j] & 0xffff0000u);
+          acc8[2 * j] += ws * __uint_as_float(v[j] << 16);
+          acc8[2 * j + 1] += ws * __uint_as_float(v[j] & 0xffff0000u);
         }
       }
+    }
     u32x4 pk;
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      pk[j] = (uint32_t)f2bf(acc8[2 * j]) | ((uint32_t)f2bf(acc8[2 * j + 1]) << 16);
+    for (int j = 0; j < 4; ++j) pk[j] = pack_bf16x2(acc8[2 * j], acc8[2 * j + 1]);
     *(u32x4*)&Os[rr * OS + d0] = pk;
   }
   __syncthreads();
-  // 3. y = x + O W_o for the block's rows, columns split over the 4 waves
+  // 3. y = x + O W_o for the block's rows, columns split over the waves
   const bf16_t* X = (const bf16_t*)a.X + (int64_t)o * a.x_stride;
   OutT* Y = (OutT*)a.Y + (int64_t)o * a.y_stride;
   const bf16_t* WoT = (const bf16_t*)a.WoT;
-  for (int nb = wave; nb < C / 32; nb += 4) {
+  const bool arow = (lane & 31) < CB_ROWS;
+  const bf16_t* orow = &Os[(arow ? (lane & 31) : 0) * OS + 8 * g];
+  for (int nb = wave; nb < C / 32; nb += CB_THREADS / 64) {
     const int col = 32 * nb + (lane & 31);
     const bf16_t* wr = WoT + (int64_t)col * D;
-    const bf16_t* orow = &Os[(lane & 31) * OS + 8 * g];
     f32x16 acc = {};
-    for (int k = 0; k < D; k += 16)
-      acc = mfma32(*(const u32x4*)(orow + k), *(const u32x4*)(wr + k + 8 * g), acc);
+    for (int k = 0; k < D; k += 16) {
+      const u32x4 av = arow ? *(const u32x4*)(orow + k) : u32x4{0, 0, 0, 0};
+      acc = mfma32(av, *(const u32x4*)(wr + k + 8 * g), acc);
+    }
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int row = r0 + c_row(r, lane);
-      if (row >= cnt || !sel_ok(sel, row, a.mn)) continue;
+      const int rr = c_row(r, lane);
+      const int row = r0 + rr;
+      if (rr >= CB_ROWS || row >= cnt || !sel_ok(sel, row, a.mn)) continue;
       const int64_t off = (int64_t)sel[row] * C + col;
       const bf16_t xv = X[off];
       if (ntiles == 0)
@@ -428,6 +502,10 @@ __global__ __launch_bounds__(256) void k_readout_f32(Rs3ReadoutArgs a) {
 
 using namespace rs3;
 
+static size_t combine_lds_bytes(int D, int H, int S) {
+  return (((size_t)CB_ROWS * (D + 8) * 2 + 15) & ~(size_t)15) + (size_t)2 * CB_ROWS * H * S * 4;
+}
+
 hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st) {
   const int64_t cells = (int64_t)a.mn * a.C;
   const bool in_place = a.Y == a.X && !a.y_fp32;
@@ -436,15 +514,15 @@ hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st
     if (dtype == RS3_BF16 && !a.y_fp32) {
       int64_t c16 = cells * 2 / 16;
       dim3 g16((unsigned)((c16 + 255) / 256 < 2048 ? (c16 + 255) / 256 : 2048), a.n_obj);
-      hipLaunchKernelGGL(k_copy_grid16, g16, dim3(256), 0, st, (const u32x4*)a.X, a.x_stride * 2 / 16,
+      RS3_LAUNCH(RS3_K_COPY, st, k_copy_grid16, g16, dim3(256), 0, st, (const u32x4*)a.X, a.x_stride * 2 / 16,
                          (u32x4*)a.Y, a.y_stride * 2 / 16, c16);
     } else if (dtype == RS3_BF16) {
-      hipLaunchKernelGGL((k_copy_grid<bf16_t, float>), grid, dim3(256), 0, st, (const bf16_t*)a.X,
+      RS3_LAUNCH(RS3_K_COPY, st, (k_copy_grid<bf16_t, float>), grid, dim3(256), 0, st, (const bf16_t*)a.X,
                          a.x_stride, (float*)a.Y, a.y_stride, cells);
     } else {
       int64_t c16 = cells * 4 / 16;
       dim3 g16((unsigned)((c16 + 255) / 256 < 2048 ? (c16 + 255) / 256 : 2048), a.n_obj);
-      hipLaunchKernelGGL(k_copy_grid16, g16, dim3(256), 0, st, (const u32x4*)a.X, a.x_stride * 4 / 16,
+      RS3_LAUNCH(RS3_K_COPY, st, k_copy_grid16, g16, dim3(256), 0, st, (const u32x4*)a.X, a.x_stride * 4 / 16,
                          (u32x4*)a.Y, a.y_stride * 4 / 16, c16);
     }
     hipError_t e = hipGetLastError();
@@ -453,36 +531,37 @@ hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st
   if (a.max_sel == 0) return hipSuccess;
   if (dtype == RS3_F32) {
     size_t lds = (size_t)(a.C + 2 * a.D) * 4;
-    hipLaunchKernelGGL(k_readout_f32, dim3(a.n_obj, a.max_sel), dim3(256), lds, st, a);
+    RS3_LAUNCH(RS3_K_READOUT_F32, st, k_readout_f32, dim3(a.n_obj, a.max_sel), dim3(256), lds, st, a);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL(k_qproj, dim3(a.n_obj, (a.max_sel + 63) / 64, a.D / 64), dim3(256), 0, st, a);
+  RS3_LAUNCH(RS3_K_QPROJ, st, k_qproj, dim3(a.n_obj, (a.max_sel + 63) / 64, a.D / 64), dim3(256), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int G = a.n_obj * a.H * a.S;
   const int nblk = 8 * a.n_qt * ((G + 7) / 8);
   switch (a.d_h) {
-    case 32: hipLaunchKernelGGL(k_attn<32>, dim3(nblk), dim3(256), 0, st, a, G); break;
-    case 64: hipLaunchKernelGGL(k_attn<64>, dim3(nblk), dim3(256), 0, st, a, G); break;
-    case 128: hipLaunchKernelGGL(k_attn<128>, dim3(nblk), dim3(256), 0, st, a, G); break;
-    case 256: hipLaunchKernelGGL(k_attn<256>, dim3(nblk), dim3(256), 0, st, a, G); break;
+    case 32: RS3_LAUNCH(RS3_K_ATTN, st, k_attn<32>, dim3(nblk), dim3(256), 0, st, a, G); break;
+    case 64: RS3_LAUNCH(RS3_K_ATTN, st, k_attn<64>, dim3(nblk), dim3(256), 0, st, a, G); break;
+    case 128: RS3_LAUNCH(RS3_K_ATTN, st, k_attn<128>, dim3(nblk), dim3(256), 0, st, a, G); break;
+    case 256: RS3_LAUNCH(RS3_K_ATTN, st, k_attn<256>, dim3(nblk), dim3(256), 0, st, a, G); break;
     default: return hipErrorInvalidValue;
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const size_t lds = (size_t)32 * (a.D + 8) * 2;
+  const size_t lds = combine_lds_bytes(a.D, a.H, a.S);
+  const dim3 cgrid(a.n_obj, (a.max_sel + CB_ROWS - 1) / CB_ROWS);
   if (a.y_fp32)
-    hipLaunchKernelGGL(k_combine<float>, dim3(a.n_obj, (a.max_sel + 31) / 32), dim3(256), lds, st, a);
+    RS3_LAUNCH(RS3_K_COMBINE, st, k_combine<float>, cgrid, dim3(CB_THREADS), lds, st, a);
   else
-    hipLaunchKernelGGL(k_combine<bf16_t>, dim3(a.n_obj, (a.max_sel + 31) / 32), dim3(256), lds, st, a);
+    RS3_LAUNCH(RS3_K_COMBINE, st, k_combine<bf16_t>, cgrid, dim3(CB_THREADS), lds, st, a);
   return hipGetLastError();
 }
 
 hipError_t rs3_readout_setup() {
-  hipError_t e = hipFuncSetAttribute((const void*)k_combine<bf16_t>,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, 32 * 1032 * 2);
+  // H * S <= RS3_MAX_SPLITS_X_HEADS and D <= 1024 (checked on the host)
+  const int max_lds = (int)combine_lds_bytes(1024, 1, RS3_MAX_SPLITS_X_HEADS);
+  hipError_t e = hipFuncSetAttribute((const void*)k_combine<bf16_t>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     max_lds);
   if (e != hipSuccess) return e;
-  e = hipFuncSetAttribute((const void*)k_combine<float>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                          32 * 1032 * 2);
-  return e;
+  return hipFuncSetAttribute((const void*)k_combine<float>, hipFuncAttributeMaxDynamicSharedMemorySize, max_lds);
 }

@@ -109,6 +109,27 @@ __device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c) {
 
 __device__ __forceinline__ int c_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
 
+// Two fp32 values -> packed bf16 pair (round to nearest even, v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+// Key splits of a query tile: every split gets at least MIN_TILES_PER_SPLIT
+// resident tiles, so with few tiles only the first splits are active.
+constexpr int MIN_TILES_PER_SPLIT = 2;
+// Key splits times heads per readout call (bounds the merge kernel's LDS).
+#define RS3_MAX_SPLITS_X_HEADS 512
+__host__ __device__ __forceinline__ int split_tiles(int ntiles, int S) {
+  int tps = (ntiles + S - 1) / S;
+  return tps < MIN_TILES_PER_SPLIT ? MIN_TILES_PER_SPLIT : tps;
+}
+__host__ __device__ __forceinline__ int active_splits(int ntiles, int S) {
+  const int tps = split_tiles(ntiles, S);
+  return (ntiles + tps - 1) / tps;
+}
+
 __device__ __forceinline__ void set_err(int32_t* hdr, int code) {
   atomicCAS(&hdr[HDR_ERR], 0, code);
 }
@@ -165,4 +186,15 @@ hipError_t rs3_launch_commit(const Rs3CommitArgs& a, int dtype, int d_kv, int D,
                              hipStream_t st);
 hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st);
 hipError_t rs3_readout_setup();
+void rs3_prof_begin(int id, hipStream_t st);
+void rs3_prof_end(int id, hipStream_t st);
+
+// Launch a kernel bracketed by the optional profiling events.
+#define RS3_LAUNCH(ID, ST, ...)  \
+  do {                           \
+    rs3_prof_begin((ID), (ST));  \
+    hipLaunchKernelGGL(__VA_ARGS__); \
+    rs3_prof_end((ID), (ST));    \
+  } while (0)
 hipError_t rs3_select_setup();
+hipError_t rs3_commit_setup();

@@ -68,7 +68,7 @@ struct SelShared {
   int bb[4];
   int mode, r, gy0, gx0, gy1, gx1;
   int hist[256];
-  int digit, remaining;
+  int digit, remaining, full;
 };
 
 __device__ __forceinline__ int wave_incl_scan(int v, int lane) {
@@ -228,8 +228,12 @@ __device__ void add_object_prior(const Rs3SelectArgs& a, int o, uint8_t* U, uint
   __syncthreads();
 }
 
-// grid n_groups, block 1024, dynamic LDS 3*mn bytes.
+// grid n_groups, block 1024, dynamic LDS 3*mn bytes.  MAXC bounds the cells
+// per thread (mn <= 1024*MAXC); with MAXC <= 16 the energy bit patterns of a
+// thread's cells stay in registers, otherwise they are re-read (L2) per pass.
+template <int MAXC>
 __global__ __launch_bounds__(SEL_THREADS) void k_select(Rs3SelectArgs a) {
+  constexpr bool REG = MAXC <= 16;
   extern __shared__ uint8_t lds[];
   __shared__ SelShared sh;
   const int g = blockIdx.x;
@@ -253,33 +257,40 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(Rs3SelectArgs a) {
   // Contiguous cells per thread so that block scans follow cell order.
   const int cpt = (mn + SEL_THREADS - 1) / SEL_THREADS;
   const int c0 = tid * cpt;
-  // Energies are re-read from global memory (L2-resident) in every pass
-  // rather than held in registers.
   const unsigned long long* ebits =
       reinterpret_cast<const unsigned long long*>(a.e + (a.x_per_obj ? (int64_t)g * mn : 0)) + c0;
   uint32_t inP = 0;
-  for (int j = 0; j < cpt; ++j) {
-    int i = c0 + j;
-    if (i < mn && U[i]) inP |= 1u << j;
+  unsigned long long kreg[REG ? MAXC : 1];
+#pragma unroll
+  for (int j = 0; j < MAXC; ++j) {
+    const int i = c0 + j;
+    const bool in = j < cpt && i < mn && U[i];
+    if (in) inP |= 1u << j;
+    if (REG) kreg[REG ? j : 0] = in ? ebits[j] : 0ull;
   }
+  auto key_of = [&](int j) -> unsigned long long { return REG ? kreg[REG ? j : 0] : ebits[j]; };
   const int k = a.k[g];
   const int countP = block_sum(__popc(inP), sh);
   uint32_t keep = inP;
   if (countP > k) {
     unsigned long long lo = ~0ull, hi = 0;
-    for (int j = 0; j < cpt; ++j)
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j)
       if (inP >> j & 1) {
-        const unsigned long long key = ebits[j];
+        const unsigned long long key = key_of(j);
         lo = key < lo ? key : lo;
         hi = key > hi ? key : hi;
       }
     const unsigned long long kmin = block_minmax_u64(lo, false, sh);
     const unsigned long long kmax = block_minmax_u64(hi, true, sh);
+    // Result: keep keys > T, plus the first need_eq keys == T in cell order;
+    // or (ge) keep every key >= T.
     unsigned long long T;
-    int need_eq;
+    int need_eq = 0;
+    bool ge = false;
     if (k == 0) {
-      T = ~0ull;  // nothing kept
-      need_eq = 0;
+      T = ~0ull;
+      ge = false;
     } else if (kmin == kmax) {
       T = kmin;
       need_eq = k;
@@ -292,12 +303,13 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(Rs3SelectArgs a) {
         const int width = top + 1 < 8 ? top + 1 : 8;
         const int shift = top - width + 1;
         const unsigned dmask = (1u << width) - 1u;
-        for (int b = tid; b < 256; b += SEL_THREADS) sh.hist[b] = 0;
+        for (int bb = tid; bb < 256; bb += SEL_THREADS) sh.hist[bb] = 0;
         __syncthreads();
-        for (int j = 0; j < cpt; ++j) {
+#pragma unroll
+        for (int j = 0; j < MAXC; ++j) {
           if (inP >> j & 1) {
-            const unsigned long long key = ebits[j];
-            bool match = (top >= 63) || (((key ^ prefix) >> (top + 1)) == 0ull);
+            const unsigned long long key = key_of(j);
+            const bool match = (top >= 63) || (((key ^ prefix) >> (top + 1)) == 0ull);
             if (match) atomicAdd(&sh.hist[(unsigned)(key >> shift) & dmask], 1);
           }
         }
@@ -305,61 +317,72 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(Rs3SelectArgs a) {
         if (tid < 64) {
           // lane owns bins 4*lane .. 4*lane+3; find the digit holding the
           // remaining-th largest candidate
-          int h0 = sh.hist[4 * lane], h1 = sh.hist[4 * lane + 1];
-          int h2 = sh.hist[4 * lane + 2], h3 = sh.hist[4 * lane + 3];
-          int mine = h0 + h1 + h2 + h3;
+          const int h0 = sh.hist[4 * lane], h1 = sh.hist[4 * lane + 1];
+          const int h2 = sh.hist[4 * lane + 2], h3 = sh.hist[4 * lane + 3];
+          const int mine = h0 + h1 + h2 + h3;
           int suf = mine;  // inclusive suffix sum over lanes >= lane
 #pragma unroll
           for (int off = 1; off < 64; off <<= 1) {
-            int t = __shfl_down(suf, off, 64);
+            const int t = __shfl_down(suf, off, 64);
             if (lane + off < 64) suf += t;
           }
-          int above = suf - mine;  // candidates in bins of higher lanes
-          int want = remaining;
+          const int above = suf - mine;  // candidates in bins of higher lanes
+          const int want = remaining;
           if (above < want && want <= suf) {
-            int hb[4] = {h0, h1, h2, h3};
+            const int hb[4] = {h0, h1, h2, h3};
             int cum = above;
-            for (int b = 3; b >= 0; --b) {
-              if (cum + hb[b] >= want) {
-                sh.digit = 4 * lane + b;
+            for (int bb = 3; bb >= 0; --bb) {
+              if (cum + hb[bb] >= want) {
+                sh.digit = 4 * lane + bb;
                 sh.remaining = want - cum;
+                sh.full = (cum + hb[bb] == want);
                 break;
               }
-              cum += hb[b];
+              cum += hb[bb];
             }
           }
         }
         __syncthreads();
         prefix |= (unsigned long long)sh.digit << shift;
         remaining = sh.remaining;
+        const bool full = sh.full;
         __syncthreads();
+        if (full) {
+          // every candidate with this prefix is kept: keep keys >= prefix
+          ge = true;
+          break;
+        }
         top = shift - 1;
       }
       T = prefix;
       need_eq = remaining;
     }
-    // rank of each candidate equal to T among equals, in cell order
     uint32_t eq = 0, gt = 0;
-    for (int j = 0; j < cpt; ++j)
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j)
       if (inP >> j & 1) {
-        const unsigned long long key = ebits[j];
-        if (key == T) eq |= 1u << j;
-        if (key > T && T != ~0ull) gt |= 1u << j;
+        const unsigned long long key = key_of(j);
+        if (ge ? key >= T : (key > T && T != ~0ull)) gt |= 1u << j;
+        if (!ge && key == T) eq |= 1u << j;
       }
-    int eqTot;
-    int eqBefore = block_excl_scan(__popc(eq), sh, &eqTot);
     keep = gt;
-    for (int j = 0; j < cpt; ++j) {
-      if (eq >> j & 1) {
-        if (eqBefore < need_eq) keep |= 1u << j;
-        ++eqBefore;
+    if (!ge && k > 0) {
+      int eqTot;
+      int eqBefore = block_excl_scan(__popc(eq), sh, &eqTot);
+#pragma unroll
+      for (int j = 0; j < MAXC; ++j) {
+        if (eq >> j & 1) {
+          if (eqBefore < need_eq) keep |= 1u << j;
+          ++eqBefore;
+        }
       }
     }
   }
   int total;
   int before = block_excl_scan(__popc(keep), sh, &total);
   int32_t* out = a.sel_idx + (int64_t)g * mn;
-  for (int j = 0; j < cpt; ++j)
+#pragma unroll
+  for (int j = 0; j < MAXC; ++j)
     if (keep >> j & 1) out[before++] = c0 + j;
   if (tid == 0) a.sel_count[g] = total;
 }
@@ -372,19 +395,25 @@ hipError_t rs3_launch_energy(const void* X, int64_t x_stride, int n_x, int mn, i
                              double* e, hipStream_t st) {
   dim3 grid((mn + 63) / 64, n_x);
   if (dtype == RS3_BF16)
-    hipLaunchKernelGGL(k_energy<bf16_t>, grid, dim3(64), 0, st, (const bf16_t*)X, x_stride, mn, C, e);
+    RS3_LAUNCH(RS3_K_ENERGY, st, k_energy<bf16_t>, grid, dim3(64), 0, st, (const bf16_t*)X, x_stride, mn, C, e);
   else
-    hipLaunchKernelGGL(k_energy<float>, grid, dim3(64), 0, st, (const float*)X, x_stride, mn, C, e);
+    RS3_LAUNCH(RS3_K_ENERGY, st, k_energy<float>, grid, dim3(64), 0, st, (const float*)X, x_stride, mn, C, e);
   return hipGetLastError();
 }
 
 hipError_t rs3_select_setup() {
-  return hipFuncSetAttribute((const void*)k_select, hipFuncAttributeMaxDynamicSharedMemorySize,
+  hipError_t e = hipFuncSetAttribute((const void*)k_select<16>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     3 * RS3_MAX_MN);
+  if (e != hipSuccess) return e;
+  return hipFuncSetAttribute((const void*)k_select<32>, hipFuncAttributeMaxDynamicSharedMemorySize,
                              3 * RS3_MAX_MN);
 }
 
 hipError_t rs3_launch_select(const Rs3SelectArgs& a, int n_groups, hipStream_t st) {
   const int mn = a.m * a.n;
-  hipLaunchKernelGGL(k_select, dim3(n_groups), dim3(SEL_THREADS), 3 * mn, st, a);
+  if (mn <= 16 * SEL_THREADS)
+    RS3_LAUNCH(RS3_K_SELECT, st, k_select<16>, dim3(n_groups), dim3(SEL_THREADS), 3 * mn, st, a);
+  else
+    RS3_LAUNCH(RS3_K_SELECT, st, k_select<32>, dim3(n_groups), dim3(SEL_THREADS), 3 * mn, st, a);
   return hipGetLastError();
 }

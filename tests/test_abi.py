@@ -1,0 +1,69 @@
+"""CPU checks of the C ABI: the library loads, exports every function that
+include/rs3.h declares, and rejects malformed arguments on the host before
+any HIP call (so these run without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from conftest import ROOT
+
+HEADER = os.path.join(ROOT, "include", "rs3.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:rs3_status|void|const char\s*\*)\s*(rs3_\w+)\s*\(", text, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2608_22526_amd as p
+    return p.lib()
+
+
+def test_library_exports_header(lib):
+    names = _declared()
+    assert len(names) >= 19
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert missing == []
+    import paper_2608_22526_amd as p
+    assert sorted(p.exported_symbols()) == names
+
+
+def test_status_strings(lib):
+    for code in range(5):
+        assert lib.rs3_status_str(code)
+    assert lib.rs3_status_str(0) == b"ok"
+
+
+def test_host_validation_before_device(lib):
+    import paper_2608_22526_amd as p
+    g = p.Grid(64, 64, 1)
+    bad = p.Grid(0, 64, 1)
+    huge = p.Grid(256, 256, 1)
+    sz = ctypes.c_size_t()
+    assert lib.rs3_select_workspace_size(ctypes.byref(g), 1, 0, ctypes.byref(sz)) == p.RS3_OK
+    assert sz.value == 64 * 64 * 8
+    assert lib.rs3_select_workspace_size(ctypes.byref(bad), 1, 0, ctypes.byref(sz)) == p.RS3_E_INVALID
+    assert lib.rs3_select_workspace_size(ctypes.byref(huge), 1, 0, ctypes.byref(sz)) == p.RS3_E_INVALID
+    assert lib.rs3_select_workspace_size(ctypes.byref(g), 0, 0, ctypes.byref(sz)) == p.RS3_E_INVALID
+    assert lib.rs3_select_workspace_size(ctypes.byref(g), p.RS3_MAX_OBJ + 1, 0, ctypes.byref(sz)) == p.RS3_E_INVALID
+    # null handles and pointers
+    assert lib.rs3_select_queries(None, 1, None, None, None, 0, 256, 1, None, None, None, 0, None, None, None,
+                                  None) == p.RS3_E_INVALID
+    assert lib.rs3_readout(None, ctypes.byref(g), 1, None, 0, None, None, None, 0, 0, 0, None, 0, 0, None, 0,
+                           None) == p.RS3_E_INVALID
+    assert lib.rs3_commit(None, 1, ctypes.byref(g), None, None, 0, None, 0, 0, 0, 4096, None, None) == p.RS3_E_INVALID
+    out = ctypes.c_void_p()
+    assert lib.rs3_track_create(0, ctypes.byref(out)) == p.RS3_E_INVALID
+    assert lib.rs3_bank_create(None, 100, 4, 1, ctypes.byref(out)) == p.RS3_E_INVALID
+    assert lib.rs3_readout_workspace_size(None, 1, 10, 0, ctypes.byref(sz)) == p.RS3_E_INVALID
+    # layer shape rules: d_h must be 32/64/128/256 for bf16, d_kv a multiple of 16
+    w = (ctypes.c_uint16 * (256 * 256))()
+    assert lib.rs3_layer_create(256, 3, 64, p.RS3_BF16, w, w, w, w, ctypes.byref(out)) == p.RS3_E_INVALID
+    assert lib.rs3_layer_create(256, 1, 60, p.RS3_BF16, w, w, w, w, ctypes.byref(out)) == p.RS3_E_INVALID
+    assert lib.rs3_layer_create(256, 1, 64, 7, w, w, w, w, ctypes.byref(out)) == p.RS3_E_INVALID
+    assert lib.rs3_profile_enable(1, 0) == p.RS3_E_INVALID
