@@ -17,6 +17,9 @@ LIB = os.path.join(PKG, "librs3.so")
 SOURCES = ["select.hip", "commit.hip", "readout.hip", "api.hip", "profile.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+# The attention kernel keeps its MFMA accumulators in arch VGPRs, so the
+# online-softmax rescale is plain VALU work instead of AGPR round trips.
+PER_FILE = {"readout.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     "-I" + os.path.join(ROOT, "include"), "-I" + CSRC,
@@ -37,7 +40,8 @@ def _run(cmd):
 def build(jobs: int = 4, verbose: bool = False) -> str:
     os.makedirs(OBJDIR, exist_ok=True)
     objs = [os.path.join(OBJDIR, s.replace(".hip", ".o")) for s in SOURCES]
-    cmds = [[HIPCC] + FLAGS + ["-c", os.path.join(CSRC, s), "-o", o] for s, o in zip(SOURCES, objs)]
+    cmds = [[HIPCC] + FLAGS + PER_FILE.get(s, []) + ["-c", os.path.join(CSRC, s), "-o", o]
+            for s, o in zip(SOURCES, objs)]
     with ThreadPoolExecutor(max_workers=max(1, jobs)) as ex:
         outs = list(ex.map(_run, cmds))
     if verbose:

@@ -73,47 +73,135 @@ __global__ __launch_bounds__(256) void k_qproj(Rs3ReadoutArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// LDS tiles are stored without padding; the 16-byte chunks of each row are
-// permuted by an XOR with a few row bits so that the 32 (or 8) rows read by
-// one MFMA operand load land in distinct LDS banks.
-template <int CPR>
-__device__ __forceinline__ int chunk_swz(int r) {
-  return CPR >= 8 ? (r & 7) : ((r >> 1) & (CPR - 1));
+// The attention streams the object's resident keys in 32-key half tiles
+// through NST LDS stages (NST-1 half tiles in flight).  One stage holds
+//   K : 32 rows (keys) x DH bf16, row pitch DH*2 + 16 bytes
+//   V : DH rows x 32 keys (slot order), row pitch 64 + 16 bytes
+// The pitch is an odd number of 16-byte chunks, so the 16 rows read by one
+// LDS cycle (64 banks x 4 bytes) fall on 16 distinct bank groups, and every
+// operand offset is a compile-time immediate.  Direct-to-LDS loads write
+// 64 x 16 contiguous bytes per wave instruction; lanes that land on a pad
+// chunk (or past the rows) load a harmless duplicate chunk.  Every wave
+// issues the same number of loads per stage, so the waits are immediates.
+template <int DH>
+struct AttnLds {
+  static constexpr int NST = 4;
+  static constexpr int CPR = DH / 8;                          // data chunks per K row
+  static constexpr int KP = (CPR + 1) * 16;                   // K row pitch, bytes
+  static constexpr int VP = 5 * 16;                           // V row pitch, bytes
+  static constexpr int NK = ((32 * (CPR + 1) + 63) / 64 + 3) / 4 * 4;   // K loads (wave instructions)
+  static constexpr int NV = ((DH * 5 + 63) / 64 + 3) / 4 * 4;           // V loads
+  static constexpr int KREG = NK * 1024;
+  static constexpr int STAGE = KREG + NV * 1024;
+  static constexpr int PER_WAVE = (NK + NV) / 4;              // loads per wave per stage
+};
+
+// Per-lane source offsets (elements) of the direct-to-LDS loads of one half
+// tile; identical for every tile, so they are computed once per kernel.
+template <int DH>
+struct AttnDmaOffsets {
+  int k[AttnLds<DH>::NK / 4];
+  int v[AttnLds<DH>::NV / 4];
+};
+
+template <int DH>
+__device__ __forceinline__ AttnDmaOffsets<DH> attn_dma_offsets(int wave, int lane) {
+  using L = AttnLds<DH>;
+  AttnDmaOffsets<DH> d;
+#pragma unroll
+  for (int j = 0; j < L::NK / 4; ++j) {
+    const int p = (4 * j + wave) * 64 + lane;
+    const int r = p / (L::CPR + 1), c = p % (L::CPR + 1);
+    d.k[j] = (r < 32 && c < L::CPR) ? (r * L::CPR + c) * 8 : 0;
+  }
+#pragma unroll
+  for (int j = 0; j < L::NV / 4; ++j) {
+    const int p = (4 * j + wave) * 64 + lane;
+    const int r = p / 5, c = p % 5;
+    d.v[j] = (r < DH && c < 4) ? r * KT + c * 8 : 0;
+  }
+  return d;
 }
 
-// Direct-to-LDS loads of resident tile t (K^ then V^ of head h) into a stage.
+// Direct-to-LDS loads of half tile `half` of bank tile `tile`, head h, into
+// a stage.  `tile`, `half` and `wave` are wave-uniform (scalar registers).
 template <int DH>
-__device__ __forceinline__ void attn_issue(const bf16_t* Kh, const bf16_t* Vh, const TileEnt* tiles, int t,
-                                           int h, int H, uint8_t* lds, int stage, int wave, const int* koff,
-                                           const int* voff) {
-  constexpr int KB = KT * DH * 2;
-  constexpr int NI = DH / 32;
-  const int tile = tiles[t].tile;
-  const bf16_t* kg = Kh + ((int64_t)tile * H + h) * (KT * DH);
-  const bf16_t* vg = Vh + ((int64_t)tile * H + h) * (DH * KT);
-  uint8_t* kd = lds + stage * 2 * KB;
-  uint8_t* vd = kd + KB;
+__device__ __forceinline__ void attn_issue(const bf16_t* Kh, const bf16_t* Vh, int tile, int half, int h, int H,
+                                           uint8_t* stage, int wave, const AttnDmaOffsets<DH>& off) {
+  using L = AttnLds<DH>;
+  const bf16_t* kg = Kh + ((int64_t)tile * H + h) * (KT * DH) + half * 32 * DH;
+  const bf16_t* vg = Vh + ((int64_t)tile * H + h) * (DH * KT) + half * 32;
 #pragma unroll
-  for (int j = 0; j < NI; ++j) {
-    const int i = wave + 4 * j;
-    __builtin_amdgcn_global_load_lds(kg + koff[j], kd + i * 1024, 16, 0, 0);
-    __builtin_amdgcn_global_load_lds(vg + voff[j], vd + i * 1024, 16, 0, 0);
+  for (int j = 0; j < L::NK / 4; ++j)
+    __builtin_amdgcn_global_load_lds(kg + off.k[j], stage + (4 * j + wave) * 1024, 16, 0, 0);
+#pragma unroll
+  for (int j = 0; j < L::NV / 4; ++j)
+    __builtin_amdgcn_global_load_lds(vg + off.v[j], stage + L::KREG + (4 * j + wave) * 1024, 16, 0, 0);
+}
+
+__device__ __forceinline__ const void* uniform_ptr(const void* p) {
+  const uint64_t v = (uint64_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return (const void*)(((uint64_t)hi << 32) | lo);
+}
+
+// Value of lane l^32 for every lane (v_permlane32_swap: both halves come back
+// in registers; op(r[0], r[1]) combines a lane with its partner).
+__device__ __forceinline__ float max_with_partner(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_with_partner(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Workgroup barrier without a memory fence: the fence of __syncthreads()
+// would wait for every outstanding load, including the K/V prefetches.
+// LDS stages are published by the explicit vmcnt waits before it.
+__device__ __forceinline__ void stage_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// s_waitcnt encoding: wait until at most n vector-memory ops are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+constexpr float RESCALE_LOG2 = 8.0f;
+
+// S^T (32 keys x 32 queries) of one half tile: K rows from LDS (kp points at
+// this lane's row and lane-group chunk), Q~ columns from registers.  Two
+// accumulation chains (even / odd 16-deep steps) keep the MFMA pipe busy.
+template <int DH>
+__device__ __forceinline__ f32x16 attn_scores(const uint8_t* kp, const u32x4* qreg) {
+  constexpr int NKS = DH / 16;
+  constexpr int KG = NKS < 8 ? NKS : 8;
+  f32x16 s0 = f32x16{}, s1 = f32x16{};
+#pragma unroll
+  for (int k0 = 0; k0 < NKS; k0 += KG) {
+    u32x4 ka[KG];
+#pragma unroll
+    for (int j = 0; j < KG; ++j) ka[j] = *(const u32x4*)(kp + (k0 + j) * 32);
+#pragma unroll
+    for (int j = 0; j < KG; ++j) {
+      if (j & 1)
+        s1 = mfma32(ka[j], qreg[k0 + j], s1);
+      else
+        s0 = mfma32(ka[j], qreg[k0 + j], s0);
+    }
   }
+  return s0 + s1;
 }
 
 // grid 8*n_qt*ceil(G/8) with G = n_obj*H*S key groups, block 256 (4 waves x
 // 32 queries).  Block b -> key group 8*((b>>3)/n_qt) + (b&7), query tile
 // (b>>3) % n_qt, so all query tiles of one key group share an XCD (and its L2).
-// K^/V^ tiles are streamed into two LDS stages with direct-to-LDS loads
-// (global_load_lds_dwordx4): the next tile is in flight while the current one
-// is multiplied.
 template <int DH>
 __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
-  constexpr int CPRK = DH / 8;            // 16-byte chunks per K row
-  constexpr int KB = KT * DH * 2;         // bytes of one K (or V) tile
-  constexpr int STAGE = 2 * KB;
-  constexpr int NI = DH / 32;             // DMA instructions per wave per tensor
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * STAGE];
+  using L = AttnLds<DH>;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[L::NST * L::STAGE];
   const int bid = blockIdx.x;
   const int rest = bid >> 3;
   const int qt = rest % a.n_qt;
@@ -124,29 +212,41 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
   const int cnt = sel_count_of(a, o, b, false);
   const int row0 = qt * 128;
   if (row0 >= cnt) return;
-  const int ntiles = b.hdr[HDR_NTILES];
+  const int ntiles = __builtin_amdgcn_readfirstlane(b.hdr[HDR_NTILES]);
   const int tps = split_tiles(ntiles, a.S);
   const int tb = min(s * tps, ntiles), te = min(tb + tps, ntiles);
   if (tb >= te) return;
+  const int ub = 2 * tb, ue = 2 * te;   // half tiles
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5;
-  const bf16_t* Kh = (const bf16_t*)b.Khat;
-  const bf16_t* Vh = (const bf16_t*)b.Vhat;
-  const TileEnt* tiles = b.tiles;
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // values loaded from the bank descriptor are wave-uniform: keep them in
+  // scalar registers so that load addresses are base (SGPR) + lane offset
+  const bf16_t* Kh = (const bf16_t*)uniform_ptr(b.Khat);
+  const bf16_t* Vh = (const bf16_t*)uniform_ptr(b.Vhat);
+  const TileEnt* tiles = (const TileEnt*)uniform_ptr(b.tiles);
   const int H = a.H;
+  const AttnDmaOffsets<DH> doff = attn_dma_offsets<DH>(wave, lane);
 
-  // per-lane DMA source offsets inside a tile (elements), fixed for all tiles
-  int koff[NI], voff[NI];
-#pragma unroll
-  for (int j = 0; j < NI; ++j) {
-    const int p = (wave + 4 * j) * 64 + lane;          // LDS chunk written by this lane
-    const int r = p / CPRK, pc = p % CPRK;
-    koff[j] = (r * CPRK + (pc ^ chunk_swz<CPRK>(r))) * 8;
-    const int rv = p >> 3, pcv = p & 7;
-    voff[j] = (rv * 8 + (pcv ^ (rv & 7))) * 8;
+  // Resident-tile entries of this split are cached one per lane (a window of
+  // 64 tiles, read back with readlane), so the loop issues no metadata loads
+  // that would drain the prefetch queue.
+  // The half tiles of the split are visited starting at an offset that
+  // depends on the query tile: the workgroups sharing a split (same XCD) then
+  // fetch different tiles at any moment and later visitors hit in L2, rather
+  // than all waiting on the same HBM misses.  (Only for splits that fit the
+  // window; the visiting order changes nothing but fp rounding.)
+  const int nh = ue - ub;
+  const int rot = (te - tb <= 64) ? ((qt & 7) * nh) >> 3 : 0;
+  int cbase = tb, c_tile = 0;
+  uint32_t c_mlo = 0, c_mhi = 0;
+  if (tb + lane < te) {
+    const TileEnt e = tiles[tb + lane];
+    c_tile = e.tile;
+    c_mlo = (uint32_t)e.mask;
+    c_mhi = (uint32_t)(e.mask >> 32);
   }
-  attn_issue<DH>(Kh, Vh, tiles, tb, h, H, lds, 0, wave, koff, voff);
-
+  // query operands
   const int qrow = row0 + 32 * wave + (lane & 31);
   const bool qv = qrow < cnt;
   const bf16_t* Qp = (const bf16_t*)a.Q + ((int64_t)o * a.max_sel + (qv ? qrow : 0)) * a.D + h * DH;
@@ -154,92 +254,127 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
 #pragma unroll
   for (int ks = 0; ks < DH / 16; ++ks)
     qreg[ks] = qv ? *(const u32x4*)(Qp + 16 * ks + 8 * g) : u32x4{0, 0, 0, 0};
+  wait_vmcnt<0>();
+  // i-th visited half tile
+  auto half_at = [&](int i) { int v = i + rot; return ub + (v >= nh ? v - nh : v); };
+#pragma unroll
+  for (int j = 0; j < L::NST - 1; ++j)
+    if (j < nh) {
+      const int v = half_at(j);
+      attn_issue<DH>(Kh, Vh, __builtin_amdgcn_readlane(c_tile, (v >> 1) - cbase), v & 1, h, H,
+                     lds + j * L::STAGE, wave, doff);
+    }
 
   f32x16 acc[DH / 32];
 #pragma unroll
   for (int dt = 0; dt < DH / 32; ++dt) acc[dt] = f32x16{};
   float m_run = -INFINITY, l_run = 0.f;
-  // LDS read offsets of this lane's operand rows
-  int kro[2], ksw[2];
-#pragma unroll
-  for (int kb = 0; kb < 2; ++kb) {
-    const int r = 32 * kb + (lane & 31);
-    kro[kb] = r * CPRK * 16;
-    ksw[kb] = chunk_swz<CPRK>(r);
-  }
-  const int vsw = lane & 7;
-  uint64_t msk = tiles[tb].mask;
+  const int kbase = (lane & 31) * L::KP + 16 * g;             // + ks*32
+  const int vbase = L::KREG + (lane & 31) * L::VP + 16 * g;   // + dt*32*VP + q*32
+  // stage 0 must land before its scores: later stages issued = min(2, nh-1)
+  if (nh >= 3)
+    wait_vmcnt<2 * L::PER_WAVE>();
+  else if (nh == 2)
+    wait_vmcnt<L::PER_WAVE>();
+  else
+    wait_vmcnt<0>();
+  stage_barrier();
 
-  for (int t = tb; t < te; ++t) {
-    const int st = (t - tb) & 1;
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    uint64_t msk_next = 0;
-    if (t + 1 < te) {
-      attn_issue<DH>(Kh, Vh, tiles, t + 1, h, H, lds, st ^ 1, wave, koff, voff);
-      msk_next = tiles[t + 1].mask;
+  // Software pipeline over the visited half tiles i = 0 .. nh-1 (stage i%NST):
+  //   iteration i: wait until stage i+1 landed; barrier (stage i-1 free);
+  //   prefetch i+3 into it; S^T(i+1) on the MFMA pipe while the VALU does
+  //   the softmax of i; then O^T += V^T(i) P(i).
+  f32x16 sc = attn_scores<DH>(lds + kbase, qreg);
+  for (int i = 0; i < nh; ++i) {
+    const int st = i & (L::NST - 1);
+    const int u = half_at(i);
+    if (i + 1 < nh) {
+      if (i + 2 < nh)
+        wait_vmcnt<L::PER_WAVE>();
+      else
+        wait_vmcnt<0>();
     }
-    const uint8_t* Kl = lds + st * STAGE;
-    const uint8_t* Vl = Kl + KB;
+    stage_barrier();
+    if (i + L::NST - 1 < nh) {
+      const int v = half_at(i + L::NST - 1);
+      if ((v >> 1) - cbase >= 64) {
+        // (unrotated splits longer than the window) slide it to the tile
+        // being computed
+        wait_vmcnt<0>();
+        cbase = u >> 1;
+        c_tile = 0;
+        if (cbase + lane < te) c_tile = tiles[cbase + lane].tile;
+        const uint64_t mm = cbase + lane < te ? tiles[cbase + lane].mask : 0ull;
+        c_mlo = (uint32_t)mm;
+        c_mhi = (uint32_t)(mm >> 32);
+        wait_vmcnt<0>();
+      }
+      attn_issue<DH>(Kh, Vh, __builtin_amdgcn_readlane(c_tile, (v >> 1) - cbase), v & 1, h, H,
+                     lds + ((st + L::NST - 1) & (L::NST - 1)) * L::STAGE, wave, doff);
+    }
+    const uint8_t* Sb = lds + st * L::STAGE;
+    const int tu = (u >> 1) - cbase;
+    const uint32_t msk = (u & 1) ? __builtin_amdgcn_readlane(c_mhi, tu) : __builtin_amdgcn_readlane(c_mlo, tu);
 
-    f32x16 sc[2];
+    // S^T of the next half tile (independent of the softmax below).  In the
+    // last iteration the stage holds an earlier tile and the result is unused.
+    const f32x16 sc_next = attn_scores<DH>(lds + ((st + 1) & (L::NST - 1)) * L::STAGE + kbase, qreg);
+
+    if (msk != 0u) {
+      if (msk != 0xffffffffu) {  // partial half tile (frame boundary)
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      sc[kb] = f32x16{};
-#pragma unroll
-      for (int ks = 0; ks < DH / 16; ++ks) {
-        const int c = (2 * ks + g) ^ ksw[kb];
-        sc[kb] = mfma32(*(const u32x4*)(Kl + kro[kb] + c * 16), qreg[ks], sc[kb]);
+        for (int r = 0; r < 16; ++r)
+          if (!(msk >> c_row(r, lane) & 1u)) sc[r] = -INFINITY;
       }
-    }
-    float mx = -INFINITY;
+      float mx = sc[0];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sc[r]);
+      mx = max_with_partner(mx);
+      // Lazy rescale: the reference max only moves when a half tile exceeds
+      // it by more than RESCALE_LOG2 (probabilities stay <= 2^RESCALE_LOG2);
+      // the accumulators are touched only when some lane of the wave moves.
+      const bool need = mx > m_run + RESCALE_LOG2;
+      if (__any(need)) {
+        const float m_new = need ? mx : m_run;
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);   // 0 on the first tile
+        l_run *= alpha;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = 32 * kb + c_row(r, lane);
-        const float v = (msk >> key & 1ull) ? sc[kb][r] : -INFINITY;
-        sc[kb][r] = v;
-        mx = fmaxf(mx, v);
+        for (int dt = 0; dt < DH / 32; ++dt) acc[dt] *= alpha;
+        m_run = m_new;
       }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-    float psum = 0.f;
-    u32x4 pk[2][2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      float psum = 0.f;
+      u32x4 pk[2];
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const float p0 = __builtin_amdgcn_exp2f(sc[kb][8 * hf + 2 * j] - m_use);
-          const float p1 = __builtin_amdgcn_exp2f(sc[kb][8 * hf + 2 * j + 1] - m_use);
+          const float p0 = __builtin_amdgcn_exp2f(sc[8 * hf + 2 * j] - m_run);
+          const float p1 = __builtin_amdgcn_exp2f(sc[8 * hf + 2 * j + 1] - m_run);
           psum += p0 + p1;
-          pk[kb][hf][j] = pack_bf16x2(p0, p1);
+          pk[hf][j] = pack_bf16x2(p0, p1);
         }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
+      l_run += psum;
+      // O^T += V^T P^T over the 32 keys (two 16-key MFMA steps per d block)
+      constexpr int DB = DH / 32 >= 2 ? 2 : 1;   // d blocks whose operands are fetched together
 #pragma unroll
-    for (int dt = 0; dt < DH / 32; ++dt) {
-      acc[dt] *= alpha;
-      const uint8_t* vrow = Vl + (32 * dt + (lane & 31)) * 128;
+      for (int dt = 0; dt < DH / 32; dt += DB) {
+        u32x4 va[2 * DB];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+        for (int q = 0; q < 2 * DB; ++q)
+          va[q] = *(const u32x4*)(Sb + vbase + (dt + (q >> 1)) * 32 * L::VP + (q & 1) * 32);
 #pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-          const int c = (4 * kb + 2 * hf + g) ^ vsw;
-          acc[dt] = mfma32(*(const u32x4*)(vrow + c * 16), pk[kb][hf], acc[dt]);
-        }
+        for (int q = 0; q < 2 * DB; ++q) acc[dt + (q >> 1)] = mfma32(va[q], pk[q & 1], acc[dt + (q >> 1)]);
+      }
     }
-    msk = msk_next;
+    sc = sc_next;
   }
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
-  if (!qv) return;
-  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  const int64_t prow = ((int64_t)o * a.S + s) * a.max_sel + qrow;
-  bf16_t* op = (bf16_t*)a.Opart + prow * a.D + h * DH;
+  const float l_tot = sum_with_partner(l_run);
+  const float inv = l_tot > 0.f ? __builtin_amdgcn_rcpf(l_tot) : 0.f;
+  // Epilogue: stage this wave's 32 normalized rows in LDS as [query][d] bf16,
+  // then write whole rows with 16-byte stores.
+  constexpr int OP = DH * 2 + 16;
+  __syncthreads();   // every wave is done with the stages
+  uint8_t* ow = lds + wave * 32 * OP;
 #pragma unroll
   for (int dt = 0; dt < DH / 32; ++dt)
 #pragma unroll
@@ -248,12 +383,22 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
       u32x2 w;
       w[0] = pack_bf16x2(acc[dt][4 * q4] * inv, acc[dt][4 * q4 + 1] * inv);
       w[1] = pack_bf16x2(acc[dt][4 * q4 + 2] * inv, acc[dt][4 * q4 + 3] * inv);
-      *(u32x2*)(op + d) = w;
+      *(u32x2*)(ow + (lane & 31) * OP + d * 2) = w;
     }
-  if (g == 0) {
+  if (g == 0 && qv) {
+    const int64_t prow = ((int64_t)o * a.S + s) * a.max_sel + qrow;
     float* ml = a.ML + (prow * a.H + h) * 2;
     ml[0] = m_run;
     ml[1] = l_tot;
+  }
+  __syncthreads();
+  constexpr int CH = DH / 8;   // 16-byte chunks per row
+  bf16_t* obase = (bf16_t*)a.Opart + (((int64_t)o * a.S + s) * a.max_sel) * a.D + h * DH;
+#pragma unroll
+  for (int q = lane; q < 32 * CH; q += 64) {
+    const int rr = q / CH, c = q - rr * CH;
+    const int row = row0 + 32 * wave + rr;
+    if (row < cnt) *(u32x4*)(obase + (int64_t)row * a.D + 8 * c) = *(const u32x4*)(ow + rr * OP + 16 * c);
   }
 }
 

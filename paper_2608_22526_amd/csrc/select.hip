@@ -125,13 +125,38 @@ __device__ unsigned long long block_minmax_u64(unsigned long long v, bool want_m
 // ---------------------------------------------------------------------------
 enum { MODE_NONE = 0, MODE_MASK = 1, MODE_BOX = 2 };
 
-// Adds one object's prior into U (LDS bitmap of the group).
-__device__ void add_object_prior(const Rs3SelectArgs& a, int o, uint8_t* U, uint8_t* base,
-                                 uint8_t* tmp, SelShared& sh) {
-  const int tid = threadIdx.x;
+// Grid rows as bitmasks of W = ceil(n/64) words (bit x%64 of word x/64).
+// Used when m*W words fit a 32 KB LDS buffer.
+constexpr int BIT_WORDS_MAX = 4096;
+
+// Word w of a row shifted by b >= 1 cells toward higher (left=true: cell x
+// takes cell x-b) or lower x.
+__device__ __forceinline__ uint64_t row_shift(const uint64_t* row, int W, int w, int b, bool left) {
+  const int q = b >> 6, rb = b & 63;
+  uint64_t v = 0;
+  if (left) {
+    if (w - q >= 0) v = row[w - q] << rb;
+    if (rb && w - q - 1 >= 0) v |= row[w - q - 1] >> (64 - rb);
+  } else {
+    if (w + q < W) v = row[w + q] >> rb;
+    if (rb && w + q + 1 < W) v |= row[w + q + 1] << (64 - rb);
+  }
+  return v;
+}
+
+__device__ __forceinline__ uint64_t last_word_mask(int n, int W, int w) {
+  const int rem = n - 64 * (W - 1);
+  return (w == W - 1 && rem < 64) ? ((1ull << rem) - 1ull) : ~0ull;
+}
+
+// Adds one object's prior into U (LDS byte map of the group).  bufA/bufB are
+// scratch areas of at least max(mn, 8*m*W) bytes.
+__device__ void add_object_prior(const Rs3SelectArgs& a, int o, uint8_t* U, uint8_t* bufA, uint8_t* bufB,
+                                 SelShared& sh) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int m = a.m, n = a.n, s = a.s, mn = m * n;
-  const int W = n * s, Hpx = m * s;
-  const uint8_t* M = a.masks + (int64_t)o * Hpx * W;
+  const int Wpx = n * s, Hpx = m * s;
+  const uint8_t* M = a.masks + (int64_t)o * Hpx * Wpx;
   if (tid == 0) {
     sh.bb[0] = 0x7fffffff;
     sh.bb[1] = 0x7fffffff;
@@ -139,18 +164,26 @@ __device__ void add_object_prior(const Rs3SelectArgs& a, int o, uint8_t* U, uint
     sh.bb[3] = -1;
   }
   __syncthreads();
+  // bounding box of the set pixels: per-thread, then per-wave, then 4 LDS atomics per wave
   int y0 = 0x7fffffff, x0 = 0x7fffffff, y1 = -1, x1 = -1;
-  const int npx = Hpx * W;
+  const int npx = Hpx * Wpx;
   for (int p = tid; p < npx; p += SEL_THREADS) {
     if (M[p]) {
-      int y = p / W, x = p - y * W;
+      const int y = p / Wpx, x = p - y * Wpx;
       y0 = min(y0, y);
       y1 = max(y1, y);
       x0 = min(x0, x);
       x1 = max(x1, x);
     }
   }
-  if (y1 >= 0) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    y0 = min(y0, __shfl_xor(y0, off, 64));
+    x0 = min(x0, __shfl_xor(x0, off, 64));
+    y1 = max(y1, __shfl_xor(y1, off, 64));
+    x1 = max(x1, __shfl_xor(x1, off, 64));
+  }
+  if (lane == 0 && y1 >= 0) {
     atomicMin(&sh.bb[0], y0);
     atomicMin(&sh.bb[1], x0);
     atomicMax(&sh.bb[2], y1);
@@ -175,7 +208,7 @@ __device__ void add_object_prior(const Rs3SelectArgs& a, int o, uint8_t* U, uint
       tr[4] = 0;
       tr[5] = 1;
     } else {
-      int d = tr[4] + 1;
+      const int d = tr[4] + 1;
       tr[4] = d;
       if (tr[5]) {
         mode = MODE_BOX;
@@ -199,49 +232,109 @@ __device__ void add_object_prior(const Rs3SelectArgs& a, int o, uint8_t* U, uint
     const int ya = max(0, sh.gy0 - r), yb = min(m - 1, sh.gy1 + r);
     const int xa = max(0, sh.gx0 - r), xb = min(n - 1, sh.gx1 + r);
     for (int i = tid; i < mn; i += SEL_THREADS) {
-      int y = i / n, x = i - y * n;
+      const int y = i / n, x = i - y * n;
       if (y >= ya && y <= yb && x >= xa && x <= xb) U[i] = 1;
     }
   } else if (mode == MODE_MASK) {
-    for (int i = tid; i < mn; i += SEL_THREADS) {
-      int y = i / n, x = i - y * n;
-      base[i] = M[(int64_t)(y * s) * W + x * s] != 0;
-    }
-    __syncthreads();
-    for (int i = tid; i < mn; i += SEL_THREADS) {
-      int y = i / n, x = i - y * n;
-      const uint8_t* row = base + y * n;
-      int xa = max(0, x - r), xb = min(n - 1, x + r);
-      uint8_t v = 0;
-      for (int xx = xa; xx <= xb && !v; ++xx) v = row[xx];
-      tmp[i] = v;
-    }
-    __syncthreads();
-    for (int i = tid; i < mn; i += SEL_THREADS) {
-      int y = i / n, x = i - y * n;
-      int ya = max(0, y - r), yb = min(m - 1, y + r);
-      uint8_t v = 0;
-      for (int yy = ya; yy <= yb && !v; ++yy) v = tmp[yy * n + x];
-      if (v) U[i] = 1;
+    const int W = (n + 63) >> 6;
+    if (m * W <= BIT_WORDS_MAX) {
+      // bitmask path: one wave per row word, ballots form the words
+      uint64_t* A = reinterpret_cast<uint64_t*>(bufA);
+      uint64_t* B = reinterpret_cast<uint64_t*>(bufB);
+      for (int q = wave; q < m * W; q += SEL_WAVES) {
+        const int y = q / W, x = 64 * (q - y * W) + lane;
+        const bool set = x < n && M[(int64_t)(y * s) * Wpx + x * s] != 0;
+        const uint64_t word = __ballot(set);
+        if (lane == 0) A[q] = word;
+      }
+      __syncthreads();
+      // row dilation by doubling: OR-ing the shifts by b of a set dilated by
+      // a (runs clipped at the row ends included) leaves no gap when
+      // b <= a+1, so the radius grows a -> a+b
+      uint64_t* src = A;
+      uint64_t* dst = B;
+      const int rr = min(r, n);
+      int done = 0;
+      while (done < rr) {
+        const int step = min(done + 1, rr - done);
+        for (int q = tid; q < m * W; q += SEL_THREADS) {
+          const int y = q / W, w = q - y * W;
+          const uint64_t* row = src + y * W;
+          dst[q] = (row[w] | row_shift(row, W, w, step, true) | row_shift(row, W, w, step, false)) &
+                   last_word_mask(n, W, w);
+        }
+        __syncthreads();
+        uint64_t* t = src;
+        src = dst;
+        dst = t;
+        done += step;
+      }
+      // column dilation, then expand into the byte map
+      for (int q = tid; q < m * W; q += SEL_THREADS) {
+        const int y = q / W, w = q - y * W;
+        const int ya = max(0, y - r), yb = min(m - 1, y + r);
+        uint64_t v = 0;
+        for (int yy = ya; yy <= yb; ++yy) v |= src[yy * W + w];
+        dst[q] = v;
+      }
+      __syncthreads();
+      for (int q = wave; q < m * W; q += SEL_WAVES) {
+        const int y = q / W, x = 64 * (q - y * W) + lane;
+        if (x < n && (dst[q] >> lane & 1ull)) U[y * n + x] = 1;
+      }
+    } else {
+      // byte path (very tall grids): separable window maxima
+      uint8_t* base = bufA;
+      uint8_t* tmp = bufB;
+      for (int i = tid; i < mn; i += SEL_THREADS) {
+        const int y = i / n, x = i - y * n;
+        base[i] = M[(int64_t)(y * s) * Wpx + x * s] != 0;
+      }
+      __syncthreads();
+      for (int i = tid; i < mn; i += SEL_THREADS) {
+        const int y = i / n, x = i - y * n;
+        const uint8_t* row = base + y * n;
+        const int xa = max(0, x - r), xb = min(n - 1, x + r);
+        uint8_t v = 0;
+        for (int xx = xa; xx <= xb; ++xx) v |= row[xx];
+        tmp[i] = v;
+      }
+      __syncthreads();
+      for (int i = tid; i < mn; i += SEL_THREADS) {
+        const int y = i / n, x = i - y * n;
+        const int ya = max(0, y - r), yb = min(m - 1, y + r);
+        uint8_t v = 0;
+        for (int yy = ya; yy <= yb; ++yy) v |= tmp[yy * n + x];
+        if (v) U[i] = 1;
+      }
     }
   }
   __syncthreads();
 }
 
-// grid n_groups, block 1024, dynamic LDS 3*mn bytes.  MAXC bounds the cells
+// Bytes of each scratch buffer of the select kernel (see add_object_prior).
+__host__ __device__ inline int select_buf_bytes(int m, int n) {
+  const int W = (n + 63) >> 6;
+  const int bits = m * W <= BIT_WORDS_MAX ? 8 * m * W : 0;
+  const int bytes = m * n > bits ? m * n : bits;
+  return (bytes + 15) & ~15;
+}
+
+// grid n_groups, block 1024, dynamic LDS select_lds_bytes().  MAXC bounds the cells
 // per thread (mn <= 1024*MAXC); with MAXC <= 16 the energy bit patterns of a
 // thread's cells stay in registers, otherwise they are re-read (L2) per pass.
 template <int MAXC>
 __global__ __launch_bounds__(SEL_THREADS) void k_select(Rs3SelectArgs a) {
   constexpr bool REG = MAXC <= 16;
-  extern __shared__ uint8_t lds[];
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   __shared__ SelShared sh;
   const int g = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63;
   const int mn = a.m * a.n;
+  const int buf = select_buf_bytes(a.m, a.n);
   uint8_t* U = lds;
-  uint8_t* base = lds + mn;
-  uint8_t* tmp = lds + 2 * mn;
+  uint8_t* base = lds + ((mn + 15) & ~15);
+  uint8_t* tmp = base + buf;
 
   for (int i = tid; i < mn; i += SEL_THREADS) U[i] = 0;
   __syncthreads();
@@ -401,19 +494,24 @@ hipError_t rs3_launch_energy(const void* X, int64_t x_stride, int n_x, int mn, i
   return hipGetLastError();
 }
 
+static size_t select_lds_bytes(int m, int n) {
+  return (size_t)((m * n + 15) & ~15) + 2 * (size_t)select_buf_bytes(m, n);
+}
+
 hipError_t rs3_select_setup() {
-  hipError_t e = hipFuncSetAttribute((const void*)k_select<16>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                     3 * RS3_MAX_MN);
+  // largest layout: mn = RS3_MAX_MN with byte-sized buffers (3 * 32 KB)
+  const int mx = 3 * RS3_MAX_MN + 64;
+  hipError_t e = hipFuncSetAttribute((const void*)k_select<16>, hipFuncAttributeMaxDynamicSharedMemorySize, mx);
   if (e != hipSuccess) return e;
-  return hipFuncSetAttribute((const void*)k_select<32>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                             3 * RS3_MAX_MN);
+  return hipFuncSetAttribute((const void*)k_select<32>, hipFuncAttributeMaxDynamicSharedMemorySize, mx);
 }
 
 hipError_t rs3_launch_select(const Rs3SelectArgs& a, int n_groups, hipStream_t st) {
   const int mn = a.m * a.n;
+  const size_t lds = select_lds_bytes(a.m, a.n);
   if (mn <= 16 * SEL_THREADS)
-    RS3_LAUNCH(RS3_K_SELECT, st, k_select<16>, dim3(n_groups), dim3(SEL_THREADS), 3 * mn, st, a);
+    RS3_LAUNCH(RS3_K_SELECT, st, k_select<16>, dim3(n_groups), dim3(SEL_THREADS), lds, st, a);
   else
-    RS3_LAUNCH(RS3_K_SELECT, st, k_select<32>, dim3(n_groups), dim3(SEL_THREADS), 3 * mn, st, a);
+    RS3_LAUNCH(RS3_K_SELECT, st, k_select<32>, dim3(n_groups), dim3(SEL_THREADS), lds, st, a);
   return hipGetLastError();
 }

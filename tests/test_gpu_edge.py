@@ -164,3 +164,29 @@ def test_invalid_selection_sets_error_and_skips_rows():
     Yh, Xh = _host(Y), _host(X)
     # rows 2 (non-ascending) and the out-of-range entry are skipped
     assert np.array_equal(Yh[0, 2], Xh[0, 2])
+
+
+def test_tall_grid_byte_path_and_max_cells():
+    """8192 x 4 grid: too many rows for the row-bitmask prior (byte path) and
+    32 cells per select thread (the largest grid, mn = 32768)."""
+    cfg = replace(SMALL, m=8192, n=4, C=64, d_kv=16, cap_frames=1, f_max=2)
+    W = make_weights(cfg)
+    sess, orc = _session(cfg, W), OraclePipeline(cfg, W)
+    rng = np.random.default_rng(5)
+    X = to_storage(rng.standard_normal((1, cfg.mn, cfg.C)).astype(np.float32), "bf16")
+    masks = (rng.random((1, cfg.m, cfg.n)) < 0.002).astype(np.uint8)
+    sel = _check_select(sess, orc, masks, X, [1000])
+    assert len(sel[0]) == 1000
+    _check_select(sess, orc, np.zeros_like(masks), X, [100])     # box fallback of the cached box
+
+
+def test_wide_grid_multiword_rows():
+    """Rows of 200 cells span four 64-bit words in the bitmask prior."""
+    cfg = replace(SMALL, m=40, n=200, C=64, d_kv=16, cap_frames=1, f_max=2, r_s=9)
+    W = make_weights(cfg)
+    sess, orc = _session(cfg, W), OraclePipeline(cfg, W)
+    rng = np.random.default_rng(6)
+    X = to_storage(rng.standard_normal((1, cfg.mn, cfg.C)).astype(np.float32), "bf16")
+    masks = (rng.random((1, cfg.m, cfg.n)) < 0.004).astype(np.uint8)
+    masks[0, 7, 63] = masks[0, 7, 64] = masks[0, 30, 127] = masks[0, 2, 199] = masks[0, 39, 0] = 1
+    _check_select(sess, orc, masks, X, [2000])
