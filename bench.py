@@ -117,6 +117,16 @@ def _traffic(kernel: str):
     return d.get("bytes_per_launch")
 
 
+def _absorb(cfg, layer: str) -> bool:
+    """Single-head layers with a narrower bank run the attention on the raw
+    bank rows (W_k folded into the query, W_v into the output projection)."""
+    if layer == "absorbed":
+        return True
+    if layer == "projected":
+        return False
+    return cfg.H == 1 and cfg.d_kv < cfg.D
+
+
 def gpu_run(args):
     import numpy as np
     import torch
@@ -130,10 +140,11 @@ def gpu_run(args):
     seq = make_sequence(cfg, n_frames=n_pre + N_DISTINCT)
     W = make_weights(cfg)
     k_all = [max(ks) for ks in seq.k]
+    absorb = _absorb(cfg, args.layer)
     sess = Session(m=cfg.m, n=cfg.n, s=cfg.s, C=cfg.C, H=cfg.H, d_kv=cfg.d_kv, dtype=cfg.dtype,
                    n_obj=cfg.n_obj, shared_x=cfg.shared_x, union_objects=cfg.union_objects, cap=cfg.cap,
                    f_max=cfg.f_max, n_pin=cfg.n_pin, weights=W, r_s=cfg.r_s, c=cfg.c, max_sel=max(k_all),
-                   n_splits=args.splits)
+                   n_splits=args.splits, absorb=absorb)
     # resident inputs
     frames = []
     for t in range(n_pre + N_DISTINCT):
@@ -190,9 +201,11 @@ def gpu_run(args):
     rs3.profile_enable(False)
     errs = [b.error() for b in sess.banks]
 
-    D = cfg.D
+    # executed attention flops: QK^T and PV at the attention width
+    Da = cfg.d_kv if absorb else cfg.D
     attn_ms, attn_n = rep["attn"]
-    flops = sum(4.0 * r["sel"][o] * r["n_keys"][o] * D for r in recs for o in range(cfg.n_obj))
+    flops = sum(4.0 * r["sel"][o] * r["n_keys"][o] * Da for r in recs for o in range(cfg.n_obj))
+    flops_projected = sum(4.0 * r["sel"][o] * r["n_keys"][o] * cfg.D for r in recs for o in range(cfg.n_obj))
     sel_tot = sum(sum(r["sel"]) for r in recs)
     per_launch_flops = flops / max(attn_n, 1)
     avg_attn_s = attn_ms / 1000.0 / max(attn_n, 1)
@@ -218,12 +231,16 @@ def gpu_run(args):
         "data": "synthetic",
         "config": {"workload": _describe(cfg), "grid": "%dx%d" % (cfg.m, cfg.n), "n_obj": cfg.n_obj,
                    "bank_frames": cfg.f_max, "d_model": cfg.C, "heads": cfg.H, "d_head": cfg.d_h,
-                   "d_kv": cfg.d_kv, "eager_launches": True, "readout": "in place" if in_place else "out of place"},
+                   "d_kv": cfg.d_kv, "eager_launches": True, "readout": "in place" if in_place else "out of place",
+                   "attention": ("absorbed: one head of width d_kv=%d on the raw bank rows" % cfg.d_kv) if absorb
+                   else ("projected: %d head(s) of width %d" % (cfg.H, cfg.d_h))},
         "roofline": {"bound": "mfma", "achieved": achieved_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved_tflops / PEAK_BF16_TFLOPS,
                      "traffic": traffic,
                      "kernel": "k_attn (split-KV attention)",
-                     "algorithmic_flops_per_launch": per_launch_flops,
+                     "flops_per_launch": per_launch_flops,
+                     "flops_basis": "executed: 4 * selected queries * bank keys * attention width (%d)" % Da,
+                     "projected_equivalent_flops_per_launch": flops_projected / max(attn_n, 1),
                      "avg_launch_us": avg_attn_s * 1e6},
         "extra": {
             "query_tokens_per_s": sel_tot / args.steps * fps,
@@ -246,6 +263,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="sam2_single")
     ap.add_argument("--splits", type=int, default=0)
+    ap.add_argument("--layer", choices=["auto", "projected", "absorbed"], default="auto")
     ap.add_argument("--cpu-frames", type=int, default=12)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-child", action="store_true")

@@ -97,9 +97,17 @@ rs3_status rs3_track_import(rs3_track* t, const int32_t* state /*[host]*/);
  * C: query token width; H heads of width d_h with D = H*d_h = C; d_kv: width
  * of the bank's raw key/value tokens.  Weights are [host] row-major arrays in
  * dtype `dt`: Wq [C][D], Wk [d_kv][D], Wv [d_kv][D], Wo [D][C]; the library
- * copies them (into its own device layouts).  d_h must be 32, 64, 128 or 256
- * for bf16 and at most 256 for fp32; C <= 1024; d_kv <= 256, multiple of 16. */
-rs3_status rs3_layer_create(int32_t C, int32_t H, int32_t d_kv, rs3_dtype dt,
+ * copies them (into its own device layouts).
+ * absorb = 0 (projected): banks store K^ = K W_k and V^ = V W_v (width D) and
+ *   the attention runs per head at width d_h.  d_h must be 32, 64, 128 or
+ *   256 for bf16 (at most 256 for fp32).
+ * absorb = 1 (H = 1 only): the attention runs directly on the raw bank rows
+ *   (width d_kv) with q' = x W_q W_k^T and y = x + o' W_v W_o, the same
+ *   function with the projections re-associated; the products W_q W_k^T and
+ *   W_v W_o are formed once here in fp64 and rounded to `dt`.  bf16 needs
+ *   d_kv in {64, 128, 256}.
+ * C <= 1024 (a multiple of 64 for bf16); d_kv <= 256, a multiple of 16. */
+rs3_status rs3_layer_create(int32_t C, int32_t H, int32_t d_kv, rs3_dtype dt, int32_t absorb,
                             const void* Wq, const void* Wk, const void* Wv,
                             const void* Wo, rs3_layer** out);
 void rs3_layer_destroy(rs3_layer* L);

@@ -44,7 +44,7 @@ _SIGS = {
     "rs3_track_destroy": (None, [c_vp]),
     "rs3_track_export": (c_i32, [c_vp, c_vp]),
     "rs3_track_import": (c_i32, [c_vp, c_vp]),
-    "rs3_layer_create": (c_i32, [c_i32, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp, c_vp, ctypes.POINTER(c_vp)]),
+    "rs3_layer_create": (c_i32, [c_i32, c_i32, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp, c_vp, ctypes.POINTER(c_vp)]),
     "rs3_layer_destroy": (None, [c_vp]),
     "rs3_bank_create": (c_i32, [c_vp, c_i32, c_i32, c_i32, ctypes.POINTER(c_vp)]),
     "rs3_bank_destroy": (None, [c_vp]),
@@ -141,14 +141,15 @@ class Track:
 
 class Layer:
     """rs3_layer: W_q [C][D], W_k/W_v [d_kv][D], W_o [D][C] host arrays
-    (uint16 bf16 bits or float32)."""
+    (uint16 bf16 bits or float32).  absorb=True runs the single-head
+    attention on the raw bank rows (see rs3.h)."""
 
-    def __init__(self, C: int, H: int, d_kv: int, dtype: int, Wq, Wk, Wv, Wo):
+    def __init__(self, C: int, H: int, d_kv: int, dtype: int, Wq, Wk, Wv, Wo, absorb: bool = False):
         arrs = [np.ascontiguousarray(w) for w in (Wq, Wk, Wv, Wo)]
         h = c_vp()
-        _check(lib().rs3_layer_create(C, H, d_kv, dtype, *(a.ctypes.data for a in arrs), ctypes.byref(h)),
-               "rs3_layer_create")
-        self.h, self.C, self.H, self.d_kv, self.dtype = h, C, H, d_kv, dtype
+        _check(lib().rs3_layer_create(C, H, d_kv, dtype, int(absorb), *(a.ctypes.data for a in arrs),
+                                      ctypes.byref(h)), "rs3_layer_create")
+        self.h, self.C, self.H, self.d_kv, self.dtype, self.absorb = h, C, H, d_kv, dtype, bool(absorb)
 
     def __del__(self):
         if getattr(self, "h", None) and _lib is not None:

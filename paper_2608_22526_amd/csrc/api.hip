@@ -137,35 +137,99 @@ rs3_status rs3_track_import(rs3_track* t, const int32_t* state) {
 }
 
 // ---- layer -----------------------------------------------------------------
-rs3_status rs3_layer_create(int32_t C, int32_t H, int32_t d_kv, rs3_dtype dt, const void* Wq,
+namespace {
+
+double load_elem(const void* p, size_t i, int dt) {
+  if (dt == RS3_F32) return (double)((const float*)p)[i];
+  uint32_t u = (uint32_t)((const uint16_t*)p)[i] << 16;
+  float f;
+  memcpy(&f, &u, 4);
+  return (double)f;
+}
+
+// Rounds to the layer dtype (bf16: nearest even) and appends the bytes.
+void store_elem(std::vector<uint8_t>& out, size_t i, double v, int dt) {
+  float f = (float)v;
+  if (dt == RS3_F32) {
+    memcpy(&out[i * 4], &f, 4);
+    return;
+  }
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  const uint16_t b = (uint16_t)(u >> 16);
+  memcpy(&out[i * 2], &b, 2);
+}
+
+// (A B)^T for row-major A [r][k], B [k][c], accumulated in fp64, as [c][r].
+std::vector<uint8_t> product_T(const void* A, const void* B, int r, int k, int c, int dt, bool b_transposed) {
+  const size_t es = dtype_size(dt);
+  std::vector<uint8_t> out((size_t)r * c * es);
+  std::vector<double> a((size_t)r * k), bb((size_t)k * c);
+  for (size_t i = 0; i < a.size(); ++i) a[i] = load_elem(A, i, dt);
+  // b_transposed: B is given as [c][k] (row-major) and used as its transpose
+  for (int kk = 0; kk < k; ++kk)
+    for (int j = 0; j < c; ++j) bb[(size_t)kk * c + j] = load_elem(B, b_transposed ? (size_t)j * k + kk : (size_t)kk * c + j, dt);
+  for (int i = 0; i < r; ++i)
+    for (int j = 0; j < c; ++j) {
+      double acc = 0.0;
+      for (int kk = 0; kk < k; ++kk) acc += a[(size_t)i * k + kk] * bb[(size_t)kk * c + j];
+      store_elem(out, (size_t)j * r + i, acc, dt);
+    }
+  return out;
+}
+
+}  // namespace
+
+rs3_status rs3_layer_create(int32_t C, int32_t H, int32_t d_kv, rs3_dtype dt, int32_t absorb, const void* Wq,
                             const void* Wk, const void* Wv, const void* Wo, rs3_layer** out) {
   if (!out || !Wq || !Wk || !Wv || !Wo) return RS3_E_INVALID;
   if (dt != RS3_BF16 && dt != RS3_F32) return RS3_E_INVALID;
+  if (absorb != 0 && absorb != 1) return RS3_E_INVALID;
   if (C <= 0 || C > 1024 || H <= 0 || C % H != 0) return RS3_E_INVALID;
   const int d_h = C / H;
   if (d_kv <= 0 || d_kv > 256 || d_kv % 16 != 0) return RS3_E_INVALID;
+  if (absorb && H != 1) return RS3_E_INVALID;
+  const int Da = absorb ? d_kv : C;
+  const int dah = absorb ? d_kv : d_h;
   if (dt == RS3_BF16) {
-    if (d_h != 32 && d_h != 64 && d_h != 128 && d_h != 256) return RS3_E_INVALID;
-    if (C % 64 != 0) return RS3_E_INVALID;
+    if (dah != 32 && dah != 64 && dah != 128 && dah != 256) return RS3_E_INVALID;
+    if (C % 64 != 0 || Da % 64 != 0) return RS3_E_INVALID;
   } else {
-    if (d_h > 256 || C % 8 != 0) return RS3_E_INVALID;
+    if (dah > 256 || C % 8 != 0) return RS3_E_INVALID;
   }
   *out = nullptr;
   const size_t es = dtype_size(dt);
   const int D = C;
   rs3_layer* L = new rs3_layer();
-  L->dev.C = C;
-  L->dev.H = H;
-  L->dev.d_h = d_h;
-  L->dev.D = D;
-  L->dev.d_kv = d_kv;
-  L->dev.dtype = dt;
-  std::vector<uint8_t> wq = transpose(Wq, C, D, es), wk = transpose(Wk, d_kv, D, es);
-  std::vector<uint8_t> wv = transpose(Wv, d_kv, D, es), wo = transpose(Wo, D, C, es);
-  void** dst[4] = {&L->dev.WqT, &L->dev.WkT, &L->dev.WvT, &L->dev.WoT};
+  LayerDev& ld = L->dev;
+  ld.C = C;
+  ld.H = H;
+  ld.d_h = d_h;
+  ld.D = D;
+  ld.d_kv = d_kv;
+  ld.dtype = dt;
+  ld.absorb = absorb;
+  ld.Da = Da;
+  ld.Ha = absorb ? 1 : H;
+  ld.dah = dah;
+  std::vector<uint8_t> wq, wk, wv, wo;
+  if (absorb) {
+    // W_qk = W_q W_k^T  [C][d_kv] -> stored transposed [d_kv][C]
+    wq = product_T(Wq, Wk, C, D, d_kv, dt, true);
+    // W_vo = W_v W_o    [d_kv][C] -> stored transposed [C][d_kv]
+    wo = product_T(Wv, Wo, d_kv, D, C, dt, false);
+  } else {
+    wq = transpose(Wq, C, D, es);
+    wk = transpose(Wk, d_kv, D, es);
+    wv = transpose(Wv, d_kv, D, es);
+    wo = transpose(Wo, D, C, es);
+  }
+  void** dst[4] = {&ld.WqT, &ld.WkT, &ld.WvT, &ld.WoT};
   std::vector<uint8_t>* src[4] = {&wq, &wk, &wv, &wo};
   hipError_t e = hipSuccess;
   for (int i = 0; i < 4 && e == hipSuccess; ++i) {
+    if (src[i]->empty()) continue;
     e = hipMalloc(dst[i], src[i]->size());
     if (e == hipSuccess) e = hipMemcpy(*dst[i], src[i]->data(), src[i]->size(), hipMemcpyHostToDevice);
   }
@@ -181,10 +245,9 @@ rs3_status rs3_layer_create(int32_t C, int32_t H, int32_t d_kv, rs3_dtype dt, co
 
 void rs3_layer_destroy(rs3_layer* L) {
   if (!L) return;
-  (void)hipFree(L->dev.WqT);
-  (void)hipFree(L->dev.WkT);
-  (void)hipFree(L->dev.WvT);
-  (void)hipFree(L->dev.WoT);
+  void* w[4] = {L->dev.WqT, L->dev.WkT, L->dev.WvT, L->dev.WoT};
+  for (void* p : w)
+    if (p) (void)hipFree(p);
   delete L;
 }
 
@@ -209,12 +272,12 @@ rs3_status rs3_bank_create(const rs3_layer* L, int32_t cap, int32_t f_max, int32
   h.f_max = f_max;
   h.n_pin = n_pin;
   h.d_kv = ld.d_kv;
-  h.H = ld.H;
-  h.d_h = ld.d_h;
+  h.H = ld.Ha;
+  h.d_h = ld.dah;
   h.dtype = ld.dtype;
   h.n_tiles_cap = (cap + KT - 1) / KT;
   const size_t raw = (size_t)cap * ld.d_kv * es;
-  const size_t proj = (size_t)h.n_tiles_cap * KT * ld.D * es;
+  const size_t proj = (size_t)h.n_tiles_cap * KT * ld.Da * es;
   struct Alloc {
     void** p;
     size_t bytes;
@@ -362,21 +425,21 @@ rs3_status rs3_select_queries(const rs3_grid* g, int32_t n_obj, const uint8_t* m
 static void readout_shape(const rs3_layer* L, int32_t n_obj, int32_t max_sel, int32_t S, size_t* q_bytes,
                           size_t* o_bytes, size_t* ml_bytes) {
   const LayerDev& ld = L->dev;
-  *q_bytes = align256((size_t)n_obj * max_sel * ld.D * 2);
-  *o_bytes = align256((size_t)n_obj * S * max_sel * ld.D * 2);
-  *ml_bytes = align256((size_t)n_obj * S * max_sel * ld.H * 8);
+  *q_bytes = align256((size_t)n_obj * max_sel * ld.Da * 2);
+  *o_bytes = align256((size_t)n_obj * S * max_sel * ld.Da * 2);
+  *ml_bytes = align256((size_t)n_obj * S * max_sel * ld.Ha * 8);
 }
 
 static int splits_for(const rs3_layer* L, int32_t n_obj, int32_t max_sel, int32_t n_splits) {
   if (n_splits > 0) return n_splits;
   const int n_qt = (max_sel + 127) / 128;
-  return auto_splits(n_obj, L->dev.H, n_qt > 0 ? n_qt : 1);
+  return auto_splits(n_obj, L->dev.Ha, n_qt > 0 ? n_qt : 1);
 }
 
 rs3_status rs3_readout_workspace_size(const rs3_layer* L, int32_t n_obj, int32_t max_sel, int32_t n_splits,
                                       size_t* bytes) {
   if (!L || !bytes || n_obj <= 0 || n_obj > RS3_MAX_OBJ || max_sel < 0 || n_splits < 0 ||
-      n_splits * L->dev.H > RS3_MAX_SPLITS_X_HEADS)
+      n_splits * L->dev.Ha > RS3_MAX_SPLITS_X_HEADS)
     return RS3_E_INVALID;
   if (L->dev.dtype == RS3_F32) {
     *bytes = 0;
@@ -407,7 +470,7 @@ rs3_status rs3_readout(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, con
   if (n_obj <= 0 || n_obj > RS3_MAX_OBJ) return RS3_E_INVALID;
   const LayerDev& ld = L->dev;
   const int mn = g->m * g->n;
-  if (max_sel < 0 || max_sel > mn || n_splits < 0 || n_splits * ld.H > RS3_MAX_SPLITS_X_HEADS)
+  if (max_sel < 0 || max_sel > mn || n_splits < 0 || n_splits * ld.Ha > RS3_MAX_SPLITS_X_HEADS)
     return RS3_E_INVALID;
   if (sel_stride != 0 && sel_stride != mn) return RS3_E_INVALID;
   const int64_t grid_elems = (int64_t)mn * ld.C;
@@ -445,12 +508,13 @@ rs3_status rs3_readout(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, con
   a.Q = ws;
   a.Opart = ws ? (uint8_t*)ws + q : nullptr;
   a.ML = ws ? (float*)((uint8_t*)ws + q + o_b) : nullptr;
+  // logits are scaled by 1/sqrt(d_h) of the layer's heads in both modes
   a.qscale = (float)(1.4426950408889634 / sqrt((double)ld.d_h));
   a.mn = mn;
   a.C = ld.C;
-  a.H = ld.H;
-  a.d_h = ld.d_h;
-  a.D = ld.D;
+  a.H = ld.Ha;
+  a.d_h = ld.dah;
+  a.D = ld.Da;
   a.n_obj = n_obj;
   a.max_sel = max_sel;
   a.S = S;
@@ -497,7 +561,8 @@ rs3_status rs3_commit(rs3_bank* const* banks, int32_t n_obj, const rs3_grid* g, 
   a.fall_min = fall_min;
   a.fall_max = fall_max;
   a.n_obj = n_obj;
-  hipError_t e = rs3_launch_commit(a, ld.dtype, ld.d_kv, ld.D, ld.H, ld.d_h, (hipStream_t)stream);
+  a.absorb = ld.absorb;
+  hipError_t e = rs3_launch_commit(a, ld.dtype, ld.d_kv, ld.Da, ld.Ha, ld.dah, (hipStream_t)stream);
   if (e != hipSuccess) return map_err(e);
   for (int o = 0; o < n_obj; ++o) {
     if (pin)

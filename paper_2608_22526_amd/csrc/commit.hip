@@ -244,10 +244,25 @@ __global__ __launch_bounds__(256) void k_commit_append_bf16(Rs3CommitArgs a) {
     *(u32x4*)(sV + r * RS + 8 * c) = vv;
   }
   __syncthreads();
-  const bf16_t* WkT = (const bf16_t*)a.WkT;
-  const bf16_t* WvT = (const bf16_t*)a.WvT;
   bf16_t* Kh = (bf16_t*)b.Khat;
   bf16_t* Vh = (bf16_t*)b.Vhat;
+  if (a.absorb) {
+    // attention on the raw rows (one head of width d_kv): K rows as they
+    // are, V rows transposed into slot order
+    for (int q = tid; q < rows * cpr; q += 256) {
+      const int r = q / cpr, c = q - r * cpr;
+      const int j = start + r0 + r;
+      *(u32x4*)(Kh + ((int64_t)(j >> 6) * KT + (j & 63)) * d_kv + 8 * c) = *(const u32x4*)(sK + r * RS + 8 * c);
+    }
+    for (int q = tid; q < rows * d_kv; q += 256) {
+      const int r = q / d_kv, d = q - r * d_kv;
+      const int j = start + r0 + r;
+      Vh[((int64_t)(j >> 6) * d_kv + d) * KT + vslot(j & 63)] = sV[r * RS + d];
+    }
+    return;
+  }
+  const bf16_t* WkT = (const bf16_t*)a.WkT;
+  const bf16_t* WvT = (const bf16_t*)a.WvT;
   const int nblk = 2 * (D / 32);
   for (int blk = wave; blk < nblk; blk += 4) {
     const int mb = blk & 1, nb = blk >> 1;
@@ -320,12 +335,19 @@ __global__ __launch_bounds__(256) void k_commit_append_f32(Rs3CommitArgs a) {
     int src = b.pos[j];
     const float* kr = Km + (int64_t)src * d_kv;
     const float* vr = Vm + (int64_t)src * d_kv;
-    const float* wk = WkT + (int64_t)d * d_kv;
-    const float* wv = WvT + (int64_t)d * d_kv;
-    float sk = 0.f, sv = 0.f;
-    for (int c = 0; c < d_kv; ++c) {
-      sk = fmaf(kr[c], wk[c], sk);
-      sv = fmaf(vr[c], wv[c], sv);
+    float sk, sv;
+    if (a.absorb) {  // attention on the raw rows
+      sk = kr[d];
+      sv = vr[d];
+    } else {
+      const float* wk = WkT + (int64_t)d * d_kv;
+      const float* wv = WvT + (int64_t)d * d_kv;
+      sk = 0.f;
+      sv = 0.f;
+      for (int c = 0; c < d_kv; ++c) {
+        sk = fmaf(kr[c], wk[c], sk);
+        sv = fmaf(vr[c], wv[c], sv);
+      }
     }
     int tile = j >> 6, kk = j & 63, h = d / d_h, dd = d - h * d_h;
     Kh[(((int64_t)tile * H + h) * KT + kk) * d_h + dd] = sk;

@@ -65,12 +65,17 @@ __host__ __device__ inline int vslot(int j) {
 // ---- layer -----------------------------------------------------------------
 // Device weights, transposed so that every MFMA operand reads contiguous
 // 16-byte runs along the contraction dimension.
+// The attention runs at width Da over Ha heads of width dah:
+//   projected: Da = D, Ha = H, dah = d_h; WqT = W_q^T [D][C], WoT = W_o^T [C][D]
+//   absorbed : Da = d_kv, Ha = 1, dah = d_kv; WqT = (W_q W_k^T)^T [d_kv][C],
+//              WoT = (W_v W_o)^T [C][d_kv]; WkT/WvT unused (null)
 struct LayerDev {
-  int32_t C, H, d_h, D, d_kv, dtype;
-  void* WqT;  // [D][C]
-  void* WkT;  // [D][d_kv]
-  void* WvT;  // [D][d_kv]
-  void* WoT;  // [C][D]
+  int32_t C, H, d_h, D, d_kv, dtype, absorb;
+  int32_t Da, Ha, dah;
+  void* WqT;
+  void* WkT;  // [D][d_kv] (projected mode)
+  void* WvT;  // [D][d_kv] (projected mode)
+  void* WoT;
 };
 
 struct Launch {
@@ -155,9 +160,9 @@ struct Rs3CommitArgs {
   const void* Vmem;
   int64_t kv_stride;      // elements between objects
   int32_t* kept_count;    // [n_obj] or null
-  const void* WkT;        // [D][d_kv]
+  const void* WkT;        // [D][d_kv] (projected mode)
   const void* WvT;
-  int m, n, s, t, pin, fall_min, fall_max, n_obj;
+  int m, n, s, t, pin, fall_min, fall_max, n_obj, absorb;
 };
 
 struct Rs3ReadoutArgs {

@@ -63,7 +63,11 @@ def test_host_validation_before_device(lib):
     assert lib.rs3_readout_workspace_size(None, 1, 10, 0, ctypes.byref(sz)) == p.RS3_E_INVALID
     # layer shape rules: d_h must be 32/64/128/256 for bf16, d_kv a multiple of 16
     w = (ctypes.c_uint16 * (256 * 256))()
-    assert lib.rs3_layer_create(256, 3, 64, p.RS3_BF16, w, w, w, w, ctypes.byref(out)) == p.RS3_E_INVALID
-    assert lib.rs3_layer_create(256, 1, 60, p.RS3_BF16, w, w, w, w, ctypes.byref(out)) == p.RS3_E_INVALID
-    assert lib.rs3_layer_create(256, 1, 64, 7, w, w, w, w, ctypes.byref(out)) == p.RS3_E_INVALID
+    assert lib.rs3_layer_create(256, 3, 64, p.RS3_BF16, 0, w, w, w, w, ctypes.byref(out)) == p.RS3_E_INVALID
+    assert lib.rs3_layer_create(256, 1, 60, p.RS3_BF16, 0, w, w, w, w, ctypes.byref(out)) == p.RS3_E_INVALID
+    assert lib.rs3_layer_create(256, 1, 64, 7, 0, w, w, w, w, ctypes.byref(out)) == p.RS3_E_INVALID
+    # absorbed attention needs one head, and a bf16 width in {64, 128, 256}
+    assert lib.rs3_layer_create(256, 8, 64, p.RS3_BF16, 1, w, w, w, w, ctypes.byref(out)) == p.RS3_E_INVALID
+    assert lib.rs3_layer_create(256, 1, 32, p.RS3_BF16, 1, w, w, w, w, ctypes.byref(out)) == p.RS3_E_INVALID
+    assert lib.rs3_layer_create(256, 1, 64, p.RS3_BF16, 2, w, w, w, w, ctypes.byref(out)) == p.RS3_E_INVALID
     assert lib.rs3_profile_enable(1, 0) == p.RS3_E_INVALID

@@ -111,9 +111,10 @@ class Runner:
         return sel
 
 
-def test_tiny_f32_sequence():
+@pytest.mark.parametrize("absorb", [False, True])
+def test_tiny_f32_sequence(absorb):
     cfg = CONFIGS["tiny_f32"]
-    r = Runner(cfg, 8)
+    r = Runner(cfg, 8, absorb=absorb)
     r.commit(0, True)
     for t in range(1, 8):
         r.select_readout(t)
@@ -121,9 +122,10 @@ def test_tiny_f32_sequence():
     print("tiny_f32 stats", r.stats)
 
 
-def test_sam2_single_steady_state():
+@pytest.mark.parametrize("absorb", [False, True])
+def test_sam2_single_steady_state(absorb):
     cfg = CONFIGS["sam2_single"]
-    r = Runner(cfg, 11, max_sel=1228)
+    r = Runner(cfg, 11, max_sel=1228, absorb=absorb)
     r.commit(0, True)
     for t in range(1, 11):
         if t >= 7:
@@ -132,10 +134,11 @@ def test_sam2_single_steady_state():
     print("sam2 stats", r.stats)
 
 
-def test_sam2_y_fp32_delta():
+@pytest.mark.parametrize("absorb", [False, True])
+def test_sam2_y_fp32_delta(absorb):
     """fp32 output exposes the attention update itself (no final rounding)."""
     cfg = CONFIGS["sam2_single"]
-    r = Runner(cfg, 9, max_sel=1228)
+    r = Runner(cfg, 9, max_sel=1228, absorb=absorb)
     r.commit(0, True)
     for t in range(1, 8):
         r.commit(t, False)
@@ -143,9 +146,10 @@ def test_sam2_y_fp32_delta():
     print("sam2 fp32-Y stats", r.stats)
 
 
-def test_multi_obj8_one_launch():
+@pytest.mark.parametrize("absorb", [False, True])
+def test_multi_obj8_one_launch(absorb):
     cfg = CONFIGS["multi_obj8"]
-    r = Runner(cfg, 10, max_sel=1228)
+    r = Runner(cfg, 10, max_sel=1228, absorb=absorb)
     r.commit(0, True)
     for t in range(1, 10):
         if t >= 8:
@@ -168,10 +172,11 @@ def test_highres_heads(rho):
     print("highres stats", r.stats)
 
 
-def test_keep_all_is_dense():
+@pytest.mark.parametrize("absorb", [False, True])
+def test_keep_all_is_dense(absorb):
     cfg = replace(CONFIGS["sam2_single"], m=32, n=32, full_prior=True, rho=1.0, rho_lo=None, rho_hi=None,
                   cap_frames=4, f_max=3)
-    r = Runner(cfg, 5, max_sel=cfg.mn)
+    r = Runner(cfg, 5, max_sel=cfg.mn, absorb=absorb)
     r.commit(0, True)
     for t in range(1, 4):
         r.commit(t, False)
