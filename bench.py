@@ -107,7 +107,7 @@ def _kernel_source_hash() -> str:
 def _traffic(kernel: str):
     """HBM bytes per launch from the committed counter summary, if it was
     taken on the current kernel source."""
-    path = os.path.join(ROOT, "profiles", "traffic_%s.json" % kernel)
+    path = os.path.join(ROOT, "profiles", "traffic_%s.txt" % kernel)
     try:
         d = json.load(open(path))
     except (OSError, ValueError):
@@ -176,6 +176,15 @@ def gpu_run(args):
         sess.commit(f["K"], f["V"], f["mask"], t, False)
         step_t[0] += 1
 
+    if args.copy_probe_mb > 0:
+        # one plain device copy of known size: calibrates the HBM byte counters
+        nb = args.copy_probe_mb << 20
+        src_t = torch.ones(nb // 4, dtype=torch.float32, device=dev)
+        dst_t = torch.empty_like(src_t)
+        torch.cuda.synchronize()
+        dst_t.copy_(src_t)
+        torch.cuda.synchronize()
+        del src_t, dst_t
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -215,7 +224,7 @@ def gpu_run(args):
         if n and not name.startswith("_"):
             kernels[name] = {"launches": n, "avg_us": 1000.0 * ms / n, "us_per_step": 1000.0 * ms / args.steps}
     kernel_sum_us = sum(v["us_per_step"] for v in kernels.values())
-    traffic = _traffic("attn_" + cfg.name)
+    traffic = _traffic("attn_%s_%s" % (cfg.name, "absorbed" if absorb else "projected"))
     out = {
         "metric": METRIC,
         "value": fps,
@@ -265,6 +274,7 @@ def main():
     ap.add_argument("--splits", type=int, default=0)
     ap.add_argument("--layer", choices=["auto", "projected", "absorbed"], default="auto")
     ap.add_argument("--cpu-frames", type=int, default=12)
+    ap.add_argument("--copy-probe-mb", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-child", action="store_true")
     args = ap.parse_args()

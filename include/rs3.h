@@ -175,7 +175,7 @@ rs3_status rs3_select_queries(const rs3_grid* g, int32_t n_obj, const uint8_t* m
  * sel_idx/sel_count : as produced by rs3_select_queries; sel_stride = m*n
  *          for per-object lists or 0 for one shared list
  * max_sel: upper bound on every sel_count used (host grid size), <= m*n
- * n_splits: key splits per query tile (0 = automatic); n_splits*H <= 512
+ * n_splits: key splits per query tile (0 = automatic); n_splits*H <= 256
  * Y      : [n_obj][m*n][C] with stride y_obj_stride (elements); may equal X
  *          (in place) only when n_obj == 1 or X is per object with the same
  *          stride.  y_fp32 = 1 writes Y as fp32 for diagnostics (never in

@@ -467,18 +467,23 @@ __global__ __launch_bounds__(CB_THREADS) void k_combine(Rs3ReadoutArgs a) {
     for (int s = 0; s < SA; ++s) mv[s] = (M != -INFINITY) ? __builtin_amdgcn_exp2f(mv[s] - M) * lv[s] * iw : 0.f;
   }
   __syncthreads();
-  // 2. merged O rows into LDS
+  // 2. merged O rows into LDS.  Each (row, 8-column chunk) is summed by
+  //    NG thread groups over interleaved splits, then reduced through LDS.
   const bf16_t* Op = (const bf16_t*)a.Opart;
   const int cpr = D / 8;
-  for (int q = tid; q < CB_ROWS * cpr; q += CB_THREADS) {
-    const int rr = q / cpr, d0 = 8 * (q - rr * cpr), h = d0 / d_h, row = r0 + rr;
+  const int items = CB_ROWS * cpr;
+  const int NG = max(1, min(8, CB_THREADS / items));   // split groups per item
+  float* red = wts + 2 * CB_ROWS * H * SA;              // [NG][items][8]
+  for (int q = tid; q < items * NG; q += CB_THREADS) {
+    const int item = q % items, grp = q / items;
+    const int rr = item / cpr, d0 = 8 * (item - rr * cpr), h = d0 / d_h, row = r0 + rr;
     float acc8[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     if (row < cnt) {
       const float* w = wts + (rr * H + h) * SA;
       const bf16_t* src = Op + (base + row) * D + d0;
       const int64_t sstride = (int64_t)a.max_sel * D;
-#pragma unroll 8
-      for (int s = 0; s < SA; ++s) {
+#pragma unroll 4
+      for (int s = grp; s < SA; s += NG) {
         const float ws = w[s];
         const u32x4 v = *(const u32x4*)(src + s * sstride);
 #pragma unroll
@@ -487,6 +492,19 @@ __global__ __launch_bounds__(CB_THREADS) void k_combine(Rs3ReadoutArgs a) {
           acc8[2 * j + 1] += ws * __uint_as_float(v[j] & 0xffff0000u);
         }
       }
+    }
+    float* dst = red + ((int64_t)grp * items + item) * 8;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) dst[j] = acc8[j];
+  }
+  __syncthreads();
+  for (int item = tid; item < items; item += CB_THREADS) {
+    const int rr = item / cpr, d0 = 8 * (item - rr * cpr);
+    float acc8[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int grp = 0; grp < NG; ++grp) {
+      const float* src = red + ((int64_t)grp * items + item) * 8;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc8[j] += src[j];
     }
     u32x4 pk;
 #pragma unroll
@@ -648,7 +666,10 @@ __global__ __launch_bounds__(256) void k_readout_f32(Rs3ReadoutArgs a) {
 using namespace rs3;
 
 static size_t combine_lds_bytes(int D, int H, int S) {
-  return (((size_t)CB_ROWS * (D + 8) * 2 + 15) & ~(size_t)15) + (size_t)2 * CB_ROWS * H * S * 4;
+  const int items = CB_ROWS * (D / 8);
+  const int NG = CB_THREADS / items < 1 ? 1 : (CB_THREADS / items > 8 ? 8 : CB_THREADS / items);
+  return (((size_t)CB_ROWS * (D + 8) * 2 + 15) & ~(size_t)15) + (size_t)2 * CB_ROWS * H * S * 4 +
+         (size_t)NG * items * 8 * 4;
 }
 
 hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st) {
@@ -703,10 +724,15 @@ hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st
 }
 
 hipError_t rs3_readout_setup() {
-  // H * S <= RS3_MAX_SPLITS_X_HEADS and D <= 1024 (checked on the host)
-  const int max_lds = (int)combine_lds_bytes(1024, 1, RS3_MAX_SPLITS_X_HEADS);
+  // H * S <= RS3_MAX_SPLITS_X_HEADS and D <= 1024 (checked on the host);
+  // the group buffer is largest for D = 1024 with one group or D = 64 with 4
+  size_t max_lds = 0;
+  for (int D = 64; D <= 1024; D *= 2) {
+    const size_t b = combine_lds_bytes(D, 1, RS3_MAX_SPLITS_X_HEADS);
+    if (b > max_lds) max_lds = b;
+  }
   hipError_t e = hipFuncSetAttribute((const void*)k_combine<bf16_t>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                     max_lds);
+                                     (int)max_lds);
   if (e != hipSuccess) return e;
-  return hipFuncSetAttribute((const void*)k_combine<float>, hipFuncAttributeMaxDynamicSharedMemorySize, max_lds);
+  return hipFuncSetAttribute((const void*)k_combine<float>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)max_lds);
 }

@@ -125,7 +125,7 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 // resident tiles, so with few tiles only the first splits are active.
 constexpr int MIN_TILES_PER_SPLIT = 2;
 // Key splits times heads per readout call (bounds the merge kernel's LDS).
-#define RS3_MAX_SPLITS_X_HEADS 512
+#define RS3_MAX_SPLITS_X_HEADS 256
 __host__ __device__ __forceinline__ int split_tiles(int ntiles, int S) {
   int tps = (ntiles + S - 1) / S;
   return tps < MIN_TILES_PER_SPLIT ? MIN_TILES_PER_SPLIT : tps;
