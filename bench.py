@@ -159,11 +159,23 @@ def gpu_run(args):
         sess.commit(f["K"], f["V"], f["mask"], t, t < cfg.n_pin)
 
     step_t = [n_pre]
+    main = torch.cuda.current_stream()
+    two = args.streams == 2
+    side = torch.cuda.Stream() if two else main
+    ev_read = torch.cuda.Event()
+    ev_commit = torch.cuda.Event()
+    ev_commit.record(main)
 
     def step(record=None):
+        # The selection of frame t needs only frame t's read mask and tokens,
+        # so it runs while frame t-1's commit is still in flight on the side
+        # stream; the readout waits for that commit (its bank must hold frame
+        # t-1), and frame t's commit waits for the readout.
         t = step_t[0]
         f = frames[n_pre + (t - n_pre) % N_DISTINCT]
         sess.select(f["rmask"], f["X"], f["k"])
+        if two:
+            main.wait_event(ev_commit)
         if record is not None:
             cnt = sess.sel_count.cpu().numpy()
             nk = [b.info()["n_keys"] for b in sess.banks]
@@ -173,15 +185,23 @@ def gpu_run(args):
             sess.readout(f["X"], f["X"], max_sel=f["max_sel"])
         else:
             sess.readout(f["X"], Y, max_sel=f["max_sel"])
-        sess.commit(f["K"], f["V"], f["mask"], t, False)
+        if two:
+            ev_read.record(main)
+            side.wait_event(ev_read)
+            sess.commit(f["K"], f["V"], f["mask"], t, False, stream=side.cuda_stream)
+            ev_commit.record(side)
+        else:
+            sess.commit(f["K"], f["V"], f["mask"], t, False)
         step_t[0] += 1
 
     if args.copy_probe_mb > 0:
-        # one plain device copy of known size: calibrates the HBM byte counters
+        # kernels of known traffic that calibrate the HBM byte counters: a fill
+        # (writes nb bytes), a sum (reads nb bytes) and a device copy (both)
         nb = args.copy_probe_mb << 20
         src_t = torch.ones(nb // 4, dtype=torch.float32, device=dev)
-        dst_t = torch.empty_like(src_t)
         torch.cuda.synchronize()
+        float(src_t.sum())
+        dst_t = torch.empty_like(src_t)
         dst_t.copy_(src_t)
         torch.cuda.synchronize()
         del src_t, dst_t
@@ -191,10 +211,13 @@ def gpu_run(args):
     # pass A: frames/s, no instrumentation
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    ev0.record()
+    ev0.record(main)
+    h0 = time.perf_counter()
     for _ in range(args.steps):
         step()
-    ev1.record()
+    host_us = (time.perf_counter() - h0) * 1e6 / args.steps
+    main.wait_event(ev_commit)
+    ev1.record(main)
     torch.cuda.synchronize()
     ms_total = ev0.elapsed_time(ev1)
     ms_step = ms_total / args.steps
@@ -240,7 +263,7 @@ def gpu_run(args):
         "data": "synthetic",
         "config": {"workload": _describe(cfg), "grid": "%dx%d" % (cfg.m, cfg.n), "n_obj": cfg.n_obj,
                    "bank_frames": cfg.f_max, "d_model": cfg.C, "heads": cfg.H, "d_head": cfg.d_h,
-                   "d_kv": cfg.d_kv, "eager_launches": True, "readout": "in place" if in_place else "out of place",
+                   "d_kv": cfg.d_kv, "eager_launches": True, "streams": args.streams, "readout": "in place" if in_place else "out of place",
                    "attention": ("absorbed: one head of width d_kv=%d on the raw bank rows" % cfg.d_kv) if absorb
                    else ("projected: %d head(s) of width %d" % (cfg.H, cfg.d_h))},
         "roofline": {"bound": "mfma", "achieved": achieved_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
@@ -260,6 +283,7 @@ def gpu_run(args):
             "kernel_sum_us_per_step": kernel_sum_us,
             "bank_errors": errs,
             "splits": sess.n_splits,
+            "host_enqueue_us_per_step": host_us,
         },
     }
     return out
@@ -273,7 +297,9 @@ def main():
     ap.add_argument("--workload", default="sam2_single")
     ap.add_argument("--splits", type=int, default=0)
     ap.add_argument("--layer", choices=["auto", "projected", "absorbed"], default="auto")
-    ap.add_argument("--cpu-frames", type=int, default=12)
+    ap.add_argument("--streams", type=int, choices=[1, 2], default=1,
+                    help="2: frame t's commit overlaps frame t+1's selection on a second stream")
+    ap.add_argument("--cpu-frames", type=int, default=40)
     ap.add_argument("--copy-probe-mb", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-child", action="store_true")
