@@ -371,7 +371,8 @@ rs3_status rs3_select_workspace_size(const rs3_grid* g, int32_t n_obj, int64_t x
   if (!bytes || !grid_ok(g) || n_obj <= 0 || n_obj > RS3_MAX_OBJ || x_obj_stride < 0) return RS3_E_INVALID;
   const int64_t mn = (int64_t)g->m * g->n;
   const int n_x = x_obj_stride ? n_obj : 1;
-  *bytes = (size_t)n_x * mn * 8;
+  // energies [n_x][mn] fp64, then per-64-cell energy ranges [n_x][ceil(mn/64)][2]
+  *bytes = align256((size_t)n_x * mn * 8) + (size_t)n_x * ((mn + 63) / 64) * 16;
   return RS3_OK;
 }
 
@@ -398,13 +399,15 @@ rs3_status rs3_select_queries(const rs3_grid* g, int32_t n_obj, const uint8_t* m
   hipStream_t st = (hipStream_t)stream;
   const int n_x = x_obj_stride ? n_obj : 1;
   double* e = (double*)ws;
-  hipError_t he = rs3_launch_energy(X, x_obj_stride, n_x, mn, C, dt, e, st);
+  unsigned long long* erange = (unsigned long long*)((uint8_t*)ws + align256((size_t)n_x * mn * 8));
+  hipError_t he = rs3_launch_energy(X, x_obj_stride, n_x, mn, C, dt, e, erange, st);
   if (he != hipSuccess) return map_err(he);
   Rs3SelectArgs a;
   memset(&a, 0, sizeof(a));
   a.masks = masks;
   a.track = tr->d_state;
   a.e = e;
+  a.erange = erange;
   a.sel_idx = sel_idx;
   a.sel_count = sel_count;
   a.prior_out = prior_out;

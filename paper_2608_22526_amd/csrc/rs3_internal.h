@@ -146,6 +146,7 @@ struct Rs3SelectArgs {
   const uint8_t* masks;   // [n_obj][m*s][n*s]
   int32_t* track;         // [n_obj][RS3_TRACK_WORDS]
   const double* e;        // [n_x][mn] energies
+  const unsigned long long* erange;   // [n_x][ceil(mn/64)][2] min/max energy bits per 64 cells
   int32_t* sel_idx;       // [n_groups][mn]
   int32_t* sel_count;     // [n_groups]
   uint8_t* prior_out;     // [n_groups][mn] or null
@@ -185,7 +186,7 @@ struct Rs3ReadoutArgs {
 
 // Launchers (all enqueue on `st` and return the launch status).
 hipError_t rs3_launch_energy(const void* X, int64_t x_stride, int n_x, int mn, int C, int dtype,
-                             double* e, hipStream_t st);
+                             double* e, unsigned long long* range, hipStream_t st);
 hipError_t rs3_launch_select(const Rs3SelectArgs& a, int n_groups, hipStream_t st);
 hipError_t rs3_launch_commit(const Rs3CommitArgs& a, int dtype, int d_kv, int D, int H, int d_h,
                              hipStream_t st);

@@ -16,6 +16,7 @@ namespace rs3 {
 
 constexpr int SEL_THREADS = 1024;
 constexpr int SEL_WAVES = SEL_THREADS / 64;
+constexpr int SEL_RANK_BYTES = SEL_THREADS * (8 + 4 + 4);
 
 // ---------------------------------------------------------------------------
 template <typename T>
@@ -42,23 +43,45 @@ __device__ __forceinline__ void load_row_chunk<float>(const float* p, double* v)
   }
 }
 
-// grid (ceil(mn/64), n_x), block 64.  C is a multiple of 8.
+// grid (ceil(mn/64), n_x), block 64.  C is a multiple of 8.  Also writes the
+// smallest and largest energy bit pattern of the block's rows to
+// range[xi][block] (energies are >= 0, so bit order is numeric order).
 template <typename T>
 __global__ __launch_bounds__(64) void k_energy(const T* __restrict__ X, int64_t x_stride, int mn,
-                                                int C, double* __restrict__ e) {
+                                                int C, double* __restrict__ e,
+                                                unsigned long long* __restrict__ range) {
   const int xi = blockIdx.y;
   const int i = blockIdx.x * 64 + threadIdx.x;
-  if (i >= mn) return;
-  const T* row = X + (int64_t)xi * x_stride + (int64_t)i * C;
-  double acc = 0.0;
-  for (int c = 0; c < C; c += 8) {
-    double v[8];
-    load_row_chunk<T>(row + c, v);
+  unsigned long long lo = ~0ull, hi = 0ull;
+  if (i < mn) {
+    const T* row = X + (int64_t)xi * x_stride + (int64_t)i * C;
+    double acc = 0.0;
+    for (int c = 0; c < C; c += 8) {
+      double v[8];
+      load_row_chunk<T>(row + c, v);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc = acc + v[j] * v[j];
+      for (int j = 0; j < 8; ++j) acc = acc + v[j] * v[j];
+    }
+    e[(int64_t)xi * mn + i] = acc;
+    lo = hi = (unsigned long long)__double_as_longlong(acc);
   }
-  e[(int64_t)xi * mn + i] = acc;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const unsigned long long ol = __shfl_xor(lo, off, 64), oh = __shfl_xor(hi, off, 64);
+    lo = ol < lo ? ol : lo;
+    hi = oh > hi ? oh : hi;
+  }
+  if (threadIdx.x == 0) {
+    unsigned long long* r = range + 2 * ((int64_t)xi * gridDim.x + blockIdx.x);
+    r[0] = lo;
+    r[1] = hi;
+  }
 }
+
+// Workgroup barrier for LDS traffic only: waits for this wave's LDS
+// operations, not for its outstanding global loads (which a __syncthreads
+// fence would drain).
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // ---------------------------------------------------------------------------
 // block-wide helpers for a 1024-thread workgroup
@@ -69,7 +92,40 @@ struct SelShared {
   int mode, r, gy0, gx0, gy1, gx1;
   int hist[256];
   int digit, remaining, full;
+  int ncand;
+  int red1[SEL_WAVES], red2[SEL_WAVES], red3[SEL_WAVES];
+  unsigned long long rowbits[SEL_WAVES];   // rows with a set cell, one bit per row
+  unsigned long long colbits[4];           // columns with a set cell
+  unsigned long long kmin, kmax;
 };
+
+// Exclusive prefix (in thread order) of the number of set bits among the
+// first cpt bits of `bits`, and the workgroup total; `red` is a private
+// SEL_WAVES-entry LDS array of the call site.  Ballot-based: no LDS or
+// cross-lane permutes inside a wave.
+template <int MAXC>
+__device__ __forceinline__ int block_scan_bits(uint32_t bits, int cpt, int* red, int* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int pre = 0, wtot = 0;
+#pragma unroll
+  for (int j = 0; j < MAXC; ++j)
+    if (j < cpt) {
+      const unsigned long long b = __ballot((bits >> j) & 1u);
+      pre += __builtin_amdgcn_mbcnt_hi((uint32_t)(b >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b, 0u));
+      wtot += __popcll(b);
+    }
+  if (lane == 0) red[wave] = wtot;
+  lds_barrier();
+  int before = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < SEL_WAVES; ++w) {
+    const int v = red[w];
+    tot += v;
+    before += w < wave ? v : 0;
+  }
+  *total = tot;
+  return before + pre;
+}
 
 __device__ __forceinline__ int wave_incl_scan(int v, int lane) {
 #pragma unroll
@@ -122,6 +178,36 @@ __device__ unsigned long long block_minmax_u64(unsigned long long v, bool want_m
   return r;
 }
 
+// One wave: the bin of sh.hist (256 bins, higher bins hold larger keys) that
+// holds the want-th largest candidate -> sh.digit, the rank of that candidate
+// inside its bin -> sh.remaining, and whether the bin is taken whole -> sh.full.
+__device__ void find_digit(SelShared& sh, int want, int lane) {
+  // lane owns bins 4*lane .. 4*lane+3
+  const int h0 = sh.hist[4 * lane], h1 = sh.hist[4 * lane + 1];
+  const int h2 = sh.hist[4 * lane + 2], h3 = sh.hist[4 * lane + 3];
+  const int mine = h0 + h1 + h2 + h3;
+  int suf = mine;  // inclusive suffix sum over lanes >= lane
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int t = __shfl_down(suf, off, 64);
+    if (lane + off < 64) suf += t;
+  }
+  const int above = suf - mine;  // candidates in bins of higher lanes
+  if (above < want && want <= suf) {
+    const int hb[4] = {h0, h1, h2, h3};
+    int cum = above;
+    for (int bb = 3; bb >= 0; --bb) {
+      if (cum + hb[bb] >= want) {
+        sh.digit = 4 * lane + bb;
+        sh.remaining = want - cum;
+        sh.full = (cum + hb[bb] == want);
+        break;
+      }
+      cum += hb[bb];
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 enum { MODE_NONE = 0, MODE_MASK = 1, MODE_BOX = 2 };
 
@@ -147,6 +233,207 @@ __device__ __forceinline__ uint64_t row_shift(const uint64_t* row, int W, int w,
 __device__ __forceinline__ uint64_t last_word_mask(int n, int W, int w) {
   const int rem = n - 64 * (W - 1);
   return (w == W - 1 && rem < 64) ? ((1ull << rem) - 1ull) : ~0ull;
+}
+
+// Tracker update of object o (single thread) from the box of its set pixels
+// (y1 < 0: empty mask), on the LDS copy of its words; writes the words back
+// and publishes the prior mode, radius and grid box in sh.
+__device__ void tracker_update(const Rs3SelectArgs& a, int o, int* tl, int by0, int bx0, int by1, int bx1,
+                               SelShared& sh) {
+  int32_t* tr = a.track + o * RS3_TRACK_WORDS;
+  const bool nonempty = by1 >= 0;
+  int mode = MODE_NONE, r = a.r_s;
+  if (nonempty) {
+    mode = a.seed_box ? MODE_BOX : MODE_MASK;
+    tl[0] = by0;
+    tl[1] = bx0;
+    tl[2] = by1;
+    tl[3] = bx1;
+    tl[4] = 0;
+    tl[5] = 1;
+  } else {
+    const int d = tl[4] + 1;
+    tl[4] = d;
+    if (tl[5]) {
+      mode = MODE_BOX;
+      by0 = tl[0];
+      bx0 = tl[1];
+      by1 = tl[2];
+      bx1 = tl[3];
+      r = a.r_s + min(d, a.c);
+    }
+  }
+  for (int w = 0; w < RS3_TRACK_WORDS; ++w) tr[w] = tl[w];
+  sh.mode = mode;
+  sh.r = r;
+  const int s = a.s;
+  if (mode == MODE_NONE) by0 = bx0 = by1 = bx1 = 0;
+  sh.gy0 = s == 1 ? by0 : by0 / s;
+  sh.gx0 = s == 1 ? bx0 : bx0 / s;
+  sh.gy1 = s == 1 ? by1 : by1 / s;
+  sh.gx1 = s == 1 ? bx1 : bx1 / s;
+}
+
+// Register path of the prior: grids of at most SEL_THREADS rows and
+// FAST_W*64 columns.  Thread y owns grid row y as FAST_W bit words; row
+// dilation is shifts inside the thread, the column dilation reads the
+// neighbouring rows once through LDS (rows: [m][FAST_W] words).
+constexpr int FAST_W = 4;
+
+__device__ __forceinline__ void row_dilate_regs(uint64_t* w, int W, int n, int rr) {
+  int done = 0;
+  while (done < rr) {
+    const int step = min(min(done + 1, rr - done), 63);   // no gaps: step <= done + 1
+    uint64_t o[FAST_W];
+#pragma unroll
+    for (int q = 0; q < FAST_W; ++q) {
+      uint64_t v = w[q];
+      if (q < W) {
+        // cell x takes x - step (left) and x + step (right); step < 64 here
+        const uint64_t lo = q > 0 ? w[q - 1] : 0ull, hi = q + 1 < W ? w[q + 1] : 0ull;
+        v |= (w[q] << step) | (lo >> (64 - step));
+        v |= (w[q] >> step) | (hi << (64 - step));
+        v &= last_word_mask(n, W, q);
+      }
+      o[q] = v;
+    }
+#pragma unroll
+    for (int q = 0; q < FAST_W; ++q) w[q] = o[q];
+    done += step;
+  }
+}
+
+// Adds object o's prior to the group rows g[] of this thread's grid row.
+// Communication is through LDS only (lds_barrier).
+__device__ void add_object_prior_fast(const Rs3SelectArgs& a, int o, uint64_t* rows, uint64_t* g,
+                                      SelShared& sh) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int m = a.m, n = a.n, s = a.s, W = (n + 63) >> 6;
+  const int Wpx = n * s, Hpx = m * s;
+  const uint8_t* M = a.masks + (int64_t)o * Hpx * Wpx;
+  int tw[RS3_TRACK_WORDS];   // tracker words (thread 0), first used after the box
+  if (tid == 0)
+    for (int w = 0; w < RS3_TRACK_WORDS; ++w) tw[w] = a.track[o * RS3_TRACK_WORDS + w];
+  const int y = tid;
+  uint64_t w[FAST_W] = {0, 0, 0, 0};
+  if (y < m) {
+    const uint8_t* rp = M + (int64_t)(y * s) * Wpx;
+    if (s == 1 && (n & 15) == 0 && (((uintptr_t)rp) & 15) == 0) {
+      for (int x0 = 0; x0 < n; x0 += 16) {
+        const u32x4 v = *(const u32x4*)(rp + x0);
+        uint32_t bits = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          uint32_t t = v[e];
+          t |= t >> 4;
+          t |= t >> 2;
+          t |= t >> 1;
+          bits |= ((t & 1u) | ((t >> 7) & 2u) | ((t >> 14) & 4u) | ((t >> 21) & 8u)) << (4 * e);
+        }
+        w[x0 >> 6] |= (uint64_t)bits << (x0 & 63);
+      }
+    } else {
+      for (int x = 0; x < n; ++x)
+        if (rp[x * s]) w[x >> 6] |= 1ull << (x & 63);
+    }
+  }
+  // bounding box in pixels.  s == 1: rows with a set cell (ballots) and the
+  // OR of all rows; otherwise a scan of every pixel.
+  if (s == 1) {
+    const uint64_t any = w[0] | w[1] | w[2] | w[3];
+    const unsigned long long rb = __ballot(any != 0ull);
+    if (lane == 0) sh.rowbits[wave] = rb;
+#pragma unroll
+    for (int q = 0; q < FAST_W; ++q)
+      if (q < W && w[q]) atomicOr(&sh.colbits[q], (unsigned long long)w[q]);
+  } else {
+    int y0 = 0x7fffffff, x0 = 0x7fffffff, y1 = -1, x1 = -1;
+    const int npx = Hpx * Wpx;
+    for (int p = tid; p < npx; p += SEL_THREADS)
+      if (M[p]) {
+        const int py = p / Wpx, px = p - py * Wpx;
+        y0 = min(y0, py);
+        y1 = max(y1, py);
+        x0 = min(x0, px);
+        x1 = max(x1, px);
+      }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      y0 = min(y0, __shfl_xor(y0, off, 64));
+      x0 = min(x0, __shfl_xor(x0, off, 64));
+      y1 = max(y1, __shfl_xor(y1, off, 64));
+      x1 = max(x1, __shfl_xor(x1, off, 64));
+    }
+    if (lane == 0 && y1 >= 0) {
+      atomicMin(&sh.bb[0], y0);
+      atomicMin(&sh.bb[1], x0);
+      atomicMax(&sh.bb[2], y1);
+      atomicMax(&sh.bb[3], x1);
+    }
+  }
+  lds_barrier();
+  if (tid == 0) {
+    int by0 = -1, bx0 = -1, by1 = -1, bx1 = -1;
+    if (s == 1) {
+      for (int q = 0; q < SEL_WAVES; ++q)
+        if (sh.rowbits[q]) {
+          const int lo = 64 * q + (int)__builtin_ctzll(sh.rowbits[q]);
+          const int hi = 64 * q + 63 - (int)__builtin_clzll(sh.rowbits[q]);
+          if (by0 < 0) by0 = lo;
+          by1 = hi;
+        }
+      for (int q = 0; q < W; ++q) {
+        const uint64_t c = sh.colbits[q];
+        sh.colbits[q] = 0ull;   // ready for the next object
+        if (c) {
+          if (bx0 < 0) bx0 = 64 * q + (int)__builtin_ctzll(c);
+          bx1 = 64 * q + 63 - (int)__builtin_clzll(c);
+        }
+      }
+    } else {
+      by0 = sh.bb[0];
+      bx0 = sh.bb[1];
+      by1 = sh.bb[2];
+      bx1 = sh.bb[3];
+      sh.bb[0] = 0x7fffffff;   // ready for the next object
+      sh.bb[1] = 0x7fffffff;
+      sh.bb[2] = -1;
+      sh.bb[3] = -1;
+    }
+    tracker_update(a, o, tw, by0, bx0, by1, bx1, sh);
+  }
+  lds_barrier();
+  const int mode = sh.mode, r = sh.r;
+  if (mode == MODE_BOX) {
+    const int ya = max(0, sh.gy0 - r), yb = min(m - 1, sh.gy1 + r);
+    const int xa = max(0, sh.gx0 - r), xb = min(n - 1, sh.gx1 + r);
+    if (y < m && y >= ya && y <= yb) {
+#pragma unroll
+      for (int q = 0; q < FAST_W; ++q) {
+        const int lo = max(xa, 64 * q), hi = min(xb, 64 * q + 63);
+        if (lo <= hi) {
+          const int len = hi - lo + 1;
+          g[q] |= (len == 64 ? ~0ull : ((1ull << len) - 1ull)) << (lo - 64 * q);
+        }
+      }
+    }
+  } else if (mode == MODE_MASK) {
+    row_dilate_regs(w, W, n, min(r, n));
+    if (y < m)
+#pragma unroll
+      for (int q = 0; q < FAST_W; ++q)
+        if (q < W) rows[y * W + q] = w[q];
+    lds_barrier();
+    if (y < m) {
+      const int ya = max(0, y - r), yb = min(m - 1, y + r);
+      for (int yy = ya; yy <= yb; ++yy)
+#pragma unroll
+        for (int q = 0; q < FAST_W; ++q)
+          if (q < W) g[q] |= rows[yy * W + q];
+    }
+  }
+  // rows, rowbits and the mode words are rewritten by the next object
+  lds_barrier();
 }
 
 // Adds one object's prior into U (LDS byte map of the group).  bufA/bufB are
@@ -191,40 +478,9 @@ __device__ void add_object_prior(const Rs3SelectArgs& a, int o, uint8_t* U, uint
   }
   __syncthreads();
   if (tid == 0) {
-    int32_t* tr = a.track + o * RS3_TRACK_WORDS;
-    const bool nonempty = sh.bb[2] >= 0;
-    int mode = MODE_NONE, r = a.r_s;
-    int by0 = 0, bx0 = 0, by1 = 0, bx1 = 0;
-    if (nonempty) {
-      by0 = sh.bb[0];
-      bx0 = sh.bb[1];
-      by1 = sh.bb[2];
-      bx1 = sh.bb[3];
-      mode = a.seed_box ? MODE_BOX : MODE_MASK;
-      tr[0] = by0;
-      tr[1] = bx0;
-      tr[2] = by1;
-      tr[3] = bx1;
-      tr[4] = 0;
-      tr[5] = 1;
-    } else {
-      const int d = tr[4] + 1;
-      tr[4] = d;
-      if (tr[5]) {
-        mode = MODE_BOX;
-        by0 = tr[0];
-        bx0 = tr[1];
-        by1 = tr[2];
-        bx1 = tr[3];
-        r = a.r_s + min(d, a.c);
-      }
-    }
-    sh.mode = mode;
-    sh.r = r;
-    sh.gy0 = by0 / s;
-    sh.gx0 = bx0 / s;
-    sh.gy1 = by1 / s;
-    sh.gx1 = bx1 / s;
+    int tw[RS3_TRACK_WORDS];
+    for (int w = 0; w < RS3_TRACK_WORDS; ++w) tw[w] = a.track[o * RS3_TRACK_WORDS + w];
+    tracker_update(a, o, tw, sh.bb[0], sh.bb[1], sh.bb[2], sh.bb[3], sh);
   }
   __syncthreads();
   const int mode = sh.mode, r = sh.r;
@@ -335,37 +591,181 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(Rs3SelectArgs a) {
   uint8_t* U = lds;
   uint8_t* base = lds + ((mn + 15) & ~15);
   uint8_t* tmp = base + buf;
+  uint8_t* rank_lds = tmp + buf;   // SEL_RANK_BYTES: candidate keys, cells, keep bits
 
-  for (int i = tid; i < mn; i += SEL_THREADS) U[i] = 0;
-  __syncthreads();
-  if (a.union_objects) {
-    for (int o = 0; o < a.n_obj; ++o) add_object_prior(a, o, U, base, tmp, sh);
-  } else {
-    add_object_prior(a, g, U, base, tmp, sh);
-  }
-  if (a.prior_out) {
-    for (int i = tid; i < mn; i += SEL_THREADS) a.prior_out[(int64_t)g * mn + i] = U[i];
-  }
-
-  // Contiguous cells per thread so that block scans follow cell order.
+  // Contiguous cells per thread so that block scans follow cell order.  The
+  // energies and tracker words do not depend on the prior: load them first.
   const int cpt = (mn + SEL_THREADS - 1) / SEL_THREADS;
   const int c0 = tid * cpt;
   const unsigned long long* ebits =
       reinterpret_cast<const unsigned long long*>(a.e + (a.x_per_obj ? (int64_t)g * mn : 0)) + c0;
-  uint32_t inP = 0;
   unsigned long long kreg[REG ? MAXC : 1];
+  if (REG) {
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) kreg[REG ? j : 0] = (j < cpt && c0 + j < mn) ? ebits[j] : 0ull;
+  }
+  // per-block energy ranges of this grid (wave 0, NR per lane), reduced later
+  constexpr int NR = MAXC / 4 > 0 ? MAXC / 4 : 1;
+  const int n_eblk = (mn + 63) >> 6;
+  unsigned long long rlo[NR], rhi[NR];
+  if (tid < 64) {
+    const unsigned long long* er = a.erange + 2 * (int64_t)(a.x_per_obj ? g : 0) * n_eblk;
+#pragma unroll
+    for (int q = 0; q < NR; ++q) {
+      const int bk = lane + 64 * q;
+      rlo[q] = bk < n_eblk ? er[2 * bk] : ~0ull;
+      rhi[q] = bk < n_eblk ? er[2 * bk + 1] : 0ull;
+    }
+  }
+  if (tid == 0) {
+    sh.bb[0] = 0x7fffffff;
+    sh.bb[1] = 0x7fffffff;
+    sh.bb[2] = -1;
+    sh.bb[3] = -1;
+  }
+  if (tid < 4) sh.colbits[tid] = 0ull;
+  if (tid < 256) sh.hist[tid] = 0;
+  const int W = (a.n + 63) >> 6;
+  const bool fast = a.m <= SEL_THREADS && W <= FAST_W;
+  uint64_t* Gs = reinterpret_cast<uint64_t*>(base);   // fast path: group prior rows [m][W]
+  if (fast) {
+    uint64_t* rows = reinterpret_cast<uint64_t*>(tmp);
+    uint64_t gw[FAST_W] = {0, 0, 0, 0};
+    lds_barrier();
+    if (a.union_objects) {
+      for (int o = 0; o < a.n_obj; ++o) add_object_prior_fast(a, o, rows, gw, sh);
+    } else {
+      add_object_prior_fast(a, g, rows, gw, sh);
+    }
+    if (tid < a.m)
+#pragma unroll
+      for (int q = 0; q < FAST_W; ++q)
+        if (q < W) Gs[tid * W + q] = gw[q];
+    lds_barrier();
+  } else {
+    for (int i = tid; i < mn; i += SEL_THREADS) U[i] = 0;
+    __syncthreads();
+    if (a.union_objects) {
+      for (int o = 0; o < a.n_obj; ++o) add_object_prior(a, o, U, base, tmp, sh);
+    } else {
+      add_object_prior(a, g, U, base, tmp, sh);
+    }
+  }
+  // this thread's cells c0 .. c0+cpt-1 start at grid row cy, column cx
+  int cy = c0 / a.n, cx = c0 - cy * a.n;
+  uint32_t inP = 0;
 #pragma unroll
   for (int j = 0; j < MAXC; ++j) {
-    const int i = c0 + j;
-    const bool in = j < cpt && i < mn && U[i];
-    if (in) inP |= 1u << j;
-    if (REG) kreg[REG ? j : 0] = in ? ebits[j] : 0ull;
+    if (j < cpt && c0 + j < mn) {
+      const bool in = fast ? ((Gs[cy * W + (cx >> 6)] >> (cx & 63)) & 1ull) : U[c0 + j] != 0;
+      if (in) inP |= 1u << j;
+      if (++cx == a.n) {
+        cx = 0;
+        ++cy;
+      }
+    }
+  }
+  if (a.prior_out) {
+    uint8_t* po = a.prior_out + (int64_t)g * mn + c0;
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j)
+      if (j < cpt && c0 + j < mn) po[j] = (inP >> j) & 1u;
   }
   auto key_of = [&](int j) -> unsigned long long { return REG ? kreg[REG ? j : 0] : ebits[j]; };
   const int k = a.k[g];
-  const int countP = block_sum(__popc(inP), sh);
+  int countP;
+  block_scan_bits<MAXC>(inP, cpt, sh.red1, &countP);
   uint32_t keep = inP;
   if (countP > k) {
+    bool done = false;
+    if (tid < 64) {
+      unsigned long long l = rlo[0], h = rhi[0];
+#pragma unroll
+      for (int q = 1; q < NR; ++q) {
+        l = rlo[q] < l ? rlo[q] : l;
+        h = rhi[q] > h ? rhi[q] : h;
+      }
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) {
+        const unsigned long long ol = __shfl_xor(l, off, 64), oh = __shfl_xor(h, off, 64);
+        l = ol < l ? ol : l;
+        h = oh > h ? oh : h;
+      }
+      if (tid == 0) {
+        sh.kmin = l;
+        sh.kmax = h;
+      }
+    }
+    lds_barrier();
+    // range of the grid's energies: it contains every candidate key
+    const unsigned long long kmin = sh.kmin, kmax = sh.kmax;
+    if (k > 0 && kmin != kmax) {
+      // One histogram over 256 equal-width bins of [kmin, kmax] (bin of a key
+      // is monotone in the key, so every key of a higher bin is larger), then
+      // an exact rank inside the bin that holds the k-th largest key.
+      const double scale = 256.0 / (double)(kmax - kmin);
+      auto bin_of = [&](unsigned long long key) -> int {
+        const int b = (int)((double)(key - kmin) * scale);
+        return b > 255 ? 255 : b;
+      };
+      if (tid == 0) sh.ncand = 0;
+#pragma unroll
+      for (int j = 0; j < MAXC; ++j)
+        if (inP >> j & 1) atomicAdd(&sh.hist[bin_of(key_of(j))], 1);
+      lds_barrier();
+      if (tid < 64) find_digit(sh, k, lane);
+      lds_barrier();
+      const int B = sh.digit, rem = sh.remaining, cntB = sh.hist[B];
+      const bool full = sh.full;
+      if (full || cntB <= SEL_THREADS) {
+        uint32_t kp = 0, inB = 0;
+#pragma unroll
+        for (int j = 0; j < MAXC; ++j)
+          if (inP >> j & 1) {
+            const int b = bin_of(key_of(j));
+            if (b > B || (full && b == B)) kp |= 1u << j;
+            if (b == B) inB |= 1u << j;
+          }
+        if (!full) {
+          unsigned long long* ck = reinterpret_cast<unsigned long long*>(rank_lds);
+          int* ci = reinterpret_cast<int*>(ck + SEL_THREADS);
+          uint32_t* kb = reinterpret_cast<uint32_t*>(ci + SEL_THREADS);
+          kb[tid] = 0;
+#pragma unroll
+          for (int j = 0; j < MAXC; ++j)
+            if (inB >> j & 1) {
+              const int q = atomicAdd(&sh.ncand, 1);
+              ck[q] = key_of(j);
+              ci[q] = c0 + j;
+            }
+          lds_barrier();
+          if (tid < cntB) {
+            const unsigned long long key = ck[tid];
+            const int idx = ci[tid];
+            int rank = 0;
+            for (int q0 = 0; q0 < cntB; q0 += 8) {
+              unsigned long long kq[8];
+              int iq[8];
+#pragma unroll
+              for (int u = 0; u < 8; ++u) {
+                const int q = q0 + u < cntB ? q0 + u : q0;
+                kq[u] = ck[q];
+                iq[u] = ci[q];
+              }
+#pragma unroll
+              for (int u = 0; u < 8; ++u)
+                rank += (q0 + u < cntB) && ((kq[u] > key) || (kq[u] == key && iq[u] < idx));
+            }
+            if (rank < rem) atomicOr(&kb[idx / cpt], 1u << (idx - (idx / cpt) * cpt));
+          }
+          lds_barrier();
+          kp |= kb[tid];
+        }
+        keep = kp;
+        done = true;
+      }
+    }
+    if (!done) {
     unsigned long long lo = ~0ull, hi = 0;
 #pragma unroll
     for (int j = 0; j < MAXC; ++j)
@@ -407,34 +807,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(Rs3SelectArgs a) {
           }
         }
         __syncthreads();
-        if (tid < 64) {
-          // lane owns bins 4*lane .. 4*lane+3; find the digit holding the
-          // remaining-th largest candidate
-          const int h0 = sh.hist[4 * lane], h1 = sh.hist[4 * lane + 1];
-          const int h2 = sh.hist[4 * lane + 2], h3 = sh.hist[4 * lane + 3];
-          const int mine = h0 + h1 + h2 + h3;
-          int suf = mine;  // inclusive suffix sum over lanes >= lane
-#pragma unroll
-          for (int off = 1; off < 64; off <<= 1) {
-            const int t = __shfl_down(suf, off, 64);
-            if (lane + off < 64) suf += t;
-          }
-          const int above = suf - mine;  // candidates in bins of higher lanes
-          const int want = remaining;
-          if (above < want && want <= suf) {
-            const int hb[4] = {h0, h1, h2, h3};
-            int cum = above;
-            for (int bb = 3; bb >= 0; --bb) {
-              if (cum + hb[bb] >= want) {
-                sh.digit = 4 * lane + bb;
-                sh.remaining = want - cum;
-                sh.full = (cum + hb[bb] == want);
-                break;
-              }
-              cum += hb[bb];
-            }
-          }
-        }
+        if (tid < 64) find_digit(sh, remaining, lane);
         __syncthreads();
         prefix |= (unsigned long long)sh.digit << shift;
         remaining = sh.remaining;
@@ -470,9 +843,10 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(Rs3SelectArgs a) {
         }
       }
     }
+    }
   }
   int total;
-  int before = block_excl_scan(__popc(keep), sh, &total);
+  int before = block_scan_bits<MAXC>(keep, cpt, sh.red3, &total);
   int32_t* out = a.sel_idx + (int64_t)g * mn;
 #pragma unroll
   for (int j = 0; j < MAXC; ++j)
@@ -485,23 +859,27 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(Rs3SelectArgs a) {
 using namespace rs3;
 
 hipError_t rs3_launch_energy(const void* X, int64_t x_stride, int n_x, int mn, int C, int dtype,
-                             double* e, hipStream_t st) {
+                             double* e, unsigned long long* range, hipStream_t st) {
   dim3 grid((mn + 63) / 64, n_x);
   if (dtype == RS3_BF16)
-    RS3_LAUNCH(RS3_K_ENERGY, st, k_energy<bf16_t>, grid, dim3(64), 0, st, (const bf16_t*)X, x_stride, mn, C, e);
+    RS3_LAUNCH(RS3_K_ENERGY, st, k_energy<bf16_t>, grid, dim3(64), 0, st, (const bf16_t*)X, x_stride, mn, C, e,
+               range);
   else
-    RS3_LAUNCH(RS3_K_ENERGY, st, k_energy<float>, grid, dim3(64), 0, st, (const float*)X, x_stride, mn, C, e);
+    RS3_LAUNCH(RS3_K_ENERGY, st, k_energy<float>, grid, dim3(64), 0, st, (const float*)X, x_stride, mn, C, e,
+               range);
   return hipGetLastError();
 }
 
 static size_t select_lds_bytes(int m, int n) {
-  return (size_t)((m * n + 15) & ~15) + 2 * (size_t)select_buf_bytes(m, n);
+  return (size_t)((m * n + 15) & ~15) + 2 * (size_t)select_buf_bytes(m, n) + SEL_RANK_BYTES;
 }
 
 hipError_t rs3_select_setup() {
   // largest layout: mn = RS3_MAX_MN with byte-sized buffers (3 * 32 KB)
-  const int mx = 3 * RS3_MAX_MN + 64;
-  hipError_t e = hipFuncSetAttribute((const void*)k_select<16>, hipFuncAttributeMaxDynamicSharedMemorySize, mx);
+  const int mx = 3 * RS3_MAX_MN + 64 + SEL_RANK_BYTES;
+  hipError_t e = hipFuncSetAttribute((const void*)k_select<4>, hipFuncAttributeMaxDynamicSharedMemorySize, mx);
+  if (e != hipSuccess) return e;
+  e = hipFuncSetAttribute((const void*)k_select<16>, hipFuncAttributeMaxDynamicSharedMemorySize, mx);
   if (e != hipSuccess) return e;
   return hipFuncSetAttribute((const void*)k_select<32>, hipFuncAttributeMaxDynamicSharedMemorySize, mx);
 }
@@ -509,7 +887,9 @@ hipError_t rs3_select_setup() {
 hipError_t rs3_launch_select(const Rs3SelectArgs& a, int n_groups, hipStream_t st) {
   const int mn = a.m * a.n;
   const size_t lds = select_lds_bytes(a.m, a.n);
-  if (mn <= 16 * SEL_THREADS)
+  if (mn <= 4 * SEL_THREADS)
+    RS3_LAUNCH(RS3_K_SELECT, st, k_select<4>, dim3(n_groups), dim3(SEL_THREADS), lds, st, a);
+  else if (mn <= 16 * SEL_THREADS)
     RS3_LAUNCH(RS3_K_SELECT, st, k_select<16>, dim3(n_groups), dim3(SEL_THREADS), lds, st, a);
   else
     RS3_LAUNCH(RS3_K_SELECT, st, k_select<32>, dim3(n_groups), dim3(SEL_THREADS), lds, st, a);
