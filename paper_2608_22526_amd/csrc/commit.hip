@@ -20,6 +20,7 @@ constexpr int CP_MAX_CPT = RS3_MAX_MN / CP_THREADS;
 
 struct CpShared {
   int red[CP_WAVES];
+  int red2[CP_WAVES];
   int ok, start, len;
 };
 
@@ -115,38 +116,83 @@ __device__ __forceinline__ uint64_t tile_mask(const int32_t* fr, int nf, int til
   return msk;
 }
 
-// grid n_obj, block 1024, dynamic LDS f_max*16 bytes.
+// Workgroup barrier for LDS traffic only (does not wait for this wave's
+// outstanding global loads).
+__device__ __forceinline__ void cp_lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// Exclusive prefix (thread order) of the set bits among the first n bits of
+// `bits`, and the workgroup total, from ballots; `red` is an LDS array of
+// CP_WAVES entries private to the call site.
+__device__ __forceinline__ int cp_scan_bits(uint32_t bits, int n, int* red, int* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int pre = 0, wtot = 0;
+  for (int j = 0; j < n; ++j) {
+    const unsigned long long b = __ballot((bits >> j) & 1u);
+    pre += __builtin_amdgcn_mbcnt_hi((uint32_t)(b >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b, 0u));
+    wtot += __popcll(b);
+  }
+  if (lane == 0) red[wave] = wtot;
+  cp_lds_barrier();
+  int before = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < CP_WAVES; ++w) {
+    const int v = red[w];
+    tot += v;
+    before += w < wave ? v : 0;
+  }
+  *total = tot;
+  return before + pre;
+}
+
+// grid n_obj, block 1024, dynamic LDS f_max*16 bytes.  Thread t owns the
+// cpt contiguous cells c0 = t*cpt ...; all cross-thread traffic is in LDS.
 __global__ __launch_bounds__(CP_THREADS) void k_commit_place(Rs3CommitArgs a) {
   extern __shared__ int32_t sfr[];
   __shared__ CpShared sh;
   const int o = blockIdx.x, tid = threadIdx.x;
-  BankDev& b = *a.banks[o];
+  const BankDev& b = *a.banks[o];
   const int m = a.m, n = a.n, s = a.s, mn = m * n, W = n * s;
   const uint8_t* M = a.masks + (int64_t)o * (m * s) * W;
   const int cpt = (mn + CP_THREADS - 1) / CP_THREADS;
   const int c0 = tid * cpt;
+  // frame table, header words and mask cells are independent: load together
+  const int f_max = b.f_max;
+  const int32_t fr_w = tid < 4 * f_max ? b.frames[tid] : 0;
+  int nf0 = 0, pin_end0 = 0;
+  if (tid == 0) {
+    nf0 = b.hdr[HDR_NFRAMES];
+    pin_end0 = b.hdr[HDR_PINEND];
+  }
   uint32_t bits = 0;
-  for (int j = 0; j < cpt; ++j) {
-    int i = c0 + j;
-    if (i < mn) {
-      int y = i / n, x = i - y * n;
+  if (s == 1 && cpt == 4 && c0 + 4 <= mn && ((((uintptr_t)M) + c0) & 3) == 0) {
+    uint32_t t = *(const uint32_t*)(M + c0);
+    t |= t >> 4;
+    t |= t >> 2;
+    t |= t >> 1;
+    bits = (t & 1u) | ((t >> 7) & 2u) | ((t >> 14) & 4u) | ((t >> 21) & 8u);
+  } else if (c0 < mn) {
+    int y = c0 / n, x = c0 - y * n;
+    for (int j = 0; j < cpt && c0 + j < mn; ++j) {
       if (M[(int64_t)(y * s) * W + x * s]) bits |= 1u << j;
+      if (++x == n) {
+        x = 0;
+        ++y;
+      }
     }
   }
+  const int nc = c0 < mn ? min(cpt, mn - c0) : 0;   // cells of this thread
   int total;
-  cp_block_excl_scan(__popc(bits), sh, &total);
-  if (total < a.fall_min || total > a.fall_max) {
-    bits = 0;
-    for (int j = 0; j < cpt; ++j)
-      if (c0 + j < mn) bits |= 1u << j;
+  int before = cp_scan_bits(bits, cpt, sh.red, &total);
+  if (total < a.fall_min || total > a.fall_max) {   // dense fall-through: every cell
+    bits = nc == 32 ? ~0u : ((1u << nc) - 1u);
+    before = c0 < mn ? c0 : mn;
+    total = mn;
   }
-  int before = cp_block_excl_scan(__popc(bits), sh, &total);
-  const int nf0 = b.hdr[HDR_NFRAMES];
-  for (int i = tid; i < 4 * nf0; i += CP_THREADS) sfr[i] = b.frames[i];
-  __syncthreads();
+  if (tid < 4 * f_max) sfr[tid] = fr_w;
+  cp_lds_barrier();
   if (tid == 0) {
     if (a.kept_count) a.kept_count[o] = total;
-    int nf = nf0, pin_end = b.hdr[HDR_PINEND];
+    int nf = nf0, pin_end = pin_end0;
     int start = place_frame(b, sfr, nf, pin_end, total, a.t, a.pin);
     sh.ok = start >= 0;
     sh.start = start;
@@ -156,16 +202,19 @@ __global__ __launch_bounds__(CP_THREADS) void k_commit_place(Rs3CommitArgs a) {
       b.hdr[HDR_PINEND] = pin_end;
       b.hdr[HDR_PSTART] = start;
       b.hdr[HDR_PLEN] = total;
+      int keys = 0;
+      for (int f = 0; f < nf; ++f) keys += sfr[4 * f + 1];
+      b.hdr[HDR_NKEYS] = keys;
     } else {
       b.hdr[HDR_PLEN] = -1;
       set_err(b.hdr, RS3_E_CAPACITY);
     }
   }
-  __syncthreads();
+  cp_lds_barrier();
   if (!sh.ok) return;
   const int start = sh.start;
   const int nf = sh.len;
-  for (int i = tid; i < 4 * nf; i += CP_THREADS) b.frames[i] = sfr[i];
+  if (tid < 4 * nf) b.frames[tid] = sfr[tid];
   for (int j = 0; j < cpt; ++j)
     if (bits >> j & 1) b.pos[start + before++] = c0 + j;
 
@@ -173,14 +222,21 @@ __global__ __launch_bounds__(CP_THREADS) void k_commit_place(Rs3CommitArgs a) {
   const int nt = b.n_tiles_cap;
   const int tpt = (nt + CP_THREADS - 1) / CP_THREADS;
   const int t0 = tid * tpt;
-  int cnt = 0;
-  for (int j = 0; j < tpt; ++j)
-    if (t0 + j < nt && tile_mask(sfr, nf, t0 + j)) ++cnt;
-  int ntot;
-  int pos = cp_block_excl_scan(cnt, sh, &ntot);
+  int ntot = 0, pos = 0;
+  if (tpt <= 32) {
+    uint32_t live = 0;
+    for (int j = 0; j < tpt; ++j)
+      if (t0 + j < nt && tile_mask(sfr, nf, t0 + j)) live |= 1u << j;
+    pos = cp_scan_bits(live, tpt, sh.red2, &ntot);
+  } else {
+    int cnt = 0;
+    for (int j = 0; j < tpt; ++j)
+      if (t0 + j < nt && tile_mask(sfr, nf, t0 + j)) ++cnt;
+    pos = cp_block_excl_scan(cnt, sh, &ntot);
+  }
   for (int j = 0; j < tpt; ++j) {
     if (t0 + j >= nt) break;
-    uint64_t msk = tile_mask(sfr, nf, t0 + j);
+    const uint64_t msk = tile_mask(sfr, nf, t0 + j);
     if (msk) {
       TileEnt te;
       te.tile = t0 + j;
@@ -189,12 +245,7 @@ __global__ __launch_bounds__(CP_THREADS) void k_commit_place(Rs3CommitArgs a) {
       b.tiles[pos++] = te;
     }
   }
-  if (tid == 0) {
-    int keys = 0;
-    for (int f = 0; f < nf; ++f) keys += sfr[4 * f + 1];
-    b.hdr[HDR_NTILES] = ntot;
-    b.hdr[HDR_NKEYS] = keys;
-  }
+  if (tid == 0) b.hdr[HDR_NTILES] = ntot;
 }
 
 // ---------------------------------------------------------------------------

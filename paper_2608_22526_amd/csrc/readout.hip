@@ -59,10 +59,19 @@ __global__ __launch_bounds__(256) void k_qproj(Rs3ReadoutArgs a) {
   const int col = c0 + 32 * (wave >> 1) + (lane & 31);
   const bf16_t* wr = (const bf16_t*)a.WqT + (int64_t)col * C;
   f32x16 acc = {};
-  for (int k = 0; k < C; k += 16) {
-    u32x4 av = *(const u32x4*)(xr + k + 8 * g);
-    u32x4 bv = *(const u32x4*)(wr + k + 8 * g);
-    acc = mfma32(av, bv, acc);
+  // 16 k steps per batch, all loads of a batch issued before its MFMAs
+  constexpr int KB = 16;
+  for (int k0 = 0; k0 < C; k0 += 16 * KB) {
+    u32x4 av[KB], bv[KB];
+#pragma unroll
+    for (int j = 0; j < KB; ++j)
+      if (k0 + 16 * j < C) {
+        av[j] = *(const u32x4*)(xr + k0 + 16 * j + 8 * g);
+        bv[j] = *(const u32x4*)(wr + k0 + 16 * j + 8 * g);
+      }
+#pragma unroll
+    for (int j = 0; j < KB; ++j)
+      if (k0 + 16 * j < C) acc = mfma32(av[j], bv[j], acc);
   }
   bf16_t* Q = (bf16_t*)a.Q + (int64_t)o * a.max_sel * D;
 #pragma unroll
@@ -423,7 +432,7 @@ __device__ __forceinline__ void copy_out<float>(float* p, bf16_t x) { *p = bf2f(
 //    the merge weights w_s = 2^(m_s - M) l_s / sum are formed in LDS;
 // 2. each thread merges one 8-column chunk over all active splits;
 // 3. y = x + O W_o on a 32x32x16 MFMA whose rows 16..31 are zero.
-constexpr int CB_ROWS = 16;
+constexpr int CB_ROWS = 16;   // the W_o step maps these rows to accumulator rows r < 8
 constexpr int CB_THREADS = 512;
 template <typename OutT>
 __global__ __launch_bounds__(CB_THREADS) void k_combine(Rs3ReadoutArgs a) {
@@ -440,6 +449,31 @@ __global__ __launch_bounds__(CB_THREADS) void k_combine(Rs3ReadoutArgs a) {
   const int SA = ntiles > 0 ? active_splits(ntiles, S) : 0;
   const int32_t* sel = a.sel_idx + (int64_t)o * a.sel_stride;
   const int64_t base = (int64_t)o * S * a.max_sel;
+  const bf16_t* X = (const bf16_t*)a.X + (int64_t)o * a.x_stride;
+  const bf16_t* WoT = (const bf16_t*)a.WoT;
+
+  // Loads of step 3 that do not depend on the merge, issued first: the
+  // destination cell of this lane's 8 accumulator rows r < 8 (rows
+  // 8*(r/4) + 4*g + r%4 < CB_ROWS; -1 = no row), and for the wave's first
+  // column block the residual inputs and the first batch of W_o operands.
+  constexpr int KB = 8;   // k steps per batch of W_o loads
+  int dst[8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    const int row = r0 + c_row(r, lane);
+    dst[r] = (row < cnt && sel_ok(sel, row, a.mn)) ? sel[row] : -1;
+  }
+  bf16_t xv0[8];
+  u32x4 bv0[KB];
+  if (wave < C / 32) {
+    const int col = 32 * wave + (lane & 31);
+#pragma unroll
+    for (int r = 0; r < 8; ++r) xv0[r] = dst[r] >= 0 ? X[(int64_t)dst[r] * C + col] : (bf16_t)0;
+    const bf16_t* wr = WoT + (int64_t)col * D;
+#pragma unroll
+    for (int j = 0; j < KB; ++j)
+      if (16 * j < D) bv0[j] = *(const u32x4*)(wr + 16 * j + 8 * g);
+  }
 
   // 1a. (m, l) of every active split: wts[(rr*H + h)*SA + s] = m, then l after
   for (int q = tid; q < CB_ROWS * H * SA; q += CB_THREADS) {
@@ -454,17 +488,23 @@ __global__ __launch_bounds__(CB_THREADS) void k_combine(Rs3ReadoutArgs a) {
     wts[CB_ROWS * H * SA + q] = l;
   }
   __syncthreads();
-  // 1b. weights per (row, head)
-  for (int rh = tid; rh < CB_ROWS * H; rh += CB_THREADS) {
+  // 1b. weights per (row, head), one wave per pair: lanes take the splits,
+  //     the max and the weight sum are wave reductions
+  for (int rh = wave; rh < CB_ROWS * H; rh += CB_THREADS / 64) {
     float* mv = wts + rh * SA;
     const float* lv = wts + CB_ROWS * H * SA + rh * SA;
     float M = -INFINITY;
-    for (int s = 0; s < SA; ++s) M = fmaxf(M, mv[s]);
+    for (int s = lane; s < SA; s += 64) M = fmaxf(M, mv[s]);
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) M = fmaxf(M, __shfl_xor(M, off, 64));
     float W = 0.f;
     if (M != -INFINITY)
-      for (int s = 0; s < SA; ++s) W += __builtin_amdgcn_exp2f(mv[s] - M) * lv[s];
+      for (int s = lane; s < SA; s += 64) W += __builtin_amdgcn_exp2f(mv[s] - M) * lv[s];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) W += __shfl_xor(W, off, 64);
     const float iw = W > 0.f ? 1.f / W : 0.f;
-    for (int s = 0; s < SA; ++s) mv[s] = (M != -INFINITY) ? __builtin_amdgcn_exp2f(mv[s] - M) * lv[s] * iw : 0.f;
+    for (int s = lane; s < SA; s += 64)
+      mv[s] = (M != -INFINITY) ? __builtin_amdgcn_exp2f(mv[s] - M) * lv[s] * iw : 0.f;
   }
   __syncthreads();
   // 2. merged O rows into LDS.  Each (row, 8-column chunk) is summed by
@@ -513,30 +553,43 @@ __global__ __launch_bounds__(CB_THREADS) void k_combine(Rs3ReadoutArgs a) {
   }
   __syncthreads();
   // 3. y = x + O W_o for the block's rows, columns split over the waves
-  const bf16_t* X = (const bf16_t*)a.X + (int64_t)o * a.x_stride;
   OutT* Y = (OutT*)a.Y + (int64_t)o * a.y_stride;
-  const bf16_t* WoT = (const bf16_t*)a.WoT;
   const bool arow = (lane & 31) < CB_ROWS;
   const bf16_t* orow = &Os[(arow ? (lane & 31) : 0) * OS + 8 * g];
   for (int nb = wave; nb < C / 32; nb += CB_THREADS / 64) {
+    const bool first = nb == wave;
     const int col = 32 * nb + (lane & 31);
     const bf16_t* wr = WoT + (int64_t)col * D;
+    bf16_t xv[8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r)
+      xv[r] = first ? xv0[r] : (dst[r] >= 0 ? X[(int64_t)dst[r] * C + col] : (bf16_t)0);
     f32x16 acc = {};
-    for (int k = 0; k < D; k += 16) {
-      const u32x4 av = arow ? *(const u32x4*)(orow + k) : u32x4{0, 0, 0, 0};
-      acc = mfma32(av, *(const u32x4*)(wr + k + 8 * g), acc);
+    for (int k0 = 0; k0 < D; k0 += 16 * KB) {
+      u32x4 bv[KB];
+      if (first && k0 == 0) {
+#pragma unroll
+        for (int j = 0; j < KB; ++j) bv[j] = bv0[j];
+      } else {
+#pragma unroll
+        for (int j = 0; j < KB; ++j)
+          if (k0 + 16 * j < D) bv[j] = *(const u32x4*)(wr + k0 + 16 * j + 8 * g);
+      }
+#pragma unroll
+      for (int j = 0; j < KB; ++j)
+        if (k0 + 16 * j < D) {
+          const u32x4 av = arow ? *(const u32x4*)(orow + k0 + 16 * j) : u32x4{0, 0, 0, 0};
+          acc = mfma32(av, bv[j], acc);
+        }
     }
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int rr = c_row(r, lane);
-      const int row = r0 + rr;
-      if (rr >= CB_ROWS || row >= cnt || !sel_ok(sel, row, a.mn)) continue;
-      const int64_t off = (int64_t)sel[row] * C + col;
-      const bf16_t xv = X[off];
+    for (int r = 0; r < 8; ++r) {
+      if (dst[r] < 0) continue;
+      const int64_t off = (int64_t)dst[r] * C + col;
       if (ntiles == 0)
-        copy_out<OutT>(&Y[off], xv);
+        copy_out<OutT>(&Y[off], xv[r]);
       else
-        store_out<OutT>(&Y[off], bf2f(xv) + acc[r]);
+        store_out<OutT>(&Y[off], bf2f(xv[r]) + acc[r]);
     }
   }
 }
