@@ -137,6 +137,20 @@ void rs3_bank_destroy(rs3_bank* b);
  * Synchronises the device. */
 rs3_status rs3_bank_export(const rs3_bank* b, int32_t* hdr, int32_t* frames,
                            void* K, void* V, int32_t* pos);
+/* Restore a bank from a snapshot in the rs3_bank_export format (checkpoint
+ * and resume).  The bank must have been created for a layer of the same
+ * shape and dtype, with at least the snapshot's capacity, frame count and
+ * pinned frames.  hdr uses words n_frames, pin_end, err and n_keys; frames,
+ * K, V and pos are as exported (rows concatenated in key order).  The
+ * snapshot must be a state the placement rule reaches: pinned frames first,
+ * packed from row 0 and adding up to pin_end, unpinned frames inside
+ * [pin_end, cap), non-empty frames disjoint, lengths adding up to n_keys;
+ * otherwise RS3_E_INVALID and the bank is unchanged.  The attention tiles
+ * are recomputed from the raw rows with this bank's layer, and the host-side
+ * pin bookkeeping follows the snapshot.  Synchronises the device. */
+rs3_status rs3_bank_import(rs3_bank* b, const int32_t* hdr /*[host]*/, const int32_t* frames /*[host]*/,
+                           const void* K /*[host]*/, const void* V /*[host]*/, const int32_t* pos /*[host]*/);
+
 /* Read (and optionally clear) the sticky device error word.  Synchronises. */
 rs3_status rs3_bank_error(rs3_bank* b, int32_t* err /*[host]*/, int32_t clear);
 

@@ -49,6 +49,7 @@ _SIGS = {
     "rs3_bank_create": (c_i32, [c_vp, c_i32, c_i32, c_i32, ctypes.POINTER(c_vp)]),
     "rs3_bank_destroy": (None, [c_vp]),
     "rs3_bank_export": (c_i32, [c_vp, c_vp, c_vp, c_vp, c_vp, c_vp]),
+    "rs3_bank_import": (c_i32, [c_vp, c_vp, c_vp, c_vp, c_vp, c_vp]),
     "rs3_bank_error": (c_i32, [c_vp, c_vp, c_i32]),
     "rs3_select_workspace_size": (c_i32, [ctypes.POINTER(Grid), c_i32, c_i64, ctypes.POINTER(c_sz)]),
     "rs3_select_queries": (c_i32, [ctypes.POINTER(Grid), c_i32, c_vp, c_vp, c_vp, c_i64, c_i32, c_i32, c_vp,
@@ -178,6 +179,18 @@ class Bank:
         nf, nk = int(hdr[0]), int(hdr[3])
         return dict(hdr=hdr, n_frames=nf, pin_end=int(hdr[1]), err=int(hdr[2]), n_keys=nk,
                     frames=frames[:nf].copy(), K=K[:nk].copy(), V=V[:nk].copy(), pos=pos[:nk].copy())
+
+    def import_snapshot(self, snap: dict):
+        """Restore from a dict in the format of export() (synchronises)."""
+        es = 2 if self.layer.dtype == RS3_BF16 else 4
+        npdt = np.uint16 if es == 2 else np.float32
+        hdr = np.ascontiguousarray(snap["hdr"], dtype=np.int32)
+        frames = np.ascontiguousarray(snap["frames"], dtype=np.int32).reshape(-1, 4)
+        K = np.ascontiguousarray(snap["K"], dtype=npdt)
+        V = np.ascontiguousarray(snap["V"], dtype=npdt)
+        pos = np.ascontiguousarray(snap["pos"], dtype=np.int32)
+        _check(lib().rs3_bank_import(self.h, hdr.ctypes.data, frames.ctypes.data, K.ctypes.data, V.ctypes.data,
+                                     pos.ctypes.data), "rs3_bank_import")
 
     def info(self) -> dict:
         """Header only (n_frames, pin_end, err, n_keys); synchronises."""

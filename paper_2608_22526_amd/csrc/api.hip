@@ -356,6 +356,92 @@ rs3_status rs3_bank_export(const rs3_bank* b, int32_t* hdr, int32_t* frames, voi
   return map_err(e);
 }
 
+rs3_status rs3_bank_import(rs3_bank* b, const int32_t* hdr, const int32_t* frames, const void* K, const void* V,
+                           const int32_t* pos) {
+  if (!b || !hdr) return RS3_E_INVALID;
+  BankDev& h = b->host;
+  const int nf = hdr[0], pin_end = hdr[1], err = hdr[2], keys = hdr[3];
+  if (nf < 0 || nf > h.f_max || pin_end < 0 || pin_end > h.cap || keys < 0 || keys > h.cap) return RS3_E_INVALID;
+  if (nf > 0 && !frames) return RS3_E_INVALID;
+  if (keys > 0 && (!K || !V || !pos)) return RS3_E_INVALID;
+  // the snapshot must be a state the placement rule can reach: pinned frames
+  // first and packed from row 0, unpinned frames inside [pin_end, cap), no
+  // two non-empty frames overlapping, lengths adding up to the key count
+  int n_pinned = 0, pinned_rows = 0, sum = 0;
+  bool unpinned = false;
+  for (int f = 0; f < nf; ++f) {
+    const int st = frames[4 * f], len = frames[4 * f + 1], pin = frames[4 * f + 3];
+    if (st < 0 || len < 0 || (int64_t)st + len > h.cap || (pin != 0 && pin != 1)) return RS3_E_INVALID;
+    if (pin) {
+      if (unpinned || st != pinned_rows) return RS3_E_INVALID;
+      ++n_pinned;
+      pinned_rows += len;
+    } else {
+      unpinned = true;
+      if (len > 0 && st < pin_end) return RS3_E_INVALID;
+    }
+    for (int q = 0; q < f; ++q) {
+      const int qs = frames[4 * q], ql = frames[4 * q + 1];
+      if (len > 0 && ql > 0 && qs < st + len && st < qs + ql) return RS3_E_INVALID;
+    }
+    sum += len;
+  }
+  if (n_pinned > h.n_pin || pinned_rows != pin_end || sum != keys) return RS3_E_INVALID;
+  const rs3_layer* L = b->L;
+  hipError_t e = hipDeviceSynchronize();
+  std::vector<int32_t> fr((size_t)h.f_max * 4, 0);
+  if (nf > 0) memcpy(fr.data(), frames, (size_t)nf * 16);
+  if (e == hipSuccess) e = hipMemcpy(h.frames, fr.data(), fr.size() * 4, hipMemcpyHostToDevice);
+  int32_t dh[HDR_WORDS] = {};
+  dh[HDR_NFRAMES] = nf;
+  dh[HDR_PINEND] = pin_end;
+  dh[HDR_ERR] = err;
+  dh[HDR_PLEN] = -1;
+  dh[HDR_NKEYS] = keys;
+  if (e == hipSuccess) e = hipMemcpy(h.hdr, dh, sizeof(dh), hipMemcpyHostToDevice);
+  const size_t row = (size_t)h.d_kv * dtype_size(h.dtype);
+  size_t off = 0;
+  for (int f = 0; f < nf && e == hipSuccess; ++f) {
+    const int st = fr[4 * f], len = fr[4 * f + 1];
+    if (len == 0) continue;
+    e = hipMemcpy((uint8_t*)h.Kraw + (size_t)st * row, (const uint8_t*)K + off * row, len * row,
+                  hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+      e = hipMemcpy((uint8_t*)h.Vraw + (size_t)st * row, (const uint8_t*)V + off * row, len * row,
+                    hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(h.pos + st, pos + off, (size_t)len * 4, hipMemcpyHostToDevice);
+    off += len;
+  }
+  if (e != hipSuccess) return map_err(e);
+  rs3_status st0 = ensure_setup();
+  if (st0 != RS3_OK) return st0;
+  // attention tiles of every resident frame, projected from the raw ring
+  Rs3CommitArgs a;
+  memset(&a, 0, sizeof(a));
+  a.banks[0] = b->d_desc;
+  a.WkT = L->dev.WkT;
+  a.WvT = L->dev.WvT;
+  a.absorb = L->dev.absorb;
+  a.n_obj = 1;
+  a.m = 1;
+  a.s = 1;
+  a.from_ring = 1;
+  for (int f = 0; f < nf && e == hipSuccess; ++f) {
+    const int span[2] = {fr[4 * f], fr[4 * f + 1]};
+    if (span[1] == 0) continue;
+    e = hipMemcpy(h.hdr + HDR_PSTART, span, sizeof(span), hipMemcpyHostToDevice);
+    a.n = span[1];
+    if (e == hipSuccess) e = rs3_launch_bank_restore(a, h.dtype, h.d_kv, 0, nullptr);
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+  }
+  if (e == hipSuccess) e = rs3_launch_bank_restore(a, h.dtype, h.d_kv, 1, nullptr);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) return map_err(e);
+  b->pin_calls = n_pinned;
+  b->unpinned_seen = unpinned ? 1 : 0;
+  return RS3_OK;
+}
+
 rs3_status rs3_bank_error(rs3_bank* b, int32_t* err, int32_t clear) {
   if (!b || !err) return RS3_E_INVALID;
   hipError_t e = hipDeviceSynchronize();

@@ -144,6 +144,39 @@ __device__ __forceinline__ int cp_scan_bits(uint32_t bits, int n, int* red, int*
   return before + pre;
 }
 
+// Rebuilds the resident tile list (ascending tiles with their row masks)
+// and hdr NTILES from the LDS frame table; every thread of the workgroup.
+__device__ void rebuild_tiles(const BankDev& b, const int32_t* sfr, int nf, CpShared& sh) {
+  const int tid = threadIdx.x;
+  const int nt = b.n_tiles_cap;
+  const int tpt = (nt + CP_THREADS - 1) / CP_THREADS;
+  const int t0 = tid * tpt;
+  int ntot = 0, pos = 0;
+  if (tpt <= 32) {
+    uint32_t live = 0;
+    for (int j = 0; j < tpt; ++j)
+      if (t0 + j < nt && tile_mask(sfr, nf, t0 + j)) live |= 1u << j;
+    pos = cp_scan_bits(live, tpt, sh.red2, &ntot);
+  } else {
+    int cnt = 0;
+    for (int j = 0; j < tpt; ++j)
+      if (t0 + j < nt && tile_mask(sfr, nf, t0 + j)) ++cnt;
+    pos = cp_block_excl_scan(cnt, sh, &ntot);
+  }
+  for (int j = 0; j < tpt; ++j) {
+    if (t0 + j >= nt) break;
+    const uint64_t msk = tile_mask(sfr, nf, t0 + j);
+    if (msk) {
+      TileEnt te;
+      te.tile = t0 + j;
+      te.pad = 0;
+      te.mask = msk;
+      b.tiles[pos++] = te;
+    }
+  }
+  if (tid == 0) b.hdr[HDR_NTILES] = ntot;
+}
+
 // grid n_obj, block 1024, dynamic LDS f_max*16 bytes.  Thread t owns the
 // cpt contiguous cells c0 = t*cpt ...; all cross-thread traffic is in LDS.
 __global__ __launch_bounds__(CP_THREADS) void k_commit_place(Rs3CommitArgs a) {
@@ -218,34 +251,26 @@ __global__ __launch_bounds__(CP_THREADS) void k_commit_place(Rs3CommitArgs a) {
   for (int j = 0; j < cpt; ++j)
     if (bits >> j & 1) b.pos[start + before++] = c0 + j;
 
-  // rebuild the resident tile list from the LDS frame table
-  const int nt = b.n_tiles_cap;
-  const int tpt = (nt + CP_THREADS - 1) / CP_THREADS;
-  const int t0 = tid * tpt;
-  int ntot = 0, pos = 0;
-  if (tpt <= 32) {
-    uint32_t live = 0;
-    for (int j = 0; j < tpt; ++j)
-      if (t0 + j < nt && tile_mask(sfr, nf, t0 + j)) live |= 1u << j;
-    pos = cp_scan_bits(live, tpt, sh.red2, &ntot);
-  } else {
-    int cnt = 0;
-    for (int j = 0; j < tpt; ++j)
-      if (t0 + j < nt && tile_mask(sfr, nf, t0 + j)) ++cnt;
-    pos = cp_block_excl_scan(cnt, sh, &ntot);
+  rebuild_tiles(b, sfr, nf, sh);
+}
+
+// Bank restore: frame table from device memory, then the tile list and the
+// key count (grid 1, block CP_THREADS, dynamic LDS f_max*16 bytes).
+__global__ __launch_bounds__(CP_THREADS) void k_bank_tiles(Rs3CommitArgs a) {
+  extern __shared__ int32_t sfr[];
+  __shared__ CpShared sh;
+  const int tid = threadIdx.x;
+  const BankDev& b = *a.banks[0];
+  const int nf = b.hdr[HDR_NFRAMES];
+  if (tid < 4 * nf) sfr[tid] = b.frames[tid];
+  __syncthreads();
+  if (tid == 0) {
+    int keys = 0;
+    for (int f = 0; f < nf; ++f) keys += sfr[4 * f + 1];
+    b.hdr[HDR_NKEYS] = keys;
+    b.hdr[HDR_PLEN] = -1;
   }
-  for (int j = 0; j < tpt; ++j) {
-    if (t0 + j >= nt) break;
-    const uint64_t msk = tile_mask(sfr, nf, t0 + j);
-    if (msk) {
-      TileEnt te;
-      te.tile = t0 + j;
-      te.pad = 0;
-      te.mask = msk;
-      b.tiles[pos++] = te;
-    }
-  }
-  if (tid == 0) b.hdr[HDR_NTILES] = ntot;
+  rebuild_tiles(b, sfr, nf, sh);
 }
 
 // ---------------------------------------------------------------------------
@@ -284,12 +309,17 @@ __global__ __launch_bounds__(256) void k_commit_append_bf16(Rs3CommitArgs a) {
     const int r = q / cpr, c = q - r * cpr;
     u32x4 kv = {0, 0, 0, 0}, vv = {0, 0, 0, 0};
     if (r < rows) {
-      const int src = spos[r];
-      kv = *(const u32x4*)(Km + (int64_t)src * d_kv + 8 * c);
-      vv = *(const u32x4*)(Vm + (int64_t)src * d_kv + 8 * c);
       const int64_t j = start + r0 + r;
-      *(u32x4*)(Kr + j * d_kv + 8 * c) = kv;
-      *(u32x4*)(Vr + j * d_kv + 8 * c) = vv;
+      if (a.from_ring) {
+        kv = *(const u32x4*)(Kr + j * d_kv + 8 * c);
+        vv = *(const u32x4*)(Vr + j * d_kv + 8 * c);
+      } else {
+        const int src = spos[r];
+        kv = *(const u32x4*)(Km + (int64_t)src * d_kv + 8 * c);
+        vv = *(const u32x4*)(Vm + (int64_t)src * d_kv + 8 * c);
+        *(u32x4*)(Kr + j * d_kv + 8 * c) = kv;
+        *(u32x4*)(Vr + j * d_kv + 8 * c) = vv;
+      }
     }
     *(u32x4*)(sK + r * RS + 8 * c) = kv;
     *(u32x4*)(sV + r * RS + 8 * c) = vv;
@@ -369,12 +399,14 @@ __global__ __launch_bounds__(256) void k_commit_append_f32(Rs3CommitArgs a) {
   const float* Vm = (const float*)a.Vmem + (int64_t)o * a.kv_stride;
   float* Kr = (float*)b.Kraw;
   float* Vr = (float*)b.Vraw;
-  for (int q = threadIdx.x; q < rows * d_kv; q += 256) {
-    int r = q / d_kv, c = q - r * d_kv;
-    int j = start + r0 + r;
-    int src = b.pos[j];
-    Kr[(int64_t)j * d_kv + c] = Km[(int64_t)src * d_kv + c];
-    Vr[(int64_t)j * d_kv + c] = Vm[(int64_t)src * d_kv + c];
+  if (!a.from_ring) {
+    for (int q = threadIdx.x; q < rows * d_kv; q += 256) {
+      int r = q / d_kv, c = q - r * d_kv;
+      int j = start + r0 + r;
+      int src = b.pos[j];
+      Kr[(int64_t)j * d_kv + c] = Km[(int64_t)src * d_kv + c];
+      Vr[(int64_t)j * d_kv + c] = Vm[(int64_t)src * d_kv + c];
+    }
   }
   const float* WkT = (const float*)a.WkT;
   const float* WvT = (const float*)a.WvT;
@@ -383,9 +415,8 @@ __global__ __launch_bounds__(256) void k_commit_append_f32(Rs3CommitArgs a) {
   for (int q = threadIdx.x; q < rows * D; q += 256) {
     int r = q / D, d = q - r * D;
     int j = start + r0 + r;
-    int src = b.pos[j];
-    const float* kr = Km + (int64_t)src * d_kv;
-    const float* vr = Vm + (int64_t)src * d_kv;
+    const float* kr = a.from_ring ? Kr + (int64_t)j * d_kv : Km + (int64_t)b.pos[j] * d_kv;
+    const float* vr = a.from_ring ? Vr + (int64_t)j * d_kv : Vm + (int64_t)b.pos[j] * d_kv;
     float sk, sv;
     if (a.absorb) {  // attention on the raw rows
       sk = kr[d];
@@ -433,5 +464,19 @@ hipError_t rs3_launch_commit(const Rs3CommitArgs& a, int dtype, int d_kv, int D,
                st, a);
   else
     RS3_LAUNCH(RS3_K_COMMIT_APPEND, st, k_commit_append_f32, grid, dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t rs3_launch_bank_restore(const Rs3CommitArgs& a, int dtype, int d_kv, int rebuild, hipStream_t st) {
+  if (rebuild) {
+    hipLaunchKernelGGL(k_bank_tiles, dim3(1), dim3(CP_THREADS), 256 * 16, st, a);
+    return hipGetLastError();
+  }
+  const int mn = a.m * a.n;   // upper bound on the rows of the span
+  dim3 grid(1, (mn + 63) / 64);
+  if (dtype == RS3_BF16)
+    hipLaunchKernelGGL(k_commit_append_bf16, grid, dim3(256), (size_t)2 * 64 * (d_kv + 8) * 2, st, a);
+  else
+    hipLaunchKernelGGL(k_commit_append_f32, grid, dim3(256), 0, st, a);
   return hipGetLastError();
 }

@@ -164,6 +164,7 @@ struct Rs3CommitArgs {
   const void* WkT;        // [D][d_kv] (projected mode)
   const void* WvT;
   int m, n, s, t, pin, fall_min, fall_max, n_obj, absorb;
+  int from_ring;          // append: rows are already in the raw ring (bank import)
 };
 
 struct Rs3ReadoutArgs {
@@ -191,6 +192,10 @@ hipError_t rs3_launch_select(const Rs3SelectArgs& a, int n_groups, hipStream_t s
 hipError_t rs3_launch_commit(const Rs3CommitArgs& a, int dtype, int d_kv, int D, int H, int d_h,
                              hipStream_t st);
 hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st);
+// Projects the raw ring rows [hdr PSTART, + PLEN) of bank 0 of `a` into its
+// attention tiles (a.from_ring = 1), or, with rebuild = 1, rebuilds the
+// resident tile list and key count from the frame table.
+hipError_t rs3_launch_bank_restore(const Rs3CommitArgs& a, int dtype, int d_kv, int rebuild, hipStream_t st);
 hipError_t rs3_readout_setup();
 void rs3_prof_begin(int id, hipStream_t st);
 void rs3_prof_end(int id, hipStream_t st);
