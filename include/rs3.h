@@ -219,6 +219,22 @@ rs3_status rs3_commit(rs3_bank* const* banks /*[host]*/, int32_t n_obj, const rs
                       const uint8_t* masks, int32_t t, int32_t pin, int32_t fall_min,
                       int32_t fall_max, int32_t* kept_count, void* stream);
 
+/* ---- bare attention core (Sec. 3.1, Eq. 6 without the projections) ---------
+ * O_h = softmax(Q_h K_h^T / sqrt(d_h)) V_h for every head h on tensors that
+ * are already projected: Qh [n_q][H][d_h], Kh and Vh [n_kv][H][d_h] in `dt`,
+ * O [n_q][H][d_h] fp32 (all device).  n_kv = 0 gives O = 0.  This entry
+ * exists to measure and check the attention kernel on its own: in bf16 the
+ * keys and values are laid out as a one-frame bank in `ws` and the readout's
+ * split-KV attention kernel runs on it unchanged (d_h in {32, 64, 128, 256},
+ * H*d_h <= 1024, n_splits*H <= 256, n_splits 0 = automatic); in fp32 a direct
+ * kernel runs (d_h <= 256, no workspace).  n_q <= RS3_MAX_MN, n_kv <= 2^26.
+ * ws: at least rs3_attend_workspace_size() bytes (bf16; may be NULL for fp32). */
+rs3_status rs3_attend_workspace_size(int32_t n_q, int32_t n_kv, int32_t H, int32_t d_h, rs3_dtype dt,
+                                     int32_t n_splits, size_t* bytes);
+rs3_status rs3_attend(const void* Qh, const void* Kh, const void* Vh, int32_t n_q, int32_t n_kv,
+                      int32_t H, int32_t d_h, rs3_dtype dt, int32_t n_splits, float* O, void* ws,
+                      size_t ws_bytes, void* stream);
+
 /* ---- per-kernel timing (diagnostics) ---------------------------------------
  * rs3_profile_enable(1, max_launches) creates a pool of HIP events; while
  * enabled, each kernel launched by the library is bracketed by two events on

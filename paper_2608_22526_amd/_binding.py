@@ -50,6 +50,8 @@ _SIGS = {
     "rs3_bank_destroy": (None, [c_vp]),
     "rs3_bank_export": (c_i32, [c_vp, c_vp, c_vp, c_vp, c_vp, c_vp]),
     "rs3_bank_import": (c_i32, [c_vp, c_vp, c_vp, c_vp, c_vp, c_vp]),
+    "rs3_attend_workspace_size": (c_i32, [c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, ctypes.POINTER(c_sz)]),
+    "rs3_attend": (c_i32, [c_vp, c_vp, c_vp, c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, c_vp, c_vp, c_sz, c_vp]),
     "rs3_bank_error": (c_i32, [c_vp, c_vp, c_i32]),
     "rs3_select_workspace_size": (c_i32, [ctypes.POINTER(Grid), c_i32, c_i64, ctypes.POINTER(c_sz)]),
     "rs3_select_queries": (c_i32, [ctypes.POINTER(Grid), c_i32, c_vp, c_vp, c_vp, c_i64, c_i32, c_i32, c_vp,
@@ -257,6 +259,21 @@ def commit(banks: Sequence[Bank], grid, Kmem, Vmem, kv_obj_stride: int, masks, t
     _check(lib().rs3_commit(ctypes.cast(harr, c_vp), len(banks), ctypes.byref(_grid(grid)), _ptr(Kmem),
                             _ptr(Vmem), kv_obj_stride, _ptr(masks), t, pin, fall_min, fall_max,
                             _ptr(kept_count), _stream(stream)), "rs3_commit")
+
+
+def attend_workspace_size(n_q: int, n_kv: int, H: int, d_h: int, dtype: int, n_splits: int = 0) -> int:
+    out = c_sz()
+    _check(lib().rs3_attend_workspace_size(n_q, n_kv, H, d_h, dtype, n_splits, ctypes.byref(out)),
+           "rs3_attend_workspace_size")
+    return out.value
+
+
+def attend(Q, K, V, n_q: int, n_kv: int, H: int, d_h: int, dtype: int, O, ws=None, n_splits: int = 0,
+           stream=None):
+    """Bare attention core: O [n_q][H*d_h] fp32 from projected Q, K, V."""
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(lib().rs3_attend(_ptr(Q), _ptr(K), _ptr(V), n_q, n_kv, H, d_h, dtype, n_splits, _ptr(O), _ptr(ws),
+                            ws_bytes, _stream(stream)), "rs3_attend")
 
 
 def profile_enable(on: bool, max_launches: int = 65536):

@@ -510,6 +510,112 @@ rs3_status rs3_select_queries(const rs3_grid* g, int32_t n_obj, const uint8_t* m
   return map_err(rs3_launch_select(a, n_groups, st));
 }
 
+// ---- bare attention core ---------------------------------------------------
+namespace {
+struct AttendLayout {
+  size_t desc, hdr, tiles, khat, vhat, qs, opart, ml, total;
+  int ntile, S;
+};
+
+bool attend_shape(int32_t n_q, int32_t n_kv, int32_t H, int32_t d_h, rs3_dtype dt, int32_t n_splits,
+                  AttendLayout* L) {
+  if (n_q < 0 || n_q > RS3_MAX_MN || n_kv < 0 || n_kv > (1 << 26) || H <= 0 || n_splits < 0) return false;
+  if (dt == RS3_BF16) {
+    if (d_h != 32 && d_h != 64 && d_h != 128 && d_h != 256) return false;
+    if (H * d_h > 1024 || n_splits * H > RS3_MAX_SPLITS_X_HEADS) return false;
+  } else if (dt == RS3_F32) {
+    if (d_h <= 0 || d_h > 256) return false;
+  } else {
+    return false;
+  }
+  memset(L, 0, sizeof(*L));
+  if (dt != RS3_BF16) return true;
+  const int D = H * d_h;
+  L->ntile = (n_kv + KT - 1) / KT;
+  const int n_qt = (n_q + 127) / 128;
+  L->S = n_splits > 0 ? n_splits : auto_splits(1, H, n_qt > 0 ? n_qt : 1);
+  size_t off = 0;
+  auto take = [&](size_t bytes) { const size_t at = off; off += align256(bytes); return at; };
+  L->desc = take(sizeof(BankDev));
+  L->hdr = take((HDR_WORDS + 8) * 4);
+  L->tiles = take((size_t)L->ntile * sizeof(TileEnt));
+  L->khat = take((size_t)L->ntile * H * KT * d_h * 2);
+  L->vhat = take((size_t)L->ntile * H * d_h * KT * 2);
+  L->qs = take((size_t)n_q * D * 2);
+  L->opart = take((size_t)L->S * n_q * D * 2);
+  L->ml = take((size_t)L->S * n_q * H * 8);
+  L->total = off;
+  return true;
+}
+}  // namespace
+
+rs3_status rs3_attend_workspace_size(int32_t n_q, int32_t n_kv, int32_t H, int32_t d_h, rs3_dtype dt,
+                                     int32_t n_splits, size_t* bytes) {
+  AttendLayout L;
+  if (!bytes || !attend_shape(n_q, n_kv, H, d_h, dt, n_splits, &L)) return RS3_E_INVALID;
+  *bytes = L.total;
+  return RS3_OK;
+}
+
+rs3_status rs3_attend(const void* Qh, const void* Kh, const void* Vh, int32_t n_q, int32_t n_kv, int32_t H,
+                      int32_t d_h, rs3_dtype dt, int32_t n_splits, float* O, void* ws, size_t ws_bytes,
+                      void* stream) {
+  AttendLayout L;
+  if (!attend_shape(n_q, n_kv, H, d_h, dt, n_splits, &L)) return RS3_E_INVALID;
+  if ((n_q > 0 && (!Qh || !O)) || (n_kv > 0 && (!Kh || !Vh))) return RS3_E_INVALID;
+  if (dt == RS3_BF16 && (!ws || ws_bytes < L.total)) return RS3_E_INVALID;
+  rs3_status st0 = ensure_setup();
+  if (st0 != RS3_OK) return st0;
+  hipStream_t st = (hipStream_t)stream;
+  const float qscale = (float)(1.4426950408889634 / sqrt((double)d_h));
+  if (dt == RS3_F32)
+    return map_err(rs3_launch_attend_f32((const float*)Qh, (const float*)Kh, (const float*)Vh, n_q, n_kv, H, d_h,
+                                         qscale, O, st));
+  if (n_q == 0) return RS3_OK;
+  uint8_t* w = (uint8_t*)ws;
+  AttendPrepArgs p;
+  memset(&p, 0, sizeof(p));
+  p.Q = (const bf16_t*)Qh;
+  p.K = (const bf16_t*)Kh;
+  p.V = (const bf16_t*)Vh;
+  p.Qs = (bf16_t*)(w + L.qs);
+  p.Khat = (bf16_t*)(w + L.khat);
+  p.Vhat = (bf16_t*)(w + L.vhat);
+  p.tiles = (TileEnt*)(w + L.tiles);
+  p.desc = (BankDev*)(w + L.desc);
+  p.hdr = (int32_t*)(w + L.hdr);
+  p.count = p.hdr + HDR_WORDS;
+  p.n_kv = n_kv;
+  p.qscale = qscale;
+  p.n_q = n_q;
+  p.H = H;
+  p.d_h = d_h;
+  p.ntile = L.ntile;
+  hipError_t e = rs3_launch_attend_prep(p, st);
+  if (e != hipSuccess) return map_err(e);
+  Rs3ReadoutArgs a;
+  memset(&a, 0, sizeof(a));
+  a.banks[0] = p.desc;
+  a.sel_count = p.count;
+  a.Q = p.Qs;
+  a.Opart = w + L.opart;
+  a.ML = (float*)(w + L.ml);
+  a.qscale = qscale;
+  a.mn = n_q;
+  a.C = H * d_h;
+  a.H = H;
+  a.d_h = d_h;
+  a.D = H * d_h;
+  a.n_obj = 1;
+  a.max_sel = n_q;
+  a.S = L.S;
+  a.n_qt = (n_q + 127) / 128;
+  e = rs3_launch_attn(a, st);
+  if (e != hipSuccess) return map_err(e);
+  const int SA = L.ntile > 0 ? active_splits(L.ntile, L.S) : 0;
+  return map_err(rs3_launch_attend_merge(a, SA, O, st));
+}
+
 // ---- readout ---------------------------------------------------------------
 static void readout_shape(const rs3_layer* L, int32_t n_obj, int32_t max_sel, int32_t S, size_t* q_bytes,
                           size_t* o_bytes, size_t* ml_bytes) {

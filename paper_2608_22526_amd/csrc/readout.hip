@@ -725,6 +725,19 @@ static size_t combine_lds_bytes(int D, int H, int S) {
          (size_t)NG * items * 8 * 4;
 }
 
+hipError_t rs3_launch_attn(const Rs3ReadoutArgs& a, hipStream_t st) {
+  const int G = a.n_obj * a.H * a.S;
+  const int nblk = 8 * a.n_qt * ((G + 7) / 8);
+  switch (a.d_h) {
+    case 32: RS3_LAUNCH(RS3_K_ATTN, st, k_attn<32>, dim3(nblk), dim3(256), 0, st, a, G); break;
+    case 64: RS3_LAUNCH(RS3_K_ATTN, st, k_attn<64>, dim3(nblk), dim3(256), 0, st, a, G); break;
+    case 128: RS3_LAUNCH(RS3_K_ATTN, st, k_attn<128>, dim3(nblk), dim3(256), 0, st, a, G); break;
+    case 256: RS3_LAUNCH(RS3_K_ATTN, st, k_attn<256>, dim3(nblk), dim3(256), 0, st, a, G); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st) {
   const int64_t cells = (int64_t)a.mn * a.C;
   const bool in_place = a.Y == a.X && !a.y_fp32;
@@ -756,16 +769,7 @@ hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st
   RS3_LAUNCH(RS3_K_QPROJ, st, k_qproj, dim3(a.n_obj, (a.max_sel + 63) / 64, a.D / 64), dim3(256), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int G = a.n_obj * a.H * a.S;
-  const int nblk = 8 * a.n_qt * ((G + 7) / 8);
-  switch (a.d_h) {
-    case 32: RS3_LAUNCH(RS3_K_ATTN, st, k_attn<32>, dim3(nblk), dim3(256), 0, st, a, G); break;
-    case 64: RS3_LAUNCH(RS3_K_ATTN, st, k_attn<64>, dim3(nblk), dim3(256), 0, st, a, G); break;
-    case 128: RS3_LAUNCH(RS3_K_ATTN, st, k_attn<128>, dim3(nblk), dim3(256), 0, st, a, G); break;
-    case 256: RS3_LAUNCH(RS3_K_ATTN, st, k_attn<256>, dim3(nblk), dim3(256), 0, st, a, G); break;
-    default: return hipErrorInvalidValue;
-  }
-  e = hipGetLastError();
+  e = rs3_launch_attn(a, st);
   if (e != hipSuccess) return e;
   const size_t lds = combine_lds_bytes(a.D, a.H, a.S);
   const dim3 cgrid(a.n_obj, (a.max_sel + CB_ROWS - 1) / CB_ROWS);

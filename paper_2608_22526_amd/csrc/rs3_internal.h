@@ -185,6 +185,24 @@ struct Rs3ReadoutArgs {
   int mn, C, H, d_h, D, n_obj, max_sel, S, n_qt, y_fp32;
 };
 
+// Bare attention core: the tensors of rs3_attend laid out as a one-frame
+// bank in the caller's workspace.
+struct AttendPrepArgs {
+  const rs3::bf16_t* Q;        // [n_q][H][d_h]
+  const rs3::bf16_t* K;        // [n_kv][H][d_h]
+  const rs3::bf16_t* V;
+  rs3::bf16_t* Qs;             // [n_q][D], Q * log2(e)/sqrt(d_h)
+  rs3::bf16_t* Khat;           // [ntile][H][64][d_h]
+  rs3::bf16_t* Vhat;           // [ntile][H][d_h][64] (slot order)
+  rs3::TileEnt* tiles;         // [ntile]
+  rs3::BankDev* desc;
+  int32_t* hdr;           // [HDR_WORDS]
+  int32_t* count;         // selected-query count read by the attention
+  int64_t n_kv;
+  float qscale;
+  int n_q, H, d_h, ntile;
+};
+
 // Launchers (all enqueue on `st` and return the launch status).
 hipError_t rs3_launch_energy(const void* X, int64_t x_stride, int n_x, int mn, int C, int dtype,
                              double* e, unsigned long long* range, hipStream_t st);
@@ -192,6 +210,11 @@ hipError_t rs3_launch_select(const Rs3SelectArgs& a, int n_groups, hipStream_t s
 hipError_t rs3_launch_commit(const Rs3CommitArgs& a, int dtype, int d_kv, int D, int H, int d_h,
                              hipStream_t st);
 hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st);
+hipError_t rs3_launch_attn(const Rs3ReadoutArgs& a, hipStream_t st);   // split-KV attention only
+hipError_t rs3_launch_attend_prep(const AttendPrepArgs& p, hipStream_t st);
+hipError_t rs3_launch_attend_merge(const Rs3ReadoutArgs& a, int SA, float* O, hipStream_t st);
+hipError_t rs3_launch_attend_f32(const float* Q, const float* K, const float* V, int n_q, int64_t n_kv, int H,
+                                 int d_h, float qscale, float* O, hipStream_t st);
 // Projects the raw ring rows [hdr PSTART, + PLEN) of bank 0 of `a` into its
 // attention tiles (a.from_ring = 1), or, with rebuild = 1, rebuilds the
 // resident tile list and key count from the frame table.
