@@ -289,6 +289,194 @@ def gpu_run(args):
     return out
 
 
+# ---------------------------------------------------------------------------
+# Report mode: every workload, the 128x128 keep-ratio sweep, the bank-length
+# curve of the long video and the object-count sweep (one JSON file).
+# ---------------------------------------------------------------------------
+def _algo_bytes(cfg, absorb, rec):
+    """Algorithmic bytes per frame of each kernel for one recorded frame:
+    what the step must move (split partials are implementation traffic and
+    are not counted), not what the kernel happens to move."""
+    b = 2 if cfg.dtype == "bf16" else 4
+    Da = cfg.d_kv if absorb else cfg.D
+    n_x = 1 if cfg.shared_x else cfg.n_obj
+    sel, kept, nk = rec["sel"], rec["kept"], rec["n_keys"]
+    mn, C, dkv = cfg.mn, cfg.C, cfg.d_kv
+    return {
+        "energy": n_x * mn * (C * b + 8),
+        "select": cfg.n_obj * mn * cfg.s * cfg.s + 8 * mn * len(set(rec["groups"])) + 4 * sum(sel),
+        "qproj": sum(q * (C * b + Da * 2) for q in sel) + Da * C * 2,
+        "attn": sum(n * Da * 2 * 2 + q * Da * 2 * 2 for q, n in zip(sel, nk)),
+        "combine": sum(q * (Da * 2 + 2 * C * b) for q in sel) + C * Da * 2,
+        "commit_place": cfg.n_obj * mn + 4 * sum(kept),
+        "commit_append": sum(k * (4 * dkv * b + 2 * Da * 2) for k in kept),
+    }
+
+
+def run_workload(cfg, *, absorb, steps, warmup, commit=True, prefill=None, splits=0):
+    """Steady-state frames of `cfg` (objects beyond 64 run as several calls per
+    frame).  Returns frame timing percentiles, per-kernel times and rates."""
+    import numpy as np
+    import torch
+    import paper_2608_22526_amd as rs3
+    from paper_2608_22526_amd.session import Session, to_device
+    from workloads import make_frame, make_sequence, make_weights
+
+    n_pre = cfg.f_max if prefill is None else prefill
+    # distinct resident input frames: fewer when every object has its own grid
+    n_gen = 2 if cfg.n_obj > 64 else n_pre + (8 if cfg.n_obj > 8 else N_DISTINCT)
+    n_dist = n_gen if cfg.n_obj > 64 else n_gen - n_pre
+    seq = make_sequence(cfg, n_frames=n_pre + n_dist)
+    W = make_weights(cfg)
+    chunks = [(o0, min(64, cfg.n_obj - o0)) for o0 in range(0, cfg.n_obj, 64)]
+    max_sel = max(max(ks) for ks in seq.k)
+    sessions = [Session(m=cfg.m, n=cfg.n, s=cfg.s, C=cfg.C, H=cfg.H, d_kv=cfg.d_kv, dtype=cfg.dtype, n_obj=no,
+                        shared_x=cfg.shared_x, union_objects=cfg.union_objects, cap=cfg.cap, f_max=cfg.f_max,
+                        n_pin=cfg.n_pin, weights=W, r_s=cfg.r_s, c=cfg.c, max_sel=max_sel, n_splits=splits,
+                        absorb=absorb) for _, no in chunks]
+    frames = []
+    for t in range(n_gen):
+        fr = make_frame(cfg, t)
+        per = []
+        for (o0, no) in chunks:
+            xs = slice(0, 1) if cfg.shared_x else slice(o0, o0 + no)
+            per.append(dict(X=to_device(fr.X[xs]), K=to_device(fr.Kmem[o0:o0 + no]), V=to_device(fr.Vmem[o0:o0 + no]),
+                            mask=to_device(seq.masks[t][o0:o0 + no]),
+                            rmask=to_device(seq.read_mask(cfg, t)[o0:o0 + no]),
+                            k=seq.k[t] if cfg.union_objects else seq.k[t][o0:o0 + no]))
+        frames.append(dict(per=per, max_sel=max(seq.k[t])))
+    outs = [None if no == 1 else
+            torch.empty((no, cfg.mn, cfg.C), dtype=frames[0]["per"][0]["X"].dtype, device="cuda") for _, no in chunks]
+    def frame_of(t):
+        return t % n_gen if cfg.n_obj > 64 else (t if t < n_pre else n_pre + (t - n_pre) % n_dist)
+
+    for t in range(n_pre):
+        for ci, sess in enumerate(sessions):
+            f = frames[frame_of(t)]["per"][ci]
+            sess.commit(f["K"], f["V"], f["mask"], t, t < cfg.n_pin)
+    step_t = [n_pre]
+
+    def step():
+        t = step_t[0]
+        fi = frame_of(t)
+        for ci, sess in enumerate(sessions):
+            f = frames[fi]["per"][ci]
+            sess.select(f["rmask"], f["X"], f["k"])
+            Y = outs[ci]
+            sess.readout(f["X"], f["X"] if Y is None else Y, max_sel=frames[fi]["max_sel"])
+            if commit:
+                sess.commit(f["K"], f["V"], f["mask"], t, False)
+        if commit:
+            step_t[0] += 1
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    ev[0].record()
+    for i in range(steps):
+        step()
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    per_frame = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]) * 1e3
+    total_ms = ev[0].elapsed_time(ev[steps])
+    rs3.profile_enable(True, 16 * steps * len(sessions) + 64)
+    rs3.profile_reset()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    rep = rs3.profile_report()
+    rs3.profile_enable(False)
+    # frame contents (selected, kept, bank keys) on a few frames
+    recs = []
+    for _ in range(3):
+        step()
+        torch.cuda.synchronize()
+        sel, kept, nks, groups = [], [], [], []
+        for sess in sessions:
+            cnt = sess.sel_count.cpu().numpy()
+            for o in range(sess.n_obj):
+                g = 0 if cfg.union_objects else o
+                sel.append(int(cnt[g]))
+                groups.append((id(sess), g))
+            kept += [int(v) for v in sess.kept_count.cpu().numpy()] if commit else [0] * sess.n_obj
+            nks += [b.info()["n_keys"] for b in sess.banks]
+        recs.append(dict(sel=sel, kept=kept, n_keys=nks, groups=groups))
+    Da = cfg.d_kv if absorb else cfg.D
+    fps = 1000.0 * steps / total_ms
+    kern = {}
+    byt = [_algo_bytes(cfg, absorb, r) for r in recs]
+    for name, (ms, n) in rep.items():
+        if not n:
+            continue
+        launches_per_frame = n / steps
+        avg_us = 1000.0 * ms / n
+        d = {"avg_us": avg_us, "launches_per_frame": launches_per_frame}
+        if name in byt[0]:
+            bytes_frame = sum(b_[name] for b_ in byt) / len(byt)
+            d["algo_bytes_per_frame"] = bytes_frame
+            d["GB_s"] = bytes_frame / launches_per_frame / (avg_us * 1e-6) / 1e9
+            d["frac_hbm"] = d["GB_s"] / PEAK_HBM_GBS
+        kern[name] = d
+    attn_flops = sum(4.0 * q * n * Da for r in recs for q, n in zip(r["sel"], r["n_keys"])) / len(recs)
+    if "attn" in kern:
+        a = kern["attn"]
+        a["flops_per_frame"] = attn_flops
+        a["TFLOP_s"] = attn_flops / a["launches_per_frame"] / (a["avg_us"] * 1e-6) / 1e12
+        a["frac_mfma"] = a["TFLOP_s"] / PEAK_BF16_TFLOPS
+    q_frame = sum(sum(r["sel"]) for r in recs) / len(recs)
+    k_frame = sum(sum(r["kept"]) for r in recs) / len(recs)
+    return {
+        "frames_per_s": fps, "ms_per_frame": total_ms / steps,
+        "frame_us_p10_p50_p90": [float(np.percentile(per_frame, q)) for q in (10, 50, 90)],
+        "query_tokens_per_s": q_frame * fps, "committed_tokens_per_s": k_frame * fps,
+        "grid_tokens_per_s": cfg.n_obj * cfg.mn * fps,
+        "selected_per_frame": q_frame, "kept_per_frame": k_frame,
+        "bank_keys_mean": sum(sum(r["n_keys"]) for r in recs) / len(recs) / cfg.n_obj,
+        "kernels": kern, "attention_width": Da, "objects": cfg.n_obj, "calls_per_frame": len(sessions),
+    }
+
+
+def report(args):
+    from dataclasses import replace
+    from workloads import CONFIGS
+    out = {"device": "one MI355X", "steps": args.steps}
+
+    def log(tag, r):
+        print("%-34s %9.0f frames/s  p50 %7.1f us  attn %s" % (
+            tag, r["frames_per_s"], r["frame_us_p10_p50_p90"][1],
+            ("%.1f us %.1f TF/s" % (r["kernels"]["attn"]["avg_us"], r["kernels"]["attn"]["TFLOP_s"]))
+            if "attn" in r["kernels"] else "-"), flush=True)
+
+    for name in ("tiny_f32", "sam2_single", "multi_obj8", "long_video", "highres"):
+        cfg = CONFIGS[name]
+        for mode in (("absorbed", "projected") if cfg.H == 1 and cfg.dtype == "bf16" else ("projected",)):
+            r = run_workload(cfg, absorb=mode == "absorbed", steps=args.steps, warmup=args.warmup)
+            out["%s/%s" % (name, mode)] = r
+            log("%s/%s" % (name, mode), r)
+    hr = CONFIGS["highres"]
+    for rho in ("0.1", "0.25", "0.5", "1.0"):
+        cfg = replace(hr, rho=float(rho))
+        r = run_workload(cfg, absorb=False, steps=max(5, args.steps // 4), warmup=3)
+        out["highres_rho/%s" % rho] = r
+        log("highres rho=%s" % rho, r)
+    lv = CONFIGS["long_video"]
+    for L in (1, 2, 4, 8, 16, 32, 64):
+        for mode in ("absorbed", "projected"):
+            r = run_workload(lv, absorb=mode == "absorbed", steps=max(5, args.steps // 4), warmup=3, commit=False,
+                             prefill=L)
+            out["long_video_bank/%d/%s" % (L, mode)] = r
+            log("long_video L=%d %s" % (L, mode), r)
+    base = CONFIGS["multi_obj8"]
+    for B in (1, 8, 64, 512):
+        cfg = replace(base, n_obj=B, shared_x=False, union_objects=False)
+        r = run_workload(cfg, absorb=True, steps=max(3, args.steps // 8), warmup=2)
+        out["objects/%d" % B] = r
+        log("objects B=%d (per-object grids)" % B, r)
+    with open(args.report, "w") as fh:
+        json.dump(out, fh, indent=1)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -303,6 +491,7 @@ def main():
     ap.add_argument("--copy-probe-mb", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-child", action="store_true")
+    ap.add_argument("--report", default="", help="write the full measurement report (JSON) to this path")
     args = ap.parse_args()
     if args.cpu_child:
         cpu_child(args.workload, args.cpu_frames)
@@ -313,6 +502,9 @@ def main():
               "sharded across GPUs with no exchange, which this benchmark does not launch). Use --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
+    if args.report:
+        report(args)
+        return
     out = gpu_run(args)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_frames)

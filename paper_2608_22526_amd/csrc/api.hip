@@ -69,13 +69,26 @@ std::vector<uint8_t> transpose(const void* src, int rows, int cols, size_t es) {
   return out;
 }
 
-// Key splits per query tile: enough attention workgroups to cover the 256
-// CUs once (each workgroup holds 128 KB of LDS, so one fits per CU).
-int auto_splits(int n_obj, int H, int n_qt) {
+// Key splits per query tile.  Enough attention workgroups to cover the 256
+// CUs once, and key ranges whose K^/V^ tiles (kv_bytes per object and head)
+// fit an XCD's 4 MB L2 in slices of at most L2_SPLIT_BYTES: the query tiles
+// of one key range run on one XCD and then share its cached tiles instead of
+// each streaming the whole range from the memory side.
+constexpr double L2_SPLIT_BYTES = 2.0 * 1024 * 1024;
+
+int max_auto_splits(int H) {
+  int S = 64;
+  if (S * H > RS3_MAX_SPLITS_X_HEADS) S = RS3_MAX_SPLITS_X_HEADS / H;
+  return S < 1 ? 1 : S;
+}
+
+int auto_splits(int n_obj, int H, int n_qt, double kv_bytes) {
   const int base = n_obj * H * n_qt;
   int S = (256 + base - 1) / base;
-  if (S > 64) S = 64;
-  if (S * H > RS3_MAX_SPLITS_X_HEADS) S = RS3_MAX_SPLITS_X_HEADS / H;
+  const double s_l2 = kv_bytes / L2_SPLIT_BYTES;
+  if (s_l2 > S) S = s_l2 > 4096.0 ? 4096 : (int)s_l2 + 1;
+  const int cap = max_auto_splits(H);
+  if (S > cap) S = cap;
   if (S < 1) S = 1;
   return S;
 }
@@ -533,7 +546,7 @@ bool attend_shape(int32_t n_q, int32_t n_kv, int32_t H, int32_t d_h, rs3_dtype d
   const int D = H * d_h;
   L->ntile = (n_kv + KT - 1) / KT;
   const int n_qt = (n_q + 127) / 128;
-  L->S = n_splits > 0 ? n_splits : auto_splits(1, H, n_qt > 0 ? n_qt : 1);
+  L->S = n_splits > 0 ? n_splits : auto_splits(1, H, n_qt > 0 ? n_qt : 1, (double)n_kv * d_h * 4);
   size_t off = 0;
   auto take = [&](size_t bytes) { const size_t at = off; off += align256(bytes); return at; };
   L->desc = take(sizeof(BankDev));
@@ -625,10 +638,13 @@ static void readout_shape(const rs3_layer* L, int32_t n_obj, int32_t max_sel, in
   *ml_bytes = align256((size_t)n_obj * S * max_sel * ld.Ha * 8);
 }
 
-static int splits_for(const rs3_layer* L, int32_t n_obj, int32_t max_sel, int32_t n_splits) {
+// kv_bytes < 0: the largest automatic choice (workspace sizing, where the
+// banks are not known).
+static int splits_for(const rs3_layer* L, int32_t n_obj, int32_t max_sel, int32_t n_splits, double kv_bytes) {
   if (n_splits > 0) return n_splits;
+  if (kv_bytes < 0) return max_auto_splits(L->dev.Ha);
   const int n_qt = (max_sel + 127) / 128;
-  return auto_splits(n_obj, L->dev.Ha, n_qt > 0 ? n_qt : 1);
+  return auto_splits(n_obj, L->dev.Ha, n_qt > 0 ? n_qt : 1, kv_bytes);
 }
 
 rs3_status rs3_readout_workspace_size(const rs3_layer* L, int32_t n_obj, int32_t max_sel, int32_t n_splits,
@@ -648,7 +664,7 @@ rs3_status rs3_readout_workspace_size(const rs3_layer* L, int32_t n_obj, int32_t
   for (int qt = 0; qt <= n_qt_max; ++qt) {
     const int ms = qt == n_qt_max ? max_sel : qt * 128;
     if (ms > max_sel) continue;
-    const int S = splits_for(L, n_obj, ms, n_splits);
+    const int S = splits_for(L, n_obj, ms, n_splits, -1.0);
     size_t q, o, ml;
     readout_shape(L, n_obj, ms, S, &q, &o, &ml);
     if (q + o + ml > best) best = q + o + ml;
@@ -682,7 +698,13 @@ rs3_status rs3_readout(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, con
     if (n_obj > 1 && x_obj_stride != y_obj_stride) return RS3_E_INVALID;
   }
   if (ld.dtype == RS3_F32) y_fp32 = 0;
-  const int S = splits_for(L, n_obj, max_sel, n_splits);
+  // K^/V^ bytes of the largest bank's full ring, per head
+  double kv_bytes = 0;
+  for (int o = 0; o < n_obj; ++o) {
+    const double kb = (double)banks[o]->host.cap * ld.dah * 4;
+    if (kb > kv_bytes) kv_bytes = kb;
+  }
+  const int S = splits_for(L, n_obj, max_sel, n_splits, kv_bytes);
   size_t q, o_b, ml;
   readout_shape(L, n_obj, max_sel, S, &q, &o_b, &ml);
   if (ld.dtype == RS3_BF16 && (!ws || ws_bytes < q + o_b + ml)) return RS3_E_INVALID;
