@@ -3,7 +3,7 @@
 // k_commit_place  : one 1024-thread workgroup per object.  Compacts the mask
 //                   to the ascending kept list (ordered block scan), applies
 //                   the dense fall-through, places the frame in the ring
-//                   (single lane; the rule is documented in rs3.h), writes
+//                   (one wave; the rule is documented in rs3.h), writes
 //                   the kept cell of every new row to `pos`, and rebuilds the
 //                   list of resident 64-row tiles with their row masks.
 // k_commit_append : 64 kept rows per workgroup.  Copies the raw K/V rows into
@@ -49,58 +49,6 @@ __device__ int cp_block_excl_scan(int v, CpShared& sh, int* total) {
   return wsum + inc - v;
 }
 
-// Removes frame `idx` from the key-ordered frame table.
-__device__ void erase_frame(int32_t* fr, int& nf, int idx) {
-  for (int f = idx; f + 1 < nf; ++f)
-    for (int w = 0; w < 4; ++w) fr[4 * f + w] = fr[4 * (f + 1) + w];
-  --nf;
-}
-
-// Returns false when no unpinned frame is resident.
-__device__ bool evict_oldest_unpinned(int32_t* fr, int& nf) {
-  for (int f = 0; f < nf; ++f)
-    if (!fr[4 * f + 3]) {
-      erase_frame(fr, nf, f);
-      return true;
-    }
-  return false;
-}
-
-// Ring placement of a frame of L rows (single lane) on the LDS copy `fr` of
-// the frame table.  Returns the start row, or -1 on a capacity error (table
-// unchanged).
-__device__ int place_frame(const BankDev& b, int32_t* fr, int& nf, int& pin_end, int L, int t,
-                           int pin) {
-  int start;
-  if (pin) {
-    if ((int64_t)pin_end + L > b.cap || nf >= b.f_max) return -1;
-    start = pin_end;
-    pin_end += L;
-  } else {
-    if (L > b.cap - pin_end) return -1;
-    while (nf >= b.f_max)
-      if (!evict_oldest_unpinned(fr, nf)) return -1;  // unreachable while n_pin < f_max
-    start = (nf > 0 && !fr[4 * (nf - 1) + 3]) ? fr[4 * (nf - 1)] + fr[4 * (nf - 1) + 1] : pin_end;
-    if ((int64_t)start + L > b.cap) start = pin_end;
-    for (;;) {
-      bool hit = false;
-      if (L > 0)
-        for (int f = 0; f < nf && !hit; ++f) {
-          int fs = fr[4 * f], fl = fr[4 * f + 1];
-          hit = !fr[4 * f + 3] && fl > 0 && fs < start + L && start < fs + fl;
-        }
-      if (!hit) break;
-      if (!evict_oldest_unpinned(fr, nf)) return -1;  // unreachable: a hit is unpinned
-    }
-  }
-  fr[4 * nf + 0] = start;
-  fr[4 * nf + 1] = L;
-  fr[4 * nf + 2] = t;
-  fr[4 * nf + 3] = pin ? 1 : 0;
-  ++nf;
-  return start;
-}
-
 __device__ __forceinline__ uint64_t tile_mask(const int32_t* fr, int nf, int tile) {
   const int64_t t0 = (int64_t)tile * KT, t1 = t0 + KT;
   uint64_t msk = 0;
@@ -144,14 +92,141 @@ __device__ __forceinline__ int cp_scan_bits(uint32_t bits, int n, int* red, int*
   return before + pre;
 }
 
+// Ring placement by one wave (lane l holds frames 4l .. 4l+3 of the
+// key-ordered table, f_max <= 256): the count and overlap evictions of the
+// placement rule both remove a prefix of the unpinned frames, found with
+// ballots; survivors move to their new slots in one scatter.  Returns the
+// start row or -1 (capacity; table unchanged), the new frame count, pin end
+// and resident key count.
+__device__ __forceinline__ int place_frame_wave(const BankDev& b, int32_t* fr, int nf, int pin_end, int L, int t, int pin,
+                                int* nf_out, int* pin_end_out, int* keys_out) {
+  const int lane = threadIdx.x & 63;
+  int fs[4], fl[4], fw[4], fp[4];
+  bool fv[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int f = 4 * lane + k;
+    fv[k] = f < nf;
+    fs[k] = fv[k] ? fr[4 * f] : 0;
+    fl[k] = fv[k] ? fr[4 * f + 1] : 0;
+    fw[k] = fv[k] ? fr[4 * f + 2] : 0;
+    fp[k] = fv[k] ? fr[4 * f + 3] : 0;
+  }
+  int n_pf = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) n_pf += __popcll(__ballot(fv[k] && fp[k]));
+  int start, E = 0;
+  if (pin) {
+    if ((int64_t)pin_end + L > b.cap || nf >= b.f_max) return -1;
+    start = pin_end;
+  } else {
+    if (L > b.cap - pin_end) return -1;
+    const int e1 = nf >= b.f_max ? nf - (b.f_max - 1) : 0;   // make room for one frame
+    if (e1 > nf - n_pf) return -1;   // unreachable while n_pin < f_max
+    start = (nf - 1 >= n_pf + e1) ? fr[4 * (nf - 1)] + fr[4 * (nf - 1) + 1] : pin_end;
+    if ((int64_t)start + L > b.cap) start = pin_end;
+    // newest remaining unpinned frame that overlaps [start, start+L)
+    int imax = -1;
+    if (L > 0) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int f = 4 * lane + k;
+        const bool hit = fv[k] && !fp[k] && f >= n_pf + e1 && fl[k] > 0 && fs[k] < start + L &&
+                         start < fs[k] + fl[k];
+        const unsigned long long bm = __ballot(hit);
+        if (bm) imax = max(imax, 4 * (63 - (int)__builtin_clzll(bm)) + k);
+      }
+    }
+    E = max(e1, imax >= 0 ? imax - n_pf + 1 : 0);
+  }
+  // survivors: pinned frames stay, unpinned frames past the evicted prefix
+  // move down by E; the new frame goes last
+  int keys = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int f = 4 * lane + k;
+    if (!fv[k] || (!fp[k] && f < n_pf + E)) continue;
+    keys += fl[k];
+    const int d = fp[k] ? f : f - E;
+    if (d != f) {
+      fr[4 * d] = fs[k];
+      fr[4 * d + 1] = fl[k];
+      fr[4 * d + 2] = fw[k];
+      fr[4 * d + 3] = fp[k];
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) keys += __shfl_xor(keys, off, 64);
+  const int slot = nf - E;
+  if (lane == 0) {
+    fr[4 * slot] = start;
+    fr[4 * slot + 1] = L;
+    fr[4 * slot + 2] = t;
+    fr[4 * slot + 3] = pin ? 1 : 0;
+  }
+  *nf_out = slot + 1;
+  *pin_end_out = pin ? pin_end + L : pin_end;
+  *keys_out = keys + L;
+  return start;
+}
+
+// Tiles per thread whose masks the rebuild keeps in registers (bank rings of
+// up to 8*1024 tiles, 512K rows).
+constexpr int TILES_REG = 8;
+
 // Rebuilds the resident tile list (ascending tiles with their row masks)
 // and hdr NTILES from the LDS frame table; every thread of the workgroup.
-__device__ void rebuild_tiles(const BankDev& b, const int32_t* sfr, int nf, CpShared& sh) {
+__device__ __forceinline__ void rebuild_tiles(const BankDev& b, const int32_t* sfr, int nf, CpShared& sh) {
   const int tid = threadIdx.x;
   const int nt = b.n_tiles_cap;
   const int tpt = (nt + CP_THREADS - 1) / CP_THREADS;
   const int t0 = tid * tpt;
   int ntot = 0, pos = 0;
+  if (tpt <= TILES_REG) {
+    // one pass over the frames: OR each frame's rows into the masks of this
+    // thread's tiles (frame entries are read by every thread at once)
+    uint64_t msk[TILES_REG];
+#pragma unroll
+    for (int j = 0; j < TILES_REG; ++j) msk[j] = 0ull;
+    // rows stay below 2^26, so 32-bit row arithmetic cannot overflow
+    const int r_lo = t0 * KT, r_hi = (t0 + tpt) * KT;
+    for (int f0 = 0; f0 < nf; f0 += 4) {
+      int4 fe4[4];   // four frame entries per LDS read burst
+#pragma unroll
+      for (int u = 0; u < 4; ++u) fe4[u] = *(const int4*)&sfr[4 * (f0 + u < nf ? f0 + u : f0)];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int fs = fe4[u].x, fe = fs + fe4[u].y;
+        const int a = fs > r_lo ? fs : r_lo, e = fe < r_hi ? fe : r_hi;
+        if (f0 + u >= nf || a >= e) continue;
+#pragma unroll
+        for (int j = 0; j < TILES_REG; ++j) {
+          const int ta = (t0 + j) * KT, te = ta + KT;
+          const int x = a > ta ? a : ta, y = e < te ? e : te;
+          if (j < tpt && x < y) {
+            const int lo = x - ta, n = y - x;
+            msk[j] |= (n == 64 ? ~0ull : ((1ull << n) - 1ull)) << lo;
+          }
+        }
+      }
+    }
+    uint32_t live = 0;
+#pragma unroll
+    for (int j = 0; j < TILES_REG; ++j)
+      if (j < tpt && t0 + j < nt && msk[j]) live |= 1u << j;
+    pos = cp_scan_bits(live, tpt, sh.red2, &ntot);
+#pragma unroll
+    for (int j = 0; j < TILES_REG; ++j)
+      if (live >> j & 1) {
+        TileEnt te;
+        te.tile = t0 + j;
+        te.pad = 0;
+        te.mask = msk[j];
+        b.tiles[pos++] = te;
+      }
+    if (tid == 0) b.hdr[HDR_NTILES] = ntot;
+    return;
+  }
   if (tpt <= 32) {
     uint32_t live = 0;
     for (int j = 0; j < tpt; ++j)
@@ -180,7 +255,7 @@ __device__ void rebuild_tiles(const BankDev& b, const int32_t* sfr, int nf, CpSh
 // grid n_obj, block 1024, dynamic LDS f_max*16 bytes.  Thread t owns the
 // cpt contiguous cells c0 = t*cpt ...; all cross-thread traffic is in LDS.
 __global__ __launch_bounds__(CP_THREADS) void k_commit_place(Rs3CommitArgs a) {
-  extern __shared__ int32_t sfr[];
+  extern __shared__ __attribute__((aligned(16))) int32_t sfr[];
   __shared__ CpShared sh;
   const int o = blockIdx.x, tid = threadIdx.x;
   const BankDev& b = *a.banks[o];
@@ -192,7 +267,7 @@ __global__ __launch_bounds__(CP_THREADS) void k_commit_place(Rs3CommitArgs a) {
   const int f_max = b.f_max;
   const int32_t fr_w = tid < 4 * f_max ? b.frames[tid] : 0;
   int nf0 = 0, pin_end0 = 0;
-  if (tid == 0) {
+  if (tid < 64) {
     nf0 = b.hdr[HDR_NFRAMES];
     pin_end0 = b.hdr[HDR_PINEND];
   }
@@ -223,24 +298,24 @@ __global__ __launch_bounds__(CP_THREADS) void k_commit_place(Rs3CommitArgs a) {
   }
   if (tid < 4 * f_max) sfr[tid] = fr_w;
   cp_lds_barrier();
-  if (tid == 0) {
-    if (a.kept_count) a.kept_count[o] = total;
-    int nf = nf0, pin_end = pin_end0;
-    int start = place_frame(b, sfr, nf, pin_end, total, a.t, a.pin);
-    sh.ok = start >= 0;
-    sh.start = start;
-    sh.len = nf;
-    if (start >= 0) {
-      b.hdr[HDR_NFRAMES] = nf;
-      b.hdr[HDR_PINEND] = pin_end;
-      b.hdr[HDR_PSTART] = start;
-      b.hdr[HDR_PLEN] = total;
-      int keys = 0;
-      for (int f = 0; f < nf; ++f) keys += sfr[4 * f + 1];
-      b.hdr[HDR_NKEYS] = keys;
-    } else {
-      b.hdr[HDR_PLEN] = -1;
-      set_err(b.hdr, RS3_E_CAPACITY);
+  if (tid < 64) {
+    int nf = nf0, pin_end = pin_end0, keys = 0;
+    const int start = place_frame_wave(b, sfr, nf0, pin_end0, total, a.t, a.pin, &nf, &pin_end, &keys);
+    if (tid == 0) {
+      if (a.kept_count) a.kept_count[o] = total;
+      sh.ok = start >= 0;
+      sh.start = start;
+      sh.len = nf;
+      if (start >= 0) {
+        b.hdr[HDR_NFRAMES] = nf;
+        b.hdr[HDR_PINEND] = pin_end;
+        b.hdr[HDR_PSTART] = start;
+        b.hdr[HDR_PLEN] = total;
+        b.hdr[HDR_NKEYS] = keys;
+      } else {
+        b.hdr[HDR_PLEN] = -1;
+        set_err(b.hdr, RS3_E_CAPACITY);
+      }
     }
   }
   cp_lds_barrier();
@@ -257,7 +332,7 @@ __global__ __launch_bounds__(CP_THREADS) void k_commit_place(Rs3CommitArgs a) {
 // Bank restore: frame table from device memory, then the tile list and the
 // key count (grid 1, block CP_THREADS, dynamic LDS f_max*16 bytes).
 __global__ __launch_bounds__(CP_THREADS) void k_bank_tiles(Rs3CommitArgs a) {
-  extern __shared__ int32_t sfr[];
+  extern __shared__ __attribute__((aligned(16))) int32_t sfr[];
   __shared__ CpShared sh;
   const int tid = threadIdx.x;
   const BankDev& b = *a.banks[0];
@@ -385,9 +460,15 @@ __global__ __launch_bounds__(256) void k_commit_append_bf16(Rs3CommitArgs a) {
   }
 }
 
-// append: fp32, 256 threads, 64 rows per workgroup, FMA loops.
+// append: fp32, 256 threads, 64 rows per workgroup.  For d_kv <= 64 the
+// kept rows are staged in LDS and each thread owns one output column d with
+// its W_k / W_v rows in registers (row operands are LDS broadcasts);
+// otherwise plain FMA loops.
+constexpr int F32_STAGE_KV = 64;
+
 __global__ __launch_bounds__(256) void k_commit_append_f32(Rs3CommitArgs a) {
-  const int o = blockIdx.x;
+  __shared__ __attribute__((aligned(16))) float sK[64 * (F32_STAGE_KV + 4)], sV[64 * (F32_STAGE_KV + 4)];
+  const int o = blockIdx.x, tid = threadIdx.x;
   BankDev& b = *a.banks[o];
   const int L = b.hdr[HDR_PLEN];
   const int r0 = blockIdx.y * 64;
@@ -395,28 +476,81 @@ __global__ __launch_bounds__(256) void k_commit_append_f32(Rs3CommitArgs a) {
   const int start = b.hdr[HDR_PSTART];
   const int rows = min(64, L - r0);
   const int d_kv = b.d_kv, d_h = b.d_h, H = b.H, D = H * d_h;
+  const bool stage = d_kv <= F32_STAGE_KV;
+  constexpr int SP = F32_STAGE_KV + 4;   // row pitch: 16-byte aligned rows
   const float* Km = (const float*)a.Kmem + (int64_t)o * a.kv_stride;
   const float* Vm = (const float*)a.Vmem + (int64_t)o * a.kv_stride;
   float* Kr = (float*)b.Kraw;
   float* Vr = (float*)b.Vraw;
-  if (!a.from_ring) {
-    for (int q = threadIdx.x; q < rows * d_kv; q += 256) {
-      int r = q / d_kv, c = q - r * d_kv;
-      int j = start + r0 + r;
-      int src = b.pos[j];
-      Kr[(int64_t)j * d_kv + c] = Km[(int64_t)src * d_kv + c];
-      Vr[(int64_t)j * d_kv + c] = Vm[(int64_t)src * d_kv + c];
+  for (int q = tid; q < rows * d_kv; q += 256) {
+    const int r = q / d_kv, c = q - r * d_kv;
+    const int64_t j = start + r0 + r;
+    float kv, vv;
+    if (a.from_ring) {
+      kv = Kr[j * d_kv + c];
+      vv = Vr[j * d_kv + c];
+    } else {
+      const int src = b.pos[j];
+      kv = Km[(int64_t)src * d_kv + c];
+      vv = Vm[(int64_t)src * d_kv + c];
+      Kr[j * d_kv + c] = kv;
+      Vr[j * d_kv + c] = vv;
+    }
+    if (stage) {
+      sK[r * SP + c] = kv;
+      sV[r * SP + c] = vv;
     }
   }
+  __syncthreads();
   const float* WkT = (const float*)a.WkT;
   const float* WvT = (const float*)a.WvT;
   float* Kh = (float*)b.Khat;
   float* Vh = (float*)b.Vhat;
-  for (int q = threadIdx.x; q < rows * D; q += 256) {
-    int r = q / D, d = q - r * D;
-    int j = start + r0 + r;
-    const float* kr = a.from_ring ? Kr + (int64_t)j * d_kv : Km + (int64_t)b.pos[j] * d_kv;
-    const float* vr = a.from_ring ? Vr + (int64_t)j * d_kv : Vm + (int64_t)b.pos[j] * d_kv;
+  if (stage) {
+    const int ngrp = D >= 256 ? 1 : 256 / D;
+    for (int dq = tid; dq < D * ngrp; dq += 256) {
+      const int d = dq % D, grp = dq / D;
+      const int h = d / d_h, dd = d - h * d_h;
+      float wk[F32_STAGE_KV], wv[F32_STAGE_KV];
+      if (!a.absorb) {
+#pragma unroll
+        for (int c = 0; c < F32_STAGE_KV; ++c) {
+          wk[c] = c < d_kv ? WkT[(int64_t)d * d_kv + c] : 0.f;
+          wv[c] = c < d_kv ? WvT[(int64_t)d * d_kv + c] : 0.f;
+        }
+      }
+      for (int r = grp; r < rows; r += ngrp) {
+        float sk, sv;
+        if (a.absorb) {   // attention on the raw rows
+          sk = sK[r * SP + d];
+          sv = sV[r * SP + d];
+        } else {
+          sk = 0.f;
+          sv = 0.f;
+#pragma unroll
+          for (int c4 = 0; c4 < F32_STAGE_KV / 4; ++c4)
+            if (4 * c4 < d_kv) {   // d_kv is a multiple of 16
+              const f32x4 k4 = *(const f32x4*)&sK[r * SP + 4 * c4];
+              const f32x4 v4 = *(const f32x4*)&sV[r * SP + 4 * c4];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                sk = fmaf(k4[e], wk[4 * c4 + e], sk);
+                sv = fmaf(v4[e], wv[4 * c4 + e], sv);
+              }
+            }
+        }
+        const int j = start + r0 + r, tile = j >> 6, kk = j & 63;
+        Kh[(((int64_t)tile * H + h) * KT + kk) * d_h + dd] = sk;
+        Vh[(((int64_t)tile * H + h) * d_h + dd) * KT + vslot(kk)] = sv;
+      }
+    }
+    return;
+  }
+  for (int q = tid; q < rows * D; q += 256) {
+    const int r = q / D, d = q - r * D;
+    const int j = start + r0 + r;
+    const float* kr = Kr + (int64_t)j * d_kv;
+    const float* vr = Vr + (int64_t)j * d_kv;
     float sk, sv;
     if (a.absorb) {  // attention on the raw rows
       sk = kr[d];
@@ -431,7 +565,7 @@ __global__ __launch_bounds__(256) void k_commit_append_f32(Rs3CommitArgs a) {
         sv = fmaf(vr[c], wv[c], sv);
       }
     }
-    int tile = j >> 6, kk = j & 63, h = d / d_h, dd = d - h * d_h;
+    const int tile = j >> 6, kk = j & 63, h = d / d_h, dd = d - h * d_h;
     Kh[(((int64_t)tile * H + h) * KT + kk) * d_h + dd] = sk;
     Vh[(((int64_t)tile * H + h) * d_h + dd) * KT + vslot(kk)] = sv;
   }
