@@ -251,6 +251,7 @@ def gpu_run(args):
     ms_total = ev0.elapsed_time(ev1)
     ms_step = ms_total / args.steps
     fps = 1000.0 / ms_step
+    graph = _graph_pass(torch, step, args.steps) if not two and args.graph else None
     # pass B: per-kernel durations from HIP events around each launch
     rs3.profile_enable(True, 16 * args.steps + 64)
     rs3.profile_reset()
@@ -313,9 +314,36 @@ def gpu_run(args):
             "bank_errors": errs,
             "splits": sess.n_splits,
             "host_enqueue_us_per_step": host_us,
+            "hip_graph": graph,
         },
     }
     return out
+
+
+def _graph_pass(torch, step, steps):
+    """Frames/s with the frame sequence replayed from one captured HIP graph
+    (the N_DISTINCT resident input frames, one graph launch each pass): the
+    same kernels with the per-launch host work removed."""
+    g = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        for _ in range(N_DISTINCT):
+            step()
+    torch.cuda.synchronize()
+    for _ in range(2):
+        g.replay()
+    torch.cuda.synchronize()
+    reps = max(1, -(-steps // N_DISTINCT))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / (reps * N_DISTINCT)
+    del g
+    return {"frames_per_s": 1000.0 / ms, "ms_per_step": ms, "frames_timed": reps * N_DISTINCT,
+            "frames_per_graph": N_DISTINCT}
 
 
 # ---------------------------------------------------------------------------
@@ -526,6 +554,8 @@ def main():
     ap.add_argument("--layer", choices=["auto", "projected", "absorbed"], default="auto")
     ap.add_argument("--streams", type=int, choices=[1, 2], default=1,
                     help="2: frame t's commit overlaps frame t+1's selection on a second stream")
+    ap.add_argument("--no-graph", dest="graph", action="store_false",
+                    help="skip the HIP-graph replay pass (reported beside the eager frames/s)")
     ap.add_argument("--cpu-frames", type=int, default=40)
     ap.add_argument("--copy-probe-mb", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
