@@ -269,6 +269,11 @@ def gpu_run(args):
     flops = sum(4.0 * r["sel"][o] * r["n_keys"][o] * Da for r in recs for o in range(cfg.n_obj))
     flops_projected = sum(4.0 * r["sel"][o] * r["n_keys"][o] * cfg.D for r in recs for o in range(cfg.n_obj))
     sel_tot = sum(sum(r["sel"]) for r in recs)
+    # launches without a separate projection kernel project their queries
+    # inside the attention: 2 * selected * d_model * width more work
+    fused_share = 1.0 - (rep.get("qproj", (0.0, 0))[1] / attn_n if attn_n else 0.0)
+    proj_flops = fused_share * sum(2.0 * r["sel"][o] * cfg.C * Da for r in recs for o in range(cfg.n_obj))
+    flops += proj_flops
     per_launch_flops = flops / max(attn_n, 1)
     avg_attn_s = attn_ms / 1000.0 / max(attn_n, 1)
     achieved_tflops = per_launch_flops / avg_attn_s / 1e12 if attn_n else 0.0
@@ -301,7 +306,9 @@ def gpu_run(args):
                      "traffic": traffic,
                      "kernel": "k_attn (split-KV attention)",
                      "flops_per_launch": per_launch_flops,
-                     "flops_basis": "executed: 4 * selected queries * bank keys * attention width (%d)" % Da,
+                     "flops_basis": ("executed: 4 * selected queries * bank keys * attention width (%d)"
+                                     " + 2 * selected * d_model * width for the query projection done inside"
+                                     " the kernel (%.0f%% of launches)") % (Da, 100.0 * fused_share),
                      "projected_equivalent_flops_per_launch": flops_projected / max(attn_n, 1),
                      "avg_launch_us": avg_attn_s * 1e6},
         "extra": {

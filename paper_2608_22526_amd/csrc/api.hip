@@ -69,11 +69,12 @@ std::vector<uint8_t> transpose(const void* src, int rows, int cols, size_t es) {
   return out;
 }
 
-// Key splits per query tile.  Enough attention workgroups to cover the 256
-// CUs once, and key ranges whose K^/V^ tiles (kv_bytes per object and head)
-// fit an XCD's 4 MB L2 in slices of at most L2_SPLIT_BYTES: the query tiles
-// of one key range run on one XCD and then share its cached tiles instead of
-// each streaming the whole range from the memory side.
+// Key splits per query tile.  The most splits whose attention launch
+// (8*n_qt*ceil(n_obj*H*S/8) work-groups) still fits the 256 CUs once, and
+// key ranges whose K^/V^ tiles (kv_bytes per object and head) fit an XCD's
+// 4 MB L2 in slices of at most L2_SPLIT_BYTES: the query tiles of one key
+// range run on one XCD and then share its cached tiles instead of each
+// streaming the whole range from the memory side.
 constexpr double L2_SPLIT_BYTES = 2.0 * 1024 * 1024;
 
 int max_auto_splits(int H) {
@@ -83,8 +84,8 @@ int max_auto_splits(int H) {
 }
 
 int auto_splits(int n_obj, int H, int n_qt, double kv_bytes) {
-  const int base = n_obj * H * n_qt;
-  int S = (256 + base - 1) / base;
+  const int groups = n_qt <= 32 ? 8 * (32 / n_qt) : 0;   // key groups that fit one launch wave
+  int S = groups / (n_obj * H);
   const double s_l2 = kv_bytes / L2_SPLIT_BYTES;
   if (s_l2 > S) S = s_l2 > 4096.0 ? 4096 : (int)s_l2 + 1;
   const int cap = max_auto_splits(H);
@@ -623,7 +624,7 @@ rs3_status rs3_attend(const void* Qh, const void* Kh, const void* Vh, int32_t n_
   a.max_sel = n_q;
   a.S = L.S;
   a.n_qt = (n_q + 127) / 128;
-  e = rs3_launch_attn(a, st);
+  e = rs3_launch_attn(a, st, false);
   if (e != hipSuccess) return map_err(e);
   const int SA = L.ntile > 0 ? active_splits(L.ntile, L.S) : 0;
   return map_err(rs3_launch_attend_merge(a, SA, O, st));

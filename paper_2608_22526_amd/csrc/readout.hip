@@ -16,13 +16,32 @@
 //              W_o (MFMA), adds the residual and scatters y into Y[sel].
 // fp32 path: one workgroup per selected row (FMA loops), for the small
 // fp32 workloads that need 1e-4 agreement.
+#include <algorithm>
+
 #include "rs3_internal.h"
 
 namespace rs3 {
 
+// Loads through global (not generic) pointers: the compiler then counts
+// them on the vector memory counter alone, and a wait for one of them does
+// not have to drain every outstanding load.
+#define RS3_GLOBAL __attribute__((address_space(1)))
+template <class T>
+__device__ __forceinline__ T gload(const T* p) {
+  return *(const RS3_GLOBAL T*)p;
+}
+
+// Keeps a loaded value alive on a path that does not use it, so the load is
+// issued before the branch rather than sunk past it (an early exit would
+// otherwise delay every load that only the main path uses).
+template <class T>
+__device__ __forceinline__ void keep(const T& v) {
+  asm volatile("" ::"v"(v));
+}
+
 __device__ __forceinline__ int sel_count_of(const Rs3ReadoutArgs& a, int o, BankDev& b,
                                             bool report) {
-  int cnt = a.sel_count[a.sel_stride ? o : 0];
+  int cnt = gload(a.sel_count + (a.sel_stride ? o : 0));
   if (cnt > a.max_sel || cnt < 0) {
     if (report) set_err(b.hdr, RS3_E_INVALID);
     cnt = cnt < 0 ? 0 : a.max_sel;
@@ -41,8 +60,7 @@ __device__ __forceinline__ bool sel_ok(const int32_t* sel, int r, int mn) {
 __global__ __launch_bounds__(256) void k_qproj(Rs3ReadoutArgs a) {
   const int o = blockIdx.x, r0 = blockIdx.y * 64, c0 = blockIdx.z * 64;
   BankDev& b = *a.banks[o];
-  const bool report = blockIdx.z == 0 && threadIdx.x == 0;
-  const int cnt = sel_count_of(a, o, b, report && blockIdx.y == 0);
+  const int cnt = sel_count_of(a, o, b, false);   // reported by the merge kernel
   if (r0 >= cnt) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, g = lane >> 5;
   const int32_t* sel = a.sel_idx + (int64_t)o * a.sel_stride;
@@ -50,9 +68,6 @@ __global__ __launch_bounds__(256) void k_qproj(Rs3ReadoutArgs a) {
   const bf16_t* X = (const bf16_t*)a.X + (int64_t)o * a.x_stride;
   const int row = r0 + 32 * (wave & 1) + (lane & 31);
   const bool rv = row < cnt;
-  if (blockIdx.z == 0 && threadIdx.x < 64 && r0 + threadIdx.x < cnt &&
-      !sel_ok(sel, r0 + threadIdx.x, a.mn))
-    set_err(b.hdr, RS3_E_INVALID);
   int src = rv ? sel[row] : 0;
   if (src < 0 || src >= a.mn) src = 0;
   const bf16_t* xr = X + (int64_t)src * C;
@@ -83,7 +98,8 @@ __global__ __launch_bounds__(256) void k_qproj(Rs3ReadoutArgs a) {
 
 // ---------------------------------------------------------------------------
 // The attention streams the object's resident keys in 32-key half tiles
-// through NST LDS stages (NST-1 half tiles in flight).  One stage holds
+// through nst LDS stages (nst-1 half tiles in flight; nst = 4 or 8, chosen
+// at launch with the dynamic LDS size).  One stage holds
 //   K : 32 rows (keys) x DH bf16, row pitch DH*2 + 16 bytes
 //   V : DH rows x 32 keys (slot order), row pitch 64 + 16 bytes
 // The pitch is an odd number of 16-byte chunks, so the 16 rows read by one
@@ -94,7 +110,6 @@ __global__ __launch_bounds__(256) void k_qproj(Rs3ReadoutArgs a) {
 // issues the same number of loads per stage, so the waits are immediates.
 template <int DH>
 struct AttnLds {
-  static constexpr int NST = 4;
   static constexpr int CPR = DH / 8;                          // data chunks per K row
   static constexpr int KP = (CPR + 1) * 16;                   // K row pitch, bytes
   static constexpr int VP = 5 * 16;                           // V row pitch, bytes
@@ -132,6 +147,12 @@ __device__ __forceinline__ AttnDmaOffsets<DH> attn_dma_offsets(int wave, int lan
   return d;
 }
 
+// One direct-to-LDS load: 16 bytes per lane from g into the wave's 1 KB at
+// lds_wave (lane l lands at lds_wave + 16 l).
+__device__ __forceinline__ void dma16(const void* g, void* lds_wave) {
+  __builtin_amdgcn_global_load_lds(g, lds_wave, 16, 0, 0);
+}
+
 // Direct-to-LDS loads of half tile `half` of bank tile `tile`, head h, into
 // a stage.  `tile`, `half` and `wave` are wave-uniform (scalar registers).
 template <int DH>
@@ -141,11 +162,9 @@ __device__ __forceinline__ void attn_issue(const bf16_t* Kh, const bf16_t* Vh, i
   const bf16_t* kg = Kh + ((int64_t)tile * H + h) * (KT * DH) + half * 32 * DH;
   const bf16_t* vg = Vh + ((int64_t)tile * H + h) * (DH * KT) + half * 32;
 #pragma unroll
-  for (int j = 0; j < L::NK / 4; ++j)
-    __builtin_amdgcn_global_load_lds(kg + off.k[j], stage + (4 * j + wave) * 1024, 16, 0, 0);
+  for (int j = 0; j < L::NK / 4; ++j) dma16(kg + off.k[j], stage + (4 * j + wave) * 1024);
 #pragma unroll
-  for (int j = 0; j < L::NV / 4; ++j)
-    __builtin_amdgcn_global_load_lds(vg + off.v[j], stage + L::KREG + (4 * j + wave) * 1024, 16, 0, 0);
+  for (int j = 0; j < L::NV / 4; ++j) dma16(vg + off.v[j], stage + L::KREG + (4 * j + wave) * 1024);
 }
 
 __device__ __forceinline__ const void* uniform_ptr(const void* p) {
@@ -178,6 +197,122 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
+// Waits until at most `later` stages of PW loads each are still in flight
+// (`later` is wave-uniform and at most MAXL).
+template <int PW, int MAXL>
+__device__ __forceinline__ void wait_stages(int later) {
+  if constexpr (MAXL >= 6) if (later >= 6) { wait_vmcnt<6 * PW>(); return; }
+  if constexpr (MAXL >= 5) if (later == 5) { wait_vmcnt<5 * PW>(); return; }
+  if constexpr (MAXL >= 4) if (later == 4) { wait_vmcnt<4 * PW>(); return; }
+  if constexpr (MAXL >= 3) if (later == 3) { wait_vmcnt<3 * PW>(); return; }
+  if constexpr (MAXL >= 2) if (later == 2) { wait_vmcnt<2 * PW>(); return; }
+  if (later == 1) {
+    wait_vmcnt<PW>();
+    return;
+  }
+  wait_vmcnt<0>();
+}
+
+// Query projection inside the attention (heads of width DH <= 64, d_model
+// C = 8*PC with PC = 32): Q~^T block dt (32 d x 32 queries) = rows
+// h*DH + 32*dt .. of W_q^T (A operand) times the wave's 32 gathered rows of
+// X (B operand), fp32 accumulation over C in 16-deep steps, as the separate
+// projection kernel does.  Both operands are staged in LDS with coalesced
+// 16-byte loads (the W_q rows of a head are one contiguous block; each X row
+// is 32 consecutive chunks), in the stage buffers, which are free until the
+// first key/value DMA.  Row pitch PC*16 + 16 bytes: conflict-free reads of
+// 32 rows x 16 bytes.
+constexpr int PJ_PC = 32;                          // 16-byte chunks per row (C = 256)
+constexpr int PJ_PITCH = PJ_PC * 16 + 16;          // bytes
+constexpr int PJ_XCH = 128 * PJ_PC / 256;          // X chunks per thread (16)
+template <int DH>
+struct AttnProj {
+  static constexpr int WCH = DH * PJ_PC / 256;     // W chunks per thread
+  static constexpr int XS = 0;                     // X rows [128][PITCH]
+  static constexpr int WS = 128 * PJ_PITCH;        // W rows [DH][PITCH]
+  static constexpr int BYTES = WS + DH * PJ_PITCH;
+};
+
+// Loads of the projection's operands: W chunks need only the arguments,
+// X chunks the gathered row indices (rows past the selected count read any
+// valid row; their results are discarded).
+template <int DH>
+__device__ __forceinline__ void attn_proj_load_w(const bf16_t* WqT, int h, int tid, u32x4 (&wv)[AttnProj<DH>::WCH]) {
+  const u32x4* wb = (const u32x4*)(WqT + (int64_t)h * DH * PJ_PC * 8);
+#pragma unroll
+  for (int j = 0; j < AttnProj<DH>::WCH; ++j) wv[j] = gload(wb + tid + 256 * j);
+}
+
+__device__ __forceinline__ void attn_proj_rows(const int32_t* sel, int row0, int max_sel, int tid,
+                                               int (&src)[PJ_XCH]) {
+#pragma unroll
+  for (int i = 0; i < PJ_XCH; ++i) src[i] = gload(sel + min(row0 + (tid >> 5) + 8 * i, max_sel - 1));
+}
+
+__device__ __forceinline__ void attn_proj_load_x(const bf16_t* X, int mn, int tid, const int (&src)[PJ_XCH],
+                                                 u32x4 (&xv)[PJ_XCH]) {
+#pragma unroll
+  for (int i = 0; i < PJ_XCH; ++i) {
+    const int r = (src[i] < 0 || src[i] >= mn) ? 0 : src[i];
+    xv[i] = gload((const u32x4*)(X + (int64_t)r * PJ_PC * 8) + (tid & 31));
+  }
+}
+
+template <int DH>
+__device__ __forceinline__ void attn_project(uint8_t* lds, int tid, int wave, int lane, float qs,
+                                             const u32x4 (&wv)[AttnProj<DH>::WCH], const u32x4 (&xv)[PJ_XCH],
+                                             u32x4* qreg) {
+  using P = AttnProj<DH>;
+  const int g = lane >> 5;
+#pragma unroll
+  for (int j = 0; j < P::WCH; ++j) {
+    const int q = tid + 256 * j;
+    *(u32x4*)(lds + P::WS + (q / PJ_PC) * PJ_PITCH + (q % PJ_PC) * 16) = wv[j];
+  }
+#pragma unroll
+  for (int i = 0; i < PJ_XCH; ++i)
+    *(u32x4*)(lds + P::XS + ((tid >> 5) + 8 * i) * PJ_PITCH + (tid & 31) * 16) = xv[i];
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  f32x16 qa[DH / 32];
+#pragma unroll
+  for (int dt = 0; dt < DH / 32; ++dt) qa[dt] = f32x16{};
+  const uint8_t* xb = lds + P::XS + (32 * wave + (lane & 31)) * PJ_PITCH + 16 * g;
+  const uint8_t* wb = lds + P::WS + (lane & 31) * PJ_PITCH + 16 * g;
+#pragma unroll
+  for (int k0 = 0; k0 < PJ_PC / 2; k0 += 4) {
+    u32x4 bx[4], aw[4][DH / 32];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      bx[j] = *(const u32x4*)(xb + (k0 + j) * 32);
+#pragma unroll
+      for (int dt = 0; dt < DH / 32; ++dt) aw[j][dt] = *(const u32x4*)(wb + dt * 32 * PJ_PITCH + (k0 + j) * 32);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int dt = 0; dt < DH / 32; ++dt) qa[dt] = mfma32(aw[j][dt], bx[j], qa[dt]);
+  }
+  // Lane l holds query l%32 at d = 8*(r/4) + 4*(l/32) + r%4 of each block;
+  // the B operand of the logits needs d = 16*ks + 8*(l/32) + 0..7.  One
+  // v_permlane32_swap per register pair moves the quads into place: the low
+  // half keeps its quad of r%8 < 4 and takes the high half's, the high half
+  // takes the low half's quad of r%8 >= 4 and keeps its own.
+#pragma unroll
+  for (int dt = 0; dt < DH / 32; ++dt)
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      const f32x16& v = qa[dt];
+      const int r = 8 * hf;
+      const uint32_t p0 = pack_bf16x2(v[r] * qs, v[r + 1] * qs), p1 = pack_bf16x2(v[r + 2] * qs, v[r + 3] * qs);
+      const uint32_t q0 = pack_bf16x2(v[r + 4] * qs, v[r + 5] * qs), q1 = pack_bf16x2(v[r + 6] * qs, v[r + 7] * qs);
+      const auto s0 = __builtin_amdgcn_permlane32_swap(p0, q0, false, false);
+      const auto s1 = __builtin_amdgcn_permlane32_swap(p1, q1, false, false);
+      qreg[2 * dt + hf] = u32x4{s0[0], s1[0], s0[1], s1[1]};
+    }
+  // every wave is done with the staged operands before the DMA reuses them
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 constexpr float RESCALE_LOG2 = 8.0f;
 
 // S^T (32 keys x 32 queries) of one half tile: K rows from LDS (kp points at
@@ -207,33 +342,93 @@ __device__ __forceinline__ f32x16 attn_scores(const uint8_t* kp, const u32x4* qr
 // grid 8*n_qt*ceil(G/8) with G = n_obj*H*S key groups, block 256 (4 waves x
 // 32 queries).  Block b -> key group 8*((b>>3)/n_qt) + (b&7), query tile
 // (b>>3) % n_qt, so all query tiles of one key group share an XCD (and its L2).
-template <int DH>
-__global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
+// PROJ: the queries are projected here from X[sel] and W_q (heads of width
+// <= 64); otherwise they are read from the projected buffer Q.
+template <int DH, bool PROJ>
+__global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G, int nst) {
   using L = AttnLds<DH>;
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[L::NST * L::STAGE];
+  constexpr int MAX_NST = 8;
+  extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];   // nst * L::STAGE bytes
   const int bid = blockIdx.x;
   const int rest = bid >> 3;
   const int qt = rest % a.n_qt;
   const int kvg = (rest / a.n_qt) * 8 + (bid & 7);
   if (kvg >= G) return;
   const int s = kvg % a.S, oh = kvg / a.S, h = oh % a.H, o = oh / a.H;
-  BankDev& b = *a.banks[o];
-  const int cnt = sel_count_of(a, o, b, false);
-  const int row0 = qt * 128;
-  if (row0 >= cnt) return;
-  const int ntiles = __builtin_amdgcn_readfirstlane(b.hdr[HDR_NTILES]);
-  const int tps = split_tiles(ntiles, a.S);
-  const int tb = min(s * tps, ntiles), te = min(tb + tps, ntiles);
-  if (tb >= te) return;
-  const int ub = 2 * tb, ue = 2 * te;   // half tiles
-
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int row0 = qt * 128;
+  const int qrow = row0 + 32 * wave + (lane & 31);
+  // Loads that need nothing but the arguments are issued before the chain
+  // descriptor -> header -> tile list: the query operands (rows past the
+  // selected count are clamped into the buffers and zeroed below), or for
+  // PROJ the W_q chunks and the gathered row indices.
+  const int qrow_c = min(qrow, a.max_sel - 1);
+  u32x4 qreg[DH / 16];
+  int src[PROJ ? PJ_XCH : 1];
+  u32x4 wv[PROJ ? AttnProj<DH>::WCH : 1];
+  if constexpr (PROJ) {
+    attn_proj_load_w<DH>((const bf16_t*)a.WqT, h, tid, wv);
+    attn_proj_rows(a.sel_idx + (int64_t)o * a.sel_stride, row0, a.max_sel, tid, src);
+  } else {
+    const bf16_t* Qp = (const bf16_t*)a.Q + ((int64_t)o * a.max_sel + qrow_c) * a.D + h * DH;
+#pragma unroll
+    for (int ks = 0; ks < DH / 16; ++ks) qreg[ks] = gload((const u32x4*)(Qp + 16 * ks + 8 * g));
+  }
+  // the bank descriptor's pointers (one cache line), issued with them
+  const BankDev* bd = a.banks[o];
+  const uint64_t p_hdr = gload((const uint64_t*)&bd->hdr);
+  const uint64_t p_tiles = gload((const uint64_t*)&bd->tiles);
+  const uint64_t p_kh = gload((const uint64_t*)&bd->Khat);
+  const uint64_t p_vh = gload((const uint64_t*)&bd->Vhat);
+  // the exits below keep every value loaded so far, so that the compiler
+  // issues those loads before the exit tests instead of after them
+  auto keep_loads = [&]() {
+    keep(p_hdr);
+    keep(p_tiles);
+    keep(p_kh);
+    keep(p_vh);
+    if constexpr (PROJ) {
+#pragma unroll
+      for (int i = 0; i < PJ_XCH; ++i) keep(src[i]);
+#pragma unroll
+      for (int j = 0; j < AttnProj<DH>::WCH; ++j) keep(wv[j]);
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < DH / 16; ++ks) keep(qreg[ks]);
+    }
+  };
+  BankDev& b = *a.banks[o];
+  const int cnt = sel_count_of(a, o, b, false);
+  if (row0 >= cnt) {
+    keep_loads();
+    return;
+  }
+  const int32_t* hdr = (const int32_t*)uniform_ptr((const void*)p_hdr);
+  u32x4 xv[PROJ ? PJ_XCH : 1];
+  if constexpr (PROJ) {
+    // the gathered X rows, in flight while the tile list arrives (invalid
+    // list entries read row 0; the merge kernel skips their rows)
+    attn_proj_load_x((const bf16_t*)a.X + (int64_t)o * a.x_stride, a.mn, tid, src, xv);
+  }
+  const int ntiles = __builtin_amdgcn_readfirstlane(gload(hdr + HDR_NTILES));
+  const int tps = split_tiles(ntiles, a.S);
+  const int tb = min(s * tps, ntiles), te = min(tb + tps, ntiles);
+  if (tb >= te) {
+    keep_loads();
+    if constexpr (PROJ) {
+#pragma unroll
+      for (int i = 0; i < PJ_XCH; ++i) keep(xv[i]);
+    }
+    return;
+  }
+  const int ub = 2 * tb, ue = 2 * te;   // half tiles
+
   // values loaded from the bank descriptor are wave-uniform: keep them in
   // scalar registers so that load addresses are base (SGPR) + lane offset
-  const bf16_t* Kh = (const bf16_t*)uniform_ptr(b.Khat);
-  const bf16_t* Vh = (const bf16_t*)uniform_ptr(b.Vhat);
-  const TileEnt* tiles = (const TileEnt*)uniform_ptr(b.tiles);
+  const bf16_t* Kh = (const bf16_t*)uniform_ptr((const void*)p_kh);
+  const bf16_t* Vh = (const bf16_t*)uniform_ptr((const void*)p_vh);
+  const TileEnt* tiles = (const TileEnt*)uniform_ptr((const void*)p_tiles);
   const int H = a.H;
   const AttnDmaOffsets<DH> doff = attn_dma_offsets<DH>(wave, lane);
 
@@ -250,29 +445,25 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
   int cbase = tb, c_tile = 0;
   uint32_t c_mlo = 0, c_mhi = 0;
   if (tb + lane < te) {
-    const TileEnt e = tiles[tb + lane];
-    c_tile = e.tile;
-    c_mlo = (uint32_t)e.mask;
-    c_mhi = (uint32_t)(e.mask >> 32);
+    c_tile = gload(&tiles[tb + lane].tile);
+    const uint64_t m = gload(&tiles[tb + lane].mask);
+    c_mlo = (uint32_t)m;
+    c_mhi = (uint32_t)(m >> 32);
   }
-  // query operands
-  const int qrow = row0 + 32 * wave + (lane & 31);
   const bool qv = qrow < cnt;
-  const bf16_t* Qp = (const bf16_t*)a.Q + ((int64_t)o * a.max_sel + (qv ? qrow : 0)) * a.D + h * DH;
-  u32x4 qreg[DH / 16];
-#pragma unroll
-  for (int ks = 0; ks < DH / 16; ++ks)
-    qreg[ks] = qv ? *(const u32x4*)(Qp + 16 * ks + 8 * g) : u32x4{0, 0, 0, 0};
-  wait_vmcnt<0>();
+  if constexpr (PROJ) attn_project<DH>(lds, tid, wave, lane, a.qscale, wv, xv, qreg);
   // i-th visited half tile
   auto half_at = [&](int i) { int v = i + rot; return ub + (v >= nh ? v - nh : v); };
 #pragma unroll
-  for (int j = 0; j < L::NST - 1; ++j)
-    if (j < nh) {
+  for (int j = 0; j < MAX_NST - 1; ++j)
+    if (j < nst - 1 && j < nh) {
       const int v = half_at(j);
-      attn_issue<DH>(Kh, Vh, __builtin_amdgcn_readlane(c_tile, (v >> 1) - cbase), v & 1, h, H,
-                     lds + j * L::STAGE, wave, doff);
+      const int tl = __builtin_amdgcn_readlane(c_tile, (v >> 1) - cbase);
+      attn_issue<DH>(Kh, Vh, tl, v & 1, h, H, lds + j * L::STAGE, wave, doff);
     }
+#pragma unroll
+  for (int ks = 0; ks < DH / 16; ++ks)
+    if (!qv) qreg[ks] = u32x4{0, 0, 0, 0};
 
   f32x16 acc[DH / 32];
 #pragma unroll
@@ -280,46 +471,37 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
   float m_run = -INFINITY, l_run = 0.f;
   const int kbase = (lane & 31) * L::KP + 16 * g;             // + ks*32
   const int vbase = L::KREG + (lane & 31) * L::VP + 16 * g;   // + dt*32*VP + q*32
-  // stage 0 must land before its scores: later stages issued = min(2, nh-1)
-  if (nh >= 3)
-    wait_vmcnt<2 * L::PER_WAVE>();
-  else if (nh == 2)
-    wait_vmcnt<L::PER_WAVE>();
-  else
-    wait_vmcnt<0>();
+  // stage 0 must land before its scores: later stages issued = min(nst-2, nh-1)
+  wait_stages<L::PER_WAVE, MAX_NST - 2>(min(nst - 2, nh - 1));
   stage_barrier();
 
   // Software pipeline over the visited half tiles i = 0 .. nh-1 (stage i%NST):
   //   iteration i: wait until stage i+1 landed; barrier (stage i-1 free);
-  //   prefetch i+3 into it; S^T(i+1) on the MFMA pipe while the VALU does
-  //   the softmax of i; then O^T += V^T(i) P(i).
+  //   prefetch i+nst-1 into it; S^T(i+1) on the MFMA pipe while the VALU
+  //   does the softmax of i; then O^T += V^T(i) P(i).
+  const int smask = nst - 1;
   f32x16 sc = attn_scores<DH>(lds + kbase, qreg);
   for (int i = 0; i < nh; ++i) {
-    const int st = i & (L::NST - 1);
+    const int st = i & smask;
     const int u = half_at(i);
-    if (i + 1 < nh) {
-      if (i + 2 < nh)
-        wait_vmcnt<L::PER_WAVE>();
-      else
-        wait_vmcnt<0>();
-    }
+    if (i + 1 < nh) wait_stages<L::PER_WAVE, MAX_NST - 2>(min(i + nst - 2, nh - 1) - (i + 1));
     stage_barrier();
-    if (i + L::NST - 1 < nh) {
-      const int v = half_at(i + L::NST - 1);
+    if (i + nst - 1 < nh) {
+      const int v = half_at(i + nst - 1);
       if ((v >> 1) - cbase >= 64) {
         // (unrotated splits longer than the window) slide it to the tile
         // being computed
         wait_vmcnt<0>();
         cbase = u >> 1;
         c_tile = 0;
-        if (cbase + lane < te) c_tile = tiles[cbase + lane].tile;
-        const uint64_t mm = cbase + lane < te ? tiles[cbase + lane].mask : 0ull;
+        if (cbase + lane < te) c_tile = gload(&tiles[cbase + lane].tile);
+        const uint64_t mm = cbase + lane < te ? gload(&tiles[cbase + lane].mask) : 0ull;
         c_mlo = (uint32_t)mm;
         c_mhi = (uint32_t)(mm >> 32);
         wait_vmcnt<0>();
       }
-      attn_issue<DH>(Kh, Vh, __builtin_amdgcn_readlane(c_tile, (v >> 1) - cbase), v & 1, h, H,
-                     lds + ((st + L::NST - 1) & (L::NST - 1)) * L::STAGE, wave, doff);
+      const int tl = __builtin_amdgcn_readlane(c_tile, (v >> 1) - cbase);
+      attn_issue<DH>(Kh, Vh, tl, v & 1, h, H, lds + ((st + nst - 1) & smask) * L::STAGE, wave, doff);
     }
     const uint8_t* Sb = lds + st * L::STAGE;
     const int tu = (u >> 1) - cbase;
@@ -327,7 +509,7 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
 
     // S^T of the next half tile (independent of the softmax below).  In the
     // last iteration the stage holds an earlier tile and the result is unused.
-    const f32x16 sc_next = attn_scores<DH>(lds + ((st + 1) & (L::NST - 1)) * L::STAGE + kbase, qreg);
+    const f32x16 sc_next = attn_scores<DH>(lds + ((st + 1) & smask) * L::STAGE + kbase, qreg);
 
     if (msk != 0u) {
       if (msk != 0xffffffffu) {  // partial half tile (frame boundary)
@@ -439,15 +621,18 @@ __global__ __launch_bounds__(CB_THREADS) void k_combine(Rs3ReadoutArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t cl[];
   const int o = blockIdx.x, r0 = blockIdx.y * CB_ROWS;
   BankDev& b = *a.banks[o];
-  const int cnt = sel_count_of(a, o, b, false);
-  if (r0 >= cnt) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5;
+  // the merge covers every selected row: it reports a count past max_sel and
+  // invalid (out of range or not ascending) list entries, whose rows it skips
+  const int cnt = sel_count_of(a, o, b, blockIdx.y == 0 && tid == 0);
+  if (r0 >= cnt) return;
   const int D = a.D, C = a.C, H = a.H, d_h = a.d_h, S = a.S, OS = D + 8;
   bf16_t* Os = (bf16_t*)cl;
   float* wts = (float*)(cl + ((CB_ROWS * OS * 2 + 15) & ~15));
   const int ntiles = b.hdr[HDR_NTILES];
   const int SA = ntiles > 0 ? active_splits(ntiles, S) : 0;
   const int32_t* sel = a.sel_idx + (int64_t)o * a.sel_stride;
+  if (tid < CB_ROWS && r0 + tid < cnt && !sel_ok(sel, r0 + tid, a.mn)) set_err(b.hdr, RS3_E_INVALID);
   const int64_t base = (int64_t)o * S * a.max_sel;
   const bf16_t* X = (const bf16_t*)a.X + (int64_t)o * a.x_stride;
   const bf16_t* WoT = (const bf16_t*)a.WoT;
@@ -725,17 +910,40 @@ static size_t combine_lds_bytes(int D, int H, int S) {
          (size_t)NG * items * 8 * 4;
 }
 
-hipError_t rs3_launch_attn(const Rs3ReadoutArgs& a, hipStream_t st) {
+// Launches of at most one work-group per CU keep 7 half tiles in flight
+// where 8 stages fit the LDS (heads of width <= 64); larger launches keep 3,
+// so that several work-groups share a CU.
+constexpr int ATTN_DEEP_MAX_BLOCKS = 256;
+
+template <int DH, bool PROJ>
+static hipError_t launch_attn_dh(const Rs3ReadoutArgs& a, int G, int nblk, hipStream_t st) {
+  const int nst = (DH <= 64 && nblk <= ATTN_DEEP_MAX_BLOCKS) ? 8 : 4;
+  size_t lds = (size_t)nst * AttnLds<DH>::STAGE;
+  if constexpr (PROJ) lds = lds > (size_t)AttnProj<DH>::BYTES ? lds : (size_t)AttnProj<DH>::BYTES;
+  RS3_LAUNCH(RS3_K_ATTN, st, (k_attn<DH, PROJ>), dim3(nblk), dim3(256), lds, st, a, G, nst);
+  return hipGetLastError();
+}
+
+// Launches of at most one work-group per CU with heads of width <= 64 at
+// d_model 256 project their queries inside the attention (the staged
+// operands would cost larger launches their occupancy).
+static bool attn_projects(const Rs3ReadoutArgs& a) {
   const int G = a.n_obj * a.H * a.S;
   const int nblk = 8 * a.n_qt * ((G + 7) / 8);
+  return a.d_h <= 64 && a.C == 8 * PJ_PC && nblk <= ATTN_DEEP_MAX_BLOCKS;
+}
+
+hipError_t rs3_launch_attn(const Rs3ReadoutArgs& a, hipStream_t st, bool project) {
+  const int G = a.n_obj * a.H * a.S;
+  const int nblk = 8 * a.n_qt * ((G + 7) / 8);
+  if (project && !attn_projects(a)) return hipErrorInvalidValue;
   switch (a.d_h) {
-    case 32: RS3_LAUNCH(RS3_K_ATTN, st, k_attn<32>, dim3(nblk), dim3(256), 0, st, a, G); break;
-    case 64: RS3_LAUNCH(RS3_K_ATTN, st, k_attn<64>, dim3(nblk), dim3(256), 0, st, a, G); break;
-    case 128: RS3_LAUNCH(RS3_K_ATTN, st, k_attn<128>, dim3(nblk), dim3(256), 0, st, a, G); break;
-    case 256: RS3_LAUNCH(RS3_K_ATTN, st, k_attn<256>, dim3(nblk), dim3(256), 0, st, a, G); break;
+    case 32: return project ? launch_attn_dh<32, true>(a, G, nblk, st) : launch_attn_dh<32, false>(a, G, nblk, st);
+    case 64: return project ? launch_attn_dh<64, true>(a, G, nblk, st) : launch_attn_dh<64, false>(a, G, nblk, st);
+    case 128: return launch_attn_dh<128, false>(a, G, nblk, st);
+    case 256: return launch_attn_dh<256, false>(a, G, nblk, st);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st) {
@@ -766,10 +974,13 @@ hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st
     RS3_LAUNCH(RS3_K_READOUT_F32, st, k_readout_f32, dim3(a.n_obj, a.max_sel), dim3(256), lds, st, a);
     return hipGetLastError();
   }
-  RS3_LAUNCH(RS3_K_QPROJ, st, k_qproj, dim3(a.n_obj, (a.max_sel + 63) / 64, a.D / 64), dim3(256), 0, st, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  e = rs3_launch_attn(a, st);
+  const bool project = attn_projects(a);
+  if (!project) {
+    RS3_LAUNCH(RS3_K_QPROJ, st, k_qproj, dim3(a.n_obj, (a.max_sel + 63) / 64, a.D / 64), dim3(256), 0, st, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipError_t e = rs3_launch_attn(a, st, project);
   if (e != hipSuccess) return e;
   const size_t lds = combine_lds_bytes(a.D, a.H, a.S);
   const dim3 cgrid(a.n_obj, (a.max_sel + CB_ROWS - 1) / CB_ROWS);
@@ -791,5 +1002,19 @@ hipError_t rs3_readout_setup() {
   hipError_t e = hipFuncSetAttribute((const void*)k_combine<bf16_t>, hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)max_lds);
   if (e != hipSuccess) return e;
+  // the attention's stages: 8 for heads of width <= 64, else 4
+  const struct {
+    const void* f;
+    int bytes;
+  } attn[] = {{(const void*)k_attn<32, false>, 8 * AttnLds<32>::STAGE},
+              {(const void*)k_attn<32, true>, std::max(8 * AttnLds<32>::STAGE, AttnProj<32>::BYTES)},
+              {(const void*)k_attn<64, false>, 8 * AttnLds<64>::STAGE},
+              {(const void*)k_attn<64, true>, std::max(8 * AttnLds<64>::STAGE, AttnProj<64>::BYTES)},
+              {(const void*)k_attn<128, false>, 4 * AttnLds<128>::STAGE},
+              {(const void*)k_attn<256, false>, 4 * AttnLds<256>::STAGE}};
+  for (const auto& k : attn) {
+    e = hipFuncSetAttribute(k.f, hipFuncAttributeMaxDynamicSharedMemorySize, k.bytes);
+    if (e != hipSuccess) return e;
+  }
   return hipFuncSetAttribute((const void*)k_combine<float>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)max_lds);
 }

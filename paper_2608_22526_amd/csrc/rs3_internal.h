@@ -210,7 +210,9 @@ hipError_t rs3_launch_select(const Rs3SelectArgs& a, int n_groups, hipStream_t s
 hipError_t rs3_launch_commit(const Rs3CommitArgs& a, int dtype, int d_kv, int D, int H, int d_h,
                              hipStream_t st);
 hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st);
-hipError_t rs3_launch_attn(const Rs3ReadoutArgs& a, hipStream_t st);   // split-KV attention only
+// Split-KV attention only; project: the queries are projected from X[sel]
+// inside the kernel (heads of width <= 64), else read from a.Q.
+hipError_t rs3_launch_attn(const Rs3ReadoutArgs& a, hipStream_t st, bool project);
 hipError_t rs3_launch_attend_prep(const AttendPrepArgs& p, hipStream_t st);
 hipError_t rs3_launch_attend_merge(const Rs3ReadoutArgs& a, int SA, float* O, hipStream_t st);
 hipError_t rs3_launch_attend_f32(const float* Q, const float* K, const float* V, int n_q, int64_t n_kv, int H,
