@@ -64,9 +64,6 @@ __device__ __forceinline__ uint64_t tile_mask(const int32_t* fr, int nf, int til
   return msk;
 }
 
-// Workgroup barrier for LDS traffic only (does not wait for this wave's
-// outstanding global loads).
-__device__ __forceinline__ void cp_lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // Exclusive prefix (thread order) of the set bits among the first n bits of
 // `bits`, and the workgroup total, from ballots; `red` is an LDS array of
@@ -80,7 +77,7 @@ __device__ __forceinline__ int cp_scan_bits(uint32_t bits, int n, int* red, int*
     wtot += __popcll(b);
   }
   if (lane == 0) red[wave] = wtot;
-  cp_lds_barrier();
+  lds_barrier();
   int before = 0, tot = 0;
 #pragma unroll
   for (int w = 0; w < CP_WAVES; ++w) {
@@ -297,7 +294,7 @@ __global__ __launch_bounds__(CP_THREADS) void k_commit_place(Rs3CommitArgs a) {
     total = mn;
   }
   if (tid < 4 * f_max) sfr[tid] = fr_w;
-  cp_lds_barrier();
+  lds_barrier();
   if (tid < 64) {
     int nf = nf0, pin_end = pin_end0, keys = 0;
     const int start = place_frame_wave(b, sfr, nf0, pin_end0, total, a.t, a.pin, &nf, &pin_end, &keys);
@@ -318,7 +315,7 @@ __global__ __launch_bounds__(CP_THREADS) void k_commit_place(Rs3CommitArgs a) {
       }
     }
   }
-  cp_lds_barrier();
+  lds_barrier();
   if (!sh.ok) return;
   const int start = sh.start;
   const int nf = sh.len;

@@ -272,7 +272,7 @@ __device__ __forceinline__ void attn_project(uint8_t* lds, int tid, int wave, in
 #pragma unroll
   for (int i = 0; i < PJ_XCH; ++i)
     *(u32x4*)(lds + P::XS + ((tid >> 5) + 8 * i) * PJ_PITCH + (tid & 31) * 16) = xv[i];
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  lds_barrier();
   f32x16 qa[DH / 32];
 #pragma unroll
   for (int dt = 0; dt < DH / 32; ++dt) qa[dt] = f32x16{};
@@ -310,7 +310,7 @@ __device__ __forceinline__ void attn_project(uint8_t* lds, int tid, int wave, in
       qreg[2 * dt + hf] = u32x4{s0[0], s1[0], s0[1], s1[1]};
     }
   // every wave is done with the staged operands before the DMA reuses them
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  lds_barrier();
 }
 
 constexpr float RESCALE_LOG2 = 8.0f;
@@ -419,6 +419,13 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G, int nst) 
     if constexpr (PROJ) {
 #pragma unroll
       for (int i = 0; i < PJ_XCH; ++i) keep(xv[i]);
+    }
+    // a split without tiles still holds a partial for each of its rows: the
+    // empty one (m = -inf, l = 0), so that the merge reads every split
+    if (g == 0 && qrow < cnt) {
+      float* ml = a.ML + ((((int64_t)o * a.S + s) * a.max_sel + qrow) * a.H + h) * 2;
+      ml[0] = -INFINITY;
+      ml[1] = 0.f;
     }
     return;
   }
@@ -608,170 +615,208 @@ __device__ __forceinline__ void copy_out<bf16_t>(bf16_t* p, bf16_t x) { *p = x; 
 template <>
 __device__ __forceinline__ void copy_out<float>(float* p, bf16_t x) { *p = bf2f(x); }
 
-// grid (n_obj, ceil(max_sel/16)), block 512.  Dynamic LDS: merged O rows
-// (16 x (D+8) bf16) then the per-(row, head, split) weights (16*H*S floats).
-// 1. every (row, head, split) triple loads its (m, l) pair; per (row, head)
-//    the merge weights w_s = 2^(m_s - M) l_s / sum are formed in LDS;
-// 2. each thread merges one 8-column chunk over all active splits;
-// 3. y = x + O W_o on a 32x32x16 MFMA whose rows 16..31 are zero.
+// grid (n_obj, ceil(max_sel/16)), block 512.  Every key split of the call
+// holds a partial for every selected row (the attention writes l = 0 for
+// splits without tiles), so the merge needs nothing from the bank.
+// 1. the row indices are loaded and checked;
+// 2. for each (row, 8-column chunk) item, each of the NG thread groups that
+//    share it loads the (m, l) pairs and partial O chunks of its splits grp,
+//    grp + NG, ... (PART_B per batch, the first batch together with the
+//    residual inputs and W_o operands) and merges them by log-sum-exp in
+//    registers; the NG groups are merged through LDS, and the normalised
+//    row goes to LDS as bf16;
+// 3. y = x + O W_o on a 32x32x16 MFMA whose rows 16..31 are zero; a row with
+//    no resident key (total weight 0) is returned as x, bit for bit.
 constexpr int CB_ROWS = 16;   // the W_o step maps these rows to accumulator rows r < 8
 constexpr int CB_THREADS = 512;
+constexpr int PART_B = 8;     // splits per batch of partial loads
+
+__host__ __device__ constexpr int cb_groups(int D) {
+  return CB_THREADS / (CB_ROWS * (D / 8)) < 1 ? 1
+         : (CB_THREADS / (CB_ROWS * (D / 8)) > 8 ? 8 : CB_THREADS / (CB_ROWS * (D / 8)));
+}
+
+struct PartBatch {
+  float m[PART_B], l[PART_B];
+  u32x4 v[PART_B];
+};
+
+// Batch j of one item's partials: splits grp + NG*(PART_B*j + i); indices
+// past S re-read split S-1 (masked in the merge), rows past max_sel re-read
+// row max_sel-1 (not stored): no branch around the loads.
+__device__ __forceinline__ void part_load(const Rs3ReadoutArgs& a, int o, int row, int d0, int h, int grp, int NG,
+                                          int j, PartBatch& pb) {
+  const int64_t rows = a.max_sel;
+  const int rw = min(row, a.max_sel - 1);
+#pragma unroll
+  for (int i = 0; i < PART_B; ++i) {
+    const int sp = min(grp + NG * (PART_B * j + i), a.S - 1);
+    const int64_t prow = ((int64_t)o * a.S + sp) * rows + rw;
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    const f32x2 ml = gload((const f32x2*)(a.ML + (prow * a.H + h) * 2));
+    pb.m[i] = ml[0];
+    pb.l[i] = ml[1];
+    pb.v[i] = gload((const u32x4*)((const bf16_t*)a.Opart + prow * a.D + d0));
+  }
+}
+
+// Online log-sum-exp over a batch: running maximum M, weight W, sum acc.
+__device__ __forceinline__ void part_merge(const PartBatch& pb, int first, int NG, int S, float& M, float& W,
+                                           float (&acc)[8]) {
+#pragma unroll
+  for (int i = 0; i < PART_B; ++i) {
+    const bool on = first + NG * i < S && pb.l[i] > 0.f;
+    const float m = on ? pb.m[i] : -INFINITY;
+    if (m > M) {
+      const float sc = __builtin_amdgcn_exp2f(M - m);
+      W *= sc;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] *= sc;
+      M = m;
+    }
+    const float w = on ? __builtin_amdgcn_exp2f(m - M) * pb.l[i] : 0.f;
+    W += w;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      acc[2 * e] += on ? w * __uint_as_float(pb.v[i][e] << 16) : 0.f;
+      acc[2 * e + 1] += on ? w * __uint_as_float(pb.v[i][e] & 0xffff0000u) : 0.f;
+    }
+  }
+}
+
 template <typename OutT>
 __global__ __launch_bounds__(CB_THREADS) void k_combine(Rs3ReadoutArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t cl[];
   const int o = blockIdx.x, r0 = blockIdx.y * CB_ROWS;
-  BankDev& b = *a.banks[o];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5;
+  const int D = a.D, C = a.C, d_h = a.d_h, S = a.S, OS = D + 8;
+  const int cpr = D / 8, items = CB_ROWS * cpr, NG = cb_groups(D);
+  const int nb = (S + NG * PART_B - 1) / (NG * PART_B);   // batches per item
+  const int32_t* sel = a.sel_idx + (int64_t)o * a.sel_stride;
+  const bf16_t* X = (const bf16_t*)a.X + (int64_t)o * a.x_stride;
+  const bf16_t* WoT = (const bf16_t*)a.WoT;
+
+  // 1. The list entries of this lane's accumulator rows r < 8 (rows
+  //    8*(r/4) + 4*g + r%4 < CB_ROWS) and their predecessors (ascending
+  //    check), and of row r0 + tid for the error report: the only loads
+  //    before the row decisions, so waiting for them waits for nothing else.
+  int srow[8], sprv[8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    const int rc = min(r0 + c_row(r, lane), a.max_sel - 1);
+    srow[r] = gload(sel + rc);
+    sprv[r] = gload(sel + max(rc - 1, 0));
+  }
+  const int erc = min(r0 + (tid & (CB_ROWS - 1)), a.max_sel - 1);
+  const int e_cur = gload(sel + erc), e_prv = gload(sel + max(erc - 1, 0));
+  BankDev& b = *a.banks[o];
   // the merge covers every selected row: it reports a count past max_sel and
   // invalid (out of range or not ascending) list entries, whose rows it skips
   const int cnt = sel_count_of(a, o, b, blockIdx.y == 0 && tid == 0);
   if (r0 >= cnt) return;
-  const int D = a.D, C = a.C, H = a.H, d_h = a.d_h, S = a.S, OS = D + 8;
-  bf16_t* Os = (bf16_t*)cl;
-  float* wts = (float*)(cl + ((CB_ROWS * OS * 2 + 15) & ~15));
-  const int ntiles = b.hdr[HDR_NTILES];
-  const int SA = ntiles > 0 ? active_splits(ntiles, S) : 0;
-  const int32_t* sel = a.sel_idx + (int64_t)o * a.sel_stride;
-  if (tid < CB_ROWS && r0 + tid < cnt && !sel_ok(sel, r0 + tid, a.mn)) set_err(b.hdr, RS3_E_INVALID);
-  const int64_t base = (int64_t)o * S * a.max_sel;
-  const bf16_t* X = (const bf16_t*)a.X + (int64_t)o * a.x_stride;
-  const bf16_t* WoT = (const bf16_t*)a.WoT;
-
-  // Loads of step 3 that do not depend on the merge, issued first: the
-  // destination cell of this lane's 8 accumulator rows r < 8 (rows
-  // 8*(r/4) + 4*g + r%4 < CB_ROWS; -1 = no row), and for the wave's first
-  // column block the residual inputs and the first batch of W_o operands.
-  constexpr int KB = 8;   // k steps per batch of W_o loads
-  int dst[8];
+  // entry i of row r is valid iff it is in range and above its predecessor
+  auto entry_ok = [&](int i, int prev, int r) { return i >= 0 && i < a.mn && (r == 0 || prev < i); };
+  if (tid < CB_ROWS && r0 + tid < cnt && !entry_ok(e_cur, e_prv, r0 + tid)) set_err(b.hdr, RS3_E_INVALID);
+  int dst[8];   // destination cell of each accumulator row (-1 = none)
 #pragma unroll
   for (int r = 0; r < 8; ++r) {
     const int row = r0 + c_row(r, lane);
-    dst[r] = (row < cnt && sel_ok(sel, row, a.mn)) ? sel[row] : -1;
+    dst[r] = (c_row(r, lane) < CB_ROWS && row < cnt && entry_ok(srow[r], sprv[r], row)) ? srow[r] : -1;
   }
+  // 2. Every data load in one batch: residual inputs of the wave's first
+  //    column block, its first W_o operands, and this thread's first item's
+  //    first batch of partials (waves past the last column block, C < 256,
+  //    re-read the last column).
+  const int col0 = 32 * wave + (lane & 31);
   bf16_t xv0[8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r) xv0[r] = gload(X + (int64_t)max(dst[r], 0) * C + min(col0, C - 1));
+  constexpr int KB = 4;   // k steps per batch of W_o operands (D is a multiple of 64)
   u32x4 bv0[KB];
-  if (wave < C / 32) {
-    const int col = 32 * wave + (lane & 31);
+  {
+    const bf16_t* wr = WoT + (int64_t)min(col0, C - 1) * D;
 #pragma unroll
-    for (int r = 0; r < 8; ++r) xv0[r] = dst[r] >= 0 ? X[(int64_t)dst[r] * C + col] : (bf16_t)0;
-    const bf16_t* wr = WoT + (int64_t)col * D;
-#pragma unroll
-    for (int j = 0; j < KB; ++j)
-      if (16 * j < D) bv0[j] = *(const u32x4*)(wr + 16 * j + 8 * g);
+    for (int j = 0; j < KB; ++j) bv0[j] = gload((const u32x4*)(wr + 16 * j + 8 * g));
+  }
+  const int q0 = tid;
+  PartBatch pb;
+  {
+    const int item0 = q0 % items, grp0 = q0 / items;
+    const int rr = item0 / cpr, d0 = 8 * (item0 - rr * cpr);
+    part_load(a, o, r0 + rr, d0, d0 / d_h, grp0, NG, 0, pb);
   }
 
-  // 1a. (m, l) of every active split: wts[(rr*H + h)*SA + s] = m, then l after
-  for (int q = tid; q < CB_ROWS * H * SA; q += CB_THREADS) {
-    const int s = q % SA, rh = q / SA, h = rh % H, rr = rh / H, row = r0 + rr;
-    float m = -INFINITY, l = 0.f;
-    if (row < cnt) {
-      const float* ml = a.ML + ((base + (int64_t)s * a.max_sel + row) * H + h) * 2;
-      m = ml[0];
-      l = ml[1];
-    }
-    wts[q] = m;
-    wts[CB_ROWS * H * SA + q] = l;
-  }
-  __syncthreads();
-  // 1b. weights per (row, head), one wave per pair: lanes take the splits,
-  //     the max and the weight sum are wave reductions
-  for (int rh = wave; rh < CB_ROWS * H; rh += CB_THREADS / 64) {
-    float* mv = wts + rh * SA;
-    const float* lv = wts + CB_ROWS * H * SA + rh * SA;
-    float M = -INFINITY;
-    for (int s = lane; s < SA; s += 64) M = fmaxf(M, mv[s]);
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) M = fmaxf(M, __shfl_xor(M, off, 64));
-    float W = 0.f;
-    if (M != -INFINITY)
-      for (int s = lane; s < SA; s += 64) W += __builtin_amdgcn_exp2f(mv[s] - M) * lv[s];
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) W += __shfl_xor(W, off, 64);
-    const float iw = W > 0.f ? 1.f / W : 0.f;
-    for (int s = lane; s < SA; s += 64)
-      mv[s] = (M != -INFINITY) ? __builtin_amdgcn_exp2f(mv[s] - M) * lv[s] * iw : 0.f;
-  }
-  __syncthreads();
-  // 2. merged O rows into LDS.  Each (row, 8-column chunk) is summed by
-  //    NG thread groups over interleaved splits, then reduced through LDS.
-  const bf16_t* Op = (const bf16_t*)a.Opart;
-  const int cpr = D / 8;
-  const int items = CB_ROWS * cpr;
-  const int NG = max(1, min(8, CB_THREADS / items));   // split groups per item
-  float* red = wts + 2 * CB_ROWS * H * SA;              // [NG][items][8]
-  for (int q = tid; q < items * NG; q += CB_THREADS) {
+  // merge.  LDS: Os [CB_ROWS][D+8] bf16 | red [NG][items][10] f32 | kept [CB_ROWS]
+  bf16_t* Os = (bf16_t*)cl;
+  float* red = (float*)(cl + ((CB_ROWS * OS * 2 + 15) & ~15));
+  int* kept = (int*)(red + (size_t)NG * items * 10);
+  for (int q = q0; q < items * NG; q += CB_THREADS) {
     const int item = q % items, grp = q / items;
-    const int rr = item / cpr, d0 = 8 * (item - rr * cpr), h = d0 / d_h, row = r0 + rr;
-    float acc8[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    if (row < cnt) {
-      const float* w = wts + (rr * H + h) * SA;
-      const bf16_t* src = Op + (base + row) * D + d0;
-      const int64_t sstride = (int64_t)a.max_sel * D;
-#pragma unroll 4
-      for (int s = grp; s < SA; s += NG) {
-        const float ws = w[s];
-        const u32x4 v = *(const u32x4*)(src + s * sstride);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          acc8[2 * j] += ws * __uint_as_float(v[j] << 16);
-          acc8[2 * j + 1] += ws * __uint_as_float(v[j] & 0xffff0000u);
-        }
-      }
+    const int rr = item / cpr, d0 = 8 * (item - rr * cpr), h = d0 / d_h;
+    float M = -INFINITY, W = 0.f;
+    float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int j = 0; j < nb; ++j) {
+      if (q != q0 || j > 0) part_load(a, o, r0 + rr, d0, h, grp, NG, j, pb);
+      part_merge(pb, grp + NG * PART_B * j, NG, S, M, W, acc);
     }
-    float* dst = red + ((int64_t)grp * items + item) * 8;
+    float* dstp = red + (size_t)grp * 10 * items + item;   // [NG][10][items]
+    dstp[0] = M;
+    dstp[items] = W;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) dst[j] = acc8[j];
+    for (int e = 0; e < 8; ++e) dstp[(2 + e) * items] = acc[e];
   }
-  __syncthreads();
+  lds_barrier();
   for (int item = tid; item < items; item += CB_THREADS) {
-    const int rr = item / cpr, d0 = 8 * (item - rr * cpr);
-    float acc8[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    for (int grp = 0; grp < NG; ++grp) {
-      const float* src = red + ((int64_t)grp * items + item) * 8;
+    float M = -INFINITY;
+    for (int grp = 0; grp < NG; ++grp) M = fmaxf(M, red[(size_t)grp * 10 * items + item]);
+    float W = 0.f, acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (M != -INFINITY)
+      for (int grp = 0; grp < NG; ++grp) {
+        const float* sp = red + (size_t)grp * 10 * items + item;
+        const float sc = __builtin_amdgcn_exp2f(sp[0] - M);   // 0 for empty groups
+        W += sc * sp[items];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) acc8[j] += src[j];
-    }
+        for (int e = 0; e < 8; ++e) acc[e] += sc * sp[(2 + e) * items];
+      }
+    const float inv = W > 0.f ? 1.f / W : 0.f;
+    const int rr = item / cpr, d0 = 8 * (item - rr * cpr);
     u32x4 pk;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) pk[j] = pack_bf16x2(acc8[2 * j], acc8[2 * j + 1]);
+    for (int j = 0; j < 4; ++j) pk[j] = pack_bf16x2(acc[2 * j] * inv, acc[2 * j + 1] * inv);
     *(u32x4*)&Os[rr * OS + d0] = pk;
+    if (d0 == 0) kept[rr] = W > 0.f;
   }
-  __syncthreads();
+  lds_barrier();
   // 3. y = x + O W_o for the block's rows, columns split over the waves
   OutT* Y = (OutT*)a.Y + (int64_t)o * a.y_stride;
   const bool arow = (lane & 31) < CB_ROWS;
   const bf16_t* orow = &Os[(arow ? (lane & 31) : 0) * OS + 8 * g];
-  for (int nb = wave; nb < C / 32; nb += CB_THREADS / 64) {
-    const bool first = nb == wave;
-    const int col = 32 * nb + (lane & 31);
-    const bf16_t* wr = WoT + (int64_t)col * D;
+  bool keys[8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r) keys[r] = c_row(r, lane) < CB_ROWS && kept[c_row(r, lane)] != 0;
+  for (int nbk = wave; nbk < C / 32; nbk += CB_THREADS / 64) {
+    const bool first = nbk == wave;
+    const int col = 32 * nbk + (lane & 31);
+    const bf16_t* wr = WoT + (int64_t)col * D + 8 * g;
     bf16_t xv[8];
 #pragma unroll
-    for (int r = 0; r < 8; ++r)
-      xv[r] = first ? xv0[r] : (dst[r] >= 0 ? X[(int64_t)dst[r] * C + col] : (bf16_t)0);
+    for (int r = 0; r < 8; ++r) xv[r] = first ? xv0[r] : gload(X + (int64_t)max(dst[r], 0) * C + col);
     f32x16 acc = {};
     for (int k0 = 0; k0 < D; k0 += 16 * KB) {
-      u32x4 bv[KB];
-      if (first && k0 == 0) {
+      u32x4 av[KB], bv[KB];
 #pragma unroll
-        for (int j = 0; j < KB; ++j) bv[j] = bv0[j];
-      } else {
-#pragma unroll
-        for (int j = 0; j < KB; ++j)
-          if (k0 + 16 * j < D) bv[j] = *(const u32x4*)(wr + k0 + 16 * j + 8 * g);
+      for (int j = 0; j < KB; ++j) {
+        av[j] = arow ? *(const u32x4*)(orow + k0 + 16 * j) : u32x4{0, 0, 0, 0};
+        bv[j] = (first && k0 == 0) ? bv0[j] : gload((const u32x4*)(wr + k0 + 16 * j));
       }
 #pragma unroll
-      for (int j = 0; j < KB; ++j)
-        if (k0 + 16 * j < D) {
-          const u32x4 av = arow ? *(const u32x4*)(orow + k0 + 16 * j) : u32x4{0, 0, 0, 0};
-          acc = mfma32(av, bv[j], acc);
-        }
+      for (int j = 0; j < KB; ++j) acc = mfma32(av[j], bv[j], acc);
     }
 #pragma unroll
     for (int r = 0; r < 8; ++r) {
       if (dst[r] < 0) continue;
       const int64_t off = (int64_t)dst[r] * C + col;
-      if (ntiles == 0)
+      if (!keys[r])
         copy_out<OutT>(&Y[off], xv[r]);
       else
         store_out<OutT>(&Y[off], bf2f(xv[r]) + acc[r]);
@@ -903,11 +948,10 @@ __global__ __launch_bounds__(256) void k_readout_f32(Rs3ReadoutArgs a) {
 
 using namespace rs3;
 
-static size_t combine_lds_bytes(int D, int H, int S) {
+static size_t combine_lds_bytes(int D) {
   const int items = CB_ROWS * (D / 8);
-  const int NG = CB_THREADS / items < 1 ? 1 : (CB_THREADS / items > 8 ? 8 : CB_THREADS / items);
-  return (((size_t)CB_ROWS * (D + 8) * 2 + 15) & ~(size_t)15) + (size_t)2 * CB_ROWS * H * S * 4 +
-         (size_t)NG * items * 8 * 4;
+  return (((size_t)CB_ROWS * (D + 8) * 2 + 15) & ~(size_t)15) + (size_t)cb_groups(D) * items * 10 * 4 +
+         CB_ROWS * 4;
 }
 
 // Launches of at most one work-group per CU keep 7 half tiles in flight
@@ -982,7 +1026,7 @@ hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st
   }
   hipError_t e = rs3_launch_attn(a, st, project);
   if (e != hipSuccess) return e;
-  const size_t lds = combine_lds_bytes(a.D, a.H, a.S);
+  const size_t lds = combine_lds_bytes(a.D);
   const dim3 cgrid(a.n_obj, (a.max_sel + CB_ROWS - 1) / CB_ROWS);
   if (a.y_fp32)
     RS3_LAUNCH(RS3_K_COMBINE, st, k_combine<float>, cgrid, dim3(CB_THREADS), lds, st, a);
@@ -992,11 +1036,10 @@ hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st
 }
 
 hipError_t rs3_readout_setup() {
-  // H * S <= RS3_MAX_SPLITS_X_HEADS and D <= 1024 (checked on the host);
-  // the group buffer is largest for D = 1024 with one group or D = 64 with 4
+  // D <= 1024 (checked on the host)
   size_t max_lds = 0;
-  for (int D = 64; D <= 1024; D *= 2) {
-    const size_t b = combine_lds_bytes(D, 1, RS3_MAX_SPLITS_X_HEADS);
+  for (int D = 64; D <= 1024; D += 64) {
+    const size_t b = combine_lds_bytes(D);
     if (b > max_lds) max_lds = b;
   }
   hipError_t e = hipFuncSetAttribute((const void*)k_combine<bf16_t>, hipFuncAttributeMaxDynamicSharedMemorySize,

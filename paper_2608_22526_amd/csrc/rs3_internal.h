@@ -135,6 +135,11 @@ __host__ __device__ __forceinline__ int active_splits(int ntiles, int S) {
   return (ntiles + tps - 1) / tps;
 }
 
+// Workgroup barrier for LDS traffic only: waits for this wave's LDS
+// operations, not for its outstanding global loads (which the fence of
+// __syncthreads would drain).
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 __device__ __forceinline__ void set_err(int32_t* hdr, int code) {
   atomicCAS(&hdr[HDR_ERR], 0, code);
 }

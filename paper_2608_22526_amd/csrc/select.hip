@@ -78,10 +78,6 @@ __global__ __launch_bounds__(64) void k_energy(const T* __restrict__ X, int64_t 
   }
 }
 
-// Workgroup barrier for LDS traffic only: waits for this wave's LDS
-// operations, not for its outstanding global loads (which a __syncthreads
-// fence would drain).
-__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // ---------------------------------------------------------------------------
 // block-wide helpers for a 1024-thread workgroup
