@@ -372,8 +372,7 @@ def _algo_bytes(cfg, absorb, rec):
         "qproj": sum(q * (C * b + Da * 2) for q in sel) + Da * C * 2,
         "attn": sum(n * Da * 2 * 2 + q * Da * 2 * 2 for q, n in zip(sel, nk)),
         "combine": sum(q * (Da * 2 + 2 * C * b) for q in sel) + C * Da * 2,
-        "commit_place": cfg.n_obj * mn + 4 * sum(kept),
-        "commit_append": sum(k * (4 * dkv * b + 2 * Da * 2) for k in kept),
+        "commit": cfg.n_obj * mn + sum(k * (4 + 4 * dkv * b + 2 * Da * 2) for k in kept),
     }
 
 

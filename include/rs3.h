@@ -246,8 +246,8 @@ rs3_status rs3_attend(const void* Qh, const void* Kh, const void* Vh, int32_t n_
 enum {
   RS3_K_ENERGY = 0,        /* token energies */
   RS3_K_SELECT = 1,        /* prior + top-k + compaction */
-  RS3_K_COMMIT_PLACE = 2,  /* mask compaction + ring placement + tile list */
-  RS3_K_COMMIT_APPEND = 3, /* row copy + K/V projection */
+  RS3_K_COMMIT = 2,        /* commit: mask compaction, ring placement, tile list, row copy and K/V projection */
+  RS3_K_COMMIT_APPEND = 3, /* row copy + K/V projection of a restored bank (rs3_bank_import) */
   RS3_K_COPY = 4,          /* X -> Y copy for out-of-place readout */
   RS3_K_QPROJ = 5,         /* gather + query projection */
   RS3_K_ATTN = 6,          /* split-KV attention */

@@ -66,7 +66,7 @@ _SIGS = {
     "rs3_profile_reset": (c_i32, []),
 }
 
-KERNEL_NAMES = ["energy", "select", "commit_place", "commit_append", "copy", "qproj", "attn", "combine",
+KERNEL_NAMES = ["energy", "select", "commit", "commit_append", "copy", "qproj", "attn", "combine",
                 "readout_f32"]
 
 _lib = None

@@ -26,6 +26,7 @@ struct rs3_bank {
   BankDev* d_desc;  // device copy of `host`
   int32_t pin_calls;
   int32_t unpinned_seen;
+  uint32_t commits;   // commits launched; the parity selects the current frame table copy
 };
 
 namespace {
@@ -280,6 +281,7 @@ rs3_status rs3_bank_create(const rs3_layer* L, int32_t cap, int32_t f_max, int32
   b->L = L;
   b->pin_calls = 0;
   b->unpinned_seen = 0;
+  b->commits = 0;
   BankDev& h = b->host;
   memset(&h, 0, sizeof(h));
   h.cap = cap;
@@ -302,7 +304,7 @@ rs3_status rs3_bank_create(const rs3_layer* L, int32_t cap, int32_t f_max, int32
       {&h.Khat, proj},
       {&h.Vhat, proj},
       {(void**)&h.hdr, HDR_WORDS * 4},
-      {(void**)&h.frames, (size_t)f_max * 16},
+      {(void**)&h.frames, (size_t)2 * f_max * 16},
       {(void**)&h.tiles, (size_t)h.n_tiles_cap * sizeof(TileEnt)},
       {(void**)&b->d_desc, sizeof(BankDev)},
   };
@@ -338,19 +340,20 @@ rs3_status rs3_bank_export(const rs3_bank* b, int32_t* hdr, int32_t* frames, voi
                            int32_t* pos) {
   if (!b || !hdr) return RS3_E_INVALID;
   const BankDev& h = b->host;
+  const int p = b->commits & 1;   // current copy of the frame table
   hipError_t e = hipDeviceSynchronize();
   int32_t dh[HDR_WORDS];
   if (e == hipSuccess) e = hipMemcpy(dh, h.hdr, sizeof(dh), hipMemcpyDeviceToHost);
   if (e != hipSuccess) return map_err(e);
-  const int nf = dh[HDR_NFRAMES];
+  const int nf = dh[HDR_NFRAMES + HDR_COPY * p];
   std::vector<int32_t> fr((size_t)h.f_max * 4, 0);
-  e = hipMemcpy(fr.data(), h.frames, fr.size() * 4, hipMemcpyDeviceToHost);
+  e = hipMemcpy(fr.data(), h.frames + (size_t)4 * h.f_max * p, fr.size() * 4, hipMemcpyDeviceToHost);
   if (e != hipSuccess) return map_err(e);
   int keys = 0;
   for (int f = 0; f < nf; ++f) keys += fr[4 * f + 1];
   memset(hdr, 0, RS3_BANK_HDR_WORDS * 4);
   hdr[0] = nf;
-  hdr[1] = dh[HDR_PINEND];
+  hdr[1] = dh[HDR_PINEND + HDR_COPY * p];
   hdr[2] = dh[HDR_ERR];
   hdr[3] = keys;
   if (frames) memcpy(frames, fr.data(), (size_t)nf * 16);
@@ -402,13 +405,15 @@ rs3_status rs3_bank_import(rs3_bank* b, const int32_t* hdr, const int32_t* frame
   }
   if (n_pinned > h.n_pin || pinned_rows != pin_end || sum != keys) return RS3_E_INVALID;
   const rs3_layer* L = b->L;
+  const int p = b->commits & 1;   // the restored state becomes the current copy
   hipError_t e = hipDeviceSynchronize();
   std::vector<int32_t> fr((size_t)h.f_max * 4, 0);
   if (nf > 0) memcpy(fr.data(), frames, (size_t)nf * 16);
-  if (e == hipSuccess) e = hipMemcpy(h.frames, fr.data(), fr.size() * 4, hipMemcpyHostToDevice);
+  if (e == hipSuccess)
+    e = hipMemcpy(h.frames + (size_t)4 * h.f_max * p, fr.data(), fr.size() * 4, hipMemcpyHostToDevice);
   int32_t dh[HDR_WORDS] = {};
-  dh[HDR_NFRAMES] = nf;
-  dh[HDR_PINEND] = pin_end;
+  dh[HDR_NFRAMES + HDR_COPY * p] = nf;
+  dh[HDR_PINEND + HDR_COPY * p] = pin_end;
   dh[HDR_ERR] = err;
   dh[HDR_PLEN] = -1;
   dh[HDR_NKEYS] = keys;
@@ -440,6 +445,7 @@ rs3_status rs3_bank_import(rs3_bank* b, const int32_t* hdr, const int32_t* frame
   a.m = 1;
   a.s = 1;
   a.from_ring = 1;
+  a.parity = (uint64_t)p;
   for (int f = 0; f < nf && e == hipSuccess; ++f) {
     const int span[2] = {fr[4 * f], fr[4 * f + 1]};
     if (span[1] == 0) continue;
@@ -780,9 +786,11 @@ rs3_status rs3_commit(rs3_bank* const* banks, int32_t n_obj, const rs3_grid* g, 
   a.fall_max = fall_max;
   a.n_obj = n_obj;
   a.absorb = ld.absorb;
+  for (int o = 0; o < n_obj; ++o) a.parity |= (uint64_t)(banks[o]->commits & 1u) << o;
   hipError_t e = rs3_launch_commit(a, ld.dtype, ld.d_kv, ld.Da, ld.Ha, ld.dah, (hipStream_t)stream);
   if (e != hipSuccess) return map_err(e);
   for (int o = 0; o < n_obj; ++o) {
+    banks[o]->commits++;
     if (pin)
       banks[o]->pin_calls++;
     else

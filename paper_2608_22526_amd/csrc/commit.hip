@@ -1,15 +1,20 @@
 // Store-sparse commit (Sec. 3.2, Eq. 8; sparse write of Algorithm 1).
 //
-// k_commit_place  : one 1024-thread workgroup per object.  Compacts the mask
-//                   to the ascending kept list (ordered block scan), applies
-//                   the dense fall-through, places the frame in the ring
-//                   (one wave; the rule is documented in rs3.h), writes
-//                   the kept cell of every new row to `pos`, and rebuilds the
-//                   list of resident 64-row tiles with their row masks.
-// k_commit_append : 64 kept rows per workgroup.  Copies the raw K/V rows into
-//                   the ring and writes their projections K^ = K W_k and
-//                   V^ = V W_v into the tile-blocked attention layouts
-//                   (bf16 MFMA with fp32 accumulation, or fp32 FMA loops).
+// k_commit : grid (n_obj, 1 + ceil(mn/64)), block 1024.  Every work-group of
+//            an object compacts the mask to the ascending kept list (ordered
+//            block scan, dense fall-through) and runs the placement rule
+//            (documented in rs3.h; one wave) on its own LDS copy of the frame
+//            table as it was before this commit (copy p of the double-
+//            buffered table), so all of them know the new frame's start row.
+//            Work-group 0 writes the new state to copy 1-p, the key count and
+//            the list of resident 64-row tiles with their row masks; work-
+//            group 1 + b appends kept rows 64b .. 64b+63: the raw K/V rows
+//            into the ring, their cells into `pos`, and their projections
+//            K^ = K W_k, V^ = V W_v into the tile-blocked attention layouts
+//            (bf16 MFMA with fp32 accumulation, or fp32 FMA loops; the raw
+//            rows re-laid in absorbed mode).
+// k_commit_append_* / k_bank_tiles : the same append and tile rebuild for a
+//            bank restored from a snapshot (rows already in the ring).
 #include "rs3_internal.h"
 
 namespace rs3 {
@@ -249,83 +254,6 @@ __device__ __forceinline__ void rebuild_tiles(const BankDev& b, const int32_t* s
   if (tid == 0) b.hdr[HDR_NTILES] = ntot;
 }
 
-// grid n_obj, block 1024, dynamic LDS f_max*16 bytes.  Thread t owns the
-// cpt contiguous cells c0 = t*cpt ...; all cross-thread traffic is in LDS.
-__global__ __launch_bounds__(CP_THREADS) void k_commit_place(Rs3CommitArgs a) {
-  extern __shared__ __attribute__((aligned(16))) int32_t sfr[];
-  __shared__ CpShared sh;
-  const int o = blockIdx.x, tid = threadIdx.x;
-  const BankDev& b = *a.banks[o];
-  const int m = a.m, n = a.n, s = a.s, mn = m * n, W = n * s;
-  const uint8_t* M = a.masks + (int64_t)o * (m * s) * W;
-  const int cpt = (mn + CP_THREADS - 1) / CP_THREADS;
-  const int c0 = tid * cpt;
-  // frame table, header words and mask cells are independent: load together
-  const int f_max = b.f_max;
-  const int32_t fr_w = tid < 4 * f_max ? b.frames[tid] : 0;
-  int nf0 = 0, pin_end0 = 0;
-  if (tid < 64) {
-    nf0 = b.hdr[HDR_NFRAMES];
-    pin_end0 = b.hdr[HDR_PINEND];
-  }
-  uint32_t bits = 0;
-  if (s == 1 && cpt == 4 && c0 + 4 <= mn && ((((uintptr_t)M) + c0) & 3) == 0) {
-    uint32_t t = *(const uint32_t*)(M + c0);
-    t |= t >> 4;
-    t |= t >> 2;
-    t |= t >> 1;
-    bits = (t & 1u) | ((t >> 7) & 2u) | ((t >> 14) & 4u) | ((t >> 21) & 8u);
-  } else if (c0 < mn) {
-    int y = c0 / n, x = c0 - y * n;
-    for (int j = 0; j < cpt && c0 + j < mn; ++j) {
-      if (M[(int64_t)(y * s) * W + x * s]) bits |= 1u << j;
-      if (++x == n) {
-        x = 0;
-        ++y;
-      }
-    }
-  }
-  const int nc = c0 < mn ? min(cpt, mn - c0) : 0;   // cells of this thread
-  int total;
-  int before = cp_scan_bits(bits, cpt, sh.red, &total);
-  if (total < a.fall_min || total > a.fall_max) {   // dense fall-through: every cell
-    bits = nc == 32 ? ~0u : ((1u << nc) - 1u);
-    before = c0 < mn ? c0 : mn;
-    total = mn;
-  }
-  if (tid < 4 * f_max) sfr[tid] = fr_w;
-  lds_barrier();
-  if (tid < 64) {
-    int nf = nf0, pin_end = pin_end0, keys = 0;
-    const int start = place_frame_wave(b, sfr, nf0, pin_end0, total, a.t, a.pin, &nf, &pin_end, &keys);
-    if (tid == 0) {
-      if (a.kept_count) a.kept_count[o] = total;
-      sh.ok = start >= 0;
-      sh.start = start;
-      sh.len = nf;
-      if (start >= 0) {
-        b.hdr[HDR_NFRAMES] = nf;
-        b.hdr[HDR_PINEND] = pin_end;
-        b.hdr[HDR_PSTART] = start;
-        b.hdr[HDR_PLEN] = total;
-        b.hdr[HDR_NKEYS] = keys;
-      } else {
-        b.hdr[HDR_PLEN] = -1;
-        set_err(b.hdr, RS3_E_CAPACITY);
-      }
-    }
-  }
-  lds_barrier();
-  if (!sh.ok) return;
-  const int start = sh.start;
-  const int nf = sh.len;
-  if (tid < 4 * nf) b.frames[tid] = sfr[tid];
-  for (int j = 0; j < cpt; ++j)
-    if (bits >> j & 1) b.pos[start + before++] = c0 + j;
-
-  rebuild_tiles(b, sfr, nf, sh);
-}
-
 // Bank restore: frame table from device memory, then the tile list and the
 // key count (grid 1, block CP_THREADS, dynamic LDS f_max*16 bytes).
 __global__ __launch_bounds__(CP_THREADS) void k_bank_tiles(Rs3CommitArgs a) {
@@ -333,8 +261,9 @@ __global__ __launch_bounds__(CP_THREADS) void k_bank_tiles(Rs3CommitArgs a) {
   __shared__ CpShared sh;
   const int tid = threadIdx.x;
   const BankDev& b = *a.banks[0];
-  const int nf = b.hdr[HDR_NFRAMES];
-  if (tid < 4 * nf) sfr[tid] = b.frames[tid];
+  const int p = (int)(a.parity & 1);
+  const int nf = b.hdr[HDR_NFRAMES + HDR_COPY * p];
+  if (tid < 4 * nf) sfr[tid] = b.frames[4 * b.f_max * p + tid];
   __syncthreads();
   if (tid == 0) {
     int keys = 0;
@@ -346,24 +275,21 @@ __global__ __launch_bounds__(CP_THREADS) void k_bank_tiles(Rs3CommitArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// append: bf16, 256 threads, 64 rows per workgroup.  The kept rows are read
-// once (16-byte loads) into LDS and written to the raw ring from the same
-// registers; the projections then read their row operands from LDS:
+// Append of rows r0 .. r0+rows-1 of the new frame (ring rows start + r0 + r)
+// by the NT threads of a work-group.  src[r] (LDS) is the kept cell of row
+// r; with a.from_ring the rows are already in the raw ring.
+// bf16: the kept rows are read once (16-byte loads) into LDS and written to
+// the raw ring from the same registers; the projections then read their row
+// operands from LDS:
 //   K^ rows: C = A B, A = kept K rows (64 x d_kv), B = W_k (d_kv x D):
 //     lane holds column d, rows = keys  -> Khat[tile][h][key][d%d_h]
 //   V^ as its transpose: C = W_v^T (D x d_kv) V^T (d_kv x 64):
 //     lane holds column = key, rows = d -> Vhat[tile][h][d%d_h][vslot(key)]
-// Dynamic LDS: 2 * 64 * (d_kv + 8) bf16.
-__global__ __launch_bounds__(256) void k_commit_append_bf16(Rs3CommitArgs a) {
-  extern __shared__ __attribute__((aligned(16))) bf16_t rows_lds[];
-  __shared__ int spos[64];
-  const int o = blockIdx.x;
-  BankDev& b = *a.banks[o];
-  const int L = b.hdr[HDR_PLEN];
-  const int r0 = blockIdx.y * 64;
-  if (L < 0 || r0 >= L) return;
-  const int start = b.hdr[HDR_PSTART];
-  const int rows = min(64, L - r0);
+// rows_lds: 2 * 64 * (d_kv + 8) bf16.
+template <int NT>
+__device__ __forceinline__ void append_bf16(const Rs3CommitArgs& a, const BankDev& b, int o, int start, int r0,
+                                            int rows, const int* src, bf16_t* rows_lds) {
+  constexpr int NW = NT / 64;
   const int d_kv = b.d_kv, d_h = b.d_h, H = b.H, D = H * d_h;
   const int lg_dh = 31 - __clz(d_h);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5;
@@ -374,10 +300,8 @@ __global__ __launch_bounds__(256) void k_commit_append_bf16(Rs3CommitArgs a) {
   const bf16_t* Vm = (const bf16_t*)a.Vmem + (int64_t)o * a.kv_stride;
   bf16_t* Kr = (bf16_t*)b.Kraw;
   bf16_t* Vr = (bf16_t*)b.Vraw;
-  if (tid < 64) spos[tid] = tid < rows ? b.pos[start + r0 + tid] : 0;
-  __syncthreads();
   const int cpr = d_kv / 8;
-  for (int q = tid; q < 64 * cpr; q += 256) {
+  for (int q = tid; q < 64 * cpr; q += NT) {
     const int r = q / cpr, c = q - r * cpr;
     u32x4 kv = {0, 0, 0, 0}, vv = {0, 0, 0, 0};
     if (r < rows) {
@@ -386,9 +310,9 @@ __global__ __launch_bounds__(256) void k_commit_append_bf16(Rs3CommitArgs a) {
         kv = *(const u32x4*)(Kr + j * d_kv + 8 * c);
         vv = *(const u32x4*)(Vr + j * d_kv + 8 * c);
       } else {
-        const int src = spos[r];
-        kv = *(const u32x4*)(Km + (int64_t)src * d_kv + 8 * c);
-        vv = *(const u32x4*)(Vm + (int64_t)src * d_kv + 8 * c);
+        const int cell = src[r];
+        kv = *(const u32x4*)(Km + (int64_t)cell * d_kv + 8 * c);
+        vv = *(const u32x4*)(Vm + (int64_t)cell * d_kv + 8 * c);
         *(u32x4*)(Kr + j * d_kv + 8 * c) = kv;
         *(u32x4*)(Vr + j * d_kv + 8 * c) = vv;
       }
@@ -396,18 +320,18 @@ __global__ __launch_bounds__(256) void k_commit_append_bf16(Rs3CommitArgs a) {
     *(u32x4*)(sK + r * RS + 8 * c) = kv;
     *(u32x4*)(sV + r * RS + 8 * c) = vv;
   }
-  __syncthreads();
+  lds_barrier();
   bf16_t* Kh = (bf16_t*)b.Khat;
   bf16_t* Vh = (bf16_t*)b.Vhat;
   if (a.absorb) {
     // attention on the raw rows (one head of width d_kv): K rows as they
     // are, V rows transposed into slot order
-    for (int q = tid; q < rows * cpr; q += 256) {
+    for (int q = tid; q < rows * cpr; q += NT) {
       const int r = q / cpr, c = q - r * cpr;
       const int j = start + r0 + r;
       *(u32x4*)(Kh + ((int64_t)(j >> 6) * KT + (j & 63)) * d_kv + 8 * c) = *(const u32x4*)(sK + r * RS + 8 * c);
     }
-    for (int q = tid; q < rows * d_kv; q += 256) {
+    for (int q = tid; q < rows * d_kv; q += NT) {
       const int r = q / d_kv, d = q - r * d_kv;
       const int j = start + r0 + r;
       Vh[((int64_t)(j >> 6) * d_kv + d) * KT + vslot(j & 63)] = sV[r * RS + d];
@@ -417,7 +341,7 @@ __global__ __launch_bounds__(256) void k_commit_append_bf16(Rs3CommitArgs a) {
   const bf16_t* WkT = (const bf16_t*)a.WkT;
   const bf16_t* WvT = (const bf16_t*)a.WvT;
   const int nblk = 2 * (D / 32);
-  for (int blk = wave; blk < nblk; blk += 4) {
+  for (int blk = wave; blk < nblk; blk += NW) {
     const int mb = blk & 1, nb = blk >> 1;
     const int rr = 32 * mb + (lane & 31);   // key row fed by this lane
     const int dcol = 32 * nb + (lane & 31);
@@ -457,29 +381,41 @@ __global__ __launch_bounds__(256) void k_commit_append_bf16(Rs3CommitArgs a) {
   }
 }
 
-// append: fp32, 256 threads, 64 rows per workgroup.  For d_kv <= 64 the
-// kept rows are staged in LDS and each thread owns one output column d with
-// its W_k / W_v rows in registers (row operands are LDS broadcasts);
-// otherwise plain FMA loops.
-constexpr int F32_STAGE_KV = 64;
-
-__global__ __launch_bounds__(256) void k_commit_append_f32(Rs3CommitArgs a) {
-  __shared__ __attribute__((aligned(16))) float sK[64 * (F32_STAGE_KV + 4)], sV[64 * (F32_STAGE_KV + 4)];
-  const int o = blockIdx.x, tid = threadIdx.x;
-  BankDev& b = *a.banks[o];
+// Restored bank: rows [hdr PSTART, + PLEN) of bank 0 from the raw ring,
+// 64 per work-group.
+__global__ __launch_bounds__(256) void k_commit_append_bf16(Rs3CommitArgs a) {
+  extern __shared__ __attribute__((aligned(16))) bf16_t rows_lds[];
+  __shared__ int spos[64];
+  const int o = blockIdx.x;
+  const BankDev& b = *a.banks[o];
   const int L = b.hdr[HDR_PLEN];
   const int r0 = blockIdx.y * 64;
   if (L < 0 || r0 >= L) return;
   const int start = b.hdr[HDR_PSTART];
   const int rows = min(64, L - r0);
+  if (threadIdx.x < 64) spos[threadIdx.x] = (int)threadIdx.x < rows ? b.pos[start + r0 + threadIdx.x] : 0;
+  __syncthreads();
+  append_bf16<256>(a, b, o, start, r0, rows, spos, rows_lds);
+}
+
+// fp32: for d_kv <= 64 the kept rows are staged in LDS (sK, sV: 64 rows of
+// F32_STAGE_KV + 4 floats each) and each thread owns one output column d
+// with its W_k / W_v rows in registers (row operands are LDS broadcasts);
+// otherwise plain FMA loops over the rows just written to the ring.
+constexpr int F32_STAGE_KV = 64;
+constexpr int F32_SP = F32_STAGE_KV + 4;   // row pitch: 16-byte aligned rows
+
+template <int NT>
+__device__ __forceinline__ void append_f32(const Rs3CommitArgs& a, const BankDev& b, int o, int start, int r0,
+                                           int rows, const int* src, float* sK, float* sV) {
+  const int tid = threadIdx.x;
   const int d_kv = b.d_kv, d_h = b.d_h, H = b.H, D = H * d_h;
   const bool stage = d_kv <= F32_STAGE_KV;
-  constexpr int SP = F32_STAGE_KV + 4;   // row pitch: 16-byte aligned rows
   const float* Km = (const float*)a.Kmem + (int64_t)o * a.kv_stride;
   const float* Vm = (const float*)a.Vmem + (int64_t)o * a.kv_stride;
   float* Kr = (float*)b.Kraw;
   float* Vr = (float*)b.Vraw;
-  for (int q = tid; q < rows * d_kv; q += 256) {
+  for (int q = tid; q < rows * d_kv; q += NT) {
     const int r = q / d_kv, c = q - r * d_kv;
     const int64_t j = start + r0 + r;
     float kv, vv;
@@ -487,63 +423,61 @@ __global__ __launch_bounds__(256) void k_commit_append_f32(Rs3CommitArgs a) {
       kv = Kr[j * d_kv + c];
       vv = Vr[j * d_kv + c];
     } else {
-      const int src = b.pos[j];
-      kv = Km[(int64_t)src * d_kv + c];
-      vv = Vm[(int64_t)src * d_kv + c];
+      const int cell = src[r];
+      kv = Km[(int64_t)cell * d_kv + c];
+      vv = Vm[(int64_t)cell * d_kv + c];
       Kr[j * d_kv + c] = kv;
       Vr[j * d_kv + c] = vv;
     }
     if (stage) {
-      sK[r * SP + c] = kv;
-      sV[r * SP + c] = vv;
+      sK[r * F32_SP + c] = kv;
+      sV[r * F32_SP + c] = vv;
     }
   }
-  __syncthreads();
+  __syncthreads();   // also publishes the ring rows read back below
   const float* WkT = (const float*)a.WkT;
   const float* WvT = (const float*)a.WvT;
   float* Kh = (float*)b.Khat;
   float* Vh = (float*)b.Vhat;
   if (stage) {
-    const int ngrp = D >= 256 ? 1 : 256 / D;
-    for (int dq = tid; dq < D * ngrp; dq += 256) {
-      const int d = dq % D, grp = dq / D;
-      const int h = d / d_h, dd = d - h * d_h;
-      float wk[F32_STAGE_KV], wv[F32_STAGE_KV];
-      if (!a.absorb) {
+    // one pass for K^ and one for V^, so that one row of weights is live
+    const int ngrp = D >= NT ? 1 : NT / D;
+    for (int pass = 0; pass < 2; ++pass) {
+      const float* WT = pass == 0 ? WkT : WvT;
+      const float* sX = pass == 0 ? sK : sV;
+      for (int dq = tid; dq < D * ngrp; dq += NT) {
+        const int d = dq % D, grp = dq / D;
+        const int h = d / d_h, dd = d - h * d_h;
+        float w[F32_STAGE_KV];
+        if (!a.absorb) {
 #pragma unroll
-        for (int c = 0; c < F32_STAGE_KV; ++c) {
-          wk[c] = c < d_kv ? WkT[(int64_t)d * d_kv + c] : 0.f;
-          wv[c] = c < d_kv ? WvT[(int64_t)d * d_kv + c] : 0.f;
+          for (int c = 0; c < F32_STAGE_KV; ++c) w[c] = c < d_kv ? WT[(int64_t)d * d_kv + c] : 0.f;
         }
-      }
-      for (int r = grp; r < rows; r += ngrp) {
-        float sk, sv;
-        if (a.absorb) {   // attention on the raw rows
-          sk = sK[r * SP + d];
-          sv = sV[r * SP + d];
-        } else {
-          sk = 0.f;
-          sv = 0.f;
+        for (int r = grp; r < rows; r += ngrp) {
+          float acc;
+          if (a.absorb) {   // attention on the raw rows
+            acc = sX[r * F32_SP + d];
+          } else {
+            acc = 0.f;
 #pragma unroll
-          for (int c4 = 0; c4 < F32_STAGE_KV / 4; ++c4)
-            if (4 * c4 < d_kv) {   // d_kv is a multiple of 16
-              const f32x4 k4 = *(const f32x4*)&sK[r * SP + 4 * c4];
-              const f32x4 v4 = *(const f32x4*)&sV[r * SP + 4 * c4];
+            for (int c4 = 0; c4 < F32_STAGE_KV / 4; ++c4)
+              if (4 * c4 < d_kv) {   // d_kv is a multiple of 16
+                const f32x4 x4 = *(const f32x4*)&sX[r * F32_SP + 4 * c4];
 #pragma unroll
-              for (int e = 0; e < 4; ++e) {
-                sk = fmaf(k4[e], wk[4 * c4 + e], sk);
-                sv = fmaf(v4[e], wv[4 * c4 + e], sv);
+                for (int e = 0; e < 4; ++e) acc = fmaf(x4[e], w[4 * c4 + e], acc);
               }
-            }
+          }
+          const int j = start + r0 + r, tile = j >> 6, kk = j & 63;
+          if (pass == 0)
+            Kh[(((int64_t)tile * H + h) * KT + kk) * d_h + dd] = acc;
+          else
+            Vh[(((int64_t)tile * H + h) * d_h + dd) * KT + vslot(kk)] = acc;
         }
-        const int j = start + r0 + r, tile = j >> 6, kk = j & 63;
-        Kh[(((int64_t)tile * H + h) * KT + kk) * d_h + dd] = sk;
-        Vh[(((int64_t)tile * H + h) * d_h + dd) * KT + vslot(kk)] = sv;
       }
     }
     return;
   }
-  for (int q = tid; q < rows * D; q += 256) {
+  for (int q = tid; q < rows * D; q += NT) {
     const int r = q / D, d = q - r * D;
     const int j = start + r0 + r;
     const float* kr = Kr + (int64_t)j * d_kv;
@@ -568,13 +502,152 @@ __global__ __launch_bounds__(256) void k_commit_append_f32(Rs3CommitArgs a) {
   }
 }
 
+// Restored bank: rows [hdr PSTART, + PLEN) of bank 0 from the raw ring,
+// 64 per work-group.
+__global__ __launch_bounds__(256) void k_commit_append_f32(Rs3CommitArgs a) {
+  __shared__ __attribute__((aligned(16))) float sK[64 * F32_SP], sV[64 * F32_SP];
+  __shared__ int spos[64];
+  const int o = blockIdx.x;
+  const BankDev& b = *a.banks[o];
+  const int L = b.hdr[HDR_PLEN];
+  const int r0 = blockIdx.y * 64;
+  if (L < 0 || r0 >= L) return;
+  const int start = b.hdr[HDR_PSTART];
+  const int rows = min(64, L - r0);
+  if (threadIdx.x < 64) spos[threadIdx.x] = (int)threadIdx.x < rows ? b.pos[start + r0 + threadIdx.x] : 0;
+  __syncthreads();
+  append_f32<256>(a, b, o, start, r0, rows, spos, sK, sV);
+}
+
+// ---------------------------------------------------------------------------
+// Frame tables of up to CP_FMAX frames are staged in LDS (f_max <= 256 is
+// checked on the host).
+constexpr int CP_FMAX = 256;
+
+template <bool BF16>
+__global__ __launch_bounds__(CP_THREADS) void k_commit(Rs3CommitArgs a) {
+  // dynamic LDS: frame table [CP_FMAX][4] int32, then the append's row stage
+  extern __shared__ __attribute__((aligned(16))) int32_t dyn[];
+  int32_t* sfr = dyn;
+  uint8_t* stage = (uint8_t*)(dyn + 4 * CP_FMAX);
+  __shared__ CpShared sh;
+  __shared__ int spos[64];
+  const int o = blockIdx.x, y = blockIdx.y, tid = threadIdx.x;
+  const BankDev& b = *a.banks[o];
+  const int p = (int)((a.parity >> o) & 1);   // current copy of the frame state
+  const int m = a.m, n = a.n, s = a.s, mn = m * n, W = n * s;
+  const uint8_t* M = a.masks + (int64_t)o * (m * s) * W;
+  const int cpt = (mn + CP_THREADS - 1) / CP_THREADS;   // thread t owns cells c0 = t*cpt ...
+  const int c0 = tid * cpt;
+  // frame table, header words and mask cells are independent: load together
+  const int f_max = b.f_max;
+  const int32_t fr_w = tid < 4 * f_max ? b.frames[4 * f_max * p + tid] : 0;
+  int nf0 = 0, pin_end0 = 0;
+  if (tid < 64) {
+    nf0 = b.hdr[HDR_NFRAMES + HDR_COPY * p];
+    pin_end0 = b.hdr[HDR_PINEND + HDR_COPY * p];
+  }
+  uint32_t bits = 0;
+  if (s == 1 && cpt == 4 && c0 + 4 <= mn && ((((uintptr_t)M) + c0) & 3) == 0) {
+    uint32_t t = *(const uint32_t*)(M + c0);
+    t |= t >> 4;
+    t |= t >> 2;
+    t |= t >> 1;
+    bits = (t & 1u) | ((t >> 7) & 2u) | ((t >> 14) & 4u) | ((t >> 21) & 8u);
+  } else if (c0 < mn) {
+    int yy = c0 / n, x = c0 - yy * n;
+    for (int j = 0; j < cpt && c0 + j < mn; ++j) {
+      if (M[(int64_t)(yy * s) * W + x * s]) bits |= 1u << j;
+      if (++x == n) {
+        x = 0;
+        ++yy;
+      }
+    }
+  }
+  const int nc = c0 < mn ? min(cpt, mn - c0) : 0;   // cells of this thread
+  int total;
+  int before = cp_scan_bits(bits, cpt, sh.red, &total);
+  if (total < a.fall_min || total > a.fall_max) {   // dense fall-through: every cell
+    bits = nc == 32 ? ~0u : ((1u << nc) - 1u);
+    before = c0 < mn ? c0 : mn;
+    total = mn;
+  }
+  if (tid < 4 * f_max) sfr[tid] = fr_w;
+  lds_barrier();
+  if (tid < 64) {
+    int nf = nf0, pin_end = pin_end0, keys = 0;
+    const int start = place_frame_wave(b, sfr, nf0, pin_end0, total, a.t, a.pin, &nf, &pin_end, &keys);
+    if (tid == 0) {
+      sh.ok = start >= 0;
+      sh.start = start;
+      sh.len = nf;
+      if (y == 0) {   // the new state goes to the other copy
+        const int q = 1 - p;
+        if (a.kept_count) a.kept_count[o] = total;
+        if (start >= 0) {
+          b.hdr[HDR_NFRAMES + HDR_COPY * q] = nf;
+          b.hdr[HDR_PINEND + HDR_COPY * q] = pin_end;
+          b.hdr[HDR_PSTART] = start;
+          b.hdr[HDR_PLEN] = total;
+          b.hdr[HDR_NKEYS] = keys;
+        } else {
+          b.hdr[HDR_NFRAMES + HDR_COPY * q] = nf0;
+          b.hdr[HDR_PINEND + HDR_COPY * q] = pin_end0;
+          b.hdr[HDR_PLEN] = -1;
+          set_err(b.hdr, RS3_E_CAPACITY);
+        }
+      }
+    }
+  }
+  lds_barrier();
+  if (y == 0) {
+    // frame table copy 1-p: the new table, or the unchanged one (the rule
+    // returns before touching it when the frame does not fit)
+    const int nfw = sh.ok ? sh.len : nf0;
+    if (tid < 4 * nfw) b.frames[4 * f_max * (1 - p) + tid] = sfr[tid];
+    if (sh.ok) rebuild_tiles(b, sfr, sh.len, sh);
+    return;
+  }
+  if (!sh.ok) return;
+  const int r0 = 64 * (y - 1);
+  if (r0 >= total) return;
+  // kept cells of rows r0 .. r0+63 of the new frame
+  {
+    int k = before;
+    for (int j = 0; j < cpt; ++j)
+      if (bits >> j & 1) {
+        if (k >= r0 && k < r0 + 64) spos[k - r0] = c0 + j;
+        ++k;
+      }
+  }
+  lds_barrier();
+  const int start = sh.start;
+  const int rows = min(64, total - r0);
+  if (tid < rows) b.pos[start + r0 + tid] = spos[tid];
+  if constexpr (BF16)
+    append_bf16<CP_THREADS>(a, b, o, start, r0, rows, spos, (bf16_t*)stage);
+  else
+    append_f32<CP_THREADS>(a, b, o, start, r0, rows, spos, (float*)stage, (float*)stage + 64 * F32_SP);
+}
+
 }  // namespace rs3
 
 using namespace rs3;
 
+static size_t commit_stage_bytes(int dtype, int d_kv) {
+  return dtype == RS3_BF16 ? (size_t)2 * 64 * (d_kv + 8) * 2 : (size_t)2 * 64 * F32_SP * 4;
+}
+
 hipError_t rs3_commit_setup() {
-  return hipFuncSetAttribute((const void*)k_commit_append_bf16, hipFuncAttributeMaxDynamicSharedMemorySize,
-                             2 * 64 * (256 + 8) * 2);
+  hipError_t e = hipFuncSetAttribute((const void*)k_commit_append_bf16, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     (int)commit_stage_bytes(RS3_BF16, 256));
+  if (e == hipSuccess)
+    e = hipFuncSetAttribute((const void*)k_commit<true>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)(CP_FMAX * 16 + commit_stage_bytes(RS3_BF16, 256)));
+  if (e == hipSuccess)
+    e = hipFuncSetAttribute((const void*)k_commit<false>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)(CP_FMAX * 16 + commit_stage_bytes(RS3_F32, 256)));
+  return e;
 }
 
 hipError_t rs3_launch_commit(const Rs3CommitArgs& a, int dtype, int d_kv, int D, int H, int d_h,
@@ -583,30 +656,24 @@ hipError_t rs3_launch_commit(const Rs3CommitArgs& a, int dtype, int d_kv, int D,
   (void)H;
   (void)d_h;
   const int mn = a.m * a.n;
-  int f_max = 0;
-  // the frame table of every bank fits the largest f_max (checked on the host)
-  f_max = 256;
-  RS3_LAUNCH(RS3_K_COMMIT_PLACE, st, k_commit_place, dim3(a.n_obj), dim3(CP_THREADS), f_max * 16, st, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  dim3 grid(a.n_obj, (mn + 63) / 64);
+  const dim3 grid(a.n_obj, 1 + (mn + 63) / 64);
+  const size_t lds = CP_FMAX * 16 + commit_stage_bytes(dtype, d_kv);
   if (dtype == RS3_BF16)
-    RS3_LAUNCH(RS3_K_COMMIT_APPEND, st, k_commit_append_bf16, grid, dim3(256), (size_t)2 * 64 * (d_kv + 8) * 2,
-               st, a);
+    RS3_LAUNCH(RS3_K_COMMIT, st, k_commit<true>, grid, dim3(CP_THREADS), lds, st, a);
   else
-    RS3_LAUNCH(RS3_K_COMMIT_APPEND, st, k_commit_append_f32, grid, dim3(256), 0, st, a);
+    RS3_LAUNCH(RS3_K_COMMIT, st, k_commit<false>, grid, dim3(CP_THREADS), lds, st, a);
   return hipGetLastError();
 }
 
 hipError_t rs3_launch_bank_restore(const Rs3CommitArgs& a, int dtype, int d_kv, int rebuild, hipStream_t st) {
   if (rebuild) {
-    hipLaunchKernelGGL(k_bank_tiles, dim3(1), dim3(CP_THREADS), 256 * 16, st, a);
+    hipLaunchKernelGGL(k_bank_tiles, dim3(1), dim3(CP_THREADS), CP_FMAX * 16, st, a);
     return hipGetLastError();
   }
   const int mn = a.m * a.n;   // upper bound on the rows of the span
   dim3 grid(1, (mn + 63) / 64);
   if (dtype == RS3_BF16)
-    hipLaunchKernelGGL(k_commit_append_bf16, grid, dim3(256), (size_t)2 * 64 * (d_kv + 8) * 2, st, a);
+    hipLaunchKernelGGL(k_commit_append_bf16, grid, dim3(256), commit_stage_bytes(RS3_BF16, d_kv), st, a);
   else
     hipLaunchKernelGGL(k_commit_append_f32, grid, dim3(256), 0, st, a);
   return hipGetLastError();

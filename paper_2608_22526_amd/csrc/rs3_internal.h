@@ -10,16 +10,20 @@
 namespace rs3 {
 
 // ---- bank layout -----------------------------------------------------------
-// Device header words of a bank.
+// Device header words of a bank.  The frame count and pin end exist twice,
+// like the frame table: a commit of parity p (the bank's commit count mod 2,
+// kept by the host) reads copy p and writes copy 1-p, so that every
+// work-group of the commit reads the state from before it.
 enum : int {
-  HDR_NFRAMES = 0,   // resident frames
-  HDR_PINEND = 1,    // rows occupied by pinned frames
+  HDR_NFRAMES = 0,   // resident frames (copy 0; copy 1 at + HDR_COPY)
+  HDR_PINEND = 1,    // rows occupied by pinned frames (copy 0; copy 1 at + HDR_COPY)
   HDR_ERR = 2,       // sticky error word (first error wins)
   HDR_PSTART = 3,    // row where the pending append starts
   HDR_PLEN = 4,      // rows of the pending append, -1 when none
   HDR_NTILES = 5,    // entries in the resident tile list
   HDR_NKEYS = 6,     // resident rows (N)
-  HDR_WORDS = 8
+  HDR_COPY = 8,
+  HDR_WORDS = 16
 };
 
 constexpr int KT = 64;  // keys per bank tile
@@ -39,7 +43,8 @@ struct TileEnt {
 //  Vhat       : [n_tiles_cap][H][d_h][64]   keys contiguous in the slot
 //               order of vslot() (see below)
 //  hdr        : [HDR_WORDS] int32
-//  frames     : [f_max][4] int32 {start, len, t, pinned} in key order
+//  frames     : [2][f_max][4] int32 {start, len, t, pinned} in key order
+//               (copy p current for a bank of commit parity p)
 //  tiles      : [n_tiles_cap] TileEnt, ascending tile index
 struct BankDev {
   int32_t cap, f_max, n_pin, d_kv, H, d_h, dtype, n_tiles_cap;
@@ -170,6 +175,7 @@ struct Rs3CommitArgs {
   const void* WvT;
   int m, n, s, t, pin, fall_min, fall_max, n_obj, absorb;
   int from_ring;          // append: rows are already in the raw ring (bank import)
+  uint64_t parity;        // bit o: current copy of bank o's frame table and frame count
 };
 
 struct Rs3ReadoutArgs {
