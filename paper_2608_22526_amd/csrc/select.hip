@@ -19,50 +19,83 @@ constexpr int SEL_WAVES = SEL_THREADS / 64;
 constexpr int SEL_RANK_BYTES = SEL_THREADS * (8 + 4 + 4);
 
 // ---------------------------------------------------------------------------
+// Energy of a row chunk (16 bytes: 8 bf16 or 4 fp32 channels) continued in
+// ascending channel order.  Squares of bf16 and fp32 values are exact in
+// fp64, so the fused multiply-add rounds exactly like the sum of the
+// definition (acc + x*x).
 template <typename T>
-__device__ __forceinline__ void load_row_chunk(const T* p, double* v);
+__device__ __forceinline__ double energy_chunk(u32x4 w, double acc);
 
 template <>
-__device__ __forceinline__ void load_row_chunk<bf16_t>(const bf16_t* p, double* v) {
-  u32x4 w = *reinterpret_cast<const u32x4*>(p);
+__device__ __forceinline__ double energy_chunk<bf16_t>(u32x4 w, double acc) {
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    v[2 * j] = (double)__uint_as_float(w[j] << 16);
-    v[2 * j + 1] = (double)__uint_as_float(w[j] & 0xffff0000u);
+    const double lo = (double)__uint_as_float(w[j] << 16), hi = (double)__uint_as_float(w[j] & 0xffff0000u);
+    acc = fma(lo, lo, acc);
+    acc = fma(hi, hi, acc);
   }
+  return acc;
 }
 
 template <>
-__device__ __forceinline__ void load_row_chunk<float>(const float* p, double* v) {
-  const f32x4* q = reinterpret_cast<const f32x4*>(p);
-  f32x4 a = q[0], b = q[1];
+__device__ __forceinline__ double energy_chunk<float>(u32x4 w, double acc) {
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    v[j] = (double)a[j];
-    v[4 + j] = (double)b[j];
+    const double v = (double)__uint_as_float(w[j]);
+    acc = fma(v, v, acc);
   }
+  return acc;
 }
 
-// grid (ceil(mn/64), n_x), block 64.  C is a multiple of 8.  Also writes the
-// smallest and largest energy bit pattern of the block's rows to
+// grid (ceil(mn/64), n_x), block 256.  The block's 64 rows (contiguous in X)
+// are read in column blocks of EB_CH 16-byte chunks per row with coalesced
+// loads into LDS (row pitch EB_CH + 1 chunks: the per-row reads below are
+// conflict-free), then lane r of wave 0 continues row r's sum.  Also writes
+// the smallest and largest energy bit pattern of the block's rows to
 // range[xi][block] (energies are >= 0, so bit order is numeric order).
+// C*sizeof(T) is a multiple of 16.
+constexpr int EB_CH = 32;
 template <typename T>
-__global__ __launch_bounds__(64) void k_energy(const T* __restrict__ X, int64_t x_stride, int mn,
-                                                int C, double* __restrict__ e,
-                                                unsigned long long* __restrict__ range) {
-  const int xi = blockIdx.y;
-  const int i = blockIdx.x * 64 + threadIdx.x;
-  unsigned long long lo = ~0ull, hi = 0ull;
-  if (i < mn) {
-    const T* row = X + (int64_t)xi * x_stride + (int64_t)i * C;
-    double acc = 0.0;
-    for (int c = 0; c < C; c += 8) {
-      double v[8];
-      load_row_chunk<T>(row + c, v);
+__global__ __launch_bounds__(256) void k_energy(const T* __restrict__ X, int64_t x_stride, int mn,
+                                                 int C, double* __restrict__ e,
+                                                 unsigned long long* __restrict__ range) {
+  __shared__ u32x4 rows[64 * (EB_CH + 1)];
+  const int xi = blockIdx.y, r0 = blockIdx.x * 64, tid = threadIdx.x;
+  const int nrows = min(64, mn - r0);
+  const int cpr = C * (int)sizeof(T) / 16;   // chunks per row
+  const u32x4* src = (const u32x4*)(X + (int64_t)xi * x_stride + (int64_t)r0 * C);
+  double acc = 0.0;
+  for (int cb = 0; cb < cpr; cb += EB_CH) {
+    const int nch = min(EB_CH, cpr - cb);
+    // chunk q = tid + 256 k of the 64 x nch block (every load issued before
+    // the first LDS write; rows past the grid re-read its last row)
+    u32x4 v[64 * EB_CH / 256];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) acc = acc + v[j] * v[j];
+    for (int k = 0; k < 64 * EB_CH / 256; ++k) {
+      const int q = min(tid + 256 * k, 64 * nch - 1);
+      const int r = q / nch, c = q - r * nch;
+      v[k] = src[(int64_t)min(r, nrows - 1) * cpr + cb + c];
     }
-    e[(int64_t)xi * mn + i] = acc;
+#pragma unroll
+    for (int k = 0; k < 64 * EB_CH / 256; ++k) {
+      const int q = tid + 256 * k;
+      if (q < 64 * nch) {
+        const int r = q / nch, c = q - r * nch;
+        rows[r * (EB_CH + 1) + c] = v[k];
+      }
+    }
+    __syncthreads();
+    if (tid < 64) {
+      const u32x4* rw = rows + tid * (EB_CH + 1);
+#pragma unroll 4
+      for (int c = 0; c < nch; ++c) acc = energy_chunk<T>(rw[c], acc);
+    }
+    __syncthreads();
+  }
+  if (tid >= 64) return;
+  unsigned long long lo = ~0ull, hi = 0ull;
+  if (tid < nrows) {
+    e[(int64_t)xi * mn + r0 + tid] = acc;
     lo = hi = (unsigned long long)__double_as_longlong(acc);
   }
 #pragma unroll
@@ -71,7 +104,7 @@ __global__ __launch_bounds__(64) void k_energy(const T* __restrict__ X, int64_t 
     lo = ol < lo ? ol : lo;
     hi = oh > hi ? oh : hi;
   }
-  if (threadIdx.x == 0) {
+  if (tid == 0) {
     unsigned long long* r = range + 2 * ((int64_t)xi * gridDim.x + blockIdx.x);
     r[0] = lo;
     r[1] = hi;
@@ -858,10 +891,10 @@ hipError_t rs3_launch_energy(const void* X, int64_t x_stride, int n_x, int mn, i
                              double* e, unsigned long long* range, hipStream_t st) {
   dim3 grid((mn + 63) / 64, n_x);
   if (dtype == RS3_BF16)
-    RS3_LAUNCH(RS3_K_ENERGY, st, k_energy<bf16_t>, grid, dim3(64), 0, st, (const bf16_t*)X, x_stride, mn, C, e,
+    RS3_LAUNCH(RS3_K_ENERGY, st, k_energy<bf16_t>, grid, dim3(256), 0, st, (const bf16_t*)X, x_stride, mn, C, e,
                range);
   else
-    RS3_LAUNCH(RS3_K_ENERGY, st, k_energy<float>, grid, dim3(64), 0, st, (const float*)X, x_stride, mn, C, e,
+    RS3_LAUNCH(RS3_K_ENERGY, st, k_energy<float>, grid, dim3(256), 0, st, (const float*)X, x_stride, mn, C, e,
                range);
   return hipGetLastError();
 }
