@@ -31,6 +31,14 @@ __device__ __forceinline__ T gload(const T* p) {
   return *(const RS3_GLOBAL T*)p;
 }
 
+// Waits for loaded values and hands them on as values the compiler did not
+// see being loaded: a loop that uses them then carries no pending load to
+// its head, where the compiler would otherwise wait for every outstanding
+// load (the key/value DMA included) in each iteration.
+__device__ __forceinline__ void settle(int& a, uint32_t& b, uint32_t& c) {
+  asm volatile("s_waitcnt vmcnt(0)" : "+v"(a), "+v"(b), "+v"(c)::"memory");
+}
+
 // Keeps a loaded value alive on a path that does not use it, so the load is
 // issued before the branch rather than sunk past it (an early exit would
 // otherwise delay every load that only the main path uses).
@@ -344,10 +352,14 @@ __device__ __forceinline__ f32x16 attn_scores(const uint8_t* kp, const u32x4* qr
 // (b>>3) % n_qt, so all query tiles of one key group share an XCD (and its L2).
 // PROJ: the queries are projected here from X[sel] and W_q (heads of width
 // <= 64); otherwise they are read from the projected buffer Q.
-template <int DH, bool PROJ>
-__global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G, int nst) {
+// DEEP (launches of at most one work-group per CU, heads of width <= 64):
+// 8 stages and a loop over pairs of half tiles (two independent chains per
+// iteration for the one wave per SIMD); otherwise 4 stages and a loop over
+// single half tiles, which keeps the registers of several work-groups per CU.
+template <int DH, bool PROJ, bool DEEP>
+__global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
   using L = AttnLds<DH>;
-  constexpr int MAX_NST = 8;
+  constexpr int nst = DEEP ? 8 : 4;   // LDS stages
   extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];   // nst * L::STAGE bytes
   const int bid = blockIdx.x;
   const int rest = bid >> 3;
@@ -457,17 +469,11 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G, int nst) 
     c_mlo = (uint32_t)m;
     c_mhi = (uint32_t)(m >> 32);
   }
+  settle(c_tile, c_mlo, c_mhi);
   const bool qv = qrow < cnt;
   if constexpr (PROJ) attn_project<DH>(lds, tid, wave, lane, a.qscale, wv, xv, qreg);
   // i-th visited half tile
   auto half_at = [&](int i) { int v = i + rot; return ub + (v >= nh ? v - nh : v); };
-#pragma unroll
-  for (int j = 0; j < MAX_NST - 1; ++j)
-    if (j < nst - 1 && j < nh) {
-      const int v = half_at(j);
-      const int tl = __builtin_amdgcn_readlane(c_tile, (v >> 1) - cbase);
-      attn_issue<DH>(Kh, Vh, tl, v & 1, h, H, lds + j * L::STAGE, wave, doff);
-    }
 #pragma unroll
   for (int ks = 0; ks < DH / 16; ++ks)
     if (!qv) qreg[ks] = u32x4{0, 0, 0, 0};
@@ -478,93 +484,206 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G, int nst) 
   float m_run = -INFINITY, l_run = 0.f;
   const int kbase = (lane & 31) * L::KP + 16 * g;             // + ks*32
   const int vbase = L::KREG + (lane & 31) * L::VP + 16 * g;   // + dt*32*VP + q*32
-  // stage 0 must land before its scores: later stages issued = min(nst-2, nh-1)
-  wait_stages<L::PER_WAVE, MAX_NST - 2>(min(nst - 2, nh - 1));
-  stage_barrier();
-
-  // Software pipeline over the visited half tiles i = 0 .. nh-1 (stage i%NST):
-  //   iteration i: wait until stage i+1 landed; barrier (stage i-1 free);
-  //   prefetch i+nst-1 into it; S^T(i+1) on the MFMA pipe while the VALU
-  //   does the softmax of i; then O^T += V^T(i) P(i).
-  const int smask = nst - 1;
-  f32x16 sc = attn_scores<DH>(lds + kbase, qreg);
-  for (int i = 0; i < nh; ++i) {
-    const int st = i & smask;
-    const int u = half_at(i);
-    if (i + 1 < nh) wait_stages<L::PER_WAVE, MAX_NST - 2>(min(i + nst - 2, nh - 1) - (i + 1));
-    stage_barrier();
-    if (i + nst - 1 < nh) {
-      const int v = half_at(i + nst - 1);
-      if ((v >> 1) - cbase >= 64) {
-        // (unrotated splits longer than the window) slide it to the tile
-        // being computed
-        wait_vmcnt<0>();
-        cbase = u >> 1;
-        c_tile = 0;
-        if (cbase + lane < te) c_tile = gload(&tiles[cbase + lane].tile);
-        const uint64_t mm = cbase + lane < te ? gload(&tiles[cbase + lane].mask) : 0ull;
-        c_mlo = (uint32_t)mm;
-        c_mhi = (uint32_t)(mm >> 32);
-        wait_vmcnt<0>();
+  if constexpr (DEEP) {
+    // the first nst-2 half tiles; each pair iteration prefetches two more
+#pragma unroll
+    for (int j = 0; j < nst - 2; ++j)
+      if (j < nh) {
+        const int v = half_at(j);
+        const int tl = __builtin_amdgcn_readlane(c_tile, (v >> 1) - cbase);
+        attn_issue<DH>(Kh, Vh, tl, v & 1, h, H, lds + j * L::STAGE, wave, doff);
       }
-      const int tl = __builtin_amdgcn_readlane(c_tile, (v >> 1) - cbase);
-      attn_issue<DH>(Kh, Vh, tl, v & 1, h, H, lds + ((st + nst - 1) & smask) * L::STAGE, wave, doff);
-    }
-    const uint8_t* Sb = lds + st * L::STAGE;
-    const int tu = (u >> 1) - cbase;
-    const uint32_t msk = (u & 1) ? __builtin_amdgcn_readlane(c_mhi, tu) : __builtin_amdgcn_readlane(c_mlo, tu);
 
-    // S^T of the next half tile (independent of the softmax below).  In the
-    // last iteration the stage holds an earlier tile and the result is unused.
-    const f32x16 sc_next = attn_scores<DH>(lds + ((st + 1) & smask) * L::STAGE + kbase, qreg);
-
-    if (msk != 0u) {
-      if (msk != 0xffffffffu) {  // partial half tile (frame boundary)
+    // Pairs of visited half tiles (nh is even; pair i/2 sits in stages i, i+1
+    // mod nst).  Iteration i: wait until its pair landed; barrier (the
+    // previous pair's stages are free); prefetch half tiles i+nst-2, i+nst-1
+    // into them; the logits of both halves (independent MFMA chains), one
+    // softmax update over the 64 keys, then O^T += V^T P^T for both.
+    const int smask = nst - 1;
+    for (int i = 0; i < nh; i += 2) {
+      wait_stages<L::PER_WAVE, nst - 2>(min(i + nst - 2, nh) - (i + 2));
+      stage_barrier();
+      const int u0 = half_at(i), u1 = half_at(i + 1);
+#pragma unroll
+      for (int k = 0; k < 2; ++k)
+        if (i + nst - 2 + k < nh) {
+          const int v = half_at(i + nst - 2 + k);
+          if ((v >> 1) - cbase >= 64) {
+            // (unrotated splits longer than the window, whose pairs are whole
+            // tiles) slide it to the tile being computed
+            wait_vmcnt<0>();
+            cbase = u0 >> 1;
+            c_tile = 0;
+            if (cbase + lane < te) c_tile = gload(&tiles[cbase + lane].tile);
+            const uint64_t mm = cbase + lane < te ? gload(&tiles[cbase + lane].mask) : 0ull;
+            c_mlo = (uint32_t)mm;
+            c_mhi = (uint32_t)(mm >> 32);
+            settle(c_tile, c_mlo, c_mhi);
+          }
+          const int tl = __builtin_amdgcn_readlane(c_tile, (v >> 1) - cbase);
+          attn_issue<DH>(Kh, Vh, tl, v & 1, h, H, lds + ((i + nst - 2 + k) & smask) * L::STAGE, wave, doff);
+        }
+      const uint8_t* SA = lds + (i & smask) * L::STAGE;
+      const uint8_t* SB = lds + ((i + 1) & smask) * L::STAGE;
+      const int t0 = (u0 >> 1) - cbase, t1 = (u1 >> 1) - cbase;
+      const uint32_t mA = (u0 & 1) ? __builtin_amdgcn_readlane(c_mhi, t0) : __builtin_amdgcn_readlane(c_mlo, t0);
+      const uint32_t mB = (u1 & 1) ? __builtin_amdgcn_readlane(c_mhi, t1) : __builtin_amdgcn_readlane(c_mlo, t1);
+      if ((mA | mB) == 0u) continue;
+      f32x16 sA = attn_scores<DH>(SA + kbase, qreg);
+      f32x16 sB = attn_scores<DH>(SB + kbase, qreg);
+      if (mA != 0xffffffffu) {   // partial or empty half tile (frame boundary)
 #pragma unroll
         for (int r = 0; r < 16; ++r)
-          if (!(msk >> c_row(r, lane) & 1u)) sc[r] = -INFINITY;
+          if (!(mA >> c_row(r, lane) & 1u)) sA[r] = -INFINITY;
       }
-      float mx = sc[0];
+      if (mB != 0xffffffffu) {
 #pragma unroll
-      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sc[r]);
+        for (int r = 0; r < 16; ++r)
+          if (!(mB >> c_row(r, lane) & 1u)) sB[r] = -INFINITY;
+      }
+      float mx = fmaxf(sA[0], sB[0]);
+#pragma unroll
+      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(sA[r], sB[r]));
       mx = max_with_partner(mx);
-      // Lazy rescale: the reference max only moves when a half tile exceeds
-      // it by more than RESCALE_LOG2 (probabilities stay <= 2^RESCALE_LOG2);
-      // the accumulators are touched only when some lane of the wave moves.
+      // Lazy rescale: the reference max only moves when a pair exceeds it by
+      // more than RESCALE_LOG2 (probabilities stay <= 2^RESCALE_LOG2); the
+      // accumulators are touched only when some lane of the wave moves.
       const bool need = mx > m_run + RESCALE_LOG2;
       if (__any(need)) {
         const float m_new = need ? mx : m_run;
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);   // 0 on the first tile
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);   // 0 on the first pair
         l_run *= alpha;
 #pragma unroll
         for (int dt = 0; dt < DH / 32; ++dt) acc[dt] *= alpha;
         m_run = m_new;
       }
       float psum = 0.f;
-      u32x4 pk[2];
+      u32x4 pkA[2], pkB[2];
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const float p0 = __builtin_amdgcn_exp2f(sc[8 * hf + 2 * j] - m_run);
-          const float p1 = __builtin_amdgcn_exp2f(sc[8 * hf + 2 * j + 1] - m_run);
-          psum += p0 + p1;
-          pk[hf][j] = pack_bf16x2(p0, p1);
+          const float a0 = __builtin_amdgcn_exp2f(sA[8 * hf + 2 * j] - m_run);
+          const float a1 = __builtin_amdgcn_exp2f(sA[8 * hf + 2 * j + 1] - m_run);
+          const float b0 = __builtin_amdgcn_exp2f(sB[8 * hf + 2 * j] - m_run);
+          const float b1 = __builtin_amdgcn_exp2f(sB[8 * hf + 2 * j + 1] - m_run);
+          psum += (a0 + a1) + (b0 + b1);
+          pkA[hf][j] = pack_bf16x2(a0, a1);
+          pkB[hf][j] = pack_bf16x2(b0, b1);
         }
       l_run += psum;
-      // O^T += V^T P^T over the 32 keys (two 16-key MFMA steps per d block)
-      constexpr int DB = DH / 32 >= 2 ? 2 : 1;   // d blocks whose operands are fetched together
+      // O^T += V^T P^T over the 64 keys (two 16-key MFMA steps per half and d block)
 #pragma unroll
-      for (int dt = 0; dt < DH / 32; dt += DB) {
-        u32x4 va[2 * DB];
+      for (int dt = 0; dt < DH / 32; ++dt) {
+        u32x4 va[4];
 #pragma unroll
-        for (int q = 0; q < 2 * DB; ++q)
-          va[q] = *(const u32x4*)(Sb + vbase + (dt + (q >> 1)) * 32 * L::VP + (q & 1) * 32);
+        for (int q = 0; q < 2; ++q) {
+          va[q] = *(const u32x4*)(SA + vbase + dt * 32 * L::VP + q * 32);
+          va[2 + q] = *(const u32x4*)(SB + vbase + dt * 32 * L::VP + q * 32);
+        }
 #pragma unroll
-        for (int q = 0; q < 2 * DB; ++q) acc[dt + (q >> 1)] = mfma32(va[q], pk[q & 1], acc[dt + (q >> 1)]);
+        for (int q = 0; q < 2; ++q) acc[dt] = mfma32(va[q], pkA[q], acc[dt]);
+#pragma unroll
+        for (int q = 0; q < 2; ++q) acc[dt] = mfma32(va[2 + q], pkB[q], acc[dt]);
       }
     }
-    sc = sc_next;
+  } else {
+#pragma unroll
+    for (int j = 0; j < nst - 1; ++j)
+      if (j < nh) {
+        const int v = half_at(j);
+        const int tl = __builtin_amdgcn_readlane(c_tile, (v >> 1) - cbase);
+        attn_issue<DH>(Kh, Vh, tl, v & 1, h, H, lds + j * L::STAGE, wave, doff);
+      }
+
+    // stage 0 must land before its scores: later stages issued = min(nst-2, nh-1)
+    wait_stages<L::PER_WAVE, nst - 2>(min(nst - 2, nh - 1));
+    stage_barrier();
+
+    // Software pipeline over the visited half tiles i = 0 .. nh-1 (stage i%NST):
+    //   iteration i: wait until stage i+1 landed; barrier (stage i-1 free);
+    //   prefetch i+nst-1 into it; S^T(i+1) on the MFMA pipe while the VALU
+    //   does the softmax of i; then O^T += V^T(i) P(i).
+    const int smask = nst - 1;
+    f32x16 sc = attn_scores<DH>(lds + kbase, qreg);
+    for (int i = 0; i < nh; ++i) {
+      const int st = i & smask;
+      const int u = half_at(i);
+      if (i + 1 < nh) wait_stages<L::PER_WAVE, nst - 2>(min(i + nst - 2, nh - 1) - (i + 1));
+      stage_barrier();
+      if (i + nst - 1 < nh) {
+        const int v = half_at(i + nst - 1);
+        if ((v >> 1) - cbase >= 64) {
+          // (unrotated splits longer than the window) slide it to the tile
+          // being computed
+          wait_vmcnt<0>();
+          cbase = u >> 1;
+          c_tile = 0;
+          if (cbase + lane < te) c_tile = gload(&tiles[cbase + lane].tile);
+          const uint64_t mm = cbase + lane < te ? gload(&tiles[cbase + lane].mask) : 0ull;
+          c_mlo = (uint32_t)mm;
+          c_mhi = (uint32_t)(mm >> 32);
+          settle(c_tile, c_mlo, c_mhi);
+        }
+        const int tl = __builtin_amdgcn_readlane(c_tile, (v >> 1) - cbase);
+        attn_issue<DH>(Kh, Vh, tl, v & 1, h, H, lds + ((st + nst - 1) & smask) * L::STAGE, wave, doff);
+      }
+      const uint8_t* Sb = lds + st * L::STAGE;
+      const int tu = (u >> 1) - cbase;
+      const uint32_t msk = (u & 1) ? __builtin_amdgcn_readlane(c_mhi, tu) : __builtin_amdgcn_readlane(c_mlo, tu);
+
+      // S^T of the next half tile (independent of the softmax below).  In the
+      // last iteration the stage holds an earlier tile and the result is unused.
+      const f32x16 sc_next = attn_scores<DH>(lds + ((st + 1) & smask) * L::STAGE + kbase, qreg);
+
+      if (msk != 0u) {
+        if (msk != 0xffffffffu) {  // partial half tile (frame boundary)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (!(msk >> c_row(r, lane) & 1u)) sc[r] = -INFINITY;
+        }
+        float mx = sc[0];
+#pragma unroll
+        for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sc[r]);
+        mx = max_with_partner(mx);
+        // Lazy rescale: the reference max only moves when a half tile exceeds
+        // it by more than RESCALE_LOG2 (probabilities stay <= 2^RESCALE_LOG2);
+        // the accumulators are touched only when some lane of the wave moves.
+        const bool need = mx > m_run + RESCALE_LOG2;
+        if (__any(need)) {
+          const float m_new = need ? mx : m_run;
+          const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);   // 0 on the first tile
+          l_run *= alpha;
+#pragma unroll
+          for (int dt = 0; dt < DH / 32; ++dt) acc[dt] *= alpha;
+          m_run = m_new;
+        }
+        float psum = 0.f;
+        u32x4 pk[2];
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const float p0 = __builtin_amdgcn_exp2f(sc[8 * hf + 2 * j] - m_run);
+            const float p1 = __builtin_amdgcn_exp2f(sc[8 * hf + 2 * j + 1] - m_run);
+            psum += p0 + p1;
+            pk[hf][j] = pack_bf16x2(p0, p1);
+          }
+        l_run += psum;
+        // O^T += V^T P^T over the 32 keys (two 16-key MFMA steps per d block)
+        constexpr int DB = DH / 32 >= 2 ? 2 : 1;   // d blocks whose operands are fetched together
+#pragma unroll
+        for (int dt = 0; dt < DH / 32; dt += DB) {
+          u32x4 va[2 * DB];
+#pragma unroll
+          for (int q = 0; q < 2 * DB; ++q)
+            va[q] = *(const u32x4*)(Sb + vbase + (dt + (q >> 1)) * 32 * L::VP + (q & 1) * 32);
+#pragma unroll
+          for (int q = 0; q < 2 * DB; ++q) acc[dt + (q >> 1)] = mfma32(va[q], pk[q & 1], acc[dt + (q >> 1)]);
+        }
+      }
+      sc = sc_next;
+    }
   }
   const float l_tot = sum_with_partner(l_run);
   const float inv = l_tot > 0.f ? __builtin_amdgcn_rcpf(l_tot) : 0.f;
@@ -954,17 +1073,15 @@ static size_t combine_lds_bytes(int D) {
          CB_ROWS * 4;
 }
 
-// Launches of at most one work-group per CU keep 7 half tiles in flight
-// where 8 stages fit the LDS (heads of width <= 64); larger launches keep 3,
-// so that several work-groups share a CU.
+// Launches of at most one work-group per CU take the deep form of the
+// attention where its 8 stages fit the LDS (heads of width <= 64).
 constexpr int ATTN_DEEP_MAX_BLOCKS = 256;
 
-template <int DH, bool PROJ>
+template <int DH, bool PROJ, bool DEEP>
 static hipError_t launch_attn_dh(const Rs3ReadoutArgs& a, int G, int nblk, hipStream_t st) {
-  const int nst = (DH <= 64 && nblk <= ATTN_DEEP_MAX_BLOCKS) ? 8 : 4;
-  size_t lds = (size_t)nst * AttnLds<DH>::STAGE;
+  size_t lds = (size_t)(DEEP ? 8 : 4) * AttnLds<DH>::STAGE;
   if constexpr (PROJ) lds = lds > (size_t)AttnProj<DH>::BYTES ? lds : (size_t)AttnProj<DH>::BYTES;
-  RS3_LAUNCH(RS3_K_ATTN, st, (k_attn<DH, PROJ>), dim3(nblk), dim3(256), lds, st, a, G, nst);
+  RS3_LAUNCH(RS3_K_ATTN, st, (k_attn<DH, PROJ, DEEP>), dim3(nblk), dim3(256), lds, st, a, G);
   return hipGetLastError();
 }
 
@@ -981,11 +1098,16 @@ hipError_t rs3_launch_attn(const Rs3ReadoutArgs& a, hipStream_t st, bool project
   const int G = a.n_obj * a.H * a.S;
   const int nblk = 8 * a.n_qt * ((G + 7) / 8);
   if (project && !attn_projects(a)) return hipErrorInvalidValue;
+  const bool deep = nblk <= ATTN_DEEP_MAX_BLOCKS;
   switch (a.d_h) {
-    case 32: return project ? launch_attn_dh<32, true>(a, G, nblk, st) : launch_attn_dh<32, false>(a, G, nblk, st);
-    case 64: return project ? launch_attn_dh<64, true>(a, G, nblk, st) : launch_attn_dh<64, false>(a, G, nblk, st);
-    case 128: return launch_attn_dh<128, false>(a, G, nblk, st);
-    case 256: return launch_attn_dh<256, false>(a, G, nblk, st);
+    case 32:
+      if (project) return launch_attn_dh<32, true, true>(a, G, nblk, st);
+      return deep ? launch_attn_dh<32, false, true>(a, G, nblk, st) : launch_attn_dh<32, false, false>(a, G, nblk, st);
+    case 64:
+      if (project) return launch_attn_dh<64, true, true>(a, G, nblk, st);
+      return deep ? launch_attn_dh<64, false, true>(a, G, nblk, st) : launch_attn_dh<64, false, false>(a, G, nblk, st);
+    case 128: return launch_attn_dh<128, false, false>(a, G, nblk, st);
+    case 256: return launch_attn_dh<256, false, false>(a, G, nblk, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -1049,12 +1171,14 @@ hipError_t rs3_readout_setup() {
   const struct {
     const void* f;
     int bytes;
-  } attn[] = {{(const void*)k_attn<32, false>, 8 * AttnLds<32>::STAGE},
-              {(const void*)k_attn<32, true>, std::max(8 * AttnLds<32>::STAGE, AttnProj<32>::BYTES)},
-              {(const void*)k_attn<64, false>, 8 * AttnLds<64>::STAGE},
-              {(const void*)k_attn<64, true>, std::max(8 * AttnLds<64>::STAGE, AttnProj<64>::BYTES)},
-              {(const void*)k_attn<128, false>, 4 * AttnLds<128>::STAGE},
-              {(const void*)k_attn<256, false>, 4 * AttnLds<256>::STAGE}};
+  } attn[] = {{(const void*)k_attn<32, false, false>, 4 * AttnLds<32>::STAGE},
+              {(const void*)k_attn<32, false, true>, 8 * AttnLds<32>::STAGE},
+              {(const void*)k_attn<32, true, true>, std::max(8 * AttnLds<32>::STAGE, AttnProj<32>::BYTES)},
+              {(const void*)k_attn<64, false, false>, 4 * AttnLds<64>::STAGE},
+              {(const void*)k_attn<64, false, true>, 8 * AttnLds<64>::STAGE},
+              {(const void*)k_attn<64, true, true>, std::max(8 * AttnLds<64>::STAGE, AttnProj<64>::BYTES)},
+              {(const void*)k_attn<128, false, false>, 4 * AttnLds<128>::STAGE},
+              {(const void*)k_attn<256, false, false>, 4 * AttnLds<256>::STAGE}};
   for (const auto& k : attn) {
     e = hipFuncSetAttribute(k.f, hipFuncAttributeMaxDynamicSharedMemorySize, k.bytes);
     if (e != hipSuccess) return e;
