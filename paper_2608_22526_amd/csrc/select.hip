@@ -372,9 +372,16 @@ __device__ void add_object_prior_fast(const Rs3SelectArgs& a, int o, uint64_t* r
     const uint64_t any = w[0] | w[1] | w[2] | w[3];
     const unsigned long long rb = __ballot(any != 0ull);
     if (lane == 0) sh.rowbits[wave] = rb;
+    // columns with a set cell: OR over the wave first, then one LDS atomic
+    // per wave and word (atomics of every lane on one address serialise)
 #pragma unroll
-    for (int q = 0; q < FAST_W; ++q)
-      if (q < W && w[q]) atomicOr(&sh.colbits[q], (unsigned long long)w[q]);
+    for (int q = 0; q < FAST_W; ++q) {
+      if (q >= W) break;
+      uint64_t c = w[q];
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) c |= __shfl_xor(c, off, 64);
+      if (lane == 0 && c) atomicOr(&sh.colbits[q], (unsigned long long)c);
+    }
   } else {
     int y0 = 0x7fffffff, x0 = 0x7fffffff, y1 = -1, x1 = -1;
     const int npx = Hpx * Wpx;
@@ -768,24 +775,32 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(Rs3SelectArgs a) {
               ci[q] = c0 + j;
             }
           lds_barrier();
-          if (tid < cntB) {
-            const unsigned long long key = ck[tid];
-            const int idx = ci[tid];
+          // exact rank of each boundary candidate among the candidates
+          // (larger key first, equal keys by cell): wave w takes candidates
+          // w, w + 16, ...; its lanes compare against candidates lane,
+          // lane + 64, ... and a ballot counts those ranked before
+          const int wave = tid >> 6;
+          unsigned long long lk = 0;
+          int li = 0;
+          if (lane < cntB) {
+            lk = ck[lane];
+            li = ci[lane];
+          }
+          for (int i = wave; i < cntB; i += SEL_WAVES) {
+            const unsigned long long key = ck[i];
+            const int idx = ci[i];
             int rank = 0;
-            for (int q0 = 0; q0 < cntB; q0 += 8) {
-              unsigned long long kq[8];
-              int iq[8];
-#pragma unroll
-              for (int u = 0; u < 8; ++u) {
-                const int q = q0 + u < cntB ? q0 + u : q0;
-                kq[u] = ck[q];
-                iq[u] = ci[q];
+            for (int j0 = 0; j0 < cntB; j0 += 64) {
+              const int j = j0 + lane;
+              unsigned long long kq = lk;
+              int iq = li;
+              if (j0 > 0 && j < cntB) {
+                kq = ck[j];
+                iq = ci[j];
               }
-#pragma unroll
-              for (int u = 0; u < 8; ++u)
-                rank += (q0 + u < cntB) && ((kq[u] > key) || (kq[u] == key && iq[u] < idx));
+              rank += __popcll(__ballot(j < cntB && (kq > key || (kq == key && iq < idx))));
             }
-            if (rank < rem) atomicOr(&kb[idx / cpt], 1u << (idx - (idx / cpt) * cpt));
+            if (lane == 0 && rank < rem) atomicOr(&kb[idx / cpt], 1u << (idx - (idx / cpt) * cpt));
           }
           lds_barrier();
           kp |= kb[tid];
