@@ -472,6 +472,118 @@ __device__ void add_object_prior_fast(const Rs3SelectArgs& a, int o, uint64_t* r
   lds_barrier();
 }
 
+// One-wave prior for grids of at most 64 rows and stride 1 (wave 0 only, no
+// block barrier): lane y holds grid row y as FAST_W bit words.  The box is a
+// ballot over the rows and a wave OR of the columns, the tracker update is
+// wave-uniform (lane 0 writes the words back), and the column dilation
+// shifts whole rows across lanes with the same doubling steps as the row
+// dilation (rows past the grid hold 0).  Same prior as the block paths.
+__device__ void add_object_prior_wave(const Rs3SelectArgs& a, int o, uint64_t* g) {
+  const int lane = threadIdx.x & 63;
+  const int m = a.m, n = a.n, W = (n + 63) >> 6;
+  const uint8_t* M = a.masks + (int64_t)o * m * n;
+  int32_t* tr = a.track + o * RS3_TRACK_WORDS;
+  int tl[RS3_TRACK_WORDS];
+#pragma unroll
+  for (int w = 0; w < RS3_TRACK_WORDS; ++w) tl[w] = tr[w];
+  uint64_t w[FAST_W] = {0, 0, 0, 0};
+  if (lane < m) {
+    const uint8_t* rp = M + (int64_t)lane * n;
+    if ((n & 15) == 0 && (((uintptr_t)rp) & 15) == 0) {
+      for (int x0 = 0; x0 < n; x0 += 16) {
+        const u32x4 v = *(const u32x4*)(rp + x0);
+        uint32_t bits = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          uint32_t t = v[e];
+          t |= t >> 4;
+          t |= t >> 2;
+          t |= t >> 1;
+          bits |= ((t & 1u) | ((t >> 7) & 2u) | ((t >> 14) & 4u) | ((t >> 21) & 8u)) << (4 * e);
+        }
+        w[x0 >> 6] |= (uint64_t)bits << (x0 & 63);
+      }
+    } else {
+      for (int x = 0; x < n; ++x)
+        if (rp[x]) w[x >> 6] |= 1ull << (x & 63);
+    }
+  }
+  // bounding box (grid cells = pixels at stride 1)
+  const unsigned long long rb = __ballot((w[0] | w[1] | w[2] | w[3]) != 0ull);
+  int by0 = -1, bx0 = -1, by1 = -1, bx1 = -1;
+  if (rb) {
+    by0 = (int)__builtin_ctzll(rb);
+    by1 = 63 - (int)__builtin_clzll(rb);
+  }
+#pragma unroll
+  for (int q = 0; q < FAST_W; ++q) {
+    if (q >= W) break;
+    uint64_t c = w[q];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) c |= __shfl_xor(c, off, 64);
+    if (c) {
+      if (bx0 < 0) bx0 = 64 * q + (int)__builtin_ctzll(c);
+      bx1 = 64 * q + 63 - (int)__builtin_clzll(c);
+    }
+  }
+  // tracker update (the rule of tracker_update)
+  int mode = MODE_NONE, r = a.r_s;
+  if (by1 >= 0) {
+    mode = a.seed_box ? MODE_BOX : MODE_MASK;
+    tl[0] = by0;
+    tl[1] = bx0;
+    tl[2] = by1;
+    tl[3] = bx1;
+    tl[4] = 0;
+    tl[5] = 1;
+  } else {
+    const int d = tl[4] + 1;
+    tl[4] = d;
+    if (tl[5]) {
+      mode = MODE_BOX;
+      by0 = tl[0];
+      bx0 = tl[1];
+      by1 = tl[2];
+      bx1 = tl[3];
+      r = a.r_s + min(d, a.c);
+    }
+  }
+  if (lane == 0)
+#pragma unroll
+    for (int q = 0; q < RS3_TRACK_WORDS; ++q) tr[q] = tl[q];
+  if (mode == MODE_BOX) {
+    const int ya = max(0, by0 - r), yb = min(m - 1, by1 + r);
+    const int xa = max(0, bx0 - r), xb = min(n - 1, bx1 + r);
+    if (lane < m && lane >= ya && lane <= yb) {
+#pragma unroll
+      for (int q = 0; q < FAST_W; ++q) {
+        const int lo = max(xa, 64 * q), hi = min(xb, 64 * q + 63);
+        if (lo <= hi) {
+          const int len = hi - lo + 1;
+          g[q] |= (len == 64 ? ~0ull : ((1ull << len) - 1ull)) << (lo - 64 * q);
+        }
+      }
+    }
+  } else if (mode == MODE_MASK) {
+    row_dilate_regs(w, W, n, min(r, n));
+    const int rr = min(r, 63);   // rows are at most 64 apart
+    int done = 0;
+    while (done < rr) {
+      const int step = min(done + 1, rr - done);   // no gaps: step <= done + 1
+#pragma unroll
+      for (int q = 0; q < FAST_W; ++q) {
+        if (q >= W) break;
+        const uint64_t up = __shfl(w[q], lane - step, 64), dn = __shfl(w[q], lane + step, 64);
+        w[q] |= (lane - step >= 0 ? up : 0ull) | (lane + step < 64 ? dn : 0ull);
+      }
+      done += step;
+    }
+    if (lane < m)
+#pragma unroll
+      for (int q = 0; q < FAST_W; ++q) g[q] |= w[q];
+  }
+}
+
 // Adds one object's prior into U (LDS byte map of the group).  bufA/bufB are
 // scratch areas of at least max(mn, 8*m*W) bytes.
 __device__ void add_object_prior(const Rs3SelectArgs& a, int o, uint8_t* U, uint8_t* bufA, uint8_t* bufB,
@@ -664,7 +776,22 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(Rs3SelectArgs a) {
   const int W = (a.n + 63) >> 6;
   const bool fast = a.m <= SEL_THREADS && W <= FAST_W;
   uint64_t* Gs = reinterpret_cast<uint64_t*>(base);   // fast path: group prior rows [m][W]
-  if (fast) {
+  if (fast && a.m <= 64 && a.s == 1) {
+    // one wave: lane y owns grid row y
+    if (tid < 64) {
+      uint64_t gw[FAST_W] = {0, 0, 0, 0};
+      if (a.union_objects) {
+        for (int o = 0; o < a.n_obj; ++o) add_object_prior_wave(a, o, gw);
+      } else {
+        add_object_prior_wave(a, g, gw);
+      }
+      if (tid < a.m)
+#pragma unroll
+        for (int q = 0; q < FAST_W; ++q)
+          if (q < W) Gs[tid * W + q] = gw[q];
+    }
+    lds_barrier();
+  } else if (fast) {
     uint64_t* rows = reinterpret_cast<uint64_t*>(tmp);
     uint64_t gw[FAST_W] = {0, 0, 0, 0};
     lds_barrier();
