@@ -1,18 +1,20 @@
 // Store-sparse commit (Sec. 3.2, Eq. 8; sparse write of Algorithm 1).
 //
-// k_commit : grid (n_obj, 1 + ceil(mn/64)), block 1024.  Every work-group of
-//            an object compacts the mask to the ascending kept list (ordered
-//            block scan, dense fall-through) and runs the placement rule
-//            (documented in rs3.h; one wave) on its own LDS copy of the frame
-//            table as it was before this commit (copy p of the double-
-//            buffered table), so all of them know the new frame's start row.
-//            Work-group 0 writes the new state to copy 1-p, the key count and
-//            the list of resident 64-row tiles with their row masks; work-
-//            group 1 + b appends kept rows 64b .. 64b+63: the raw K/V rows
-//            into the ring, their cells into `pos`, and their projections
-//            K^ = K W_k, V^ = V W_v into the tile-blocked attention layouts
-//            (bf16 MFMA with fp32 accumulation, or fp32 FMA loops; the raw
-//            rows re-laid in absorbed mode).
+// k_commit : grid (n_obj, 1 + ceil(mn/R)), block 1024, R = rows_per_wg.
+//            Every work-group of an object compacts the mask to the ascending
+//            kept list (ordered block scan, dense fall-through) and runs the
+//            placement rule (documented in rs3.h; one wave) on its own LDS
+//            copy of the frame table as it was before this commit (copy p of
+//            the double-buffered table), so all of them know the new frame's
+//            start row.  Work-group 0 writes the new state to copy 1-p, the
+//            key count and the list of resident 64-row tiles with their row
+//            masks; work-group 1 + b appends kept rows Rb .. Rb+R-1, 64 per
+//            round (R = 64 unless a call would launch far more work-groups
+//            than CUs): the raw K/V rows into the ring, their cells into
+//            `pos`, and their projections K^ = K W_k, V^ = V W_v into the
+//            tile-blocked attention layouts (bf16 MFMA with fp32
+//            accumulation, or fp32 FMA loops; the raw rows re-laid in
+//            absorbed mode).
 // k_commit_append_* / k_bank_tiles : the same append and tile rebuild for a
 //            bank restored from a snapshot (rows already in the ring).
 #include "rs3_internal.h"
@@ -609,25 +611,27 @@ __global__ __launch_bounds__(CP_THREADS) void k_commit(Rs3CommitArgs a) {
     return;
   }
   if (!sh.ok) return;
-  const int r0 = 64 * (y - 1);
-  if (r0 >= total) return;
-  // kept cells of rows r0 .. r0+63 of the new frame
-  {
-    int k = before;
-    for (int j = 0; j < cpt; ++j)
-      if (bits >> j & 1) {
-        if (k >= r0 && k < r0 + 64) spos[k - r0] = c0 + j;
-        ++k;
-      }
-  }
-  lds_barrier();
+  // kept rows [(y-1)*rows_per_wg, y*rows_per_wg) of the new frame, 64 per round
   const int start = sh.start;
-  const int rows = min(64, total - r0);
-  if (tid < rows) b.pos[start + r0 + tid] = spos[tid];
-  if constexpr (BF16)
-    append_bf16<CP_THREADS>(a, b, o, start, r0, rows, spos, (bf16_t*)stage);
-  else
-    append_f32<CP_THREADS>(a, b, o, start, r0, rows, spos, (float*)stage, (float*)stage + 64 * F32_SP);
+  const int r_end = min(total, y * a.rows_per_wg);
+  for (int r0 = (y - 1) * a.rows_per_wg; r0 < r_end; r0 += 64) {
+    {   // kept cells of rows r0 .. r0+63
+      int k = before;
+      for (int j = 0; j < cpt; ++j)
+        if (bits >> j & 1) {
+          if (k >= r0 && k < r0 + 64) spos[k - r0] = c0 + j;
+          ++k;
+        }
+    }
+    lds_barrier();
+    const int rows = min(64, total - r0);
+    if (tid < rows) b.pos[start + r0 + tid] = spos[tid];
+    if constexpr (BF16)
+      append_bf16<CP_THREADS>(a, b, o, start, r0, rows, spos, (bf16_t*)stage);
+    else
+      append_f32<CP_THREADS>(a, b, o, start, r0, rows, spos, (float*)stage, (float*)stage + 64 * F32_SP);
+    __syncthreads();   // the next round rewrites spos and the row stage
+  }
 }
 
 }  // namespace rs3
@@ -656,12 +660,20 @@ hipError_t rs3_launch_commit(const Rs3CommitArgs& a, int dtype, int d_kv, int D,
   (void)H;
   (void)d_h;
   const int mn = a.m * a.n;
-  const dim3 grid(a.n_obj, 1 + (mn + 63) / 64);
+  // 64 kept rows per work-group, or a multiple of 64 (appended in rounds) so
+  // that a call launches about CP_MAX_WGS work-groups: every work-group scans
+  // the whole mask, which many-object calls would otherwise repeat thousands
+  // of times
+  constexpr int CP_MAX_WGS = 1024;
+  const int64_t blocks64 = (int64_t)a.n_obj * ((mn + 63) / 64);
+  Rs3CommitArgs b = a;
+  b.rows_per_wg = 64 * (int)((blocks64 + CP_MAX_WGS - 1) / CP_MAX_WGS);
+  const dim3 grid(a.n_obj, 1 + (mn + b.rows_per_wg - 1) / b.rows_per_wg);
   const size_t lds = CP_FMAX * 16 + commit_stage_bytes(dtype, d_kv);
   if (dtype == RS3_BF16)
-    RS3_LAUNCH(RS3_K_COMMIT, st, k_commit<true>, grid, dim3(CP_THREADS), lds, st, a);
+    RS3_LAUNCH(RS3_K_COMMIT, st, k_commit<true>, grid, dim3(CP_THREADS), lds, st, b);
   else
-    RS3_LAUNCH(RS3_K_COMMIT, st, k_commit<false>, grid, dim3(CP_THREADS), lds, st, a);
+    RS3_LAUNCH(RS3_K_COMMIT, st, k_commit<false>, grid, dim3(CP_THREADS), lds, st, b);
   return hipGetLastError();
 }
 

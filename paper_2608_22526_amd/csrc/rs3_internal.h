@@ -176,6 +176,7 @@ struct Rs3CommitArgs {
   int m, n, s, t, pin, fall_min, fall_max, n_obj, absorb;
   int from_ring;          // append: rows are already in the raw ring (bank import)
   uint64_t parity;        // bit o: current copy of bank o's frame table and frame count
+  int rows_per_wg;        // commit: kept rows appended per work-group (a multiple of 64)
 };
 
 struct Rs3ReadoutArgs {
