@@ -12,13 +12,17 @@ Modules:
             (Sec. 3.1, Eqs. 1, 2 and 5; Algorithm 1)
   select    token energy and the read keep-set (Sec. 3.1, Eq. 4)
   readout   the sparse memory readout with scatter (Sec. 3.1, Eq. 6)
+  rope      rotary positions on the gathered subset (Sec. 3.1, Eq. 7)
   bank      write compaction and the ring memory bank (Sec. 3.2, Eq. 8)
 
 Parity unpinned: absolute readout values at the workload sizes (the paper
 prints no tensors and its weights are not available); every other function is
-pinned by the tests in tests/test_oracle_*.py.
+pinned by the tests in tests/test_oracle_*.py.  The axial rotary table is a
+reading (the paper gives only its shape); its stated form is pinned, its
+choice is not.
 """
 from .geometry import Track, bbox, down_s, down_s_box, fill_box, dilate, prior_object  # noqa: F401
 from .select import energy, topk_keep, select_queries  # noqa: F401
+from .rope import axial_table, table_from_pairs, rotate, rotate_heads  # noqa: F401
 from .readout import project_bank, attention_weights, readout, readout_dense, attend  # noqa: F401
 from .bank import compact, RingBank, FrameListBank, RS3_OK, RS3_E_INVALID, RS3_E_CAPACITY  # noqa: F401

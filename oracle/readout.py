@@ -15,6 +15,10 @@ Readings:
   * with an empty bank or an empty keep-set, Y = X.
 At keep-all the gather and scatter are identities and the readout equals the
 dense layer (end of Sec. 3.1), which `readout_dense` computes independently.
+
+With a rotary table (Eq. 7, readings in `rope`), each kept query is turned by
+the table row of its own cell and each bank key by the row of the cell stored
+with it; `readout_dense` turns its rows by the cells it is given.
 """
 from __future__ import annotations
 
@@ -22,11 +26,22 @@ import math
 
 import numpy as np
 
+from .rope import rotate_heads
+
 
 def project_bank(Kraw: np.ndarray, Vraw: np.ndarray, Wk: np.ndarray, Wv: np.ndarray):
     """Bank keys and values in the attention space: K^ = K W_k, V^ = V W_v."""
     return (np.asarray(Kraw, np.float64) @ np.asarray(Wk, np.float64),
             np.asarray(Vraw, np.float64) @ np.asarray(Wv, np.float64))
+
+
+def rotate_keys(Kh: np.ndarray, rope, kpos, H: int) -> np.ndarray:
+    """Projected bank keys turned by the table rows of their stored cells
+    (unchanged without a table)."""
+    if rope is None:
+        return Kh
+    kpos = np.asarray(kpos, dtype=np.int64)
+    return np.stack([rotate_heads(Kh[j], rope[kpos[j]], H) for j in range(Kh.shape[0])]) if len(kpos) else Kh
 
 
 def attention_weights(q_h: np.ndarray, Kh_h: np.ndarray) -> np.ndarray:
@@ -37,9 +52,11 @@ def attention_weights(q_h: np.ndarray, Kh_h: np.ndarray) -> np.ndarray:
     return w / w.sum()
 
 
-def readout(X, sel, Kraw, Vraw, Wq, Wk, Wv, Wo, H: int) -> np.ndarray:
+def readout(X, sel, Kraw, Vraw, Wq, Wk, Wv, Wo, H: int, rope=None, kpos=None) -> np.ndarray:
     """Row-by-row readout.  X: [mn][C]; sel: kept cell indices; Kraw/Vraw:
-    [N][d_kv] bank rows in key order.  Returns float64 [mn][C]."""
+    [N][d_kv] bank rows in key order.  rope: optional complex table
+    [mn][d_h/2] with kpos [N], the cell of each bank row.  Returns float64
+    [mn][C]."""
     X = np.asarray(X, np.float64)
     Wq, Wo = np.asarray(Wq, np.float64), np.asarray(Wo, np.float64)
     Y = X.copy()
@@ -47,10 +64,13 @@ def readout(X, sel, Kraw, Vraw, Wq, Wk, Wv, Wo, H: int) -> np.ndarray:
     if N == 0:
         return Y
     Kh, Vh = project_bank(Kraw, Vraw, Wk, Wv)
+    Kh = rotate_keys(Kh, rope, kpos, H)
     D = Wq.shape[1]
     d_h = D // H
     for i in np.asarray(sel, dtype=np.int64):
         q = X[i] @ Wq
+        if rope is not None:
+            q = rotate_heads(q, rope[i], H)   # f~ = f[K_r] (Eq. 7)
         o = np.zeros(D)
         for h in range(H):
             cols = slice(h * d_h, (h + 1) * d_h)
@@ -60,15 +80,21 @@ def readout(X, sel, Kraw, Vraw, Wq, Wk, Wv, Wo, H: int) -> np.ndarray:
     return Y
 
 
-def readout_dense(X, Kraw, Vraw, Wq, Wk, Wv, Wo, H: int) -> np.ndarray:
-    """Unpruned layer on all mn rows as whole-matrix products (no gather or
-    scatter): Y = X + softmax(Q K^T / sqrt(d_h)) V W_o per head."""
+def readout_dense(X, Kraw, Vraw, Wq, Wk, Wv, Wo, H: int, rope=None, kpos=None, qpos=None) -> np.ndarray:
+    """Unpruned layer on all rows of X as whole-matrix products (no gather or
+    scatter): Y = X + softmax(Q K^T / sqrt(d_h)) V W_o per head.  With a
+    rotary table, row r of X is turned by rope[qpos[r]] (qpos defaults to
+    0..rows-1, the cells of a whole grid)."""
     X = np.asarray(X, np.float64)
     N = np.asarray(Kraw).shape[0]
     if N == 0:
         return X.copy()
     Kh, Vh = project_bank(Kraw, Vraw, Wk, Wv)
+    Kh = rotate_keys(Kh, rope, kpos, H)
     Q = X @ np.asarray(Wq, np.float64)
+    if rope is not None:
+        qpos = np.arange(X.shape[0]) if qpos is None else np.asarray(qpos, dtype=np.int64)
+        Q = np.stack([rotate_heads(Q[r], rope[qpos[r]], H) for r in range(Q.shape[0])])
     D = Q.shape[1]
     d_h = D // H
     O = np.zeros_like(Q)
