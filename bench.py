@@ -43,16 +43,17 @@ def _describe(cfg) -> str:
 # ---------------------------------------------------------------------------
 # CPU baseline (child process, fp64 oracle, one thread)
 # ---------------------------------------------------------------------------
-def cpu_child(workload: str, frames: int):
+def cpu_child(workload: str, frames: int, rope_theta: float = 0.0):
     import numpy as np  # noqa: F401  (threads pinned by the parent's env)
     sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import oracle
     from harness import OraclePipeline
     from workloads import CONFIGS, make_frame, make_sequence, make_weights
     cfg = CONFIGS[workload]
     n_pre = cfg.f_max
     seq = make_sequence(cfg, n_frames=n_pre + frames + 1)
     W = make_weights(cfg)
-    orc = OraclePipeline(cfg, W)
+    orc = OraclePipeline(cfg, W, rope=oracle.axial_table(cfg.m, cfg.n, cfg.d_h, rope_theta) if rope_theta else None)
     for t in range(n_pre):
         fr = make_frame(cfg, t)
         orc.commit(fr.Kmem, fr.Vmem, seq.masks[t], t, t < cfg.n_pin)
@@ -68,13 +69,13 @@ def cpu_child(workload: str, frames: int):
     print(json.dumps({"seconds": dt, "frames": frames, "prefill": n_pre}))
 
 
-def cpu_baseline(workload: str, frames: int):
+def cpu_baseline(workload: str, frames: int, rope_theta: float = 0.0):
     env = dict(os.environ)
     for v in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS", "NUMEXPR_NUM_THREADS"):
         env[v] = "1"
     env["HIP_VISIBLE_DEVICES"] = ""
     p = subprocess.run([sys.executable, os.path.abspath(__file__), "--cpu-child", "--workload", workload,
-                        "--cpu-frames", str(frames)], stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True,
+                        "--cpu-frames", str(frames), "--rope", str(rope_theta)], stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True,
                        env=env, timeout=600)
     if p.returncode != 0:
         return {"value": None, "unit": "frames/s", "cores": 1, "kind": "oracle", "error": p.stderr[-500:]}
@@ -164,11 +165,11 @@ def gpu_run(args):
     seq = make_sequence(cfg, n_frames=n_pre + N_DISTINCT)
     W = make_weights(cfg)
     k_all = [max(ks) for ks in seq.k]
-    absorb = _absorb(cfg, args.layer)
+    absorb = _absorb(cfg, args.layer) and not args.rope
     sess = Session(m=cfg.m, n=cfg.n, s=cfg.s, C=cfg.C, H=cfg.H, d_kv=cfg.d_kv, dtype=cfg.dtype,
                    n_obj=cfg.n_obj, shared_x=cfg.shared_x, union_objects=cfg.union_objects, cap=cfg.cap,
                    f_max=cfg.f_max, n_pin=cfg.n_pin, weights=W, r_s=cfg.r_s, c=cfg.c, max_sel=max(k_all),
-                   n_splits=args.splits, absorb=absorb)
+                   n_splits=args.splits, absorb=absorb, rope_theta=args.rope or None)
     # resident inputs
     frames = []
     for t in range(n_pre + N_DISTINCT):
@@ -300,7 +301,8 @@ def gpu_run(args):
                    "bank_frames": cfg.f_max, "d_model": cfg.C, "heads": cfg.H, "d_head": cfg.d_h,
                    "d_kv": cfg.d_kv, "eager_launches": True, "streams": args.streams, "readout": "in place" if in_place else "out of place",
                    "attention": ("absorbed: one head of width d_kv=%d on the raw bank rows" % cfg.d_kv) if absorb
-                   else ("projected: %d head(s) of width %d" % (cfg.H, cfg.d_h))},
+                   else ("projected: %d head(s) of width %d%s" % (cfg.H, cfg.d_h,
+                         ", axial rotary table (theta %g) on queries and keys" % args.rope if args.rope else ""))},
         "roofline": {"bound": "mfma", "achieved": achieved_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved_tflops / PEAK_BF16_TFLOPS,
                      "traffic": traffic,
@@ -376,7 +378,7 @@ def _algo_bytes(cfg, absorb, rec):
     }
 
 
-def run_workload(cfg, *, absorb, steps, warmup, commit=True, prefill=None, splits=0):
+def run_workload(cfg, *, absorb, steps, warmup, commit=True, prefill=None, splits=0, rope_theta=None):
     """Steady-state frames of `cfg` (objects beyond 64 run as several calls per
     frame).  Returns frame timing percentiles, per-kernel times and rates."""
     import numpy as np
@@ -396,7 +398,7 @@ def run_workload(cfg, *, absorb, steps, warmup, commit=True, prefill=None, split
     sessions = [Session(m=cfg.m, n=cfg.n, s=cfg.s, C=cfg.C, H=cfg.H, d_kv=cfg.d_kv, dtype=cfg.dtype, n_obj=no,
                         shared_x=cfg.shared_x, union_objects=cfg.union_objects, cap=cfg.cap, f_max=cfg.f_max,
                         n_pin=cfg.n_pin, weights=W, r_s=cfg.r_s, c=cfg.c, max_sel=max_sel, n_splits=splits,
-                        absorb=absorb) for _, no in chunks]
+                        absorb=absorb, rope_theta=rope_theta) for _, no in chunks]
     frames = []
     for t in range(n_gen):
         fr = make_frame(cfg, t)
@@ -525,6 +527,12 @@ def report(args):
             r = run_workload(cfg, absorb=mode == "absorbed", steps=args.steps, warmup=args.warmup)
             out["%s/%s" % (name, mode)] = r
             log("%s/%s" % (name, mode), r)
+    # rotary positions on the gathered subset (Eq. 7): projected layers only
+    for name in ("sam2_single", "highres"):
+        cfg = CONFIGS[name]
+        r = run_workload(cfg, absorb=False, steps=args.steps, warmup=args.warmup, rope_theta=10000.0)
+        out["%s/projected+rope" % name] = r
+        log("%s/projected+rope" % name, r)
     hr = CONFIGS["highres"]
     for rho in ("0.1", "0.25", "0.5", "1.0"):
         cfg = replace(hr, rho=float(rho))
@@ -557,6 +565,8 @@ def main():
                          "(a stall of tens of ms) after the first thousand-odd launches of a process")
     ap.add_argument("--workload", default="sam2_single")
     ap.add_argument("--splits", type=int, default=0)
+    ap.add_argument("--rope", type=float, default=0.0,
+                    help="axial rotary table with this theta on a projected layer (0 = none)")
     ap.add_argument("--layer", choices=["auto", "projected", "absorbed"], default="auto")
     ap.add_argument("--streams", type=int, choices=[1, 2], default=1,
                     help="2: frame t's commit overlaps frame t+1's selection on a second stream")
@@ -569,8 +579,12 @@ def main():
     ap.add_argument("--report", default="", help="write the full measurement report (JSON) to this path")
     args = ap.parse_args()
     if args.cpu_child:
-        cpu_child(args.workload, args.cpu_frames)
+        cpu_child(args.workload, args.cpu_frames, args.rope)
         return
+    if args.rope and args.layer == "absorbed":
+        print("--rope needs a projected layer: the rotation sits between the projections that absorption "
+              "folds together", file=sys.stderr)
+        sys.exit(2)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one MI355X: the path runs on a single GPU (objects or bank frames would be "
@@ -582,7 +596,7 @@ def main():
         return
     out = gpu_run(args)
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_frames)
+        out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_frames, args.rope)
     print(json.dumps(out))
 
 

@@ -112,6 +112,31 @@ rs3_status rs3_layer_create(int32_t C, int32_t H, int32_t d_kv, rs3_dtype dt, in
                             const void* Wo, rs3_layer** out);
 void rs3_layer_destroy(rs3_layer* L);
 
+/* ---- rotary positions on the gathered subset (Sec. 3.1, Eq. 7) ------------
+ * Attaches a rotary table to a projected layer (absorb = 0) whose attention
+ * then turns each head's channel pairs (2p, 2p+1), read as the complex number
+ * x_2p + i x_2p+1, by the table row of the token's grid cell: a selected query
+ * by the row of the cell it was gathered from (f~ = f[K_r], not the first
+ * |K_r| rows), a bank key by the row of the cell it was kept from.  Values
+ * are not turned.  The heads share the table, which has d_h/2 columns.  The
+ * grid of every later rs3_readout and rs3_commit with this layer must be
+ * m x n (else RS3_E_INVALID).  Keys are turned once, when they are committed
+ * (or restored by rs3_bank_import), so the table must be set before the
+ * first bank is created from the layer: with a bank alive the call returns
+ * RS3_E_INVALID and changes nothing.  Both calls are synchronous.
+ *
+ * rs3_layer_set_rope: table [host] fp32 [m*n][d_h/2][2] holding (cos, sin)
+ *   of each factor, copied to the device; table = NULL with m = n = 0
+ *   removes the table.
+ * rs3_layer_set_rope_axial: builds the axial two-dimensional table on the
+ *   device: for p < d_h/4 the angle of cell (row, col) = (i / n, i % n) is
+ *   col * theta^(-4p/d_h), for the other d_h/4 factors it is
+ *   row * theta^(-4(p - d_h/4)/d_h) (computed in fp64, stored as fp32).
+ *   Requires theta > 1 and d_h divisible by 4.
+ * Both require 1 <= m*n <= RS3_MAX_MN and an even d_h. */
+rs3_status rs3_layer_set_rope(rs3_layer* L, int32_t m, int32_t n, const float* table /*[host]*/);
+rs3_status rs3_layer_set_rope_axial(rs3_layer* L, int32_t m, int32_t n, double theta);
+
 /* ---- bank (Sec. 3.2; placement rule below) --------------------------------
  * A ring of `cap` token rows holding at most `f_max` frames, of which the
  * first commits (at most n_pin, all before any unpinned commit) may be pinned.

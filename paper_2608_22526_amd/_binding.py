@@ -46,6 +46,8 @@ _SIGS = {
     "rs3_track_import": (c_i32, [c_vp, c_vp]),
     "rs3_layer_create": (c_i32, [c_i32, c_i32, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp, c_vp, ctypes.POINTER(c_vp)]),
     "rs3_layer_destroy": (None, [c_vp]),
+    "rs3_layer_set_rope": (c_i32, [c_vp, c_i32, c_i32, c_vp]),
+    "rs3_layer_set_rope_axial": (c_i32, [c_vp, c_i32, c_i32, ctypes.c_double]),
     "rs3_bank_create": (c_i32, [c_vp, c_i32, c_i32, c_i32, ctypes.POINTER(c_vp)]),
     "rs3_bank_destroy": (None, [c_vp]),
     "rs3_bank_export": (c_i32, [c_vp, c_vp, c_vp, c_vp, c_vp, c_vp]),
@@ -153,6 +155,16 @@ class Layer:
         _check(lib().rs3_layer_create(C, H, d_kv, dtype, int(absorb), *(a.ctypes.data for a in arrs),
                                       ctypes.byref(h)), "rs3_layer_create")
         self.h, self.C, self.H, self.d_kv, self.dtype, self.absorb = h, C, H, d_kv, dtype, bool(absorb)
+
+    def set_rope(self, m: int, n: int, table=None):
+        """Attach a rotary table: float32 host array [m*n][d_h/2][2] of
+        (cos, sin) pairs; table=None with m = n = 0 removes it."""
+        t = None if table is None else np.ascontiguousarray(table, dtype=np.float32)
+        _check(lib().rs3_layer_set_rope(self.h, m, n, None if t is None else t.ctypes.data), "rs3_layer_set_rope")
+
+    def set_rope_axial(self, m: int, n: int, theta: float):
+        """Attach the axial rotary table built on the device."""
+        _check(lib().rs3_layer_set_rope_axial(self.h, m, n, float(theta)), "rs3_layer_set_rope_axial")
 
     def __del__(self):
         if getattr(self, "h", None) and _lib is not None:

@@ -17,7 +17,8 @@ struct rs3_track {
 };
 
 struct rs3_layer {
-  LayerDev dev;  // host copy holding device pointers
+  LayerDev dev;         // host copy holding device pointers
+  mutable int n_banks;  // banks created from the layer and not yet destroyed
 };
 
 struct rs3_bank {
@@ -260,10 +261,76 @@ rs3_status rs3_layer_create(int32_t C, int32_t H, int32_t d_kv, rs3_dtype dt, in
 
 void rs3_layer_destroy(rs3_layer* L) {
   if (!L) return;
-  void* w[4] = {L->dev.WqT, L->dev.WkT, L->dev.WvT, L->dev.WoT};
+  void* w[5] = {L->dev.WqT, L->dev.WkT, L->dev.WvT, L->dev.WoT, L->dev.rope};
   for (void* p : w)
     if (p) (void)hipFree(p);
   delete L;
+}
+
+// ---- rotary table ------------------------------------------------------------
+namespace {
+
+rs3_status rope_args_ok(const rs3_layer* L, int32_t m, int32_t n) {
+  if (!L || L->dev.absorb || L->n_banks > 0 || L->dev.dah % 2 != 0) return RS3_E_INVALID;
+  if (m <= 0 || n <= 0 || (int64_t)m * n > RS3_MAX_MN) return RS3_E_INVALID;
+  return RS3_OK;
+}
+
+// Replaces the layer's table by a fresh uninitialised one of m x n rows.
+rs3_status rope_alloc(rs3_layer* L, int32_t m, int32_t n, float** out) {
+  const size_t bytes = (size_t)m * n * L->dev.dah * 4;   // d_h/2 pairs of two floats
+  float* t = nullptr;
+  hipError_t e = hipMalloc((void**)&t, bytes);
+  if (e != hipSuccess) return map_err(e);
+  *out = t;
+  return RS3_OK;
+}
+
+void rope_install(rs3_layer* L, float* t, int32_t m, int32_t n) {
+  if (L->dev.rope) (void)hipFree(L->dev.rope);
+  L->dev.rope = t;
+  L->dev.rope_m = m;
+  L->dev.rope_n = n;
+}
+
+}  // namespace
+
+rs3_status rs3_layer_set_rope(rs3_layer* L, int32_t m, int32_t n, const float* table) {
+  if (!L) return RS3_E_INVALID;
+  if (!table) {
+    if (m != 0 || n != 0 || L->dev.absorb || L->n_banks > 0) return RS3_E_INVALID;
+    rope_install(L, nullptr, 0, 0);
+    return RS3_OK;
+  }
+  rs3_status st = rope_args_ok(L, m, n);
+  if (st != RS3_OK) return st;
+  float* t = nullptr;
+  st = rope_alloc(L, m, n, &t);
+  if (st != RS3_OK) return st;
+  hipError_t e = hipMemcpy(t, table, (size_t)m * n * L->dev.dah * 4, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipFree(t);
+    return map_err(e);
+  }
+  rope_install(L, t, m, n);
+  return RS3_OK;
+}
+
+rs3_status rs3_layer_set_rope_axial(rs3_layer* L, int32_t m, int32_t n, double theta) {
+  rs3_status st = rope_args_ok(L, m, n);
+  if (st != RS3_OK) return st;
+  if (!(theta > 1.0) || L->dev.dah % 4 != 0) return RS3_E_INVALID;
+  float* t = nullptr;
+  st = rope_alloc(L, m, n, &t);
+  if (st != RS3_OK) return st;
+  hipError_t e = rs3_launch_rope_axial(t, m, n, L->dev.dah, theta, nullptr);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) {
+    (void)hipFree(t);
+    return map_err(e);
+  }
+  rope_install(L, t, m, n);
+  return RS3_OK;
 }
 
 // ---- bank ------------------------------------------------------------------
@@ -323,12 +390,14 @@ rs3_status rs3_bank_create(const rs3_layer* L, int32_t cap, int32_t f_max, int32
     delete b;
     return map_err(e);
   }
+  L->n_banks++;
   *out = b;
   return RS3_OK;
 }
 
 void rs3_bank_destroy(rs3_bank* b) {
   if (!b) return;
+  b->L->n_banks--;
   BankDev& h = b->host;
   void* ptrs[] = {h.Kraw, h.Vraw, h.pos, h.Khat, h.Vhat, h.hdr, h.frames, h.tiles, b->d_desc};
   for (void* p : ptrs)
@@ -441,6 +510,8 @@ rs3_status rs3_bank_import(rs3_bank* b, const int32_t* hdr, const int32_t* frame
   a.WkT = L->dev.WkT;
   a.WvT = L->dev.WvT;
   a.absorb = L->dev.absorb;
+  a.rope = L->dev.rope;
+  a.rope_mn = L->dev.rope_m * L->dev.rope_n;
   a.n_obj = 1;
   a.m = 1;
   a.s = 1;
@@ -704,6 +775,7 @@ rs3_status rs3_readout(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, con
     if (y_fp32) return RS3_E_INVALID;
     if (n_obj > 1 && x_obj_stride != y_obj_stride) return RS3_E_INVALID;
   }
+  if (ld.rope && (g->m != ld.rope_m || g->n != ld.rope_n)) return RS3_E_INVALID;
   if (ld.dtype == RS3_F32) y_fp32 = 0;
   // K^/V^ bytes of the largest bank's full ring, per head
   double kv_bytes = 0;
@@ -744,6 +816,7 @@ rs3_status rs3_readout(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, con
   a.S = S;
   a.n_qt = (max_sel + 127) / 128;
   a.y_fp32 = y_fp32 ? 1 : 0;
+  a.rope = ld.rope;
   return map_err(rs3_launch_readout(a, ld.dtype, (hipStream_t)stream));
 }
 
@@ -759,6 +832,7 @@ rs3_status rs3_commit(rs3_bank* const* banks, int32_t n_obj, const rs3_grid* g, 
   const LayerDev& ld = L->dev;
   if (n_obj > 1 && kv_obj_stride < (int64_t)mn * ld.d_kv) return RS3_E_INVALID;
   if (kv_obj_stride < 0) return RS3_E_INVALID;
+  if (ld.rope && (g->m != ld.rope_m || g->n != ld.rope_n)) return RS3_E_INVALID;
   for (int o = 0; o < n_obj; ++o) {
     if (!banks[o] || banks[o]->L != L) return RS3_E_INVALID;
     for (int p = 0; p < o; ++p)
@@ -786,6 +860,8 @@ rs3_status rs3_commit(rs3_bank* const* banks, int32_t n_obj, const rs3_grid* g, 
   a.fall_max = fall_max;
   a.n_obj = n_obj;
   a.absorb = ld.absorb;
+  a.rope = ld.rope;
+  a.rope_mn = mn;
   for (int o = 0; o < n_obj; ++o) a.parity |= (uint64_t)(banks[o]->commits & 1u) << o;
   hipError_t e = rs3_launch_commit(a, ld.dtype, ld.d_kv, ld.Da, ld.Ha, ld.dah, (hipStream_t)stream);
   if (e != hipSuccess) return map_err(e);

@@ -359,6 +359,21 @@ __device__ __forceinline__ void append_bf16(const Rs3CommitArgs& a, const BankDe
     // K^: row = key (32mb + c_row), column = d (dcol)
     {
       const int h = dcol >> lg_dh, dd = dcol & (d_h - 1);
+      if (a.rope) {
+        // Eq. 7 on the key side: the key kept from cell src[row] turns by
+        // that cell's factors (lanes l and l^1 hold columns 2p and 2p+1)
+        const float2* rope = (const float2*)a.rope;
+        const int hp = d_h >> 1, p = dd >> 1;
+        const float sgn = (dd & 1) ? 1.f : -1.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int kr = 32 * mb + c_row(r, lane);
+          const int cell = kr < rows ? min(max(src[kr], 0), a.rope_mn - 1) : 0;
+          const float2 cs = rope[(int64_t)cell * hp + p];
+          const float v = ck[r], w = __shfl_xor(v, 1);
+          ck[r] = v * cs.x + sgn * w * cs.y;
+        }
+      }
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int kr = 32 * mb + c_row(r, lane);
@@ -477,30 +492,47 @@ __device__ __forceinline__ void append_f32(const Rs3CommitArgs& a, const BankDev
         }
       }
     }
-    return;
-  }
-  for (int q = tid; q < rows * D; q += NT) {
-    const int r = q / D, d = q - r * D;
-    const int j = start + r0 + r;
-    const float* kr = Kr + (int64_t)j * d_kv;
-    const float* vr = Vr + (int64_t)j * d_kv;
-    float sk, sv;
-    if (a.absorb) {  // attention on the raw rows
-      sk = kr[d];
-      sv = vr[d];
-    } else {
-      const float* wk = WkT + (int64_t)d * d_kv;
-      const float* wv = WvT + (int64_t)d * d_kv;
-      sk = 0.f;
-      sv = 0.f;
-      for (int c = 0; c < d_kv; ++c) {
-        sk = fmaf(kr[c], wk[c], sk);
-        sv = fmaf(vr[c], wv[c], sv);
+  } else {
+    for (int q = tid; q < rows * D; q += NT) {
+      const int r = q / D, d = q - r * D;
+      const int j = start + r0 + r;
+      const float* kr = Kr + (int64_t)j * d_kv;
+      const float* vr = Vr + (int64_t)j * d_kv;
+      float sk, sv;
+      if (a.absorb) {  // attention on the raw rows
+        sk = kr[d];
+        sv = vr[d];
+      } else {
+        const float* wk = WkT + (int64_t)d * d_kv;
+        const float* wv = WvT + (int64_t)d * d_kv;
+        sk = 0.f;
+        sv = 0.f;
+        for (int c = 0; c < d_kv; ++c) {
+          sk = fmaf(kr[c], wk[c], sk);
+          sv = fmaf(vr[c], wv[c], sv);
+        }
       }
+      const int tile = j >> 6, kk = j & 63, h = d / d_h, dd = d - h * d_h;
+      Kh[(((int64_t)tile * H + h) * KT + kk) * d_h + dd] = sk;
+      Vh[(((int64_t)tile * H + h) * d_h + dd) * KT + vslot(kk)] = sv;
     }
-    const int tile = j >> 6, kk = j & 63, h = d / d_h, dd = d - h * d_h;
-    Kh[(((int64_t)tile * H + h) * KT + kk) * d_h + dd] = sk;
-    Vh[(((int64_t)tile * H + h) * d_h + dd) * KT + vslot(kk)] = sv;
+  }
+  if (a.rope) {
+    // Eq. 7 on the key side: each K^ row written above turns by the factors
+    // of the cell it was kept from
+    __syncthreads();
+    const int hp = d_h / 2;
+    for (int q = tid; q < rows * (D / 2); q += NT) {
+      const int r = q / (D / 2), d = 2 * (q - r * (D / 2));
+      const int h = d / d_h, dd = d - h * d_h;
+      const int j = start + r0 + r, tile = j >> 6, kk = j & 63;
+      const int cell = min(max(src[r], 0), a.rope_mn - 1);
+      const float* f = a.rope + ((int64_t)cell * hp + (dd >> 1)) * 2;
+      float* kp = Kh + (((int64_t)tile * H + h) * KT + kk) * d_h + dd;
+      const float xe = kp[0], xo = kp[1];
+      kp[0] = xe * f[0] - xo * f[1];
+      kp[1] = xe * f[1] + xo * f[0];
+    }
   }
 }
 

@@ -96,6 +96,21 @@ __global__ __launch_bounds__(256) void k_qproj(Rs3ReadoutArgs a) {
     for (int j = 0; j < KB; ++j)
       if (k0 + 16 * j < C) acc = mfma32(av[j], bv[j], acc);
   }
+  if (a.rope) {
+    // Eq. 7: the row gathered from cell sel[row] turns by that cell's
+    // factors.  Lanes l and l^1 hold columns 2p and 2p+1 of the same rows;
+    // lane j < 32 holds the cell of row j of this wave's 32.
+    const float2* rope = (const float2*)a.rope;
+    const int hp = a.d_h >> 1, p = (col & (a.d_h - 1)) >> 1;
+    const float sgn = (col & 1) ? 1.f : -1.f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int cell = __shfl(src, c_row(r, lane));
+      const float2 cs = rope[(int64_t)cell * hp + p];
+      const float v = acc[r], w = __shfl_xor(v, 1);
+      acc[r] = v * cs.x + sgn * w * cs.y;
+    }
+  }
   bf16_t* Q = (bf16_t*)a.Q + (int64_t)o * a.max_sel * D;
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
@@ -1006,6 +1021,17 @@ __global__ __launch_bounds__(256) void k_readout_f32(Rs3ReadoutArgs a) {
     oacc[d] = 0.f;
   }
   __syncthreads();
+  if (a.rope) {
+    // Eq. 7: turn each head's channel pairs by the factors of cell i
+    const float* f = a.rope + (int64_t)i * d_h;   // d_h/2 (cos, sin) pairs
+    for (int pp = tid; pp < D / 2; pp += 256) {
+      const int d = 2 * pp, fp = (d % d_h) & ~1;
+      const float c = f[fp], sn = f[fp + 1], xe = q[d], xo = q[d + 1];
+      q[d] = xe * c - xo * sn;
+      q[d + 1] = xe * sn + xo * c;
+    }
+    __syncthreads();
+  }
   const float* Kh = (const float*)b.Khat;
   const float* Vh = (const float*)b.Vhat;
   for (int h = 0; h < H; ++h) {
@@ -1087,11 +1113,12 @@ static hipError_t launch_attn_dh(const Rs3ReadoutArgs& a, int G, int nblk, hipSt
 
 // Launches of at most one work-group per CU with heads of width <= 64 at
 // d_model 256 project their queries inside the attention (the staged
-// operands would cost larger launches their occupancy).
+// operands would cost larger launches their occupancy); rotary layers
+// project in k_qproj, which turns the rows.
 static bool attn_projects(const Rs3ReadoutArgs& a) {
   const int G = a.n_obj * a.H * a.S;
   const int nblk = 8 * a.n_qt * ((G + 7) / 8);
-  return a.d_h <= 64 && a.C == 8 * PJ_PC && nblk <= ATTN_DEEP_MAX_BLOCKS;
+  return a.d_h <= 64 && a.C == 8 * PJ_PC && nblk <= ATTN_DEEP_MAX_BLOCKS && !a.rope;
 }
 
 hipError_t rs3_launch_attn(const Rs3ReadoutArgs& a, hipStream_t st, bool project) {

@@ -74,6 +74,8 @@ __host__ __device__ inline int vslot(int j) {
 //   projected: Da = D, Ha = H, dah = d_h; WqT = W_q^T [D][C], WoT = W_o^T [C][D]
 //   absorbed : Da = d_kv, Ha = 1, dah = d_kv; WqT = (W_q W_k^T)^T [d_kv][C],
 //              WoT = (W_v W_o)^T [C][d_kv]; WkT/WvT unused (null)
+// Optional rotary table (projected mode): rope [rope_m*rope_n][d_h/2] of
+// (cos, sin) fp32 pairs, null when absent.
 struct LayerDev {
   int32_t C, H, d_h, D, d_kv, dtype, absorb;
   int32_t Da, Ha, dah;
@@ -81,6 +83,8 @@ struct LayerDev {
   void* WkT;  // [D][d_kv] (projected mode)
   void* WvT;  // [D][d_kv] (projected mode)
   void* WoT;
+  float* rope;
+  int32_t rope_m, rope_n;
 };
 
 struct Launch {
@@ -177,6 +181,8 @@ struct Rs3CommitArgs {
   int from_ring;          // append: rows are already in the raw ring (bank import)
   uint64_t parity;        // bit o: current copy of bank o's frame table and frame count
   int rows_per_wg;        // commit: kept rows appended per work-group (a multiple of 64)
+  const float* rope;      // [rope_mn][d_h/2][2] rotary table for the keys, or null
+  int rope_mn;
 };
 
 struct Rs3ReadoutArgs {
@@ -195,6 +201,7 @@ struct Rs3ReadoutArgs {
   float* ML;              // [n_obj][S][max_sel][H][2] workspace
   float qscale;           // log2(e) / sqrt(d_h)
   int mn, C, H, d_h, D, n_obj, max_sel, S, n_qt, y_fp32;
+  const float* rope;      // [mn][d_h/2][2] rotary table for the queries, or null
 };
 
 // Bare attention core: the tensors of rs3_attend laid out as a one-frame
@@ -234,6 +241,8 @@ hipError_t rs3_launch_attend_f32(const float* Q, const float* K, const float* V,
 // resident tile list and key count from the frame table.
 hipError_t rs3_launch_bank_restore(const Rs3CommitArgs& a, int dtype, int d_kv, int rebuild, hipStream_t st);
 hipError_t rs3_readout_setup();
+// Fills the axial rotary table (see rs3_layer_set_rope_axial).
+hipError_t rs3_launch_rope_axial(float* table, int m, int n, int d_h, double theta, hipStream_t st);
 void rs3_prof_begin(int id, hipStream_t st);
 void rs3_prof_end(int id, hipStream_t st);
 

@@ -30,7 +30,8 @@ class Session:
     def __init__(self, *, m: int, n: int, s: int, C: int, H: int, d_kv: int, dtype: str, n_obj: int,
                  shared_x: bool, union_objects: bool, cap: int, f_max: int, n_pin: int, weights,
                  r_s: int = 4, c: int = 14, max_sel: Optional[int] = None, n_splits: int = 0,
-                 absorb: bool = False, device: str = "cuda"):
+                 absorb: bool = False, rope_theta: Optional[float] = None, rope_table=None,
+                 device: str = "cuda"):
         import torch
         self.torch = torch
         self.m, self.n, self.s, self.mn = m, n, s, m * n
@@ -41,6 +42,10 @@ class Session:
         self.grid = B.Grid(m, n, s)
         self.params = B.SelectParams(r_s, c, 0, 1 if union_objects else 0)
         self.layer = B.Layer(C, H, d_kv, self.dt, weights.Wq, weights.Wk, weights.Wv, weights.Wo, absorb)
+        if rope_table is not None:
+            self.layer.set_rope(m, n, rope_table)
+        elif rope_theta is not None:
+            self.layer.set_rope_axial(m, n, rope_theta)
         self.banks = [B.Bank(self.layer, cap, f_max, n_pin) for _ in range(n_obj)]
         self.track = B.Track(n_obj)
         self.device = device

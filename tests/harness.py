@@ -20,8 +20,12 @@ def grid_masks(cfg: Config, masks_px: np.ndarray) -> np.ndarray:
 
 
 class OraclePipeline:
-    def __init__(self, cfg: Config, W):
+    """rope: optional complex rotary table [mn][d_h/2] (Eq. 7) applied to the
+    selected queries and to the bank keys by their stored cells."""
+
+    def __init__(self, cfg: Config, W, rope=None):
         self.cfg = cfg
+        self.rope = rope
         self.W = {k: storage_to_f64(getattr(W, k), cfg.dtype) for k in ("Wq", "Wk", "Wv", "Wo")}
         npdt = np.uint16 if cfg.dtype == "bf16" else np.float32
         self.tracks: List[oracle.Track] = [oracle.Track() for _ in range(cfg.n_obj)]
@@ -44,18 +48,21 @@ class OraclePipeline:
         cfg = self.cfg
         xi = 0 if X_store.shape[0] == 1 else o
         X = storage_to_f64(X_store[xi], cfg.dtype)
-        K, V, _ = self.banks[o].key_rows()
+        K, V, pos = self.banks[o].key_rows()
         Kf, Vf = storage_to_f64(K, cfg.dtype), storage_to_f64(V, cfg.dtype)
-        Y = oracle.readout(X, rows, Kf, Vf, self.W["Wq"], self.W["Wk"], self.W["Wv"], self.W["Wo"], cfg.H)
+        Y = oracle.readout(X, rows, Kf, Vf, self.W["Wq"], self.W["Wk"], self.W["Wv"], self.W["Wo"], cfg.H,
+                           rope=self.rope, kpos=pos)
         return Y[np.asarray(rows, dtype=np.int64)]
 
     def readout_dense_rows(self, X_store, o, rows):
         cfg = self.cfg
         xi = 0 if X_store.shape[0] == 1 else o
-        X = storage_to_f64(X_store[xi], cfg.dtype)[np.asarray(rows, dtype=np.int64)]
-        K, V, _ = self.banks[o].key_rows()
+        rows = np.asarray(rows, dtype=np.int64)
+        X = storage_to_f64(X_store[xi], cfg.dtype)[rows]
+        K, V, pos = self.banks[o].key_rows()
         Kf, Vf = storage_to_f64(K, cfg.dtype), storage_to_f64(V, cfg.dtype)
-        return oracle.readout_dense(X, Kf, Vf, self.W["Wq"], self.W["Wk"], self.W["Wv"], self.W["Wo"], cfg.H)
+        return oracle.readout_dense(X, Kf, Vf, self.W["Wq"], self.W["Wk"], self.W["Wv"], self.W["Wo"], cfg.H,
+                                    rope=self.rope, kpos=pos, qpos=rows)
 
 
 def compare_bank(gpu_export: dict, ring: oracle.RingBank):

@@ -57,6 +57,8 @@ def test_host_validation_before_device(lib):
     assert lib.rs3_readout(None, ctypes.byref(g), 1, None, 0, None, None, None, 0, 0, 0, None, 0, 0, None, 0,
                            None) == p.RS3_E_INVALID
     assert lib.rs3_commit(None, 1, ctypes.byref(g), None, None, 0, None, 0, 0, 0, 4096, None, None) == p.RS3_E_INVALID
+    assert lib.rs3_layer_set_rope(None, 4, 4, None) == p.RS3_E_INVALID
+    assert lib.rs3_layer_set_rope_axial(None, 4, 4, 10000.0) == p.RS3_E_INVALID
     out = ctypes.c_void_p()
     assert lib.rs3_track_create(0, ctypes.byref(out)) == p.RS3_E_INVALID
     assert lib.rs3_bank_create(None, 100, 4, 1, ctypes.byref(out)) == p.RS3_E_INVALID

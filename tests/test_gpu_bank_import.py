@@ -25,8 +25,12 @@ def _snap_equal(a, b):
         assert np.array_equal(a[key], b[key]), key
 
 
-@pytest.mark.parametrize("name,absorb", [("sam2_single", False), ("sam2_single", True), ("tiny_f32", False)])
-def test_export_import_round_trip(name, absorb):
+@pytest.mark.parametrize("name,absorb,rope_theta", [("sam2_single", False, None), ("sam2_single", True, None),
+                                                   ("tiny_f32", False, None), ("sam2_single", False, 10000.0),
+                                                   ("tiny_f32", False, 100.0)])
+def test_export_import_round_trip(name, absorb, rope_theta):
+    """With a rotary table the restored keys are turned again from the
+    snapshot's stored cells, so the readout stays bit-identical."""
     import paper_2608_22526_amd as rs3
     from paper_2608_22526_amd.session import Session, to_device, to_host
 
@@ -37,7 +41,7 @@ def test_export_import_round_trip(name, absorb):
     seq = make_sequence(cfg, n_frames=9)
     sess = Session(m=cfg.m, n=cfg.n, s=cfg.s, C=cfg.C, H=cfg.H, d_kv=cfg.d_kv, dtype=cfg.dtype, n_obj=1,
                    shared_x=True, union_objects=True, cap=cfg.cap, f_max=cfg.f_max, n_pin=cfg.n_pin, weights=W,
-                   max_sel=cfg.mn, absorb=absorb)
+                   max_sel=cfg.mn, absorb=absorb, rope_theta=rope_theta)
     orc = OraclePipeline(cfg, W)
     for t in range(7):
         fr = make_frame(cfg, t)

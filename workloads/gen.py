@@ -22,7 +22,7 @@ from typing import List, Optional
 import numpy as np
 
 # stream ids for default_rng([seed, frame, stream])
-_S_X, _S_K, _S_V, _S_MASK, _S_RHO, _S_W = 1, 2, 3, 4, 5, 6
+_S_X, _S_K, _S_V, _S_MASK, _S_RHO, _S_W, _S_ROPE = 1, 2, 3, 4, 5, 6, 7
 
 
 # ----------------------------------------------------------------------------
@@ -198,6 +198,15 @@ def make_weights(cfg: Config, logit_scale: float = 1.0) -> Weights:
     wo = rng.standard_normal((D, cfg.C), dtype=np.float32) / np.float32(math.sqrt(D))
     wq = wq * np.float32(logit_scale)
     return Weights(*(to_storage(w, cfg.dtype) for w in (wq, wk, wv, wo)))
+
+
+def make_rope_table(cfg: Config, seed: int = 0) -> np.ndarray:
+    """A random rotary table of unit factors, float32 [mn][d_h/2][2] holding
+    (cos, sin) of angles drawn uniformly from [0, 2 pi): an arbitrary table
+    for the gather of Eq. 7, passed to both sides as it is."""
+    rng = np.random.default_rng([cfg.seed, seed, _S_ROPE])
+    ang = rng.uniform(0.0, 2.0 * math.pi, (cfg.mn, cfg.d_h // 2))
+    return np.stack([np.cos(ang), np.sin(ang)], axis=-1).astype(np.float32)
 
 
 @dataclass
