@@ -14,6 +14,7 @@ Modules:
   readout   the sparse memory readout with scatter (Sec. 3.1, Eq. 6)
   rope      rotary positions on the gathered subset (Sec. 3.1, Eq. 7)
   bank      write compaction and the ring memory bank (Sec. 3.2, Eq. 8)
+  write     the paper's fixed write keep-set K_w (Sec. 3.2, Eq. 8)
 
 Parity unpinned: absolute readout values at the workload sizes (the paper
 prints no tensors and its weights are not available); every other function is
@@ -25,4 +26,5 @@ from .geometry import Track, bbox, down_s, down_s_box, fill_box, dilate, prior_o
 from .select import energy, topk_keep, select_queries  # noqa: F401
 from .rope import axial_table, table_from_pairs, rotate, rotate_heads  # noqa: F401
 from .readout import project_bank, attention_weights, readout, readout_dense, attend  # noqa: F401
+from .write import write_keepset  # noqa: F401
 from .bank import compact, RingBank, FrameListBank, RS3_OK, RS3_E_INVALID, RS3_E_CAPACITY  # noqa: F401

@@ -138,7 +138,9 @@ def k_from_rho(rho, mn: int) -> int:
 def fall_counts(lo, hi, mn: int):
     """Integer thresholds for the write fall-through: a frame falls through
     when count < fall_min or count > fall_max; (lo, hi) = (0, 1) is off."""
-    flo, fhi = Fraction(lo), Fraction(hi)
+    # floats go through their shortest decimal form (0.05 -> 1/20, not the
+    # binary value just above it)
+    flo, fhi = (Fraction(repr(v)) if isinstance(v, float) else Fraction(v) for v in (lo, hi))
     fall_min = int(math.ceil(flo * mn))
     fall_max = int(math.floor(fhi * mn))
     return fall_min, fall_max
