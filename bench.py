@@ -43,7 +43,7 @@ def _describe(cfg) -> str:
 # ---------------------------------------------------------------------------
 # CPU baseline (child process, fp64 oracle, one thread)
 # ---------------------------------------------------------------------------
-def cpu_child(workload: str, frames: int, rope_theta: float = 0.0):
+def cpu_child(workload: str, frames: int, rope_theta: float = 0.0, write_dw: int = -1):
     import numpy as np  # noqa: F401  (threads pinned by the parent's env)
     sys.path.insert(0, os.path.join(ROOT, "tests"))
     import oracle
@@ -54,9 +54,21 @@ def cpu_child(workload: str, frames: int, rope_theta: float = 0.0):
     seq = make_sequence(cfg, n_frames=n_pre + frames + 1)
     W = make_weights(cfg)
     orc = OraclePipeline(cfg, W, rope=oracle.axial_table(cfg.m, cfg.n, cfg.d_h, rope_theta) if rope_theta else None)
+    keep = None
+    if write_dw >= 0:
+        from workloads import fall_counts
+        lo, hi = fall_counts("0.05", "0.95", cfg.mn)
+        keep = oracle.write_keepset(seq.masks[0], cfg.s, cfg.m, cfg.n, write_dw, lo, hi)[0].reshape(-1).astype(np.uint8)
+
+    def commit(fr, t, pin):
+        if keep is None:
+            orc.commit(fr.Kmem, fr.Vmem, seq.masks[t], t, pin)
+        else:
+            for o in range(cfg.n_obj):
+                orc.banks[o].commit(fr.Kmem[o], fr.Vmem[o], keep, t, pin)
+
     for t in range(n_pre):
-        fr = make_frame(cfg, t)
-        orc.commit(fr.Kmem, fr.Vmem, seq.masks[t], t, t < cfg.n_pin)
+        commit(make_frame(cfg, t), t, t < cfg.n_pin)
     t0 = time.perf_counter()
     for t in range(n_pre, n_pre + frames):
         fr = make_frame(cfg, t)
@@ -64,18 +76,18 @@ def cpu_child(workload: str, frames: int, rope_theta: float = 0.0):
         for o in range(cfg.n_obj):
             g = 0 if cfg.union_objects else o
             orc.readout_rows(fr.X, o, sel[g])
-        orc.commit(fr.Kmem, fr.Vmem, seq.masks[t], t, False)
+        commit(fr, t, False)
     dt = time.perf_counter() - t0
     print(json.dumps({"seconds": dt, "frames": frames, "prefill": n_pre}))
 
 
-def cpu_baseline(workload: str, frames: int, rope_theta: float = 0.0):
+def cpu_baseline(workload: str, frames: int, rope_theta: float = 0.0, write_dw: int = -1):
     env = dict(os.environ)
     for v in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS", "NUMEXPR_NUM_THREADS"):
         env[v] = "1"
     env["HIP_VISIBLE_DEVICES"] = ""
     p = subprocess.run([sys.executable, os.path.abspath(__file__), "--cpu-child", "--workload", workload,
-                        "--cpu-frames", str(frames), "--rope", str(rope_theta)], stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True,
+                        "--cpu-frames", str(frames), "--rope", str(rope_theta), "--write-dw", str(write_dw)], stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True,
                        env=env, timeout=600)
     if p.returncode != 0:
         return {"value": None, "unit": "frames/s", "cores": 1, "kind": "oracle", "error": p.stderr[-500:]}
@@ -152,6 +164,26 @@ class QueueWindow:
             self.events[i] = ev
 
 
+def _fixed_keepset(torch, rs3, sess, cfg, seed_masks, D_w):
+    """The paper's write keep-set K_w (Eq. 8) from the first frame's masks,
+    once per sequence, as the commit mask of every object (grid stride 1).
+    Returns (keep [n_obj][mn] u8 on the device, |K_w|, kernel us)."""
+    from workloads import fall_counts
+    if cfg.s != 1:
+        raise SystemExit("the fixed write keep-set workloads use stride-1 grids")
+    lo, hi = fall_counts("0.05", "0.95", cfg.mn)
+    keep = torch.zeros((cfg.n_obj, cfg.mn), dtype=torch.uint8, device="cuda")
+    counts = torch.zeros(2, dtype=torch.int32, device="cuda")
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    rs3.write_keepset(sess.grid, cfg.n_obj, seed_masks, D_w, lo, hi, cfg.n_obj, keep, counts)   # warm
+    ev[0].record()
+    for _ in range(10):
+        rs3.write_keepset(sess.grid, cfg.n_obj, seed_masks, D_w, lo, hi, cfg.n_obj, keep, counts)
+    ev[1].record()
+    torch.cuda.synchronize()
+    return keep, int(counts[1].item()), 1000.0 * ev[0].elapsed_time(ev[1]) / 10
+
+
 def gpu_run(args):
     import numpy as np
     import torch
@@ -179,6 +211,12 @@ def gpu_run(args):
                            max_sel=max(seq.k[t])))
     in_place = cfg.n_obj == 1
     Y = None if in_place else torch.empty((cfg.n_obj, cfg.mn, cfg.C), dtype=frames[0]["X"].dtype, device=dev)
+    fixed = None
+    if args.write_dw >= 0:
+        keep, kw, kw_us = _fixed_keepset(torch, rs3, sess, cfg, frames[0]["mask"], args.write_dw)
+        fixed = {"D_w": args.write_dw, "keep_cells": kw, "keepset_kernel_us": kw_us}
+        for f in frames:
+            f["mask"] = keep
     for t in range(n_pre):
         f = frames[t]
         sess.commit(f["K"], f["V"], f["mask"], t, t < cfg.n_pin)
@@ -324,6 +362,7 @@ def gpu_run(args):
             "splits": sess.n_splits,
             "host_enqueue_us_per_step": host_us,
             "hip_graph": graph,
+            "fixed_write_keepset": fixed,
         },
     }
     return out
@@ -378,7 +417,8 @@ def _algo_bytes(cfg, absorb, rec):
     }
 
 
-def run_workload(cfg, *, absorb, steps, warmup, commit=True, prefill=None, splits=0, rope_theta=None):
+def run_workload(cfg, *, absorb, steps, warmup, commit=True, prefill=None, splits=0, rope_theta=None,
+                 write_dw=-1):
     """Steady-state frames of `cfg` (objects beyond 64 run as several calls per
     frame).  Returns frame timing percentiles, per-kernel times and rates."""
     import numpy as np
@@ -410,6 +450,13 @@ def run_workload(cfg, *, absorb, steps, warmup, commit=True, prefill=None, split
                             rmask=to_device(seq.read_mask(cfg, t)[o0:o0 + no]),
                             k=seq.k[t] if cfg.union_objects else seq.k[t][o0:o0 + no]))
         frames.append(dict(per=per, max_sel=max(seq.k[t])))
+    keep_cells = None
+    if write_dw >= 0:
+        if len(sessions) != 1:
+            raise SystemExit("the fixed write keep-set workloads run one call per frame")
+        keep, keep_cells, _ = _fixed_keepset(torch, rs3, sessions[0], cfg, frames[0]["per"][0]["mask"], write_dw)
+        for fr_ in frames:
+            fr_["per"][0]["mask"] = keep
     outs = [None if no == 1 else
             torch.empty((no, cfg.mn, cfg.C), dtype=frames[0]["per"][0]["X"].dtype, device="cuda") for _, no in chunks]
     def frame_of(t):
@@ -505,6 +552,7 @@ def run_workload(cfg, *, absorb, steps, warmup, commit=True, prefill=None, split
         "selected_per_frame": q_frame, "kept_per_frame": k_frame,
         "bank_keys_mean": sum(sum(r["n_keys"]) for r in recs) / len(recs) / cfg.n_obj,
         "kernels": kern, "attention_width": Da, "objects": cfg.n_obj, "calls_per_frame": len(sessions),
+        "fixed_write_keep_cells": keep_cells,
     }
 
 
@@ -533,6 +581,13 @@ def report(args):
         r = run_workload(cfg, absorb=False, steps=args.steps, warmup=args.warmup, rope_theta=10000.0)
         out["%s/projected+rope" % name] = r
         log("%s/projected+rope" % name, r)
+    # the paper's own write rule (Eq. 8): every frame written at the fixed
+    # keep-set of the first frame's mask, default and aggressive radius
+    for D_w in (24, 12):
+        for name in ("sam2_single", "long_video"):
+            r = run_workload(CONFIGS[name], absorb=True, steps=args.steps, warmup=args.warmup, write_dw=D_w)
+            out["%s/absorbed+fixed_write%d" % (name, D_w)] = r
+            log("%s/absorbed fixed write D_w=%d" % (name, D_w), r)
     hr = CONFIGS["highres"]
     for rho in ("0.1", "0.25", "0.5", "1.0"):
         cfg = replace(hr, rho=float(rho))
@@ -565,6 +620,9 @@ def main():
                          "(a stall of tens of ms) after the first thousand-odd launches of a process")
     ap.add_argument("--workload", default="sam2_single")
     ap.add_argument("--splits", type=int, default=0)
+    ap.add_argument("--write-dw", type=int, default=-1,
+                    help="write every frame at the fixed keep-set K_w of this dilation radius (Eq. 8), built "
+                         "from the first frame's masks; -1 = each frame's own mask")
     ap.add_argument("--rope", type=float, default=0.0,
                     help="axial rotary table with this theta on a projected layer (0 = none)")
     ap.add_argument("--layer", choices=["auto", "projected", "absorbed"], default="auto")
@@ -579,7 +637,7 @@ def main():
     ap.add_argument("--report", default="", help="write the full measurement report (JSON) to this path")
     args = ap.parse_args()
     if args.cpu_child:
-        cpu_child(args.workload, args.cpu_frames, args.rope)
+        cpu_child(args.workload, args.cpu_frames, args.rope, args.write_dw)
         return
     if args.rope and args.layer == "absorbed":
         print("--rope needs a projected layer: the rotation sits between the projections that absorption "
@@ -596,7 +654,7 @@ def main():
         return
     out = gpu_run(args)
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_frames, args.rope)
+        out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_frames, args.rope, args.write_dw)
     print(json.dumps(out))
 
 

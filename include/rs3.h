@@ -244,6 +244,28 @@ rs3_status rs3_commit(rs3_bank* const* banks /*[host]*/, int32_t n_obj, const rs
                       const uint8_t* masks, int32_t t, int32_t pin, int32_t fall_min,
                       int32_t fall_max, int32_t* kept_count, void* stream);
 
+/* ---- the paper's fixed write keep-set (Sec. 3.2, Eq. 8) -------------------
+ * K_w = union over the n_obj objects of dilate_{D_w}(down_s(seed_masks[o])),
+ * where seed_masks[o] is object o's mask at its first frame ([n_obj][m*s][n*s]
+ * u8, nonzero = set; cell (y, x) samples pixel (y*s, x*s)) and the dilation is
+ * the Chebyshev radius D_w in grid cells.  If the undilated footprint (the
+ * union of the down-sampled seeds) has fewer than fall_min or more than
+ * fall_max cells, K_w is every cell (the dense fall-through; 0 and m*n turn
+ * it off).  K_w is computed once and passed unchanged to every later
+ * rs3_commit of the sequence (with the grid {m, n, 1}: the keep-set is at
+ * grid resolution), so every stored frame holds |K_w| rows: a constant
+ * per-frame stride, and fixed ring slots when the bank holds the pinned rows
+ * plus a multiple of |K_w|.
+ * keep   : device out u8 [n_copies][m*n], 1 = kept; the keep-set is written
+ *          n_copies times so that it serves as the mask of n_copies objects.
+ * counts : optional device out int32 [2]: footprint cells, |K_w|.
+ * Asynchronous on `stream`, allocates nothing.  Requires a valid grid,
+ * 1 <= n_obj <= RS3_MAX_OBJ, 1 <= n_copies <= RS3_MAX_OBJ, D_w >= 0 (radii
+ * beyond the grid act as max(m, n)). */
+rs3_status rs3_write_keepset(const rs3_grid* g, int32_t n_obj, const uint8_t* seed_masks, int32_t D_w,
+                             int32_t fall_min, int32_t fall_max, int32_t n_copies, uint8_t* keep,
+                             int32_t* counts, void* stream);
+
 /* ---- bare attention core (Sec. 3.1, Eq. 6 without the projections) ---------
  * O_h = softmax(Q_h K_h^T / sqrt(d_h)) V_h for every head h on tensors that
  * are already projected: Qh [n_q][H][d_h], Kh and Vh [n_kv][H][d_h] in `dt`,

@@ -63,6 +63,7 @@ _SIGS = {
                             c_i32, c_vp, c_i64, c_i32, c_vp, c_sz, c_vp]),
     "rs3_commit": (c_i32, [c_vp, c_i32, ctypes.POINTER(Grid), c_vp, c_vp, c_i64, c_vp, c_i32, c_i32, c_i32,
                            c_i32, c_vp, c_vp]),
+    "rs3_write_keepset": (c_i32, [ctypes.POINTER(Grid), c_i32, c_vp, c_i32, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp]),
     "rs3_profile_enable": (c_i32, [c_i32, c_i32]),
     "rs3_profile_report": (c_i32, [c_vp, c_vp, c_vp]),
     "rs3_profile_reset": (c_i32, []),
@@ -271,6 +272,13 @@ def commit(banks: Sequence[Bank], grid, Kmem, Vmem, kv_obj_stride: int, masks, t
     _check(lib().rs3_commit(ctypes.cast(harr, c_vp), len(banks), ctypes.byref(_grid(grid)), _ptr(Kmem),
                             _ptr(Vmem), kv_obj_stride, _ptr(masks), t, pin, fall_min, fall_max,
                             _ptr(kept_count), _stream(stream)), "rs3_commit")
+
+
+def write_keepset(grid, n_obj: int, seed_masks, D_w: int, fall_min: int, fall_max: int, n_copies: int, keep,
+                  counts=None, stream=None):
+    """The fixed write keep-set K_w (u8 [n_copies][m*n]) from the seed masks."""
+    _check(lib().rs3_write_keepset(ctypes.byref(_grid(grid)), n_obj, _ptr(seed_masks), D_w, fall_min, fall_max,
+                                   n_copies, _ptr(keep), _ptr(counts), _stream(stream)), "rs3_write_keepset")
 
 
 def attend_workspace_size(n_q: int, n_kv: int, H: int, d_h: int, dtype: int, n_splits: int = 0) -> int:

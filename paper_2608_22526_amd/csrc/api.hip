@@ -820,6 +820,18 @@ rs3_status rs3_readout(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, con
   return map_err(rs3_launch_readout(a, ld.dtype, (hipStream_t)stream));
 }
 
+// ---- write keep-set ----------------------------------------------------------
+rs3_status rs3_write_keepset(const rs3_grid* g, int32_t n_obj, const uint8_t* seed_masks, int32_t D_w,
+                             int32_t fall_min, int32_t fall_max, int32_t n_copies, uint8_t* keep, int32_t* counts,
+                             void* stream) {
+  if (!grid_ok(g) || !seed_masks || !keep) return RS3_E_INVALID;
+  if (n_obj <= 0 || n_obj > RS3_MAX_OBJ || n_copies <= 0 || n_copies > RS3_MAX_OBJ || D_w < 0)
+    return RS3_E_INVALID;
+  const int reach = g->m > g->n ? g->m : g->n;
+  return map_err(rs3_launch_write_keepset(seed_masks, n_obj, g->m, g->n, g->s, D_w < reach ? D_w : reach, fall_min,
+                                          fall_max, n_copies, keep, counts, (hipStream_t)stream));
+}
+
 // ---- commit ----------------------------------------------------------------
 rs3_status rs3_commit(rs3_bank* const* banks, int32_t n_obj, const rs3_grid* g, const void* Kmem,
                       const void* Vmem, int64_t kv_obj_stride, const uint8_t* masks, int32_t t, int32_t pin,

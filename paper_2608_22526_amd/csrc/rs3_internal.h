@@ -241,6 +241,9 @@ hipError_t rs3_launch_attend_f32(const float* Q, const float* K, const float* V,
 // resident tile list and key count from the frame table.
 hipError_t rs3_launch_bank_restore(const Rs3CommitArgs& a, int dtype, int d_kv, int rebuild, hipStream_t st);
 hipError_t rs3_readout_setup();
+// The fixed write keep-set (see rs3_write_keepset); D is already clamped.
+hipError_t rs3_launch_write_keepset(const uint8_t* seed, int n_obj, int m, int n, int s, int D, int fall_min,
+                                    int fall_max, int n_copies, uint8_t* keep, int32_t* counts, hipStream_t st);
 // Fills the axial rotary table (see rs3_layer_set_rope_axial).
 hipError_t rs3_launch_rope_axial(float* table, int m, int n, int d_h, double theta, hipStream_t st);
 void rs3_prof_begin(int id, hipStream_t st);
