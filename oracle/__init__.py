@@ -15,6 +15,7 @@ Modules:
   rope      rotary positions on the gathered subset (Sec. 3.1, Eq. 7)
   bank      write compaction and the ring memory bank (Sec. 3.2, Eq. 8)
   write     the paper's fixed write keep-set K_w (Sec. 3.2, Eq. 8)
+  post      closure of the decoded masks and the palette argmax (Sec. 3.3)
 
 Parity unpinned: absolute readout values at the workload sizes (the paper
 prints no tensors and its weights are not available); every other function is
@@ -27,4 +28,5 @@ from .select import energy, topk_keep, select_queries  # noqa: F401
 from .rope import axial_table, table_from_pairs, rotate, rotate_heads  # noqa: F401
 from .readout import project_bank, attention_weights, readout, readout_dense, attend  # noqa: F401
 from .write import write_keepset  # noqa: F401
+from .post import close_square, palette, close_masks  # noqa: F401
 from .bank import compact, RingBank, FrameListBank, RS3_OK, RS3_E_INVALID, RS3_E_CAPACITY  # noqa: F401
