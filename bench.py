@@ -556,6 +556,33 @@ def run_workload(cfg, *, absorb, steps, warmup, commit=True, prefill=None, split
     }
 
 
+def run_post(n_obj, H, W, k=9, reps=50):
+    """The closure and palette step on decoder logits of n_obj x H x W (bf16):
+    time per call and algorithmic bandwidth (logits read once, closed masks
+    and palette written once)."""
+    import torch
+    import paper_2608_22526_amd as rs3
+    from paper_2608_22526_amd.session import to_device
+    from workloads import make_decoder_logits
+    L = to_device(make_decoder_logits(n_obj, H, W, seed=1))
+    ws = torch.zeros(rs3.close_workspace_size(n_obj, H, W), dtype=torch.uint8, device="cuda")
+    closed = torch.empty((n_obj, H, W), dtype=torch.uint8, device="cuda")
+    pal = torch.empty((H, W), dtype=torch.uint8, device="cuda")
+    for _ in range(5):
+        rs3.close_masks(n_obj, H, W, L, rs3.RS3_BF16, k, closed, pal, ws)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    for _ in range(reps):
+        rs3.close_masks(n_obj, H, W, L, rs3.RS3_BF16, k, closed, pal, ws)
+    ev[1].record()
+    torch.cuda.synchronize()
+    us = 1000.0 * ev[0].elapsed_time(ev[1]) / reps
+    algo = n_obj * H * W * 2 + n_obj * H * W + H * W
+    return {"us_per_call": us, "algo_bytes": algo, "GB_s": algo / (us * 1e-6) / 1e9,
+            "frac_hbm": algo / (us * 1e-6) / 1e9 / PEAK_HBM_GBS}
+
+
 def report(args):
     from dataclasses import replace
     from workloads import CONFIGS
@@ -581,6 +608,11 @@ def report(args):
         r = run_workload(cfg, absorb=False, steps=args.steps, warmup=args.warmup, rope_theta=10000.0)
         out["%s/projected+rope" % name] = r
         log("%s/projected+rope" % name, r)
+    # closure of the decoded masks and the palette (Sec. 3.3), 9x9
+    for (no, H, W) in ((1, 256, 256), (8, 256, 256), (1, 1024, 1024), (8, 1024, 1024)):
+        r = run_post(no, H, W)
+        out["post/%dx%dx%d" % (no, H, W)] = r
+        print("post %d x %dx%d: %.1f us, %.0f GB/s" % (no, H, W, r["us_per_call"], r["GB_s"]), flush=True)
     # the paper's own write rule (Eq. 8): every frame written at the fixed
     # keep-set of the first frame's mask, default and aggressive radius
     for D_w in (24, 12):
@@ -635,6 +667,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-child", action="store_true")
     ap.add_argument("--report", default="", help="write the full measurement report (JSON) to this path")
+    ap.add_argument("--post-only", action="store_true", help="time only the closure and palette step")
     args = ap.parse_args()
     if args.cpu_child:
         cpu_child(args.workload, args.cpu_frames, args.rope, args.write_dw)
@@ -649,6 +682,10 @@ def main():
               "sharded across GPUs with no exchange, which this benchmark does not launch). Use --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
+    if args.post_only:
+        for (no, H, W) in ((1, 256, 256), (8, 256, 256), (1, 1024, 1024), (8, 1024, 1024)):
+            print(json.dumps({"post": [no, H, W], **run_post(no, H, W)}), flush=True)
+        return
     if args.report:
         report(args)
         return

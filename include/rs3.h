@@ -266,6 +266,26 @@ rs3_status rs3_write_keepset(const rs3_grid* g, int32_t n_obj, const uint8_t* se
                              int32_t fall_min, int32_t fall_max, int32_t n_copies, uint8_t* keep,
                              int32_t* counts, void* stream);
 
+/* ---- closure of the decoded masks and the palette (Sec. 3.3) ----------------
+ * The steps after the mask decoder in Algorithm 1.  For each object o its
+ * binary mask is logits[o] > 0 at decoder resolution H x W; it is closed
+ * with a k x k square (k odd, 9 in the paper): a dilation for which pixels
+ * outside the image are unset, then an erosion for which they are set, so
+ * the closing never removes a pixel.  The palette is, per pixel, 1 + the
+ * object with the largest logit among the objects whose closed mask covers
+ * the pixel (the lowest index on ties), or 0 where none does.  The closed
+ * masks are what the next frame's tracker update reads: with H = m*s and
+ * W = n*s they are the `masks` argument of rs3_select_queries.
+ * logits  : device [n_obj][H][W] in `dt` (bf16 or fp32).
+ * closed  : optional device out u8 [n_obj][H][W] (1 = set).
+ * palette : optional device out u8 [H][W].
+ * ws      : device workspace of at least rs3_close_workspace_size() bytes.
+ * Asynchronous on `stream`, allocates nothing.  Requires 1 <= n_obj <=
+ * RS3_MAX_OBJ, 1 <= H <= 16384, 1 <= W <= 4096, k odd in [1, 15]. */
+rs3_status rs3_close_workspace_size(int32_t n_obj, int32_t H, int32_t W, size_t* bytes);
+rs3_status rs3_close_masks(int32_t n_obj, int32_t H, int32_t W, const void* logits, rs3_dtype dt, int32_t k,
+                           uint8_t* closed, uint8_t* palette, void* ws, size_t ws_bytes, void* stream);
+
 /* ---- bare attention core (Sec. 3.1, Eq. 6 without the projections) ---------
  * O_h = softmax(Q_h K_h^T / sqrt(d_h)) V_h for every head h on tensors that
  * are already projected: Qh [n_q][H][d_h], Kh and Vh [n_kv][H][d_h] in `dt`,

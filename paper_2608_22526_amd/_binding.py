@@ -64,6 +64,8 @@ _SIGS = {
     "rs3_commit": (c_i32, [c_vp, c_i32, ctypes.POINTER(Grid), c_vp, c_vp, c_i64, c_vp, c_i32, c_i32, c_i32,
                            c_i32, c_vp, c_vp]),
     "rs3_write_keepset": (c_i32, [ctypes.POINTER(Grid), c_i32, c_vp, c_i32, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp]),
+    "rs3_close_workspace_size": (c_i32, [c_i32, c_i32, c_i32, ctypes.POINTER(c_sz)]),
+    "rs3_close_masks": (c_i32, [c_i32, c_i32, c_i32, c_vp, c_i32, c_i32, c_vp, c_vp, c_vp, c_sz, c_vp]),
     "rs3_profile_enable": (c_i32, [c_i32, c_i32]),
     "rs3_profile_report": (c_i32, [c_vp, c_vp, c_vp]),
     "rs3_profile_reset": (c_i32, []),
@@ -279,6 +281,20 @@ def write_keepset(grid, n_obj: int, seed_masks, D_w: int, fall_min: int, fall_ma
     """The fixed write keep-set K_w (u8 [n_copies][m*n]) from the seed masks."""
     _check(lib().rs3_write_keepset(ctypes.byref(_grid(grid)), n_obj, _ptr(seed_masks), D_w, fall_min, fall_max,
                                    n_copies, _ptr(keep), _ptr(counts), _stream(stream)), "rs3_write_keepset")
+
+
+def close_workspace_size(n_obj: int, H: int, W: int) -> int:
+    out = c_sz()
+    _check(lib().rs3_close_workspace_size(n_obj, H, W, ctypes.byref(out)), "rs3_close_workspace_size")
+    return out.value
+
+
+def close_masks(n_obj: int, H: int, W: int, logits, dtype: int, k: int, closed=None, palette=None, ws=None,
+                stream=None):
+    """k x k closure of each object's decoded mask and the palette argmax."""
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(lib().rs3_close_masks(n_obj, H, W, _ptr(logits), dtype, k, _ptr(closed), _ptr(palette), _ptr(ws),
+                                 ws_bytes, _stream(stream)), "rs3_close_masks")
 
 
 def attend_workspace_size(n_q: int, n_kv: int, H: int, d_h: int, dtype: int, n_splits: int = 0) -> int:

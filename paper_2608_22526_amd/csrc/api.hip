@@ -832,6 +832,26 @@ rs3_status rs3_write_keepset(const rs3_grid* g, int32_t n_obj, const uint8_t* se
                                           fall_max, n_copies, keep, counts, (hipStream_t)stream));
 }
 
+// ---- closure and palette -------------------------------------------------------
+static bool close_shape_ok(int32_t n_obj, int32_t H, int32_t W) {
+  return n_obj >= 1 && n_obj <= RS3_MAX_OBJ && H >= 1 && H <= 16384 && W >= 1 && W <= 4096;
+}
+
+rs3_status rs3_close_workspace_size(int32_t n_obj, int32_t H, int32_t W, size_t* bytes) {
+  if (!bytes || !close_shape_ok(n_obj, H, W)) return RS3_E_INVALID;
+  *bytes = rs3_post_workspace_bytes(n_obj, H, W);
+  return RS3_OK;
+}
+
+rs3_status rs3_close_masks(int32_t n_obj, int32_t H, int32_t W, const void* logits, rs3_dtype dt, int32_t k,
+                           uint8_t* closed, uint8_t* palette, void* ws, size_t ws_bytes, void* stream) {
+  if (!logits || !ws || !close_shape_ok(n_obj, H, W)) return RS3_E_INVALID;
+  if (dt != RS3_BF16 && dt != RS3_F32) return RS3_E_INVALID;
+  if (k < 1 || k > 15 || k % 2 == 0) return RS3_E_INVALID;
+  if (ws_bytes < rs3_post_workspace_bytes(n_obj, H, W)) return RS3_E_INVALID;
+  return map_err(rs3_launch_close_masks(n_obj, H, W, logits, dt, k, closed, palette, ws, (hipStream_t)stream));
+}
+
 // ---- commit ----------------------------------------------------------------
 rs3_status rs3_commit(rs3_bank* const* banks, int32_t n_obj, const rs3_grid* g, const void* Kmem,
                       const void* Vmem, int64_t kv_obj_stride, const uint8_t* masks, int32_t t, int32_t pin,

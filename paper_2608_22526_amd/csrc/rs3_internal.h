@@ -244,6 +244,10 @@ hipError_t rs3_readout_setup();
 // The fixed write keep-set (see rs3_write_keepset); D is already clamped.
 hipError_t rs3_launch_write_keepset(const uint8_t* seed, int n_obj, int m, int n, int s, int D, int fall_min,
                                     int fall_max, int n_copies, uint8_t* keep, int32_t* counts, hipStream_t st);
+// Closure of decoded masks and the palette (see rs3_close_masks).
+size_t rs3_post_workspace_bytes(int n_obj, int H, int W);
+hipError_t rs3_launch_close_masks(int n_obj, int H, int W, const void* logits, int dtype, int k, uint8_t* closed,
+                                  uint8_t* palette, void* ws, hipStream_t st);
 // Fills the axial rotary table (see rs3_layer_set_rope_axial).
 hipError_t rs3_launch_rope_axial(float* table, int m, int n, int d_h, double theta, hipStream_t st);
 void rs3_prof_begin(int id, hipStream_t st);

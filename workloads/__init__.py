@@ -7,6 +7,6 @@ sides of every parity check consume the exact arrays produced here.
 from .gen import (  # noqa: F401
     CONFIGS, Config, Weights, FrameInputs, Sequence,
     bf16_bits, bits_to_f32, to_storage, storage_to_f64,
-    ellipse_mask, make_weights, make_frame, make_sequence, make_rope_table, k_from_rho,
+    ellipse_mask, make_weights, make_frame, make_sequence, make_rope_table, make_decoder_logits, k_from_rho,
     fall_counts,
 )

@@ -211,6 +211,31 @@ def make_rope_table(cfg: Config, seed: int = 0) -> np.ndarray:
     return np.stack([np.cos(ang), np.sin(ang)], axis=-1).astype(np.float32)
 
 
+def make_decoder_logits(n_obj: int, H: int, W: int, seed: int, dtype: str = "bf16",
+                        area=(0.05, 0.3), hole_p: float = 0.04, n_blobs: int = 6) -> np.ndarray:
+    """Synthetic mask-decoder logits [n_obj][H][W]: per object a seeded
+    rotated ellipse with logits ~ +|N(2, 1)| inside and -|N(2, 1)| outside,
+    salt-and-pepper holes (inside pixels turned negative with probability
+    hole_p) and n_blobs square holes of side 1..12 inside it.  Objects
+    overlap where their ellipses do."""
+    rng = np.random.default_rng([seed, H, W, _S_MASK])
+    out = np.empty((n_obj, H, W), dtype=np.float32)
+    for o in range(n_obj):
+        inside = ellipse_mask(rng, H, W, float(rng.uniform(*area))).astype(bool)
+        mag = np.abs(rng.normal(2.0, 1.0, (H, W))).astype(np.float32)
+        lo = np.where(inside, mag, -mag)
+        flip = inside & (rng.random((H, W)) < hole_p)
+        lo[flip] = -lo[flip]
+        ys, xs = np.nonzero(inside)
+        for _ in range(n_blobs if len(ys) else 0):
+            j = int(rng.integers(len(ys)))
+            side = int(rng.integers(1, 13))
+            blk = lo[ys[j]:ys[j] + side, xs[j]:xs[j] + side]
+            blk[...] = -np.abs(blk)
+        out[o] = lo
+    return to_storage(out, dtype)
+
+
 @dataclass
 class FrameInputs:
     X: np.ndarray       # [n_x][mn][C] (n_x = 1 when the grid is shared)
