@@ -31,6 +31,16 @@ __device__ __forceinline__ T gload(const T* p) {
   return *(const RS3_GLOBAL T*)p;
 }
 
+// Loads of wave-uniform values that earlier launches wrote (bank headers,
+// descriptors, selected counts): through the constant address space the
+// compiler uses scalar loads, which are counted apart from the vector loads,
+// so waiting for them does not wait for the operand loads issued before.
+#define RS3_CONST __attribute__((address_space(4)))
+template <class T>
+__device__ __forceinline__ T sload(const T* p) {
+  return *(const RS3_CONST T*)p;
+}
+
 // Waits for loaded values and hands them on as values the compiler did not
 // see being loaded: a loop that uses them then carries no pending load to
 // its head, where the compiler would otherwise wait for every outstanding
@@ -45,6 +55,10 @@ __device__ __forceinline__ void settle(int& a, uint32_t& b, uint32_t& c) {
 template <class T>
 __device__ __forceinline__ void keep(const T& v) {
   asm volatile("" ::"v"(v));
+}
+template <class T>
+__device__ __forceinline__ void keep_s(const T& v) {
+  asm volatile("" ::"s"(v));
 }
 
 __device__ __forceinline__ int sel_count_of(const Rs3ReadoutArgs& a, int o, BankDev& b,
@@ -190,18 +204,11 @@ __device__ __forceinline__ void attn_issue(const bf16_t* Kh, const bf16_t* Vh, i
   for (int j = 0; j < L::NV / 4; ++j) dma16(vg + off.v[j], stage + L::KREG + (4 * j + wave) * 1024);
 }
 
-__device__ __forceinline__ const void* uniform_ptr(const void* p) {
-  const uint64_t v = (uint64_t)p;
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
-  return (const void*)(((uint64_t)hi << 32) | lo);
-}
-
 // Value of lane l^32 for every lane (v_permlane32_swap: both halves come back
 // in registers; op(r[0], r[1]) combines a lane with its partner).
 __device__ __forceinline__ float max_with_partner(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  return __builtin_elementwise_maximum(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 __device__ __forceinline__ float sum_with_partner(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -339,9 +346,11 @@ __device__ __forceinline__ void attn_project(uint8_t* lds, int tid, int wave, in
 constexpr float RESCALE_LOG2 = 8.0f;
 
 // S^T (32 keys x 32 queries) of one half tile: K rows from LDS (kp points at
-// this lane's row and lane-group chunk), Q~ columns from registers.  Two
-// accumulation chains (even / odd 16-deep steps) keep the MFMA pipe busy.
-template <int DH>
+// this lane's row and lane-group chunk), Q~ columns from registers.  CH = 2:
+// two accumulation chains (even / odd 16-deep steps) keep the MFMA pipe busy
+// when one half tile is scored at a time; CH = 1 when two independent half
+// tiles are scored together (no VALU sum of the chains).
+template <int DH, int CH = 2>
 __device__ __forceinline__ f32x16 attn_scores(const uint8_t* kp, const u32x4* qreg) {
   constexpr int NKS = DH / 16;
   constexpr int KG = NKS < 8 ? NKS : 8;
@@ -353,13 +362,28 @@ __device__ __forceinline__ f32x16 attn_scores(const uint8_t* kp, const u32x4* qr
     for (int j = 0; j < KG; ++j) ka[j] = *(const u32x4*)(kp + (k0 + j) * 32);
 #pragma unroll
     for (int j = 0; j < KG; ++j) {
-      if (j & 1)
+      if (CH == 2 && (j & 1))
         s1 = mfma32(ka[j], qreg[k0 + j], s1);
       else
         s0 = mfma32(ka[j], qreg[k0 + j], s0);
     }
   }
-  return s0 + s1;
+  if constexpr (CH == 2) return s0 + s1;
+  return s0;
+}
+
+// Maximum that propagates NaN (the logits hold none): v_maximum3_f32 needs
+// no canonicalising of its inputs, unlike fmaxf.
+__device__ __forceinline__ float max3f(float a, float b, float c) {
+  return __builtin_elementwise_maximum(__builtin_elementwise_maximum(a, b), c);
+}
+
+// Sum of the two bf16 values of a packed pair added to acc (v_dot2 with 1,1):
+// the row sums then add exactly the rounded probabilities the PV product uses.
+__device__ __forceinline__ float add_bf16x2(uint32_t p, float acc) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  const bf16x2_t one = {(__bf16)1.0f, (__bf16)1.0f};
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, p), one, acc, false);
 }
 
 // grid 8*n_qt*ceil(G/8) with G = n_obj*H*S key groups, block 256 (4 waves x
@@ -395,26 +419,27 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
   int src[PROJ ? PJ_XCH : 1];
   u32x4 wv[PROJ ? AttnProj<DH>::WCH : 1];
   if constexpr (PROJ) {
-    attn_proj_load_w<DH>((const bf16_t*)a.WqT, h, tid, wv);
+    // the row indices first: the X loads wait for them alone
     attn_proj_rows(a.sel_idx + (int64_t)o * a.sel_stride, row0, a.max_sel, tid, src);
+    attn_proj_load_w<DH>((const bf16_t*)a.WqT, h, tid, wv);
   } else {
     const bf16_t* Qp = (const bf16_t*)a.Q + ((int64_t)o * a.max_sel + qrow_c) * a.D + h * DH;
 #pragma unroll
     for (int ks = 0; ks < DH / 16; ++ks) qreg[ks] = gload((const u32x4*)(Qp + 16 * ks + 8 * g));
   }
-  // the bank descriptor's pointers (one cache line), issued with them
+  // the bank descriptor's pointers (one cache line), by scalar loads
   const BankDev* bd = a.banks[o];
-  const uint64_t p_hdr = gload((const uint64_t*)&bd->hdr);
-  const uint64_t p_tiles = gload((const uint64_t*)&bd->tiles);
-  const uint64_t p_kh = gload((const uint64_t*)&bd->Khat);
-  const uint64_t p_vh = gload((const uint64_t*)&bd->Vhat);
+  const uint64_t p_hdr = sload((const uint64_t*)&bd->hdr);
+  const uint64_t p_tiles = sload((const uint64_t*)&bd->tiles);
+  const uint64_t p_kh = sload((const uint64_t*)&bd->Khat);
+  const uint64_t p_vh = sload((const uint64_t*)&bd->Vhat);
   // the exits below keep every value loaded so far, so that the compiler
   // issues those loads before the exit tests instead of after them
   auto keep_loads = [&]() {
-    keep(p_hdr);
-    keep(p_tiles);
-    keep(p_kh);
-    keep(p_vh);
+    keep_s(p_hdr);
+    keep_s(p_tiles);
+    keep_s(p_kh);
+    keep_s(p_vh);
     if constexpr (PROJ) {
 #pragma unroll
       for (int i = 0; i < PJ_XCH; ++i) keep(src[i]);
@@ -425,20 +450,20 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
       for (int ks = 0; ks < DH / 16; ++ks) keep(qreg[ks]);
     }
   };
-  BankDev& b = *a.banks[o];
-  const int cnt = sel_count_of(a, o, b, false);
+  int cnt = sload(a.sel_count + (a.sel_stride ? o : 0));   // out of range: reported by the merge
+  cnt = cnt < 0 ? 0 : min(cnt, a.max_sel);
   if (row0 >= cnt) {
     keep_loads();
     return;
   }
-  const int32_t* hdr = (const int32_t*)uniform_ptr((const void*)p_hdr);
+  const int32_t* hdr = (const int32_t*)p_hdr;
   u32x4 xv[PROJ ? PJ_XCH : 1];
   if constexpr (PROJ) {
     // the gathered X rows, in flight while the tile list arrives (invalid
     // list entries read row 0; the merge kernel skips their rows)
     attn_proj_load_x((const bf16_t*)a.X + (int64_t)o * a.x_stride, a.mn, tid, src, xv);
   }
-  const int ntiles = __builtin_amdgcn_readfirstlane(gload(hdr + HDR_NTILES));
+  const int ntiles = sload(hdr + HDR_NTILES);
   const int tps = split_tiles(ntiles, a.S);
   const int tb = min(s * tps, ntiles), te = min(tb + tps, ntiles);
   if (tb >= te) {
@@ -458,11 +483,11 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
   }
   const int ub = 2 * tb, ue = 2 * te;   // half tiles
 
-  // values loaded from the bank descriptor are wave-uniform: keep them in
-  // scalar registers so that load addresses are base (SGPR) + lane offset
-  const bf16_t* Kh = (const bf16_t*)uniform_ptr((const void*)p_kh);
-  const bf16_t* Vh = (const bf16_t*)uniform_ptr((const void*)p_vh);
-  const TileEnt* tiles = (const TileEnt*)uniform_ptr((const void*)p_tiles);
+  // values loaded from the bank descriptor are wave-uniform scalar loads, so
+  // load addresses are base (SGPR) + lane offset
+  const bf16_t* Kh = (const bf16_t*)p_kh;
+  const bf16_t* Vh = (const bf16_t*)p_vh;
+  const TileEnt* tiles = (const TileEnt*)p_tiles;
   const int H = a.H;
   const AttnDmaOffsets<DH> doff = attn_dma_offsets<DH>(wave, lane);
 
@@ -544,8 +569,8 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
       const uint32_t mA = (u0 & 1) ? __builtin_amdgcn_readlane(c_mhi, t0) : __builtin_amdgcn_readlane(c_mlo, t0);
       const uint32_t mB = (u1 & 1) ? __builtin_amdgcn_readlane(c_mhi, t1) : __builtin_amdgcn_readlane(c_mlo, t1);
       if ((mA | mB) == 0u) continue;
-      f32x16 sA = attn_scores<DH>(SA + kbase, qreg);
-      f32x16 sB = attn_scores<DH>(SB + kbase, qreg);
+      f32x16 sA = attn_scores<DH, 1>(SA + kbase, qreg);
+      f32x16 sB = attn_scores<DH, 1>(SB + kbase, qreg);
       if (mA != 0xffffffffu) {   // partial or empty half tile (frame boundary)
 #pragma unroll
         for (int r = 0; r < 16; ++r)
@@ -556,9 +581,9 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
         for (int r = 0; r < 16; ++r)
           if (!(mB >> c_row(r, lane) & 1u)) sB[r] = -INFINITY;
       }
-      float mx = fmaxf(sA[0], sB[0]);
+      float mx = __builtin_elementwise_maximum(sA[0], sB[0]);
 #pragma unroll
-      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(sA[r], sB[r]));
+      for (int r = 1; r < 16; ++r) mx = max3f(mx, sA[r], sB[r]);
       mx = max_with_partner(mx);
       // Lazy rescale: the reference max only moves when a pair exceeds it by
       // more than RESCALE_LOG2 (probabilities stay <= 2^RESCALE_LOG2); the
@@ -582,9 +607,9 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
           const float a1 = __builtin_amdgcn_exp2f(sA[8 * hf + 2 * j + 1] - m_run);
           const float b0 = __builtin_amdgcn_exp2f(sB[8 * hf + 2 * j] - m_run);
           const float b1 = __builtin_amdgcn_exp2f(sB[8 * hf + 2 * j + 1] - m_run);
-          psum += (a0 + a1) + (b0 + b1);
           pkA[hf][j] = pack_bf16x2(a0, a1);
           pkB[hf][j] = pack_bf16x2(b0, b1);
+          psum = add_bf16x2(pkB[hf][j], add_bf16x2(pkA[hf][j], psum));
         }
       l_run += psum;
       // O^T += V^T P^T over the 64 keys (two 16-key MFMA steps per half and d block)
@@ -657,9 +682,9 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
           for (int r = 0; r < 16; ++r)
             if (!(msk >> c_row(r, lane) & 1u)) sc[r] = -INFINITY;
         }
-        float mx = sc[0];
+        float mx = __builtin_elementwise_maximum(sc[0], sc[1]);
 #pragma unroll
-        for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sc[r]);
+        for (int r = 2; r < 16; r += 2) mx = max3f(mx, sc[r], sc[r + 1]);
         mx = max_with_partner(mx);
         // Lazy rescale: the reference max only moves when a half tile exceeds
         // it by more than RESCALE_LOG2 (probabilities stay <= 2^RESCALE_LOG2);
@@ -681,8 +706,8 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
           for (int j = 0; j < 4; ++j) {
             const float p0 = __builtin_amdgcn_exp2f(sc[8 * hf + 2 * j] - m_run);
             const float p1 = __builtin_amdgcn_exp2f(sc[8 * hf + 2 * j + 1] - m_run);
-            psum += p0 + p1;
             pk[hf][j] = pack_bf16x2(p0, p1);
+            psum = add_bf16x2(pk[hf][j], psum);
           }
         l_run += psum;
         // O^T += V^T P^T over the 32 keys (two 16-key MFMA steps per d block)
