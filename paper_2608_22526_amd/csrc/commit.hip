@@ -356,6 +356,19 @@ __device__ __forceinline__ void append_bf16(const Rs3CommitArgs& a, const BankDe
       ck = mfma32(*(const u32x4*)(krow + ks), *(const u32x4*)(wk + ks), ck);   // rows = keys, cols = d
       cv = mfma32(*(const u32x4*)(wv + ks), *(const u32x4*)(vrow + ks), cv);   // rows = d, cols = keys
     }
+    // V^ first (its accumulators are then free while K^ is turned):
+    // row = d (32nb + c_row), column = key (rr)
+    if (rr < rows) {
+      const int j = start + r0 + rr;
+      const int64_t tb = (int64_t)(j >> 6) * H;
+      const int slot = vslot(j & 63);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int d = 32 * nb + c_row(r, lane);
+        const int h = d >> lg_dh, dd = d & (d_h - 1);
+        Vh[((tb + h) * d_h + dd) * KT + slot] = __builtin_bit_cast(bf16_t, (__bf16)cv[r]);
+      }
+    }
     // K^: row = key (32mb + c_row), column = d (dcol)
     {
       const int h = dcol >> lg_dh, dd = dcol & (d_h - 1);
@@ -381,18 +394,6 @@ __device__ __forceinline__ void append_bf16(const Rs3CommitArgs& a, const BankDe
           const int j = start + r0 + kr;
           Kh[(((int64_t)(j >> 6) * H + h) * KT + (j & 63)) * d_h + dd] = __builtin_bit_cast(bf16_t, (__bf16)ck[r]);
         }
-      }
-    }
-    // V^: row = d (32nb + c_row), column = key (rr)
-    if (rr < rows) {
-      const int j = start + r0 + rr;
-      const int64_t tb = (int64_t)(j >> 6) * H;
-      const int slot = vslot(j & 63);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int d = 32 * nb + c_row(r, lane);
-        const int h = d >> lg_dh, dd = d & (d_h - 1);
-        Vh[((tb + h) * d_h + dd) * KT + slot] = __builtin_bit_cast(bf16_t, (__bf16)cv[r]);
       }
     }
   }
