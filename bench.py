@@ -224,6 +224,7 @@ def gpu_run(args):
     step_t = [n_pre]
     main = torch.cuda.current_stream()
     two = args.streams == 2
+    fused = not two and not args.separate
     side = torch.cuda.Stream() if two else main
     ev_read = torch.cuda.Event()
     ev_commit = torch.cuda.Event()
@@ -244,6 +245,13 @@ def gpu_run(args):
             nk = [b.info()["n_keys"] for b in sess.banks]
             g = [0 if cfg.union_objects else o for o in range(cfg.n_obj)]
             record.append(dict(sel=[int(cnt[g[o]]) for o in range(cfg.n_obj)], n_keys=nk))
+        if fused:
+            # readout and commit in one call (the split merge and the commit
+            # share one launch)
+            sess.readout_commit(f["X"], f["X"] if in_place else Y, f["K"], f["V"], f["mask"], t, False,
+                                max_sel=f["max_sel"])
+            step_t[0] += 1
+            return
         if in_place:
             sess.readout(f["X"], f["X"], max_sel=f["max_sel"])
         else:
@@ -337,7 +345,9 @@ def gpu_run(args):
         "data": "synthetic",
         "config": {"workload": _describe(cfg), "grid": "%dx%d" % (cfg.m, cfg.n), "n_obj": cfg.n_obj,
                    "bank_frames": cfg.f_max, "d_model": cfg.C, "heads": cfg.H, "d_head": cfg.d_h,
-                   "d_kv": cfg.d_kv, "eager_launches": True, "streams": args.streams, "readout": "in place" if in_place else "out of place",
+                   "d_kv": cfg.d_kv, "eager_launches": True, "streams": args.streams,
+                   "calls": "select + readout + commit" if (args.separate or args.streams == 2)
+                   else "select + readout_commit", "readout": "in place" if in_place else "out of place",
                    "attention": ("absorbed: one head of width d_kv=%d on the raw bank rows" % cfg.d_kv) if absorb
                    else ("projected: %d head(s) of width %d%s" % (cfg.H, cfg.d_h,
                          ", axial rotary table (theta %g) on queries and keys" % args.rope if args.rope else ""))},
@@ -660,6 +670,8 @@ def main():
     ap.add_argument("--layer", choices=["auto", "projected", "absorbed"], default="auto")
     ap.add_argument("--streams", type=int, choices=[1, 2], default=1,
                     help="2: frame t's commit overlaps frame t+1's selection on a second stream")
+    ap.add_argument("--separate", action="store_true",
+                    help="readout and commit as two calls (default: rs3_readout_commit, one call)")
     ap.add_argument("--no-graph", dest="graph", action="store_false",
                     help="skip the HIP-graph replay pass (reported beside the eager frames/s)")
     ap.add_argument("--cpu-frames", type=int, default=40)

@@ -244,6 +244,24 @@ rs3_status rs3_commit(rs3_bank* const* banks /*[host]*/, int32_t n_obj, const rs
                       const uint8_t* masks, int32_t t, int32_t pin, int32_t fall_min,
                       int32_t fall_max, int32_t* kept_count, void* stream);
 
+/* ---- readout and commit of one frame in one call ---------------------------
+ * Exactly rs3_readout(...) followed by rs3_commit(...) on the same stream
+ * and banks (arguments as there; the commit's banks are the readout's), with
+ * the readout's split merge and the commit in one launch for bf16 layers:
+ * the merge reads the attention partials, X and W_o and writes Y, the commit
+ * writes the banks, so their work-groups run side by side (Algorithm 1 writes
+ * a frame to memory right after its readout).  Both argument sets are checked
+ * before any device work; either failing returns RS3_E_INVALID with no state
+ * changed.  When the selection list and the commit both find device errors,
+ * the bank's sticky word keeps whichever is recorded first. */
+rs3_status rs3_readout_commit(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, const void* X,
+                              int64_t x_obj_stride, rs3_bank* const* banks /*[host]*/, const int32_t* sel_idx,
+                              const int32_t* sel_count, int32_t sel_stride, int32_t max_sel, int32_t n_splits,
+                              void* Y, int64_t y_obj_stride, int32_t y_fp32, void* ws, size_t ws_bytes,
+                              const void* Kmem, const void* Vmem, int64_t kv_obj_stride, const uint8_t* masks,
+                              int32_t t, int32_t pin, int32_t fall_min, int32_t fall_max, int32_t* kept_count,
+                              void* stream);
+
 /* ---- the paper's fixed write keep-set (Sec. 3.2, Eq. 8) -------------------
  * K_w = union over the n_obj objects of dilate_{D_w}(down_s(seed_masks[o])),
  * where seed_masks[o] is object o's mask at its first frame ([n_obj][m*s][n*s]
@@ -320,7 +338,8 @@ enum {
   RS3_K_ATTN = 6,          /* split-KV attention */
   RS3_K_COMBINE = 7,       /* split merge + W_o + residual + scatter */
   RS3_K_READOUT_F32 = 8,   /* fp32 readout */
-  RS3_K_COUNT = 9
+  RS3_K_MERGE_COMMIT = 9,  /* split merge and commit in one launch (rs3_readout_commit) */
+  RS3_K_COUNT = 10
 };
 rs3_status rs3_profile_enable(int32_t on, int32_t max_launches);
 rs3_status rs3_profile_report(double* total_ms, int64_t* launches, int64_t* dropped);

@@ -10,7 +10,7 @@ from ._binding import (  # noqa: F401
     Rs3Error, lib, lib_path, exported_symbols, Grid, SelectParams,
     Track, Layer, Bank,
     select_workspace_size, select_queries,
-    readout_workspace_size, readout, commit, write_keepset, close_workspace_size, close_masks,
+    readout_workspace_size, readout, commit, readout_commit, write_keepset, close_workspace_size, close_masks,
     attend_workspace_size, attend,
     KERNEL_NAMES, profile_enable, profile_reset, profile_report,
 )

@@ -61,6 +61,9 @@ _SIGS = {
     "rs3_readout_workspace_size": (c_i32, [c_vp, c_i32, c_i32, c_i32, ctypes.POINTER(c_sz)]),
     "rs3_readout": (c_i32, [c_vp, ctypes.POINTER(Grid), c_i32, c_vp, c_i64, c_vp, c_vp, c_vp, c_i32, c_i32,
                             c_i32, c_vp, c_i64, c_i32, c_vp, c_sz, c_vp]),
+    "rs3_readout_commit": (c_i32, [c_vp, ctypes.POINTER(Grid), c_i32, c_vp, c_i64, c_vp, c_vp, c_vp, c_i32, c_i32,
+                                   c_i32, c_vp, c_i64, c_i32, c_vp, c_sz, c_vp, c_vp, c_i64, c_vp, c_i32, c_i32,
+                                   c_i32, c_i32, c_vp, c_vp]),
     "rs3_commit": (c_i32, [c_vp, c_i32, ctypes.POINTER(Grid), c_vp, c_vp, c_i64, c_vp, c_i32, c_i32, c_i32,
                            c_i32, c_vp, c_vp]),
     "rs3_write_keepset": (c_i32, [ctypes.POINTER(Grid), c_i32, c_vp, c_i32, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp]),
@@ -72,7 +75,7 @@ _SIGS = {
 }
 
 KERNEL_NAMES = ["energy", "select", "commit", "commit_append", "copy", "qproj", "attn", "combine",
-                "readout_f32"]
+                "readout_f32", "merge_commit"]
 
 _lib = None
 
@@ -274,6 +277,20 @@ def commit(banks: Sequence[Bank], grid, Kmem, Vmem, kv_obj_stride: int, masks, t
     _check(lib().rs3_commit(ctypes.cast(harr, c_vp), len(banks), ctypes.byref(_grid(grid)), _ptr(Kmem),
                             _ptr(Vmem), kv_obj_stride, _ptr(masks), t, pin, fall_min, fall_max,
                             _ptr(kept_count), _stream(stream)), "rs3_commit")
+
+
+def readout_commit(layer: Layer, grid, n_obj: int, X, x_obj_stride: int, banks: Sequence[Bank], sel_idx, sel_count,
+                   sel_stride: int, max_sel: int, n_splits: int, Y, y_obj_stride: int, y_fp32: int, ws, Kmem, Vmem,
+                   kv_obj_stride: int, masks, t: int, pin: int, fall_min: int, fall_max: int, kept_count=None,
+                   stream=None):
+    """rs3_readout followed by rs3_commit, merged into fewer launches."""
+    harr = (c_vp * len(banks))(*[b.h for b in banks])
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(lib().rs3_readout_commit(layer.h, ctypes.byref(_grid(grid)), n_obj, _ptr(X), x_obj_stride,
+                                    ctypes.cast(harr, c_vp), _ptr(sel_idx), _ptr(sel_count), sel_stride, max_sel,
+                                    n_splits, _ptr(Y), y_obj_stride, y_fp32, _ptr(ws), ws_bytes, _ptr(Kmem),
+                                    _ptr(Vmem), kv_obj_stride, _ptr(masks), t, pin, fall_min, fall_max,
+                                    _ptr(kept_count), _stream(stream)), "rs3_readout_commit")
 
 
 def write_keepset(grid, n_obj: int, seed_masks, D_w: int, fall_min: int, fall_max: int, n_copies: int, keep,

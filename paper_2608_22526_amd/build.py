@@ -14,12 +14,12 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OBJDIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "librs3.so")
-SOURCES = ["select.hip", "commit.hip", "readout.hip", "attend.hip", "rope.hip", "keepset.hip", "post.hip", "api.hip", "profile.hip"]
+SOURCES = ["select.hip", "commit.hip", "readout.hip", "attend.hip", "rope.hip", "keepset.hip", "post.hip", "fused.hip", "api.hip", "profile.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # The attention kernel keeps its MFMA accumulators in arch VGPRs, so the
 # online-softmax rescale is plain VALU work instead of AGPR round trips.
-PER_FILE = {"readout.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+PER_FILE = {"readout.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"], "fused.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     "-I" + os.path.join(ROOT, "include"), "-I" + CSRC,

@@ -47,6 +47,7 @@ rs3_status ensure_setup() {
   hipError_t e = rs3_readout_setup();
   if (e == hipSuccess) e = rs3_select_setup();
   if (e == hipSuccess) e = rs3_commit_setup();
+  if (e == hipSuccess) e = rs3_fused_setup();
   if (e != hipSuccess) return RS3_E_DEVICE;
   setup_done = true;
   return RS3_OK;
@@ -751,10 +752,12 @@ rs3_status rs3_readout_workspace_size(const rs3_layer* L, int32_t n_obj, int32_t
   return RS3_OK;
 }
 
-rs3_status rs3_readout(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, const void* X, int64_t x_obj_stride,
-                       rs3_bank* const* banks, const int32_t* sel_idx, const int32_t* sel_count, int32_t sel_stride,
-                       int32_t max_sel, int32_t n_splits, void* Y, int64_t y_obj_stride, int32_t y_fp32, void* ws,
-                       size_t ws_bytes, void* stream) {
+// Validates a readout call and fills its kernel arguments (no device work).
+static rs3_status readout_args(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, const void* X,
+                               int64_t x_obj_stride, rs3_bank* const* banks, const int32_t* sel_idx,
+                               const int32_t* sel_count, int32_t sel_stride, int32_t max_sel, int32_t n_splits,
+                               void* Y, int64_t y_obj_stride, int32_t y_fp32, void* ws, size_t ws_bytes,
+                               Rs3ReadoutArgs& a) {
   if (!L || !grid_ok(g) || !X || !banks || !sel_idx || !sel_count || !Y) return RS3_E_INVALID;
   if (n_obj <= 0 || n_obj > RS3_MAX_OBJ) return RS3_E_INVALID;
   const LayerDev& ld = L->dev;
@@ -787,9 +790,6 @@ rs3_status rs3_readout(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, con
   size_t q, o_b, ml;
   readout_shape(L, n_obj, max_sel, S, &q, &o_b, &ml);
   if (ld.dtype == RS3_BF16 && (!ws || ws_bytes < q + o_b + ml)) return RS3_E_INVALID;
-  rs3_status st0 = ensure_setup();
-  if (st0 != RS3_OK) return st0;
-  Rs3ReadoutArgs a;
   memset(&a, 0, sizeof(a));
   for (int o = 0; o < n_obj; ++o) a.banks[o] = banks[o]->d_desc;
   a.X = X;
@@ -817,7 +817,20 @@ rs3_status rs3_readout(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, con
   a.n_qt = (max_sel + 127) / 128;
   a.y_fp32 = y_fp32 ? 1 : 0;
   a.rope = ld.rope;
-  return map_err(rs3_launch_readout(a, ld.dtype, (hipStream_t)stream));
+  return RS3_OK;
+}
+
+rs3_status rs3_readout(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, const void* X, int64_t x_obj_stride,
+                       rs3_bank* const* banks, const int32_t* sel_idx, const int32_t* sel_count, int32_t sel_stride,
+                       int32_t max_sel, int32_t n_splits, void* Y, int64_t y_obj_stride, int32_t y_fp32, void* ws,
+                       size_t ws_bytes, void* stream) {
+  Rs3ReadoutArgs a;
+  rs3_status st = readout_args(L, g, n_obj, X, x_obj_stride, banks, sel_idx, sel_count, sel_stride, max_sel, n_splits,
+                               Y, y_obj_stride, y_fp32, ws, ws_bytes, a);
+  if (st != RS3_OK) return st;
+  st = ensure_setup();
+  if (st != RS3_OK) return st;
+  return map_err(rs3_launch_readout(a, L->dev.dtype, (hipStream_t)stream));
 }
 
 // ---- write keep-set ----------------------------------------------------------
@@ -853,9 +866,10 @@ rs3_status rs3_close_masks(int32_t n_obj, int32_t H, int32_t W, const void* logi
 }
 
 // ---- commit ----------------------------------------------------------------
-rs3_status rs3_commit(rs3_bank* const* banks, int32_t n_obj, const rs3_grid* g, const void* Kmem,
-                      const void* Vmem, int64_t kv_obj_stride, const uint8_t* masks, int32_t t, int32_t pin,
-                      int32_t fall_min, int32_t fall_max, int32_t* kept_count, void* stream) {
+// Validates a commit call and fills its kernel arguments (no device work).
+static rs3_status commit_args(rs3_bank* const* banks, int32_t n_obj, const rs3_grid* g, const void* Kmem,
+                              const void* Vmem, int64_t kv_obj_stride, const uint8_t* masks, int32_t t, int32_t pin,
+                              int32_t fall_min, int32_t fall_max, int32_t* kept_count, Rs3CommitArgs& a) {
   if (!banks || !grid_ok(g) || !Kmem || !Vmem || !masks) return RS3_E_INVALID;
   if (n_obj <= 0 || n_obj > RS3_MAX_OBJ) return RS3_E_INVALID;
   const int mn = g->m * g->n;
@@ -871,9 +885,6 @@ rs3_status rs3_commit(rs3_bank* const* banks, int32_t n_obj, const rs3_grid* g, 
       if (banks[p] == banks[o]) return RS3_E_INVALID;
     if (pin && (banks[o]->unpinned_seen || banks[o]->pin_calls >= banks[o]->host.n_pin)) return RS3_E_INVALID;
   }
-  rs3_status st0 = ensure_setup();
-  if (st0 != RS3_OK) return st0;
-  Rs3CommitArgs a;
   memset(&a, 0, sizeof(a));
   for (int o = 0; o < n_obj; ++o) a.banks[o] = banks[o]->d_desc;
   a.masks = masks;
@@ -895,8 +906,11 @@ rs3_status rs3_commit(rs3_bank* const* banks, int32_t n_obj, const rs3_grid* g, 
   a.rope = ld.rope;
   a.rope_mn = mn;
   for (int o = 0; o < n_obj; ++o) a.parity |= (uint64_t)(banks[o]->commits & 1u) << o;
-  hipError_t e = rs3_launch_commit(a, ld.dtype, ld.d_kv, ld.Da, ld.Ha, ld.dah, (hipStream_t)stream);
-  if (e != hipSuccess) return map_err(e);
+  return RS3_OK;
+}
+
+// Host bookkeeping of a launched commit: frame-state parity and pin rules.
+static void commit_done(rs3_bank* const* banks, int32_t n_obj, int32_t pin) {
   for (int o = 0; o < n_obj; ++o) {
     banks[o]->commits++;
     if (pin)
@@ -904,6 +918,49 @@ rs3_status rs3_commit(rs3_bank* const* banks, int32_t n_obj, const rs3_grid* g, 
     else
       banks[o]->unpinned_seen = 1;
   }
+}
+
+rs3_status rs3_commit(rs3_bank* const* banks, int32_t n_obj, const rs3_grid* g, const void* Kmem,
+                      const void* Vmem, int64_t kv_obj_stride, const uint8_t* masks, int32_t t, int32_t pin,
+                      int32_t fall_min, int32_t fall_max, int32_t* kept_count, void* stream) {
+  Rs3CommitArgs a;
+  rs3_status st = commit_args(banks, n_obj, g, Kmem, Vmem, kv_obj_stride, masks, t, pin, fall_min, fall_max,
+                              kept_count, a);
+  if (st != RS3_OK) return st;
+  st = ensure_setup();
+  if (st != RS3_OK) return st;
+  const LayerDev& ld = banks[0]->L->dev;
+  hipError_t e = rs3_launch_commit(a, ld.dtype, ld.d_kv, ld.Da, ld.Ha, ld.dah, (hipStream_t)stream);
+  if (e != hipSuccess) return map_err(e);
+  commit_done(banks, n_obj, pin);
+  return RS3_OK;
+}
+
+rs3_status rs3_readout_commit(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, const void* X,
+                              int64_t x_obj_stride, rs3_bank* const* banks, const int32_t* sel_idx,
+                              const int32_t* sel_count, int32_t sel_stride, int32_t max_sel, int32_t n_splits,
+                              void* Y, int64_t y_obj_stride, int32_t y_fp32, void* ws, size_t ws_bytes,
+                              const void* Kmem, const void* Vmem, int64_t kv_obj_stride, const uint8_t* masks,
+                              int32_t t, int32_t pin, int32_t fall_min, int32_t fall_max, int32_t* kept_count,
+                              void* stream) {
+  Rs3ReadoutArgs ra;
+  Rs3CommitArgs ca;
+  rs3_status st = readout_args(L, g, n_obj, X, x_obj_stride, banks, sel_idx, sel_count, sel_stride, max_sel,
+                               n_splits, Y, y_obj_stride, y_fp32, ws, ws_bytes, ra);
+  if (st != RS3_OK) return st;
+  st = commit_args(banks, n_obj, g, Kmem, Vmem, kv_obj_stride, masks, t, pin, fall_min, fall_max, kept_count, ca);
+  if (st != RS3_OK) return st;
+  st = ensure_setup();
+  if (st != RS3_OK) return st;
+  const LayerDev& ld = L->dev;
+  const hipStream_t s = (hipStream_t)stream;
+  bool pending = false;
+  hipError_t e = rs3_launch_readout(ra, ld.dtype, s, false, &pending);
+  if (e == hipSuccess)
+    e = pending ? rs3_launch_merge_commit(ra, ca, ld.d_kv, s)
+                : rs3_launch_commit(ca, ld.dtype, ld.d_kv, ld.Da, ld.Ha, ld.dah, s);
+  if (e != hipSuccess) return map_err(e);
+  commit_done(banks, n_obj, pin);
   return RS3_OK;
 }
 

@@ -1,0 +1,64 @@
+// Device helpers shared by the readout kernels and the fused merge + commit
+// launch (gfx950 only).
+#pragma once
+
+#include "rs3_internal.h"
+
+namespace rs3 {
+
+// Loads through global (not generic) pointers: the compiler then counts
+// them on the vector memory counter alone, and a wait for one of them does
+// not have to drain every outstanding load.
+#define RS3_GLOBAL __attribute__((address_space(1)))
+template <class T>
+__device__ __forceinline__ T gload(const T* p) {
+  return *(const RS3_GLOBAL T*)p;
+}
+
+// Loads of wave-uniform values that earlier launches wrote (bank headers,
+// descriptors, selected counts): through the constant address space the
+// compiler uses scalar loads, which are counted apart from the vector loads,
+// so waiting for them does not wait for the operand loads issued before.
+#define RS3_CONST __attribute__((address_space(4)))
+template <class T>
+__device__ __forceinline__ T sload(const T* p) {
+  return *(const RS3_CONST T*)p;
+}
+
+// Waits for loaded values and hands them on as values the compiler did not
+// see being loaded: a loop that uses them then carries no pending load to
+// its head, where the compiler would otherwise wait for every outstanding
+// load (the key/value DMA included) in each iteration.
+__device__ __forceinline__ void settle(int& a, uint32_t& b, uint32_t& c) {
+  asm volatile("s_waitcnt vmcnt(0)" : "+v"(a), "+v"(b), "+v"(c)::"memory");
+}
+
+// Keeps a loaded value alive on a path that does not use it, so the load is
+// issued before the branch rather than sunk past it (an early exit would
+// otherwise delay every load that only the main path uses).
+template <class T>
+__device__ __forceinline__ void keep(const T& v) {
+  asm volatile("" ::"v"(v));
+}
+template <class T>
+__device__ __forceinline__ void keep_s(const T& v) {
+  asm volatile("" ::"s"(v));
+}
+
+__device__ __forceinline__ int sel_count_of(const Rs3ReadoutArgs& a, int o, BankDev& b,
+                                            bool report) {
+  int cnt = gload(a.sel_count + (a.sel_stride ? o : 0));
+  if (cnt > a.max_sel || cnt < 0) {
+    if (report) set_err(b.hdr, RS3_E_INVALID);
+    cnt = cnt < 0 ? 0 : a.max_sel;
+  }
+  return cnt;
+}
+
+// True iff sel[r] is in range and larger than its predecessor.
+__device__ __forceinline__ bool sel_ok(const int32_t* sel, int r, int mn) {
+  int i = sel[r];
+  return i >= 0 && i < mn && (r == 0 || sel[r - 1] < i);
+}
+
+}  // namespace rs3

@@ -1,0 +1,69 @@
+// One launch for the tail of a frame: the merge of the readout's key splits
+// (output projection and residual scatter, Sec. 3.1, Eq. 6) and the commit
+// of the frame's memory tokens (Sec. 3.2, Eq. 8).  The two touch disjoint
+// data -- the merge reads the attention partials, X and W_o and writes Y;
+// the commit reads the memory tokens and the bank state and writes the bank
+// -- so their work-groups run side by side in one grid instead of one launch
+// after the other.
+//
+// Block b < n_cb is merge block (b % n_obj, b / n_obj) of the readout; the
+// others are commit blocks in the same flattened order.  The block size is
+// the commit's; a merge block uses its first CB_THREADS threads and the rest
+// end at once (a work-group barrier waits only for the waves still running).
+#include "combine.h"
+#include "commit_body.h"
+
+namespace rs3 {
+
+template <typename OutT, bool BF16>
+__global__ __launch_bounds__(CP_THREADS) void k_merge_commit(Rs3ReadoutArgs ra, Rs3CommitArgs ca, int n_cb) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t dyn[];
+  const int b = blockIdx.x;
+  if (b < n_cb) {
+    if (threadIdx.x >= CB_THREADS) return;
+    combine_block<OutT>(ra, b % ra.n_obj, b / ra.n_obj, dyn);
+  } else {
+    const int c = b - n_cb;
+    commit_block<BF16>(ca, c % ca.n_obj, c / ca.n_obj, (int32_t*)dyn);
+  }
+}
+
+}  // namespace rs3
+
+using namespace rs3;
+
+static size_t merge_commit_lds(int D, int d_kv) {
+  const size_t cb = combine_lds_bytes(D), cp = CP_FMAX * 16 + commit_stage_bytes(RS3_BF16, d_kv);
+  return cb > cp ? cb : cp;
+}
+
+hipError_t rs3_fused_setup() {
+  // D <= 1024, d_kv <= 256 (checked on the host)
+  size_t max_lds = 0;
+  for (int D = 64; D <= 1024; D += 64) {
+    const size_t b = merge_commit_lds(D, 256);
+    if (b > max_lds) max_lds = b;
+  }
+  hipError_t e = hipFuncSetAttribute((const void*)k_merge_commit<bf16_t, true>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)max_lds);
+  if (e == hipSuccess)
+    e = hipFuncSetAttribute((const void*)k_merge_commit<float, true>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)max_lds);
+  return e;
+}
+
+hipError_t rs3_launch_merge_commit(const Rs3ReadoutArgs& ra, const Rs3CommitArgs& ca, int d_kv, hipStream_t st) {
+  const int n_cb = ra.n_obj * ((ra.max_sel + CB_ROWS - 1) / CB_ROWS);
+  const int mn = ca.m * ca.n;
+  Rs3CommitArgs c = ca;
+  c.rows_per_wg = commit_rows_per_wg(ca.n_obj, mn);
+  const int n_cp = ca.n_obj * (1 + (mn + c.rows_per_wg - 1) / c.rows_per_wg);
+  const size_t lds = merge_commit_lds(ra.D, d_kv);
+  if (ra.y_fp32)
+    RS3_LAUNCH(RS3_K_MERGE_COMMIT, st, (k_merge_commit<float, true>), dim3(n_cb + n_cp), dim3(CP_THREADS), lds, st,
+               ra, c, n_cb);
+  else
+    RS3_LAUNCH(RS3_K_MERGE_COMMIT, st, (k_merge_commit<bf16_t, true>), dim3(n_cb + n_cp), dim3(CP_THREADS), lds, st,
+               ra, c, n_cb);
+  return hipGetLastError();
+}

@@ -18,64 +18,9 @@
 // fp32 workloads that need 1e-4 agreement.
 #include <algorithm>
 
-#include "rs3_internal.h"
+#include "combine.h"
 
 namespace rs3 {
-
-// Loads through global (not generic) pointers: the compiler then counts
-// them on the vector memory counter alone, and a wait for one of them does
-// not have to drain every outstanding load.
-#define RS3_GLOBAL __attribute__((address_space(1)))
-template <class T>
-__device__ __forceinline__ T gload(const T* p) {
-  return *(const RS3_GLOBAL T*)p;
-}
-
-// Loads of wave-uniform values that earlier launches wrote (bank headers,
-// descriptors, selected counts): through the constant address space the
-// compiler uses scalar loads, which are counted apart from the vector loads,
-// so waiting for them does not wait for the operand loads issued before.
-#define RS3_CONST __attribute__((address_space(4)))
-template <class T>
-__device__ __forceinline__ T sload(const T* p) {
-  return *(const RS3_CONST T*)p;
-}
-
-// Waits for loaded values and hands them on as values the compiler did not
-// see being loaded: a loop that uses them then carries no pending load to
-// its head, where the compiler would otherwise wait for every outstanding
-// load (the key/value DMA included) in each iteration.
-__device__ __forceinline__ void settle(int& a, uint32_t& b, uint32_t& c) {
-  asm volatile("s_waitcnt vmcnt(0)" : "+v"(a), "+v"(b), "+v"(c)::"memory");
-}
-
-// Keeps a loaded value alive on a path that does not use it, so the load is
-// issued before the branch rather than sunk past it (an early exit would
-// otherwise delay every load that only the main path uses).
-template <class T>
-__device__ __forceinline__ void keep(const T& v) {
-  asm volatile("" ::"v"(v));
-}
-template <class T>
-__device__ __forceinline__ void keep_s(const T& v) {
-  asm volatile("" ::"s"(v));
-}
-
-__device__ __forceinline__ int sel_count_of(const Rs3ReadoutArgs& a, int o, BankDev& b,
-                                            bool report) {
-  int cnt = gload(a.sel_count + (a.sel_stride ? o : 0));
-  if (cnt > a.max_sel || cnt < 0) {
-    if (report) set_err(b.hdr, RS3_E_INVALID);
-    cnt = cnt < 0 ? 0 : a.max_sel;
-  }
-  return cnt;
-}
-
-// True iff sel[r] is in range and larger than its predecessor.
-__device__ __forceinline__ bool sel_ok(const int32_t* sel, int r, int mn) {
-  int i = sel[r];
-  return i >= 0 && i < mn && (r == 0 || sel[r - 1] < i);
-}
 
 // ---------------------------------------------------------------------------
 // grid (n_obj, ceil(max_sel/64), D/64), block 256: 64 rows x 64 columns.
@@ -760,227 +705,11 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
 }
 
 // ---------------------------------------------------------------------------
-template <typename OutT>
-__device__ __forceinline__ void store_out(OutT* p, float v);
-template <>
-__device__ __forceinline__ void store_out<bf16_t>(bf16_t* p, float v) { *p = f2bf(v); }
-template <>
-__device__ __forceinline__ void store_out<float>(float* p, float v) { *p = v; }
-
-template <typename OutT>
-__device__ __forceinline__ void copy_out(OutT* p, bf16_t x);
-template <>
-__device__ __forceinline__ void copy_out<bf16_t>(bf16_t* p, bf16_t x) { *p = x; }
-template <>
-__device__ __forceinline__ void copy_out<float>(float* p, bf16_t x) { *p = bf2f(x); }
-
-// grid (n_obj, ceil(max_sel/16)), block 512.  Every key split of the call
-// holds a partial for every selected row (the attention writes l = 0 for
-// splits without tiles), so the merge needs nothing from the bank.
-// 1. the row indices are loaded and checked;
-// 2. for each (row, 8-column chunk) item, each of the NG thread groups that
-//    share it loads the (m, l) pairs and partial O chunks of its splits grp,
-//    grp + NG, ... (PART_B per batch, the first batch together with the
-//    residual inputs and W_o operands) and merges them by log-sum-exp in
-//    registers; the NG groups are merged through LDS, and the normalised
-//    row goes to LDS as bf16;
-// 3. y = x + O W_o on a 32x32x16 MFMA whose rows 16..31 are zero; a row with
-//    no resident key (total weight 0) is returned as x, bit for bit.
-constexpr int CB_ROWS = 16;   // the W_o step maps these rows to accumulator rows r < 8
-constexpr int CB_THREADS = 512;
-constexpr int PART_B = 8;     // splits per batch of partial loads
-
-__host__ __device__ constexpr int cb_groups(int D) {
-  return CB_THREADS / (CB_ROWS * (D / 8)) < 1 ? 1
-         : (CB_THREADS / (CB_ROWS * (D / 8)) > 8 ? 8 : CB_THREADS / (CB_ROWS * (D / 8)));
-}
-
-struct PartBatch {
-  float m[PART_B], l[PART_B];
-  u32x4 v[PART_B];
-};
-
-// Batch j of one item's partials: splits grp + NG*(PART_B*j + i); indices
-// past S re-read split S-1 (masked in the merge), rows past max_sel re-read
-// row max_sel-1 (not stored): no branch around the loads.
-__device__ __forceinline__ void part_load(const Rs3ReadoutArgs& a, int o, int row, int d0, int h, int grp, int NG,
-                                          int j, PartBatch& pb) {
-  const int64_t rows = a.max_sel;
-  const int rw = min(row, a.max_sel - 1);
-#pragma unroll
-  for (int i = 0; i < PART_B; ++i) {
-    const int sp = min(grp + NG * (PART_B * j + i), a.S - 1);
-    const int64_t prow = ((int64_t)o * a.S + sp) * rows + rw;
-    typedef float f32x2 __attribute__((ext_vector_type(2)));
-    const f32x2 ml = gload((const f32x2*)(a.ML + (prow * a.H + h) * 2));
-    pb.m[i] = ml[0];
-    pb.l[i] = ml[1];
-    pb.v[i] = gload((const u32x4*)((const bf16_t*)a.Opart + prow * a.D + d0));
-  }
-}
-
-// Online log-sum-exp over a batch: running maximum M, weight W, sum acc.
-__device__ __forceinline__ void part_merge(const PartBatch& pb, int first, int NG, int S, float& M, float& W,
-                                           float (&acc)[8]) {
-#pragma unroll
-  for (int i = 0; i < PART_B; ++i) {
-    const bool on = first + NG * i < S && pb.l[i] > 0.f;
-    const float m = on ? pb.m[i] : -INFINITY;
-    if (m > M) {
-      const float sc = __builtin_amdgcn_exp2f(M - m);
-      W *= sc;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] *= sc;
-      M = m;
-    }
-    const float w = on ? __builtin_amdgcn_exp2f(m - M) * pb.l[i] : 0.f;
-    W += w;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      acc[2 * e] += on ? w * __uint_as_float(pb.v[i][e] << 16) : 0.f;
-      acc[2 * e + 1] += on ? w * __uint_as_float(pb.v[i][e] & 0xffff0000u) : 0.f;
-    }
-  }
-}
-
+// grid (n_obj, ceil(max_sel/16)), block CB_THREADS: one merge block each.
 template <typename OutT>
 __global__ __launch_bounds__(CB_THREADS) void k_combine(Rs3ReadoutArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t cl[];
-  const int o = blockIdx.x, r0 = blockIdx.y * CB_ROWS;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5;
-  const int D = a.D, C = a.C, d_h = a.d_h, S = a.S, OS = D + 8;
-  const int cpr = D / 8, items = CB_ROWS * cpr, NG = cb_groups(D);
-  const int nb = (S + NG * PART_B - 1) / (NG * PART_B);   // batches per item
-  const int32_t* sel = a.sel_idx + (int64_t)o * a.sel_stride;
-  const bf16_t* X = (const bf16_t*)a.X + (int64_t)o * a.x_stride;
-  const bf16_t* WoT = (const bf16_t*)a.WoT;
-
-  // 1. The list entries of this lane's accumulator rows r < 8 (rows
-  //    8*(r/4) + 4*g + r%4 < CB_ROWS) and their predecessors (ascending
-  //    check), and of row r0 + tid for the error report: the only loads
-  //    before the row decisions, so waiting for them waits for nothing else.
-  int srow[8], sprv[8];
-#pragma unroll
-  for (int r = 0; r < 8; ++r) {
-    const int rc = min(r0 + c_row(r, lane), a.max_sel - 1);
-    srow[r] = gload(sel + rc);
-    sprv[r] = gload(sel + max(rc - 1, 0));
-  }
-  const int erc = min(r0 + (tid & (CB_ROWS - 1)), a.max_sel - 1);
-  const int e_cur = gload(sel + erc), e_prv = gload(sel + max(erc - 1, 0));
-  BankDev& b = *a.banks[o];
-  // the merge covers every selected row: it reports a count past max_sel and
-  // invalid (out of range or not ascending) list entries, whose rows it skips
-  const int cnt = sel_count_of(a, o, b, blockIdx.y == 0 && tid == 0);
-  if (r0 >= cnt) return;
-  // entry i of row r is valid iff it is in range and above its predecessor
-  auto entry_ok = [&](int i, int prev, int r) { return i >= 0 && i < a.mn && (r == 0 || prev < i); };
-  if (tid < CB_ROWS && r0 + tid < cnt && !entry_ok(e_cur, e_prv, r0 + tid)) set_err(b.hdr, RS3_E_INVALID);
-  int dst[8];   // destination cell of each accumulator row (-1 = none)
-#pragma unroll
-  for (int r = 0; r < 8; ++r) {
-    const int row = r0 + c_row(r, lane);
-    dst[r] = (c_row(r, lane) < CB_ROWS && row < cnt && entry_ok(srow[r], sprv[r], row)) ? srow[r] : -1;
-  }
-  // 2. Every data load in one batch: residual inputs of the wave's first
-  //    column block, its first W_o operands, and this thread's first item's
-  //    first batch of partials (waves past the last column block, C < 256,
-  //    re-read the last column).
-  const int col0 = 32 * wave + (lane & 31);
-  bf16_t xv0[8];
-#pragma unroll
-  for (int r = 0; r < 8; ++r) xv0[r] = gload(X + (int64_t)max(dst[r], 0) * C + min(col0, C - 1));
-  constexpr int KB = 4;   // k steps per batch of W_o operands (D is a multiple of 64)
-  u32x4 bv0[KB];
-  {
-    const bf16_t* wr = WoT + (int64_t)min(col0, C - 1) * D;
-#pragma unroll
-    for (int j = 0; j < KB; ++j) bv0[j] = gload((const u32x4*)(wr + 16 * j + 8 * g));
-  }
-  const int q0 = tid;
-  PartBatch pb;
-  {
-    const int item0 = q0 % items, grp0 = q0 / items;
-    const int rr = item0 / cpr, d0 = 8 * (item0 - rr * cpr);
-    part_load(a, o, r0 + rr, d0, d0 / d_h, grp0, NG, 0, pb);
-  }
-
-  // merge.  LDS: Os [CB_ROWS][D+8] bf16 | red [NG][items][10] f32 | kept [CB_ROWS]
-  bf16_t* Os = (bf16_t*)cl;
-  float* red = (float*)(cl + ((CB_ROWS * OS * 2 + 15) & ~15));
-  int* kept = (int*)(red + (size_t)NG * items * 10);
-  for (int q = q0; q < items * NG; q += CB_THREADS) {
-    const int item = q % items, grp = q / items;
-    const int rr = item / cpr, d0 = 8 * (item - rr * cpr), h = d0 / d_h;
-    float M = -INFINITY, W = 0.f;
-    float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    for (int j = 0; j < nb; ++j) {
-      if (q != q0 || j > 0) part_load(a, o, r0 + rr, d0, h, grp, NG, j, pb);
-      part_merge(pb, grp + NG * PART_B * j, NG, S, M, W, acc);
-    }
-    float* dstp = red + (size_t)grp * 10 * items + item;   // [NG][10][items]
-    dstp[0] = M;
-    dstp[items] = W;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) dstp[(2 + e) * items] = acc[e];
-  }
-  lds_barrier();
-  for (int item = tid; item < items; item += CB_THREADS) {
-    float M = -INFINITY;
-    for (int grp = 0; grp < NG; ++grp) M = fmaxf(M, red[(size_t)grp * 10 * items + item]);
-    float W = 0.f, acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    if (M != -INFINITY)
-      for (int grp = 0; grp < NG; ++grp) {
-        const float* sp = red + (size_t)grp * 10 * items + item;
-        const float sc = __builtin_amdgcn_exp2f(sp[0] - M);   // 0 for empty groups
-        W += sc * sp[items];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[e] += sc * sp[(2 + e) * items];
-      }
-    const float inv = W > 0.f ? 1.f / W : 0.f;
-    const int rr = item / cpr, d0 = 8 * (item - rr * cpr);
-    u32x4 pk;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) pk[j] = pack_bf16x2(acc[2 * j] * inv, acc[2 * j + 1] * inv);
-    *(u32x4*)&Os[rr * OS + d0] = pk;
-    if (d0 == 0) kept[rr] = W > 0.f;
-  }
-  lds_barrier();
-  // 3. y = x + O W_o for the block's rows, columns split over the waves
-  OutT* Y = (OutT*)a.Y + (int64_t)o * a.y_stride;
-  const bool arow = (lane & 31) < CB_ROWS;
-  const bf16_t* orow = &Os[(arow ? (lane & 31) : 0) * OS + 8 * g];
-  bool keys[8];
-#pragma unroll
-  for (int r = 0; r < 8; ++r) keys[r] = c_row(r, lane) < CB_ROWS && kept[c_row(r, lane)] != 0;
-  for (int nbk = wave; nbk < C / 32; nbk += CB_THREADS / 64) {
-    const bool first = nbk == wave;
-    const int col = 32 * nbk + (lane & 31);
-    const bf16_t* wr = WoT + (int64_t)col * D + 8 * g;
-    bf16_t xv[8];
-#pragma unroll
-    for (int r = 0; r < 8; ++r) xv[r] = first ? xv0[r] : gload(X + (int64_t)max(dst[r], 0) * C + col);
-    f32x16 acc = {};
-    for (int k0 = 0; k0 < D; k0 += 16 * KB) {
-      u32x4 av[KB], bv[KB];
-#pragma unroll
-      for (int j = 0; j < KB; ++j) {
-        av[j] = arow ? *(const u32x4*)(orow + k0 + 16 * j) : u32x4{0, 0, 0, 0};
-        bv[j] = (first && k0 == 0) ? bv0[j] : gload((const u32x4*)(wr + k0 + 16 * j));
-      }
-#pragma unroll
-      for (int j = 0; j < KB; ++j) acc = mfma32(av[j], bv[j], acc);
-    }
-#pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      if (dst[r] < 0) continue;
-      const int64_t off = (int64_t)dst[r] * C + col;
-      if (!keys[r])
-        copy_out<OutT>(&Y[off], xv[r]);
-      else
-        store_out<OutT>(&Y[off], bf2f(xv[r]) + acc[r]);
-    }
-  }
+  combine_block<OutT>(a, blockIdx.x, blockIdx.y, cl);
 }
 
 // Y[o] = X[o] (or the shared X) for every cell, converting to OutT.
@@ -1118,12 +847,6 @@ __global__ __launch_bounds__(256) void k_readout_f32(Rs3ReadoutArgs a) {
 
 using namespace rs3;
 
-static size_t combine_lds_bytes(int D) {
-  const int items = CB_ROWS * (D / 8);
-  return (((size_t)CB_ROWS * (D + 8) * 2 + 15) & ~(size_t)15) + (size_t)cb_groups(D) * items * 10 * 4 +
-         CB_ROWS * 4;
-}
-
 // Launches of at most one work-group per CU take the deep form of the
 // attention where its 8 stages fit the LDS (heads of width <= 64).
 constexpr int ATTN_DEEP_MAX_BLOCKS = 256;
@@ -1164,7 +887,8 @@ hipError_t rs3_launch_attn(const Rs3ReadoutArgs& a, hipStream_t st, bool project
   }
 }
 
-hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st) {
+hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st, bool merge, bool* pending) {
+  if (pending) *pending = false;
   const int64_t cells = (int64_t)a.mn * a.C;
   const bool in_place = a.Y == a.X && !a.y_fp32;
   if (!in_place) {
@@ -1200,6 +924,10 @@ hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st
   }
   hipError_t e = rs3_launch_attn(a, st, project);
   if (e != hipSuccess) return e;
+  if (!merge) {
+    if (pending) *pending = true;
+    return hipSuccess;
+  }
   const size_t lds = combine_lds_bytes(a.D);
   const dim3 cgrid(a.n_obj, (a.max_sel + CB_ROWS - 1) / CB_ROWS);
   if (a.y_fp32)

@@ -228,7 +228,13 @@ hipError_t rs3_launch_energy(const void* X, int64_t x_stride, int n_x, int mn, i
 hipError_t rs3_launch_select(const Rs3SelectArgs& a, int n_groups, hipStream_t st);
 hipError_t rs3_launch_commit(const Rs3CommitArgs& a, int dtype, int d_kv, int D, int H, int d_h,
                              hipStream_t st);
-hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st);
+// merge = false leaves the split merge of the bf16 path to the caller (the
+// fused merge + commit launch); returns whether a merge is pending in *pending.
+hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st, bool merge = true,
+                              bool* pending = nullptr);
+// The readout's split merge and a commit in one launch (bf16 layers).
+hipError_t rs3_launch_merge_commit(const Rs3ReadoutArgs& ra, const Rs3CommitArgs& ca, int d_kv, hipStream_t st);
+hipError_t rs3_fused_setup();
 // Split-KV attention only; project: the queries are projected from X[sel]
 // inside the kernel (heads of width <= 64), else read from a.Q.
 hipError_t rs3_launch_attn(const Rs3ReadoutArgs& a, hipStream_t st, bool project);

@@ -74,6 +74,17 @@ class Session:
         B.readout(self.layer, self.grid, self.n_obj, X, self.x_stride, self.banks, self.sel_idx, self.sel_count,
                   sel_stride, ms, self.n_splits, Y, y_stride, y_fp32, self.ws_read, stream)
 
+    def readout_commit(self, X, Y, Kmem, Vmem, masks, t: int, pin: bool, max_sel: Optional[int] = None,
+                       y_fp32: int = 0, fall_min: int = 0, fall_max: Optional[int] = None, stream=None):
+        """readout(X, Y) then commit(Kmem, Vmem, masks, t, pin) in one call."""
+        ms = self.max_sel if max_sel is None else max_sel
+        sel_stride = 0 if self.union_objects else self.mn
+        y_stride = self.mn * self.C if self.n_obj > 1 else 0
+        fmax = self.mn if fall_max is None else fall_max
+        B.readout_commit(self.layer, self.grid, self.n_obj, X, self.x_stride, self.banks, self.sel_idx,
+                         self.sel_count, sel_stride, ms, self.n_splits, Y, y_stride, y_fp32, self.ws_read, Kmem,
+                         Vmem, self.mn * self.d_kv, masks, t, int(pin), fall_min, fmax, self.kept_count, stream)
+
     def commit(self, Kmem, Vmem, masks, t: int, pin: bool, fall_min: int = 0, fall_max: Optional[int] = None,
                stream=None):
         fmax = self.mn if fall_max is None else fall_max

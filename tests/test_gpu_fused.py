@@ -1,0 +1,62 @@
+"""rs3_readout_commit (a frame's readout and commit in one call, the split
+merge and the commit sharing one launch) through the C ABI against the fp64
+oracle: outputs within 2e-2 (bf16) or 1e-4 (fp32), unselected rows
+bit-identical, banks bit-exact after every fused call, for one object in
+both layer modes, eight objects with per-object lists and out-of-place
+outputs, fp32 outputs, a rotary layer, the fp32 path (no merge launch) and a
+frame with an empty selection."""
+from dataclasses import replace
+
+import numpy as np
+import pytest
+
+import oracle
+from test_gpu_parity import Runner
+from workloads import CONFIGS
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+
+def _fused_run(cfg, n_frames, first, rows=None, y_fp32=0, tol=None, rope=None, **kw):
+    r = Runner(cfg, n_frames, rope_theta=rope, **kw)
+    if rope:
+        r.orc.rope = oracle.axial_table(cfg.m, cfg.n, cfg.d_h, rope)
+    r.commit(0, True)
+    for t in range(1, n_frames):
+        if t < first:
+            r.commit(t, False)
+        else:
+            r.select_readout(t, rows_per_obj=None if t == n_frames - 1 else rows, y_fp32=y_fp32, tol=tol,
+                             fused=True)
+    return r
+
+
+@pytest.mark.parametrize("absorb", [False, True])
+def test_sam2_single_fused(absorb):
+    _fused_run(CONFIGS["sam2_single"], 10, 4, rows=48, max_sel=1228, absorb=absorb)
+
+
+def test_multi_obj8_fused():
+    _fused_run(CONFIGS["multi_obj8"], 9, 6, rows=24, max_sel=1228, absorb=True)
+
+
+def test_fused_fp32_output_and_rotary():
+    cfg = CONFIGS["sam2_single"]
+    _fused_run(cfg, 9, 7, rows=64, y_fp32=1, tol=4e-3, max_sel=1228)
+    _fused_run(replace(cfg, m=32, n=32, f_max=4, cap_frames=4), 7, 2, rows=64, rope=10000.0)
+
+
+def test_fused_fp32_layer_and_small_banks():
+    # the fp32 path has no merge launch: the call runs readout then commit;
+    # a small ring wraps and evicts during the fused calls
+    _fused_run(CONFIGS["tiny_f32"], 8, 1)
+    _fused_run(replace(CONFIGS["sam2_single"], m=16, n=16, f_max=3, cap_frames=2), 9, 1, absorb=True)
+
+
+def test_fused_empty_selection():
+    cfg = CONFIGS["sam2_single"]
+    r = Runner(replace(cfg, m=32, n=32, f_max=4, cap_frames=4), 5, rho_override="0.0")
+    r.commit(0, True)
+    for t in range(1, 5):
+        r.select_readout(t, fused=True)

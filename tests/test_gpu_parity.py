@@ -54,7 +54,10 @@ class Runner:
         for o in range(cfg.n_obj):
             compare_bank(self.sess.banks[o].export(), self.orc.banks[o])
 
-    def select_readout(self, t, rows_per_obj=None, in_place=None, y_fp32=0, dense_check=False, tol=None):
+    def select_readout(self, t, rows_per_obj=None, in_place=None, y_fp32=0, dense_check=False, tol=None,
+                       fused=False):
+        """fused: the readout and frame t's commit run as one rs3_readout_commit
+        call; the bank is then checked against the oracle's after its commit."""
         cfg, sess = self.cfg, self.sess
         fr = make_frame(cfg, t)
         rmask = self.seq.read_mask(cfg, t)
@@ -75,13 +78,18 @@ class Runner:
         # readout
         if in_place is None:
             in_place = cfg.n_obj == 1 and not y_fp32
+        if fused:
+            fk = (_dev(fr.Kmem), _dev(fr.Vmem), _dev(self.seq.masks[t]), t, False)
+            run = lambda Xi, Yo, **k: sess.readout_commit(Xi, Yo, *fk, **k)
+        else:
+            run = sess.readout
         if in_place:
             Y = Xd.clone()
-            sess.readout(Y, Y)
+            run(Y, Y)
         else:
             dt = torch.float32 if (y_fp32 or cfg.dtype == "f32") else torch.bfloat16
             Y = torch.empty((cfg.n_obj, cfg.mn, cfg.C), dtype=dt, device="cuda")
-            sess.readout(Xd, Y, y_fp32=y_fp32)
+            run(Xd, Y, y_fp32=y_fp32)
         torch.cuda.synchronize()
         Yh = _host(Y).reshape(cfg.n_obj if not in_place else 1, cfg.mn, cfg.C)
         tol = TOL[cfg.dtype] if tol is None else tol
@@ -108,6 +116,11 @@ class Runner:
             if dense_check:
                 dense = self.orc.readout_dense_rows(fr.X, o, rows)
                 assert max_abs(got, dense) <= tol
+        if fused:
+            counts = self.orc.commit(fr.Kmem, fr.Vmem, self.seq.masks[t], t, False)
+            assert _host(sess.kept_count).tolist() == counts
+            for o in range(cfg.n_obj):
+                compare_bank(sess.banks[o].export(), self.orc.banks[o])
         return sel
 
 
