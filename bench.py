@@ -112,7 +112,7 @@ def cpu_baseline(workload: str, frames: int, rope_theta: float = 0.0, write_dw: 
 # ---------------------------------------------------------------------------
 def _kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("readout.hip", "rs3_internal.h"):
+    for f in ("readout.hip", "device_util.h", "rs3_internal.h"):
         h.update(open(os.path.join(ROOT, "paper_2608_22526_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 
@@ -485,9 +485,11 @@ def run_workload(cfg, *, absorb, steps, warmup, commit=True, prefill=None, split
             f = frames[fi]["per"][ci]
             sess.select(f["rmask"], f["X"], f["k"])
             Y = outs[ci]
-            sess.readout(f["X"], f["X"] if Y is None else Y, max_sel=frames[fi]["max_sel"])
-            if commit:
-                sess.commit(f["K"], f["V"], f["mask"], t, False)
+            if commit:   # readout and commit in one call
+                sess.readout_commit(f["X"], f["X"] if Y is None else Y, f["K"], f["V"], f["mask"], t, False,
+                                    max_sel=frames[fi]["max_sel"])
+            else:
+                sess.readout(f["X"], f["X"] if Y is None else Y, max_sel=frames[fi]["max_sel"])
         if commit:
             step_t[0] += 1
 
