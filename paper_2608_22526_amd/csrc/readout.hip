@@ -211,42 +211,48 @@ struct AttnProj {
 // Loads of the projection's operands: W chunks need only the arguments,
 // X chunks the gathered row indices (rows past the selected count read any
 // valid row; their results are discarded).
-template <int DH>
-__device__ __forceinline__ void attn_proj_load_w(const bf16_t* WqT, int h, int tid, u32x4 (&wv)[AttnProj<DH>::WCH]) {
+// NT threads share the loads (256 or 512): thread t loads W chunks
+// t + NT*j and X chunk t%32 of rows t/32 + (NT/32)*i.
+template <int DH, int NT>
+__device__ __forceinline__ void attn_proj_load_w(const bf16_t* WqT, int h, int tid,
+                                                 u32x4 (&wv)[AttnProj<DH>::WCH * 256 / NT]) {
   const u32x4* wb = (const u32x4*)(WqT + (int64_t)h * DH * PJ_PC * 8);
 #pragma unroll
-  for (int j = 0; j < AttnProj<DH>::WCH; ++j) wv[j] = gload(wb + tid + 256 * j);
+  for (int j = 0; j < AttnProj<DH>::WCH * 256 / NT; ++j) wv[j] = gload(wb + tid + NT * j);
 }
 
+template <int NT>
 __device__ __forceinline__ void attn_proj_rows(const int32_t* sel, int row0, int max_sel, int tid,
-                                               int (&src)[PJ_XCH]) {
+                                               int (&src)[PJ_XCH * 256 / NT]) {
 #pragma unroll
-  for (int i = 0; i < PJ_XCH; ++i) src[i] = gload(sel + min(row0 + (tid >> 5) + 8 * i, max_sel - 1));
+  for (int i = 0; i < PJ_XCH * 256 / NT; ++i)
+    src[i] = gload(sel + min(row0 + (tid >> 5) + (NT / 32) * i, max_sel - 1));
 }
 
-__device__ __forceinline__ void attn_proj_load_x(const bf16_t* X, int mn, int tid, const int (&src)[PJ_XCH],
-                                                 u32x4 (&xv)[PJ_XCH]) {
+template <int NT>
+__device__ __forceinline__ void attn_proj_load_x(const bf16_t* X, int mn, int tid, const int (&src)[PJ_XCH * 256 / NT],
+                                                 u32x4 (&xv)[PJ_XCH * 256 / NT]) {
 #pragma unroll
-  for (int i = 0; i < PJ_XCH; ++i) {
+  for (int i = 0; i < PJ_XCH * 256 / NT; ++i) {
     const int r = (src[i] < 0 || src[i] >= mn) ? 0 : src[i];
     xv[i] = gload((const u32x4*)(X + (int64_t)r * PJ_PC * 8) + (tid & 31));
   }
 }
 
-template <int DH>
+template <int DH, int NT>
 __device__ __forceinline__ void attn_project(uint8_t* lds, int tid, int wave, int lane, float qs,
-                                             const u32x4 (&wv)[AttnProj<DH>::WCH], const u32x4 (&xv)[PJ_XCH],
-                                             u32x4* qreg) {
+                                             const u32x4 (&wv)[AttnProj<DH>::WCH * 256 / NT],
+                                             const u32x4 (&xv)[PJ_XCH * 256 / NT], u32x4* qreg) {
   using P = AttnProj<DH>;
   const int g = lane >> 5;
 #pragma unroll
-  for (int j = 0; j < P::WCH; ++j) {
-    const int q = tid + 256 * j;
+  for (int j = 0; j < P::WCH * 256 / NT; ++j) {
+    const int q = tid + NT * j;
     *(u32x4*)(lds + P::WS + (q / PJ_PC) * PJ_PITCH + (q % PJ_PC) * 16) = wv[j];
   }
 #pragma unroll
-  for (int i = 0; i < PJ_XCH; ++i)
-    *(u32x4*)(lds + P::XS + ((tid >> 5) + 8 * i) * PJ_PITCH + (tid & 31) * 16) = xv[i];
+  for (int i = 0; i < PJ_XCH * 256 / NT; ++i)
+    *(u32x4*)(lds + P::XS + ((tid >> 5) + (NT / 32) * i) * PJ_PITCH + (tid & 31) * 16) = xv[i];
   lds_barrier();
   f32x16 qa[DH / 32];
 #pragma unroll
@@ -317,6 +323,28 @@ __device__ __forceinline__ f32x16 attn_scores(const uint8_t* kp, const u32x4* qr
   return s0;
 }
 
+// Logits of two half tiles: all K operand reads are issued before the
+// MFMAs, so that the chain waits for LDS once rather than once per step.
+template <int DH>
+__device__ __forceinline__ void attn_scores_pair(const uint8_t* ka, const uint8_t* kb, const u32x4* qreg,
+                                                 f32x16& sa, f32x16& sb) {
+  constexpr int NKS = DH / 16;
+  u32x4 ra[NKS], rb[NKS];
+#pragma unroll
+  for (int j = 0; j < NKS; ++j) {
+    ra[j] = *(const u32x4*)(ka + j * 32);
+    rb[j] = *(const u32x4*)(kb + j * 32);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  sa = f32x16{};
+  sb = f32x16{};
+#pragma unroll
+  for (int j = 0; j < NKS; ++j) {
+    sa = mfma32(ra[j], qreg[j], sa);
+    sb = mfma32(rb[j], qreg[j], sb);
+  }
+}
+
 // Maximum that propagates NaN (the logits hold none): v_maximum3_f32 needs
 // no canonicalising of its inputs, unlike fmaxf.
 __device__ __forceinline__ float max3f(float a, float b, float c) {
@@ -340,8 +368,14 @@ __device__ __forceinline__ float add_bf16x2(uint32_t p, float acc) {
 // 8 stages and a loop over pairs of half tiles (two independent chains per
 // iteration for the one wave per SIMD); otherwise 4 stages and a loop over
 // single half tiles, which keeps the registers of several work-groups per CU.
-template <int DH, bool PROJ, bool DEEP>
-__global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
+// NG = 2 (deep form with the projection only): eight waves, two groups of
+// four on the same 128 queries, each group taking every other pair of half
+// tiles, so that two waves share each SIMD; their partials are merged at the
+// end through LDS.
+template <int DH, bool PROJ, bool DEEP, int NG = 1>
+__global__ __launch_bounds__(256 * NG) void k_attn(Rs3ReadoutArgs a, int G) {
+  static_assert(NG == 1 || (NG == 2 && DEEP && PROJ), "two wave groups need the deep form");
+  constexpr int NT = 256 * NG;
   using L = AttnLds<DH>;
   constexpr int nst = DEEP ? 8 : 4;   // LDS stages
   extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];   // nst * L::STAGE bytes
@@ -352,7 +386,9 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
   if (kvg >= G) return;
   const int s = kvg % a.S, oh = kvg / a.S, h = oh % a.H, o = oh / a.H;
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wave_all = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wave = wave_all & 3;                 // the wave's 32 queries: rows 32*wave of the tile
+  const int grp = NG == 2 ? wave_all >> 2 : 0;   // its group of key pairs
   const int row0 = qt * 128;
   const int qrow = row0 + 32 * wave + (lane & 31);
   // Loads that need nothing but the arguments are issued before the chain
@@ -361,12 +397,12 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
   // PROJ the W_q chunks and the gathered row indices.
   const int qrow_c = min(qrow, a.max_sel - 1);
   u32x4 qreg[DH / 16];
-  int src[PROJ ? PJ_XCH : 1];
-  u32x4 wv[PROJ ? AttnProj<DH>::WCH : 1];
+  int src[PROJ ? PJ_XCH / NG : 1];
+  u32x4 wv[PROJ ? AttnProj<DH>::WCH / NG : 1];
   if constexpr (PROJ) {
     // the row indices first: the X loads wait for them alone
-    attn_proj_rows(a.sel_idx + (int64_t)o * a.sel_stride, row0, a.max_sel, tid, src);
-    attn_proj_load_w<DH>((const bf16_t*)a.WqT, h, tid, wv);
+    attn_proj_rows<NT>(a.sel_idx + (int64_t)o * a.sel_stride, row0, a.max_sel, tid, src);
+    attn_proj_load_w<DH, NT>((const bf16_t*)a.WqT, h, tid, wv);
   } else {
     const bf16_t* Qp = (const bf16_t*)a.Q + ((int64_t)o * a.max_sel + qrow_c) * a.D + h * DH;
 #pragma unroll
@@ -387,9 +423,9 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
     keep_s(p_vh);
     if constexpr (PROJ) {
 #pragma unroll
-      for (int i = 0; i < PJ_XCH; ++i) keep(src[i]);
+      for (int i = 0; i < PJ_XCH / NG; ++i) keep(src[i]);
 #pragma unroll
-      for (int j = 0; j < AttnProj<DH>::WCH; ++j) keep(wv[j]);
+      for (int j = 0; j < AttnProj<DH>::WCH / NG; ++j) keep(wv[j]);
     } else {
 #pragma unroll
       for (int ks = 0; ks < DH / 16; ++ks) keep(qreg[ks]);
@@ -402,11 +438,11 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
     return;
   }
   const int32_t* hdr = (const int32_t*)p_hdr;
-  u32x4 xv[PROJ ? PJ_XCH : 1];
+  u32x4 xv[PROJ ? PJ_XCH / NG : 1];
   if constexpr (PROJ) {
     // the gathered X rows, in flight while the tile list arrives (invalid
     // list entries read row 0; the merge kernel skips their rows)
-    attn_proj_load_x((const bf16_t*)a.X + (int64_t)o * a.x_stride, a.mn, tid, src, xv);
+    attn_proj_load_x<NT>((const bf16_t*)a.X + (int64_t)o * a.x_stride, a.mn, tid, src, xv);
   }
   const int ntiles = sload(hdr + HDR_NTILES);
   const int tps = split_tiles(ntiles, a.S);
@@ -415,11 +451,11 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
     keep_loads();
     if constexpr (PROJ) {
 #pragma unroll
-      for (int i = 0; i < PJ_XCH; ++i) keep(xv[i]);
+      for (int i = 0; i < PJ_XCH / NG; ++i) keep(xv[i]);
     }
     // a split without tiles still holds a partial for each of its rows: the
     // empty one (m = -inf, l = 0), so that the merge reads every split
-    if (g == 0 && qrow < cnt) {
+    if (g == 0 && grp == 0 && qrow < cnt) {
       float* ml = a.ML + ((((int64_t)o * a.S + s) * a.max_sel + qrow) * a.H + h) * 2;
       ml[0] = -INFINITY;
       ml[1] = 0.f;
@@ -456,7 +492,7 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
   }
   settle(c_tile, c_mlo, c_mhi);
   const bool qv = qrow < cnt;
-  if constexpr (PROJ) attn_project<DH>(lds, tid, wave, lane, a.qscale, wv, xv, qreg);
+  if constexpr (PROJ) attn_project<DH, NT>(lds, tid, wave, lane, a.qscale, wv, xv, qreg);
   // i-th visited half tile
   auto half_at = [&](int i) { int v = i + rot; return ub + (v >= nh ? v - nh : v); };
 #pragma unroll
@@ -469,7 +505,132 @@ __global__ __launch_bounds__(256) void k_attn(Rs3ReadoutArgs a, int G) {
   float m_run = -INFINITY, l_run = 0.f;
   const int kbase = (lane & 31) * L::KP + 16 * g;             // + ks*32
   const int vbase = L::KREG + (lane & 31) * L::VP + 16 * g;   // + dt*32*VP + q*32
-  if constexpr (DEEP) {
+  if constexpr (NG == 2) {
+    // Group g takes the pairs p = g, g+2, ... (pair p = half tiles 2p, 2p+1
+    // in stages 2(p&3), 2(p&3)+1), so each group has two stage pairs.
+    // Iteration j: wait for this wave's DMA of its pair p = 2j+g (issued one
+    // iteration earlier); barrier (the group's previous pair is done and its
+    // stages free); issue pair p+2 into them; compute pair p.  Every wave runs
+    // the same iterations, so the barriers match.
+    const int npair = nh >> 1;
+    auto issue_pair = [&](int p) {
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const int v = half_at(2 * p + k);
+        if ((v >> 1) - cbase >= 64) {
+          // (unrotated splits longer than the window) slide it to this tile;
+          // the masks of the pair being computed were read before
+          wait_vmcnt<0>();
+          cbase = v >> 1;
+          c_tile = 0;
+          if (cbase + lane < te) c_tile = gload(&tiles[cbase + lane].tile);
+          const uint64_t mm = cbase + lane < te ? gload(&tiles[cbase + lane].mask) : 0ull;
+          c_mlo = (uint32_t)mm;
+          c_mhi = (uint32_t)(mm >> 32);
+          settle(c_tile, c_mlo, c_mhi);
+        }
+        const int tl = __builtin_amdgcn_readlane(c_tile, (v >> 1) - cbase);
+        attn_issue<DH>(Kh, Vh, tl, v & 1, h, H, lds + (2 * (p & 3) + k) * L::STAGE, wave, doff);
+      }
+    };
+    if (grp < npair) issue_pair(grp);
+    const int nit = (npair + 1) >> 1;
+    for (int j = 0; j < nit; ++j) {
+      const int p = 2 * j + grp;
+      wait_vmcnt<0>();   // this wave's DMA of pair p, the only one in flight
+      stage_barrier();
+      uint32_t mA = 0, mB = 0;
+      if (p < npair) {
+        const int u0 = half_at(2 * p), u1 = half_at(2 * p + 1);
+        const int t0 = (u0 >> 1) - cbase, t1 = (u1 >> 1) - cbase;
+        mA = (u0 & 1) ? __builtin_amdgcn_readlane(c_mhi, t0) : __builtin_amdgcn_readlane(c_mlo, t0);
+        mB = (u1 & 1) ? __builtin_amdgcn_readlane(c_mhi, t1) : __builtin_amdgcn_readlane(c_mlo, t1);
+      }
+      if (p + 2 < npair) issue_pair(p + 2);
+      if ((mA | mB) == 0u) continue;
+      const uint8_t* SA = lds + (2 * (p & 3)) * L::STAGE;
+      const uint8_t* SB = SA + L::STAGE;
+      f32x16 sA, sB;
+      attn_scores_pair<DH>(SA + kbase, SB + kbase, qreg, sA, sB);
+      if (mA != 0xffffffffu) {   // partial or empty half tile (frame boundary)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (!(mA >> c_row(r, lane) & 1u)) sA[r] = -INFINITY;
+      }
+      if (mB != 0xffffffffu) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (!(mB >> c_row(r, lane) & 1u)) sB[r] = -INFINITY;
+      }
+      float mx = __builtin_elementwise_maximum(sA[0], sB[0]);
+#pragma unroll
+      for (int r = 1; r < 16; ++r) mx = max3f(mx, sA[r], sB[r]);
+      mx = max_with_partner(mx);
+      const bool need = mx > m_run + RESCALE_LOG2;   // lazy rescale, as below
+      if (__any(need)) {
+        const float m_new = need ? mx : m_run;
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        l_run *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < DH / 32; ++dt) acc[dt] *= alpha;
+        m_run = m_new;
+      }
+      float psum = 0.f;
+      u32x4 pkA[2], pkB[2];
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          const float a0 = __builtin_amdgcn_exp2f(sA[8 * hf + 2 * jj] - m_run);
+          const float a1 = __builtin_amdgcn_exp2f(sA[8 * hf + 2 * jj + 1] - m_run);
+          const float b0 = __builtin_amdgcn_exp2f(sB[8 * hf + 2 * jj] - m_run);
+          const float b1 = __builtin_amdgcn_exp2f(sB[8 * hf + 2 * jj + 1] - m_run);
+          pkA[hf][jj] = pack_bf16x2(a0, a1);
+          pkB[hf][jj] = pack_bf16x2(b0, b1);
+          psum = add_bf16x2(pkB[hf][jj], add_bf16x2(pkA[hf][jj], psum));
+        }
+      l_run += psum;
+#pragma unroll
+      for (int dt = 0; dt < DH / 32; ++dt) {
+        u32x4 va[4];
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          va[q] = *(const u32x4*)(SA + vbase + dt * 32 * L::VP + q * 32);
+          va[2 + q] = *(const u32x4*)(SB + vbase + dt * 32 * L::VP + q * 32);
+        }
+#pragma unroll
+        for (int q = 0; q < 2; ++q) acc[dt] = mfma32(va[q], pkA[q], acc[dt]);
+#pragma unroll
+        for (int q = 0; q < 2; ++q) acc[dt] = mfma32(va[2 + q], pkB[q], acc[dt]);
+      }
+    }
+    // Group 1 hands its (m, l, O^T) per lane to its partner wave of group 0
+    // through LDS (past the epilogue's row stage), then ends; group 0 merges
+    // the two partials to the larger reference maximum.
+    constexpr int SW = 2 + 16 * (DH / 32);   // floats per lane
+    float* xs = (float*)(lds + 4 * 32 * (DH * 2 + 16)) + wave * SW * 64 + lane;
+    __syncthreads();   // every wave is done with the stages
+    if (grp == 1) {
+      xs[0] = m_run;
+      xs[64] = l_run;
+#pragma unroll
+      for (int dt = 0; dt < DH / 32; ++dt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) xs[(2 + 16 * dt + r) * 64] = acc[dt][r];
+    }
+    __syncthreads();
+    if (grp == 1) return;
+    const float m1 = xs[0], l1 = xs[64];
+    const float mm = __builtin_elementwise_maximum(m_run, m1);
+    const float s0 = mm == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - mm);
+    const float s1 = mm == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - mm);
+    l_run = l_run * s0 + l1 * s1;
+#pragma unroll
+    for (int dt = 0; dt < DH / 32; ++dt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[dt][r] = acc[dt][r] * s0 + xs[(2 + 16 * dt + r) * 64] * s1;
+    m_run = mm;
+  } else if constexpr (DEEP) {
     // the first nst-2 half tiles; each pair iteration prefetches two more
 #pragma unroll
     for (int j = 0; j < nst - 2; ++j)
@@ -851,11 +1012,11 @@ using namespace rs3;
 // attention where its 8 stages fit the LDS (heads of width <= 64).
 constexpr int ATTN_DEEP_MAX_BLOCKS = 256;
 
-template <int DH, bool PROJ, bool DEEP>
+template <int DH, bool PROJ, bool DEEP, int NG = 1>
 static hipError_t launch_attn_dh(const Rs3ReadoutArgs& a, int G, int nblk, hipStream_t st) {
   size_t lds = (size_t)(DEEP ? 8 : 4) * AttnLds<DH>::STAGE;
   if constexpr (PROJ) lds = lds > (size_t)AttnProj<DH>::BYTES ? lds : (size_t)AttnProj<DH>::BYTES;
-  RS3_LAUNCH(RS3_K_ATTN, st, (k_attn<DH, PROJ, DEEP>), dim3(nblk), dim3(256), lds, st, a, G);
+  RS3_LAUNCH(RS3_K_ATTN, st, (k_attn<DH, PROJ, DEEP, NG>), dim3(nblk), dim3(256 * NG), lds, st, a, G);
   return hipGetLastError();
 }
 
@@ -876,10 +1037,10 @@ hipError_t rs3_launch_attn(const Rs3ReadoutArgs& a, hipStream_t st, bool project
   const bool deep = nblk <= ATTN_DEEP_MAX_BLOCKS;
   switch (a.d_h) {
     case 32:
-      if (project) return launch_attn_dh<32, true, true>(a, G, nblk, st);
+      if (project) return launch_attn_dh<32, true, true, 2>(a, G, nblk, st);
       return deep ? launch_attn_dh<32, false, true>(a, G, nblk, st) : launch_attn_dh<32, false, false>(a, G, nblk, st);
     case 64:
-      if (project) return launch_attn_dh<64, true, true>(a, G, nblk, st);
+      if (project) return launch_attn_dh<64, true, true, 2>(a, G, nblk, st);
       return deep ? launch_attn_dh<64, false, true>(a, G, nblk, st) : launch_attn_dh<64, false, false>(a, G, nblk, st);
     case 128: return launch_attn_dh<128, false, false>(a, G, nblk, st);
     case 256: return launch_attn_dh<256, false, false>(a, G, nblk, st);
@@ -953,10 +1114,10 @@ hipError_t rs3_readout_setup() {
     int bytes;
   } attn[] = {{(const void*)k_attn<32, false, false>, 4 * AttnLds<32>::STAGE},
               {(const void*)k_attn<32, false, true>, 8 * AttnLds<32>::STAGE},
-              {(const void*)k_attn<32, true, true>, std::max(8 * AttnLds<32>::STAGE, AttnProj<32>::BYTES)},
+              {(const void*)k_attn<32, true, true, 2>, std::max(8 * AttnLds<32>::STAGE, AttnProj<32>::BYTES)},
               {(const void*)k_attn<64, false, false>, 4 * AttnLds<64>::STAGE},
               {(const void*)k_attn<64, false, true>, 8 * AttnLds<64>::STAGE},
-              {(const void*)k_attn<64, true, true>, std::max(8 * AttnLds<64>::STAGE, AttnProj<64>::BYTES)},
+              {(const void*)k_attn<64, true, true, 2>, std::max(8 * AttnLds<64>::STAGE, AttnProj<64>::BYTES)},
               {(const void*)k_attn<128, false, false>, 4 * AttnLds<128>::STAGE},
               {(const void*)k_attn<256, false, false>, 4 * AttnLds<256>::STAGE}};
   for (const auto& k : attn) {
