@@ -549,8 +549,10 @@ rs3_status rs3_select_workspace_size(const rs3_grid* g, int32_t n_obj, int64_t x
   if (!bytes || !grid_ok(g) || n_obj <= 0 || n_obj > RS3_MAX_OBJ || x_obj_stride < 0) return RS3_E_INVALID;
   const int64_t mn = (int64_t)g->m * g->n;
   const int n_x = x_obj_stride ? n_obj : 1;
-  // energies [n_x][mn] fp64, then per-64-cell energy ranges [n_x][ceil(mn/64)][2]
-  *bytes = align256((size_t)n_x * mn * 8) + (size_t)n_x * ((mn + 63) / 64) * 16;
+  // energies [n_x][mn] fp64, per-64-cell energy ranges [n_x][ceil(mn/64)][2],
+  // then the priors computed beside the energies [n_obj][64][4] u64
+  *bytes = align256((size_t)n_x * mn * 8) + align256((size_t)n_x * ((mn + 63) / 64) * 16) +
+           (size_t)n_obj * 64 * 4 * 8;
   return RS3_OK;
 }
 
@@ -578,8 +580,7 @@ rs3_status rs3_select_queries(const rs3_grid* g, int32_t n_obj, const uint8_t* m
   const int n_x = x_obj_stride ? n_obj : 1;
   double* e = (double*)ws;
   unsigned long long* erange = (unsigned long long*)((uint8_t*)ws + align256((size_t)n_x * mn * 8));
-  hipError_t he = rs3_launch_energy(X, x_obj_stride, n_x, mn, C, dt, e, erange, st);
-  if (he != hipSuccess) return map_err(he);
+  uint64_t* pbits = (uint64_t*)((uint8_t*)erange + align256((size_t)n_x * ((mn + 63) / 64) * 16));
   Rs3SelectArgs a;
   memset(&a, 0, sizeof(a));
   a.masks = masks;
@@ -599,6 +600,14 @@ rs3_status rs3_select_queries(const rs3_grid* g, int32_t n_obj, const uint8_t* m
   a.c = p->c;
   a.x_per_obj = n_x > 1;
   for (int i = 0; i < n_groups; ++i) a.k[i] = k[i];
+  hipError_t he;
+  if (rs3_select_prior_beside(g->m, g->n, g->s)) {
+    a.prior_bits = pbits;
+    he = rs3_launch_energy_prior(X, x_obj_stride, n_x, mn, C, dt, e, erange, a, n_groups, st);
+  } else {
+    he = rs3_launch_energy(X, x_obj_stride, n_x, mn, C, dt, e, erange, st);
+  }
+  if (he != hipSuccess) return map_err(he);
   return map_err(rs3_launch_select(a, n_groups, st));
 }
 

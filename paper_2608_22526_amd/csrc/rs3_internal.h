@@ -164,6 +164,7 @@ struct Rs3SelectArgs {
   int32_t* sel_idx;       // [n_groups][mn]
   int32_t* sel_count;     // [n_groups]
   uint8_t* prior_out;     // [n_groups][mn] or null
+  uint64_t* prior_bits;   // [n_groups][64][4] prior rows computed beside the energies, or null
   int m, n, s, n_obj, union_objects, seed_box, r_s, c, x_per_obj;
   int k[RS3_MAX_OBJ];
 };
@@ -226,6 +227,11 @@ struct AttendPrepArgs {
 hipError_t rs3_launch_energy(const void* X, int64_t x_stride, int n_x, int mn, int C, int dtype,
                              double* e, unsigned long long* range, hipStream_t st);
 hipError_t rs3_launch_select(const Rs3SelectArgs& a, int n_groups, hipStream_t st);
+// Grids for which the prior runs beside the energies (one wave per group).
+bool rs3_select_prior_beside(int m, int n, int s);
+// Energies and the one-wave priors (written to a.prior_bits) in one launch.
+hipError_t rs3_launch_energy_prior(const void* X, int64_t x_stride, int n_x, int mn, int C, int dtype, double* e,
+                                   unsigned long long* range, const Rs3SelectArgs& a, int n_groups, hipStream_t st);
 hipError_t rs3_launch_commit(const Rs3CommitArgs& a, int dtype, int d_kv, int D, int H, int d_h,
                              hipStream_t st);
 // merge = false leaves the split merge of the bf16 path to the caller (the

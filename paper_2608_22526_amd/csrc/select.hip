@@ -55,12 +55,13 @@ __device__ __forceinline__ double energy_chunk<float>(u32x4 w, double acc) {
 // range[xi][block] (energies are >= 0, so bit order is numeric order).
 // C*sizeof(T) is a multiple of 16.
 constexpr int EB_CH = 32;
+// Rows 64*bx .. of grid xi by one 256-thread block (nbx blocks per grid).
 template <typename T>
-__global__ __launch_bounds__(256) void k_energy(const T* __restrict__ X, int64_t x_stride, int mn,
-                                                 int C, double* __restrict__ e,
-                                                 unsigned long long* __restrict__ range) {
+__device__ __forceinline__ void energy_block(const T* __restrict__ X, int64_t x_stride, int mn, int C,
+                                             double* __restrict__ e, unsigned long long* __restrict__ range,
+                                             int bx, int xi, int nbx) {
   __shared__ u32x4 rows[64 * (EB_CH + 1)];
-  const int xi = blockIdx.y, r0 = blockIdx.x * 64, tid = threadIdx.x;
+  const int r0 = bx * 64, tid = threadIdx.x;
   const int nrows = min(64, mn - r0);
   const int cpr = C * (int)sizeof(T) / 16;   // chunks per row
   const u32x4* src = (const u32x4*)(X + (int64_t)xi * x_stride + (int64_t)r0 * C);
@@ -105,10 +106,17 @@ __global__ __launch_bounds__(256) void k_energy(const T* __restrict__ X, int64_t
     hi = oh > hi ? oh : hi;
   }
   if (tid == 0) {
-    unsigned long long* r = range + 2 * ((int64_t)xi * gridDim.x + blockIdx.x);
+    unsigned long long* r = range + 2 * ((int64_t)xi * nbx + bx);
     r[0] = lo;
     r[1] = hi;
   }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_energy(const T* __restrict__ X, int64_t x_stride, int mn,
+                                                 int C, double* __restrict__ e,
+                                                 unsigned long long* __restrict__ range) {
+  energy_block<T>(X, x_stride, mn, C, e, range, blockIdx.x, blockIdx.y, gridDim.x);
 }
 
 
@@ -776,7 +784,12 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(Rs3SelectArgs a) {
   const int W = (a.n + 63) >> 6;
   const bool fast = a.m <= SEL_THREADS && W <= FAST_W;
   uint64_t* Gs = reinterpret_cast<uint64_t*>(base);   // fast path: group prior rows [m][W]
-  if (fast && a.m <= 64 && a.s == 1) {
+  if (fast && a.m <= 64 && a.s == 1 && a.prior_bits) {
+    // the prior (and the tracker update) ran beside the energies
+    const uint64_t* pb = a.prior_bits + (int64_t)g * 64 * FAST_W;
+    if (tid < a.m * W) Gs[tid] = pb[tid];
+    lds_barrier();
+  } else if (fast && a.m <= 64 && a.s == 1) {
     // one wave: lane y owns grid row y
     if (tid < 64) {
       uint64_t gw[FAST_W] = {0, 0, 0, 0};
@@ -1025,6 +1038,36 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(Rs3SelectArgs a) {
   if (tid == 0) a.sel_count[g] = total;
 }
 
+// The energies and, for grids of at most 64 rows and 256 columns at stride 1,
+// the one-wave prior of every group in one launch: the prior depends only on
+// the masks and the tracker state, the energies only on X, so the prior
+// blocks (after the energy blocks) run beside them and leave the group's
+// prior rows [m][W] in prior_bits for the selection.
+template <typename T>
+__global__ __launch_bounds__(256) void k_energy_prior(const T* __restrict__ X, int64_t x_stride, int mn, int C,
+                                                      double* __restrict__ e, unsigned long long* __restrict__ range,
+                                                      Rs3SelectArgs a, int nbx, int n_e) {
+  const int b = blockIdx.x;
+  if (b < n_e) {
+    energy_block<T>(X, x_stride, mn, C, e, range, b % nbx, b / nbx, nbx);
+    return;
+  }
+  const int g = b - n_e, tid = threadIdx.x;
+  if (tid >= 64) return;
+  const int W = (a.n + 63) >> 6;
+  uint64_t gw[FAST_W] = {0, 0, 0, 0};
+  if (a.union_objects) {
+    for (int o = 0; o < a.n_obj; ++o) add_object_prior_wave(a, o, gw);
+  } else {
+    add_object_prior_wave(a, g, gw);
+  }
+  uint64_t* pb = a.prior_bits + (int64_t)g * 64 * FAST_W;
+  if (tid < a.m)
+#pragma unroll
+    for (int q = 0; q < FAST_W; ++q)
+      if (q < W) pb[tid * W + q] = gw[q];
+}
+
 }  // namespace rs3
 
 using namespace rs3;
@@ -1038,6 +1081,21 @@ hipError_t rs3_launch_energy(const void* X, int64_t x_stride, int n_x, int mn, i
   else
     RS3_LAUNCH(RS3_K_ENERGY, st, k_energy<float>, grid, dim3(256), 0, st, (const float*)X, x_stride, mn, C, e,
                range);
+  return hipGetLastError();
+}
+
+bool rs3_select_prior_beside(int m, int n, int s) { return m <= 64 && s == 1 && n <= 64 * FAST_W; }
+
+hipError_t rs3_launch_energy_prior(const void* X, int64_t x_stride, int n_x, int mn, int C, int dtype, double* e,
+                                   unsigned long long* range, const Rs3SelectArgs& a, int n_groups, hipStream_t st) {
+  const int nbx = (mn + 63) / 64, n_e = nbx * n_x;
+  const dim3 grid(n_e + n_groups);
+  if (dtype == RS3_BF16)
+    RS3_LAUNCH(RS3_K_ENERGY, st, k_energy_prior<bf16_t>, grid, dim3(256), 0, st, (const bf16_t*)X, x_stride, mn, C, e,
+               range, a, nbx, n_e);
+  else
+    RS3_LAUNCH(RS3_K_ENERGY, st, k_energy_prior<float>, grid, dim3(256), 0, st, (const float*)X, x_stride, mn, C, e,
+               range, a, nbx, n_e);
   return hipGetLastError();
 }
 
