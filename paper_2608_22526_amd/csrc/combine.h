@@ -124,7 +124,18 @@ __device__ __forceinline__ void combine_block(const Rs3ReadoutArgs& a, int o, in
   if (r0 >= cnt) return;
   // entry i of row r is valid iff it is in range and above its predecessor
   auto entry_ok = [&](int i, int prev, int r) { return i >= 0 && i < a.mn && (r == 0 || prev < i); };
-  if (tid < CB_ROWS && r0 + tid < cnt && !entry_ok(e_cur, e_prv, r0 + tid)) set_err(b.hdr, RS3_E_INVALID);
+  // LDS: Os [CB_ROWS][D+8] bf16 | red [NG][items][10] f32 | kept [CB_ROWS] | sdst [CB_ROWS]
+  bf16_t* Os = (bf16_t*)cl;
+  float* red = (float*)(cl + ((CB_ROWS * OS * 2 + 15) & ~15));
+  int* kept = (int*)(red + (size_t)NG * items * 10);
+  int* sdst = kept + CB_ROWS;
+  // destination cell of each row of the block (-1 = none), kept in LDS for
+  // the output step rather than in registers across the merge
+  if (tid < CB_ROWS) {
+    const bool ok = r0 + tid < cnt && entry_ok(e_cur, e_prv, r0 + tid);
+    if (r0 + tid < cnt && !ok) set_err(b.hdr, RS3_E_INVALID);
+    sdst[tid] = ok ? e_cur : -1;
+  }
   int dst[8];   // destination cell of each accumulator row (-1 = none)
 #pragma unroll
   for (int r = 0; r < 8; ++r) {
@@ -154,10 +165,7 @@ __device__ __forceinline__ void combine_block(const Rs3ReadoutArgs& a, int o, in
     part_load(a, o, r0 + rr, d0, d0 / d_h, grp0, NG, 0, pb);
   }
 
-  // merge.  LDS: Os [CB_ROWS][D+8] bf16 | red [NG][items][10] f32 | kept [CB_ROWS]
-  bf16_t* Os = (bf16_t*)cl;
-  float* red = (float*)(cl + ((CB_ROWS * OS * 2 + 15) & ~15));
-  int* kept = (int*)(red + (size_t)NG * items * 10);
+  // merge
   for (int q = q0; q < items * NG; q += CB_THREADS) {
     const int item = q % items, grp = q / items;
     const int rr = item / cpr, d0 = 8 * (item - rr * cpr), h = d0 / d_h;
@@ -201,7 +209,10 @@ __device__ __forceinline__ void combine_block(const Rs3ReadoutArgs& a, int o, in
   const bf16_t* orow = &Os[(arow ? (lane & 31) : 0) * OS + 8 * g];
   bool keys[8];
 #pragma unroll
-  for (int r = 0; r < 8; ++r) keys[r] = c_row(r, lane) < CB_ROWS && kept[c_row(r, lane)] != 0;
+  for (int r = 0; r < 8; ++r) {
+    keys[r] = c_row(r, lane) < CB_ROWS && kept[c_row(r, lane)] != 0;
+    dst[r] = c_row(r, lane) < CB_ROWS ? sdst[c_row(r, lane)] : -1;
+  }
   for (int nbk = wave; nbk < C / 32; nbk += CB_THREADS / 64) {
     const bool first = nbk == wave;
     const int col = 32 * nbk + (lane & 31);
@@ -235,7 +246,7 @@ __device__ __forceinline__ void combine_block(const Rs3ReadoutArgs& a, int o, in
 __host__ __device__ inline size_t combine_lds_bytes(int D) {
   const int items = CB_ROWS * (D / 8);
   return (((size_t)CB_ROWS * (D + 8) * 2 + 15) & ~(size_t)15) + (size_t)cb_groups(D) * items * 10 * 4 +
-         CB_ROWS * 4;
+         2 * CB_ROWS * 4;
 }
 
 }  // namespace rs3
