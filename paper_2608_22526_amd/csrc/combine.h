@@ -67,28 +67,38 @@ __device__ __forceinline__ void part_load(const Rs3ReadoutArgs& a, int o, int ro
   }
 }
 
-// Online log-sum-exp over a batch: running maximum M, weight W, sum acc.
+// Log-sum-exp merge of a batch into the running maximum M, weight W and sum
+// acc: the batch's largest maximum is found first, so the running sums are
+// rescaled once per batch instead of once per split.  Splits that are off
+// (past S, or empty with l = 0) add nothing; their partial O words are
+// replaced by zero before use, since an empty split leaves its O unwritten.
 __device__ __forceinline__ void part_merge(const PartBatch& pb, int first, int NG, int S, float& M, float& W,
                                            float (&acc)[8]) {
+  bool on[PART_B];
+  float mb = -INFINITY;
 #pragma unroll
   for (int i = 0; i < PART_B; ++i) {
-    const bool on = first + NG * i < S && pb.l[i] > 0.f;
-    const float m = on ? pb.m[i] : -INFINITY;
-    if (m > M) {
-      const float sc = __builtin_amdgcn_exp2f(M - m);
-      W *= sc;
+    on[i] = first + NG * i < S && pb.l[i] > 0.f;
+    mb = __builtin_elementwise_maximum(mb, on[i] ? pb.m[i] : -INFINITY);
+  }
+  if (mb == -INFINITY) return;
+  const float Mn = __builtin_elementwise_maximum(M, mb);
+  const float sc = __builtin_amdgcn_exp2f(M - Mn);   // 0 while M = -inf
+  W *= sc;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] *= sc;
-      M = m;
-    }
-    const float w = on ? __builtin_amdgcn_exp2f(m - M) * pb.l[i] : 0.f;
+  for (int e = 0; e < 8; ++e) acc[e] *= sc;
+#pragma unroll
+  for (int i = 0; i < PART_B; ++i) {
+    const float w = on[i] ? __builtin_amdgcn_exp2f(pb.m[i] - Mn) * pb.l[i] : 0.f;
     W += w;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      acc[2 * e] += on ? w * __uint_as_float(pb.v[i][e] << 16) : 0.f;
-      acc[2 * e + 1] += on ? w * __uint_as_float(pb.v[i][e] & 0xffff0000u) : 0.f;
+      const uint32_t x = on[i] ? pb.v[i][e] : 0u;
+      acc[2 * e] += w * __uint_as_float(x << 16);
+      acc[2 * e + 1] += w * __uint_as_float(x & 0xffff0000u);
     }
   }
+  M = Mn;
 }
 
 // The merge of rows [ry*CB_ROWS, +CB_ROWS) of object o by CB_THREADS threads
