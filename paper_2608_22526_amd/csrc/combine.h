@@ -22,25 +22,31 @@ __device__ __forceinline__ void copy_out<bf16_t>(bf16_t* p, bf16_t x) { *p = x; 
 template <>
 __device__ __forceinline__ void copy_out<float>(float* p, bf16_t x) { *p = bf2f(x); }
 
-// grid (n_obj, ceil(max_sel/16)), block 512.  Every key split of the call
+// grid (n_obj, ceil(max_sel/cb_rows_for(D))), block 512.  Every key split of the call
 // holds a partial for every selected row (the attention writes l = 0 for
 // splits without tiles), so the merge needs nothing from the bank.
 // 1. the row indices are loaded and checked;
 // 2. for each (row, 8-column chunk) item, each of the NG thread groups that
 //    share it loads the (m, l) pairs and partial O chunks of its splits grp,
-//    grp + NG, ... (PART_B per batch, the first batch together with the
+//    grp + NG, ... (PART_B per batch; NG is as large as the threads allow
+//    but no larger than S needs, the first batch together with the
 //    residual inputs and W_o operands) and merges them by log-sum-exp in
 //    registers; the NG groups are merged through LDS, and the normalised
 //    row goes to LDS as bf16;
-// 3. y = x + O W_o on a 32x32x16 MFMA whose rows 16..31 are zero; a row with
+// 3. y = x + O W_o on a 32x32x16 MFMA whose rows past the block's are zero; a row with
 //    no resident key (total weight 0) is returned as x, bit for bit.
-constexpr int CB_ROWS = 16;   // the W_o step maps these rows to accumulator rows r < 8
+// Rows per work-group, at most CB_ROWS (the W_o step maps them to
+// accumulator rows r < 8): 8 at attention widths up to 64, where the merge of
+// many splits dominates and is VALU-bound per work-group, so the rows spread
+// over more CUs; else 16, since every work-group reads all of W_o.
+constexpr int CB_ROWS = 16;
+__host__ __device__ inline int cb_rows_for(int D) { return D <= 64 ? 8 : CB_ROWS; }
 constexpr int CB_THREADS = 512;
 constexpr int PART_B = 8;     // splits per batch of partial loads
 
-__host__ __device__ constexpr int cb_groups(int D) {
-  return CB_THREADS / (CB_ROWS * (D / 8)) < 1 ? 1
-         : (CB_THREADS / (CB_ROWS * (D / 8)) > 8 ? 8 : CB_THREADS / (CB_ROWS * (D / 8)));
+__host__ __device__ constexpr int cb_groups(int D, int rows) {
+  return CB_THREADS / (rows * (D / 8)) < 1 ? 1
+         : (CB_THREADS / (rows * (D / 8)) > 8 ? 8 : CB_THREADS / (rows * (D / 8)));
 }
 
 struct PartBatch {
@@ -101,21 +107,23 @@ __device__ __forceinline__ void part_merge(const PartBatch& pb, int first, int N
   M = Mn;
 }
 
-// The merge of rows [ry*CB_ROWS, +CB_ROWS) of object o by CB_THREADS threads
+// The merge of rows [ry*RB, +RB) of object o, RB = cb_rows_for(D), by CB_THREADS threads
 // (threadIdx.x < CB_THREADS), cl: combine_lds_bytes(D) bytes of LDS.
 template <typename OutT>
 __device__ __forceinline__ void combine_block(const Rs3ReadoutArgs& a, int o, int ry, uint8_t* cl) {
-  const int r0 = ry * CB_ROWS;
+  const int RB = cb_rows_for(a.D);
+  const int r0 = ry * RB;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5;
   const int D = a.D, C = a.C, d_h = a.d_h, S = a.S, OS = D + 8;
-  const int cpr = D / 8, items = CB_ROWS * cpr, NG = cb_groups(D);
+  const int cpr = D / 8, items = RB * cpr;
+  const int NG = min(cb_groups(D, RB), max(1, (S + PART_B - 1) / PART_B));   // thread groups per item
   const int nb = (S + NG * PART_B - 1) / (NG * PART_B);   // batches per item
   const int32_t* sel = a.sel_idx + (int64_t)o * a.sel_stride;
   const bf16_t* X = (const bf16_t*)a.X + (int64_t)o * a.x_stride;
   const bf16_t* WoT = (const bf16_t*)a.WoT;
 
   // 1. The list entries of this lane's accumulator rows r < 8 (rows
-  //    8*(r/4) + 4*g + r%4 < CB_ROWS) and their predecessors (ascending
+  //    8*(r/4) + 4*g + r%4 < RB) and their predecessors (ascending
   //    check), and of row r0 + tid for the error report: the only loads
   //    before the row decisions, so waiting for them waits for nothing else.
   int srow[8], sprv[8];
@@ -125,7 +133,7 @@ __device__ __forceinline__ void combine_block(const Rs3ReadoutArgs& a, int o, in
     srow[r] = gload(sel + rc);
     sprv[r] = gload(sel + max(rc - 1, 0));
   }
-  const int erc = min(r0 + (tid & (CB_ROWS - 1)), a.max_sel - 1);
+  const int erc = min(r0 + (tid & (RB - 1)), a.max_sel - 1);
   const int e_cur = gload(sel + erc), e_prv = gload(sel + max(erc - 1, 0));
   BankDev& b = *a.banks[o];
   // the merge covers every selected row: it reports a count past max_sel and
@@ -141,7 +149,7 @@ __device__ __forceinline__ void combine_block(const Rs3ReadoutArgs& a, int o, in
   int* sdst = kept + CB_ROWS;
   // destination cell of each row of the block (-1 = none), kept in LDS for
   // the output step rather than in registers across the merge
-  if (tid < CB_ROWS) {
+  if (tid < RB) {
     const bool ok = r0 + tid < cnt && entry_ok(e_cur, e_prv, r0 + tid);
     if (r0 + tid < cnt && !ok) set_err(b.hdr, RS3_E_INVALID);
     sdst[tid] = ok ? e_cur : -1;
@@ -150,7 +158,7 @@ __device__ __forceinline__ void combine_block(const Rs3ReadoutArgs& a, int o, in
 #pragma unroll
   for (int r = 0; r < 8; ++r) {
     const int row = r0 + c_row(r, lane);
-    dst[r] = (c_row(r, lane) < CB_ROWS && row < cnt && entry_ok(srow[r], sprv[r], row)) ? srow[r] : -1;
+    dst[r] = (c_row(r, lane) < RB && row < cnt && entry_ok(srow[r], sprv[r], row)) ? srow[r] : -1;
   }
   // 2. Every data load in one batch: residual inputs of the wave's first
   //    column block, its first W_o operands, and this thread's first item's
@@ -172,7 +180,7 @@ __device__ __forceinline__ void combine_block(const Rs3ReadoutArgs& a, int o, in
   {
     const int item0 = q0 % items, grp0 = q0 / items;
     const int rr = item0 / cpr, d0 = 8 * (item0 - rr * cpr);
-    part_load(a, o, r0 + rr, d0, d0 / d_h, grp0, NG, 0, pb);
+    if (q0 < items * NG) part_load(a, o, r0 + rr, d0, d0 / d_h, grp0, NG, 0, pb);
   }
 
   // merge
@@ -215,13 +223,13 @@ __device__ __forceinline__ void combine_block(const Rs3ReadoutArgs& a, int o, in
   lds_barrier();
   // 3. y = x + O W_o for the block's rows, columns split over the waves
   OutT* Y = (OutT*)a.Y + (int64_t)o * a.y_stride;
-  const bool arow = (lane & 31) < CB_ROWS;
+  const bool arow = (lane & 31) < RB;
   const bf16_t* orow = &Os[(arow ? (lane & 31) : 0) * OS + 8 * g];
   bool keys[8];
 #pragma unroll
   for (int r = 0; r < 8; ++r) {
-    keys[r] = c_row(r, lane) < CB_ROWS && kept[c_row(r, lane)] != 0;
-    dst[r] = c_row(r, lane) < CB_ROWS ? sdst[c_row(r, lane)] : -1;
+    keys[r] = c_row(r, lane) < RB && kept[c_row(r, lane)] != 0;
+    dst[r] = c_row(r, lane) < RB ? sdst[c_row(r, lane)] : -1;
   }
   for (int nbk = wave; nbk < C / 32; nbk += CB_THREADS / 64) {
     const bool first = nbk == wave;
@@ -254,8 +262,8 @@ __device__ __forceinline__ void combine_block(const Rs3ReadoutArgs& a, int o, in
 }
 
 __host__ __device__ inline size_t combine_lds_bytes(int D) {
-  const int items = CB_ROWS * (D / 8);
-  return (((size_t)CB_ROWS * (D + 8) * 2 + 15) & ~(size_t)15) + (size_t)cb_groups(D) * items * 10 * 4 +
+  const int rb = cb_rows_for(D), items = rb * (D / 8);
+  return (((size_t)CB_ROWS * (D + 8) * 2 + 15) & ~(size_t)15) + (size_t)cb_groups(D, rb) * items * 10 * 4 +
          2 * CB_ROWS * 4;
 }
 

@@ -1090,7 +1090,7 @@ hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st
     return hipSuccess;
   }
   const size_t lds = combine_lds_bytes(a.D);
-  const dim3 cgrid(a.n_obj, (a.max_sel + CB_ROWS - 1) / CB_ROWS);
+  const dim3 cgrid(a.n_obj, (a.max_sel + cb_rows_for(a.D) - 1) / cb_rows_for(a.D));
   if (a.y_fp32)
     RS3_LAUNCH(RS3_K_COMBINE, st, k_combine<float>, cgrid, dim3(CB_THREADS), lds, st, a);
   else
