@@ -242,42 +242,6 @@ __device__ __forceinline__ void rebuild_tiles(const BankDev& b, const int32_t* s
   if (tid == 0) b.hdr[HDR_NTILES] = ntot;
 }
 
-// 16-byte chunks of a 64-row stage per thread of a CP_THREADS work-group
-// (d_kv <= 256).
-constexpr int CP_PRE = (64 * 32 + CP_THREADS - 1) / CP_THREADS;
-
-// Loads of the key and value rows of the kept cells src[0 .. rows-1] (bf16
-// memory tokens) into the append's row stage (rows_lds, as append_bf16 lays
-// it out; zero past the rows), by the CP_THREADS threads of a work-group.
-__device__ __forceinline__ void append_gather(const Rs3CommitArgs& a, const BankDev& b, int o, int rows,
-                                              const int* src, bf16_t* rows_lds) {
-  const int d_kv = b.d_kv, cpr = d_kv / 8, RS = d_kv + 8;
-  const bf16_t* Km = (const bf16_t*)a.Kmem + (int64_t)o * a.kv_stride;
-  const bf16_t* Vm = (const bf16_t*)a.Vmem + (int64_t)o * a.kv_stride;
-  u32x4 pk[CP_PRE], pv[CP_PRE];
-#pragma unroll
-  for (int i = 0; i < CP_PRE; ++i) {
-    const int q = threadIdx.x + i * CP_THREADS;
-    const int r = q / cpr, c = q - r * cpr;
-    pk[i] = u32x4{0, 0, 0, 0};
-    pv[i] = u32x4{0, 0, 0, 0};
-    if (q < 64 * cpr && r < rows) {
-      const int cell = src[r];
-      pk[i] = *(const u32x4*)(Km + (int64_t)cell * d_kv + 8 * c);
-      pv[i] = *(const u32x4*)(Vm + (int64_t)cell * d_kv + 8 * c);
-    }
-  }
-#pragma unroll
-  for (int i = 0; i < CP_PRE; ++i) {
-    const int q = threadIdx.x + i * CP_THREADS;
-    const int r = q / cpr, c = q - r * cpr;
-    if (q < 64 * cpr) {
-      *(u32x4*)(rows_lds + r * RS + 8 * c) = pk[i];
-      *(u32x4*)(rows_lds + 64 * RS + r * RS + 8 * c) = pv[i];
-    }
-  }
-}
-
 // ---------------------------------------------------------------------------
 // Append of rows r0 .. r0+rows-1 of the new frame (ring rows start + r0 + r)
 // by the NT threads of a work-group.  src[r] (LDS) is the kept cell of row
@@ -292,7 +256,7 @@ __device__ __forceinline__ void append_gather(const Rs3CommitArgs& a, const Bank
 // rows_lds: 2 * 64 * (d_kv + 8) bf16.
 template <int NT>
 __device__ __forceinline__ void append_bf16(const Rs3CommitArgs& a, const BankDev& b, int o, int start, int r0,
-                                            int rows, const int* src, bf16_t* rows_lds, bool gathered = false) {
+                                            int rows, const int* src, bf16_t* rows_lds) {
   constexpr int NW = NT / 64;
   const int d_kv = b.d_kv, d_h = b.d_h, H = b.H, D = H * d_h;
   const int lg_dh = 31 - __clz(d_h);
@@ -305,16 +269,7 @@ __device__ __forceinline__ void append_bf16(const Rs3CommitArgs& a, const BankDe
   bf16_t* Kr = (bf16_t*)b.Kraw;
   bf16_t* Vr = (bf16_t*)b.Vraw;
   const int cpr = d_kv / 8;
-  if (gathered) {
-    // the rows are in the stage already (append_gather): copy them to the ring
-    for (int q = tid; q < rows * cpr; q += NT) {
-      const int r = q / cpr, c = q - r * cpr;
-      const int64_t j = start + r0 + r;
-      *(u32x4*)(Kr + j * d_kv + 8 * c) = *(const u32x4*)(sK + r * RS + 8 * c);
-      *(u32x4*)(Vr + j * d_kv + 8 * c) = *(const u32x4*)(sV + r * RS + 8 * c);
-    }
-  }
-  for (int q = gathered ? 64 * cpr : tid; q < 64 * cpr; q += NT) {
+  for (int q = tid; q < 64 * cpr; q += NT) {
     const int r = q / cpr, c = q - r * cpr;
     u32x4 kv = {0, 0, 0, 0}, vv = {0, 0, 0, 0};
     if (r < rows) {
@@ -585,21 +540,6 @@ __device__ __forceinline__ void commit_block(const Rs3CommitArgs& a, int o, int 
     before = c0 < mn ? c0 : mn;
     total = mn;
   }
-  // The kept cells of an append block's first 64 rows follow from the mask
-  // alone: their key/value rows are loaded into the row stage now, so that
-  // the gather overlaps the frame-table loads and the placement.
-  const int rpre = (y - 1) * a.rows_per_wg;
-  const bool pre = BF16 && y > 0 && !a.from_ring && rpre < total;
-  if (pre) {
-    int k = before;
-    for (int j = 0; j < cpt; ++j)
-      if (bits >> j & 1) {
-        if (k >= rpre && k < rpre + 64) spos[k - rpre] = c0 + j;
-        ++k;
-      }
-    lds_barrier();
-    append_gather(a, b, o, min(64, total - rpre), spos, (bf16_t*)stage);
-  }
   if (tid < 4 * f_max) sfr[tid] = fr_w;
   lds_barrier();
   if (tid < 64) {
@@ -641,20 +581,19 @@ __device__ __forceinline__ void commit_block(const Rs3CommitArgs& a, int o, int 
   const int start = sh.start;
   const int r_end = min(total, y * a.rows_per_wg);
   for (int r0 = (y - 1) * a.rows_per_wg; r0 < r_end; r0 += 64) {
-    const bool gathered = pre && r0 == rpre;   // spos and the rows are in place
-    if (!gathered) {   // kept cells of rows r0 .. r0+63
+    {   // kept cells of rows r0 .. r0+63
       int k = before;
       for (int j = 0; j < cpt; ++j)
         if (bits >> j & 1) {
           if (k >= r0 && k < r0 + 64) spos[k - r0] = c0 + j;
           ++k;
         }
-      lds_barrier();
     }
+    lds_barrier();
     const int rows = min(64, total - r0);
     if (tid < rows) b.pos[start + r0 + tid] = spos[tid];
     if constexpr (BF16)
-      append_bf16<CP_THREADS>(a, b, o, start, r0, rows, spos, (bf16_t*)stage, gathered);
+      append_bf16<CP_THREADS>(a, b, o, start, r0, rows, spos, (bf16_t*)stage);
     else
       append_f32<CP_THREADS>(a, b, o, start, r0, rows, spos, (float*)stage, (float*)stage + 64 * F32_SP);
     __syncthreads();   // the next round rewrites spos and the row stage
