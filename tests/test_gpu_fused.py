@@ -3,8 +3,8 @@ merge and the commit sharing one launch) through the C ABI against the fp64
 oracle: outputs within 2e-2 (bf16) or 1e-4 (fp32), unselected rows
 bit-identical, banks bit-exact after every fused call, for one object in
 both layer modes, eight objects with per-object lists and out-of-place
-outputs, fp32 outputs, a rotary layer, the fp32 path (no merge launch) and a
-frame with an empty selection."""
+outputs, fp32 outputs, a rotary layer, the fp32 path (no merge launch), a frame
+with an empty selection, and forced key-split counts from 1 to 100."""
 from dataclasses import replace
 
 import numpy as np
@@ -60,3 +60,13 @@ def test_fused_empty_selection():
     r.commit(0, True)
     for t in range(1, 5):
         r.select_readout(t, fused=True)
+
+
+@pytest.mark.parametrize("absorb", [True, False])
+@pytest.mark.parametrize("n_splits", [1, 3, 9, 40, 100])
+def test_fused_forced_splits(absorb, n_splits):
+    # forced key-split counts: one split, fewer splits than a merge batch,
+    # several merge batches per thread group (S > 8 NG), and more splits
+    # than resident tiles (empty splits with l = 0, whose O is never written)
+    cfg = replace(CONFIGS["sam2_single"], m=32, n=32, f_max=4, cap_frames=4)
+    _fused_run(cfg, 6, 2, rows=64, absorb=absorb, n_splits=n_splits)
