@@ -299,8 +299,10 @@ __device__ __forceinline__ void append_bf16(const Rs3CommitArgs& a, const BankDe
       const int j = start + r0 + r;
       *(u32x4*)(Kh + ((int64_t)(j >> 6) * KT + (j & 63)) * d_kv + 8 * c) = *(const u32x4*)(sK + r * RS + 8 * c);
     }
+    // consecutive lanes take consecutive keys of one V^ row, so that a
+    // wave's stores fall in one or two 128-byte lines of the tile
     for (int q = tid; q < rows * d_kv; q += NT) {
-      const int r = q / d_kv, d = q - r * d_kv;
+      const int d = q / rows, r = q - d * rows;
       const int j = start + r0 + r;
       Vh[((int64_t)(j >> 6) * d_kv + d) * KT + vslot(j & 63)] = sV[r * RS + d];
     }
