@@ -22,7 +22,7 @@ __device__ __forceinline__ void copy_out<bf16_t>(bf16_t* p, bf16_t x) { *p = x; 
 template <>
 __device__ __forceinline__ void copy_out<float>(float* p, bf16_t x) { *p = bf2f(x); }
 
-// grid (n_obj, ceil(max_sel/cb_rows_for(D))), block 512.  Every key split of the call
+// grid (n_obj, ceil(max_sel/cb_rows_for(D, n_obj, max_sel))), block 512.  Every key split of the call
 // holds a partial for every selected row (the attention writes l = 0 for
 // splits without tiles), so the merge needs nothing from the bank.
 // 1. the row indices are loaded and checked;
@@ -36,11 +36,15 @@ __device__ __forceinline__ void copy_out<float>(float* p, bf16_t x) { *p = bf2f(
 // 3. y = x + O W_o on a 32x32x16 MFMA whose rows past the block's are zero; a row with
 //    no resident key (total weight 0) is returned as x, bit for bit.
 // Rows per work-group, at most CB_ROWS (the W_o step maps them to
-// accumulator rows r < 8): 8 at attention widths up to 64, where the merge of
-// many splits dominates and is VALU-bound per work-group, so the rows spread
-// over more CUs; else 16, since every work-group reads all of W_o.
+// accumulator rows r < 8).  8 at attention widths up to 64 when the call's
+// 8-row blocks fit the chip's 256 CUs at once: the merge of many splits is
+// VALU-bound per work-group, so the rows spread over more CUs.  Else 16,
+// since every work-group reads all of W_o and larger grids gain nothing from
+// smaller blocks.
 constexpr int CB_ROWS = 16;
-__host__ __device__ inline int cb_rows_for(int D) { return D <= 64 ? 8 : CB_ROWS; }
+__host__ __device__ inline int cb_rows_for(int D, int n_obj, int max_sel) {
+  return D <= 64 && (int64_t)n_obj * ((max_sel + 7) / 8) <= 256 ? 8 : CB_ROWS;
+}
 constexpr int CB_THREADS = 512;
 constexpr int PART_B = 8;     // splits per batch of partial loads
 
@@ -107,11 +111,11 @@ __device__ __forceinline__ void part_merge(const PartBatch& pb, int first, int N
   M = Mn;
 }
 
-// The merge of rows [ry*RB, +RB) of object o, RB = cb_rows_for(D), by CB_THREADS threads
+// The merge of rows [ry*RB, +RB) of object o, RB = cb_rows_for(D, n_obj, max_sel), by CB_THREADS threads
 // (threadIdx.x < CB_THREADS), cl: combine_lds_bytes(D) bytes of LDS.
 template <typename OutT>
 __device__ __forceinline__ void combine_block(const Rs3ReadoutArgs& a, int o, int ry, uint8_t* cl) {
-  const int RB = cb_rows_for(a.D);
+  const int RB = cb_rows_for(a.D, a.n_obj, a.max_sel);
   const int r0 = ry * RB;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5;
   const int D = a.D, C = a.C, d_h = a.d_h, S = a.S, OS = D + 8;
@@ -262,9 +266,12 @@ __device__ __forceinline__ void combine_block(const Rs3ReadoutArgs& a, int o, in
 }
 
 __host__ __device__ inline size_t combine_lds_bytes(int D) {
-  const int rb = cb_rows_for(D), items = rb * (D / 8);
-  return (((size_t)CB_ROWS * (D + 8) * 2 + 15) & ~(size_t)15) + (size_t)cb_groups(D, rb) * items * 10 * 4 +
-         2 * CB_ROWS * 4;
+  size_t red = 0;   // the larger of the two row counts' merge buffers
+  for (int rb = 8; rb <= CB_ROWS; rb *= 2) {
+    const size_t b = (size_t)cb_groups(D, rb) * rb * (D / 8) * 10 * 4;
+    red = b > red ? b : red;
+  }
+  return (((size_t)CB_ROWS * (D + 8) * 2 + 15) & ~(size_t)15) + red + 2 * CB_ROWS * 4;
 }
 
 }  // namespace rs3

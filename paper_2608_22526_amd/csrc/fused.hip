@@ -53,7 +53,7 @@ hipError_t rs3_fused_setup() {
 }
 
 hipError_t rs3_launch_merge_commit(const Rs3ReadoutArgs& ra, const Rs3CommitArgs& ca, int d_kv, hipStream_t st) {
-  const int rb = cb_rows_for(ra.D), n_cb = ra.n_obj * ((ra.max_sel + rb - 1) / rb);
+  const int rb = cb_rows_for(ra.D, ra.n_obj, ra.max_sel), n_cb = ra.n_obj * ((ra.max_sel + rb - 1) / rb);
   const int mn = ca.m * ca.n;
   Rs3CommitArgs c = ca;
   c.rows_per_wg = commit_rows_per_wg(ca.n_obj, mn);

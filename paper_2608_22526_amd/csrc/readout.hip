@@ -866,7 +866,7 @@ __global__ __launch_bounds__(256 * NG) void k_attn(Rs3ReadoutArgs a, int G) {
 }
 
 // ---------------------------------------------------------------------------
-// grid (n_obj, ceil(max_sel/16)), block CB_THREADS: one merge block each.
+// grid (n_obj, ceil(max_sel/cb_rows_for(D, n_obj, max_sel))), block CB_THREADS: one merge block each.
 template <typename OutT>
 __global__ __launch_bounds__(CB_THREADS) void k_combine(Rs3ReadoutArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t cl[];
@@ -1090,7 +1090,8 @@ hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st
     return hipSuccess;
   }
   const size_t lds = combine_lds_bytes(a.D);
-  const dim3 cgrid(a.n_obj, (a.max_sel + cb_rows_for(a.D) - 1) / cb_rows_for(a.D));
+  const int rb = cb_rows_for(a.D, a.n_obj, a.max_sel);
+  const dim3 cgrid(a.n_obj, (a.max_sel + rb - 1) / rb);
   if (a.y_fp32)
     RS3_LAUNCH(RS3_K_COMBINE, st, k_combine<float>, cgrid, dim3(CB_THREADS), lds, st, a);
   else
