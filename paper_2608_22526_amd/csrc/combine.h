@@ -28,11 +28,11 @@ __device__ __forceinline__ void copy_out<float>(float* p, bf16_t x) { *p = bf2f(
 // 1. the row indices are loaded and checked;
 // 2. for each (row, 8-column chunk) item, each of the NG thread groups that
 //    share it loads the (m, l) pairs and partial O chunks of its splits grp,
-//    grp + NG, ... (PART_B per batch; NG is as large as the threads allow
-//    but no larger than S needs, the first batch together with the
+//    grp + NG, ... (PART_B per batch, the first batch together with the
 //    residual inputs and W_o operands) and merges them by log-sum-exp in
-//    registers; the NG groups are merged through LDS, and the normalised
-//    row goes to LDS as bf16;
+//    registers; NG is as large as the threads allow but no larger than S
+//    needs.  The NG groups are merged through LDS, and the normalised row
+//    goes to LDS as bf16;
 // 3. y = x + O W_o on a 32x32x16 MFMA whose rows past the block's are zero; a row with
 //    no resident key (total weight 0) is returned as x, bit for bit.
 // Rows per work-group, at most CB_ROWS (the W_o step maps them to
