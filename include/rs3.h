@@ -34,6 +34,11 @@
  *    unchanged (commit) or skips the offending rows (readout).  The word keeps
  *    the first error; rs3_bank_error reads it.  HIP failures map to
  *    RS3_E_DEVICE (launch/copy) or RS3_E_OOM (allocation).
+ *  - Token tensors (X, Y, the memory tokens, the rs3_attend operands) and
+ *    workspaces are moved in 16-byte vectors: their base pointers must be
+ *    16-byte aligned and per-object strides whole multiples of 16 bytes, else
+ *    RS3_E_INVALID (torch allocations and contiguous slices of whole grids
+ *    meet this).
  *  - A handle must not be used from two streams at once.
  */
 #ifndef RS3_H
@@ -87,7 +92,13 @@ const char* rs3_status_str(rs3_status s);
  * Holds, per object, the last non-empty bounding box in pixel coordinates
  * (inclusive), the count of consecutive empty frames and whether a box was
  * ever seen.  Created zeroed (no box).  export/import copy
- * int32 [n_obj][RS3_TRACK_WORDS] host arrays and synchronise the device. */
+ * int32 [n_obj][RS3_TRACK_WORDS] host arrays and synchronise the device
+ * (checkpoint and resume).  import accepts only states the tracker update
+ * reaches, else RS3_E_INVALID with the state unchanged: has_box 0 or 1;
+ * streak in [0, 2^30]; with has_box = 1, 0 <= y0 <= y1 < 2^30 and
+ * 0 <= x0 <= x1 < 2^30; with has_box = 0, a zero box.  (The tracker does not
+ * know the grid: a box past the pixel grid of a later select is clipped to
+ * the grid when the prior is drawn.) */
 rs3_status rs3_track_create(int32_t n_obj, rs3_track** out);
 void rs3_track_destroy(rs3_track* t);
 rs3_status rs3_track_export(const rs3_track* t, int32_t* state /*[host]*/);

@@ -26,7 +26,8 @@ choice is not.
 from .geometry import Track, bbox, down_s, down_s_box, fill_box, dilate, prior_object  # noqa: F401
 from .select import energy, topk_keep, select_queries  # noqa: F401
 from .rope import axial_table, table_from_pairs, rotate, rotate_heads  # noqa: F401
-from .readout import project_bank, attention_weights, readout, readout_dense, attend  # noqa: F401
+from .readout import (project_bank, rotate_keys, attention_weights, readout, readout_dense,  # noqa: F401
+                      readout_dense_projected, attend)
 from .write import write_keepset  # noqa: F401
 from .post import close_square, palette, close_masks  # noqa: F401
 from .bank import compact, RingBank, FrameListBank, RS3_OK, RS3_E_INVALID, RS3_E_CAPACITY  # noqa: F401

@@ -91,6 +91,16 @@ def readout_dense(X, Kraw, Vraw, Wq, Wk, Wv, Wo, H: int, rope=None, kpos=None, q
         return X.copy()
     Kh, Vh = project_bank(Kraw, Vraw, Wk, Wv)
     Kh = rotate_keys(Kh, rope, kpos, H)
+    return readout_dense_projected(X, Kh, Vh, Wq, Wo, H, rope=rope, qpos=qpos)
+
+
+def readout_dense_projected(X, Kh, Vh, Wq, Wo, H: int, rope=None, qpos=None) -> np.ndarray:
+    """The whole-matrix layer of `readout_dense` on a bank already in the
+    attention space (K^ turned by its cells when there is a table), so that
+    callers can evaluate many row blocks against one projection."""
+    X = np.asarray(X, np.float64)
+    if Kh.shape[0] == 0:
+        return X.copy()
     Q = X @ np.asarray(Wq, np.float64)
     if rope is not None:
         qpos = np.arange(X.shape[0]) if qpos is None else np.asarray(qpos, dtype=np.int64)

@@ -5,6 +5,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
 #include <vector>
 
 #include "rs3_internal.h"
@@ -62,6 +63,11 @@ bool grid_ok(const rs3_grid* g) {
 }
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Token tensors are read and written in 16-byte vectors: their base pointers
+// must be 16-byte aligned and their per-object strides whole 16-byte units.
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+bool stride16(int64_t elems, size_t es) { return ((uint64_t)elems * es) % 16 == 0; }
 
 // Transpose a row-major [rows][cols] host matrix of `es`-byte elements.
 std::vector<uint8_t> transpose(const void* src, int rows, int cols, size_t es) {
@@ -147,6 +153,21 @@ rs3_status rs3_track_export(const rs3_track* t, int32_t* state) {
 
 rs3_status rs3_track_import(rs3_track* t, const int32_t* state) {
   if (!t || !state) return RS3_E_INVALID;
+  // only states the tracker update reaches: has_box 0 or 1, a streak in
+  // [0, 2^30], an ordered non-negative box when has_box is set (pixel
+  // coordinates below 2^30) and a zero box before any box was seen
+  constexpr int32_t LIM = 1 << 30;
+  for (int o = 0; o < t->n_obj; ++o) {
+    const int32_t* w = state + o * RS3_TRACK_WORDS;
+    const int32_t y0 = w[0], x0 = w[1], y1 = w[2], x1 = w[3], streak = w[4], has = w[5];
+    if (has != 0 && has != 1) return RS3_E_INVALID;
+    if (streak < 0 || streak > LIM) return RS3_E_INVALID;
+    if (has) {
+      if (y0 < 0 || x0 < 0 || y0 > y1 || x0 > x1 || y1 >= LIM || x1 >= LIM) return RS3_E_INVALID;
+    } else if (y0 != 0 || x0 != 0 || y1 != 0 || x1 != 0) {
+      return RS3_E_INVALID;
+    }
+  }
   hipError_t e = hipDeviceSynchronize();
   if (e == hipSuccess)
     e = hipMemcpy(t->d_state, state, (size_t)t->n_obj * RS3_TRACK_WORDS * 4, hipMemcpyHostToDevice);
@@ -567,6 +588,7 @@ rs3_status rs3_select_queries(const rs3_grid* g, int32_t n_obj, const uint8_t* m
   const int mn = g->m * g->n;
   if (x_obj_stride < 0 || (x_obj_stride != 0 && x_obj_stride < (int64_t)mn * C)) return RS3_E_INVALID;
   if (x_obj_stride != 0 && p->union_objects && n_obj > 1) return RS3_E_INVALID;
+  if (!aligned16(X) || !stride16(x_obj_stride, dtype_size(dt))) return RS3_E_INVALID;
   if (p->r_s < 0 || p->c < 0) return RS3_E_INVALID;
   const int n_groups = p->union_objects ? 1 : n_obj;
   for (int i = 0; i < n_groups; ++i)
@@ -665,6 +687,7 @@ rs3_status rs3_attend(const void* Qh, const void* Kh, const void* Vh, int32_t n_
   if (!attend_shape(n_q, n_kv, H, d_h, dt, n_splits, &L)) return RS3_E_INVALID;
   if ((n_q > 0 && (!Qh || !O)) || (n_kv > 0 && (!Kh || !Vh))) return RS3_E_INVALID;
   if (dt == RS3_BF16 && (!ws || ws_bytes < L.total)) return RS3_E_INVALID;
+  if (!aligned16(Qh) || !aligned16(Kh) || !aligned16(Vh) || !aligned16(O) || !aligned16(ws)) return RS3_E_INVALID;
   rs3_status st0 = ensure_setup();
   if (st0 != RS3_OK) return st0;
   hipStream_t st = (hipStream_t)stream;
@@ -766,7 +789,7 @@ static rs3_status readout_args(const rs3_layer* L, const rs3_grid* g, int32_t n_
                                int64_t x_obj_stride, rs3_bank* const* banks, const int32_t* sel_idx,
                                const int32_t* sel_count, int32_t sel_stride, int32_t max_sel, int32_t n_splits,
                                void* Y, int64_t y_obj_stride, int32_t y_fp32, void* ws, size_t ws_bytes,
-                               Rs3ReadoutArgs& a) {
+                               Rs3ReadoutArgs& a, bool fit_splits = false) {
   if (!L || !grid_ok(g) || !X || !banks || !sel_idx || !sel_count || !Y) return RS3_E_INVALID;
   if (n_obj <= 0 || n_obj > RS3_MAX_OBJ) return RS3_E_INVALID;
   const LayerDev& ld = L->dev;
@@ -778,6 +801,10 @@ static rs3_status readout_args(const rs3_layer* L, const rs3_grid* g, int32_t n_
   if (x_obj_stride < 0 || (x_obj_stride != 0 && x_obj_stride < grid_elems)) return RS3_E_INVALID;
   if (n_obj > 1 && y_obj_stride < grid_elems) return RS3_E_INVALID;
   if (y_obj_stride < 0) return RS3_E_INVALID;
+  const size_t y_es = (y_fp32 || ld.dtype == RS3_F32) ? 4 : 2;
+  if (!aligned16(X) || !aligned16(Y) || !stride16(x_obj_stride, dtype_size(ld.dtype)) ||
+      !stride16(y_obj_stride, y_es))
+    return RS3_E_INVALID;
   for (int o = 0; o < n_obj; ++o) {
     if (!banks[o] || banks[o]->L != L) return RS3_E_INVALID;
     for (int p = 0; p < o; ++p)
@@ -795,9 +822,15 @@ static rs3_status readout_args(const rs3_layer* L, const rs3_grid* g, int32_t n_
     const double kb = (double)banks[o]->host.cap * ld.dah * 4;
     if (kb > kv_bytes) kv_bytes = kb;
   }
-  const int S = splits_for(L, n_obj, max_sel, n_splits, kv_bytes);
+  int S = splits_for(L, n_obj, max_sel, n_splits, kv_bytes);
   size_t q, o_b, ml;
   readout_shape(L, n_obj, max_sel, S, &q, &o_b, &ml);
+  // fit_splits (automatic count into a fixed workspace): fewer key splits
+  // until the partials fit
+  while (fit_splits && n_splits == 0 && S > 1 && q + o_b + ml > ws_bytes) {
+    --S;
+    readout_shape(L, n_obj, max_sel, S, &q, &o_b, &ml);
+  }
   if (ld.dtype == RS3_BF16 && (!ws || ws_bytes < q + o_b + ml)) return RS3_E_INVALID;
   memset(&a, 0, sizeof(a));
   for (int o = 0; o < n_obj; ++o) a.banks[o] = banks[o]->d_desc;
@@ -887,6 +920,7 @@ static rs3_status commit_args(rs3_bank* const* banks, int32_t n_obj, const rs3_g
   const LayerDev& ld = L->dev;
   if (n_obj > 1 && kv_obj_stride < (int64_t)mn * ld.d_kv) return RS3_E_INVALID;
   if (kv_obj_stride < 0) return RS3_E_INVALID;
+  if (!aligned16(Kmem) || !aligned16(Vmem) || !stride16(kv_obj_stride, dtype_size(ld.dtype))) return RS3_E_INVALID;
   if (ld.rope && (g->m != ld.rope_m || g->n != ld.rope_n)) return RS3_E_INVALID;
   for (int o = 0; o < n_obj; ++o) {
     if (!banks[o] || banks[o]->L != L) return RS3_E_INVALID;

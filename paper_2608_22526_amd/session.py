@@ -1,7 +1,13 @@
 """Convenience owner of the handles and device buffers for one stream of
-frames (argument marshalling only; all work runs in librs3.so)."""
+frames (argument marshalling only; all work runs in librs3.so).
+
+The per-frame calls keep their argument objects (grid and parameter structs,
+the bank handle array, the keep-budget array and the bound C functions)
+across calls, so that a frame costs the host two foreign calls and little
+else."""
 from __future__ import annotations
 
+import ctypes
 from typing import Optional, Sequence
 
 import numpy as np
@@ -60,33 +66,79 @@ class Session:
         self.ws_sel = torch.zeros(max(ws, 8), dtype=torch.uint8, device=device)
         wr = B.readout_workspace_size(self.layer, n_obj, self.max_sel, n_splits)
         self.ws_read = torch.zeros(max(wr, 256), dtype=torch.uint8, device=device)
+        # argument objects reused by every call
+        L = B.lib()
+        self._f_select, self._f_readout = L.rs3_select_queries, L.rs3_readout
+        self._f_commit, self._f_readout_commit = L.rs3_commit, L.rs3_readout_commit
+        self._grid_ref = ctypes.byref(self.grid)
+        self._params_ref = ctypes.byref(self.params)
+        self._harr_src = None
+        self._k = (ctypes.c_int32 * self.n_groups)()
+        self._k_addr = ctypes.addressof(self._k)
+        self._ws_sel = (self.ws_sel.data_ptr(), self.ws_sel.numel())
+        self._ws_read = (self.ws_read.data_ptr(), self.ws_read.numel())
+        self._p_sel_idx, self._p_sel_count = self.sel_idx.data_ptr(), self.sel_count.data_ptr()
+        self._p_kept = self.kept_count.data_ptr()
+        self._sel_stride = 0 if union_objects else self.mn
+        self._y_stride = self.mn * C if n_obj > 1 else 0
+        self._dev_index = torch.device(device).index or 0
+        raw = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+        self._raw_stream = (lambda: raw(self._dev_index)) if raw is not None else \
+            (lambda: torch.cuda.current_stream().cuda_stream)
+
+    def _handles(self):
+        """Device address of the bank handle array, rebuilt when the bank
+        list has changed (a bank replaced by a restored one, say)."""
+        if self.banks != self._harr_src:
+            self._harr_keep = (B.c_vp * len(self.banks))(*[b.h for b in self.banks])
+            self._harr = ctypes.cast(self._harr_keep, B.c_vp).value
+            self._harr_src = list(self.banks)
+        return self._harr
+
+    def _stream(self, stream):
+        return self._raw_stream() if stream is None else stream
+
+    @staticmethod
+    def _check(status, what):
+        if status != B.RS3_OK:
+            raise B.Rs3Error(status, what)
 
     # -- calls ---------------------------------------------------------------
     def select(self, masks, X, k: Sequence[int], seed_box: bool = False, prior_out=None, stream=None):
+        if len(k) != self.n_groups:
+            raise ValueError("select: %d keep budgets for %d groups" % (len(k), self.n_groups))
         self.params.seed_box = 1 if seed_box else 0
-        B.select_queries(self.grid, self.n_obj, masks, self.track, X, self.x_stride, self.C, self.dt, k,
-                         self.params, self.ws_sel, self.sel_idx, self.sel_count, prior_out, stream)
+        kk = self._k
+        for i, v in enumerate(k):
+            kk[i] = v
+        self._check(self._f_select(self._grid_ref, self.n_obj, masks.data_ptr(), self.track.h, X.data_ptr(),
+                                   self.x_stride, self.C, self.dt, self._k_addr, self._params_ref, self._ws_sel[0],
+                                   self._ws_sel[1], self._p_sel_idx, self._p_sel_count,
+                                   None if prior_out is None else prior_out.data_ptr(), self._stream(stream)),
+                    "rs3_select_queries")
 
     def readout(self, X, Y, max_sel: Optional[int] = None, y_fp32: int = 0, stream=None):
         ms = self.max_sel if max_sel is None else max_sel
-        sel_stride = 0 if self.union_objects else self.mn
-        y_stride = self.mn * self.C if self.n_obj > 1 else 0
-        B.readout(self.layer, self.grid, self.n_obj, X, self.x_stride, self.banks, self.sel_idx, self.sel_count,
-                  sel_stride, ms, self.n_splits, Y, y_stride, y_fp32, self.ws_read, stream)
+        self._check(self._f_readout(self.layer.h, self._grid_ref, self.n_obj, X.data_ptr(), self.x_stride,
+                                    self._handles(), self._p_sel_idx, self._p_sel_count, self._sel_stride, ms,
+                                    self.n_splits, Y.data_ptr(), self._y_stride, y_fp32, self._ws_read[0],
+                                    self._ws_read[1], self._stream(stream)), "rs3_readout")
 
     def readout_commit(self, X, Y, Kmem, Vmem, masks, t: int, pin: bool, max_sel: Optional[int] = None,
                        y_fp32: int = 0, fall_min: int = 0, fall_max: Optional[int] = None, stream=None):
         """readout(X, Y) then commit(Kmem, Vmem, masks, t, pin) in one call."""
         ms = self.max_sel if max_sel is None else max_sel
-        sel_stride = 0 if self.union_objects else self.mn
-        y_stride = self.mn * self.C if self.n_obj > 1 else 0
         fmax = self.mn if fall_max is None else fall_max
-        B.readout_commit(self.layer, self.grid, self.n_obj, X, self.x_stride, self.banks, self.sel_idx,
-                         self.sel_count, sel_stride, ms, self.n_splits, Y, y_stride, y_fp32, self.ws_read, Kmem,
-                         Vmem, self.mn * self.d_kv, masks, t, int(pin), fall_min, fmax, self.kept_count, stream)
+        self._check(self._f_readout_commit(
+            self.layer.h, self._grid_ref, self.n_obj, X.data_ptr(), self.x_stride, self._handles(), self._p_sel_idx,
+            self._p_sel_count, self._sel_stride, ms, self.n_splits, Y.data_ptr(), self._y_stride, y_fp32,
+            self._ws_read[0], self._ws_read[1], Kmem.data_ptr(), Vmem.data_ptr(), self.mn * self.d_kv,
+            masks.data_ptr(), t, int(pin), fall_min, fmax, self._p_kept, self._stream(stream)),
+            "rs3_readout_commit")
 
     def commit(self, Kmem, Vmem, masks, t: int, pin: bool, fall_min: int = 0, fall_max: Optional[int] = None,
                stream=None):
         fmax = self.mn if fall_max is None else fall_max
-        B.commit(self.banks, self.grid, Kmem, Vmem, self.mn * self.d_kv, masks, t, int(pin), fall_min, fmax,
-                 self.kept_count, stream)
+        self._check(self._f_commit(self._handles(), self.n_obj, self._grid_ref, Kmem.data_ptr(), Vmem.data_ptr(),
+                                   self.mn * self.d_kv, masks.data_ptr(), t, int(pin), fall_min, fmax, self._p_kept,
+                                   self._stream(stream)), "rs3_commit")

@@ -2,7 +2,9 @@
 same seeded inputs (test infrastructure)."""
 from __future__ import annotations
 
+import json
 import math
+import os
 from typing import List
 
 import numpy as np
@@ -11,6 +13,33 @@ import oracle
 from workloads import Config, storage_to_f64
 
 TOL = {"bf16": 2e-2, "f32": 1e-4}
+
+# Largest error seen by each parity check, next to its tolerance: written as
+# JSON at the end of the session when RS3_MARGINS_OUT names a file.
+MARGINS: List[dict] = []
+
+
+def record_margin(case: str, n_rows: int, err: float, tol: float):
+    test = os.environ.get("PYTEST_CURRENT_TEST", "").split(" ")[0]
+    MARGINS.append(dict(test=test, case=case, rows=int(n_rows), max_abs_err=float(err), tol=float(tol),
+                        margin=float(tol - err)))
+
+
+def write_margins():
+    path = os.environ.get("RS3_MARGINS_OUT")
+    if not path or not MARGINS:
+        return
+    worst = {}
+    for r in MARGINS:
+        w = worst.get(r["test"])
+        if w is None or r["max_abs_err"] / r["tol"] > w["max_abs_err"] / w["tol"]:
+            worst[r["test"]] = dict(r, checks=0, rows_total=0)
+    for r in MARGINS:
+        worst[r["test"]]["checks"] += 1
+        worst[r["test"]]["rows_total"] += r["rows"]
+    os.makedirs(os.path.dirname(os.path.abspath(path)), exist_ok=True)
+    with open(path, "w") as fh:
+        json.dump({"per_test_worst": sorted(worst.values(), key=lambda r: r["test"]), "all": MARGINS}, fh, indent=1)
 
 
 def grid_masks(cfg: Config, masks_px: np.ndarray) -> np.ndarray:
@@ -53,6 +82,38 @@ class OraclePipeline:
         Y = oracle.readout(X, rows, Kf, Vf, self.W["Wq"], self.W["Wk"], self.W["Wv"], self.W["Wo"], cfg.H,
                            rope=self.rope, kpos=pos)
         return Y[np.asarray(rows, dtype=np.int64)]
+
+    def projected_bank(self, o):
+        """(K^, V^, key cells) of object o's resident keys in key order, the
+        keys turned by their cells when there is a table; cached until the
+        bank changes."""
+        cfg = self.cfg
+        bank = self.banks[o]
+        sig = (len(bank.frames), tuple(tuple(f) for f in bank.frame_table().tolist()), bank.err)
+        cache = getattr(self, "_proj", {})
+        if cache.get(o, (None,))[0] != sig:
+            K, V, pos = bank.key_rows()
+            Kh, Vh = oracle.project_bank(storage_to_f64(K, cfg.dtype), storage_to_f64(V, cfg.dtype),
+                                         self.W["Wk"], self.W["Wv"])
+            Kh = oracle.rotate_keys(Kh, self.rope, pos, cfg.H)
+            cache[o] = (sig, Kh, Vh)
+            self._proj = cache
+        return cache[o][1], cache[o][2]
+
+    def readout_dense_blocked(self, X_store, o, rows, block=256):
+        """Oracle y for cells `rows` of object o by the whole-matrix
+        evaluation, in row blocks against one projection of the bank."""
+        cfg = self.cfg
+        xi = 0 if X_store.shape[0] == 1 else o
+        rows = np.asarray(rows, dtype=np.int64)
+        X = storage_to_f64(X_store[xi], cfg.dtype)
+        Kh, Vh = self.projected_bank(o)
+        out = np.empty((len(rows), cfg.C))
+        for b0 in range(0, len(rows), block):
+            r = rows[b0:b0 + block]
+            out[b0:b0 + block] = oracle.readout_dense_projected(X[r], Kh, Vh, self.W["Wq"], self.W["Wo"], cfg.H,
+                                                                rope=self.rope, qpos=r)
+        return out
 
     def readout_dense_rows(self, X_store, o, rows):
         cfg = self.cfg

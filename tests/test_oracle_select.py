@@ -95,3 +95,61 @@ def test_topk_special_cases():
     # a hand example: energies 5,9,9,1 on cells 0..3, k = 2 -> cells 1 and 2
     assert oracle.topk_keep(np.ones(4, bool), np.array([5.0, 9, 9, 1]), 2).tolist() == [1, 2]
     assert oracle.topk_keep(np.ones(4, bool), np.array([9.0, 5, 9, 9]), 2).tolist() == [0, 2]
+
+
+def _brute_prior(mask_px, s, m, n, r):
+    """Chebyshev dilation by r of the down-sampled mask, one cell at a time."""
+    cells = [(y, x) for y in range(m) for x in range(n) if mask_px[y * s, x * s]]
+    P = np.zeros(m * n, dtype=bool)
+    for y in range(m):
+        for x in range(n):
+            P[y * n + x] = any(max(abs(y - yy), abs(x - xx)) <= r for yy, xx in cells)
+    return P
+
+
+@pytest.mark.parametrize("shared_x", [True, False])
+def test_per_object_groups(shared_x):
+    """union_objects = False: group o is object o alone, ranked on its own
+    token grid (shared or per object) with its own budget k[o].  Each group
+    must equal a one-object call on that object, and a brute-force prior,
+    integer energy and full sort; the tracker states must match too."""
+    rng = np.random.default_rng(11)
+    m, n, s, C, n_obj, r_s, c = 12, 10, 2, 6, 3, 2, 3
+    n_x = 1 if shared_x else n_obj
+    # integer-valued tokens: the energies are exact integers, and each
+    # object's grid differs, so ranking on another object's grid shows
+    X = rng.integers(-9, 10, size=(n_x, m * n, C)).astype(np.float64)
+    k = [5, 17, 60]
+    tracks = [oracle.Track() for _ in range(n_obj)]
+    single = [oracle.Track() for _ in range(n_obj)]
+    for frame in range(3):
+        masks = (rng.random((n_obj, m * s, n * s)) < 0.04).astype(np.uint8)
+        if frame == 2:
+            masks[1] = 0      # object 1 lost: its cached box with a grown radius
+        sel, pri, tracks = oracle.select_queries(masks, s, m, n, tracks, X, k, r_s, c, False, False)
+        assert pri.shape == (n_obj, m * n)
+        for o in range(n_obj):
+            xo = 0 if shared_x else o
+            so, po, to = oracle.select_queries(masks[o:o + 1], s, m, n, [single[o]], X[xo:xo + 1], [k[o]],
+                                               r_s, c, False, True)
+            single[o] = to[0]
+            assert np.array_equal(sel[o], so[0])
+            assert np.array_equal(pri[o], po[0])
+            assert tracks[o].as_list() == single[o].as_list()
+            # brute force: prior, exact integer energies, full sort
+            if masks[o].any():
+                bp = _brute_prior(masks[o], s, m, n, r_s)
+            else:
+                y0, x0, y1, x1 = (v // s for v in tracks[o].box)
+                r = r_s + min(tracks[o].delta, c)
+                bp = np.zeros(m * n, dtype=bool)
+                for y in range(m):
+                    for x in range(n):
+                        bp[y * n + x] = (y0 - r <= y <= y1 + r) and (x0 - r <= x <= x1 + r)
+            assert np.array_equal(pri[o], bp)
+            e = [sum(int(v) * int(v) for v in X[xo, i]) for i in range(m * n)]
+            ranked = sorted(np.flatnonzero(bp).tolist(), key=lambda i: (-e[i], i))
+            assert sel[o].tolist() == sorted(ranked[:k[o]])
+    # the objects' lists differ, so a group ranked on the wrong grid, with the
+    # wrong budget or the wrong prior would have shown above
+    assert len({tuple(v.tolist()) for v in sel}) == n_obj

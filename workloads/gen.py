@@ -33,10 +33,10 @@ def bf16_bits(x: np.ndarray) -> np.ndarray:
 
     Inputs here are finite, so no NaN handling is needed.
     """
-    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    lsb = (u >> 16) & 1
-    u = (u + 0x7FFF + lsb) >> 16
-    return u.astype(np.uint16)
+    # finite values: u + 0x7FFF + lsb stays below 2^32, so uint32 suffices
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    u = u + (np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1)))
+    return (u >> np.uint32(16)).astype(np.uint16)
 
 
 def bits_to_f32(b: np.ndarray) -> np.ndarray:
