@@ -240,6 +240,32 @@ rs3_status rs3_readout(const rs3_layer* L, const rs3_grid* g, int32_t n_obj,
                        int32_t max_sel, int32_t n_splits, void* Y, int64_t y_obj_stride,
                        int32_t y_fp32, void* ws, size_t ws_bytes, void* stream);
 
+/* ---- readout for callers that cannot allocate ------------------------------
+ * For code that may not call hipMalloc or take a workspace (work recorded
+ * under HIP graph capture, fixed serving loops, hosts that forbid device
+ * allocation): rs3_readout with the same arguments and results, minus
+ * ws/ws_bytes.  The split partials and projected queries go to a fixed
+ * device array of RS3_NOALLOC_SCRATCH_BYTES inside the library, one copy per
+ * GPU, held until the process ends; the call allocates nothing.
+ * n_splits = 0 takes the automatic key-split count, reduced until the
+ * partials fit the array (the results then differ from rs3_readout's only in
+ * rounding); a call whose layout does not fit even with one split (or with
+ * the n_splits given) returns RS3_E_INVALID and launches nothing.  The bf16
+ * partials of one call need about
+ *   n_obj*max_sel*Da*2 + S*n_obj*max_sel*(Da*2 + H*8) bytes
+ * for S key splits, Da the attention width (D, or d_kv in the absorbed form)
+ * and H its heads.  E.g. one object on a 64x64 grid with one head of 256 fits
+ * every max_sel up to 4096, with at most 6 key splits projected and 29
+ * absorbed.  fp32 layers use no scratch.
+ * Every call on one GPU shares that GPU's array, and no call clears it
+ * (nothing in it must start at zero): calls that overlap in time on one GPU
+ * (two streams, or two host threads) race and give undefined results. */
+#define RS3_NOALLOC_SCRATCH_BYTES (16u << 20)
+rs3_status rs3_readout_noalloc(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, const void* X,
+                               int64_t x_obj_stride, rs3_bank* const* banks /*[host]*/, const int32_t* sel_idx,
+                               const int32_t* sel_count, int32_t sel_stride, int32_t max_sel, int32_t n_splits,
+                               void* Y, int64_t y_obj_stride, int32_t y_fp32, void* stream);
+
 /* ---- commit (Sec. 3.2, Eq. 8 and the sparse write of Algorithm 1) ----------
  * For each object o: kept = ascending cells set in masks[o] (sampled at
  * stride s); if kept_count < fall_min or > fall_max all m*n cells are kept

@@ -17,6 +17,7 @@ RS3_MAX_OBJ = 64
 RS3_MAX_MN = 32768
 RS3_TRACK_WORDS = 6
 RS3_BANK_HDR_WORDS = 8
+RS3_NOALLOC_SCRATCH_BYTES = 16 << 20
 
 lib_path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librs3.so")
 
@@ -61,6 +62,8 @@ _SIGS = {
     "rs3_readout_workspace_size": (c_i32, [c_vp, c_i32, c_i32, c_i32, ctypes.POINTER(c_sz)]),
     "rs3_readout": (c_i32, [c_vp, ctypes.POINTER(Grid), c_i32, c_vp, c_i64, c_vp, c_vp, c_vp, c_i32, c_i32,
                             c_i32, c_vp, c_i64, c_i32, c_vp, c_sz, c_vp]),
+    "rs3_readout_noalloc": (c_i32, [c_vp, ctypes.POINTER(Grid), c_i32, c_vp, c_i64, c_vp, c_vp, c_vp, c_i32, c_i32,
+                                    c_i32, c_vp, c_i64, c_i32, c_vp]),
     "rs3_readout_commit": (c_i32, [c_vp, ctypes.POINTER(Grid), c_i32, c_vp, c_i64, c_vp, c_vp, c_vp, c_i32, c_i32,
                                    c_i32, c_vp, c_i64, c_i32, c_vp, c_sz, c_vp, c_vp, c_i64, c_vp, c_i32, c_i32,
                                    c_i32, c_i32, c_vp, c_vp]),
@@ -269,6 +272,16 @@ def readout(layer: Layer, grid, n_obj: int, X, x_obj_stride: int, banks: Sequenc
                              ctypes.cast(harr, c_vp), _ptr(sel_idx), _ptr(sel_count), sel_stride, max_sel,
                              n_splits, _ptr(Y), y_obj_stride, y_fp32, _ptr(ws), ws_bytes, _stream(stream)),
            "rs3_readout")
+
+
+def readout_noalloc(layer: Layer, grid, n_obj: int, X, x_obj_stride: int, banks: Sequence[Bank], sel_idx, sel_count,
+                    sel_stride: int, max_sel: int, n_splits: int, Y, y_obj_stride: int, y_fp32: int = 0, stream=None):
+    """rs3_readout without a workspace: the library's fixed per-GPU scratch
+    holds the split partials (nothing is allocated)."""
+    harr = (c_vp * len(banks))(*[b.h for b in banks])
+    _check(lib().rs3_readout_noalloc(layer.h, ctypes.byref(_grid(grid)), n_obj, _ptr(X), x_obj_stride,
+                                     ctypes.cast(harr, c_vp), _ptr(sel_idx), _ptr(sel_count), sel_stride, max_sel,
+                                     n_splits, _ptr(Y), y_obj_stride, y_fp32, _stream(stream)), "rs3_readout_noalloc")
 
 
 def commit(banks: Sequence[Bank], grid, Kmem, Vmem, kv_obj_stride: int, masks, t: int, pin: int,

@@ -875,6 +875,57 @@ rs3_status rs3_readout(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, con
   return map_err(rs3_launch_readout(a, L->dev.dtype, (hipStream_t)stream));
 }
 
+// ---- readout without a caller workspace ----------------------------------------
+// The split partials and projected queries of rs3_readout_noalloc live in a
+// fixed device array, one copy per GPU, held until the process ends.  Host
+// code never passes the array's name to a kernel (in host code it stands for
+// a host-side shadow): the device address comes from hipGetSymbolAddress,
+// taken once per device with that device current, and is kept per device.
+static __device__ __align__(256) uint8_t scratch[RS3_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int SCRATCH_MAX_DEVICES = 64;
+std::mutex scratch_mu;
+void* scratch_ptr[SCRATCH_MAX_DEVICES];
+
+// The current device's copy of `scratch` (null when the device cannot be
+// queried or the symbol has no address).
+void* scratch_for_current_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= SCRATCH_MAX_DEVICES) return nullptr;
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (!scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+    scratch_ptr[dev] = ptr;
+  }
+  return scratch_ptr[dev];
+}
+
+}  // namespace
+
+rs3_status rs3_readout_noalloc(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, const void* X,
+                               int64_t x_obj_stride, rs3_bank* const* banks, const int32_t* sel_idx,
+                               const int32_t* sel_count, int32_t sel_stride, int32_t max_sel, int32_t n_splits,
+                               void* Y, int64_t y_obj_stride, int32_t y_fp32, void* stream) {
+  if (!L) return RS3_E_INVALID;
+  void* ws = nullptr;
+  size_t ws_bytes = 0;
+  if (L->dev.dtype == RS3_BF16) {
+    ws = scratch_for_current_device();
+    if (!ws) return RS3_E_DEVICE;
+    ws_bytes = RS3_NOALLOC_SCRATCH_BYTES;
+  }
+  Rs3ReadoutArgs a;
+  rs3_status st = readout_args(L, g, n_obj, X, x_obj_stride, banks, sel_idx, sel_count, sel_stride, max_sel, n_splits,
+                               Y, y_obj_stride, y_fp32, ws, ws_bytes, a, true);
+  if (st != RS3_OK) return st;
+  st = ensure_setup();
+  if (st != RS3_OK) return st;
+  return map_err(rs3_launch_readout(a, L->dev.dtype, (hipStream_t)stream));
+}
+
 // ---- write keep-set ----------------------------------------------------------
 rs3_status rs3_write_keepset(const rs3_grid* g, int32_t n_obj, const uint8_t* seed_masks, int32_t D_w,
                              int32_t fall_min, int32_t fall_max, int32_t n_copies, uint8_t* keep, int32_t* counts,
