@@ -734,7 +734,14 @@ rs3_status rs3_attend(const void* Qh, const void* Kh, const void* Vh, int32_t n_
   a.max_sel = n_q;
   a.S = L.S;
   a.n_qt = (n_q + 127) / 128;
-  e = rs3_launch_attn(a, st, false);
+  Rs3AttnBanks ab;
+  memset(&ab, 0, sizeof(ab));
+  ab.hdr[0] = p.hdr;
+  ab.tiles[0] = p.tiles;
+  ab.kh[0] = p.Khat;
+  ab.vh[0] = p.Vhat;
+  ab.ntcap[0] = L.ntile;
+  e = rs3_launch_attn(a, ab, st, false);
   if (e != hipSuccess) return map_err(e);
   const int SA = L.ntile > 0 ? active_splits(L.ntile, L.S) : 0;
   return map_err(rs3_launch_attend_merge(a, SA, O, st));
@@ -789,7 +796,7 @@ static rs3_status readout_args(const rs3_layer* L, const rs3_grid* g, int32_t n_
                                int64_t x_obj_stride, rs3_bank* const* banks, const int32_t* sel_idx,
                                const int32_t* sel_count, int32_t sel_stride, int32_t max_sel, int32_t n_splits,
                                void* Y, int64_t y_obj_stride, int32_t y_fp32, void* ws, size_t ws_bytes,
-                               Rs3ReadoutArgs& a, bool fit_splits = false) {
+                               Rs3ReadoutArgs& a, Rs3AttnBanks& ab, bool fit_splits = false) {
   if (!L || !grid_ok(g) || !X || !banks || !sel_idx || !sel_count || !Y) return RS3_E_INVALID;
   if (n_obj <= 0 || n_obj > RS3_MAX_OBJ) return RS3_E_INVALID;
   const LayerDev& ld = L->dev;
@@ -834,6 +841,15 @@ static rs3_status readout_args(const rs3_layer* L, const rs3_grid* g, int32_t n_
   if (ld.dtype == RS3_BF16 && (!ws || ws_bytes < q + o_b + ml)) return RS3_E_INVALID;
   memset(&a, 0, sizeof(a));
   for (int o = 0; o < n_obj; ++o) a.banks[o] = banks[o]->d_desc;
+  memset(&ab, 0, sizeof(ab));
+  for (int o = 0; o < n_obj; ++o) {
+    const BankDev& h = banks[o]->host;
+    ab.hdr[o] = h.hdr;
+    ab.tiles[o] = h.tiles;
+    ab.kh[o] = h.Khat;
+    ab.vh[o] = h.Vhat;
+    ab.ntcap[o] = h.n_tiles_cap;
+  }
   a.X = X;
   a.x_stride = x_obj_stride;
   a.Y = Y;
@@ -867,12 +883,13 @@ rs3_status rs3_readout(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, con
                        int32_t max_sel, int32_t n_splits, void* Y, int64_t y_obj_stride, int32_t y_fp32, void* ws,
                        size_t ws_bytes, void* stream) {
   Rs3ReadoutArgs a;
+  Rs3AttnBanks ab;
   rs3_status st = readout_args(L, g, n_obj, X, x_obj_stride, banks, sel_idx, sel_count, sel_stride, max_sel, n_splits,
-                               Y, y_obj_stride, y_fp32, ws, ws_bytes, a);
+                               Y, y_obj_stride, y_fp32, ws, ws_bytes, a, ab);
   if (st != RS3_OK) return st;
   st = ensure_setup();
   if (st != RS3_OK) return st;
-  return map_err(rs3_launch_readout(a, L->dev.dtype, (hipStream_t)stream));
+  return map_err(rs3_launch_readout(a, ab, L->dev.dtype, (hipStream_t)stream));
 }
 
 // ---- readout without a caller workspace ----------------------------------------
@@ -918,12 +935,13 @@ rs3_status rs3_readout_noalloc(const rs3_layer* L, const rs3_grid* g, int32_t n_
     ws_bytes = RS3_NOALLOC_SCRATCH_BYTES;
   }
   Rs3ReadoutArgs a;
+  Rs3AttnBanks ab;
   rs3_status st = readout_args(L, g, n_obj, X, x_obj_stride, banks, sel_idx, sel_count, sel_stride, max_sel, n_splits,
-                               Y, y_obj_stride, y_fp32, ws, ws_bytes, a, true);
+                               Y, y_obj_stride, y_fp32, ws, ws_bytes, a, ab, true);
   if (st != RS3_OK) return st;
   st = ensure_setup();
   if (st != RS3_OK) return st;
-  return map_err(rs3_launch_readout(a, L->dev.dtype, (hipStream_t)stream));
+  return map_err(rs3_launch_readout(a, ab, L->dev.dtype, (hipStream_t)stream));
 }
 
 // ---- write keep-set ----------------------------------------------------------
@@ -1038,9 +1056,10 @@ rs3_status rs3_readout_commit(const rs3_layer* L, const rs3_grid* g, int32_t n_o
                               int32_t t, int32_t pin, int32_t fall_min, int32_t fall_max, int32_t* kept_count,
                               void* stream) {
   Rs3ReadoutArgs ra;
+  Rs3AttnBanks ab;
   Rs3CommitArgs ca;
   rs3_status st = readout_args(L, g, n_obj, X, x_obj_stride, banks, sel_idx, sel_count, sel_stride, max_sel,
-                               n_splits, Y, y_obj_stride, y_fp32, ws, ws_bytes, ra);
+                               n_splits, Y, y_obj_stride, y_fp32, ws, ws_bytes, ra, ab);
   if (st != RS3_OK) return st;
   st = commit_args(banks, n_obj, g, Kmem, Vmem, kv_obj_stride, masks, t, pin, fall_min, fall_max, kept_count, ca);
   if (st != RS3_OK) return st;
@@ -1049,7 +1068,7 @@ rs3_status rs3_readout_commit(const rs3_layer* L, const rs3_grid* g, int32_t n_o
   const LayerDev& ld = L->dev;
   const hipStream_t s = (hipStream_t)stream;
   bool pending = false;
-  hipError_t e = rs3_launch_readout(ra, ld.dtype, s, false, &pending);
+  hipError_t e = rs3_launch_readout(ra, ab, ld.dtype, s, false, &pending);
   if (e == hipSuccess)
     e = pending ? rs3_launch_merge_commit(ra, ca, ld.d_kv, s)
                 : rs3_launch_commit(ca, ld.dtype, ld.d_kv, ld.Da, ld.Ha, ld.dah, s);

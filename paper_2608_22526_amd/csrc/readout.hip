@@ -866,6 +866,397 @@ __global__ __launch_bounds__(256 * NG) void k_attn(Rs3ReadoutArgs a, int G) {
 }
 
 // ---------------------------------------------------------------------------
+// The attention of launches whose heads are 64 wide at d_model 256, that
+// project their queries inside (no rotary table) and that fit the chip once
+// (at most one work-group per CU): 512 threads, two groups of four waves on
+// the same 128 queries, group g taking the pairs of half tiles g, g+2, ... of
+// the split.  Split s holds the resident tiles s, s+S, s+2S, ... of the bank
+// (interleaved rather than a contiguous range), so its tile entries can be
+// loaded before the resident tile count is known.  The bank pointers come in
+// the arguments.  The prologue issues every load as soon as its inputs exist:
+//   1. from the arguments alone: the 128 row indices, the head's 64 rows of
+//      W_q^T (coalesced), the split's tile entries (one per lane), the
+//      resident tile count, the selected count;
+//   2. the gathered X rows once the indices land, and each group's first pair
+//      of half tiles (DMA into stages 0-3) once the entries and the count land;
+//   3. the query projection in two passes over the channel halves (the X and
+//      W_q halves are staged in LDS above stages 0-3, each thread writing its
+//      chunks in one of the passes): group g computes d = 32g .. 32g+31 of
+//      its wave's 32 queries (8 MFMAs per pass), and the partner waves of the
+//      two groups swap their halves through LDS.
+// The key loop and the merge of the two groups' partials follow the
+// two-group form of k_attn.
+constexpr int G2_DH = 64;
+constexpr int G2_HC = PJ_PC / 2;                 // 16-byte chunks per row half
+
+// A 16-byte LDS store the compiler does not see as one: after direct-to-LDS
+// loads it orders every LDS store behind all of them (a full wait for the
+// vector memory counter), while these stores touch none of their stages and
+// need only their own data, which the register operand makes it wait for.
+__device__ __forceinline__ void ds_store16(const uint8_t* p, const u32x4& v) {
+  const uint32_t off = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)p;
+  asm volatile("ds_write_b128 %0, %1" ::"v"(off), "v"(v) : "memory");
+}
+constexpr int G2_PITCH = (G2_HC + 1) * 16;       // odd chunk count: conflict-free operand reads
+struct G2Lds {
+  static constexpr int STAGE = AttnLds<G2_DH>::STAGE;
+  static constexpr int XOFF = 4 * STAGE;               // X row halves [128][G2_PITCH] during the projection
+  static constexpr int WOFF = XOFF + 128 * G2_PITCH;   // W_q^T row halves [64][G2_PITCH]
+  static constexpr int XCH = WOFF + G2_DH * G2_PITCH;  // halves of Q~: [8 waves][64 lanes][2] u32x4
+  static constexpr int BYTES = XCH + 8 * 64 * 32;
+};
+static_assert(G2Lds::BYTES >= 8 * G2Lds::STAGE, "the eight stages fit");
+static_assert(G2Lds::BYTES <= 160 * 1024, "one CU's LDS");
+
+__global__ __launch_bounds__(512) void k_attn_g2(Rs3ReadoutArgs a, int G, Rs3AttnBanks ab) {
+  constexpr int DH = G2_DH, NT = 512;
+  using L = AttnLds<DH>;
+  extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];   // G2Lds::BYTES
+  const int bid = blockIdx.x;
+  const int rest = bid >> 3;
+  const int qt = rest % a.n_qt;
+  const int kvg = (rest / a.n_qt) * 8 + (bid & 7);
+  if (kvg >= G) return;
+  const int S = a.S;
+  const int s = kvg % S, oh = kvg / S, h = oh % a.H, o = oh / a.H;
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5;
+  const int wave_all = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wave = wave_all & 3;    // the wave's 32 queries: rows 32*wave of the tile
+  const int grp = wave_all >> 2;    // its group: pairs grp, grp+2, ...; d-block grp of the projection
+  const int row0 = qt * 128;
+  const int qrow = row0 + 32 * wave + (lane & 31);
+
+  // 1. loads that need only the arguments (the row indices first: the X loads
+  //    wait for them alone).  Group g holds channel half g of the operands:
+  //    thread lt = tid % 256 of the group holds chunk 16g + lt%16 of X rows
+  //    lt/16 + 16 i and of W_q^T rows h*64 + lt/16 + 16 j.
+  constexpr int NX = 8, NW = 4;
+  const int lt = tid & 255, hchunk = G2_HC * grp + (lt & 15);
+  int src[NX];
+  {
+    const int32_t* sel = a.sel_idx + (int64_t)o * a.sel_stride;
+#pragma unroll
+    for (int i = 0; i < NX; ++i) src[i] = gload(sel + min(row0 + (lt >> 4) + 16 * i, a.max_sel - 1));
+  }
+  u32x4 wreg[NW];
+  {
+    const u32x4* wb = (const u32x4*)((const bf16_t*)a.WqT + (int64_t)h * DH * PJ_PC * 8) + hchunk;
+#pragma unroll
+    for (int j = 0; j < NW; ++j) wreg[j] = gload(wb + ((lt >> 4) + 16 * j) * PJ_PC);
+  }
+  const TileEnt* tiles = ab.tiles[o];
+  const int ntcap = ab.ntcap[o];
+  int c_tile;
+  uint32_t c_mlo, c_mhi;
+  {
+    const int e = s + S * lane;   // entries past the list are read clamped and discarded
+    const int ec = max(min(e, ntcap - 1), 0);
+    c_tile = gload(&tiles[ec].tile);
+    const uint64_t m = gload(&tiles[ec].mask);
+    c_mlo = (uint32_t)m;
+    c_mhi = (uint32_t)(m >> 32);
+  }
+  const int ntiles = sload(ab.hdr[o] + HDR_NTILES);
+  int cnt = sload(a.sel_count + (a.sel_stride ? o : 0));   // out of range: reported by the merge
+  cnt = cnt < 0 ? 0 : min(cnt, a.max_sel);
+  auto keep_loads = [&]() {
+#pragma unroll
+    for (int i = 0; i < NX; ++i) keep(src[i]);
+#pragma unroll
+    for (int j = 0; j < NW; ++j) keep(wreg[j]);
+    keep(c_tile);
+    keep(c_mlo);
+    keep(c_mhi);
+  };
+  if (row0 >= cnt) {
+    keep_loads();
+    return;
+  }
+  // 2. the gathered X rows (invalid list entries read row 0; the merge skips
+  //    their rows)
+  u32x4 xv[NX];
+  {
+    const bf16_t* X = (const bf16_t*)a.X + (int64_t)o * a.x_stride;
+#pragma unroll
+    for (int i = 0; i < NX; ++i) {
+      const int r = (src[i] < 0 || src[i] >= a.mn) ? 0 : src[i];
+      xv[i] = gload((const u32x4*)(X + (int64_t)r * PJ_PC * 8) + hchunk);
+    }
+  }
+  const int nts = ntiles > s ? (ntiles - s + S - 1) / S : 0;   // tiles of this split
+  if (nts == 0) {
+    keep_loads();
+#pragma unroll
+    for (int i = 0; i < NX; ++i) keep(xv[i]);
+    // the empty partial (m = -inf, l = 0), so that the merge reads every split
+    if (g == 0 && grp == 0 && qrow < cnt) {
+      float* ml = a.ML + ((((int64_t)o * S + s) * a.max_sel + qrow) * a.H + h) * 2;
+      ml[0] = -INFINITY;
+      ml[1] = 0.f;
+    }
+    return;
+  }
+  if (c_tile < 0) c_tile = 0;   // (entries are tile indices; keeps the DMA in the ring)
+  const int nh = 2 * nts;   // half tiles, visited from an offset that depends on the query tile
+  const int rot = nts <= 64 ? ((qt & 7) * nh) >> 3 : 0;
+  auto half_at = [&](int i) { int v = i + rot; return v >= nh ? v - nh : v; };
+  const bf16_t* Kh = (const bf16_t*)ab.kh[o];
+  const bf16_t* Vh = (const bf16_t*)ab.vh[o];
+  const int H = a.H;
+  const AttnDmaOffsets<DH> doff = attn_dma_offsets<DH>(wave, lane);
+  int cbase = 0;   // local tile of lane 0's cached entry
+  const int npair = nts;   // pairs of half tiles (nh is even)
+  // DMA of pair p into stage slot `slot` (stages 2*slot, 2*slot+1)
+  auto issue_pair = [&](int p, int slot) {
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int v = half_at(2 * p + k);
+      if ((v >> 1) - cbase >= 64) {
+        // (splits of more than 64 tiles, which are not rotated) slide the
+        // window of cached entries to this tile; the masks of the pair being
+        // computed were read before
+        wait_vmcnt<0>();
+        cbase = v >> 1;
+        const int j = min(cbase + lane, nts - 1);
+        c_tile = gload(&tiles[s + S * j].tile);
+        const uint64_t mm = gload(&tiles[s + S * j].mask);
+        c_mlo = (uint32_t)mm;
+        c_mhi = (uint32_t)(mm >> 32);
+        settle(c_tile, c_mlo, c_mhi);
+      }
+      const int tl = __builtin_amdgcn_readlane(c_tile, (v >> 1) - cbase);
+      attn_issue<DH>(Kh, Vh, tl, v & 1, h, H, lds + (2 * slot + k) * L::STAGE, wave, doff);
+    }
+  };
+  // 3. query projection, d-block grp of the wave's 32 queries, in two passes
+  //    over the channel halves: group p writes half p of the operands in pass
+  //    p.  Pass 0's operands are stored before the first key/value DMA is
+  //    issued: with ordinary loads and direct-to-LDS loads in flight together
+  //    the compiler waits for all of them, so the X rows (which land last of
+  //    the ordinary loads) are waited for first.
+  f32x16 qa = f32x16{};
+  const int cpos = (lt & 15) * 16;   // the thread's chunk within the row half
+  // every wave's operands have landed before any DMA goes out (the empty
+  // asm hands them on as settled values)
+#pragma unroll
+  for (int i = 0; i < NX; ++i) asm volatile("" : "+v"(xv[i]));
+#pragma unroll
+  for (int j = 0; j < NW; ++j) asm volatile("" : "+v"(wreg[j]));
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    if (pass == 1) lds_barrier();   // every wave is done with pass 0's operands
+    if (grp == pass) {
+#pragma unroll
+      for (int i = 0; i < NX; ++i) ds_store16(lds + G2Lds::XOFF + ((lt >> 4) + 16 * i) * G2_PITCH + cpos, xv[i]);
+#pragma unroll
+      for (int j = 0; j < NW; ++j) ds_store16(lds + G2Lds::WOFF + ((lt >> 4) + 16 * j) * G2_PITCH + cpos, wreg[j]);
+    }
+    if (pass == 0) {
+      // each group's first pair (a group without one loads the last pair into
+      // its own slot, never computed); it lies in the window of cached entries
+      // (a split of more than 64 tiles is not rotated)
+      const int p0 = min(grp, npair - 1);
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const int v = half_at(2 * p0 + k);
+        const int tl = __builtin_amdgcn_readlane(c_tile, v >> 1);
+        attn_issue<DH>(Kh, Vh, tl, v & 1, h, H, lds + (2 * grp + k) * L::STAGE, wave, doff);
+      }
+    }
+    lds_barrier();
+    const uint8_t* xb = lds + G2Lds::XOFF + (32 * wave + (lane & 31)) * G2_PITCH + 16 * g;
+    const uint8_t* wb = lds + G2Lds::WOFF + (32 * grp + (lane & 31)) * G2_PITCH + 16 * g;
+    u32x4 bx[G2_HC / 2], aw[G2_HC / 2];
+#pragma unroll
+    for (int ks = 0; ks < G2_HC / 2; ++ks) {
+      bx[ks] = *(const u32x4*)(xb + ks * 32);
+      aw[ks] = *(const u32x4*)(wb + ks * 32);
+    }
+#pragma unroll
+    for (int ks = 0; ks < G2_HC / 2; ++ks) qa = mfma32(aw[ks], bx[ks], qa);
+  }
+  // Lane l holds query l%32 at d = 32*grp + 8*(r/4) + 4*(l/32) + r%4; the B
+  // operand of the logits needs d = 16*ks + 8*(l/32) + 0..7: one
+  // v_permlane32_swap per register pair (as in attn_project).
+  u32x4 mine[2];
+  const float qs = a.qscale;
+#pragma unroll
+  for (int hf = 0; hf < 2; ++hf) {
+    const int r = 8 * hf;
+    const uint32_t p0 = pack_bf16x2(qa[r] * qs, qa[r + 1] * qs), p1 = pack_bf16x2(qa[r + 2] * qs, qa[r + 3] * qs);
+    const uint32_t q0 = pack_bf16x2(qa[r + 4] * qs, qa[r + 5] * qs), q1 = pack_bf16x2(qa[r + 6] * qs, qa[r + 7] * qs);
+    const auto s0 = __builtin_amdgcn_permlane32_swap(p0, q0, false, false);
+    const auto s1 = __builtin_amdgcn_permlane32_swap(p1, q1, false, false);
+    mine[hf] = u32x4{s0[0], s1[0], s0[1], s1[1]};
+  }
+  const uint8_t* xw = lds + G2Lds::XCH + (wave_all * 64 + lane) * 32;
+  ds_store16(xw, mine[0]);
+  ds_store16(xw + 16, mine[1]);
+  lds_barrier();
+  const u32x4* xr = (const u32x4*)(lds + G2Lds::XCH) + ((wave_all ^ 4) * 64 + lane) * 2;
+  u32x4 qreg[DH / 16];
+  if (grp == 0) {
+    qreg[0] = mine[0];
+    qreg[1] = mine[1];
+    qreg[2] = xr[0];
+    qreg[3] = xr[1];
+  } else {
+    qreg[0] = xr[0];
+    qreg[1] = xr[1];
+    qreg[2] = mine[0];
+    qreg[3] = mine[1];
+  }
+  const bool qv = qrow < cnt;
+#pragma unroll
+  for (int ks = 0; ks < DH / 16; ++ks)
+    if (!qv) qreg[ks] = u32x4{0, 0, 0, 0};
+
+  // key loop: iteration j waits for this wave's DMA of its pair p = 2j+grp
+  // (issued one iteration earlier, or in the prologue), passes one barrier
+  // (the group's previous pair is done and its stages free; in the first
+  // iteration: every wave is done with the projection's LDS), issues pair
+  // p+2 and computes pair p.
+  f32x16 acc[DH / 32];
+#pragma unroll
+  for (int dt = 0; dt < DH / 32; ++dt) acc[dt] = f32x16{};
+  float m_run = -INFINITY, l_run = 0.f;
+  const int kbase = (lane & 31) * L::KP + 16 * g;
+  const int vbase = L::KREG + (lane & 31) * L::VP + 16 * g;
+  const int nit = (npair + 1) >> 1;
+  for (int j = 0; j < nit; ++j) {
+    const int p = 2 * j + grp;
+    wait_vmcnt<0>();
+    stage_barrier();
+    uint32_t mA = 0, mB = 0;
+    if (p < npair) {
+      const int u0 = half_at(2 * p), u1 = half_at(2 * p + 1);
+      const int t0 = (u0 >> 1) - cbase, t1 = (u1 >> 1) - cbase;
+      mA = (u0 & 1) ? __builtin_amdgcn_readlane(c_mhi, t0) : __builtin_amdgcn_readlane(c_mlo, t0);
+      mB = (u1 & 1) ? __builtin_amdgcn_readlane(c_mhi, t1) : __builtin_amdgcn_readlane(c_mlo, t1);
+    }
+    if (p + 2 < npair) issue_pair(p + 2, (p + 2) & 3);
+    if ((mA | mB) == 0u) continue;
+    const uint8_t* SA = lds + (2 * (p & 3)) * L::STAGE;
+    const uint8_t* SB = SA + L::STAGE;
+    f32x16 sA, sB;
+    attn_scores_pair<DH>(SA + kbase, SB + kbase, qreg, sA, sB);
+    if (mA != 0xffffffffu) {   // partial or empty half tile (frame boundary)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        if (!(mA >> c_row(r, lane) & 1u)) sA[r] = -INFINITY;
+    }
+    if (mB != 0xffffffffu) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        if (!(mB >> c_row(r, lane) & 1u)) sB[r] = -INFINITY;
+    }
+    float mx = __builtin_elementwise_maximum(sA[0], sB[0]);
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mx = max3f(mx, sA[r], sB[r]);
+    mx = max_with_partner(mx);
+    const bool need = mx > m_run + RESCALE_LOG2;   // lazy rescale, as in k_attn
+    if (__any(need)) {
+      const float m_new = need ? mx : m_run;
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < DH / 32; ++dt) acc[dt] *= alpha;
+      m_run = m_new;
+    }
+    float psum = 0.f;
+    u32x4 pkA[2], pkB[2];
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const float a0 = __builtin_amdgcn_exp2f(sA[8 * hf + 2 * jj] - m_run);
+        const float a1 = __builtin_amdgcn_exp2f(sA[8 * hf + 2 * jj + 1] - m_run);
+        const float b0 = __builtin_amdgcn_exp2f(sB[8 * hf + 2 * jj] - m_run);
+        const float b1 = __builtin_amdgcn_exp2f(sB[8 * hf + 2 * jj + 1] - m_run);
+        pkA[hf][jj] = pack_bf16x2(a0, a1);
+        pkB[hf][jj] = pack_bf16x2(b0, b1);
+        psum = add_bf16x2(pkB[hf][jj], add_bf16x2(pkA[hf][jj], psum));
+      }
+    l_run += psum;
+#pragma unroll
+    for (int dt = 0; dt < DH / 32; ++dt) {
+      u32x4 va[4];
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        va[q] = *(const u32x4*)(SA + vbase + dt * 32 * L::VP + q * 32);
+        va[2 + q] = *(const u32x4*)(SB + vbase + dt * 32 * L::VP + q * 32);
+      }
+#pragma unroll
+      for (int q = 0; q < 2; ++q) acc[dt] = mfma32(va[q], pkA[q], acc[dt]);
+#pragma unroll
+      for (int q = 0; q < 2; ++q) acc[dt] = mfma32(va[2 + q], pkB[q], acc[dt]);
+    }
+  }
+  // Group 1 hands its (m, l, O^T) per lane to its partner wave of group 0
+  // through LDS, then ends; group 0 merges the two partials to the larger
+  // reference maximum and stores the split's partial rows.
+  constexpr int SW = 2 + 16 * (DH / 32);   // floats per lane
+  float* xs = (float*)(lds + 4 * 32 * (DH * 2 + 16)) + wave * SW * 64 + lane;
+  wait_vmcnt<0>();   // (a group without its last pair left a DMA in flight)
+  __syncthreads();   // every wave is done with the stages
+  if (grp == 1) {
+    xs[0] = m_run;
+    xs[64] = l_run;
+#pragma unroll
+    for (int dt = 0; dt < DH / 32; ++dt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) xs[(2 + 16 * dt + r) * 64] = acc[dt][r];
+  }
+  __syncthreads();
+  if (grp == 1) return;
+  {
+    const float m1 = xs[0], l1 = xs[64];
+    const float mm = __builtin_elementwise_maximum(m_run, m1);
+    const float s0 = mm == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - mm);
+    const float s1 = mm == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - mm);
+    l_run = l_run * s0 + l1 * s1;
+#pragma unroll
+    for (int dt = 0; dt < DH / 32; ++dt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[dt][r] = acc[dt][r] * s0 + xs[(2 + 16 * dt + r) * 64] * s1;
+    m_run = mm;
+  }
+  const float l_tot = sum_with_partner(l_run);
+  const float inv = l_tot > 0.f ? __builtin_amdgcn_rcpf(l_tot) : 0.f;
+  // stage the wave's 32 normalised rows in LDS as [query][d] bf16 (below the
+  // handed-over partials), then whole rows with 16-byte stores
+  constexpr int OP = DH * 2 + 16;
+  uint8_t* ow = lds + wave * 32 * OP;
+#pragma unroll
+  for (int dt = 0; dt < DH / 32; ++dt)
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4) {
+      const int d = 32 * dt + 8 * q4 + 4 * g;
+      u32x2 w;
+      w[0] = pack_bf16x2(acc[dt][4 * q4] * inv, acc[dt][4 * q4 + 1] * inv);
+      w[1] = pack_bf16x2(acc[dt][4 * q4 + 2] * inv, acc[dt][4 * q4 + 3] * inv);
+      *(u32x2*)(ow + (lane & 31) * OP + d * 2) = w;
+    }
+  if (g == 0 && qv) {
+    float* ml = a.ML + ((((int64_t)o * S + s) * a.max_sel + qrow) * a.H + h) * 2;
+    ml[0] = m_run;
+    ml[1] = l_tot;
+  }
+  // the staged rows of this wave are written by this wave alone: a wave-local
+  // wait for its LDS stores suffices
+  __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+  __builtin_amdgcn_wave_barrier();
+  constexpr int CH = DH / 8;   // 16-byte chunks per row
+  bf16_t* obase = (bf16_t*)a.Opart + (((int64_t)o * S + s) * a.max_sel) * a.D + h * DH;
+#pragma unroll
+  for (int q = lane; q < 32 * CH; q += 64) {
+    const int rr = q / CH, c = q - rr * CH;
+    const int row = row0 + 32 * wave + rr;
+    if (row < cnt) *(u32x4*)(obase + (int64_t)row * a.D + 8 * c) = *(const u32x4*)(ow + rr * OP + 16 * c);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // grid (n_obj, ceil(max_sel/cb_rows_for(D, n_obj, max_sel))), block CB_THREADS: one merge block each.
 template <typename OutT>
 __global__ __launch_bounds__(CB_THREADS) void k_combine(Rs3ReadoutArgs a) {
@@ -1030,7 +1421,7 @@ static bool attn_projects(const Rs3ReadoutArgs& a) {
   return a.d_h <= 64 && a.C == 8 * PJ_PC && nblk <= ATTN_DEEP_MAX_BLOCKS && !a.rope;
 }
 
-hipError_t rs3_launch_attn(const Rs3ReadoutArgs& a, hipStream_t st, bool project) {
+hipError_t rs3_launch_attn(const Rs3ReadoutArgs& a, const Rs3AttnBanks& ab, hipStream_t st, bool project) {
   const int G = a.n_obj * a.H * a.S;
   const int nblk = 8 * a.n_qt * ((G + 7) / 8);
   if (project && !attn_projects(a)) return hipErrorInvalidValue;
@@ -1040,7 +1431,10 @@ hipError_t rs3_launch_attn(const Rs3ReadoutArgs& a, hipStream_t st, bool project
       if (project) return launch_attn_dh<32, true, true, 2>(a, G, nblk, st);
       return deep ? launch_attn_dh<32, false, true>(a, G, nblk, st) : launch_attn_dh<32, false, false>(a, G, nblk, st);
     case 64:
-      if (project) return launch_attn_dh<64, true, true, 2>(a, G, nblk, st);
+      if (project) {
+        RS3_LAUNCH(RS3_K_ATTN, st, k_attn_g2, dim3(nblk), dim3(512), G2Lds::BYTES, st, a, G, ab);
+        return hipGetLastError();
+      }
       return deep ? launch_attn_dh<64, false, true>(a, G, nblk, st) : launch_attn_dh<64, false, false>(a, G, nblk, st);
     case 128: return launch_attn_dh<128, false, false>(a, G, nblk, st);
     case 256: return launch_attn_dh<256, false, false>(a, G, nblk, st);
@@ -1048,7 +1442,8 @@ hipError_t rs3_launch_attn(const Rs3ReadoutArgs& a, hipStream_t st, bool project
   }
 }
 
-hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st, bool merge, bool* pending) {
+hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, const Rs3AttnBanks& ab, int dtype, hipStream_t st, bool merge,
+                              bool* pending) {
   if (pending) *pending = false;
   const int64_t cells = (int64_t)a.mn * a.C;
   const bool in_place = a.Y == a.X && !a.y_fp32;
@@ -1083,7 +1478,7 @@ hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  hipError_t e = rs3_launch_attn(a, st, project);
+  hipError_t e = rs3_launch_attn(a, ab, st, project);
   if (e != hipSuccess) return e;
   if (!merge) {
     if (pending) *pending = true;
@@ -1118,7 +1513,7 @@ hipError_t rs3_readout_setup() {
               {(const void*)k_attn<32, true, true, 2>, std::max(8 * AttnLds<32>::STAGE, AttnProj<32>::BYTES)},
               {(const void*)k_attn<64, false, false>, 4 * AttnLds<64>::STAGE},
               {(const void*)k_attn<64, false, true>, 8 * AttnLds<64>::STAGE},
-              {(const void*)k_attn<64, true, true, 2>, std::max(8 * AttnLds<64>::STAGE, AttnProj<64>::BYTES)},
+              {(const void*)k_attn_g2, G2Lds::BYTES},
               {(const void*)k_attn<128, false, false>, 4 * AttnLds<128>::STAGE},
               {(const void*)k_attn<256, false, false>, 4 * AttnLds<256>::STAGE}};
   for (const auto& k : attn) {

@@ -205,6 +205,17 @@ struct Rs3ReadoutArgs {
   const float* rope;      // [mn][d_h/2][2] rotary table for the queries, or null
 };
 
+// The attention-side pointers of every object's bank, handed to the
+// attention launch by value: its first loads (header word, tile entries, key
+// and value tiles) then need no read of the bank descriptor first.
+struct Rs3AttnBanks {
+  const int32_t* hdr[RS3_MAX_OBJ];
+  const rs3::TileEnt* tiles[RS3_MAX_OBJ];
+  const void* kh[RS3_MAX_OBJ];
+  const void* vh[RS3_MAX_OBJ];
+  int32_t ntcap[RS3_MAX_OBJ];   // entries of the tile list (n_tiles_cap)
+};
+
 // Bare attention core: the tensors of rs3_attend laid out as a one-frame
 // bank in the caller's workspace.
 struct AttendPrepArgs {
@@ -236,14 +247,14 @@ hipError_t rs3_launch_commit(const Rs3CommitArgs& a, int dtype, int d_kv, int D,
                              hipStream_t st);
 // merge = false leaves the split merge of the bf16 path to the caller (the
 // fused merge + commit launch); returns whether a merge is pending in *pending.
-hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, int dtype, hipStream_t st, bool merge = true,
-                              bool* pending = nullptr);
+hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, const Rs3AttnBanks& ab, int dtype, hipStream_t st,
+                              bool merge = true, bool* pending = nullptr);
 // The readout's split merge and a commit in one launch (bf16 layers).
 hipError_t rs3_launch_merge_commit(const Rs3ReadoutArgs& ra, const Rs3CommitArgs& ca, int d_kv, hipStream_t st);
 hipError_t rs3_fused_setup();
 // Split-KV attention only; project: the queries are projected from X[sel]
 // inside the kernel (heads of width <= 64), else read from a.Q.
-hipError_t rs3_launch_attn(const Rs3ReadoutArgs& a, hipStream_t st, bool project);
+hipError_t rs3_launch_attn(const Rs3ReadoutArgs& a, const Rs3AttnBanks& ab, hipStream_t st, bool project);
 hipError_t rs3_launch_attend_prep(const AttendPrepArgs& p, hipStream_t st);
 hipError_t rs3_launch_attend_merge(const Rs3ReadoutArgs& a, int SA, float* O, hipStream_t st);
 hipError_t rs3_launch_attend_f32(const float* Q, const float* K, const float* V, int n_q, int64_t n_kv, int H,

@@ -142,6 +142,7 @@ WINDOW_CASES = {
     "projected_d256": (CONFIGS["sam2_single"], dict(absorb=False), None, None),           # flat, d_h 256
     "projected_2x128": (replace(CONFIGS["sam2_single"], H=2, d_h=128), {}, None, None),    # flat, d_h 128
     "rope_4x64": (replace(CONFIGS["sam2_single"], H=4, d_h=64), {}, 10000.0, None),       # deep, d_h 64
+    "projected_4x64": (replace(CONFIGS["sam2_single"], H=4, d_h=64), {}, None, None),     # projecting, 2 wave groups
     "rope_8x32_rho0.1": (replace(CONFIGS["highres"], f_max=3, cap_frames=4), {}, 10000.0, "0.1"),   # deep, d_h 32
     "8x32_rho0.5": (replace(CONFIGS["highres"], f_max=3, cap_frames=4), {}, None, "0.5"),   # flat, d_h 32
 }
@@ -163,6 +164,21 @@ def test_single_split_window_slide(case):
     r.select_readout(cfg.f_max, fused=True, dense_oracle=True)
     r.select_readout(cfg.f_max + 1, dense_oracle=True)
     _log("window %s: %d keys, stats %s" % (case, keys, r.stats))
+
+
+@pytest.mark.parametrize("n_splits", [0, 3])
+def test_four_heads_of_64_projecting(n_splits):
+    """Four heads of 64 at d_model 256 without a rotary table: the attention
+    projects its queries inside, with the head index selecting W_q rows,
+    partial columns and (m, l) slots."""
+    cfg = replace(CONFIGS["sam2_single"], H=4, d_h=64)
+    r = Runner(cfg, cfg.f_max + 2, max_sel=k_from_rho("0.3", cfg.mn), n_splits=n_splits)
+    r.commit(0, True)
+    for t in range(1, cfg.f_max):
+        r.commit(t, False)
+    r.select_readout(cfg.f_max, fused=True, dense_oracle=True)
+    r.select_readout(cfg.f_max + 1, dense_oracle=True)
+    _log("4x64 splits=%d stats %s" % (n_splits, r.stats))
 
 
 # ---------------------------------------------------------------------------
