@@ -224,7 +224,8 @@ def gpu_run(args):
     step_t = [n_pre]
     main = torch.cuda.current_stream()
     two = args.streams == 2
-    fused = not two and not args.separate
+    calls = "separate" if (two or args.separate) else args.calls
+    fused = calls == "readout_commit"
     side = torch.cuda.Stream() if two else main
     ev_read = torch.cuda.Event()
     ev_commit = torch.cuda.Event()
@@ -237,6 +238,18 @@ def gpu_run(args):
         # t-1), and frame t's commit waits for the readout.
         t = step_t[0]
         f = frames[n_pre + (t - n_pre) % N_DISTINCT]
+        if calls == "frame":
+            # the whole frame in one call (rs3_frame)
+            if record is not None:
+                nk = [b.info()["n_keys"] for b in sess.banks]
+            sess.frame(f["rmask"], f["X"], f["k"], f["X"] if in_place else Y, f["K"], f["V"], f["mask"], t, False,
+                       max_sel=f["max_sel"])
+            if record is not None:
+                cnt = sess.sel_count.cpu().numpy()
+                g = [0 if cfg.union_objects else o for o in range(cfg.n_obj)]
+                record.append(dict(sel=[int(cnt[g[o]]) for o in range(cfg.n_obj)], n_keys=nk))
+            step_t[0] += 1
+            return
         sess.select(f["rmask"], f["X"], f["k"])
         if two:
             main.wait_event(ev_commit)
@@ -346,8 +359,9 @@ def gpu_run(args):
         "config": {"workload": _describe(cfg), "grid": "%dx%d" % (cfg.m, cfg.n), "n_obj": cfg.n_obj,
                    "bank_frames": cfg.f_max, "d_model": cfg.C, "heads": cfg.H, "d_head": cfg.d_h,
                    "d_kv": cfg.d_kv, "eager_launches": True, "streams": args.streams,
-                   "calls": "select + readout + commit" if (args.separate or args.streams == 2)
-                   else "select + readout_commit", "readout": "in place" if in_place else "out of place",
+                   "calls": {"separate": "select + readout + commit", "readout_commit": "select + readout_commit",
+                             "frame": "rs3_frame (select + readout + commit in one call)"}[calls],
+                   "readout": "in place" if in_place else "out of place",
                    "attention": ("absorbed: one head of width d_kv=%d on the raw bank rows" % cfg.d_kv) if absorb
                    else ("projected: %d head(s) of width %d%s" % (cfg.H, cfg.d_h,
                          ", axial rotary table (theta %g) on queries and keys" % args.rope if args.rope else ""))},
@@ -483,12 +497,12 @@ def run_workload(cfg, *, absorb, steps, warmup, commit=True, prefill=None, split
         fi = frame_of(t)
         for ci, sess in enumerate(sessions):
             f = frames[fi]["per"][ci]
-            sess.select(f["rmask"], f["X"], f["k"])
             Y = outs[ci]
-            if commit:   # readout and commit in one call
-                sess.readout_commit(f["X"], f["X"] if Y is None else Y, f["K"], f["V"], f["mask"], t, False,
-                                    max_sel=frames[fi]["max_sel"])
+            if commit:   # the whole frame in one call
+                sess.frame(f["rmask"], f["X"], f["k"], f["X"] if Y is None else Y, f["K"], f["V"], f["mask"], t,
+                           False, max_sel=frames[fi]["max_sel"])
             else:
+                sess.select(f["rmask"], f["X"], f["k"])
                 sess.readout(f["X"], f["X"] if Y is None else Y, max_sel=frames[fi]["max_sel"])
         if commit:
             step_t[0] += 1
@@ -673,7 +687,10 @@ def main():
     ap.add_argument("--streams", type=int, choices=[1, 2], default=1,
                     help="2: frame t's commit overlaps frame t+1's selection on a second stream")
     ap.add_argument("--separate", action="store_true",
-                    help="readout and commit as two calls (default: rs3_readout_commit, one call)")
+                    help="select, readout and commit as three calls (same as --calls separate)")
+    ap.add_argument("--calls", choices=["frame", "readout_commit", "separate"], default="frame",
+                    help="frame: one rs3_frame call per frame (default); readout_commit: rs3_select_queries + "
+                         "rs3_readout_commit; separate: select, readout and commit")
     ap.add_argument("--no-graph", dest="graph", action="store_false",
                     help="skip the HIP-graph replay pass (reported beside the eager frames/s)")
     ap.add_argument("--cpu-frames", type=int, default=40)

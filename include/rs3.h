@@ -299,6 +299,52 @@ rs3_status rs3_readout_commit(const rs3_layer* L, const rs3_grid* g, int32_t n_o
                               int32_t t, int32_t pin, int32_t fall_min, int32_t fall_max, int32_t* kept_count,
                               void* stream);
 
+/* ---- one frame of the path in one call (Algorithm 1's per-frame body) -------
+ * rs3_select_queries, then rs3_readout_commit, on the same stream, for one
+ * frame of every object: the previous masks select the queries (Eqs. 1, 2,
+ * 4, 5), the selected queries read the banks (Eq. 6), and the frame's memory
+ * tokens are committed (Eq. 8).  The results are those of the separate calls
+ * with the same arguments (bit for bit).  C and the dtype are the layer's;
+ * the selection lists are per group with sel_stride 0 (one union group) or
+ * m*n (one group per object), as in rs3_select_queries.
+ * Because one call sees the whole frame, it may fuse across the calls: with
+ * one attention head of width 64 at d_model 256 (the absorbed form, d_kv =
+ * 64, no rotary table), the energy launch also projects the query of every
+ * cell (it reads every row of X anyway) and the attention gathers projected
+ * rows; the projection then runs for all m*n cells rather than the selected
+ * ones (2*m*n*256*64 flops per grid).
+ * ws: device workspace of at least rs3_frame_workspace_size() bytes (a size
+ * queried for max_sel also serves every smaller max_sel).  Errors as in the
+ * separate calls; every argument is checked before any device work. */
+typedef struct {
+  /* selection (rs3_select_queries) */
+  const uint8_t* read_masks;   /* [n_obj][m*s][n*s] masks of the previous frame */
+  const void* X;               /* [n_x][m*n][C] query tokens */
+  int64_t x_obj_stride;        /* 0 = one grid shared by all objects */
+  const int32_t* k;            /* [host][n_groups] keep budgets */
+  rs3_select_params params;
+  int32_t* sel_idx;            /* out [n_groups][m*n] */
+  int32_t* sel_count;          /* out [n_groups] */
+  uint8_t* prior_out;          /* optional out [n_groups][m*n] */
+  /* readout (rs3_readout) */
+  int32_t max_sel, n_splits;
+  void* Y;                     /* may equal X as in rs3_readout */
+  int64_t y_obj_stride;
+  int32_t y_fp32;
+  /* commit (rs3_commit) */
+  const void* Kmem;
+  const void* Vmem;
+  int64_t kv_obj_stride;
+  const uint8_t* commit_masks; /* [n_obj][m*s][n*s] masks of this frame */
+  int32_t t, pin, fall_min, fall_max;
+  int32_t* kept_count;         /* optional out [n_obj] */
+} rs3_frame_io;
+rs3_status rs3_frame_workspace_size(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, int64_t x_obj_stride,
+                                    int32_t max_sel, int32_t n_splits, size_t* bytes);
+rs3_status rs3_frame(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, rs3_track* tr,
+                     rs3_bank* const* banks /*[host]*/, const rs3_frame_io* io /*[host]*/, void* ws,
+                     size_t ws_bytes, void* stream);
+
 /* ---- the paper's fixed write keep-set (Sec. 3.2, Eq. 8) -------------------
  * K_w = union over the n_obj objects of dilate_{D_w}(down_s(seed_masks[o])),
  * where seed_masks[o] is object o's mask at its first frame ([n_obj][m*s][n*s]

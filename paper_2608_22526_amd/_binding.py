@@ -33,6 +33,15 @@ class SelectParams(ctypes.Structure):
     _fields_ = [("r_s", c_i32), ("c", c_i32), ("seed_box", c_i32), ("union_objects", c_i32)]
 
 
+class FrameIO(ctypes.Structure):
+    """rs3_frame_io: the arguments of one frame (select, readout, commit)."""
+    _fields_ = [("read_masks", c_vp), ("X", c_vp), ("x_obj_stride", c_i64), ("k", c_vp), ("params", SelectParams),
+                ("sel_idx", c_vp), ("sel_count", c_vp), ("prior_out", c_vp), ("max_sel", c_i32),
+                ("n_splits", c_i32), ("Y", c_vp), ("y_obj_stride", c_i64), ("y_fp32", c_i32), ("Kmem", c_vp),
+                ("Vmem", c_vp), ("kv_obj_stride", c_i64), ("commit_masks", c_vp), ("t", c_i32), ("pin", c_i32),
+                ("fall_min", c_i32), ("fall_max", c_i32), ("kept_count", c_vp)]
+
+
 class Rs3Error(RuntimeError):
     def __init__(self, status: int, what: str):
         self.status = status
@@ -69,6 +78,9 @@ _SIGS = {
                                    c_i32, c_i32, c_vp, c_vp]),
     "rs3_commit": (c_i32, [c_vp, c_i32, ctypes.POINTER(Grid), c_vp, c_vp, c_i64, c_vp, c_i32, c_i32, c_i32,
                            c_i32, c_vp, c_vp]),
+    "rs3_frame_workspace_size": (c_i32, [c_vp, ctypes.POINTER(Grid), c_i32, c_i64, c_i32, c_i32,
+                                         ctypes.POINTER(c_sz)]),
+    "rs3_frame": (c_i32, [c_vp, ctypes.POINTER(Grid), c_i32, c_vp, c_vp, ctypes.POINTER(FrameIO), c_vp, c_sz, c_vp]),
     "rs3_write_keepset": (c_i32, [ctypes.POINTER(Grid), c_i32, c_vp, c_i32, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp]),
     "rs3_close_workspace_size": (c_i32, [c_i32, c_i32, c_i32, ctypes.POINTER(c_sz)]),
     "rs3_close_masks": (c_i32, [c_i32, c_i32, c_i32, c_vp, c_i32, c_i32, c_vp, c_vp, c_vp, c_sz, c_vp]),
@@ -304,6 +316,21 @@ def readout_commit(layer: Layer, grid, n_obj: int, X, x_obj_stride: int, banks: 
                                     n_splits, _ptr(Y), y_obj_stride, y_fp32, _ptr(ws), ws_bytes, _ptr(Kmem),
                                     _ptr(Vmem), kv_obj_stride, _ptr(masks), t, pin, fall_min, fall_max,
                                     _ptr(kept_count), _stream(stream)), "rs3_readout_commit")
+
+
+def frame_workspace_size(layer: Layer, grid, n_obj: int, x_obj_stride: int, max_sel: int, n_splits: int = 0) -> int:
+    out = c_sz()
+    _check(lib().rs3_frame_workspace_size(layer.h, ctypes.byref(_grid(grid)), n_obj, x_obj_stride, max_sel, n_splits,
+                                          ctypes.byref(out)), "rs3_frame_workspace_size")
+    return out.value
+
+
+def frame(layer: Layer, grid, n_obj: int, track: Track, banks: Sequence[Bank], io: FrameIO, ws, stream=None):
+    """One frame: rs3_select_queries then rs3_readout_commit in one call
+    (`io` holds the arguments of both)."""
+    harr = (c_vp * len(banks))(*[b.h for b in banks])
+    _check(lib().rs3_frame(layer.h, ctypes.byref(_grid(grid)), n_obj, track.h, ctypes.cast(harr, c_vp),
+                           ctypes.byref(io), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)), "rs3_frame")
 
 
 def write_keepset(grid, n_obj: int, seed_masks, D_w: int, fall_min: int, fall_max: int, n_copies: int, keep,

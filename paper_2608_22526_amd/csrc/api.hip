@@ -577,10 +577,21 @@ rs3_status rs3_select_workspace_size(const rs3_grid* g, int32_t n_obj, int64_t x
   return RS3_OK;
 }
 
-rs3_status rs3_select_queries(const rs3_grid* g, int32_t n_obj, const uint8_t* masks, rs3_track* tr,
-                              const void* X, int64_t x_obj_stride, int32_t C, rs3_dtype dt,
-                              const int32_t* k, const rs3_select_params* p, void* ws, size_t ws_bytes,
-                              int32_t* sel_idx, int32_t* sel_count, uint8_t* prior_out, void* stream) {
+// Validates a select call and fills its kernel arguments (no device work).
+struct SelectLaunch {
+  Rs3SelectArgs a;
+  const void* X;
+  int64_t x_stride;
+  int n_x, mn, C, dtype, n_groups;
+  double* e;
+  unsigned long long* erange;
+  uint64_t* pbits;
+};
+
+static rs3_status select_args(const rs3_grid* g, int32_t n_obj, const uint8_t* masks, rs3_track* tr, const void* X,
+                              int64_t x_obj_stride, int32_t C, rs3_dtype dt, const int32_t* k,
+                              const rs3_select_params* p, void* ws, size_t ws_bytes, int32_t* sel_idx,
+                              int32_t* sel_count, uint8_t* prior_out, SelectLaunch& sl) {
   if (!grid_ok(g) || !masks || !tr || !X || !k || !p || !ws || !sel_idx || !sel_count) return RS3_E_INVALID;
   if (n_obj <= 0 || n_obj > RS3_MAX_OBJ || tr->n_obj != n_obj) return RS3_E_INVALID;
   if (dt != RS3_BF16 && dt != RS3_F32) return RS3_E_INVALID;
@@ -596,19 +607,16 @@ rs3_status rs3_select_queries(const rs3_grid* g, int32_t n_obj, const uint8_t* m
   size_t need;
   rs3_select_workspace_size(g, n_obj, x_obj_stride, &need);
   if (ws_bytes < need) return RS3_E_INVALID;
-  rs3_status st0 = ensure_setup();
-  if (st0 != RS3_OK) return st0;
-  hipStream_t st = (hipStream_t)stream;
   const int n_x = x_obj_stride ? n_obj : 1;
-  double* e = (double*)ws;
-  unsigned long long* erange = (unsigned long long*)((uint8_t*)ws + align256((size_t)n_x * mn * 8));
-  uint64_t* pbits = (uint64_t*)((uint8_t*)erange + align256((size_t)n_x * ((mn + 63) / 64) * 16));
-  Rs3SelectArgs a;
+  sl.e = (double*)ws;
+  sl.erange = (unsigned long long*)((uint8_t*)ws + align256((size_t)n_x * mn * 8));
+  sl.pbits = (uint64_t*)((uint8_t*)sl.erange + align256((size_t)n_x * ((mn + 63) / 64) * 16));
+  Rs3SelectArgs& a = sl.a;
   memset(&a, 0, sizeof(a));
   a.masks = masks;
   a.track = tr->d_state;
-  a.e = e;
-  a.erange = erange;
+  a.e = sl.e;
+  a.erange = sl.erange;
   a.sel_idx = sel_idx;
   a.sel_count = sel_count;
   a.prior_out = prior_out;
@@ -622,15 +630,43 @@ rs3_status rs3_select_queries(const rs3_grid* g, int32_t n_obj, const uint8_t* m
   a.c = p->c;
   a.x_per_obj = n_x > 1;
   for (int i = 0; i < n_groups; ++i) a.k[i] = k[i];
+  sl.X = X;
+  sl.x_stride = x_obj_stride;
+  sl.n_x = n_x;
+  sl.mn = mn;
+  sl.C = C;
+  sl.dtype = dt;
+  sl.n_groups = n_groups;
+  return RS3_OK;
+}
+
+// Energies (and the priors beside them, and with qp every row's projected
+// query), then the selection.
+static hipError_t select_launch(SelectLaunch& sl, hipStream_t st, const Rs3QProjArgs* qp = nullptr) {
+  Rs3SelectArgs& a = sl.a;
   hipError_t he;
-  if (rs3_select_prior_beside(g->m, g->n, g->s)) {
-    a.prior_bits = pbits;
-    he = rs3_launch_energy_prior(X, x_obj_stride, n_x, mn, C, dt, e, erange, a, n_groups, st);
+  if (rs3_select_prior_beside(a.m, a.n, a.s)) {
+    a.prior_bits = sl.pbits;
+    he = rs3_launch_energy_prior(sl.X, sl.x_stride, sl.n_x, sl.mn, sl.C, sl.dtype, sl.e, sl.erange, a, sl.n_groups, st,
+                                 qp);
   } else {
-    he = rs3_launch_energy(X, x_obj_stride, n_x, mn, C, dt, e, erange, st);
+    he = rs3_launch_energy(sl.X, sl.x_stride, sl.n_x, sl.mn, sl.C, sl.dtype, sl.e, sl.erange, st, qp);
   }
-  if (he != hipSuccess) return map_err(he);
-  return map_err(rs3_launch_select(a, n_groups, st));
+  if (he != hipSuccess) return he;
+  return rs3_launch_select(a, sl.n_groups, st);
+}
+
+rs3_status rs3_select_queries(const rs3_grid* g, int32_t n_obj, const uint8_t* masks, rs3_track* tr,
+                              const void* X, int64_t x_obj_stride, int32_t C, rs3_dtype dt,
+                              const int32_t* k, const rs3_select_params* p, void* ws, size_t ws_bytes,
+                              int32_t* sel_idx, int32_t* sel_count, uint8_t* prior_out, void* stream) {
+  SelectLaunch sl;
+  rs3_status st = select_args(g, n_obj, masks, tr, X, x_obj_stride, C, dt, k, p, ws, ws_bytes, sel_idx, sel_count,
+                              prior_out, sl);
+  if (st != RS3_OK) return st;
+  st = ensure_setup();
+  if (st != RS3_OK) return st;
+  return map_err(select_launch(sl, (hipStream_t)stream));
 }
 
 // ---- bare attention core ---------------------------------------------------
@@ -1074,6 +1110,90 @@ rs3_status rs3_readout_commit(const rs3_layer* L, const rs3_grid* g, int32_t n_o
                 : rs3_launch_commit(ca, ld.dtype, ld.d_kv, ld.Da, ld.Ha, ld.dah, s);
   if (e != hipSuccess) return map_err(e);
   commit_done(banks, n_obj, pin);
+  return RS3_OK;
+}
+
+// ---- one frame ------------------------------------------------------------
+namespace {
+// Layers whose attention, when it projects inside, can take the energy
+// launch's projection of every cell: one head of width 64 at d_model 256.
+bool frame_qproj_layer(const LayerDev& ld) {
+  return ld.dtype == RS3_BF16 && ld.Ha == 1 && ld.Da == 64 && ld.C == 256 && !ld.rope;
+}
+struct FrameLayout {
+  size_t sel, read, q, total;
+};
+rs3_status frame_layout(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, int64_t x_obj_stride, int32_t max_sel,
+                        int32_t n_splits, FrameLayout* fl) {
+  size_t sel = 0, read = 0;
+  rs3_status st = rs3_select_workspace_size(g, n_obj, x_obj_stride, &sel);
+  if (st != RS3_OK) return st;
+  st = rs3_readout_workspace_size(L, n_obj, max_sel, n_splits, &read);
+  if (st != RS3_OK) return st;
+  const int64_t mn = (int64_t)g->m * g->n;
+  const int n_x = x_obj_stride ? n_obj : 1;
+  fl->sel = align256(sel);
+  fl->read = align256(read);
+  fl->q = frame_qproj_layer(L->dev) ? align256((size_t)n_x * mn * 64 * 2) : 0;
+  fl->total = fl->sel + fl->read + fl->q;
+  return RS3_OK;
+}
+}  // namespace
+
+rs3_status rs3_frame_workspace_size(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, int64_t x_obj_stride,
+                                    int32_t max_sel, int32_t n_splits, size_t* bytes) {
+  if (!L || !bytes) return RS3_E_INVALID;
+  FrameLayout fl;
+  rs3_status st = frame_layout(L, g, n_obj, x_obj_stride, max_sel, n_splits, &fl);
+  if (st != RS3_OK) return st;
+  *bytes = fl.total;
+  return RS3_OK;
+}
+
+rs3_status rs3_frame(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, rs3_track* tr, rs3_bank* const* banks,
+                     const rs3_frame_io* io, void* ws, size_t ws_bytes, void* stream) {
+  if (!L || !io || !ws) return RS3_E_INVALID;
+  FrameLayout fl;
+  rs3_status st = frame_layout(L, g, n_obj, io->x_obj_stride, io->max_sel, io->n_splits, &fl);
+  if (st != RS3_OK) return st;
+  if (ws_bytes < fl.total) return RS3_E_INVALID;
+  uint8_t* w = (uint8_t*)ws;
+  const LayerDev& ld = L->dev;
+  SelectLaunch sl;
+  st = select_args(g, n_obj, io->read_masks, tr, io->X, io->x_obj_stride, ld.C, (rs3_dtype)ld.dtype, io->k,
+                   &io->params, w, fl.sel, io->sel_idx, io->sel_count, io->prior_out, sl);
+  if (st != RS3_OK) return st;
+  const int mn = g->m * g->n;
+  Rs3ReadoutArgs ra;
+  Rs3AttnBanks ab;
+  Rs3CommitArgs ca;
+  st = readout_args(L, g, n_obj, io->X, io->x_obj_stride, banks, io->sel_idx, io->sel_count,
+                    io->params.union_objects ? 0 : mn, io->max_sel, io->n_splits, io->Y, io->y_obj_stride, io->y_fp32,
+                    w + fl.sel, fl.read, ra, ab);
+  if (st != RS3_OK) return st;
+  st = commit_args(banks, n_obj, g, io->Kmem, io->Vmem, io->kv_obj_stride, io->commit_masks, io->t, io->pin,
+                   io->fall_min, io->fall_max, io->kept_count, ca);
+  if (st != RS3_OK) return st;
+  st = ensure_setup();
+  if (st != RS3_OK) return st;
+  const hipStream_t s = (hipStream_t)stream;
+  Rs3QProjArgs qp;
+  const bool pre = fl.q > 0 && io->max_sel > 0 && rs3_attn_projects(ra);
+  if (pre) {
+    qp.WqT = (const bf16_t*)ld.WqT;
+    qp.Qall = (bf16_t*)(w + fl.sel + fl.read);
+    qp.qscale = ra.qscale;
+    ra.Qall = qp.Qall;
+    ra.qall_stride = io->x_obj_stride ? (int64_t)mn * 64 : 0;
+  }
+  hipError_t e = select_launch(sl, s, pre ? &qp : nullptr);
+  bool pending = false;
+  if (e == hipSuccess) e = rs3_launch_readout(ra, ab, ld.dtype, s, false, &pending);
+  if (e == hipSuccess)
+    e = pending ? rs3_launch_merge_commit(ra, ca, ld.d_kv, s)
+                : rs3_launch_commit(ca, ld.dtype, ld.d_kv, ld.Da, ld.Ha, ld.dah, s);
+  if (e != hipSuccess) return map_err(e);
+  commit_done(banks, n_obj, io->pin);
   return RS3_OK;
 }
 

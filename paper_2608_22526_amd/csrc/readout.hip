@@ -908,6 +908,10 @@ struct G2Lds {
 static_assert(G2Lds::BYTES >= 8 * G2Lds::STAGE, "the eight stages fit");
 static_assert(G2Lds::BYTES <= 160 * 1024, "one CU's LDS");
 
+// QPRE (rs3_frame): the queries of every cell were projected by the energy
+// launch (a.Qall); each lane gathers its query's projected row instead, and
+// the projection steps 2-3 fall away.
+template <bool QPRE>
 __global__ __launch_bounds__(512) void k_attn_g2(Rs3ReadoutArgs a, int G, Rs3AttnBanks ab) {
   constexpr int DH = G2_DH, NT = 512;
   using L = AttnLds<DH>;
@@ -930,16 +934,16 @@ __global__ __launch_bounds__(512) void k_attn_g2(Rs3ReadoutArgs a, int G, Rs3Att
   //    wait for them alone).  Group g holds channel half g of the operands:
   //    thread lt = tid % 256 of the group holds chunk 16g + lt%16 of X rows
   //    lt/16 + 16 i and of W_q^T rows h*64 + lt/16 + 16 j.
-  constexpr int NX = 8, NW = 4;
+  constexpr int NX = QPRE ? 1 : 8, NW = QPRE ? 1 : 4;
   const int lt = tid & 255, hchunk = G2_HC * grp + (lt & 15);
   int src[NX];
-  {
-    const int32_t* sel = a.sel_idx + (int64_t)o * a.sel_stride;
+  u32x4 wreg[NW];
+  const int32_t* sel = a.sel_idx + (int64_t)o * a.sel_stride;
+  if constexpr (QPRE) {
+    src[0] = gload(sel + min(qrow, a.max_sel - 1));   // this lane's query cell
+  } else {
 #pragma unroll
     for (int i = 0; i < NX; ++i) src[i] = gload(sel + min(row0 + (lt >> 4) + 16 * i, a.max_sel - 1));
-  }
-  u32x4 wreg[NW];
-  {
     const u32x4* wb = (const u32x4*)((const bf16_t*)a.WqT + (int64_t)h * DH * PJ_PC * 8) + hchunk;
 #pragma unroll
     for (int j = 0; j < NW; ++j) wreg[j] = gload(wb + ((lt >> 4) + 16 * j) * PJ_PC);
@@ -962,8 +966,10 @@ __global__ __launch_bounds__(512) void k_attn_g2(Rs3ReadoutArgs a, int G, Rs3Att
   auto keep_loads = [&]() {
 #pragma unroll
     for (int i = 0; i < NX; ++i) keep(src[i]);
+    if constexpr (!QPRE) {
 #pragma unroll
-    for (int j = 0; j < NW; ++j) keep(wreg[j]);
+      for (int j = 0; j < NW; ++j) keep(wreg[j]);
+    }
     keep(c_tile);
     keep(c_mlo);
     keep(c_mhi);
@@ -975,7 +981,7 @@ __global__ __launch_bounds__(512) void k_attn_g2(Rs3ReadoutArgs a, int G, Rs3Att
   // 2. the gathered X rows (invalid list entries read row 0; the merge skips
   //    their rows)
   u32x4 xv[NX];
-  {
+  if constexpr (!QPRE) {
     const bf16_t* X = (const bf16_t*)a.X + (int64_t)o * a.x_stride;
 #pragma unroll
     for (int i = 0; i < NX; ++i) {
@@ -986,8 +992,10 @@ __global__ __launch_bounds__(512) void k_attn_g2(Rs3ReadoutArgs a, int G, Rs3Att
   const int nts = ntiles > s ? (ntiles - s + S - 1) / S : 0;   // tiles of this split
   if (nts == 0) {
     keep_loads();
+    if constexpr (!QPRE) {
 #pragma unroll
-    for (int i = 0; i < NX; ++i) keep(xv[i]);
+      for (int i = 0; i < NX; ++i) keep(xv[i]);
+    }
     // the empty partial (m = -inf, l = 0), so that the merge reads every split
     if (g == 0 && grp == 0 && qrow < cnt) {
       float* ml = a.ML + ((((int64_t)o * S + s) * a.max_sel + qrow) * a.H + h) * 2;
@@ -1028,6 +1036,27 @@ __global__ __launch_bounds__(512) void k_attn_g2(Rs3ReadoutArgs a, int G, Rs3Att
       attn_issue<DH>(Kh, Vh, tl, v & 1, h, H, lds + (2 * slot + k) * L::STAGE, wave, doff);
     }
   };
+  u32x4 qreg[DH / 16];
+  if constexpr (QPRE) {
+    // each group's first pair (as below), then this lane's projected query
+    // row (invalid list entries read row 0; the merge skips their rows)
+    const int p0 = min(grp, npair - 1);
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int v = half_at(2 * p0 + k);
+      const int tl = __builtin_amdgcn_readlane(c_tile, v >> 1);
+      attn_issue<DH>(Kh, Vh, tl, v & 1, h, H, lds + (2 * grp + k) * L::STAGE, wave, doff);
+    }
+    const int cell = (src[0] < 0 || src[0] >= a.mn) ? 0 : src[0];
+    const bf16_t* qp = (const bf16_t*)a.Qall + (int64_t)o * a.qall_stride + (int64_t)cell * DH + 8 * g;
+#pragma unroll
+    for (int ks = 0; ks < DH / 16; ++ks) qreg[ks] = gload((const u32x4*)(qp + 16 * ks));
+    // both in: the loop's first wait then finds nothing outstanding, and the
+    // empty asm hands the rows on as settled values
+    wait_vmcnt<0>();
+#pragma unroll
+    for (int ks = 0; ks < DH / 16; ++ks) asm volatile("" : "+v"(qreg[ks]));
+  } else {
   // 3. query projection, d-block grp of the wave's 32 queries, in two passes
   //    over the channel halves: group p writes half p of the operands in pass
   //    p.  Pass 0's operands are stored before the first key/value DMA is
@@ -1094,7 +1123,6 @@ __global__ __launch_bounds__(512) void k_attn_g2(Rs3ReadoutArgs a, int G, Rs3Att
   ds_store16(xw + 16, mine[1]);
   lds_barrier();
   const u32x4* xr = (const u32x4*)(lds + G2Lds::XCH) + ((wave_all ^ 4) * 64 + lane) * 2;
-  u32x4 qreg[DH / 16];
   if (grp == 0) {
     qreg[0] = mine[0];
     qreg[1] = mine[1];
@@ -1106,6 +1134,7 @@ __global__ __launch_bounds__(512) void k_attn_g2(Rs3ReadoutArgs a, int G, Rs3Att
     qreg[2] = mine[0];
     qreg[3] = mine[1];
   }
+  }   // !QPRE
   const bool qv = qrow < cnt;
 #pragma unroll
   for (int ks = 0; ks < DH / 16; ++ks)
@@ -1116,10 +1145,17 @@ __global__ __launch_bounds__(512) void k_attn_g2(Rs3ReadoutArgs a, int G, Rs3Att
   // (the group's previous pair is done and its stages free; in the first
   // iteration: every wave is done with the projection's LDS), issues pair
   // p+2 and computes pair p.
+  // The logits come out of the MFMA already shifted by the running reference
+  // maximum: the accumulator input is -m_run (one tile per lane, whose 16
+  // values all belong to its query), so the common pair needs no
+  // subtraction before the exponentials; only a pair that moves the
+  // reference (the first one, then rarely) shifts its own logits.
   f32x16 acc[DH / 32];
 #pragma unroll
   for (int dt = 0; dt < DH / 32; ++dt) acc[dt] = f32x16{};
   float m_run = -INFINITY, l_run = 0.f;
+  f32x16 negm = f32x16{};   // -reference (0 until the first pair sets it)
+  bool first = true;
   const int kbase = (lane & 31) * L::KP + 16 * g;
   const int vbase = L::KREG + (lane & 31) * L::VP + 16 * g;
   const int nit = (npair + 1) >> 1;
@@ -1139,7 +1175,22 @@ __global__ __launch_bounds__(512) void k_attn_g2(Rs3ReadoutArgs a, int G, Rs3Att
     const uint8_t* SA = lds + (2 * (p & 3)) * L::STAGE;
     const uint8_t* SB = SA + L::STAGE;
     f32x16 sA, sB;
-    attn_scores_pair<DH>(SA + kbase, SB + kbase, qreg, sA, sB);
+    {
+      u32x4 ra[DH / 16], rb[DH / 16];
+#pragma unroll
+      for (int jj = 0; jj < DH / 16; ++jj) {
+        ra[jj] = *(const u32x4*)(SA + kbase + jj * 32);
+        rb[jj] = *(const u32x4*)(SB + kbase + jj * 32);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      sA = mfma32(ra[0], qreg[0], negm);
+      sB = mfma32(rb[0], qreg[0], negm);
+#pragma unroll
+      for (int jj = 1; jj < DH / 16; ++jj) {
+        sA = mfma32(ra[jj], qreg[jj], sA);
+        sB = mfma32(rb[jj], qreg[jj], sB);
+      }
+    }
     if (mA != 0xffffffffu) {   // partial or empty half tile (frame boundary)
 #pragma unroll
       for (int r = 0; r < 16; ++r)
@@ -1153,26 +1204,35 @@ __global__ __launch_bounds__(512) void k_attn_g2(Rs3ReadoutArgs a, int G, Rs3Att
     float mx = __builtin_elementwise_maximum(sA[0], sB[0]);
 #pragma unroll
     for (int r = 1; r < 16; ++r) mx = max3f(mx, sA[r], sB[r]);
-    mx = max_with_partner(mx);
-    const bool need = mx > m_run + RESCALE_LOG2;   // lazy rescale, as in k_attn
+    mx = max_with_partner(mx);   // relative to the reference
+    // lazy rescale as in k_attn: the reference moves when a pair exceeds it
+    // by more than RESCALE_LOG2 (and at the first pair, to its maximum)
+    const bool need = first || mx > RESCALE_LOG2;
     if (__any(need)) {
-      const float m_new = need ? mx : m_run;
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      const float d = need ? mx : 0.f;
+      const float alpha = first ? 0.f : __builtin_amdgcn_exp2f(-d);
       l_run *= alpha;
 #pragma unroll
       for (int dt = 0; dt < DH / 32; ++dt) acc[dt] *= alpha;
-      m_run = m_new;
+      m_run = first ? d : m_run + d;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        sA[r] -= d;
+        sB[r] -= d;
+        negm[r] = -m_run;
+      }
     }
+    first = false;
     float psum = 0.f;
     u32x4 pkA[2], pkB[2];
 #pragma unroll
     for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
-        const float a0 = __builtin_amdgcn_exp2f(sA[8 * hf + 2 * jj] - m_run);
-        const float a1 = __builtin_amdgcn_exp2f(sA[8 * hf + 2 * jj + 1] - m_run);
-        const float b0 = __builtin_amdgcn_exp2f(sB[8 * hf + 2 * jj] - m_run);
-        const float b1 = __builtin_amdgcn_exp2f(sB[8 * hf + 2 * jj + 1] - m_run);
+        const float a0 = __builtin_amdgcn_exp2f(sA[8 * hf + 2 * jj]);
+        const float a1 = __builtin_amdgcn_exp2f(sA[8 * hf + 2 * jj + 1]);
+        const float b0 = __builtin_amdgcn_exp2f(sB[8 * hf + 2 * jj]);
+        const float b1 = __builtin_amdgcn_exp2f(sB[8 * hf + 2 * jj + 1]);
         pkA[hf][jj] = pack_bf16x2(a0, a1);
         pkB[hf][jj] = pack_bf16x2(b0, b1);
         psum = add_bf16x2(pkB[hf][jj], add_bf16x2(pkA[hf][jj], psum));
@@ -1421,6 +1481,8 @@ static bool attn_projects(const Rs3ReadoutArgs& a) {
   return a.d_h <= 64 && a.C == 8 * PJ_PC && nblk <= ATTN_DEEP_MAX_BLOCKS && !a.rope;
 }
 
+bool rs3_attn_projects(const Rs3ReadoutArgs& a) { return attn_projects(a); }
+
 hipError_t rs3_launch_attn(const Rs3ReadoutArgs& a, const Rs3AttnBanks& ab, hipStream_t st, bool project) {
   const int G = a.n_obj * a.H * a.S;
   const int nblk = 8 * a.n_qt * ((G + 7) / 8);
@@ -1432,7 +1494,10 @@ hipError_t rs3_launch_attn(const Rs3ReadoutArgs& a, const Rs3AttnBanks& ab, hipS
       return deep ? launch_attn_dh<32, false, true>(a, G, nblk, st) : launch_attn_dh<32, false, false>(a, G, nblk, st);
     case 64:
       if (project) {
-        RS3_LAUNCH(RS3_K_ATTN, st, k_attn_g2, dim3(nblk), dim3(512), G2Lds::BYTES, st, a, G, ab);
+        if (a.Qall)
+          RS3_LAUNCH(RS3_K_ATTN, st, k_attn_g2<true>, dim3(nblk), dim3(512), 8 * G2Lds::STAGE, st, a, G, ab);
+        else
+          RS3_LAUNCH(RS3_K_ATTN, st, k_attn_g2<false>, dim3(nblk), dim3(512), G2Lds::BYTES, st, a, G, ab);
         return hipGetLastError();
       }
       return deep ? launch_attn_dh<64, false, true>(a, G, nblk, st) : launch_attn_dh<64, false, false>(a, G, nblk, st);
@@ -1513,7 +1578,8 @@ hipError_t rs3_readout_setup() {
               {(const void*)k_attn<32, true, true, 2>, std::max(8 * AttnLds<32>::STAGE, AttnProj<32>::BYTES)},
               {(const void*)k_attn<64, false, false>, 4 * AttnLds<64>::STAGE},
               {(const void*)k_attn<64, false, true>, 8 * AttnLds<64>::STAGE},
-              {(const void*)k_attn_g2, G2Lds::BYTES},
+              {(const void*)k_attn_g2<false>, G2Lds::BYTES},
+              {(const void*)k_attn_g2<true>, 8 * G2Lds::STAGE},
               {(const void*)k_attn<128, false, false>, 4 * AttnLds<128>::STAGE},
               {(const void*)k_attn<256, false, false>, 4 * AttnLds<256>::STAGE}};
   for (const auto& k : attn) {

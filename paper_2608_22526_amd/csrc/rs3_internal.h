@@ -169,6 +169,16 @@ struct Rs3SelectArgs {
   int k[RS3_MAX_OBJ];
 };
 
+// Query projection of every grid row inside the energy launch (rs3_frame
+// with a single 64-wide attention head at d_model 256): the launch reads
+// every row of X anyway, and the attention then gathers projected rows.
+//   Qall[xi][i] = bf16(qscale * x_i W_q)  (W_q the attention's query weights)
+struct Rs3QProjArgs {
+  const rs3::bf16_t* WqT;   // [64][256] (W_q^T of the one head)
+  rs3::bf16_t* Qall;        // [n_x][mn][64]
+  float qscale;             // log2(e) / sqrt(d_h)
+};
+
 struct Rs3CommitArgs {
   rs3::BankDev* banks[RS3_MAX_OBJ];
   const uint8_t* masks;   // [n_obj][m*s][n*s]
@@ -203,6 +213,8 @@ struct Rs3ReadoutArgs {
   float qscale;           // log2(e) / sqrt(d_h)
   int mn, C, H, d_h, D, n_obj, max_sel, S, n_qt, y_fp32;
   const float* rope;      // [mn][d_h/2][2] rotary table for the queries, or null
+  const void* Qall;       // queries of every cell projected by the energy launch (rs3_frame), or null:
+  int64_t qall_stride;    //   [n_x][mn][64] bf16, elements between objects' grids (0 = shared)
 };
 
 // The attention-side pointers of every object's bank, handed to the
@@ -235,14 +247,18 @@ struct AttendPrepArgs {
 };
 
 // Launchers (all enqueue on `st` and return the launch status).
+// qp (optional, bf16 grids of 256 channels only): the launch also projects
+// every row (Rs3QProjArgs).
 hipError_t rs3_launch_energy(const void* X, int64_t x_stride, int n_x, int mn, int C, int dtype,
-                             double* e, unsigned long long* range, hipStream_t st);
+                             double* e, unsigned long long* range, hipStream_t st,
+                             const Rs3QProjArgs* qp = nullptr);
 hipError_t rs3_launch_select(const Rs3SelectArgs& a, int n_groups, hipStream_t st);
 // Grids for which the prior runs beside the energies (one wave per group).
 bool rs3_select_prior_beside(int m, int n, int s);
 // Energies and the one-wave priors (written to a.prior_bits) in one launch.
 hipError_t rs3_launch_energy_prior(const void* X, int64_t x_stride, int n_x, int mn, int C, int dtype, double* e,
-                                   unsigned long long* range, const Rs3SelectArgs& a, int n_groups, hipStream_t st);
+                                   unsigned long long* range, const Rs3SelectArgs& a, int n_groups, hipStream_t st,
+                                   const Rs3QProjArgs* qp = nullptr);
 hipError_t rs3_launch_commit(const Rs3CommitArgs& a, int dtype, int d_kv, int D, int H, int d_h,
                              hipStream_t st);
 // merge = false leaves the split merge of the bf16 path to the caller (the
@@ -255,6 +271,9 @@ hipError_t rs3_fused_setup();
 // Split-KV attention only; project: the queries are projected from X[sel]
 // inside the kernel (heads of width <= 64), else read from a.Q.
 hipError_t rs3_launch_attn(const Rs3ReadoutArgs& a, const Rs3AttnBanks& ab, hipStream_t st, bool project);
+// Whether the attention of this launch projects its queries inside (then a
+// frame may hand it the energy launch's projection of every cell instead).
+bool rs3_attn_projects(const Rs3ReadoutArgs& a);
 hipError_t rs3_launch_attend_prep(const AttendPrepArgs& p, hipStream_t st);
 hipError_t rs3_launch_attend_merge(const Rs3ReadoutArgs& a, int SA, float* O, hipStream_t st);
 hipError_t rs3_launch_attend_f32(const float* Q, const float* K, const float* V, int n_q, int64_t n_kv, int H,

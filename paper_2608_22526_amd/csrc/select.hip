@@ -56,10 +56,15 @@ __device__ __forceinline__ double energy_chunk<float>(u32x4 w, double acc) {
 // C*sizeof(T) is a multiple of 16.
 constexpr int EB_CH = 32;
 // Rows 64*bx .. of grid xi by one 256-thread block (nbx blocks per grid).
-template <typename T>
+// QP (bf16 rows of 256 channels, so the block holds whole rows): waves 1 and
+// 2 also project rows 0-31 and 32-63 of the block by W_q on MFMA while wave
+// 0 continues the energy chains, and store them, scaled, to qp.Qall.  They
+// load their W_q operands after the block's barrier, so the chains start as
+// early as without the projection.
+template <typename T, bool QP = false>
 __device__ __forceinline__ void energy_block(const T* __restrict__ X, int64_t x_stride, int mn, int C,
                                              double* __restrict__ e, unsigned long long* __restrict__ range,
-                                             int bx, int xi, int nbx) {
+                                             int bx, int xi, int nbx, const Rs3QProjArgs* qp = nullptr) {
   __shared__ u32x4 rows[64 * (EB_CH + 1)];
   const int r0 = bx * 64, tid = threadIdx.x;
   const int nrows = min(64, mn - r0);
@@ -90,6 +95,41 @@ __device__ __forceinline__ void energy_block(const T* __restrict__ X, int64_t x_
       const u32x4* rw = rows + tid * (EB_CH + 1);
 #pragma unroll 4
       for (int c = 0; c < nch; ++c) acc = energy_chunk<T>(rw[c], acc);
+    } else if constexpr (QP) {
+      if (tid < 192) {
+        // wave 1 + w: rows 32w .. 32w+31; A = W_q^T rows (d), B = X rows; lane
+        // l ends with row 32w + l%32 at d = 32 db + 8 (r/4) + 4 (l/32) + r%4
+        const int w = (tid >> 6) - 1, lane = tid & 63, g = lane >> 5;
+        const u32x4* xb = rows + (32 * w + (lane & 31)) * (EB_CH + 1) + g;
+        // A operands: W_q^T rows 32 db + lane%32, chunk 2 ks + lane/32
+        const u32x4* wg = (const u32x4*)qp->WqT + (lane & 31) * EB_CH + g;
+        u32x4 wa[2][EB_CH / 2];
+#pragma unroll
+        for (int db = 0; db < 2; ++db)
+#pragma unroll
+          for (int ks = 0; ks < EB_CH / 2; ++ks) wa[db][ks] = wg[db * 32 * EB_CH + 2 * ks];
+        f32x16 qa[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+        for (int ks = 0; ks < EB_CH / 2; ++ks) {
+          const u32x4 bx = xb[2 * ks];
+#pragma unroll
+          for (int db = 0; db < 2; ++db) qa[db] = mfma32(wa[db][ks], bx, qa[db]);
+        }
+        const int row = 32 * w + (lane & 31);
+        if (row < nrows) {
+          bf16_t* qrow = qp->Qall + ((int64_t)xi * mn + r0 + row) * 64;
+          const float qs = qp->qscale;
+#pragma unroll
+          for (int db = 0; db < 2; ++db)
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+              u32x2 pk;
+              pk[0] = pack_bf16x2(qa[db][4 * q4] * qs, qa[db][4 * q4 + 1] * qs);
+              pk[1] = pack_bf16x2(qa[db][4 * q4 + 2] * qs, qa[db][4 * q4 + 3] * qs);
+              *(u32x2*)(qrow + 32 * db + 8 * q4 + 4 * g) = pk;
+            }
+        }
+      }
     }
     __syncthreads();
   }
@@ -112,11 +152,11 @@ __device__ __forceinline__ void energy_block(const T* __restrict__ X, int64_t x_
   }
 }
 
-template <typename T>
+template <typename T, bool QP = false>
 __global__ __launch_bounds__(256) void k_energy(const T* __restrict__ X, int64_t x_stride, int mn,
                                                  int C, double* __restrict__ e,
-                                                 unsigned long long* __restrict__ range) {
-  energy_block<T>(X, x_stride, mn, C, e, range, blockIdx.x, blockIdx.y, gridDim.x);
+                                                 unsigned long long* __restrict__ range, Rs3QProjArgs qp) {
+  energy_block<T, QP>(X, x_stride, mn, C, e, range, blockIdx.x, blockIdx.y, gridDim.x, &qp);
 }
 
 
@@ -1043,13 +1083,13 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(Rs3SelectArgs a) {
 // the masks and the tracker state, the energies only on X, so the prior
 // blocks (after the energy blocks) run beside them and leave the group's
 // prior rows [m][W] in prior_bits for the selection.
-template <typename T>
+template <typename T, bool QP = false>
 __global__ __launch_bounds__(256) void k_energy_prior(const T* __restrict__ X, int64_t x_stride, int mn, int C,
                                                       double* __restrict__ e, unsigned long long* __restrict__ range,
-                                                      Rs3SelectArgs a, int nbx, int n_e) {
+                                                      Rs3SelectArgs a, int nbx, int n_e, Rs3QProjArgs qp) {
   const int b = blockIdx.x;
   if (b < n_e) {
-    energy_block<T>(X, x_stride, mn, C, e, range, b % nbx, b / nbx, nbx);
+    energy_block<T, QP>(X, x_stride, mn, C, e, range, b % nbx, b / nbx, nbx, &qp);
     return;
   }
   const int g = b - n_e, tid = threadIdx.x;
@@ -1072,30 +1112,47 @@ __global__ __launch_bounds__(256) void k_energy_prior(const T* __restrict__ X, i
 
 using namespace rs3;
 
+// The projection in the energy launch needs whole 256-channel bf16 rows in
+// one column block.
+static bool qproj_ok(int C, int dtype, const Rs3QProjArgs* qp) {
+  return qp && dtype == RS3_BF16 && C == 8 * EB_CH;
+}
+
 hipError_t rs3_launch_energy(const void* X, int64_t x_stride, int n_x, int mn, int C, int dtype,
-                             double* e, unsigned long long* range, hipStream_t st) {
+                             double* e, unsigned long long* range, hipStream_t st, const Rs3QProjArgs* qp) {
   dim3 grid((mn + 63) / 64, n_x);
-  if (dtype == RS3_BF16)
+  if (qp && !qproj_ok(C, dtype, qp)) return hipErrorInvalidValue;
+  const Rs3QProjArgs q = qp ? *qp : Rs3QProjArgs{};
+  if (qp)
+    RS3_LAUNCH(RS3_K_ENERGY, st, (k_energy<bf16_t, true>), grid, dim3(256), 0, st, (const bf16_t*)X, x_stride, mn, C,
+               e, range, q);
+  else if (dtype == RS3_BF16)
     RS3_LAUNCH(RS3_K_ENERGY, st, k_energy<bf16_t>, grid, dim3(256), 0, st, (const bf16_t*)X, x_stride, mn, C, e,
-               range);
+               range, q);
   else
     RS3_LAUNCH(RS3_K_ENERGY, st, k_energy<float>, grid, dim3(256), 0, st, (const float*)X, x_stride, mn, C, e,
-               range);
+               range, q);
   return hipGetLastError();
 }
 
 bool rs3_select_prior_beside(int m, int n, int s) { return m <= 64 && s == 1 && n <= 64 * FAST_W; }
 
 hipError_t rs3_launch_energy_prior(const void* X, int64_t x_stride, int n_x, int mn, int C, int dtype, double* e,
-                                   unsigned long long* range, const Rs3SelectArgs& a, int n_groups, hipStream_t st) {
+                                   unsigned long long* range, const Rs3SelectArgs& a, int n_groups, hipStream_t st,
+                                   const Rs3QProjArgs* qp) {
   const int nbx = (mn + 63) / 64, n_e = nbx * n_x;
   const dim3 grid(n_e + n_groups);
-  if (dtype == RS3_BF16)
+  if (qp && !qproj_ok(C, dtype, qp)) return hipErrorInvalidValue;
+  const Rs3QProjArgs q = qp ? *qp : Rs3QProjArgs{};
+  if (qp)
+    RS3_LAUNCH(RS3_K_ENERGY, st, (k_energy_prior<bf16_t, true>), grid, dim3(256), 0, st, (const bf16_t*)X, x_stride,
+               mn, C, e, range, a, nbx, n_e, q);
+  else if (dtype == RS3_BF16)
     RS3_LAUNCH(RS3_K_ENERGY, st, k_energy_prior<bf16_t>, grid, dim3(256), 0, st, (const bf16_t*)X, x_stride, mn, C, e,
-               range, a, nbx, n_e);
+               range, a, nbx, n_e, q);
   else
     RS3_LAUNCH(RS3_K_ENERGY, st, k_energy_prior<float>, grid, dim3(256), 0, st, (const float*)X, x_stride, mn, C, e,
-               range, a, nbx, n_e);
+               range, a, nbx, n_e, q);
   return hipGetLastError();
 }
 

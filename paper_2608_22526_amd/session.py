@@ -66,10 +66,15 @@ class Session:
         self.ws_sel = torch.zeros(max(ws, 8), dtype=torch.uint8, device=device)
         wr = B.readout_workspace_size(self.layer, n_obj, self.max_sel, n_splits)
         self.ws_read = torch.zeros(max(wr, 256), dtype=torch.uint8, device=device)
+        wf = B.frame_workspace_size(self.layer, self.grid, n_obj, self.x_stride, self.max_sel, n_splits)
+        self.ws_frame = torch.zeros(max(wf, 256), dtype=torch.uint8, device=device)
         # argument objects reused by every call
         L = B.lib()
         self._f_select, self._f_readout = L.rs3_select_queries, L.rs3_readout
         self._f_commit, self._f_readout_commit = L.rs3_commit, L.rs3_readout_commit
+        self._f_frame = L.rs3_frame
+        self._io = B.FrameIO()
+        self._io_ref = ctypes.byref(self._io)
         self._grid_ref = ctypes.byref(self.grid)
         self._params_ref = ctypes.byref(self.params)
         self._harr_src = None
@@ -77,6 +82,12 @@ class Session:
         self._k_addr = ctypes.addressof(self._k)
         self._ws_sel = (self.ws_sel.data_ptr(), self.ws_sel.numel())
         self._ws_read = (self.ws_read.data_ptr(), self.ws_read.numel())
+        self._ws_frame = (self.ws_frame.data_ptr(), self.ws_frame.numel())
+        io = self._io
+        io.x_obj_stride, io.k, io.params = self.x_stride, self._k_addr, self.params
+        io.sel_idx, io.sel_count = self.sel_idx.data_ptr(), self.sel_count.data_ptr()
+        io.n_splits, io.y_obj_stride = n_splits, self.mn * C if n_obj > 1 else 0
+        io.kv_obj_stride, io.kept_count = self.mn * d_kv, self.kept_count.data_ptr()
         self._p_sel_idx, self._p_sel_count = self.sel_idx.data_ptr(), self.sel_count.data_ptr()
         self._p_kept = self.kept_count.data_ptr()
         self._sel_stride = 0 if union_objects else self.mn
@@ -135,6 +146,29 @@ class Session:
             self._ws_read[0], self._ws_read[1], Kmem.data_ptr(), Vmem.data_ptr(), self.mn * self.d_kv,
             masks.data_ptr(), t, int(pin), fall_min, fmax, self._p_kept, self._stream(stream)),
             "rs3_readout_commit")
+
+    def frame(self, read_masks, X, k: Sequence[int], Y, Kmem, Vmem, commit_masks, t: int, pin: bool = False,
+              max_sel: Optional[int] = None, y_fp32: int = 0, seed_box: bool = False, prior_out=None,
+              fall_min: int = 0, fall_max: Optional[int] = None, stream=None):
+        """select(read_masks, X, k), then readout_commit(X, Y, Kmem, Vmem,
+        commit_masks, t, pin), as one rs3_frame call."""
+        if len(k) != self.n_groups:
+            raise ValueError("frame: %d keep budgets for %d groups" % (len(k), self.n_groups))
+        kk = self._k
+        for i, v in enumerate(k):
+            kk[i] = v
+        io = self._io
+        io.params.seed_box = 1 if seed_box else 0
+        io.read_masks, io.X, io.Y = read_masks.data_ptr(), X.data_ptr(), Y.data_ptr()
+        io.prior_out = None if prior_out is None else prior_out.data_ptr()
+        io.max_sel = self.max_sel if max_sel is None else max_sel
+        io.y_fp32 = y_fp32
+        io.Kmem, io.Vmem, io.commit_masks = Kmem.data_ptr(), Vmem.data_ptr(), commit_masks.data_ptr()
+        io.t, io.pin, io.fall_min = t, int(pin), fall_min
+        io.fall_max = self.mn if fall_max is None else fall_max
+        self._check(self._f_frame(self.layer.h, self._grid_ref, self.n_obj, self.track.h, self._handles(),
+                                  self._io_ref, self._ws_frame[0], self._ws_frame[1], self._stream(stream)),
+                    "rs3_frame")
 
     def commit(self, Kmem, Vmem, masks, t: int, pin: bool, fall_min: int = 0, fall_max: Optional[int] = None,
                stream=None):

@@ -73,3 +73,24 @@ def test_host_validation_before_device(lib):
     assert lib.rs3_layer_create(256, 1, 32, p.RS3_BF16, 1, w, w, w, w, ctypes.byref(out)) == p.RS3_E_INVALID
     assert lib.rs3_layer_create(256, 1, 64, p.RS3_BF16, 2, w, w, w, w, ctypes.byref(out)) == p.RS3_E_INVALID
     assert lib.rs3_profile_enable(1, 0) == p.RS3_E_INVALID
+
+
+def test_frame_io_layout_matches_header(tmp_path):
+    """The binding's rs3_frame_io mirror has the header's size and field
+    offsets (compiled here with the host C compiler)."""
+    import shutil
+    import subprocess
+    from paper_2608_22526_amd._binding import FrameIO
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no host C compiler")
+    names = [n for n, _ in FrameIO._fields_]
+    src = tmp_path / "layout.c"
+    src.write_text("#include <stdio.h>\n#include <stddef.h>\n#include \"rs3.h\"\nint main(void) {\n"
+                   "  printf(\"%zu\", sizeof(rs3_frame_io));\n"
+                   + "".join("  printf(\" %%zu\", offsetof(rs3_frame_io, %s));\n" % n for n in names)
+                   + "  return 0;\n}\n")
+    exe = tmp_path / "layout"
+    subprocess.check_call([cc, "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)])
+    got = [int(v) for v in subprocess.check_output([str(exe)]).split()]
+    assert got == [ctypes.sizeof(FrameIO)] + [getattr(FrameIO, n).offset for n in names]

@@ -181,6 +181,31 @@ def test_four_heads_of_64_projecting(n_splits):
     _log("4x64 splits=%d stats %s" % (n_splits, r.stats))
 
 
+@pytest.mark.parametrize("form", ["absorbed", "projected", "4x64", "8x32"])
+def test_growing_logits_rescale(form):
+    """Keys of later frames scaled by 1, 2, 2, 4, 4, 8 (powers of two: exact
+    in bf16, both sides get the same values), so tiles of later frames give
+    logits far above those of earlier ones and the online softmax moves its
+    reference maximum in the middle of a split (the lazy rescale with a
+    nonzero weight for what was accumulated); values scaled by 1/8 keep the
+    update small against the bf16 rounding of the projected queries at these
+    logits.  fp32 outputs, every selected row within 2e-2 (Eq. 6)."""
+    base = CONFIGS["sam2_single"]
+    cfg, kw = {"absorbed": (base, dict(absorb=True)), "projected": (base, dict(absorb=False)),
+               "4x64": (replace(base, H=4, d_h=64), {}),
+               "8x32": (replace(base, H=8, d_h=32, m=32, n=32), {})}[form]
+    r = Runner(cfg, cfg.f_max + 2, max_sel=k_from_rho("0.3", cfg.mn), **kw)
+    kscale = [1, 1, 2, 2, 4, 4, 8]
+    for t in range(cfg.f_max):
+        fr = make_frame(cfg, t)
+        K = to_storage(storage_to_f64(fr.Kmem, cfg.dtype).astype(np.float32) * np.float32(kscale[t]), cfg.dtype)
+        V = to_storage(storage_to_f64(fr.Vmem, cfg.dtype).astype(np.float32) * np.float32(0.125), cfg.dtype)
+        r.sess.commit(_dev(K), _dev(V), _dev(r.seq.masks[t]), t, t == 0)
+        r.orc.commit(K, V, r.seq.masks[t], t, t == 0)
+    r.select_readout(cfg.f_max, dense_oracle=True, y_fp32=1, tol=2e-2)
+    _log("growing logits %s stats %s" % (form, r.stats))
+
+
 # ---------------------------------------------------------------------------
 # frame tables of 64 and 256 frames on a small grid
 # ---------------------------------------------------------------------------
