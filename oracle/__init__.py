@@ -16,8 +16,10 @@ Modules:
   bank      write compaction and the ring memory bank (Sec. 3.2, Eq. 8)
   write     the paper's fixed write keep-set K_w (Sec. 3.2, Eq. 8)
   post      closure of the decoded masks and the palette argmax (Sec. 3.3)
+  stack     the L-layer memory-attention stack on the kept queries (Sec. 3.1,
+            "Sparse memory attention"; the layer is a reading, see its doc)
 
-Parity unpinned: absolute readout values at the workload sizes (the paper
+Parity unpinned: absolute readout and stack values at the workload sizes (the paper
 prints no tensors and its weights are not available); every other function is
 pinned by the tests in tests/test_oracle_*.py.  The axial rotary table is a
 reading (the paper gives only its shape); its stated form is pinned, its

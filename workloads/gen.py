@@ -22,7 +22,7 @@ from typing import List, Optional
 import numpy as np
 
 # stream ids for default_rng([seed, frame, stream])
-_S_X, _S_K, _S_V, _S_MASK, _S_RHO, _S_W, _S_ROPE = 1, 2, 3, 4, 5, 6, 7
+_S_X, _S_K, _S_V, _S_MASK, _S_RHO, _S_W, _S_ROPE, _S_STACK = 1, 2, 3, 4, 5, 6, 7, 8
 
 
 # ----------------------------------------------------------------------------
@@ -200,6 +200,39 @@ def make_weights(cfg: Config, logit_scale: float = 1.0) -> Weights:
     wo = rng.standard_normal((D, cfg.C), dtype=np.float32) / np.float32(math.sqrt(D))
     wq = wq * np.float32(logit_scale)
     return Weights(*(to_storage(w, cfg.dtype) for w in (wq, wk, wv, wo)))
+
+
+STACK_MATRICES = ("Wqs", "Wks", "Wvs", "Wos", "Wq", "Wk", "Wv", "Wo", "W1", "W2")
+STACK_NORMS = ("ln1_g", "ln1_b", "ln2_g", "ln2_b", "ln3_g", "ln3_b")
+
+
+def make_stack_weights(C: int, d_kv: int, F: int, n_layers: int, dtype: str = "bf16", seed: int = 0,
+                       branch_scale: float = 0.5) -> List[dict]:
+    """Synthetic weights of an L-layer memory-attention stack (no trained
+    weights exist for it).  Per layer: Gaussian matrices N(0, 1/fan_in)
+    W_qs, W_ks, W_vs, W_os [C][C], W_q [C][C], W_k, W_v [d_kv][C],
+    W_o [C][C], W_1 [C][F], W_2 [F][C] in the storage dtype, the three
+    output maps of the residual branches (W_os, W_o, W_2) times
+    `branch_scale` so that each layer changes the stream by a fraction of
+    its size; norm gains 1 + 0.1 N(0, 1) and shifts 0.1 N(0, 1) in float32.
+    Layer l draws from default_rng([seed, l, stream])."""
+    shapes = {"Wqs": (C, C), "Wks": (C, C), "Wvs": (C, C), "Wos": (C, C), "Wq": (C, C), "Wk": (d_kv, C),
+              "Wv": (d_kv, C), "Wo": (C, C), "W1": (C, F), "W2": (F, C)}
+    out = []
+    for layer in range(n_layers):
+        rng = np.random.default_rng([seed, layer, _S_STACK])
+        w = {}
+        for name in STACK_MATRICES:
+            r, c = shapes[name]
+            a = rng.standard_normal((r, c), dtype=np.float32) / np.float32(math.sqrt(r))
+            if name in ("Wos", "Wo", "W2"):
+                a = a * np.float32(branch_scale)
+            w[name] = to_storage(a, dtype)
+        for name in STACK_NORMS:
+            v = rng.standard_normal(C, dtype=np.float32) * np.float32(0.1)
+            w[name] = (v + np.float32(1.0)) if name.endswith("_g") else v
+        out.append(w)
+    return out
 
 
 def make_rope_table(cfg: Config, seed: int = 0) -> np.ndarray:
