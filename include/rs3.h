@@ -403,6 +403,71 @@ rs3_status rs3_attend(const void* Qh, const void* Kh, const void* Vh, int32_t n_
                       int32_t H, int32_t d_h, rs3_dtype dt, int32_t n_splits, float* O, void* ws,
                       size_t ws_bytes, void* stream);
 
+/* ---- the L-layer memory-attention stack on the kept queries -----------------
+ * Sec. 3.1 ("Sparse memory attention"): the memory attention of the VOS model
+ * is a stack of L self-/cross-attention layers, patched at every layer's
+ * entry so that each layer runs on the kept queries only.  The paper gives no
+ * layer, so the layer is this pre-norm residual one, in the shape of
+ * SAM2-class memory attention (z the fp32 residual stream of a kept row):
+ *   z += SA(LN1(z))    self-attention among the kept rows: H_s heads of
+ *                      width C/H_s, q, k, v = a W_qs, a W_ks, a W_vs, logits
+ *                      scaled by 1/sqrt(C/H_s), output o W_os
+ *   z += CA(LN2(z))    the readout of Eq. 6 against the bank: one head,
+ *                      q = b W_q, bank keys/values K W_k, V W_v, logits scaled
+ *                      by 1/sqrt(C), output o W_o
+ *   z += relu(LN3(z) W_1) W_2
+ * LN(z) = (z - mean) / sqrt(biased variance + 1e-5) * gain + shift, per row;
+ * no biases, no norm after the last layer.  The kept rows are gathered from
+ * X once before the first layer and scattered to Y once after the last; every
+ * other cell of Y is X's, bit for bit (a dropped row gets a zero update at
+ * every layer, so one gather and one scatter equal one per layer).
+ *
+ * rs3_stack_create: n_layers in [1, 16]; C = 256; H_s in {1, 2, 4, 8};
+ * d_kv = 64; F a multiple of 256 up to 8192; dt = RS3_BF16.  layers: host
+ * array of n_layers weight sets; matrices row-major bf16 (input dimension
+ * first): W_qs, W_ks, W_vs, W_os, W_q, W_o [C][C], W_k, W_v [d_kv][C],
+ * W_1 [C][F], W_2 [F][C]; gains and shifts fp32 [C].  Everything is copied
+ * to the device at create time (the caller keeps ownership of its arrays);
+ * the cross-attention's products W_q W_k^T and W_v W_o are formed there in
+ * fp64 and rounded to bf16 once.  Allocates device memory; synchronous.
+ *
+ * rs3_stack_readout: one object.  X: device bf16 grid [m*n][C]; bank: a bank
+ * of a bf16 layer created with absorb = 1, C = 256, d_kv = 64 and no rotary
+ * table (its raw rows serve every layer); sel_idx / sel_count / max_sel as in
+ * rs3_readout (one list; entries out of range or not ascending, or a count
+ * outside [0, max_sel], set the bank's error word, and the rows of such a
+ * call are unspecified); n_splits: key splits of the cross-attention, 0 =
+ * automatic; Y: device [m*n][C], bf16 or (y_fp32 = 1) fp32, may equal X when
+ * bf16.  ws: device workspace of at least rs3_stack_workspace_size(max_sel,
+ * n_splits) bytes, 16-byte aligned like X and Y.  Asynchronous on `stream`, allocates
+ * nothing; the bank is read only. */
+typedef struct rs3_stack rs3_stack;
+typedef struct {
+  const float* ln1_g;
+  const float* ln1_b;
+  const void* Wqs;
+  const void* Wks;
+  const void* Wvs;
+  const void* Wos;
+  const float* ln2_g;
+  const float* ln2_b;
+  const void* Wq;
+  const void* Wk;
+  const void* Wv;
+  const void* Wo;
+  const float* ln3_g;
+  const float* ln3_b;
+  const void* W1;
+  const void* W2;
+} rs3_stack_weights;
+rs3_status rs3_stack_create(int32_t n_layers, int32_t C, int32_t H_s, int32_t d_kv, int32_t F, rs3_dtype dt,
+                            const rs3_stack_weights* layers /*[host]*/, rs3_stack** out);
+void rs3_stack_destroy(rs3_stack* S);
+rs3_status rs3_stack_workspace_size(const rs3_stack* S, int32_t max_sel, int32_t n_splits, size_t* bytes);
+rs3_status rs3_stack_readout(const rs3_stack* S, const rs3_grid* g, const void* X, rs3_bank* bank,
+                             const int32_t* sel_idx, const int32_t* sel_count, int32_t max_sel, int32_t n_splits,
+                             void* Y, int32_t y_fp32, void* ws, size_t ws_bytes, void* stream);
+
 /* ---- per-kernel timing (diagnostics) ---------------------------------------
  * rs3_profile_enable(1, max_launches) creates a pool of HIP events; while
  * enabled, each kernel launched by the library is bracketed by two events on
@@ -422,7 +487,8 @@ enum {
   RS3_K_COMBINE = 7,       /* split merge + W_o + residual + scatter */
   RS3_K_READOUT_F32 = 8,   /* fp32 readout */
   RS3_K_MERGE_COMMIT = 9,  /* split merge and commit in one launch (rs3_readout_commit) */
-  RS3_K_COUNT = 10
+  RS3_K_STACK_GEMM = 10,   /* matrix products of the memory-attention stack (with their norms and merges) */
+  RS3_K_COUNT = 11
 };
 rs3_status rs3_profile_enable(int32_t on, int32_t max_launches);
 rs3_status rs3_profile_report(double* total_ms, int64_t* launches, int64_t* dropped);

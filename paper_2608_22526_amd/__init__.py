@@ -8,7 +8,7 @@ from ._binding import (  # noqa: F401
     RS3_OK, RS3_E_INVALID, RS3_E_CAPACITY, RS3_E_DEVICE, RS3_E_OOM,
     RS3_F32, RS3_BF16, RS3_MAX_OBJ, RS3_MAX_MN, RS3_TRACK_WORDS, RS3_BANK_HDR_WORDS, RS3_NOALLOC_SCRATCH_BYTES,
     Rs3Error, lib, lib_path, exported_symbols, Grid, SelectParams, FrameIO,
-    Track, Layer, Bank,
+    Track, Layer, Bank, Stack, StackWeights,
     select_workspace_size, select_queries,
     readout_workspace_size, readout, readout_noalloc, commit, frame_workspace_size, frame, readout_commit, write_keepset, close_workspace_size, close_masks,
     attend_workspace_size, attend,

@@ -42,6 +42,12 @@ class FrameIO(ctypes.Structure):
                 ("fall_min", c_i32), ("fall_max", c_i32), ("kept_count", c_vp)]
 
 
+class StackWeights(ctypes.Structure):
+    """rs3_stack_weights: one layer's host arrays (see rs3.h)."""
+    _fields_ = [(n, c_vp) for n in ("ln1_g", "ln1_b", "Wqs", "Wks", "Wvs", "Wos", "ln2_g", "ln2_b", "Wq", "Wk",
+                                    "Wv", "Wo", "ln3_g", "ln3_b", "W1", "W2")]
+
+
 class Rs3Error(RuntimeError):
     def __init__(self, status: int, what: str):
         self.status = status
@@ -84,13 +90,19 @@ _SIGS = {
     "rs3_write_keepset": (c_i32, [ctypes.POINTER(Grid), c_i32, c_vp, c_i32, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp]),
     "rs3_close_workspace_size": (c_i32, [c_i32, c_i32, c_i32, ctypes.POINTER(c_sz)]),
     "rs3_close_masks": (c_i32, [c_i32, c_i32, c_i32, c_vp, c_i32, c_i32, c_vp, c_vp, c_vp, c_sz, c_vp]),
+    "rs3_stack_create": (c_i32, [c_i32, c_i32, c_i32, c_i32, c_i32, c_i32, ctypes.POINTER(StackWeights),
+                                 ctypes.POINTER(c_vp)]),
+    "rs3_stack_destroy": (None, [c_vp]),
+    "rs3_stack_workspace_size": (c_i32, [c_vp, c_i32, c_i32, ctypes.POINTER(c_sz)]),
+    "rs3_stack_readout": (c_i32, [c_vp, ctypes.POINTER(Grid), c_vp, c_vp, c_vp, c_vp, c_i32, c_i32, c_vp, c_i32,
+                                  c_vp, c_sz, c_vp]),
     "rs3_profile_enable": (c_i32, [c_i32, c_i32]),
     "rs3_profile_report": (c_i32, [c_vp, c_vp, c_vp]),
     "rs3_profile_reset": (c_i32, []),
 }
 
 KERNEL_NAMES = ["energy", "select", "commit", "commit_append", "copy", "qproj", "attn", "combine",
-                "readout_f32", "merge_commit"]
+                "readout_f32", "merge_commit", "stack_gemm"]
 
 _lib = None
 
@@ -367,6 +379,43 @@ def attend(Q, K, V, n_q: int, n_kv: int, H: int, d_h: int, dtype: int, O, ws=Non
     ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check(lib().rs3_attend(_ptr(Q), _ptr(K), _ptr(V), n_q, n_kv, H, d_h, dtype, n_splits, _ptr(O), _ptr(ws),
                             ws_bytes, _stream(stream)), "rs3_attend")
+
+
+class Stack:
+    """rs3_stack: the L-layer memory-attention stack on the kept queries.
+    layers: one dict per layer with the keys of StackWeights (matrices uint16
+    bf16 bits, row-major input dimension first; norm gains/shifts float32)."""
+
+    def __init__(self, layers: Sequence[dict], C: int = 256, H_s: int = 1, d_kv: int = 64, F: int = 2048,
+                 dtype: int = RS3_BF16):
+        keep = []
+        arr = (StackWeights * len(layers))()
+        for i, w in enumerate(layers):
+            for name, _ in StackWeights._fields_:
+                a = np.ascontiguousarray(w[name], dtype=np.float32 if name.startswith("ln") else np.uint16)
+                keep.append(a)
+                setattr(arr[i], name, a.ctypes.data)
+        h = c_vp()
+        _check(lib().rs3_stack_create(len(layers), C, H_s, d_kv, F, dtype, arr, ctypes.byref(h)), "rs3_stack_create")
+        self.h, self.n_layers, self.C, self.H_s, self.d_kv, self.F = h, len(layers), C, H_s, d_kv, F
+
+    def workspace_size(self, max_sel: int, n_splits: int = 0) -> int:
+        out = c_sz()
+        _check(lib().rs3_stack_workspace_size(self.h, max_sel, n_splits, ctypes.byref(out)),
+               "rs3_stack_workspace_size")
+        return out.value
+
+    def readout(self, grid, X, bank: Bank, sel_idx, sel_count, max_sel: int, Y, y_fp32: int = 0, ws=None,
+                n_splits: int = 0, stream=None):
+        ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+        _check(lib().rs3_stack_readout(self.h, ctypes.byref(_grid(grid)), _ptr(X), bank.h, _ptr(sel_idx),
+                                       _ptr(sel_count), max_sel, n_splits, _ptr(Y), y_fp32, _ptr(ws), ws_bytes,
+                                       _stream(stream)), "rs3_stack_readout")
+
+    def __del__(self):
+        if getattr(self, "h", None) and _lib is not None:
+            _lib.rs3_stack_destroy(self.h)
+            self.h = None
 
 
 def profile_enable(on: bool, max_launches: int = 65536):

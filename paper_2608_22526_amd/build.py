@@ -14,7 +14,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OBJDIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "librs3.so")
-SOURCES = ["select.hip", "commit.hip", "readout.hip", "attend.hip", "rope.hip", "keepset.hip", "post.hip", "fused.hip", "api.hip", "profile.hip"]
+SOURCES = ["select.hip", "commit.hip", "readout.hip", "attend.hip", "rope.hip", "keepset.hip", "post.hip", "fused.hip", "stack.hip", "api.hip", "profile.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # The attention kernel keeps its MFMA accumulators in arch VGPRs, so the

@@ -1198,3 +1198,317 @@ rs3_status rs3_frame(const rs3_layer* L, const rs3_grid* g, int32_t n_obj, rs3_t
 }
 
 }  // extern "C"
+
+// ---- the memory-attention stack ---------------------------------------------
+struct rs3_stack {
+  struct Layer {
+    const float* ln_g[3];
+    const float* ln_b[3];
+    const bf16_t* WqkvT;   // [3C][C]: W_qs | W_ks | W_vs, transposed
+    const bf16_t* WosT;    // [C][C]
+    const bf16_t* WqcT;    // [d_kv][C]: (W_q W_k^T)^T
+    const bf16_t* WvoT;    // [C][d_kv]: (W_v W_o)^T
+    const bf16_t* W1T;     // [F][C]
+    const bf16_t* W2T;     // [C][F]
+  };
+  int32_t n_layers, C, Hs, dhs, d_kv, F;
+  void* dmem;   // every layer's weights, one allocation
+  std::vector<Layer> layers;
+};
+
+namespace {
+
+// Key splits of the self-attention: a launch of about 256 work-groups
+// (8*n_qt*ceil(H_s*S/8)), at least two key tiles per split.
+int stack_self_splits(int M, int Hs) {
+  const int ntile = (M + KT - 1) / KT, n_qt = (M + 127) / 128;
+  int S = 256 / (n_qt * Hs);
+  const int most = (ntile + 1) / 2;
+  if (S > most) S = most;
+  if (S * Hs > RS3_MAX_SPLITS_X_HEADS) S = RS3_MAX_SPLITS_X_HEADS / Hs;
+  return S < 1 ? 1 : S;
+}
+
+struct StackLayout {
+  size_t z, qs, qc, kh, vh, tiles, desc, hdr, opart, ml, hbuf, total;
+  int S_s, ntile;
+};
+
+// Workspace of a call with M kept rows at most and S_c cross-attention splits.
+void stack_layout(const rs3_stack* S, int M, int S_c, StackLayout* L) {
+  const int C = S->C;
+  L->S_s = stack_self_splits(M, S->Hs);
+  L->ntile = (M + KT - 1) / KT;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += align256(bytes);
+    return at;
+  };
+  L->z = take((size_t)M * C * 4);
+  L->qs = take((size_t)M * C * 2);
+  L->qc = take((size_t)M * S->d_kv * 2);
+  L->kh = take((size_t)L->ntile * KT * C * 2);
+  L->vh = take((size_t)L->ntile * KT * C * 2);
+  L->tiles = take((size_t)L->ntile * sizeof(TileEnt));
+  L->desc = take(sizeof(BankDev));
+  L->hdr = take(HDR_WORDS * 4);
+  const size_t op_s = (size_t)L->S_s * M * C, op_c = (size_t)S_c * M * S->d_kv;
+  L->opart = take((op_s > op_c ? op_s : op_c) * 2);
+  const size_t ml_s = (size_t)L->S_s * M * S->Hs, ml_c = (size_t)S_c * M;
+  L->ml = take((ml_s > ml_c ? ml_s : ml_c) * 8);
+  L->hbuf = take((size_t)M * S->F * 2);
+  L->total = off;
+}
+
+}  // namespace
+
+extern "C" {
+
+rs3_status rs3_stack_create(int32_t n_layers, int32_t C, int32_t H_s, int32_t d_kv, int32_t F, rs3_dtype dt,
+                            const rs3_stack_weights* layers, rs3_stack** out) {
+  if (!out || !layers) return RS3_E_INVALID;
+  if (n_layers < 1 || n_layers > 16 || C != 256 || d_kv != 64 || dt != RS3_BF16) return RS3_E_INVALID;
+  if (H_s != 1 && H_s != 2 && H_s != 4 && H_s != 8) return RS3_E_INVALID;
+  if (F < 256 || F > 8192 || F % 256 != 0) return RS3_E_INVALID;
+  for (int l = 0; l < n_layers; ++l) {
+    const rs3_stack_weights& w = layers[l];
+    const void* ptrs[] = {w.ln1_g, w.ln1_b, w.Wqs, w.Wks, w.Wvs, w.Wos, w.ln2_g, w.ln2_b,
+                          w.Wq, w.Wk, w.Wv, w.Wo, w.ln3_g, w.ln3_b, w.W1, w.W2};
+    for (const void* q : ptrs)
+      if (!q) return RS3_E_INVALID;
+  }
+  *out = nullptr;
+  const size_t es = 2;
+  // per layer: QKV, W_os, W_qc, W_vo, W_1, W_2 (bf16), then six norm vectors
+  const size_t mats[6] = {(size_t)3 * C * C, (size_t)C * C, (size_t)d_kv * C, (size_t)C * d_kv, (size_t)F * C,
+                          (size_t)C * F};
+  size_t per = 0;
+  for (size_t m : mats) per += align256(m * es);
+  per += 6 * align256((size_t)C * 4);
+  std::vector<uint8_t> host(per * n_layers);
+  rs3_stack* S = new rs3_stack();
+  S->n_layers = n_layers;
+  S->C = C;
+  S->Hs = H_s;
+  S->dhs = C / H_s;
+  S->d_kv = d_kv;
+  S->F = F;
+  S->dmem = nullptr;
+  hipError_t e = hipMalloc(&S->dmem, host.size());
+  if (e != hipSuccess) {
+    delete S;
+    return map_err(e);
+  }
+  uint8_t* dbase = (uint8_t*)S->dmem;
+  for (int l = 0; l < n_layers; ++l) {
+    const rs3_stack_weights& w = layers[l];
+    size_t off = per * l;
+    auto put = [&](const std::vector<uint8_t>& src) {
+      memcpy(&host[off], src.data(), src.size());
+      const uint8_t* d = dbase + off;
+      off += align256(src.size());
+      return (const bf16_t*)d;
+    };
+    rs3_stack::Layer L;
+    std::vector<uint8_t> qkv((size_t)3 * C * C * es);
+    const void* in3[3] = {w.Wqs, w.Wks, w.Wvs};
+    for (int j = 0; j < 3; ++j) {
+      std::vector<uint8_t> t = transpose(in3[j], C, C, es);
+      memcpy(&qkv[(size_t)j * C * C * es], t.data(), t.size());
+    }
+    L.WqkvT = put(qkv);
+    L.WosT = put(transpose(w.Wos, C, C, es));
+    L.WqcT = put(product_T(w.Wq, w.Wk, C, C, d_kv, dt, true));
+    L.WvoT = put(product_T(w.Wv, w.Wo, d_kv, C, C, dt, false));
+    L.W1T = put(transpose(w.W1, C, F, es));
+    L.W2T = put(transpose(w.W2, F, C, es));
+    const float* nv[6] = {w.ln1_g, w.ln1_b, w.ln2_g, w.ln2_b, w.ln3_g, w.ln3_b};
+    for (int j = 0; j < 6; ++j) {
+      std::vector<uint8_t> v((size_t)C * 4);
+      memcpy(v.data(), nv[j], v.size());
+      const float* d = (const float*)put(v);
+      if (j % 2 == 0)
+        L.ln_g[j / 2] = d;
+      else
+        L.ln_b[j / 2] = d;
+    }
+    S->layers.push_back(L);
+  }
+  e = hipMemcpy(S->dmem, host.data(), host.size(), hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipFree(S->dmem);
+    delete S;
+    return map_err(e);
+  }
+  *out = S;
+  return RS3_OK;
+}
+
+void rs3_stack_destroy(rs3_stack* S) {
+  if (!S) return;
+  if (S->dmem) (void)hipFree(S->dmem);
+  delete S;
+}
+
+rs3_status rs3_stack_workspace_size(const rs3_stack* S, int32_t max_sel, int32_t n_splits, size_t* bytes) {
+  if (!S || !bytes || max_sel < 0 || max_sel > RS3_MAX_MN || n_splits < 0 || n_splits > RS3_MAX_SPLITS_X_HEADS)
+    return RS3_E_INVALID;
+  StackLayout L;
+  stack_layout(S, max_sel, n_splits > 0 ? n_splits : max_auto_splits(1), &L);
+  *bytes = L.total;
+  return RS3_OK;
+}
+
+rs3_status rs3_stack_readout(const rs3_stack* S, const rs3_grid* g, const void* X, rs3_bank* bank,
+                             const int32_t* sel_idx, const int32_t* sel_count, int32_t max_sel, int32_t n_splits,
+                             void* Y, int32_t y_fp32, void* ws, size_t ws_bytes, void* stream) {
+  if (!S || !grid_ok(g) || !X || !bank || !sel_idx || !sel_count || !Y) return RS3_E_INVALID;
+  const int mn = g->m * g->n;
+  if (max_sel < 0 || max_sel > mn || n_splits < 0 || n_splits > RS3_MAX_SPLITS_X_HEADS) return RS3_E_INVALID;
+  if (y_fp32 != 0 && y_fp32 != 1) return RS3_E_INVALID;
+  if (Y == X && y_fp32) return RS3_E_INVALID;
+  const LayerDev& bl = bank->L->dev;
+  if (!bl.absorb || bl.dtype != RS3_BF16 || bl.C != S->C || bl.d_kv != S->d_kv || bl.rope) return RS3_E_INVALID;
+  if (!aligned16(X) || !aligned16(Y) || !aligned16(ws)) return RS3_E_INVALID;
+  const int n_qt = (max_sel + 127) / 128;
+  const int S_c = n_splits > 0 ? n_splits
+                               : auto_splits(1, 1, n_qt > 0 ? n_qt : 1, (double)bank->host.cap * bl.dah * 4);
+  StackLayout L;
+  stack_layout(S, max_sel, S_c, &L);
+  if (max_sel > 0 && (!ws || ws_bytes < L.total)) return RS3_E_INVALID;
+  rs3_status st0 = ensure_setup();
+  if (st0 != RS3_OK) return st0;
+  const hipStream_t st = (hipStream_t)stream;
+  hipError_t e = hipSuccess;
+  if (Y != X) e = rs3_launch_stack_copy(X, Y, (int64_t)mn * S->C, y_fp32, st);
+  if (e != hipSuccess || max_sel == 0) return map_err(e);
+  uint8_t* w = (uint8_t*)ws;
+  const int C = S->C;
+  const double log2e = 1.4426950408889634;
+
+  StkGemmArgs p;
+  memset(&p, 0, sizeof(p));
+  p.Z = (const float*)(w + L.z);
+  p.Zw = (float*)(w + L.z);
+  p.X = X;
+  p.sel = sel_idx;
+  p.Opart = (const bf16_t*)(w + L.opart);
+  p.ML = (const float*)(w + L.ml);
+  p.count = sel_count;
+  p.err_hdr = bank->host.hdr;
+  p.M = max_sel;
+  p.mn = mn;
+  p.Y = Y;
+  p.y_f32 = y_fp32;
+  p.Qs = (bf16_t*)(w + L.qs);
+  p.Kh = (bf16_t*)(w + L.kh);
+  p.Vh = (bf16_t*)(w + L.vh);
+  p.tiles = (TileEnt*)(w + L.tiles);
+  p.desc = (BankDev*)(w + L.desc);
+  p.shdr = (int32_t*)(w + L.hdr);
+  p.Hs = S->Hs;
+  p.dhs = S->dhs;
+  p.ntile_cap = L.ntile;
+
+  // the two attentions: self (the kept rows as a one-frame bank) and cross
+  Rs3ReadoutArgs as, ac;
+  Rs3AttnBanks abs_, abc;
+  memset(&as, 0, sizeof(as));
+  memset(&abs_, 0, sizeof(abs_));
+  as.banks[0] = p.desc;
+  as.sel_count = sel_count;
+  as.Q = p.Qs;
+  as.Opart = w + L.opart;
+  as.ML = (float*)(w + L.ml);
+  as.mn = mn;
+  as.C = C;
+  as.H = S->Hs;
+  as.d_h = S->dhs;
+  as.D = C;
+  as.n_obj = 1;
+  as.max_sel = max_sel;
+  as.S = L.S_s;
+  as.n_qt = n_qt;
+  abs_.hdr[0] = p.shdr;
+  abs_.tiles[0] = p.tiles;
+  abs_.kh[0] = p.Kh;
+  abs_.vh[0] = p.Vh;
+  abs_.ntcap[0] = L.ntile;
+  ac = as;
+  ac.banks[0] = bank->d_desc;
+  ac.Q = w + L.qc;
+  ac.H = 1;
+  ac.d_h = bl.dah;
+  ac.D = bl.Da;
+  ac.S = S_c;
+  memset(&abc, 0, sizeof(abc));
+  abc.hdr[0] = bank->host.hdr;
+  abc.tiles[0] = bank->host.tiles;
+  abc.kh[0] = bank->host.Khat;
+  abc.vh[0] = bank->host.Vhat;
+  abc.ntcap[0] = bank->host.n_tiles_cap;
+
+  for (int l = 0; l < S->n_layers && e == hipSuccess; ++l) {
+    const rs3_stack::Layer& ly = S->layers[l];
+    const bool last = l == S->n_layers - 1;
+    // z += SA(LN1(z))
+    StkGemmArgs q = p;
+    q.ln_g = ly.ln_g[0];
+    q.ln_b = ly.ln_b[0];
+    q.WT = ly.WqkvT;
+    q.N = 3 * C;
+    q.K = C;
+    q.scale = (float)(log2e / sqrt((double)S->dhs));
+    q.write_bank = l == 0;
+    e = rs3_launch_stack_gemm(q, l == 0 ? STK_A_GLN : STK_A_LN, STK_E_QKV, st);
+    if (e == hipSuccess) e = rs3_launch_attn(as, abs_, st, false);
+    StkGemmArgs o = p;
+    o.WT = ly.WosT;
+    o.N = C;
+    o.K = C;
+    o.S = L.S_s;
+    o.H_att = S->Hs;
+    o.d_att = S->dhs;
+    if (e == hipSuccess) e = rs3_launch_stack_gemm(o, STK_A_MERGE, STK_E_RESID, st);
+    // z += CA(LN2(z)): one absorbed head of width C
+    StkGemmArgs c = p;
+    c.ln_g = ly.ln_g[1];
+    c.ln_b = ly.ln_b[1];
+    c.WT = ly.WqcT;
+    c.N = S->d_kv;
+    c.K = C;
+    c.out = w + L.qc;
+    c.scale = (float)(log2e / sqrt((double)C));
+    if (e == hipSuccess) e = rs3_launch_stack_gemm(c, STK_A_LN, STK_E_STORE, st);
+    if (e == hipSuccess) e = rs3_launch_attn(ac, abc, st, false);
+    StkGemmArgs v = p;
+    v.WT = ly.WvoT;
+    v.N = C;
+    v.K = S->d_kv;
+    v.S = S_c;
+    v.H_att = 1;
+    v.d_att = S->d_kv;
+    if (e == hipSuccess) e = rs3_launch_stack_gemm(v, STK_A_MERGE, STK_E_RESID, st);
+    // z += relu(LN3(z) W_1) W_2; after the last layer the rows go to Y
+    StkGemmArgs m1 = p;
+    m1.ln_g = ly.ln_g[2];
+    m1.ln_b = ly.ln_b[2];
+    m1.WT = ly.W1T;
+    m1.N = S->F;
+    m1.K = C;
+    m1.out = w + L.hbuf;
+    m1.scale = 1.f;
+    m1.relu = 1;
+    if (e == hipSuccess) e = rs3_launch_stack_gemm(m1, STK_A_LN, STK_E_STORE, st);
+    StkGemmArgs m2 = p;
+    m2.A = w + L.hbuf;
+    m2.WT = ly.W2T;
+    m2.N = C;
+    m2.K = S->F;
+    if (e == hipSuccess) e = rs3_launch_stack_gemm(m2, STK_A_BF16, last ? STK_E_SCATTER : STK_E_RESID, st);
+  }
+  return map_err(e);
+}
+
+}  // extern "C"

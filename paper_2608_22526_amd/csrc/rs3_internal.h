@@ -246,6 +246,53 @@ struct AttendPrepArgs {
   int n_q, H, d_h, ntile;
 };
 
+// One matrix product of the memory-attention stack (k_stk_gemm): out = A W
+// over the kept rows, A [M][K] from one of the prologues, W given
+// transposed as WT [N][K].
+enum StkAMode { STK_A_BF16 = 0, STK_A_LN = 1, STK_A_GLN = 2, STK_A_MERGE = 3 };
+//  BF16 : A rows of a bf16 buffer [M][K]
+//  LN   : LayerNorm (gain ln_g, shift ln_b) of the fp32 stream rows Z [M][256]
+//  GLN  : the same of the kept cells X[sel[r]] of the bf16 grid, which also
+//         become the stream rows (Zw)
+//  MERGE: the key splits of the attention (Opart, ML: S splits, H_att heads of
+//         width d_att = K / H_att) merged into the normalised output rows
+enum StkEMode { STK_E_STORE = 0, STK_E_RESID = 1, STK_E_SCATTER = 2, STK_E_QKV = 3 };
+//  STORE  : out [M][N] bf16 = scale * (A W), with relu if set
+//  RESID  : Zw [M][256] += A W
+//  SCATTER: Y[sel[r]] = Z[r] + (A W)[r] (bf16 or fp32 Y [mn][256])
+//  QKV    : N = 768; columns [0,256) -> Qs [M][256] (times scale), [256,512)
+//           -> the self-attention's K^ tiles, [512,768) -> its V^ tiles; with
+//           write_bank, work-group (0,0) also writes that bank's descriptor,
+//           header and tile list from the device count
+struct StkGemmArgs {
+  const void* A;
+  const float* Z;
+  float* Zw;
+  const float* ln_g;
+  const float* ln_b;
+  const void* X;
+  const int32_t* sel;
+  const rs3::bf16_t* Opart;   // [S][M][K]
+  const float* ML;            // [S][M][H_att][2]
+  int S, H_att, d_att;
+  const int32_t* count;       // kept rows (device), clamped into [0, M]
+  int32_t* err_hdr;           // header of the bank whose error word takes the reports
+  const rs3::bf16_t* WT;      // [N][K]
+  int M, N, K, mn;
+  float scale;
+  int relu;
+  void* out;
+  void* Y;
+  int y_f32;
+  rs3::bf16_t* Qs;
+  rs3::bf16_t* Kh;            // [ntile_cap][Hs][64][dhs]
+  rs3::bf16_t* Vh;            // [ntile_cap][Hs][dhs][64] (slot order)
+  rs3::TileEnt* tiles;        // [ntile_cap]
+  rs3::BankDev* desc;
+  int32_t* shdr;              // [HDR_WORDS]
+  int Hs, dhs, ntile_cap, write_bank;
+};
+
 // Launchers (all enqueue on `st` and return the launch status).
 // qp (optional, bf16 grids of 256 channels only): the launch also projects
 // every row (Rs3QProjArgs).
@@ -302,5 +349,9 @@ void rs3_prof_end(int id, hipStream_t st);
     hipLaunchKernelGGL(__VA_ARGS__); \
     rs3_prof_end((ID), (ST));    \
   } while (0)
+// Stack products (k_stk_gemm with prologue am and epilogue em) and the
+// X -> Y copy of the grid (bf16 -> bf16 or fp32) before the scatter.
+hipError_t rs3_launch_stack_gemm(const StkGemmArgs& p, int am, int em, hipStream_t st);
+hipError_t rs3_launch_stack_copy(const void* X, void* Y, int64_t elems, int y_f32, hipStream_t st);
 hipError_t rs3_select_setup();
 hipError_t rs3_commit_setup();

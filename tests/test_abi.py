@@ -94,3 +94,50 @@ def test_frame_io_layout_matches_header(tmp_path):
     subprocess.check_call([cc, "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)])
     got = [int(v) for v in subprocess.check_output([str(exe)]).split()]
     assert got == [ctypes.sizeof(FrameIO)] + [getattr(FrameIO, n).offset for n in names]
+
+
+def test_stack_host_validation(lib):
+    """rs3_stack_create / rs3_stack_readout reject bad shapes and pointers on
+    the host, before any device call."""
+    import paper_2608_22526_amd as p
+    from paper_2608_22526_amd._binding import StackWeights
+    out = ctypes.c_void_p()
+    buf = (ctypes.c_uint16 * (256 * 2048))()
+    w = (StackWeights * 2)()
+    for i in range(2):
+        for name, _ in StackWeights._fields_:
+            setattr(w[i], name, ctypes.addressof(buf))
+    bad = [(0, 256, 1, 64, 2048, p.RS3_BF16), (17, 256, 1, 64, 2048, p.RS3_BF16),   # layer count
+           (2, 128, 1, 64, 2048, p.RS3_BF16), (2, 256, 3, 64, 2048, p.RS3_BF16),    # d_model, heads
+           (2, 256, 16, 64, 2048, p.RS3_BF16), (2, 256, 1, 32, 2048, p.RS3_BF16),   # head width 16, d_kv
+           (2, 256, 1, 64, 2000, p.RS3_BF16), (2, 256, 1, 64, 8448, p.RS3_BF16),    # F
+           (2, 256, 1, 64, 2048, p.RS3_F32)]
+    for args in bad:
+        assert lib.rs3_stack_create(*args, w, ctypes.byref(out)) == p.RS3_E_INVALID, args
+    w[1].W2 = None
+    assert lib.rs3_stack_create(2, 256, 1, 64, 2048, p.RS3_BF16, w, ctypes.byref(out)) == p.RS3_E_INVALID
+    assert lib.rs3_stack_create(2, 256, 1, 64, 2048, p.RS3_BF16, None, ctypes.byref(out)) == p.RS3_E_INVALID
+    g = p.Grid(64, 64, 1)
+    sz = ctypes.c_size_t()
+    assert lib.rs3_stack_workspace_size(None, 10, 0, ctypes.byref(sz)) == p.RS3_E_INVALID
+    assert lib.rs3_stack_readout(None, ctypes.byref(g), None, None, None, None, 0, 0, None, 0, None, 0,
+                                 None) == p.RS3_E_INVALID
+
+
+def test_stack_weights_layout_matches_header(tmp_path):
+    import shutil
+    import subprocess
+    from paper_2608_22526_amd._binding import StackWeights
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no host C compiler")
+    names = [n for n, _ in StackWeights._fields_]
+    src = tmp_path / "layout.c"
+    src.write_text("#include <stdio.h>\n#include <stddef.h>\n#include \"rs3.h\"\nint main(void) {\n"
+                   "  printf(\"%zu\", sizeof(rs3_stack_weights));\n"
+                   + "".join("  printf(\" %%zu\", offsetof(rs3_stack_weights, %s));\n" % n for n in names)
+                   + "  return 0;\n}\n")
+    exe = tmp_path / "layout"
+    subprocess.check_call([cc, "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)])
+    got = [int(v) for v in subprocess.check_output([str(exe)]).split()]
+    assert got == [ctypes.sizeof(StackWeights)] + [getattr(StackWeights, n).offset for n in names]
