@@ -392,6 +392,190 @@ def gpu_run(args):
     return out
 
 
+# ---------------------------------------------------------------------------
+# The L-layer memory-attention stack (rs3_stack_readout) in the frame
+# ---------------------------------------------------------------------------
+STACK_F = 2048
+STACK_METRIC = "select + L-layer memory-attention stack + commit frames/s at 64x64 grid, 7-frame bank"
+
+
+def _stack_flops(n, N, L, C, F, d_kv):
+    """Algorithmic flops of one stack call on n kept rows and N bank keys:
+    (matrix products, self-attention, cross-attention)."""
+    gemm = 2.0 * n * C * (3 * C) + 2.0 * n * C * C + 2.0 * n * C * d_kv + 2.0 * n * d_kv * C + 4.0 * n * C * F
+    return L * gemm, L * 4.0 * n * n * C, L * 4.0 * n * N * d_kv
+
+
+def cpu_child_stack(workload: str, frames: int, n_layers: int, H_s: int):
+    import numpy as np
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from harness import OraclePipeline
+    from oracle import stack as ostack
+    from workloads import CONFIGS, make_frame, make_sequence, make_stack_weights, make_weights, storage_to_f64
+    cfg = CONFIGS[workload]
+    n_pre = cfg.f_max
+    seq = make_sequence(cfg, n_frames=n_pre + frames + 1)
+    orc = OraclePipeline(cfg, make_weights(cfg))
+    ws = [{k: (storage_to_f64(v, "bf16") if v.dtype == np.uint16 else v.astype(np.float64)) for k, v in w.items()}
+          for w in make_stack_weights(cfg.C, cfg.d_kv, STACK_F, n_layers, "bf16", seed=0)]
+    for t in range(n_pre):
+        orc.commit(make_frame(cfg, t).Kmem, make_frame(cfg, t).Vmem, seq.masks[t], t, t < cfg.n_pin)
+    t0 = time.perf_counter()
+    for t in range(n_pre, n_pre + frames):
+        fr = make_frame(cfg, t)
+        sel, _ = orc.select(seq.read_mask(cfg, t), fr.X, seq.k[t])
+        K, V, _ = orc.banks[0].key_rows()
+        ostack.stack(storage_to_f64(fr.X[0], cfg.dtype), sel[0], storage_to_f64(K, cfg.dtype),
+                     storage_to_f64(V, cfg.dtype), ws, H_s, 1)
+        orc.commit(fr.Kmem, fr.Vmem, seq.masks[t], t, False)
+    dt = time.perf_counter() - t0
+    print(json.dumps({"seconds": dt, "frames": frames, "prefill": n_pre}))
+
+
+def cpu_baseline_stack(workload: str, frames: int, n_layers: int, H_s: int):
+    env = dict(os.environ)
+    for v in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS", "NUMEXPR_NUM_THREADS"):
+        env[v] = "1"
+    env["HIP_VISIBLE_DEVICES"] = ""
+    p = subprocess.run([sys.executable, os.path.abspath(__file__), "--cpu-child", "--workload", workload,
+                        "--cpu-frames", str(frames), "--stack", str(n_layers), "--stack-heads", str(H_s)],
+                       stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True, env=env, timeout=600)
+    if p.returncode != 0:
+        return {"value": None, "unit": "frames/s", "cores": 1, "kind": "oracle", "error": p.stderr[-500:]}
+    r = json.loads(p.stdout.strip().splitlines()[-1])
+    return {"value": r["frames"] / r["seconds"], "unit": "frames/s", "cores": 1, "kind": "oracle",
+            "sample": "%d frame(s) (select + the %d-layer stack row by row on the kept rows + commit) after a "
+                      "%d-frame prefill, fp64 NumPy, 1 thread" % (r["frames"], n_layers, r.get("prefill", 0)),
+            "seconds": r["seconds"]}
+
+
+def gpu_run_stack(args):
+    import torch
+    import paper_2608_22526_amd as rs3
+    from paper_2608_22526_amd.session import Session, to_device
+    from workloads import CONFIGS, make_frame, make_sequence, make_stack_weights, make_weights
+
+    cfg = CONFIGS[args.workload]
+    if cfg.dtype != "bf16" or cfg.C != 256 or cfg.d_kv != 64 or cfg.n_obj != 1:
+        raise SystemExit("--stack runs single-object bf16 workloads of d_model 256 and bank rows of 64")
+    L, H_s = args.stack, args.stack_heads
+    n_pre = cfg.f_max
+    seq = make_sequence(cfg, n_frames=n_pre + N_DISTINCT)
+    k_all = [max(ks) for ks in seq.k]
+    sess = Session(m=cfg.m, n=cfg.n, s=cfg.s, C=cfg.C, H=cfg.H, d_kv=cfg.d_kv, dtype=cfg.dtype, n_obj=1,
+                   shared_x=cfg.shared_x, union_objects=cfg.union_objects, cap=cfg.cap, f_max=cfg.f_max,
+                   n_pin=cfg.n_pin, weights=make_weights(cfg), r_s=cfg.r_s, c=cfg.c, max_sel=max(k_all),
+                   absorb=True)
+    stack = rs3.Stack(make_stack_weights(cfg.C, cfg.d_kv, STACK_F, L, "bf16", seed=0), H_s=H_s, F=STACK_F)
+    ws = torch.empty(stack.workspace_size(max(k_all), args.splits), dtype=torch.uint8, device="cuda")
+    Y = torch.empty((cfg.mn, cfg.C), dtype=torch.bfloat16, device="cuda")
+    frames = []
+    for t in range(n_pre + N_DISTINCT):
+        fr = make_frame(cfg, t)
+        frames.append(dict(X=to_device(fr.X), K=to_device(fr.Kmem), V=to_device(fr.Vmem),
+                           mask=to_device(seq.masks[t]), rmask=to_device(seq.read_mask(cfg, t)), k=seq.k[t],
+                           max_sel=max(seq.k[t])))
+    for t in range(n_pre):
+        f = frames[t]
+        sess.commit(f["K"], f["V"], f["mask"], t, t < cfg.n_pin)
+    step_t = [n_pre]
+    bank = sess.banks[0]
+
+    def step(record=None):
+        t = step_t[0]
+        f = frames[n_pre + (t - n_pre) % N_DISTINCT]
+        sess.select(f["rmask"], f["X"], f["k"])
+        if record is not None:
+            record.append(dict(sel=int(sess.sel_count.cpu()[0]), n_keys=bank.info()["n_keys"]))
+        stack.readout(sess.grid, f["X"], bank, sess.sel_idx, sess.sel_count, f["max_sel"], Y, 0, ws, args.splits)
+        sess.commit(f["K"], f["V"], f["mask"], t, False)
+        step_t[0] += 1
+
+    for i in range(args.warmup):
+        if i % 8 == 7:
+            torch.cuda.synchronize()
+        step()
+    torch.cuda.synchronize()
+    main = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(main)
+    h0 = time.perf_counter()
+    qw = QueueWindow(torch, window=16, every=4)
+    for i in range(args.steps):
+        qw.before(i)
+        step()
+        qw.after(i)
+    host_us = (time.perf_counter() - h0) * 1e6 / args.steps
+    ev1.record(main)
+    torch.cuda.synchronize()
+    ms_step = ev0.elapsed_time(ev1) / args.steps
+    fps = 1000.0 / ms_step
+    graph = _graph_pass(torch, step, args.steps) if args.graph else None
+    rs3.profile_enable(True, (8 * L + 8) * args.steps + 64)
+    rs3.profile_reset()
+    recs = []
+    for _ in range(args.steps):
+        step(record=recs)
+    torch.cuda.synchronize()
+    rep = rs3.profile_report()
+    rs3.profile_enable(False)
+    fl = [_stack_flops(r["sel"], r["n_keys"], L, cfg.C, STACK_F, cfg.d_kv) for r in recs]
+    gemm_fl, sa_fl, ca_fl = (sum(f[i] for f in fl) for i in range(3))
+    kernels = {}
+    for name, (ms, n) in rep.items():
+        if n and not name.startswith("_"):
+            kernels[name] = {"launches": n, "avg_us": 1000.0 * ms / n, "us_per_step": 1000.0 * ms / args.steps}
+    g_ms, g_n = rep["stack_gemm"]
+    a_ms, a_n = rep["attn"]
+    gemm_tf = gemm_fl / (g_ms / 1000.0) / 1e12 if g_ms else 0.0
+    attn_tf = (sa_fl + ca_fl) / (a_ms / 1000.0) / 1e12 if a_ms else 0.0
+    dom = "stack_gemm" if g_ms >= a_ms else "attn"
+    ach = gemm_tf if dom == "stack_gemm" else attn_tf
+    per_launch = (gemm_fl / max(g_n, 1)) if dom == "stack_gemm" else ((sa_fl + ca_fl) / max(a_n, 1))
+    sel_mean = sum(r["sel"] for r in recs) / len(recs)
+    return {
+        "metric": STACK_METRIC,
+        "value": fps,
+        "unit": "frames/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": _describe(cfg) + "; memory attention: %d-layer stack on the kept rows "
+                   "(self-attention %d head(s) of %d, cross-attention one absorbed head on the raw bank rows, "
+                   "MLP %d hidden), fp32 residual stream, bf16 output out of place" % (L, H_s, cfg.C // H_s,
+                                                                                      STACK_F),
+                   "grid": "%dx%d" % (cfg.m, cfg.n), "layers": L, "d_model": cfg.C, "self_heads": H_s,
+                   "mlp_hidden": STACK_F, "d_kv": cfg.d_kv, "bank_frames": cfg.f_max},
+        "roofline": {"bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": ach / PEAK_BF16_TFLOPS, "traffic": None,
+                     "kernel": "k_stk_gemm (all products of the stack)" if dom == "stack_gemm"
+                     else "k_attn (self- and cross-attention of the stack)",
+                     "flops_per_launch": per_launch,
+                     "flops_basis": "algorithmic: per layer 2n*C*(3C + C + 2 d_kv) + 4n*C*F for the products, "
+                                    "4n^2*C self-attention, 4n*N*d_kv cross-attention (n kept rows, N bank keys)",
+                     "avg_launch_us": 1000.0 * (g_ms / max(g_n, 1) if dom == "stack_gemm" else a_ms / max(a_n, 1))},
+        "extra": {
+            "mean_selected_per_frame": sel_mean,
+            "mean_bank_keys": sum(r["n_keys"] for r in recs) / len(recs),
+            "stack_gemm_TFLOP_s": gemm_tf,
+            "attention_TFLOP_s": attn_tf,
+            "flops_per_frame": {"products": gemm_fl / len(recs), "self_attention": sa_fl / len(recs),
+                                "cross_attention": ca_fl / len(recs)},
+            "kernels": kernels,
+            "kernel_sum_us_per_step": sum(v["us_per_step"] for v in kernels.values()),
+            "bank_errors": [bank.error()],
+            "host_enqueue_us_per_step": host_us,
+            "hip_graph": graph,
+        },
+    }
+
+
 def _graph_pass(torch, step, steps):
     """Frames/s with the frame sequence replayed from one captured HIP graph
     (the N_DISTINCT resident input frames, one graph launch each pass): the
@@ -699,9 +883,16 @@ def main():
     ap.add_argument("--cpu-child", action="store_true")
     ap.add_argument("--report", default="", help="write the full measurement report (JSON) to this path")
     ap.add_argument("--post-only", action="store_true", help="time only the closure and palette step")
+    ap.add_argument("--stack", type=int, default=0,
+                    help="run the frame with an L-layer memory-attention stack on the kept rows (rs3_stack_readout) "
+                         "in place of the single readout layer; 0 = the single layer")
+    ap.add_argument("--stack-heads", type=int, default=1, help="self-attention heads of the stack")
     args = ap.parse_args()
     if args.cpu_child:
-        cpu_child(args.workload, args.cpu_frames, args.rope, args.write_dw)
+        if args.stack:
+            cpu_child_stack(args.workload, args.cpu_frames, args.stack, args.stack_heads)
+        else:
+            cpu_child(args.workload, args.cpu_frames, args.rope, args.write_dw)
         return
     if args.rope and args.layer == "absorbed":
         print("--rope needs a projected layer: the rotation sits between the projections that absorption "
@@ -719,6 +910,12 @@ def main():
         return
     if args.report:
         report(args)
+        return
+    if args.stack:
+        out = gpu_run_stack(args)
+        if not args.no_cpu_baseline:
+            out["cpu_baseline"] = cpu_baseline_stack(args.workload, 2, args.stack, args.stack_heads)
+        print(json.dumps(out))
         return
     out = gpu_run(args)
     if not args.no_cpu_baseline:

@@ -487,8 +487,9 @@ enum {
   RS3_K_COMBINE = 7,       /* split merge + W_o + residual + scatter */
   RS3_K_READOUT_F32 = 8,   /* fp32 readout */
   RS3_K_MERGE_COMMIT = 9,  /* split merge and commit in one launch (rs3_readout_commit) */
-  RS3_K_STACK_GEMM = 10,   /* matrix products of the memory-attention stack (with their norms and merges) */
-  RS3_K_COUNT = 11
+  RS3_K_STACK_GEMM = 10,   /* matrix products of the memory-attention stack (with their norms) */
+  RS3_K_STACK_MERGE = 11,  /* split merge of the stack's attentions */
+  RS3_K_COUNT = 12
 };
 rs3_status rs3_profile_enable(int32_t on, int32_t max_launches);
 rs3_status rs3_profile_report(double* total_ms, int64_t* launches, int64_t* dropped);

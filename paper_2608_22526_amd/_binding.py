@@ -102,7 +102,7 @@ _SIGS = {
 }
 
 KERNEL_NAMES = ["energy", "select", "commit", "commit_append", "copy", "qproj", "attn", "combine",
-                "readout_f32", "merge_commit", "stack_gemm"]
+                "readout_f32", "merge_commit", "stack_gemm", "stack_merge"]
 
 _lib = None
 

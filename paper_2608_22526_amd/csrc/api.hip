@@ -1463,14 +1463,20 @@ rs3_status rs3_stack_readout(const rs3_stack* S, const rs3_grid* g, const void* 
     q.write_bank = l == 0;
     e = rs3_launch_stack_gemm(q, l == 0 ? STK_A_GLN : STK_A_LN, STK_E_QKV, st);
     if (e == hipSuccess) e = rs3_launch_attn(as, abs_, st, false);
+    // the key splits merged into the query buffer the attention has read
+    StkGemmArgs ms = p;
+    ms.K = C;
+    ms.S = L.S_s;
+    ms.H_att = S->Hs;
+    ms.d_att = S->dhs;
+    ms.out = p.Qs;
+    if (e == hipSuccess) e = rs3_launch_stack_merge(ms, st);
     StkGemmArgs o = p;
+    o.A = p.Qs;
     o.WT = ly.WosT;
     o.N = C;
     o.K = C;
-    o.S = L.S_s;
-    o.H_att = S->Hs;
-    o.d_att = S->dhs;
-    if (e == hipSuccess) e = rs3_launch_stack_gemm(o, STK_A_MERGE, STK_E_RESID, st);
+    if (e == hipSuccess) e = rs3_launch_stack_gemm(o, STK_A_BF16, STK_E_RESID, st);
     // z += CA(LN2(z)): one absorbed head of width C
     StkGemmArgs c = p;
     c.ln_g = ly.ln_g[1];
@@ -1482,14 +1488,19 @@ rs3_status rs3_stack_readout(const rs3_stack* S, const rs3_grid* g, const void* 
     c.scale = (float)(log2e / sqrt((double)C));
     if (e == hipSuccess) e = rs3_launch_stack_gemm(c, STK_A_LN, STK_E_STORE, st);
     if (e == hipSuccess) e = rs3_launch_attn(ac, abc, st, false);
+    StkGemmArgs mc = p;
+    mc.K = S->d_kv;
+    mc.S = S_c;
+    mc.H_att = 1;
+    mc.d_att = S->d_kv;
+    mc.out = w + L.qc;
+    if (e == hipSuccess) e = rs3_launch_stack_merge(mc, st);
     StkGemmArgs v = p;
+    v.A = w + L.qc;
     v.WT = ly.WvoT;
     v.N = C;
     v.K = S->d_kv;
-    v.S = S_c;
-    v.H_att = 1;
-    v.d_att = S->d_kv;
-    if (e == hipSuccess) e = rs3_launch_stack_gemm(v, STK_A_MERGE, STK_E_RESID, st);
+    if (e == hipSuccess) e = rs3_launch_stack_gemm(v, STK_A_BF16, STK_E_RESID, st);
     // z += relu(LN3(z) W_1) W_2; after the last layer the rows go to Y
     StkGemmArgs m1 = p;
     m1.ln_g = ly.ln_g[2];

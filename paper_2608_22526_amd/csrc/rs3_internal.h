@@ -249,13 +249,11 @@ struct AttendPrepArgs {
 // One matrix product of the memory-attention stack (k_stk_gemm): out = A W
 // over the kept rows, A [M][K] from one of the prologues, W given
 // transposed as WT [N][K].
-enum StkAMode { STK_A_BF16 = 0, STK_A_LN = 1, STK_A_GLN = 2, STK_A_MERGE = 3 };
-//  BF16 : A rows of a bf16 buffer [M][K]
+enum StkAMode { STK_A_BF16 = 0, STK_A_LN = 1, STK_A_GLN = 2 };
+//  BF16 : A rows of a bf16 buffer [M][K] (K a multiple of 64)
 //  LN   : LayerNorm (gain ln_g, shift ln_b) of the fp32 stream rows Z [M][256]
 //  GLN  : the same of the kept cells X[sel[r]] of the bf16 grid, which also
 //         become the stream rows (Zw)
-//  MERGE: the key splits of the attention (Opart, ML: S splits, H_att heads of
-//         width d_att = K / H_att) merged into the normalised output rows
 enum StkEMode { STK_E_STORE = 0, STK_E_RESID = 1, STK_E_SCATTER = 2, STK_E_QKV = 3 };
 //  STORE  : out [M][N] bf16 = scale * (A W), with relu if set
 //  RESID  : Zw [M][256] += A W
@@ -272,8 +270,8 @@ struct StkGemmArgs {
   const float* ln_b;
   const void* X;
   const int32_t* sel;
-  const rs3::bf16_t* Opart;   // [S][M][K]
-  const float* ML;            // [S][M][H_att][2]
+  const rs3::bf16_t* Opart;   // [S][M][K]  (k_stk_merge: the attention's key splits,
+  const float* ML;            // [S][M][H_att][2]   H_att heads of width d_att = K / H_att)
   int S, H_att, d_att;
   const int32_t* count;       // kept rows (device), clamped into [0, M]
   int32_t* err_hdr;           // header of the bank whose error word takes the reports
@@ -352,6 +350,9 @@ void rs3_prof_end(int id, hipStream_t st);
 // Stack products (k_stk_gemm with prologue am and epilogue em) and the
 // X -> Y copy of the grid (bf16 -> bf16 or fp32) before the scatter.
 hipError_t rs3_launch_stack_gemm(const StkGemmArgs& p, int am, int em, hipStream_t st);
+// Merge of the attention's key splits (Opart, ML, S, H_att, d_att, K = the
+// attention width) into the normalised bf16 rows `out` [M][K].
+hipError_t rs3_launch_stack_merge(const StkGemmArgs& p, hipStream_t st);
 hipError_t rs3_launch_stack_copy(const void* X, void* Y, int64_t elems, int y_f32, hipStream_t st);
 hipError_t rs3_select_setup();
 hipError_t rs3_commit_setup();

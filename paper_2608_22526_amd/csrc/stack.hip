@@ -30,10 +30,24 @@ constexpr size_t SG_LDS = (size_t)SG_BM * SG_PITCH * 2;
 constexpr int SG_C = 256;    // d_model of the stack
 constexpr float SG_LN_EPS = 1e-5f;
 
+template <int CTRL>
+__device__ __forceinline__ float dppf(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over the 64 lanes, the same value in every lane: within rows of 16
+// lanes by DPP (quad swaps, half-row and row mirrors), then across rows by
+// v_permlane16_swap and v_permlane32_swap.  Each step adds a lane to a
+// partner that adds it back, so every lane holds the same bits.
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
+  v += dppf<0xB1>(v);    // quad_perm(1, 0, 3, 2)
+  v += dppf<0x4E>(v);    // quad_perm(2, 3, 0, 1)
+  v += dppf<0x141>(v);   // row_half_mirror
+  v += dppf<0x140>(v);   // row_mirror
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
 // Kept-row count of the call, clamped into [0, M]; a count outside that
@@ -56,20 +70,11 @@ __device__ __forceinline__ int stk_cell(const StkGemmArgs& p, int r) {
 }
 
 // ---- prologues: the A chunk [64][kn] of rows row0.. in LDS (bf16) ----------
-// plain bf16 rows of A [M][K]
-__device__ __forceinline__ void pro_bf16(const StkGemmArgs& p, int row0, int cnt, int kc, int kn, bf16_t* As) {
-  const int cpr = kn / 8;
-  for (int u = threadIdx.x; u < SG_BM * cpr; u += 256) {
-    const int r = u / cpr, c8 = u - r * cpr;
-    u32x4 v = {0, 0, 0, 0};
-    if (row0 + r < cnt) v = gload((const u32x4*)((const bf16_t*)p.A + (int64_t)(row0 + r) * p.K + kc + 8 * c8));
-    *(u32x4*)(As + r * SG_PITCH + 8 * c8) = v;
-  }
-}
-
 // LayerNorm of the fp32 rows of Z (GATHER: of the kept cells of the bf16
 // grid X, and the column-block-0 work-group stores them to Z): each wave
-// normalises 16 rows, a lane holding 4 channels.
+// normalises 16 rows, a lane holding 4 channels.  Rows past the count are
+// computed on a clamped row and stored as zero, so the 16 reductions carry
+// no branch and interleave.
 template <bool GATHER>
 __device__ __forceinline__ void pro_ln(const StkGemmArgs& p, int row0, int cnt, bf16_t* As) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -89,64 +94,89 @@ __device__ __forceinline__ void pro_ln(const StkGemmArgs& p, int row0, int cnt, 
   }
   const f32x4 g = gload((const f32x4*)(p.ln_g + 4 * lane));
   const f32x4 b = gload((const f32x4*)(p.ln_b + 4 * lane));
+  if constexpr (GATHER) {
+    if (blockIdx.y == 0) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        if (row0 + 16 * wave + i < cnt) *(f32x4*)(p.Zw + (int64_t)(row0 + 16 * wave + i) * SG_C + 4 * lane) = z[i];
+    }
+  }
+  float sm[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) sm[i] = wave_sum(z[i][0] + z[i][1] + z[i][2] + z[i][3]);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    z[i] -= sm[i] * (1.f / SG_C);
+    sm[i] = wave_sum(z[i][0] * z[i][0] + z[i][1] * z[i][1] + z[i][2] * z[i][2] + z[i][3] * z[i][3]);
+  }
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     const int lr = 16 * wave + i;
-    u32x2 o = {0, 0};
-    if (row0 + lr < cnt) {
-      if constexpr (GATHER) {
-        if (blockIdx.y == 0) *(f32x4*)(p.Zw + (int64_t)(row0 + lr) * SG_C + 4 * lane) = z[i];
-      }
-      const float mean = wave_sum(z[i][0] + z[i][1] + z[i][2] + z[i][3]) * (1.f / SG_C);
-      const f32x4 d = z[i] - mean;
-      const float var = wave_sum(d[0] * d[0] + d[1] * d[1] + d[2] * d[2] + d[3] * d[3]) * (1.f / SG_C);
-      const float rs = 1.f / sqrtf(var + SG_LN_EPS);
-      const f32x4 y = d * rs * g + b;
-      o = u32x2{pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3])};
-    }
+    const float rs = 1.f / sqrtf(sm[i] * (1.f / SG_C) + SG_LN_EPS);
+    const f32x4 y = z[i] * rs * g + b;
+    u32x2 o = {pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3])};
+    if (row0 + lr >= cnt) o = u32x2{0, 0};
     *(u32x2*)(As + lr * SG_PITCH + 4 * lane) = o;
   }
 }
 
-// Log-sum-exp merge of the attention's key splits (partials O/l, (m, l) per
-// split, row and head) into the normalised rows O [64][K] (K = the attention
-// width).  A split without keys holds l = 0 and adds nothing; a row with no
-// key at all (empty bank) gets O = 0.
-__device__ __forceinline__ void pro_merge(const StkGemmArgs& p, int row0, int cnt, bf16_t* As) {
+// grid ceil(M*K/8 / 256), block 256: one thread per (kept row, 8 columns)
+// merges the attention's key splits (partials O/l and (m, l) per split, row
+// and head: Opart [S][M][K], ML [S][M][H_att][2]) by log-sum-exp into the
+// normalised bf16 rows out [M][K].  The splits are loaded eight at a time
+// without branches (split indices past S re-read the last split and are
+// masked); a split without keys holds l = 0 and adds nothing, its O words
+// (never written) replaced by zero; a row with no key at all gets O = 0.
+__global__ __launch_bounds__(256) void k_stk_merge(StkGemmArgs p) {
   const int D = p.K, cpr = D / 8;
-  for (int it = threadIdx.x; it < SG_BM * cpr; it += 256) {
-    const int r = it / cpr, d0 = 8 * (it - r * cpr), h = d0 / p.d_att;
-    u32x4 out = {0, 0, 0, 0};
-    const int row = row0 + r;
-    if (row < cnt) {
-      float M = -INFINITY, W = 0.f;
-      float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-      for (int s = 0; s < p.S; ++s) {
-        const int64_t prow = (int64_t)s * p.M + row;
-        const float m = gload(p.ML + (prow * p.H_att + h) * 2), l = gload(p.ML + (prow * p.H_att + h) * 2 + 1);
-        if (!(l > 0.f)) continue;
-        const u32x4 v = gload((const u32x4*)(p.Opart + prow * D + d0));
-        if (m > M) {
-          const float sc = __builtin_amdgcn_exp2f(M - m);
-          W *= sc;
+  const int64_t it = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (it >= (int64_t)p.M * cpr) return;
+  const int row = (int)(it / cpr), d0 = 8 * (int)(it - (int64_t)row * cpr), h = d0 / p.d_att;
+  const int cnt = stk_count(p);
+  if (row >= cnt) return;
+  float M = -INFINITY, W = 0.f;
+  float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  for (int s0 = 0; s0 < p.S; s0 += 8) {
+    f32x2 ml[8];
+    u32x4 v[8];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) acc[e] *= sc;
-          M = m;
-        }
-        const float w = __builtin_amdgcn_exp2f(m - M) * l;
-        W += w;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          acc[2 * e] += w * __uint_as_float(v[e] << 16);
-          acc[2 * e + 1] += w * __uint_as_float(v[e] & 0xffff0000u);
-        }
-      }
-      const float inv = W > 0.f ? 1.f / W : 0.f;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) out[e] = pack_bf16x2(acc[2 * e] * inv, acc[2 * e + 1] * inv);
+    for (int i = 0; i < 8; ++i) {
+      const int64_t prow = (int64_t)min(s0 + i, p.S - 1) * p.M + row;
+      ml[i] = gload((const f32x2*)(p.ML + (prow * p.H_att + h) * 2));
+      v[i] = gload((const u32x4*)(p.Opart + prow * D + d0));
     }
-    *(u32x4*)(As + r * SG_PITCH + d0) = out;
+    bool on[8];
+    float mb = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      on[i] = s0 + i < p.S && ml[i][1] > 0.f;
+      mb = __builtin_elementwise_maximum(mb, on[i] ? ml[i][0] : -INFINITY);
+    }
+    if (mb == -INFINITY) continue;
+    const float Mn = __builtin_elementwise_maximum(M, mb);
+    const float sc = __builtin_amdgcn_exp2f(M - Mn);   // 0 while M = -inf
+    W *= sc;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] *= sc;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float w = on[i] ? __builtin_amdgcn_exp2f(ml[i][0] - Mn) * ml[i][1] : 0.f;
+      W += w;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t x = on[i] ? v[i][e] : 0u;
+        acc[2 * e] += w * __uint_as_float(x << 16);
+        acc[2 * e + 1] += w * __uint_as_float(x & 0xffff0000u);
+      }
+    }
+    M = Mn;
   }
+  const float inv = W > 0.f ? 1.f / W : 0.f;
+  u32x4 out;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) out[e] = pack_bf16x2(acc[2 * e] * inv, acc[2 * e + 1] * inv);
+  *(u32x4*)((bf16_t*)p.out + (int64_t)row * D + d0) = out;
 }
 
 // The self-attention's one-frame bank: descriptor, header (tile and key
@@ -204,22 +234,53 @@ __global__ __launch_bounds__(256) void k_stk_gemm(StkGemmArgs p) {
   const int col = col0 + 32 * wc + (lane & 31);
   const bf16_t* wrow = p.WT + (int64_t)col * p.K;
   f32x16 acc = {};
-  for (int kc = 0; kc < p.K; kc += SG_KC) {
-    const int kn = min(SG_KC, p.K - kc);
+  if constexpr (AM == STK_A_BF16) {
+    // register double buffer: chunk kc+1's A rows and B operands are in
+    // flight while chunk kc is multiplied
+    constexpr int AU = SG_BM * SG_KC / 8 / 256;   // 16-byte A units per thread and chunk
+    u32x4 av[AU], bw[SG_KC / 16];
+    auto load = [&](int kc) {
+      const int kn = min(SG_KC, p.K - kc), cpr = kn / 8;
+#pragma unroll
+      for (int j = 0; j < AU; ++j) {
+        const int u = threadIdx.x + 256 * j, r = u / cpr, c8 = u - r * cpr;
+        const int rr = min(row0 + r, cnt - 1);
+        if (u < SG_BM * cpr) av[j] = gload((const u32x4*)((const bf16_t*)p.A + (int64_t)rr * p.K + kc + 8 * c8));
+      }
+#pragma unroll
+      for (int ks = 0; ks < SG_KC / 16; ++ks)
+        if (16 * ks < kn) bw[ks] = gload((const u32x4*)(wrow + kc + 16 * ks + 8 * g));
+    };
+    load(0);
+    for (int kc = 0; kc < p.K; kc += SG_KC) {
+      const int kn = min(SG_KC, p.K - kc), cpr = kn / 8;
+      if (kc > 0) __syncthreads();   // the previous chunk's operands are read
+#pragma unroll
+      for (int j = 0; j < AU; ++j) {
+        const int u = threadIdx.x + 256 * j, r = u / cpr, c8 = u - r * cpr;
+        if (u < SG_BM * cpr) *(u32x4*)(As + r * SG_PITCH + 8 * c8) = row0 + r < cnt ? av[j] : u32x4{0, 0, 0, 0};
+      }
+      u32x4 bc[SG_KC / 16];
+#pragma unroll
+      for (int ks = 0; ks < SG_KC / 16; ++ks) bc[ks] = bw[ks];
+      __syncthreads();
+      if (kc + SG_KC < p.K) load(kc + SG_KC);
+      const bf16_t* arow = As + (32 * wr + (lane & 31)) * SG_PITCH + 8 * g;
+#pragma unroll
+      for (int ks = 0; ks < SG_KC / 16; ++ks)
+        if (16 * ks < kn) acc = mfma32(*(const u32x4*)(arow + 16 * ks), bc[ks], acc);
+    }
+  } else {
+    // LayerNorm prologues: K = d_model = one chunk
     u32x4 bw[SG_KC / 16];
 #pragma unroll
-    for (int ks = 0; ks < SG_KC / 16; ++ks)
-      if (16 * ks < kn) bw[ks] = gload((const u32x4*)(wrow + kc + 16 * ks + 8 * g));
-    if (kc > 0) __syncthreads();   // the previous chunk's operands are read
-    if constexpr (AM == STK_A_BF16) pro_bf16(p, row0, cnt, kc, kn, As);
+    for (int ks = 0; ks < SG_KC / 16; ++ks) bw[ks] = gload((const u32x4*)(wrow + 16 * ks + 8 * g));
     if constexpr (AM == STK_A_LN) pro_ln<false>(p, row0, cnt, As);
     if constexpr (AM == STK_A_GLN) pro_ln<true>(p, row0, cnt, As);
-    if constexpr (AM == STK_A_MERGE) pro_merge(p, row0, cnt, As);
     __syncthreads();
     const bf16_t* arow = As + (32 * wr + (lane & 31)) * SG_PITCH + 8 * g;
 #pragma unroll
-    for (int ks = 0; ks < SG_KC / 16; ++ks)
-      if (16 * ks < kn) acc = mfma32(*(const u32x4*)(arow + 16 * ks), bw[ks], acc);
+    for (int ks = 0; ks < SG_KC / 16; ++ks) acc = mfma32(*(const u32x4*)(arow + 16 * ks), bw[ks], acc);
   }
   const int rbase = row0 + 32 * wr;
   if constexpr (EM == STK_E_STORE) {
@@ -322,17 +383,24 @@ hipError_t rs3_launch_stack_gemm(const StkGemmArgs& p, int am, int em, hipStream
   if (p.M <= 0) return hipSuccess;
   if (p.N % SG_BN != 0 || p.K % 16 != 0) return hipErrorInvalidValue;
   if ((am == STK_A_LN || am == STK_A_GLN) && p.K != SG_C) return hipErrorInvalidValue;
-  if (am == STK_A_MERGE && p.K > SG_KC) return hipErrorInvalidValue;
+  if (am == STK_A_BF16 && p.K % 64 != 0) return hipErrorInvalidValue;
 #define RS3_SG(A, E) \
   if (am == A && em == E) return launch_gemm<A, E>(p, st);
   RS3_SG(STK_A_GLN, STK_E_QKV)
   RS3_SG(STK_A_LN, STK_E_QKV)
-  RS3_SG(STK_A_MERGE, STK_E_RESID)
   RS3_SG(STK_A_LN, STK_E_STORE)
   RS3_SG(STK_A_BF16, STK_E_RESID)
   RS3_SG(STK_A_BF16, STK_E_SCATTER)
 #undef RS3_SG
   return hipErrorInvalidValue;
+}
+
+hipError_t rs3_launch_stack_merge(const StkGemmArgs& p, hipStream_t st) {
+  const int64_t items = (int64_t)p.M * (p.K / 8);
+  if (items == 0) return hipSuccess;
+  if (p.K % 8 != 0 || p.d_att % 8 != 0) return hipErrorInvalidValue;
+  RS3_LAUNCH(RS3_K_STACK_MERGE, st, k_stk_merge, dim3((unsigned)((items + 255) / 256)), dim3(256), 0, st, p);
+  return hipGetLastError();
 }
 
 hipError_t rs3_launch_stack_copy(const void* X, void* Y, int64_t elems, int y_f32, hipStream_t st) {
