@@ -487,9 +487,11 @@ enum {
   RS3_K_COMBINE = 7,       /* split merge + W_o + residual + scatter */
   RS3_K_READOUT_F32 = 8,   /* fp32 readout */
   RS3_K_MERGE_COMMIT = 9,  /* split merge and commit in one launch (rs3_readout_commit) */
-  RS3_K_STACK_GEMM = 10,   /* matrix products of the memory-attention stack (with their norms) */
-  RS3_K_STACK_MERGE = 11,  /* split merge of the stack's attentions */
-  RS3_K_COUNT = 12
+  RS3_K_STACK_GEMM = 10,   /* stack: QKV product, and W_os + LN2 + cross-attention queries */
+  RS3_K_STACK_MERGE = 11,  /* stack: split merge of its attentions */
+  RS3_K_STACK_MLP = 12,    /* stack: W_vo + LN3 + MLP chunk partials */
+  RS3_K_STACK_ROWS = 13,   /* stack: gather / partial sum + LN1 / scatter */
+  RS3_K_COUNT = 14
 };
 rs3_status rs3_profile_enable(int32_t on, int32_t max_launches);
 rs3_status rs3_profile_report(double* total_ms, int64_t* launches, int64_t* dropped);

@@ -102,7 +102,7 @@ _SIGS = {
 }
 
 KERNEL_NAMES = ["energy", "select", "commit", "commit_append", "copy", "qproj", "attn", "combine",
-                "readout_f32", "merge_commit", "stack_gemm", "stack_merge"]
+                "readout_f32", "merge_commit", "stack_gemm", "stack_merge", "stack_mlp", "stack_rows"]
 
 _lib = None
 

@@ -49,6 +49,7 @@ rs3_status ensure_setup() {
   if (e == hipSuccess) e = rs3_select_setup();
   if (e == hipSuccess) e = rs3_commit_setup();
   if (e == hipSuccess) e = rs3_fused_setup();
+  if (e == hipSuccess) e = rs3_stack_setup();
   if (e != hipSuccess) return RS3_E_DEVICE;
   setup_done = true;
   return RS3_OK;
@@ -1204,12 +1205,12 @@ struct rs3_stack {
   struct Layer {
     const float* ln_g[3];
     const float* ln_b[3];
-    const bf16_t* WqkvT;   // [3C][C]: W_qs | W_ks | W_vs, transposed
-    const bf16_t* WosT;    // [C][C]
-    const bf16_t* WqcT;    // [d_kv][C]: (W_q W_k^T)^T
-    const bf16_t* WvoT;    // [C][d_kv]: (W_v W_o)^T
-    const bf16_t* W1T;     // [F][C]
-    const bf16_t* W2T;     // [C][F]
+    const bf16_t* Wqkv;   // packed [256][768]: W_qs | W_ks | W_vs
+    const bf16_t* Wos;    // packed [256][256]
+    const bf16_t* Wqc;    // packed [256][d_kv]: W_q W_k^T
+    const bf16_t* Wvo;    // packed [d_kv][256]: W_v W_o
+    const bf16_t* W1;     // packed [256][F]
+    const bf16_t* W2;     // packed [F][256]
   };
   int32_t n_layers, C, Hs, dhs, d_kv, F;
   void* dmem;   // every layer's weights, one allocation
@@ -1218,11 +1219,46 @@ struct rs3_stack {
 
 namespace {
 
+// A weight W [K][N] (out = a W) in MFMA B-operand order: for each 32-column
+// block nb and 16-deep step ks, 64 lanes x 8 values, lane l holding column
+// 32*nb + l%32 and rows 16*ks + 8*(l/32) .. +7.  `at(k, n)` gives bf16 bits.
+template <class At>
+std::vector<uint8_t> pack_b(int K, int N, At at) {
+  std::vector<uint8_t> out((size_t)K * N * 2);
+  uint16_t* o = (uint16_t*)out.data();
+  const int KS = K / 16;
+  for (int nb = 0; nb < N / 32; ++nb)
+    for (int ks = 0; ks < KS; ++ks)
+      for (int l = 0; l < 64; ++l)
+        for (int e = 0; e < 8; ++e)
+          o[(((size_t)nb * KS + ks) * 64 + l) * 8 + e] = at(16 * ks + 8 * (l / 32) + e, 32 * nb + l % 32);
+  return out;
+}
+
+uint16_t bits_at(const void* W, int cols, int k, int n) { return ((const uint16_t*)W)[(size_t)k * cols + n]; }
+
+// Row-major product A [r][k] B [k][c] of bf16 matrices, accumulated in fp64
+// and rounded to bf16 (nearest even); b_transposed: B is given as [c][k].
+std::vector<uint16_t> product_bits(const void* A, const void* B, int r, int k, int c, bool b_transposed) {
+  std::vector<uint16_t> out((size_t)r * c);
+  std::vector<uint8_t> tmp(2);
+  for (int i = 0; i < r; ++i)
+    for (int j = 0; j < c; ++j) {
+      double acc = 0.0;
+      for (int kk = 0; kk < k; ++kk)
+        acc += load_elem(A, (size_t)i * k + kk, RS3_BF16) *
+               load_elem(B, b_transposed ? (size_t)j * k + kk : (size_t)kk * c + j, RS3_BF16);
+      store_elem(tmp, 0, acc, RS3_BF16);
+      memcpy(&out[(size_t)i * c + j], tmp.data(), 2);
+    }
+  return out;
+}
+
 // Key splits of the self-attention: a launch of about 256 work-groups
 // (8*n_qt*ceil(H_s*S/8)), at least two key tiles per split.
 int stack_self_splits(int M, int Hs) {
   const int ntile = (M + KT - 1) / KT, n_qt = (M + 127) / 128;
-  int S = 256 / (n_qt * Hs);
+  int S = n_qt > 0 ? 256 / (n_qt * Hs) : 1;
   const int most = (ntile + 1) / 2;
   if (S > most) S = most;
   if (S * Hs > RS3_MAX_SPLITS_X_HEADS) S = RS3_MAX_SPLITS_X_HEADS / Hs;
@@ -1230,7 +1266,7 @@ int stack_self_splits(int M, int Hs) {
 }
 
 struct StackLayout {
-  size_t z, qs, qc, kh, vh, tiles, desc, hdr, opart, ml, hbuf, total;
+  size_t z, zp, part, a1, qs, qc, kh, vh, tiles, desc, hdr, opart, ml, total;
   int S_s, ntile;
 };
 
@@ -1246,6 +1282,9 @@ void stack_layout(const rs3_stack* S, int M, int S_c, StackLayout* L) {
     return at;
   };
   L->z = take((size_t)M * C * 4);
+  L->zp = take((size_t)M * C * 4);
+  L->part = take((size_t)(S->F / 256) * M * C * 4);
+  L->a1 = take((size_t)M * C * 2);
   L->qs = take((size_t)M * C * 2);
   L->qc = take((size_t)M * S->d_kv * 2);
   L->kh = take((size_t)L->ntile * KT * C * 2);
@@ -1257,7 +1296,6 @@ void stack_layout(const rs3_stack* S, int M, int S_c, StackLayout* L) {
   L->opart = take((op_s > op_c ? op_s : op_c) * 2);
   const size_t ml_s = (size_t)L->S_s * M * S->Hs, ml_c = (size_t)S_c * M;
   L->ml = take((ml_s > ml_c ? ml_s : ml_c) * 8);
-  L->hbuf = take((size_t)M * S->F * 2);
   L->total = off;
 }
 
@@ -1279,12 +1317,11 @@ rs3_status rs3_stack_create(int32_t n_layers, int32_t C, int32_t H_s, int32_t d_
       if (!q) return RS3_E_INVALID;
   }
   *out = nullptr;
-  const size_t es = 2;
   // per layer: QKV, W_os, W_qc, W_vo, W_1, W_2 (bf16), then six norm vectors
-  const size_t mats[6] = {(size_t)3 * C * C, (size_t)C * C, (size_t)d_kv * C, (size_t)C * d_kv, (size_t)F * C,
-                          (size_t)C * F};
+  const size_t mats[6] = {(size_t)3 * C * C, (size_t)C * C, (size_t)C * d_kv, (size_t)d_kv * C, (size_t)C * F,
+                          (size_t)F * C};
   size_t per = 0;
-  for (size_t m : mats) per += align256(m * es);
+  for (size_t m : mats) per += align256(m * 2);
   per += 6 * align256((size_t)C * 4);
   std::vector<uint8_t> host(per * n_layers);
   rs3_stack* S = new rs3_stack();
@@ -1311,18 +1348,17 @@ rs3_status rs3_stack_create(int32_t n_layers, int32_t C, int32_t H_s, int32_t d_
       return (const bf16_t*)d;
     };
     rs3_stack::Layer L;
-    std::vector<uint8_t> qkv((size_t)3 * C * C * es);
-    const void* in3[3] = {w.Wqs, w.Wks, w.Wvs};
-    for (int j = 0; j < 3; ++j) {
-      std::vector<uint8_t> t = transpose(in3[j], C, C, es);
-      memcpy(&qkv[(size_t)j * C * C * es], t.data(), t.size());
-    }
-    L.WqkvT = put(qkv);
-    L.WosT = put(transpose(w.Wos, C, C, es));
-    L.WqcT = put(product_T(w.Wq, w.Wk, C, C, d_kv, dt, true));
-    L.WvoT = put(product_T(w.Wv, w.Wo, d_kv, C, C, dt, false));
-    L.W1T = put(transpose(w.W1, C, F, es));
-    L.W2T = put(transpose(w.W2, F, C, es));
+    L.Wqkv = put(pack_b(C, 3 * C, [&](int k, int n) {
+      const void* W = n < C ? w.Wqs : (n < 2 * C ? w.Wks : w.Wvs);
+      return bits_at(W, C, k, n % C);
+    }));
+    L.Wos = put(pack_b(C, C, [&](int k, int n) { return bits_at(w.Wos, C, k, n); }));
+    const std::vector<uint16_t> qc = product_bits(w.Wq, w.Wk, C, C, d_kv, true);    // [C][d_kv]
+    const std::vector<uint16_t> vo = product_bits(w.Wv, w.Wo, d_kv, C, C, false);   // [d_kv][C]
+    L.Wqc = put(pack_b(C, d_kv, [&](int k, int n) { return qc[(size_t)k * d_kv + n]; }));
+    L.Wvo = put(pack_b(d_kv, C, [&](int k, int n) { return vo[(size_t)k * C + n]; }));
+    L.W1 = put(pack_b(C, F, [&](int k, int n) { return bits_at(w.W1, F, k, n); }));
+    L.W2 = put(pack_b(F, C, [&](int k, int n) { return bits_at(w.W2, C, k, n); }));
     const float* nv[6] = {w.ln1_g, w.ln1_b, w.ln2_g, w.ln2_b, w.ln3_g, w.ln3_b};
     for (int j = 0; j < 6; ++j) {
       std::vector<uint8_t> v((size_t)C * 4);
@@ -1387,21 +1423,28 @@ rs3_status rs3_stack_readout(const rs3_stack* S, const rs3_grid* g, const void* 
   const int C = S->C;
   const double log2e = 1.4426950408889634;
 
-  StkGemmArgs p;
+  StkArgs p;
   memset(&p, 0, sizeof(p));
-  p.Z = (const float*)(w + L.z);
-  p.Zw = (float*)(w + L.z);
-  p.X = X;
-  p.sel = sel_idx;
-  p.Opart = (const bf16_t*)(w + L.opart);
-  p.ML = (const float*)(w + L.ml);
   p.count = sel_count;
   p.err_hdr = bank->host.hdr;
+  p.sel = sel_idx;
   p.M = max_sel;
   p.mn = mn;
+  p.X = X;
   p.Y = Y;
   p.y_f32 = y_fp32;
+  p.Z = (float*)(w + L.z);
+  p.Zp = (float*)(w + L.zp);
+  p.P = (float*)(w + L.part);
+  p.NC = S->F / 256;
+  p.F = S->F;
+  p.A1 = (bf16_t*)(w + L.a1);
   p.Qs = (bf16_t*)(w + L.qs);
+  p.Qc = (bf16_t*)(w + L.qc);
+  p.qscale_s = (float)(log2e / sqrt((double)S->dhs));
+  p.qscale_c = (float)(log2e / sqrt((double)C));
+  p.Opart = (const bf16_t*)(w + L.opart);
+  p.ML = (const float*)(w + L.ml);
   p.Kh = (bf16_t*)(w + L.kh);
   p.Vh = (bf16_t*)(w + L.vh);
   p.tiles = (TileEnt*)(w + L.tiles);
@@ -1437,7 +1480,7 @@ rs3_status rs3_stack_readout(const rs3_stack* S, const rs3_grid* g, const void* 
   abs_.ntcap[0] = L.ntile;
   ac = as;
   ac.banks[0] = bank->d_desc;
-  ac.Q = w + L.qc;
+  ac.Q = p.Qc;
   ac.H = 1;
   ac.d_h = bl.dah;
   ac.D = bl.Da;
@@ -1449,75 +1492,51 @@ rs3_status rs3_stack_readout(const rs3_stack* S, const rs3_grid* g, const void* 
   abc.vh[0] = bank->host.Vhat;
   abc.ntcap[0] = bank->host.n_tiles_cap;
 
+  // gather + the first layer's LN1
+  p.ln_g = S->layers[0].ln_g[0];
+  p.ln_b = S->layers[0].ln_b[0];
+  e = rs3_launch_stack_rows(p, 0, st);
   for (int l = 0; l < S->n_layers && e == hipSuccess; ++l) {
     const rs3_stack::Layer& ly = S->layers[l];
-    const bool last = l == S->n_layers - 1;
-    // z += SA(LN1(z))
-    StkGemmArgs q = p;
-    q.ln_g = ly.ln_g[0];
-    q.ln_b = ly.ln_b[0];
-    q.WT = ly.WqkvT;
-    q.N = 3 * C;
-    q.K = C;
-    q.scale = (float)(log2e / sqrt((double)S->dhs));
+    StkArgs q = p;
+    q.Wqkv = ly.Wqkv;
+    q.Wos = ly.Wos;
+    q.Wqc = ly.Wqc;
+    q.Wvo = ly.Wvo;
+    q.W1 = ly.W1;
+    q.W2 = ly.W2;
+    q.ln2_g = ly.ln_g[1];
+    q.ln2_b = ly.ln_b[1];
+    q.ln3_g = ly.ln_g[2];
+    q.ln3_b = ly.ln_b[2];
     q.write_bank = l == 0;
-    e = rs3_launch_stack_gemm(q, l == 0 ? STK_A_GLN : STK_A_LN, STK_E_QKV, st);
+    // z += SA(LN1(z)), then LN2 and the cross-attention's queries
+    e = rs3_launch_stack_qkv(q, st);
     if (e == hipSuccess) e = rs3_launch_attn(as, abs_, st, false);
-    // the key splits merged into the query buffer the attention has read
-    StkGemmArgs ms = p;
-    ms.K = C;
-    ms.S = L.S_s;
-    ms.H_att = S->Hs;
-    ms.d_att = S->dhs;
-    ms.out = p.Qs;
-    if (e == hipSuccess) e = rs3_launch_stack_merge(ms, st);
-    StkGemmArgs o = p;
-    o.A = p.Qs;
-    o.WT = ly.WosT;
-    o.N = C;
-    o.K = C;
-    if (e == hipSuccess) e = rs3_launch_stack_gemm(o, STK_A_BF16, STK_E_RESID, st);
+    q.S = L.S_s;
+    q.H_att = S->Hs;
+    q.d_att = S->dhs;
+    q.D_att = C;
+    q.mout = p.Qs;   // the merged rows replace the queries the attention has read
+    if (e == hipSuccess) e = rs3_launch_stack_merge(q, st);
+    if (e == hipSuccess) e = rs3_launch_stack_post_sa(q, st);
     // z += CA(LN2(z)): one absorbed head of width C
-    StkGemmArgs c = p;
-    c.ln_g = ly.ln_g[1];
-    c.ln_b = ly.ln_b[1];
-    c.WT = ly.WqcT;
-    c.N = S->d_kv;
-    c.K = C;
-    c.out = w + L.qc;
-    c.scale = (float)(log2e / sqrt((double)C));
-    if (e == hipSuccess) e = rs3_launch_stack_gemm(c, STK_A_LN, STK_E_STORE, st);
     if (e == hipSuccess) e = rs3_launch_attn(ac, abc, st, false);
-    StkGemmArgs mc = p;
-    mc.K = S->d_kv;
-    mc.S = S_c;
-    mc.H_att = 1;
-    mc.d_att = S->d_kv;
-    mc.out = w + L.qc;
-    if (e == hipSuccess) e = rs3_launch_stack_merge(mc, st);
-    StkGemmArgs v = p;
-    v.A = w + L.qc;
-    v.WT = ly.WvoT;
-    v.N = C;
-    v.K = S->d_kv;
-    if (e == hipSuccess) e = rs3_launch_stack_gemm(v, STK_A_BF16, STK_E_RESID, st);
-    // z += relu(LN3(z) W_1) W_2; after the last layer the rows go to Y
-    StkGemmArgs m1 = p;
-    m1.ln_g = ly.ln_g[2];
-    m1.ln_b = ly.ln_b[2];
-    m1.WT = ly.W1T;
-    m1.N = S->F;
-    m1.K = C;
-    m1.out = w + L.hbuf;
-    m1.scale = 1.f;
-    m1.relu = 1;
-    if (e == hipSuccess) e = rs3_launch_stack_gemm(m1, STK_A_LN, STK_E_STORE, st);
-    StkGemmArgs m2 = p;
-    m2.A = w + L.hbuf;
-    m2.WT = ly.W2T;
-    m2.N = C;
-    m2.K = S->F;
-    if (e == hipSuccess) e = rs3_launch_stack_gemm(m2, STK_A_BF16, last ? STK_E_SCATTER : STK_E_RESID, st);
+    q.S = S_c;
+    q.H_att = 1;
+    q.d_att = S->d_kv;
+    q.D_att = S->d_kv;
+    q.mout = p.Qc;
+    if (e == hipSuccess) e = rs3_launch_stack_merge(q, st);
+    // z += relu(LN3(z) W_1) W_2 in hidden chunks, summed with the next LN1
+    // (or, after the last layer, with the scatter to Y)
+    if (e == hipSuccess) e = rs3_launch_stack_mlp(q, st);
+    const bool last = l == S->n_layers - 1;
+    if (!last) {
+      q.ln_g = S->layers[l + 1].ln_g[0];
+      q.ln_b = S->layers[l + 1].ln_b[0];
+    }
+    if (e == hipSuccess) e = rs3_launch_stack_rows(q, last ? 2 : 1, st);
   }
   return map_err(e);
 }

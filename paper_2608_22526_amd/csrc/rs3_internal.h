@@ -246,43 +246,44 @@ struct AttendPrepArgs {
   int n_q, H, d_h, ntile;
 };
 
-// One matrix product of the memory-attention stack (k_stk_gemm): out = A W
-// over the kept rows, A [M][K] from one of the prologues, W given
-// transposed as WT [N][K].
-enum StkAMode { STK_A_BF16 = 0, STK_A_LN = 1, STK_A_GLN = 2 };
-//  BF16 : A rows of a bf16 buffer [M][K] (K a multiple of 64)
-//  LN   : LayerNorm (gain ln_g, shift ln_b) of the fp32 stream rows Z [M][256]
-//  GLN  : the same of the kept cells X[sel[r]] of the bf16 grid, which also
-//         become the stream rows (Zw)
-enum StkEMode { STK_E_STORE = 0, STK_E_RESID = 1, STK_E_SCATTER = 2, STK_E_QKV = 3 };
-//  STORE  : out [M][N] bf16 = scale * (A W), with relu if set
-//  RESID  : Zw [M][256] += A W
-//  SCATTER: Y[sel[r]] = Z[r] + (A W)[r] (bf16 or fp32 Y [mn][256])
-//  QKV    : N = 768; columns [0,256) -> Qs [M][256] (times scale), [256,512)
-//           -> the self-attention's K^ tiles, [512,768) -> its V^ tiles; with
-//           write_bank, work-group (0,0) also writes that bank's descriptor,
-//           header and tile list from the device count
-struct StkGemmArgs {
-  const void* A;
-  const float* Z;
-  float* Zw;
-  const float* ln_g;
-  const float* ln_b;
-  const void* X;
-  const int32_t* sel;
-  const rs3::bf16_t* Opart;   // [S][M][K]  (k_stk_merge: the attention's key splits,
-  const float* ML;            // [S][M][H_att][2]   H_att heads of width d_att = K / H_att)
-  int S, H_att, d_att;
-  const int32_t* count;       // kept rows (device), clamped into [0, M]
+// Arguments of the memory-attention stack's launches (stack.hip); every
+// launch reads the fields it needs.  n = the device count, clamped into
+// [0, M]; row-indexed buffers hold M rows.
+struct StkArgs {
+  const int32_t* count;       // kept rows (device)
   int32_t* err_hdr;           // header of the bank whose error word takes the reports
-  const rs3::bf16_t* WT;      // [N][K]
-  int M, N, K, mn;
-  float scale;
-  int relu;
-  void* out;
-  void* Y;
+  const int32_t* sel;         // kept cells (gather, scatter)
+  int M, mn;
+  const void* X;              // bf16 grid [mn][256]
+  void* Y;                    // bf16 or fp32 grid [mn][256]
   int y_f32;
-  rs3::bf16_t* Qs;
+  float* Z;                   // [M][256] residual stream
+  float* Zp;                  // [M][256] stream after the cross-attention
+  float* P;                   // [NC][M][256] MLP partials, one per 256 hidden units
+  int NC, F;
+  rs3::bf16_t* A1;            // [M][256] LN1 rows, the QKV product's input
+  const float* ln_g;          // the norm of k_stk_rows (LN1 of the layer it feeds)
+  const float* ln_b;
+  const float* ln2_g;
+  const float* ln2_b;
+  const float* ln3_g;
+  const float* ln3_b;
+  rs3::bf16_t* Qs;            // [M][256] self-attention queries, then its merged output
+  rs3::bf16_t* Qc;            // [M][64] cross-attention queries, then its merged output
+  // packed weights (MFMA B-operand order, see pack_b)
+  const rs3::bf16_t* Wqkv;    // [256][768]
+  const rs3::bf16_t* Wos;     // [256][256]
+  const rs3::bf16_t* Wqc;     // [256][64]   W_q W_k^T
+  const rs3::bf16_t* Wvo;     // [64][256]   W_v W_o
+  const rs3::bf16_t* W1;      // [256][F]
+  const rs3::bf16_t* W2;      // [F][256]
+  float qscale_s, qscale_c;   // log2(e) / sqrt(head width)
+  // split merge (k_stk_merge): Opart [S][M][D_att], ML [S][M][H_att][2]
+  const rs3::bf16_t* Opart;
+  const float* ML;
+  int S, H_att, d_att, D_att;
+  rs3::bf16_t* mout;          // [M][D_att]
+  // the self-attention's one-frame bank
   rs3::bf16_t* Kh;            // [ntile_cap][Hs][64][dhs]
   rs3::bf16_t* Vh;            // [ntile_cap][Hs][dhs][64] (slot order)
   rs3::TileEnt* tiles;        // [ntile_cap]
@@ -347,12 +348,16 @@ void rs3_prof_end(int id, hipStream_t st);
     hipLaunchKernelGGL(__VA_ARGS__); \
     rs3_prof_end((ID), (ST));    \
   } while (0)
-// Stack products (k_stk_gemm with prologue am and epilogue em) and the
-// X -> Y copy of the grid (bf16 -> bf16 or fp32) before the scatter.
-hipError_t rs3_launch_stack_gemm(const StkGemmArgs& p, int am, int em, hipStream_t st);
-// Merge of the attention's key splits (Opart, ML, S, H_att, d_att, K = the
-// attention width) into the normalised bf16 rows `out` [M][K].
-hipError_t rs3_launch_stack_merge(const StkGemmArgs& p, hipStream_t st);
+// The stack's launches (stack.hip): k_stk_rows (mode 0 gather + LN1,
+// 1 partial sum + LN1, 2 partial sum + scatter), the QKV product, the
+// post-self-attention block, the MLP chunks, the split merge and the
+// X -> Y copy before the scatter.
+hipError_t rs3_launch_stack_rows(const StkArgs& p, int mode, hipStream_t st);
+hipError_t rs3_launch_stack_qkv(const StkArgs& p, hipStream_t st);
+hipError_t rs3_launch_stack_post_sa(const StkArgs& p, hipStream_t st);
+hipError_t rs3_launch_stack_mlp(const StkArgs& p, hipStream_t st);
+hipError_t rs3_launch_stack_merge(const StkArgs& p, hipStream_t st);
 hipError_t rs3_launch_stack_copy(const void* X, void* Y, int64_t elems, int y_f32, hipStream_t st);
+hipError_t rs3_stack_setup();
 hipError_t rs3_select_setup();
 hipError_t rs3_commit_setup();

@@ -5,7 +5,8 @@
 //     z += SA(LN1(z))  among the kept rows      (one-frame bank of the kept rows)
 //     z += CA(LN2(z))  against the memory bank  (the readout of Eq. 6, absorbed)
 //     z += W2 relu(W1 LN3(z))
-// with the residual stream z in fp32 and every matrix product on bf16 MFMA.
+// with the residual stream z in fp32 and every matrix product on bf16 MFMA
+// (32x32x16, fp32 accumulation).
 //
 // The attentions run on the readout's split-KV attention kernel unchanged.
 // The self-attention's keys and values are laid out by the QKV product's
@@ -14,20 +15,28 @@
 // of one absorbed head uses as they are (W_q W_k^T on the query side,
 // W_v W_o on the output side), so one bank serves every layer.
 //
-// Every product is one launch of k_stk_gemm: a 64x64 output tile per
-// work-group of four waves (one 32x32 MFMA tile each), the A operand staged
-// in LDS by one of the prologues, B read from the transposed weights W^T
-// [N][K] (16-byte runs along K).
+// Launches of one layer (n kept rows; the first layer's LN1 comes from the
+// gather launch, every later one from the previous layer's last launch):
+//   k_stk_qkv      64x64 tiles: LN1 rows x [W_qs | W_ks | W_vs] -> queries,
+//                  key and value tiles of the self-attention's bank
+//   k_attn         self-attention; k_stk_merge merges its key splits
+//   k_stk_post_sa  32 whole rows per work-group: z += O W_os, LN2, queries of
+//                  the cross-attention (x W_q W_k^T)
+//   k_attn         cross-attention; k_stk_merge merges its key splits
+//   k_stk_mlp      64 rows x 256 hidden units per work-group: z' = z + O W_vo
+//                  (kept by the first hidden chunk), LN3, relu(. W_1[:, chunk])
+//                  W_2[chunk, :] -> an fp32 partial per chunk
+//   k_stk_rows     z = z' + the partials in chunk order, then the next
+//                  layer's LN1, or after the last layer the scatter to Y
+// Weights are stored in MFMA operand order (pack_b on the host): the B
+// operand of one 32-column block and one 16-deep step is 64 lanes x 16
+// bytes, contiguous, so every weight load of a wave is one 1 KB run.
 #include "device_util.h"
 
 namespace rs3 {
 
-constexpr int SG_BM = 64;    // rows per work-group (= keys per bank tile)
-constexpr int SG_BN = 64;    // columns per work-group
-constexpr int SG_KC = 256;   // contraction chunk staged in LDS
-constexpr int SG_PITCH = SG_KC + 8;   // bf16 elements per LDS row
-constexpr size_t SG_LDS = (size_t)SG_BM * SG_PITCH * 2;
 constexpr int SG_C = 256;    // d_model of the stack
+constexpr int SG_PITCH = SG_C + 8;   // bf16 elements per LDS row of a 256-wide A operand
 constexpr float SG_LN_EPS = 1e-5f;
 
 template <int CTRL>
@@ -50,9 +59,30 @@ __device__ __forceinline__ float wave_sum(float v) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// B operand of the packed weight Wp (KS 16-deep steps) for 32-column block
+// nb and step ks: lane l holds column 32*nb + l%32, rows 16*ks + 8*(l/32) .. +7.
+__device__ __forceinline__ u32x4 ldb(const bf16_t* Wp, int KS, int nb, int ks, int lane) {
+  return gload((const u32x4*)(Wp + (((int64_t)nb * KS + ks) * 64 + lane) * 8));
+}
+
+// A operand from a row-major LDS tile: rows r0 + l%32, columns 16*ks + 8*(l/32) .. +7.
+__device__ __forceinline__ u32x4 lda(const bf16_t* As, int pitch, int r0, int ks, int lane) {
+  return *(const u32x4*)(As + (r0 + (lane & 31)) * pitch + 16 * ks + 8 * (lane >> 5));
+}
+
+// LayerNorm of one 256-wide row held 4 channels per lane (every lane of the
+// wave holds a quarter-row slice), with gain g and shift b: bf16 pairs.
+__device__ __forceinline__ u32x2 ln_row(f32x4 z, const f32x4& g, const f32x4& b) {
+  const float mean = wave_sum(z[0] + z[1] + z[2] + z[3]) * (1.f / SG_C);
+  z -= mean;
+  const float var = wave_sum(z[0] * z[0] + z[1] * z[1] + z[2] * z[2] + z[3] * z[3]) * (1.f / SG_C);
+  const f32x4 y = z * (1.f / sqrtf(var + SG_LN_EPS)) * g + b;
+  return u32x2{pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3])};
+}
+
 // Kept-row count of the call, clamped into [0, M]; a count outside that
 // range is reported in the bank's error word by work-group (0, 0).
-__device__ __forceinline__ int stk_count(const StkGemmArgs& p) {
+__device__ __forceinline__ int stk_count(const StkArgs& p) {
   int cnt = gload(p.count);
   if (cnt < 0 || cnt > p.M) {
     if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) set_err(p.err_hdr, RS3_E_INVALID);
@@ -63,72 +93,22 @@ __device__ __forceinline__ int stk_count(const StkGemmArgs& p) {
 
 // Cell of kept row r, or -1 for an entry out of range or not above its
 // predecessor (such rows are reported and never written to Y).
-__device__ __forceinline__ int stk_cell(const StkGemmArgs& p, int r) {
+__device__ __forceinline__ int stk_cell(const StkArgs& p, int r) {
   const int i = gload(p.sel + r);
   const int prev = r > 0 ? gload(p.sel + r - 1) : -1;
   return (i >= 0 && i < p.mn && prev < i) ? i : -1;
 }
 
 // ---- prologues: the A chunk [64][kn] of rows row0.. in LDS (bf16) ----------
-// LayerNorm of the fp32 rows of Z (GATHER: of the kept cells of the bf16
-// grid X, and the column-block-0 work-group stores them to Z): each wave
-// normalises 16 rows, a lane holding 4 channels.  Rows past the count are
-// computed on a clamped row and stored as zero, so the 16 reductions carry
-// no branch and interleave.
-template <bool GATHER>
-__device__ __forceinline__ void pro_ln(const StkGemmArgs& p, int row0, int cnt, bf16_t* As) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  f32x4 z[16];
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int r = min(row0 + 16 * wave + i, cnt - 1);
-    if constexpr (GATHER) {
-      const int cell = stk_cell(p, r);
-      if (cell < 0 && blockIdx.y == 0 && lane == 0) set_err(p.err_hdr, RS3_E_INVALID);
-      const u32x2 v = gload((const u32x2*)((const bf16_t*)p.X + (int64_t)max(cell, 0) * SG_C + 4 * lane));
-      z[i] = f32x4{__uint_as_float(v[0] << 16), __uint_as_float(v[0] & 0xffff0000u), __uint_as_float(v[1] << 16),
-                   __uint_as_float(v[1] & 0xffff0000u)};
-    } else {
-      z[i] = gload((const f32x4*)(p.Z + (int64_t)r * SG_C + 4 * lane));
-    }
-  }
-  const f32x4 g = gload((const f32x4*)(p.ln_g + 4 * lane));
-  const f32x4 b = gload((const f32x4*)(p.ln_b + 4 * lane));
-  if constexpr (GATHER) {
-    if (blockIdx.y == 0) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i)
-        if (row0 + 16 * wave + i < cnt) *(f32x4*)(p.Zw + (int64_t)(row0 + 16 * wave + i) * SG_C + 4 * lane) = z[i];
-    }
-  }
-  float sm[16];
-#pragma unroll
-  for (int i = 0; i < 16; ++i) sm[i] = wave_sum(z[i][0] + z[i][1] + z[i][2] + z[i][3]);
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    z[i] -= sm[i] * (1.f / SG_C);
-    sm[i] = wave_sum(z[i][0] * z[i][0] + z[i][1] * z[i][1] + z[i][2] * z[i][2] + z[i][3] * z[i][3]);
-  }
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int lr = 16 * wave + i;
-    const float rs = 1.f / sqrtf(sm[i] * (1.f / SG_C) + SG_LN_EPS);
-    const f32x4 y = z[i] * rs * g + b;
-    u32x2 o = {pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3])};
-    if (row0 + lr >= cnt) o = u32x2{0, 0};
-    *(u32x2*)(As + lr * SG_PITCH + 4 * lane) = o;
-  }
-}
-
-// grid ceil(M*K/8 / 256), block 256: one thread per (kept row, 8 columns)
+// grid ceil(M*D_att/8 / 256), block 256: one thread per (kept row, 8 columns)
 // merges the attention's key splits (partials O/l and (m, l) per split, row
-// and head: Opart [S][M][K], ML [S][M][H_att][2]) by log-sum-exp into the
-// normalised bf16 rows out [M][K].  The splits are loaded eight at a time
+// and head: Opart [S][M][D_att], ML [S][M][H_att][2]) by log-sum-exp into the
+// normalised bf16 rows mout [M][D_att].  The splits are loaded eight at a time
 // without branches (split indices past S re-read the last split and are
 // masked); a split without keys holds l = 0 and adds nothing, its O words
 // (never written) replaced by zero; a row with no key at all gets O = 0.
-__global__ __launch_bounds__(256) void k_stk_merge(StkGemmArgs p) {
-  const int D = p.K, cpr = D / 8;
+__global__ __launch_bounds__(256) void k_stk_merge(StkArgs p) {
+  const int D = p.D_att, cpr = D / 8;
   const int64_t it = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (it >= (int64_t)p.M * cpr) return;
   const int row = (int)(it / cpr), d0 = 8 * (int)(it - (int64_t)row * cpr), h = d0 / p.d_att;
@@ -176,13 +156,13 @@ __global__ __launch_bounds__(256) void k_stk_merge(StkGemmArgs p) {
   u32x4 out;
 #pragma unroll
   for (int e = 0; e < 4; ++e) out[e] = pack_bf16x2(acc[2 * e] * inv, acc[2 * e + 1] * inv);
-  *(u32x4*)((bf16_t*)p.out + (int64_t)row * D + d0) = out;
+  *(u32x4*)(p.mout + (int64_t)row * D + d0) = out;
 }
 
 // The self-attention's one-frame bank: descriptor, header (tile and key
 // counts from the device count) and tile list, by work-group (0, 0) of the
 // first layer's QKV product.
-__device__ __forceinline__ void write_self_bank(const StkGemmArgs& p, int cnt) {
+__device__ __forceinline__ void write_self_bank(const StkArgs& p, int cnt) {
   const int tid = threadIdx.x;
   const int ntiles = (cnt + KT - 1) / KT;
   if (tid == 0) {
@@ -218,137 +198,363 @@ __device__ __forceinline__ void write_self_bank(const StkGemmArgs& p, int cnt) {
   }
 }
 
-// grid (ceil(M/64), N/64), block 256, LDS SG_LDS.
-template <int AM, int EM>
-__global__ __launch_bounds__(256) void k_stk_gemm(StkGemmArgs p) {
-  extern __shared__ __attribute__((aligned(16))) uint8_t lds_raw[];
-  bf16_t* As = (bf16_t*)lds_raw;
-  const int row0 = blockIdx.x * SG_BM, col0 = blockIdx.y * SG_BN;
+// grid ceil(n/4), block 256: one row per wave, 4 channels per lane.
+//  ROWS_GATHER: z = X[sel[r]] (the gather; invalid entries are reported)
+//  ROWS_REDUCE: z = z' + P[0] + P[1] + ... (the MLP's chunk partials, in order)
+//  both       : Z[r] = z and A1[r] = LN(z) (the next QKV product's rows)
+//  ROWS_FINAL : z as in REDUCE, scattered to Y[sel[r]] (bf16 or fp32)
+enum { ROWS_GATHER = 0, ROWS_REDUCE = 1, ROWS_FINAL = 2 };
+template <int MODE>
+__global__ __launch_bounds__(256) void k_stk_rows(StkArgs p) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int cnt = stk_count(p);
+  const int r = blockIdx.x * 4 + wave;
+  if (r >= cnt) return;
+  const int64_t off = (int64_t)r * SG_C + 4 * lane;
+  f32x4 z;
+  int cell = 0;
+  if constexpr (MODE != ROWS_REDUCE) cell = stk_cell(p, r);
+  if constexpr (MODE == ROWS_GATHER) {
+    if (cell < 0 && lane == 0) set_err(p.err_hdr, RS3_E_INVALID);
+    const u32x2 v = gload((const u32x2*)((const bf16_t*)p.X + (int64_t)max(cell, 0) * SG_C + 4 * lane));
+    z = f32x4{__uint_as_float(v[0] << 16), __uint_as_float(v[0] & 0xffff0000u), __uint_as_float(v[1] << 16),
+              __uint_as_float(v[1] & 0xffff0000u)};
+  } else {
+    constexpr int B = 8;   // partials loaded per batch
+    z = gload((const f32x4*)(p.Zp + off));
+    for (int c0 = 0; c0 < p.NC; c0 += B) {
+      f32x4 pc[B];
+#pragma unroll
+      for (int c = 0; c < B; ++c)
+        if (c0 + c < p.NC) pc[c] = gload((const f32x4*)(p.P + (int64_t)(c0 + c) * p.M * SG_C + off));
+#pragma unroll
+      for (int c = 0; c < B; ++c)
+        if (c0 + c < p.NC) z += pc[c];
+    }
+  }
+  if constexpr (MODE == ROWS_FINAL) {
+    if (cell < 0) return;
+    const int64_t yo = (int64_t)cell * SG_C + 4 * lane;
+    if (p.y_f32)
+      *(f32x4*)((float*)p.Y + yo) = z;
+    else
+      *(u32x2*)((bf16_t*)p.Y + yo) = u32x2{pack_bf16x2(z[0], z[1]), pack_bf16x2(z[2], z[3])};
+  } else {
+    const f32x4 g = gload((const f32x4*)(p.ln_g + 4 * lane));
+    const f32x4 b = gload((const f32x4*)(p.ln_b + 4 * lane));
+    *(f32x4*)(p.Z + off) = z;
+    *(u32x2*)(p.A1 + off) = ln_row(z, g, b);
+  }
+}
+
+// grid (ceil(n/64), 12), block 256: the 64x64 output tile (blockIdx.x,
+// blockIdx.y) of A1 [n][256] x [W_qs | W_ks | W_vs]; each wave one 32x32
+// MFMA tile.  Columns [0, 256) -> Qs (times qscale_s), [256, 512) -> the
+// key tile blockIdx.x of the self-attention's bank ([H][64][d_h], rows past
+// the count zero), [512, 768) -> its value tile ([H][d_h][64] in slot order).
+// With write_bank, work-group (0, 0) also writes that bank's descriptor,
+// header and tile list from the device count.
+__global__ __launch_bounds__(256) void k_stk_qkv(StkArgs p) {
+  __shared__ __attribute__((aligned(16))) bf16_t As[64 * SG_PITCH];
+  const int row0 = blockIdx.x * 64, col0 = blockIdx.y * 64;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5;
   const int cnt = stk_count(p);
-  if constexpr (EM == STK_E_QKV) {
-    if (p.write_bank && blockIdx.x == 0 && blockIdx.y == 0) write_self_bank(p, cnt);
-  }
+  if (p.write_bank && blockIdx.x == 0 && blockIdx.y == 0) write_self_bank(p, cnt);
   if (row0 >= cnt) return;
   const int wr = wave & 1, wc = wave >> 1;
-  const int col = col0 + 32 * wc + (lane & 31);
-  const bf16_t* wrow = p.WT + (int64_t)col * p.K;
+  const int nb = (col0 >> 5) + wc;
+  u32x4 bw[16];
+#pragma unroll
+  for (int ks = 0; ks < 16; ++ks) bw[ks] = ldb(p.Wqkv, 16, nb, ks, lane);
+  u32x4 av[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int u = tid + 256 * j, r = u >> 5, c8 = u & 31;
+    av[j] = gload((const u32x4*)(p.A1 + (int64_t)min(row0 + r, cnt - 1) * SG_C + 8 * c8));
+  }
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int u = tid + 256 * j, r = u >> 5, c8 = u & 31;
+    *(u32x4*)(As + r * SG_PITCH + 8 * c8) = row0 + r < cnt ? av[j] : u32x4{0, 0, 0, 0};
+  }
+  __syncthreads();
   f32x16 acc = {};
-  if constexpr (AM == STK_A_BF16) {
-    // register double buffer: chunk kc+1's A rows and B operands are in
-    // flight while chunk kc is multiplied
-    constexpr int AU = SG_BM * SG_KC / 8 / 256;   // 16-byte A units per thread and chunk
-    u32x4 av[AU], bw[SG_KC / 16];
-    auto load = [&](int kc) {
-      const int kn = min(SG_KC, p.K - kc), cpr = kn / 8;
 #pragma unroll
-      for (int j = 0; j < AU; ++j) {
-        const int u = threadIdx.x + 256 * j, r = u / cpr, c8 = u - r * cpr;
-        const int rr = min(row0 + r, cnt - 1);
-        if (u < SG_BM * cpr) av[j] = gload((const u32x4*)((const bf16_t*)p.A + (int64_t)rr * p.K + kc + 8 * c8));
-      }
+  for (int ks = 0; ks < 16; ++ks) acc = mfma32(lda(As, SG_PITCH, 32 * wr, ks, lane), bw[ks], acc);
+  const int col = col0 + 32 * wc + (lane & 31);
+  const int rbase = row0 + 32 * wr;
+  const int region = col0 / SG_C, c = col - region * SG_C;
+  const int h = c / p.dhs, d = c - h * p.dhs;
+  if (region == 0) {
 #pragma unroll
-      for (int ks = 0; ks < SG_KC / 16; ++ks)
-        if (16 * ks < kn) bw[ks] = gload((const u32x4*)(wrow + kc + 16 * ks + 8 * g));
-    };
-    load(0);
-    for (int kc = 0; kc < p.K; kc += SG_KC) {
-      const int kn = min(SG_KC, p.K - kc), cpr = kn / 8;
-      if (kc > 0) __syncthreads();   // the previous chunk's operands are read
+    for (int r = 0; r < 16; ++r) {
+      const int row = rbase + c_row(r, lane);
+      if (row < cnt) p.Qs[(int64_t)row * SG_C + c] = f2bf(acc[r] * p.qscale_s);
+    }
+  } else if (region == 1) {
+    bf16_t* kt = p.Kh + ((int64_t)blockIdx.x * p.Hs + h) * KT * p.dhs + d;
 #pragma unroll
-      for (int j = 0; j < AU; ++j) {
-        const int u = threadIdx.x + 256 * j, r = u / cpr, c8 = u - r * cpr;
-        if (u < SG_BM * cpr) *(u32x4*)(As + r * SG_PITCH + 8 * c8) = row0 + r < cnt ? av[j] : u32x4{0, 0, 0, 0};
-      }
-      u32x4 bc[SG_KC / 16];
-#pragma unroll
-      for (int ks = 0; ks < SG_KC / 16; ++ks) bc[ks] = bw[ks];
-      __syncthreads();
-      if (kc + SG_KC < p.K) load(kc + SG_KC);
-      const bf16_t* arow = As + (32 * wr + (lane & 31)) * SG_PITCH + 8 * g;
-#pragma unroll
-      for (int ks = 0; ks < SG_KC / 16; ++ks)
-        if (16 * ks < kn) acc = mfma32(*(const u32x4*)(arow + 16 * ks), bc[ks], acc);
+    for (int r = 0; r < 16; ++r) {
+      const int j = 32 * wr + c_row(r, lane);
+      kt[j * p.dhs] = row0 + j < cnt ? f2bf(acc[r]) : (bf16_t)0;
     }
   } else {
-    // LayerNorm prologues: K = d_model = one chunk
-    u32x4 bw[SG_KC / 16];
+    // the eight results r = 0..7 (and 8..15) of a lane are keys whose V^
+    // slots are 32*wr + 8*g + r (+16): one 16-byte store each
+    bf16_t* vt = p.Vh + (((int64_t)blockIdx.x * p.Hs + h) * p.dhs + d) * KT + 32 * wr + 8 * g;
 #pragma unroll
-    for (int ks = 0; ks < SG_KC / 16; ++ks) bw[ks] = gload((const u32x4*)(wrow + 16 * ks + 8 * g));
-    if constexpr (AM == STK_A_LN) pro_ln<false>(p, row0, cnt, As);
-    if constexpr (AM == STK_A_GLN) pro_ln<true>(p, row0, cnt, As);
-    __syncthreads();
-    const bf16_t* arow = As + (32 * wr + (lane & 31)) * SG_PITCH + 8 * g;
+    for (int hf = 0; hf < 2; ++hf) {
+      u32x4 pk;
 #pragma unroll
-    for (int ks = 0; ks < SG_KC / 16; ++ks) acc = mfma32(*(const u32x4*)(arow + 16 * ks), bw[ks], acc);
-  }
-  const int rbase = row0 + 32 * wr;
-  if constexpr (EM == STK_E_STORE) {
-    bf16_t* out = (bf16_t*)p.out;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = rbase + c_row(r, lane);
-      if (row >= cnt) continue;
-      float v = acc[r] * p.scale;
-      if (p.relu) v = fmaxf(v, 0.f);
-      out[(int64_t)row * p.N + col] = f2bf(v);
-    }
-  } else if constexpr (EM == STK_E_RESID) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = rbase + c_row(r, lane);
-      if (row >= cnt) continue;
-      float* zp = p.Zw + (int64_t)row * SG_C + col;
-      *zp = *zp + acc[r];
-    }
-  } else if constexpr (EM == STK_E_SCATTER) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = rbase + c_row(r, lane);
-      if (row >= cnt) continue;
-      const int cell = stk_cell(p, row);
-      if (cell < 0) continue;
-      const float y = p.Z[(int64_t)row * SG_C + col] + acc[r];
-      if (p.y_f32)
-        ((float*)p.Y)[(int64_t)cell * SG_C + col] = y;
-      else
-        ((bf16_t*)p.Y)[(int64_t)cell * SG_C + col] = f2bf(y);
-    }
-  } else {   // STK_E_QKV: columns [0, C) queries, [C, 2C) keys, [2C, 3C) values
-    const int region = col0 / SG_C, c = col - region * SG_C;
-    const int h = c / p.dhs, d = c - h * p.dhs;
-    if (region == 0) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = rbase + c_row(r, lane);
-        if (row < cnt) p.Qs[(int64_t)row * SG_C + c] = f2bf(acc[r] * p.scale);
+      for (int e = 0; e < 4; ++e) {
+        const int q0 = 8 * hf + 2 * e;
+        const float v0 = rbase + c_row(q0, lane) < cnt ? acc[q0] : 0.f;
+        const float v1 = rbase + c_row(q0 + 1, lane) < cnt ? acc[q0 + 1] : 0.f;
+        pk[e] = pack_bf16x2(v0, v1);
       }
-    } else if (region == 1) {
-      // K^ tile rb: [H][64][d_h], rows past the count zero
-      bf16_t* kt = p.Kh + ((int64_t)blockIdx.x * p.Hs + h) * KT * p.dhs + d;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int j = 32 * wr + c_row(r, lane);
-        kt[j * p.dhs] = row0 + j < cnt ? f2bf(acc[r]) : (bf16_t)0;
-      }
-    } else {
-      // V^ tile rb: [H][d_h][64] in slot order; the eight results r = 0..7
-      // (and 8..15) of a lane are keys whose slots are 32*wr + 8*g + r (+16)
-      bf16_t* vt = p.Vh + (((int64_t)blockIdx.x * p.Hs + h) * p.dhs + d) * KT + 32 * wr + 8 * g;
-#pragma unroll
-      for (int hf = 0; hf < 2; ++hf) {
-        u32x4 pk;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r0 = 8 * hf + 2 * e;
-          const float v0 = rbase + c_row(r0, lane) < cnt ? acc[r0] : 0.f;
-          const float v1 = rbase + c_row(r0 + 1, lane) < cnt ? acc[r0 + 1] : 0.f;
-          pk[e] = pack_bf16x2(v0, v1);
-        }
-        *(u32x4*)(vt + 16 * hf) = pk;
-      }
+      *(u32x4*)(vt + 16 * hf) = pk;
     }
   }
+}
+
+// grid ceil(n/32), block 256, LDS PS_LDS: 32 whole rows per work-group.
+//   z += O W_os  (O: the self-attention's merged output, in Qs)
+//   Qc = qscale_c * LN2(z) (W_q W_k^T)
+// Wave w holds output columns [64w, 64w+64) of the first product (two
+// 32x32 tiles); waves 0 and 1 take the two 32-column blocks of the second.
+constexpr size_t PS_O = 0, PS_Z = 32 * SG_PITCH * 2, PS_A = PS_Z + 32 * SG_C * 4;
+constexpr size_t PS_LDS = PS_A + 32 * SG_PITCH * 2;
+__global__ __launch_bounds__(256) void k_stk_post_sa(StkArgs p) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  bf16_t* Os = (bf16_t*)(lds + PS_O);
+  float* Zs = (float*)(lds + PS_Z);
+  bf16_t* As = (bf16_t*)(lds + PS_A);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int row0 = blockIdx.x * 32;
+  const int cnt = stk_count(p);
+  if (row0 >= cnt) return;
+  u32x4 bo[2][16];
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int ks = 0; ks < 16; ++ks) bo[t][ks] = ldb(p.Wos, 16, 2 * wave + t, ks, lane);
+  u32x4 ov[4];
+  f32x4 zv[8];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int u = tid + 256 * j, r = u >> 5, c8 = u & 31;
+    ov[j] = gload((const u32x4*)(p.Qs + (int64_t)min(row0 + r, cnt - 1) * SG_C + 8 * c8));
+  }
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int u = tid + 256 * j, r = u >> 6, c4 = u & 63;
+    zv[j] = gload((const f32x4*)(p.Z + (int64_t)min(row0 + r, cnt - 1) * SG_C + 4 * c4));
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int u = tid + 256 * j, r = u >> 5, c8 = u & 31;
+    *(u32x4*)(Os + r * SG_PITCH + 8 * c8) = row0 + r < cnt ? ov[j] : u32x4{0, 0, 0, 0};
+  }
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int u = tid + 256 * j, r = u >> 6, c4 = u & 63;
+    *(f32x4*)(Zs + r * SG_C + 4 * c4) = zv[j];
+  }
+  __syncthreads();
+  f32x16 acc[2] = {};
+#pragma unroll
+  for (int ks = 0; ks < 16; ++ks) {
+    const u32x4 a = lda(Os, SG_PITCH, 0, ks, lane);
+    acc[0] = mfma32(a, bo[0][ks], acc[0]);
+    acc[1] = mfma32(a, bo[1][ks], acc[1]);
+  }
+  // the cross-attention's W_q W_k^T operands (waves 0 and 1), in flight over the norm
+  u32x4 bq[16];
+  if (wave < 2) {
+#pragma unroll
+    for (int ks = 0; ks < 16; ++ks) bq[ks] = ldb(p.Wqc, 16, wave, ks, lane);
+  }
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) Zs[c_row(r, lane) * SG_C + 64 * wave + 32 * t + (lane & 31)] += acc[t][r];
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int u = tid + 256 * j, r = u >> 6, c4 = u & 63;
+    if (row0 + r < cnt) *(f32x4*)(p.Z + (int64_t)(row0 + r) * SG_C + 4 * c4) = *(const f32x4*)(Zs + r * SG_C + 4 * c4);
+  }
+  {
+    const f32x4 g = gload((const f32x4*)(p.ln2_g + 4 * lane));
+    const f32x4 b = gload((const f32x4*)(p.ln2_b + 4 * lane));
+    f32x4 zz[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) zz[i] = *(const f32x4*)(Zs + (8 * wave + i) * SG_C + 4 * lane);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      u32x2 y = ln_row(zz[i], g, b);
+      if (row0 + 8 * wave + i >= cnt) y = u32x2{0, 0};
+      *(u32x2*)(As + (8 * wave + i) * SG_PITCH + 4 * lane) = y;
+    }
+  }
+  __syncthreads();
+  if (wave < 2) {
+    f32x16 q = {};
+#pragma unroll
+    for (int ks = 0; ks < 16; ++ks) q = mfma32(lda(As, SG_PITCH, 0, ks, lane), bq[ks], q);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = row0 + c_row(r, lane);
+      if (row < cnt) p.Qc[(int64_t)row * 64 + 32 * wave + (lane & 31)] = f2bf(q[r] * p.qscale_c);
+    }
+  }
+}
+
+// grid (ceil(n/64), F/256), block 256, LDS ML_LDS: rows [64 bx, +64) and
+// hidden units [256 by, +256).
+//   z' = z + O W_vo            (O: the cross-attention's merged output, in Qc;
+//                               the chunk-0 work-group stores z' to Zp)
+//   P[by] = relu(LN3(z') W_1[:, chunk]) W_2[chunk, :]    (fp32)
+// Wave w holds output columns [64w, 64w+64) of every product, both 32-row
+// halves (four 32x32 tiles).  The hidden units reuse the LDS of z'.
+constexpr int ML_OP = 64 + 8;   // LDS pitch of the 64-wide O rows
+constexpr size_t ML_O = 0, ML_A = 64 * ML_OP * 2, ML_Z = ML_A + 64 * SG_PITCH * 2;
+constexpr size_t ML_LDS = ML_Z + 64 * SG_C * 4;
+__global__ __launch_bounds__(256) void k_stk_mlp(StkArgs p) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  bf16_t* Ob = (bf16_t*)(lds + ML_O);
+  bf16_t* As = (bf16_t*)(lds + ML_A);
+  float* Zs = (float*)(lds + ML_Z);
+  bf16_t* Hs = (bf16_t*)(lds + ML_Z);   // after LN3
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int row0 = blockIdx.x * 64, chunk = blockIdx.y;
+  const int cnt = stk_count(p);
+  if (row0 >= cnt) return;
+  u32x4 bv[2][4];
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) bv[t][ks] = ldb(p.Wvo, 4, 2 * wave + t, ks, lane);
+  u32x4 ov[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int u = tid + 256 * j, r = u >> 3, c8 = u & 7;
+    ov[j] = gload((const u32x4*)(p.Qc + (int64_t)min(row0 + r, cnt - 1) * 64 + 8 * c8));
+  }
+  f32x4 zv[16];
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    const int u = tid + 256 * j, r = u >> 6, c4 = u & 63;
+    zv[j] = gload((const f32x4*)(p.Z + (int64_t)min(row0 + r, cnt - 1) * SG_C + 4 * c4));
+  }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int u = tid + 256 * j, r = u >> 3, c8 = u & 7;
+    *(u32x4*)(Ob + r * ML_OP + 8 * c8) = row0 + r < cnt ? ov[j] : u32x4{0, 0, 0, 0};
+  }
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    const int u = tid + 256 * j, r = u >> 6, c4 = u & 63;
+    *(f32x4*)(Zs + r * SG_C + 4 * c4) = zv[j];
+  }
+  __syncthreads();
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int t = 0; t < 2; ++t) acc[i][t] = f32x16{};
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const u32x4 a = lda(Ob, ML_OP, 32 * i, ks, lane);
+#pragma unroll
+      for (int t = 0; t < 2; ++t) acc[i][t] = mfma32(a, bv[t][ks], acc[i][t]);
+    }
+  // W_1 operands of this hidden chunk, in flight over the residual and the norm
+  u32x4 bw[2][16];
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int ks = 0; ks < 16; ++ks) bw[t][ks] = ldb(p.W1, 16, 8 * chunk + 2 * wave + t, ks, lane);
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        Zs[(32 * i + c_row(r, lane)) * SG_C + 64 * wave + 32 * t + (lane & 31)] += acc[i][t][r];
+  __syncthreads();
+  if (chunk == 0) {
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int u = tid + 256 * j, r = u >> 6, c4 = u & 63;
+      if (row0 + r < cnt)
+        *(f32x4*)(p.Zp + (int64_t)(row0 + r) * SG_C + 4 * c4) = *(const f32x4*)(Zs + r * SG_C + 4 * c4);
+    }
+  }
+  {
+    const f32x4 g = gload((const f32x4*)(p.ln3_g + 4 * lane));
+    const f32x4 b = gload((const f32x4*)(p.ln3_b + 4 * lane));
+    f32x4 zz[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) zz[i] = *(const f32x4*)(Zs + (16 * wave + i) * SG_C + 4 * lane);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      u32x2 y = ln_row(zz[i], g, b);
+      if (row0 + 16 * wave + i >= cnt) y = u32x2{0, 0};
+      *(u32x2*)(As + (16 * wave + i) * SG_PITCH + 4 * lane) = y;
+    }
+  }
+  __syncthreads();   // LN3 rows complete; z' no longer read (its LDS takes the hidden units)
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int t = 0; t < 2; ++t) acc[i][t] = f32x16{};
+#pragma unroll
+  for (int ks = 0; ks < 16; ++ks)
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const u32x4 a = lda(As, SG_PITCH, 32 * i, ks, lane);
+#pragma unroll
+      for (int t = 0; t < 2; ++t) acc[i][t] = mfma32(a, bw[t][ks], acc[i][t]);
+    }
+  // W_2 operands: rows [256 chunk, +256) of W_2 are its steps [16 chunk, +16)
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int ks = 0; ks < 16; ++ks) bw[t][ks] = ldb(p.W2, p.F / 16, 2 * wave + t, 16 * chunk + ks, lane);
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        Hs[(32 * i + c_row(r, lane)) * SG_PITCH + 64 * wave + 32 * t + (lane & 31)] =
+            f2bf(fmaxf(acc[i][t][r], 0.f));
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int t = 0; t < 2; ++t) acc[i][t] = f32x16{};
+#pragma unroll
+  for (int ks = 0; ks < 16; ++ks)
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const u32x4 a = lda(Hs, SG_PITCH, 32 * i, ks, lane);
+#pragma unroll
+      for (int t = 0; t < 2; ++t) acc[i][t] = mfma32(a, bw[t][ks], acc[i][t]);
+    }
+  float* P = p.P + (int64_t)chunk * p.M * SG_C;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = row0 + 32 * i + c_row(r, lane);
+      if (row >= cnt) continue;
+#pragma unroll
+      for (int t = 0; t < 2; ++t) P[(int64_t)row * SG_C + 64 * wave + 32 * t + (lane & 31)] = acc[i][t][r];
+    }
 }
 
 // Y <- X for every cell (bf16 -> bf16 or fp32), 8 channels per thread.
@@ -372,33 +578,41 @@ __global__ __launch_bounds__(256) void k_stk_copy(const bf16_t* X, void* Y, int6
 
 using namespace rs3;
 
-template <int AM, int EM>
-static hipError_t launch_gemm(const StkGemmArgs& p, hipStream_t st) {
-  const dim3 grid((unsigned)((p.M + SG_BM - 1) / SG_BM), (unsigned)(p.N / SG_BN));
-  RS3_LAUNCH(RS3_K_STACK_GEMM, st, (k_stk_gemm<AM, EM>), grid, dim3(256), SG_LDS, st, p);
+hipError_t rs3_launch_stack_rows(const StkArgs& p, int mode, hipStream_t st) {
+  if (p.M <= 0) return hipSuccess;
+  const dim3 grid((unsigned)((p.M + 3) / 4));
+  if (mode == ROWS_GATHER)
+    RS3_LAUNCH(RS3_K_STACK_ROWS, st, k_stk_rows<ROWS_GATHER>, grid, dim3(256), 0, st, p);
+  else if (mode == ROWS_REDUCE)
+    RS3_LAUNCH(RS3_K_STACK_ROWS, st, k_stk_rows<ROWS_REDUCE>, grid, dim3(256), 0, st, p);
+  else
+    RS3_LAUNCH(RS3_K_STACK_ROWS, st, k_stk_rows<ROWS_FINAL>, grid, dim3(256), 0, st, p);
   return hipGetLastError();
 }
 
-hipError_t rs3_launch_stack_gemm(const StkGemmArgs& p, int am, int em, hipStream_t st) {
+hipError_t rs3_launch_stack_qkv(const StkArgs& p, hipStream_t st) {
   if (p.M <= 0) return hipSuccess;
-  if (p.N % SG_BN != 0 || p.K % 16 != 0) return hipErrorInvalidValue;
-  if ((am == STK_A_LN || am == STK_A_GLN) && p.K != SG_C) return hipErrorInvalidValue;
-  if (am == STK_A_BF16 && p.K % 64 != 0) return hipErrorInvalidValue;
-#define RS3_SG(A, E) \
-  if (am == A && em == E) return launch_gemm<A, E>(p, st);
-  RS3_SG(STK_A_GLN, STK_E_QKV)
-  RS3_SG(STK_A_LN, STK_E_QKV)
-  RS3_SG(STK_A_LN, STK_E_STORE)
-  RS3_SG(STK_A_BF16, STK_E_RESID)
-  RS3_SG(STK_A_BF16, STK_E_SCATTER)
-#undef RS3_SG
-  return hipErrorInvalidValue;
+  RS3_LAUNCH(RS3_K_STACK_GEMM, st, k_stk_qkv, dim3((unsigned)((p.M + 63) / 64), 3 * SG_C / 64), dim3(256), 0, st, p);
+  return hipGetLastError();
 }
 
-hipError_t rs3_launch_stack_merge(const StkGemmArgs& p, hipStream_t st) {
-  const int64_t items = (int64_t)p.M * (p.K / 8);
+hipError_t rs3_launch_stack_post_sa(const StkArgs& p, hipStream_t st) {
+  if (p.M <= 0) return hipSuccess;
+  RS3_LAUNCH(RS3_K_STACK_GEMM, st, k_stk_post_sa, dim3((unsigned)((p.M + 31) / 32)), dim3(256), PS_LDS, st, p);
+  return hipGetLastError();
+}
+
+hipError_t rs3_launch_stack_mlp(const StkArgs& p, hipStream_t st) {
+  if (p.M <= 0) return hipSuccess;
+  if (p.F % 256 != 0 || p.NC != p.F / 256) return hipErrorInvalidValue;
+  RS3_LAUNCH(RS3_K_STACK_MLP, st, k_stk_mlp, dim3((unsigned)((p.M + 63) / 64), p.NC), dim3(256), ML_LDS, st, p);
+  return hipGetLastError();
+}
+
+hipError_t rs3_launch_stack_merge(const StkArgs& p, hipStream_t st) {
+  const int64_t items = (int64_t)p.M * (p.D_att / 8);
   if (items == 0) return hipSuccess;
-  if (p.K % 8 != 0 || p.d_att % 8 != 0) return hipErrorInvalidValue;
+  if (p.D_att % 8 != 0 || p.d_att % 8 != 0) return hipErrorInvalidValue;
   RS3_LAUNCH(RS3_K_STACK_MERGE, st, k_stk_merge, dim3((unsigned)((items + 255) / 256)), dim3(256), 0, st, p);
   return hipGetLastError();
 }
@@ -412,4 +626,11 @@ hipError_t rs3_launch_stack_copy(const void* X, void* Y, int64_t elems, int y_f3
   else
     RS3_LAUNCH(RS3_K_COPY, st, k_stk_copy<false>, dim3(nb), dim3(256), 0, st, (const bf16_t*)X, Y, chunks);
   return hipGetLastError();
+}
+
+hipError_t rs3_stack_setup() {
+  hipError_t e = hipFuncSetAttribute((const void*)k_stk_mlp, hipFuncAttributeMaxDynamicSharedMemorySize, (int)ML_LDS);
+  if (e == hipSuccess)
+    e = hipFuncSetAttribute((const void*)k_stk_post_sa, hipFuncAttributeMaxDynamicSharedMemorySize, (int)PS_LDS);
+  return e;
 }
