@@ -323,20 +323,30 @@ def gpu_run(args):
     rs3.profile_enable(False)
     errs = [b.error() for b in sess.banks]
 
-    # executed attention flops: QK^T and PV at the attention width
+    # algorithmic attention flops (the method's work: QK^T and PV at the model
+    # width D = H*d_h, whatever width the kernel runs at) and executed flops
+    # (QK^T and PV at the kernel's attention width, plus the query projection
+    # when the attention kernel does it)
     Da = cfg.d_kv if absorb else cfg.D
     attn_ms, attn_n = rep["attn"]
-    flops = sum(4.0 * r["sel"][o] * r["n_keys"][o] * Da for r in recs for o in range(cfg.n_obj))
-    flops_projected = sum(4.0 * r["sel"][o] * r["n_keys"][o] * cfg.D for r in recs for o in range(cfg.n_obj))
+    alg_flops = sum(4.0 * r["sel"][o] * r["n_keys"][o] * cfg.D for r in recs for o in range(cfg.n_obj))
+    exec_flops = sum(4.0 * r["sel"][o] * r["n_keys"][o] * Da for r in recs for o in range(cfg.n_obj))
     sel_tot = sum(sum(r["sel"]) for r in recs)
-    # launches without a separate projection kernel project their queries
-    # inside the attention: 2 * selected * d_model * width more work
-    fused_share = 1.0 - (rep.get("qproj", (0.0, 0))[1] / attn_n if attn_n else 0.0)
-    proj_flops = fused_share * sum(2.0 * r["sel"][o] * cfg.C * Da for r in recs for o in range(cfg.n_obj))
-    flops += proj_flops
-    per_launch_flops = flops / max(attn_n, 1)
+    # the frame call of a single 64-wide head at d_model 256 projects every
+    # cell's query in the energy launch; otherwise launches without a separate
+    # projection kernel project their queries inside the attention
+    pre_projected = calls == "frame" and cfg.dtype == "bf16" and absorb and Da == 64 and cfg.C == 256 \
+        and not args.rope and rep.get("qproj", (0.0, 0))[1] == 0
+    if pre_projected:
+        proj_share = 0.0
+    else:
+        proj_share = 1.0 - (rep.get("qproj", (0.0, 0))[1] / attn_n if attn_n else 0.0)
+    exec_flops += proj_share * sum(2.0 * r["sel"][o] * cfg.C * Da for r in recs for o in range(cfg.n_obj))
     avg_attn_s = attn_ms / 1000.0 / max(attn_n, 1)
-    achieved_tflops = per_launch_flops / avg_attn_s / 1e12 if attn_n else 0.0
+    alg_per_launch = alg_flops / max(attn_n, 1)
+    exec_per_launch = exec_flops / max(attn_n, 1)
+    achieved_tflops = alg_per_launch / avg_attn_s / 1e12 if attn_n else 0.0
+    exec_tflops = exec_per_launch / avg_attn_s / 1e12 if attn_n else 0.0
     kernels = {}
     for name, (ms, n) in rep.items():
         if n and not name.startswith("_"):
@@ -368,12 +378,19 @@ def gpu_run(args):
         "roofline": {"bound": "mfma", "achieved": achieved_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved_tflops / PEAK_BF16_TFLOPS,
                      "traffic": traffic,
-                     "kernel": "k_attn (split-KV attention)",
-                     "flops_per_launch": per_launch_flops,
-                     "flops_basis": ("executed: 4 * selected queries * bank keys * attention width (%d)"
-                                     " + 2 * selected * d_model * width for the query projection done inside"
-                                     " the kernel (%.0f%% of launches)") % (Da, 100.0 * fused_share),
-                     "projected_equivalent_flops_per_launch": flops_projected / max(attn_n, 1),
+                     "kernel": ("k_attn_g2 (split-KV attention, heads of 64; queries projected by the energy launch)"
+                                if pre_projected else "k_attn (split-KV attention)"),
+                     "flops_per_launch": alg_per_launch,
+                     "flops_basis": "algorithmic: 4 * selected queries * bank keys * D (D = H * d_h = %d), the "
+                                    "method's QK^T and PV at the model width" % cfg.D,
+                     "executed_flops_per_launch": exec_per_launch,
+                     "executed_achieved": exec_tflops,
+                     "executed_frac": exec_tflops / PEAK_BF16_TFLOPS,
+                     "executed_basis": ("4 * selected * keys * %d (the kernel's attention width%s)%s"
+                                        % (Da, ", absorbed" if absorb else "",
+                                           "" if proj_share == 0.0 else
+                                           " + 2 * selected * d_model * width for the query projection inside"
+                                           " the kernel (%.0f%% of launches)" % (100.0 * proj_share))),
                      "avg_launch_us": avg_attn_s * 1e6},
         "extra": {
             "query_tokens_per_s": sel_tot / args.steps * fps,
@@ -387,6 +404,7 @@ def gpu_run(args):
             "host_enqueue_us_per_step": host_us,
             "hip_graph": graph,
             "fixed_write_keepset": fixed,
+            "copy_bandwidth": copy_bandwidth() if args.copy_bw else None,
         },
     }
     return out
@@ -622,13 +640,18 @@ def _algo_bytes(cfg, absorb, rec):
         "attn": sum(n * Da * 2 * 2 + q * Da * 2 * 2 for q, n in zip(sel, nk)),
         "combine": sum(q * (Da * 2 + 2 * C * b) for q in sel) + C * Da * 2,
         "commit": cfg.n_obj * mn + sum(k * (4 + 4 * dkv * b + 2 * Da * 2) for k in kept),
+        # the split merge with the scatter and the commit in one launch
+        "merge_commit": sum(q * (Da * 2 + 2 * C * b) for q in sel) + C * Da * 2
+                        + cfg.n_obj * mn + sum(k * (4 + 4 * dkv * b + 2 * Da * 2) for k in kept),
     }
 
 
 def run_workload(cfg, *, absorb, steps, warmup, commit=True, prefill=None, splits=0, rope_theta=None,
-                 write_dw=-1):
+                 write_dw=-1, separate=False):
     """Steady-state frames of `cfg` (objects beyond 64 run as several calls per
-    frame).  Returns frame timing percentiles, per-kernel times and rates."""
+    frame).  separate: select, readout and commit as three calls (the split
+    merge with the scatter, and the commit, then run as launches of their own).
+    Returns frame timing percentiles, per-kernel times and rates."""
     import numpy as np
     import torch
     import paper_2608_22526_amd as rs3
@@ -682,7 +705,11 @@ def run_workload(cfg, *, absorb, steps, warmup, commit=True, prefill=None, split
         for ci, sess in enumerate(sessions):
             f = frames[fi]["per"][ci]
             Y = outs[ci]
-            if commit:   # the whole frame in one call
+            if commit and separate:
+                sess.select(f["rmask"], f["X"], f["k"])
+                sess.readout(f["X"], f["X"] if Y is None else Y, max_sel=frames[fi]["max_sel"])
+                sess.commit(f["K"], f["V"], f["mask"], t, False)
+            elif commit:   # the whole frame in one call
                 sess.frame(f["rmask"], f["X"], f["k"], f["X"] if Y is None else Y, f["K"], f["V"], f["mask"], t,
                            False, max_sel=frames[fi]["max_sel"])
             else:
@@ -747,11 +774,17 @@ def run_workload(cfg, *, absorb, steps, warmup, commit=True, prefill=None, split
             d["frac_hbm"] = d["GB_s"] / PEAK_HBM_GBS
         kern[name] = d
     attn_flops = sum(4.0 * q * n * Da for r in recs for q, n in zip(r["sel"], r["n_keys"])) / len(recs)
+    alg_flops = sum(4.0 * q * n * cfg.D for r in recs for q, n in zip(r["sel"], r["n_keys"])) / len(recs)
     if "attn" in kern:
+        # executed: QK^T and PV at the kernel's attention width; algorithmic:
+        # the same at the model width D (what the method computes)
         a = kern["attn"]
         a["flops_per_frame"] = attn_flops
         a["TFLOP_s"] = attn_flops / a["launches_per_frame"] / (a["avg_us"] * 1e-6) / 1e12
         a["frac_mfma"] = a["TFLOP_s"] / PEAK_BF16_TFLOPS
+        a["algorithmic_flops_per_frame"] = alg_flops
+        a["TFLOP_s_algorithmic"] = alg_flops / a["launches_per_frame"] / (a["avg_us"] * 1e-6) / 1e12
+        a["frac_mfma_algorithmic"] = a["TFLOP_s_algorithmic"] / PEAK_BF16_TFLOPS
     q_frame = sum(sum(r["sel"]) for r in recs) / len(recs)
     k_frame = sum(sum(r["kept"]) for r in recs) / len(recs)
     return {
@@ -764,6 +797,50 @@ def run_workload(cfg, *, absorb, steps, warmup, commit=True, prefill=None, split
         "kernels": kern, "attention_width": Da, "objects": cfg.n_obj, "calls_per_frame": len(sessions),
         "fixed_write_keep_cells": keep_cells,
     }
+
+
+def copy_bandwidth(mib: int = 512, reps: int = 10):
+    """Bandwidth of the library's own grid copy kernel (the out-of-place
+    readout's X -> Y copy: a readout with no selected row launches only that
+    copy) on `mib` MiB read and `mib` MiB written: 64 per-object bf16 grids of
+    d_model 256, larger than the 256 MB Infinity Cache together.  Returns
+    GB/s of bytes read + written."""
+    import numpy as np
+    import torch
+    import paper_2608_22526_amd as rs3
+    n_obj = 64
+    mn = mib * (1 << 20) // (n_obj * 256 * 2)
+    m = 1
+    while m * m < mn:
+        m *= 2
+    n = mn // m
+    C = 256
+    w = np.zeros((C, C), np.uint16)
+    wk = np.zeros((64, C), np.uint16)
+    layer = rs3.Layer(C, 1, 64, rs3.RS3_BF16, w, wk, wk, w, absorb=True)
+    banks = [rs3.Bank(layer, 64, 2, 0) for _ in range(n_obj)]
+    X = torch.empty((n_obj, m * n, C), dtype=torch.bfloat16, device="cuda").fill_(1.0)
+    Y = torch.empty_like(X)
+    sel = torch.zeros((n_obj, m * n), dtype=torch.int32, device="cuda")
+    cnt = torch.zeros(n_obj, dtype=torch.int32, device="cuda")
+    ws = torch.zeros(256, dtype=torch.uint8, device="cuda")
+
+    def once():
+        rs3.readout(layer, (m, n, 1), n_obj, X, m * n * C, banks, sel, cnt, m * n, 0, 0, Y, m * n * C, ws=ws)
+    once()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record()
+    for _ in range(reps):
+        once()
+    ev[1].record()
+    torch.cuda.synchronize()
+    s_per = ev[0].elapsed_time(ev[1]) / 1000.0 / reps
+    moved = 2.0 * X.numel() * 2
+    ok = bool(torch.equal(X, Y))
+    del X, Y
+    return {"GB_s": moved / s_per / 1e9, "bytes_read_plus_written": moved, "us_per_copy": s_per * 1e6,
+            "copy_exact": ok, "kernel": "k_copy_grid16 (16-byte vectors, grid-stride)"}
 
 
 def run_post(n_obj, H, W, k=9, reps=50):
@@ -849,6 +926,18 @@ def report(args):
         r = run_workload(cfg, absorb=True, steps=max(3, args.steps // 8), warmup=2)
         out["objects/%d" % B] = r
         log("objects B=%d (per-object grids)" % B, r)
+    # the scatter (split merge + W_o + residual) and the commit as launches of
+    # their own, with the library's copy kernel as the bandwidth reference
+    out["copy_bandwidth"] = copy_bandwidth()
+    print("copy kernel: %.0f GB/s" % out["copy_bandwidth"]["GB_s"], flush=True)
+    for B in (1, 8, 64, 512):
+        cfg = replace(base, n_obj=B, shared_x=False, union_objects=False) if B > 1 else CONFIGS["sam2_single"]
+        r = run_workload(cfg, absorb=True, steps=max(3, args.steps // 8) if B > 8 else args.steps, warmup=2 if B > 8
+                         else args.warmup, separate=True)
+        out["separate/%d" % B] = r
+        log("separate launches B=%d" % B, r)
+        print("   " + ", ".join("%s %.0f GB/s" % (k, v["GB_s"]) for k, v in r["kernels"].items() if "GB_s" in v),
+              flush=True)
     with open(args.report, "w") as fh:
         json.dump(out, fh, indent=1)
 
@@ -879,6 +968,8 @@ def main():
                     help="skip the HIP-graph replay pass (reported beside the eager frames/s)")
     ap.add_argument("--cpu-frames", type=int, default=40)
     ap.add_argument("--copy-probe-mb", type=int, default=0)
+    ap.add_argument("--no-copy-bw", dest="copy_bw", action="store_false",
+                    help="skip the measurement of the library's copy-kernel bandwidth (512 MiB each way)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-child", action="store_true")
     ap.add_argument("--report", default="", help="write the full measurement report (JSON) to this path")

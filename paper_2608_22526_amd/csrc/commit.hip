@@ -61,7 +61,7 @@ __global__ __launch_bounds__(256) void k_commit_append_bf16(Rs3CommitArgs a) {
 // Restored bank: rows [hdr PSTART, + PLEN) of bank 0 from the raw ring,
 // 64 per work-group.
 __global__ __launch_bounds__(256) void k_commit_append_f32(Rs3CommitArgs a) {
-  __shared__ __attribute__((aligned(16))) float sK[64 * F32_SP], sV[64 * F32_SP];
+  __shared__ __attribute__((aligned(16))) float sK[64 * F32_SP], sV[64 * F32_SP], sW[64 * F32_WP];
   __shared__ int spos[64];
   const int o = blockIdx.x;
   const BankDev& b = *a.banks[o];
@@ -72,7 +72,7 @@ __global__ __launch_bounds__(256) void k_commit_append_f32(Rs3CommitArgs a) {
   const int rows = min(64, L - r0);
   if (threadIdx.x < 64) spos[threadIdx.x] = (int)threadIdx.x < rows ? b.pos[start + r0 + threadIdx.x] : 0;
   __syncthreads();
-  append_f32<256>(a, b, o, start, r0, rows, spos, sK, sV);
+  append_f32<256>(a, b, o, start, r0, rows, spos, sK, sV, sW);
 }
 
 // grid (n_obj, 1 + ceil(kept rows / rows_per_wg)), block CP_THREADS.

@@ -3,7 +3,7 @@
 // by the commit kernels and the fused merge + commit launch.
 #pragma once
 
-#include "rs3_internal.h"
+#include "device_util.h"
 
 namespace rs3 {
 
@@ -368,15 +368,18 @@ __device__ __forceinline__ void append_bf16(const Rs3CommitArgs& a, const BankDe
 }
 
 // fp32: for d_kv <= 64 the kept rows are staged in LDS (sK, sV: 64 rows of
-// F32_STAGE_KV + 4 floats each) and each thread owns one output column d
-// with its W_k / W_v rows in registers (row operands are LDS broadcasts);
-// otherwise plain FMA loops over the rows just written to the ring.
+// F32_STAGE_KV + 4 floats each), and so is each block of 64 rows of W_k^T or
+// W_v^T (sW: 64 x (d_kv + 1) floats, the odd pitch keeps the 64 lanes of a
+// wave, one output column each, on distinct banks); a thread computes the
+// output columns d0 + lane of the rows wave, wave + NT/64, ...  Otherwise
+// plain FMA loops over the rows just written to the ring.
 constexpr int F32_STAGE_KV = 64;
 constexpr int F32_SP = F32_STAGE_KV + 4;   // row pitch: 16-byte aligned rows
+constexpr int F32_WP = F32_STAGE_KV + 1;   // W block pitch
 
 template <int NT>
 __device__ __forceinline__ void append_f32(const Rs3CommitArgs& a, const BankDev& b, int o, int start, int r0,
-                                           int rows, const int* src, float* sK, float* sV) {
+                                           int rows, const int* src, float* sK, float* sV, float* sW) {
   const int tid = threadIdx.x;
   const int d_kv = b.d_kv, d_h = b.d_h, H = b.H, D = H * d_h;
   const bool stage = d_kv <= F32_STAGE_KV;
@@ -389,14 +392,14 @@ __device__ __forceinline__ void append_f32(const Rs3CommitArgs& a, const BankDev
     const int64_t j = start + r0 + r;
     float kv, vv;
     if (a.from_ring) {
-      kv = Kr[j * d_kv + c];
-      vv = Vr[j * d_kv + c];
+      kv = gload(Kr + j * d_kv + c);
+      vv = gload(Vr + j * d_kv + c);
     } else {
       const int cell = src[r];
-      kv = Km[(int64_t)cell * d_kv + c];
-      vv = Vm[(int64_t)cell * d_kv + c];
-      Kr[j * d_kv + c] = kv;
-      Vr[j * d_kv + c] = vv;
+      kv = gload(Km + (int64_t)cell * d_kv + c);
+      vv = gload(Vm + (int64_t)cell * d_kv + c);
+      gstore(Kr + j * d_kv + c, kv);
+      gstore(Vr + j * d_kv + c, vv);
     }
     if (stage) {
       sK[r * F32_SP + c] = kv;
@@ -409,39 +412,42 @@ __device__ __forceinline__ void append_f32(const Rs3CommitArgs& a, const BankDev
   float* Kh = (float*)b.Khat;
   float* Vh = (float*)b.Vhat;
   if (stage) {
-    // one pass for K^ and one for V^, so that one row of weights is live
-    const int ngrp = D >= NT ? 1 : NT / D;
+    const int lane = tid & 63, wave = tid >> 6;
     for (int pass = 0; pass < 2; ++pass) {
       const float* WT = pass == 0 ? WkT : WvT;
       const float* sX = pass == 0 ? sK : sV;
-      for (int dq = tid; dq < D * ngrp; dq += NT) {
-        const int d = dq % D, grp = dq / D;
-        const int h = d / d_h, dd = d - h * d_h;
-        float w[F32_STAGE_KV];
+      for (int d0 = 0; d0 < D; d0 += 64) {
+        const int nd = min(64, D - d0);
         if (!a.absorb) {
-#pragma unroll
-          for (int c = 0; c < F32_STAGE_KV; ++c) w[c] = c < d_kv ? WT[(int64_t)d * d_kv + c] : 0.f;
-        }
-        for (int r = grp; r < rows; r += ngrp) {
-          float acc;
-          if (a.absorb) {   // attention on the raw rows
-            acc = sX[r * F32_SP + d];
-          } else {
-            acc = 0.f;
-#pragma unroll
-            for (int c4 = 0; c4 < F32_STAGE_KV / 4; ++c4)
-              if (4 * c4 < d_kv) {   // d_kv is a multiple of 16
-                const f32x4 x4 = *(const f32x4*)&sX[r * F32_SP + 4 * c4];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) acc = fmaf(x4[e], w[4 * c4 + e], acc);
-              }
+          for (int q = tid; q < nd * d_kv; q += NT) {
+            const int dd = q / d_kv, c = q - dd * d_kv;
+            sW[dd * F32_WP + c] = gload(WT + (int64_t)(d0 + dd) * d_kv + c);
           }
-          const int j = start + r0 + r, tile = j >> 6, kk = j & 63;
-          if (pass == 0)
-            Kh[(((int64_t)tile * H + h) * KT + kk) * d_h + dd] = acc;
-          else
-            Vh[(((int64_t)tile * H + h) * d_h + dd) * KT + vslot(kk)] = acc;
+          __syncthreads();
         }
+        const int d = d0 + lane;
+        if (lane < nd) {
+          const int h = d / d_h, dd = d - h * d_h;
+          for (int r = wave; r < rows; r += NT / 64) {
+            float acc;
+            if (a.absorb) {   // attention on the raw rows
+              acc = sX[r * F32_SP + d];
+            } else {
+              float a0 = 0.f, a1 = 0.f;
+              for (int c = 0; c < d_kv; c += 2) {   // d_kv is a multiple of 16
+                a0 = fmaf(sX[r * F32_SP + c], sW[lane * F32_WP + c], a0);
+                a1 = fmaf(sX[r * F32_SP + c + 1], sW[lane * F32_WP + c + 1], a1);
+              }
+              acc = a0 + a1;
+            }
+            const int j = start + r0 + r, tile = j >> 6, kk = j & 63;
+            if (pass == 0)
+              gstore(Kh + (((int64_t)tile * H + h) * KT + kk) * d_h + dd, acc);
+            else
+              gstore(Vh + (((int64_t)tile * H + h) * d_h + dd) * KT + vslot(kk), acc);
+          }
+        }
+        if (!a.absorb) __syncthreads();   // the next block rewrites sW
       }
     }
   } else {
@@ -452,21 +458,21 @@ __device__ __forceinline__ void append_f32(const Rs3CommitArgs& a, const BankDev
       const float* vr = Vr + (int64_t)j * d_kv;
       float sk, sv;
       if (a.absorb) {  // attention on the raw rows
-        sk = kr[d];
-        sv = vr[d];
+        sk = gload(kr + d);
+        sv = gload(vr + d);
       } else {
         const float* wk = WkT + (int64_t)d * d_kv;
         const float* wv = WvT + (int64_t)d * d_kv;
         sk = 0.f;
         sv = 0.f;
         for (int c = 0; c < d_kv; ++c) {
-          sk = fmaf(kr[c], wk[c], sk);
-          sv = fmaf(vr[c], wv[c], sv);
+          sk = fmaf(gload(kr + c), gload(wk + c), sk);
+          sv = fmaf(gload(vr + c), gload(wv + c), sv);
         }
       }
       const int tile = j >> 6, kk = j & 63, h = d / d_h, dd = d - h * d_h;
-      Kh[(((int64_t)tile * H + h) * KT + kk) * d_h + dd] = sk;
-      Vh[(((int64_t)tile * H + h) * d_h + dd) * KT + vslot(kk)] = sv;
+      gstore(Kh + (((int64_t)tile * H + h) * KT + kk) * d_h + dd, sk);
+      gstore(Vh + (((int64_t)tile * H + h) * d_h + dd) * KT + vslot(kk), sv);
     }
   }
   if (a.rope) {
@@ -597,7 +603,8 @@ __device__ __forceinline__ void commit_block(const Rs3CommitArgs& a, int o, int 
     if constexpr (BF16)
       append_bf16<CP_THREADS>(a, b, o, start, r0, rows, spos, (bf16_t*)stage);
     else
-      append_f32<CP_THREADS>(a, b, o, start, r0, rows, spos, (float*)stage, (float*)stage + 64 * F32_SP);
+      append_f32<CP_THREADS>(a, b, o, start, r0, rows, spos, (float*)stage, (float*)stage + 64 * F32_SP,
+                             (float*)stage + 2 * 64 * F32_SP);
     __syncthreads();   // the next round rewrites spos and the row stage
   }
 }
@@ -613,7 +620,7 @@ inline int commit_rows_per_wg(int n_obj, int mn) {
 }
 
 inline size_t commit_stage_bytes(int dtype, int d_kv) {
-  return dtype == RS3_BF16 ? (size_t)2 * 64 * (d_kv + 8) * 2 : (size_t)2 * 64 * F32_SP * 4;
+  return dtype == RS3_BF16 ? (size_t)2 * 64 * (d_kv + 8) * 2 : (size_t)(2 * 64 * F32_SP + 64 * F32_WP) * 4;
 }
 
 }  // namespace rs3

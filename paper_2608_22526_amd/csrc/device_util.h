@@ -15,6 +15,14 @@ __device__ __forceinline__ T gload(const T* p) {
   return *(const RS3_GLOBAL T*)p;
 }
 
+// Stores through global pointers, for the same reason: a generic (flat)
+// store counts on the LDS counter too, so a later wait for an LDS read would
+// also wait for the store to land.
+template <class T>
+__device__ __forceinline__ void gstore(T* p, const T& v) {
+  *(RS3_GLOBAL T*)p = v;
+}
+
 // Loads of wave-uniform values that earlier launches wrote (bank headers,
 // descriptors, selected counts): through the constant address space the
 // compiler uses scalar loads, which are counted apart from the vector loads,
@@ -59,6 +67,38 @@ __device__ __forceinline__ int sel_count_of(const Rs3ReadoutArgs& a, int o, Bank
 __device__ __forceinline__ bool sel_ok(const int32_t* sel, int r, int mn) {
   int i = sel[r];
   return i >= 0 && i < mn && (r == 0 || sel[r - 1] < i);
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dppf(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over the 64 lanes, the same value in every lane: within rows of 16
+// lanes by DPP (quad swaps, half-row and row mirrors), then across rows by
+// v_permlane16_swap and v_permlane32_swap.  Each step adds a lane to a
+// partner that adds it back, so every lane holds the same bits.
+__device__ __forceinline__ float wave_sum(float v) {
+  v += dppf<0xB1>(v);    // quad_perm(1, 0, 3, 2)
+  v += dppf<0x4E>(v);    // quad_perm(2, 3, 0, 1)
+  v += dppf<0x141>(v);   // row_half_mirror
+  v += dppf<0x140>(v);   // row_mirror
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Maximum over the 64 lanes by the same exchange pattern.
+__device__ __forceinline__ float wave_max(float v) {
+  v = fmaxf(v, dppf<0xB1>(v));
+  v = fmaxf(v, dppf<0x4E>(v));
+  v = fmaxf(v, dppf<0x141>(v));
+  v = fmaxf(v, dppf<0x140>(v));
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
 }  // namespace rs3

@@ -1351,40 +1351,96 @@ __global__ __launch_bounds__(256) void k_copy_grid16(const u32x4* X, int64_t x_s
 }
 
 // ---------------------------------------------------------------------------
-// fp32 path: grid (n_obj, max_sel), block 256, one selected row per block.
-__global__ __launch_bounds__(256) void k_readout_f32(Rs3ReadoutArgs a) {
+// fp32 path: grid (n_obj, max_sel), block 256, one selected row per
+// work-group; its four waves split the resident tiles (wave w takes tiles
+// w, w+4, ...) and merge their softmax states at the end.  For row i:
+//   q = qscale * x W_q              threads over the attention columns
+//   per head and tile of a wave:    lanes over the tile's 64 keys: logits,
+//     wave max / sum (online softmax); lanes over the head's columns:
+//     o = alpha*o + sum_k p_k v_k   (weights broadcast from LDS)
+//   merge of the four waves' (m, l, o) per head, then
+//   y = x + (o / l) W_o             threads over the output channels
+// Every load that needs only the arguments (count, header, the first tile
+// entries, the list entries, W_q rows) is issued first, and a wave's first
+// key and value rows (heads of at most 64 columns) before the query is
+// ready, so that the row's chain of dependent loads stays short.
+// LDS: x [C], q [D], o [4][D], p [4][64], (m, l) [4][H] floats.
+__global__ __launch_bounds__(256) void k_readout_f32(Rs3ReadoutArgs a, Rs3AttnBanks ab) {
   extern __shared__ float sm[];
-  __shared__ float pr[KT];
-  __shared__ float st[4];  // m_run, l_run, alpha
-  const int o = blockIdx.x, r = blockIdx.y, tid = threadIdx.x;
-  BankDev& b = *a.banks[o];
-  const int cnt = sel_count_of(a, o, b, r == 0 && tid == 0);
-  if (r >= cnt) return;
+  const int o = blockIdx.x, r = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int C = a.C, D = a.D, H = a.H, d_h = a.d_h;
+  float* xs = sm;
+  float* q = xs + C;
+  float* ow = q + D + wave * D;        // this wave's o
+  float* pr = q + 5 * D + wave * 64;   // this wave's weights of one tile
+  float* ml = q + 5 * D + 256;         // [4][H][2]
+  int32_t* hdr = (int32_t*)ab.hdr[o];
+  const TileEnt* tiles = ab.tiles[o];
+  const int ntcap = ab.ntcap[o];
+  int cnt = gload(a.sel_count + (a.sel_stride ? o : 0));
+  const int ntiles = gload(hdr + HDR_NTILES);
+  // tile entries t = wave + 4*lane (a wave's first 64 tiles)
+  int c_tile = 0;
+  uint32_t c_lo = 0, c_hi = 0;
+  if (wave + 4 * lane < ntcap) {
+    c_tile = gload(&tiles[wave + 4 * lane].tile);
+    const uint64_t mm = gload(&tiles[wave + 4 * lane].mask);
+    c_lo = (uint32_t)mm;
+    c_hi = (uint32_t)(mm >> 32);
+  }
   const int32_t* sel = a.sel_idx + (int64_t)o * a.sel_stride;
-  if (!sel_ok(sel, r, a.mn)) {
-    if (tid == 0) set_err(b.hdr, RS3_E_INVALID);
+  const int rc = min(r, a.max_sel - 1);
+  const int i_raw = gload(sel + rc), i_prev = rc > 0 ? gload(sel + rc - 1) : -1;
+  if (cnt < 0 || cnt > a.max_sel) {
+    if (r == 0 && tid == 0) set_err(hdr, RS3_E_INVALID);
+    cnt = cnt < 0 ? 0 : a.max_sel;
+  }
+  if (r >= cnt) return;
+  if (!(i_raw >= 0 && i_raw < a.mn && i_prev < i_raw)) {
+    if (tid == 0) set_err(hdr, RS3_E_INVALID);
     return;
   }
-  const int C = a.C, D = a.D, H = a.H, d_h = a.d_h;
-  float* xs = sm;        // [C]
-  float* q = sm + C;     // [D]
-  float* oacc = q + D;   // [D]
-  const int i = sel[r];
+  const int i = i_raw;
   const float* x = (const float*)a.X + (int64_t)o * a.x_stride + (int64_t)i * C;
   float* y = (float*)a.Y + (int64_t)o * a.y_stride + (int64_t)i * C;
-  for (int c = tid; c < C; c += 256) xs[c] = x[c];
-  const int ntiles = b.hdr[HDR_NTILES];
-  __syncthreads();
   if (ntiles == 0) {
-    for (int c = tid; c < C; c += 256) y[c] = xs[c];
+    for (int c = tid; c < C; c += 256) gstore(y + c, gload(x + c));
     return;
   }
+  const float* Kh = (const float*)ab.kh[o];
+  const float* Vh = (const float*)ab.vh[o];
+  const bool fast = d_h <= 64 && (d_h & 3) == 0 && ntiles <= 256;
+  // fast path: the key row (lane = key) and value row (lane = column) of a
+  // tile of this wave, first tile in flight before the query is ready
+  f32x4 kc[16], vc[16];
+  auto load_tile = [&](int j, int h) {   // j: the wave's j-th tile
+    const int tl = __builtin_amdgcn_readlane(c_tile, j);
+    const f32x4* kr = (const f32x4*)(Kh + (((int64_t)tl * H + h) * KT + lane) * d_h);
+    const f32x4* vr = (const f32x4*)(Vh + (((int64_t)tl * H + h) * d_h + min(lane, d_h - 1)) * KT);
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      if (4 * u < d_h) kc[u] = gload(kr + u);
+      vc[u] = gload(vr + u);
+    }
+  };
+  const int nmine = ntiles > wave ? (ntiles - wave + 3) / 4 : 0;   // this wave's tiles
+  if (fast && nmine > 0) load_tile(0, 0);
+  for (int c = tid; c < C; c += 256) xs[c] = gload(x + c);
+  __syncthreads();
   const float* WqT = (const float*)a.WqT;
   for (int d = tid; d < D; d += 256) {
-    float s = 0.f;
-    for (int c = 0; c < C; ++c) s = fmaf(xs[c], WqT[(int64_t)d * C + c], s);
-    q[d] = s * a.qscale;
-    oacc[d] = 0.f;
+    const f32x4* wr = (const f32x4*)(WqT + (int64_t)d * C);
+    float s0 = 0.f, s1 = 0.f;
+    for (int c4 = 0; c4 < C / 4; c4 += 2) {
+      const f32x4 w0 = gload(wr + c4), x0 = *(const f32x4*)(xs + 4 * c4);
+      s0 = fmaf(x0[0], w0[0], fmaf(x0[1], w0[1], fmaf(x0[2], w0[2], fmaf(x0[3], w0[3], s0))));
+      if (c4 + 1 < C / 4) {
+        const f32x4 w1 = gload(wr + c4 + 1), x1 = *(const f32x4*)(xs + 4 * c4 + 4);
+        s1 = fmaf(x1[0], w1[0], fmaf(x1[1], w1[1], fmaf(x1[2], w1[2], fmaf(x1[3], w1[3], s1))));
+      }
+    }
+    q[d] = (s0 + s1) * a.qscale;
   }
   __syncthreads();
   if (a.rope) {
@@ -1392,66 +1448,116 @@ __global__ __launch_bounds__(256) void k_readout_f32(Rs3ReadoutArgs a) {
     const float* f = a.rope + (int64_t)i * d_h;   // d_h/2 (cos, sin) pairs
     for (int pp = tid; pp < D / 2; pp += 256) {
       const int d = 2 * pp, fp = (d % d_h) & ~1;
-      const float c = f[fp], sn = f[fp + 1], xe = q[d], xo = q[d + 1];
+      const float c = gload(f + fp), sn = gload(f + fp + 1), xe = q[d], xo = q[d + 1];
       q[d] = xe * c - xo * sn;
       q[d + 1] = xe * sn + xo * c;
     }
     __syncthreads();
   }
-  const float* Kh = (const float*)b.Khat;
-  const float* Vh = (const float*)b.Vhat;
   for (int h = 0; h < H; ++h) {
-    if (tid == 0) {
-      st[0] = -INFINITY;
-      st[1] = 0.f;
-    }
-    __syncthreads();
-    for (int t = 0; t < ntiles; ++t) {
-      const TileEnt ent = b.tiles[t];
-      const float* kg = Kh + ((int64_t)ent.tile * H + h) * (KT * d_h);
-      const float* vg = Vh + ((int64_t)ent.tile * H + h) * (d_h * KT);
-      if (tid < KT) {
-        float s = -INFINITY;
-        if (ent.mask >> tid & 1ull) {
-          s = 0.f;
-          for (int u = 0; u < d_h; ++u) s = fmaf(q[h * d_h + u], kg[tid * d_h + u], s);
+    float m_run = -INFINITY, l_run = 0.f;
+    const float* qh = q + h * d_h;
+    for (int dd = lane; dd < d_h; dd += 64) ow[h * d_h + dd] = 0.f;
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    for (int j = 0; j < nmine; ++j) {
+      const int t = wave + 4 * j;
+      int etile;
+      uint64_t emask;
+      if (fast) {
+        etile = __builtin_amdgcn_readlane(c_tile, j);
+        emask = (uint64_t)__builtin_amdgcn_readlane(c_lo, j) | ((uint64_t)__builtin_amdgcn_readlane(c_hi, j) << 32);
+        if (j > 0 || h > 0) load_tile(j, h);
+      } else {
+        etile = gload(&tiles[t].tile);
+        emask = gload(&tiles[t].mask);
+      }
+      const bool valid = emask >> lane & 1ull;
+      float s0 = 0.f, s1 = 0.f;
+      if (fast) {
+#pragma unroll
+        for (int u = 0; u < 16; u += 2) {
+          if (4 * u < d_h) {
+            const f32x4 q0 = *(const f32x4*)(qh + 4 * u);
+            s0 = fmaf(q0[0], kc[u][0], fmaf(q0[1], kc[u][1], fmaf(q0[2], kc[u][2], fmaf(q0[3], kc[u][3], s0))));
+          }
+          if (4 * u + 4 < d_h) {
+            const f32x4 q1 = *(const f32x4*)(qh + 4 * u + 4);
+            s1 = fmaf(q1[0], kc[u + 1][0], fmaf(q1[1], kc[u + 1][1], fmaf(q1[2], kc[u + 1][2], fmaf(q1[3], kc[u + 1][3], s1))));
+          }
         }
-        pr[tid] = s;
+      } else {
+        const float* krow = Kh + (((int64_t)etile * H + h) * KT + lane) * d_h;
+        for (int u = 0; u < d_h; ++u) s0 = fmaf(qh[u], gload(krow + u), s0);
       }
-      __syncthreads();
-      if (tid == 0) {
-        float mx = -INFINITY;
-        for (int j = 0; j < KT; ++j) mx = fmaxf(mx, pr[j]);
-        const float m_new = fmaxf(st[0], mx);
-        const float alpha = exp2f(st[0] - m_new);
-        float ps = 0.f;
-        for (int j = 0; j < KT; ++j) {
-          const float p = exp2f(pr[j] - m_new);
-          pr[j] = p;
-          ps += p;
+      const float s = valid ? s0 + s1 : -INFINITY;
+      const float mx = wave_max(s);
+      if (mx == -INFINITY) continue;   // no resident key in the tile
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = exp2f(m_run - m_new);   // 0 on the wave's first keys
+      const float p = valid ? exp2f(s - m_new) : 0.f;
+      l_run = l_run * alpha + wave_sum(p);
+      m_run = m_new;
+      pr[lane] = p;
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      // slot quad 4j of a V^ row holds the key quad vslot(4j) (the slot
+      // permutation swaps whole quads and is its own inverse)
+      if (fast) {
+        if (lane < d_h) {
+          float acc = ow[h * d_h + lane] * alpha;
+#pragma unroll
+          for (int u = 0; u < 16; ++u) {
+            const f32x4 pk = *(const f32x4*)(pr + vslot(4 * u));
+            acc = fmaf(pk[0], vc[u][0], fmaf(pk[1], vc[u][1], fmaf(pk[2], vc[u][2], fmaf(pk[3], vc[u][3], acc))));
+          }
+          ow[h * d_h + lane] = acc;
         }
-        st[1] = st[1] * alpha + ps;
-        st[0] = m_new;
-        st[2] = alpha;
+      } else {
+        for (int dd = lane; dd < d_h; dd += 64) {
+          const float* vr = Vh + (((int64_t)etile * H + h) * d_h + dd) * KT;
+          float acc = ow[h * d_h + dd] * alpha;
+          for (int k = 0; k < KT; ++k) acc = fmaf(pr[vslot(k)], gload(vr + k), acc);
+          ow[h * d_h + dd] = acc;
+        }
       }
-      __syncthreads();
-      const float alpha = st[2];
-      for (int u = tid; u < d_h; u += 256) {
-        float acc = oacc[h * d_h + u] * alpha;
-        for (int j = 0; j < KT; ++j) acc = fmaf(pr[j], vg[u * KT + vslot(j)], acc);
-        oacc[h * d_h + u] = acc;
-      }
-      __syncthreads();
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     }
-    const float inv = 1.f / st[1];
-    for (int u = tid; u < d_h; u += 256) oacc[h * d_h + u] *= inv;
-    __syncthreads();
+    if (lane == 0) {
+      ml[(wave * H + h) * 2] = m_run;
+      ml[(wave * H + h) * 2 + 1] = l_run;
+    }
   }
+  __syncthreads();
+  // merge the waves' states into q's place: o = sum_w e^(m_w - M) o_w / sum_w e^(m_w - M) l_w
+  float* of = q;
+  for (int d = tid; d < D; d += 256) {
+    const int h = d / d_h;
+    float M = -INFINITY;
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, ml[(w * H + h) * 2]);
+    float num = 0.f, den = 0.f;
+    if (M != -INFINITY)
+      for (int w = 0; w < 4; ++w) {
+        const float mw = ml[(w * H + h) * 2];
+        if (mw == -INFINITY) continue;
+        const float sc = exp2f(mw - M);
+        num = fmaf(sc, q[D + w * D + d], num);
+        den = fmaf(sc, ml[(w * H + h) * 2 + 1], den);
+      }
+    of[d] = den > 0.f ? num / den : 0.f;
+  }
+  __syncthreads();
   const float* WoT = (const float*)a.WoT;
   for (int c = tid; c < C; c += 256) {
-    float s = 0.f;
-    for (int d = 0; d < D; ++d) s = fmaf(oacc[d], WoT[(int64_t)c * D + d], s);
-    y[c] = xs[c] + s;
+    const f32x4* wr = (const f32x4*)(WoT + (int64_t)c * D);
+    float s0 = 0.f, s1 = 0.f;
+    for (int d4 = 0; d4 < D / 4; d4 += 2) {
+      const f32x4 w0 = gload(wr + d4), o0 = *(const f32x4*)(of + 4 * d4);
+      s0 = fmaf(o0[0], w0[0], fmaf(o0[1], w0[1], fmaf(o0[2], w0[2], fmaf(o0[3], w0[3], s0))));
+      if (d4 + 1 < D / 4) {
+        const f32x4 w1 = gload(wr + d4 + 1), o1 = *(const f32x4*)(of + 4 * d4 + 4);
+        s1 = fmaf(o1[0], w1[0], fmaf(o1[1], w1[1], fmaf(o1[2], w1[2], fmaf(o1[3], w1[3], s1))));
+      }
+    }
+    gstore(y + c, xs[c] + (s0 + s1));
   }
 }
 
@@ -1533,8 +1639,8 @@ hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, const Rs3AttnBanks& ab, i
   }
   if (a.max_sel == 0) return hipSuccess;
   if (dtype == RS3_F32) {
-    size_t lds = (size_t)(a.C + 2 * a.D) * 4;
-    RS3_LAUNCH(RS3_K_READOUT_F32, st, k_readout_f32, dim3(a.n_obj, a.max_sel), dim3(256), lds, st, a);
+    size_t lds = (size_t)(a.C + 5 * a.D + 256 + 8 * a.H) * 4;
+    RS3_LAUNCH(RS3_K_READOUT_F32, st, k_readout_f32, dim3(a.n_obj, a.max_sel), dim3(256), lds, st, a, ab);
     return hipGetLastError();
   }
   const bool project = attn_projects(a);

@@ -39,26 +39,6 @@ constexpr int SG_C = 256;    // d_model of the stack
 constexpr int SG_PITCH = SG_C + 8;   // bf16 elements per LDS row of a 256-wide A operand
 constexpr float SG_LN_EPS = 1e-5f;
 
-template <int CTRL>
-__device__ __forceinline__ float dppf(float v) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
-}
-
-// Sum over the 64 lanes, the same value in every lane: within rows of 16
-// lanes by DPP (quad swaps, half-row and row mirrors), then across rows by
-// v_permlane16_swap and v_permlane32_swap.  Each step adds a lane to a
-// partner that adds it back, so every lane holds the same bits.
-__device__ __forceinline__ float wave_sum(float v) {
-  v += dppf<0xB1>(v);    // quad_perm(1, 0, 3, 2)
-  v += dppf<0x4E>(v);    // quad_perm(2, 3, 0, 1)
-  v += dppf<0x141>(v);   // row_half_mirror
-  v += dppf<0x140>(v);   // row_mirror
-  auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  v = __uint_as_float(r[0]) + __uint_as_float(r[1]);
-  r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-
 // B operand of the packed weight Wp (KS 16-deep steps) for 32-column block
 // nb and step ks: lane l holds column 32*nb + l%32, rows 16*ks + 8*(l/32) .. +7.
 __device__ __forceinline__ u32x4 ldb(const bf16_t* Wp, int KS, int nb, int ks, int lane) {

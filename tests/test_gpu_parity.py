@@ -219,3 +219,23 @@ def test_determinism():
         torch.cuda.synchronize()
         outs.append(_host(Y))
     assert np.array_equal(outs[0], outs[1])
+
+
+@pytest.mark.parametrize("C,H,d_kv,rope", [(40, 4, 16, True), (24, 8, 16, False), (256, 2, 64, False),
+                                           (64, 4, 32, True)])
+def test_f32_layer_shapes(C, H, d_kv, rope):
+    """fp32 layers whose heads are not 16-byte multiples (widths 10 and 3),
+    heads wider than the 64 lanes of a wave (128), several heads, with and
+    without a rotary table: every selected row within 1e-4 of the oracle."""
+    import oracle
+    from workloads import make_rope_table
+    cfg = replace(CONFIGS["tiny_f32"], C=C, H=H, d_h=C // H, d_kv=d_kv)
+    tbl = make_rope_table(cfg, seed=3) if rope else None
+    r = Runner(cfg, 6, rope_table=tbl)
+    if rope:
+        r.orc.rope = oracle.table_from_pairs(tbl)
+    r.commit(0, True)
+    for t in range(1, 6):
+        r.select_readout(t)
+        r.commit(t, False)
+    print("f32 shapes", C, H, d_kv, rope, r.stats)
