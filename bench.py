@@ -150,16 +150,19 @@ class QueueWindow:
     def __init__(self, torch, window=48, every=8):
         self.torch, self.window, self.every = torch, window, every
         self.events = {}
+        # events are created here, outside any timed region, and reused
+        self.pool = [torch.cuda.Event() for _ in range(window // every + 2)]
 
     def before(self, i):
         if i % self.every == 0:
             ev = self.events.pop(i - self.window, None)
             if ev is not None:
                 ev.synchronize()
+                self.pool.append(ev)
 
     def after(self, i):
         if i % self.every == 0:
-            ev = self.torch.cuda.Event()
+            ev = self.pool.pop() if self.pool else self.torch.cuda.Event()
             ev.record()
             self.events[i] = ev
 
@@ -296,11 +299,11 @@ def gpu_run(args):
     torch.cuda.synchronize()
     # pass A: frames/s, no instrumentation
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    qw = QueueWindow(torch)
+    enq = []
     torch.cuda.synchronize()
     ev0.record(main)
     h0 = time.perf_counter()
-    qw = QueueWindow(torch)
-    enq = []
     for i in range(args.steps):
         qw.before(i)
         t_in = time.perf_counter()
@@ -308,10 +311,10 @@ def gpu_run(args):
         enq.append(time.perf_counter() - t_in)
         qw.after(i)
     host_loop_us = (time.perf_counter() - h0) * 1e6 / args.steps
-    host_us = float(np.median(enq)) * 1e6
     main.wait_event(ev_commit)
     ev1.record(main)
     torch.cuda.synchronize()
+    host_us = float(np.median(enq)) * 1e6   # (after the end event: numpy's first call can take tens of ms)
     ms_total = ev0.elapsed_time(ev1)
     ms_step = ms_total / args.steps
     fps = 1000.0 / ms_step
@@ -524,10 +527,10 @@ def gpu_run_stack(args):
     torch.cuda.synchronize()
     main = torch.cuda.current_stream()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    ev0.record(main)
-    h0 = time.perf_counter()
     qw = QueueWindow(torch, window=16, every=4)
     enq = []
+    ev0.record(main)
+    h0 = time.perf_counter()
     for i in range(args.steps):
         qw.before(i)
         t_in = time.perf_counter()
@@ -535,9 +538,9 @@ def gpu_run_stack(args):
         enq.append(time.perf_counter() - t_in)
         qw.after(i)
     host_loop_us = (time.perf_counter() - h0) * 1e6 / args.steps
-    host_us = float(np.median(enq)) * 1e6
     ev1.record(main)
     torch.cuda.synchronize()
+    host_us = float(np.median(enq)) * 1e6   # (after the end event: numpy's first call can take tens of ms)
     ms_step = ev0.elapsed_time(ev1) / args.steps
     fps = 1000.0 / ms_step
     graph = _graph_pass(torch, step, args.steps) if args.graph else None

@@ -11,16 +11,16 @@ namespace rs3 {
 template <typename OutT>
 __device__ __forceinline__ void store_out(OutT* p, float v);
 template <>
-__device__ __forceinline__ void store_out<bf16_t>(bf16_t* p, float v) { *p = f2bf(v); }
+__device__ __forceinline__ void store_out<bf16_t>(bf16_t* p, float v) { gstore(p, f2bf(v)); }
 template <>
-__device__ __forceinline__ void store_out<float>(float* p, float v) { *p = v; }
+__device__ __forceinline__ void store_out<float>(float* p, float v) { gstore(p, v); }
 
 template <typename OutT>
 __device__ __forceinline__ void copy_out(OutT* p, bf16_t x);
 template <>
-__device__ __forceinline__ void copy_out<bf16_t>(bf16_t* p, bf16_t x) { *p = x; }
+__device__ __forceinline__ void copy_out<bf16_t>(bf16_t* p, bf16_t x) { gstore(p, x); }
 template <>
-__device__ __forceinline__ void copy_out<float>(float* p, bf16_t x) { *p = bf2f(x); }
+__device__ __forceinline__ void copy_out<float>(float* p, bf16_t x) { gstore(p, bf2f(x)); }
 
 // grid (n_obj, ceil(max_sel/cb_rows_for(D, n_obj, max_sel))), block 512.  Every key split of the call
 // holds a partial for every selected row (the attention writes l = 0 for

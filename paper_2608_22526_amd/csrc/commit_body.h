@@ -275,14 +275,14 @@ __device__ __forceinline__ void append_bf16(const Rs3CommitArgs& a, const BankDe
     if (r < rows) {
       const int64_t j = start + r0 + r;
       if (a.from_ring) {
-        kv = *(const u32x4*)(Kr + j * d_kv + 8 * c);
-        vv = *(const u32x4*)(Vr + j * d_kv + 8 * c);
+        kv = gload((const u32x4*)(Kr + j * d_kv + 8 * c));
+        vv = gload((const u32x4*)(Vr + j * d_kv + 8 * c));
       } else {
         const int cell = src[r];
-        kv = *(const u32x4*)(Km + (int64_t)cell * d_kv + 8 * c);
-        vv = *(const u32x4*)(Vm + (int64_t)cell * d_kv + 8 * c);
-        *(u32x4*)(Kr + j * d_kv + 8 * c) = kv;
-        *(u32x4*)(Vr + j * d_kv + 8 * c) = vv;
+        kv = gload((const u32x4*)(Km + (int64_t)cell * d_kv + 8 * c));
+        vv = gload((const u32x4*)(Vm + (int64_t)cell * d_kv + 8 * c));
+        gstore((u32x4*)(Kr + j * d_kv + 8 * c), kv);
+        gstore((u32x4*)(Vr + j * d_kv + 8 * c), vv);
       }
     }
     *(u32x4*)(sK + r * RS + 8 * c) = kv;
@@ -297,14 +297,14 @@ __device__ __forceinline__ void append_bf16(const Rs3CommitArgs& a, const BankDe
     for (int q = tid; q < rows * cpr; q += NT) {
       const int r = q / cpr, c = q - r * cpr;
       const int j = start + r0 + r;
-      *(u32x4*)(Kh + ((int64_t)(j >> 6) * KT + (j & 63)) * d_kv + 8 * c) = *(const u32x4*)(sK + r * RS + 8 * c);
+      gstore((u32x4*)(Kh + ((int64_t)(j >> 6) * KT + (j & 63)) * d_kv + 8 * c), *(const u32x4*)(sK + r * RS + 8 * c));
     }
     // consecutive lanes take consecutive keys of one V^ row, so that a
     // wave's stores fall in one or two 128-byte lines of the tile
     for (int q = tid; q < rows * d_kv; q += NT) {
       const int d = q / rows, r = q - d * rows;
       const int j = start + r0 + r;
-      Vh[((int64_t)(j >> 6) * d_kv + d) * KT + vslot(j & 63)] = sV[r * RS + d];
+      gstore(Vh + ((int64_t)(j >> 6) * d_kv + d) * KT + vslot(j & 63), sV[r * RS + d]);
     }
     return;
   }
@@ -321,8 +321,8 @@ __device__ __forceinline__ void append_bf16(const Rs3CommitArgs& a, const BankDe
     const bf16_t* wv = WvT + (int64_t)dcol * d_kv + 8 * g;
     f32x16 ck = {}, cv = {};
     for (int ks = 0; ks < d_kv; ks += 16) {
-      ck = mfma32(*(const u32x4*)(krow + ks), *(const u32x4*)(wk + ks), ck);   // rows = keys, cols = d
-      cv = mfma32(*(const u32x4*)(wv + ks), *(const u32x4*)(vrow + ks), cv);   // rows = d, cols = keys
+      ck = mfma32(*(const u32x4*)(krow + ks), gload((const u32x4*)(wk + ks)), ck);   // rows = keys, cols = d
+      cv = mfma32(gload((const u32x4*)(wv + ks)), *(const u32x4*)(vrow + ks), cv);   // rows = d, cols = keys
     }
     // V^ first (its accumulators are then free while K^ is turned):
     // row = d (32nb + c_row), column = key (rr)
@@ -334,7 +334,7 @@ __device__ __forceinline__ void append_bf16(const Rs3CommitArgs& a, const BankDe
       for (int r = 0; r < 16; ++r) {
         const int d = 32 * nb + c_row(r, lane);
         const int h = d >> lg_dh, dd = d & (d_h - 1);
-        Vh[((tb + h) * d_h + dd) * KT + slot] = __builtin_bit_cast(bf16_t, (__bf16)cv[r]);
+        gstore(Vh + ((tb + h) * d_h + dd) * KT + slot, __builtin_bit_cast(bf16_t, (__bf16)cv[r]));
       }
     }
     // K^: row = key (32mb + c_row), column = d (dcol)
@@ -350,9 +350,10 @@ __device__ __forceinline__ void append_bf16(const Rs3CommitArgs& a, const BankDe
         for (int r = 0; r < 16; ++r) {
           const int kr = 32 * mb + c_row(r, lane);
           const int cell = kr < rows ? min(max(src[kr], 0), a.rope_mn - 1) : 0;
-          const float2 cs = rope[(int64_t)cell * hp + p];
+          typedef float f32x2 __attribute__((ext_vector_type(2)));
+          const f32x2 cs = gload((const f32x2*)(rope + (int64_t)cell * hp + p));
           const float v = ck[r], w = __shfl_xor(v, 1);
-          ck[r] = v * cs.x + sgn * w * cs.y;
+          ck[r] = v * cs[0] + sgn * w * cs[1];
         }
       }
 #pragma unroll
@@ -360,7 +361,7 @@ __device__ __forceinline__ void append_bf16(const Rs3CommitArgs& a, const BankDe
         const int kr = 32 * mb + c_row(r, lane);
         if (kr < rows) {
           const int j = start + r0 + kr;
-          Kh[(((int64_t)(j >> 6) * H + h) * KT + (j & 63)) * d_h + dd] = __builtin_bit_cast(bf16_t, (__bf16)ck[r]);
+          gstore(Kh + (((int64_t)(j >> 6) * H + h) * KT + (j & 63)) * d_h + dd, __builtin_bit_cast(bf16_t, (__bf16)ck[r]));
         }
       }
     }
