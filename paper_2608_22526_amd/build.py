@@ -14,7 +14,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OBJDIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "librs3.so")
-SOURCES = ["select.hip", "commit.hip", "readout.hip", "attend.hip", "rope.hip", "keepset.hip", "post.hip", "fused.hip", "stack.hip", "api.hip", "profile.hip"]
+SOURCES = ["host_check.cpp", "select.hip", "commit.hip", "readout.hip", "attend.hip", "rope.hip", "keepset.hip", "post.hip", "fused.hip", "stack.hip", "api.hip", "profile.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # The attention kernel keeps its MFMA accumulators in arch VGPRs, so the
@@ -39,7 +39,7 @@ def _run(cmd):
 
 def build(jobs: int = 4, verbose: bool = False) -> str:
     os.makedirs(OBJDIR, exist_ok=True)
-    objs = [os.path.join(OBJDIR, s.replace(".hip", ".o")) for s in SOURCES]
+    objs = [os.path.join(OBJDIR, os.path.splitext(s)[0] + ".o") for s in SOURCES]
     cmds = [[HIPCC] + FLAGS + PER_FILE.get(s, []) + ["-c", os.path.join(CSRC, s), "-o", o]
             for s, o in zip(SOURCES, objs)]
     with ThreadPoolExecutor(max_workers=max(1, jobs)) as ex:

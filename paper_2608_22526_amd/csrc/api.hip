@@ -8,6 +8,7 @@
 #include <mutex>
 #include <vector>
 
+#include "host_check.h"
 #include "rs3_internal.h"
 
 using namespace rs3;
@@ -154,26 +155,15 @@ rs3_status rs3_track_export(const rs3_track* t, int32_t* state) {
 
 rs3_status rs3_track_import(rs3_track* t, const int32_t* state) {
   if (!t || !state) return RS3_E_INVALID;
-  // only states the tracker update reaches: has_box 0 or 1, a streak in
-  // [0, 2^30], an ordered non-negative box when has_box is set (pixel
-  // coordinates below 2^30) and a zero box before any box was seen
-  constexpr int32_t LIM = 1 << 30;
-  for (int o = 0; o < t->n_obj; ++o) {
-    const int32_t* w = state + o * RS3_TRACK_WORDS;
-    const int32_t y0 = w[0], x0 = w[1], y1 = w[2], x1 = w[3], streak = w[4], has = w[5];
-    if (has != 0 && has != 1) return RS3_E_INVALID;
-    if (streak < 0 || streak > LIM) return RS3_E_INVALID;
-    if (has) {
-      if (y0 < 0 || x0 < 0 || y0 > y1 || x0 > x1 || y1 >= LIM || x1 >= LIM) return RS3_E_INVALID;
-    } else if (y0 != 0 || x0 != 0 || y1 != 0 || x1 != 0) {
-      return RS3_E_INVALID;
-    }
-  }
+  // only states the tracker update reaches (host_check.h)
+  if (!rs3host::track_state_ok(t->n_obj, state)) return RS3_E_INVALID;
   hipError_t e = hipDeviceSynchronize();
   if (e == hipSuccess)
     e = hipMemcpy(t->d_state, state, (size_t)t->n_obj * RS3_TRACK_WORDS * 4, hipMemcpyHostToDevice);
   return map_err(e);
 }
+
+}  // extern "C"
 
 // ---- layer -----------------------------------------------------------------
 namespace {
@@ -219,6 +209,8 @@ std::vector<uint8_t> product_T(const void* A, const void* B, int r, int k, int c
 }
 
 }  // namespace
+
+extern "C" {
 
 rs3_status rs3_layer_create(int32_t C, int32_t H, int32_t d_kv, rs3_dtype dt, int32_t absorb, const void* Wq,
                             const void* Wk, const void* Wv, const void* Wo, rs3_layer** out) {
@@ -469,33 +461,12 @@ rs3_status rs3_bank_import(rs3_bank* b, const int32_t* hdr, const int32_t* frame
                            const int32_t* pos) {
   if (!b || !hdr) return RS3_E_INVALID;
   BankDev& h = b->host;
-  const int nf = hdr[0], pin_end = hdr[1], err = hdr[2], keys = hdr[3];
-  if (nf < 0 || nf > h.f_max || pin_end < 0 || pin_end > h.cap || keys < 0 || keys > h.cap) return RS3_E_INVALID;
-  if (nf > 0 && !frames) return RS3_E_INVALID;
-  if (keys > 0 && (!K || !V || !pos)) return RS3_E_INVALID;
-  // the snapshot must be a state the placement rule can reach: pinned frames
-  // first and packed from row 0, unpinned frames inside [pin_end, cap), no
-  // two non-empty frames overlapping, lengths adding up to the key count
-  int n_pinned = 0, pinned_rows = 0, sum = 0;
+  // the snapshot must be a state the placement rule can reach (host_check.h)
+  int32_t n_pinned = 0;
   bool unpinned = false;
-  for (int f = 0; f < nf; ++f) {
-    const int st = frames[4 * f], len = frames[4 * f + 1], pin = frames[4 * f + 3];
-    if (st < 0 || len < 0 || (int64_t)st + len > h.cap || (pin != 0 && pin != 1)) return RS3_E_INVALID;
-    if (pin) {
-      if (unpinned || st != pinned_rows) return RS3_E_INVALID;
-      ++n_pinned;
-      pinned_rows += len;
-    } else {
-      unpinned = true;
-      if (len > 0 && st < pin_end) return RS3_E_INVALID;
-    }
-    for (int q = 0; q < f; ++q) {
-      const int qs = frames[4 * q], ql = frames[4 * q + 1];
-      if (len > 0 && ql > 0 && qs < st + len && st < qs + ql) return RS3_E_INVALID;
-    }
-    sum += len;
-  }
-  if (n_pinned > h.n_pin || pinned_rows != pin_end || sum != keys) return RS3_E_INVALID;
+  if (!rs3host::bank_snapshot_ok(h.cap, h.f_max, h.n_pin, hdr, frames, K && V && pos, &n_pinned, &unpinned))
+    return RS3_E_INVALID;
+  const int nf = hdr[0], pin_end = hdr[1], err = hdr[2], keys = hdr[3];
   const rs3_layer* L = b->L;
   const int p = b->commits & 1;   // the restored state becomes the current copy
   hipError_t e = hipDeviceSynchronize();
