@@ -140,6 +140,17 @@ def _absorb(cfg, layer: str) -> bool:
     return cfg.H == 1 and cfg.d_kv < cfg.D
 
 
+def made_events(torch, n, timing=False):
+    """n events whose HIP objects exist already: torch creates an event's HIP
+    object on its first record, which costs 10-40 us of host time, so every
+    event a timed region records is recorded once here, before it starts."""
+    evs = [torch.cuda.Event(enable_timing=timing) for _ in range(n)]
+    for e in evs:
+        e.record()
+    torch.cuda.synchronize()
+    return evs
+
+
 class QueueWindow:
     """Keeps at most about `window` frames queued ahead of the GPU: every
     `every` frames an event is recorded, and before queueing more the host
@@ -150,8 +161,8 @@ class QueueWindow:
     def __init__(self, torch, window=48, every=8):
         self.torch, self.window, self.every = torch, window, every
         self.events = {}
-        # events are created here, outside any timed region, and reused
-        self.pool = [torch.cuda.Event() for _ in range(window // every + 2)]
+        # events are made here, outside any timed region, and reused
+        self.pool = made_events(torch, window // every + 2)
 
     def before(self, i):
         if i % self.every == 0:
@@ -177,7 +188,7 @@ def _fixed_keepset(torch, rs3, sess, cfg, seed_masks, D_w):
     lo, hi = fall_counts("0.05", "0.95", cfg.mn)
     keep = torch.zeros((cfg.n_obj, cfg.mn), dtype=torch.uint8, device="cuda")
     counts = torch.zeros(2, dtype=torch.int32, device="cuda")
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev = made_events(torch, 2, timing=True)
     rs3.write_keepset(sess.grid, cfg.n_obj, seed_masks, D_w, lo, hi, cfg.n_obj, keep, counts)   # warm
     ev[0].record()
     for _ in range(10):
@@ -298,7 +309,7 @@ def gpu_run(args):
         step()
     torch.cuda.synchronize()
     # pass A: frames/s, no instrumentation
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0, ev1 = made_events(torch, 2, timing=True)
     qw = QueueWindow(torch)
     enq = []
     torch.cuda.synchronize()
@@ -526,9 +537,10 @@ def gpu_run_stack(args):
         step()
     torch.cuda.synchronize()
     main = torch.cuda.current_stream()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0, ev1 = made_events(torch, 2, timing=True)
     qw = QueueWindow(torch, window=16, every=4)
     enq = []
+    torch.cuda.synchronize()
     ev0.record(main)
     h0 = time.perf_counter()
     for i in range(args.steps):
@@ -624,7 +636,7 @@ def _graph_pass(torch, step, steps):
         g.replay()
     torch.cuda.synchronize()
     reps = max(1, -(-steps // N_DISTINCT))
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0, e1 = made_events(torch, 2, timing=True)
     e0.record()
     for _ in range(reps):
         g.replay()
@@ -739,7 +751,7 @@ def run_workload(cfg, *, absorb, steps, warmup, commit=True, prefill=None, split
             torch.cuda.synchronize()
         step()
     torch.cuda.synchronize()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    ev = made_events(torch, steps + 1, timing=True)
     ev[0].record()
     for i in range(steps):
         if i >= 48:
@@ -845,7 +857,7 @@ def copy_bandwidth(mib: int = 512, reps: int = 10):
         rs3.readout(layer, (m, n, 1), n_obj, X, m * n * C, banks, sel, cnt, m * n, 0, 0, Y, m * n * C, ws=ws)
     once()
     torch.cuda.synchronize()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev = made_events(torch, 2, timing=True)
     ev[0].record()
     for _ in range(reps):
         once()
@@ -873,8 +885,7 @@ def run_post(n_obj, H, W, k=9, reps=50):
     pal = torch.empty((H, W), dtype=torch.uint8, device="cuda")
     for _ in range(5):
         rs3.close_masks(n_obj, H, W, L, rs3.RS3_BF16, k, closed, pal, ws)
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    torch.cuda.synchronize()
+    ev = made_events(torch, 2, timing=True)
     ev[0].record()
     for _ in range(reps):
         rs3.close_masks(n_obj, H, W, L, rs3.RS3_BF16, k, closed, pal, ws)
