@@ -287,7 +287,9 @@ rs3_status rs3_commit(rs3_bank* const* banks /*[host]*/, int32_t n_obj, const rs
  * the readout's split merge and the commit in one launch for bf16 layers:
  * the merge reads the attention partials, X and W_o and writes Y, the commit
  * writes the banks, so their work-groups run side by side (Algorithm 1 writes
- * a frame to memory right after its readout).  Both argument sets are checked
+ * a frame to memory right after its readout).  Calls whose two parts come to
+ * more than 1,024 work-groups (many objects) run them as two launches, which
+ * fit the chip better at that size.  Both argument sets are checked
  * before any device work; either failing returns RS3_E_INVALID with no state
  * changed.  When the selection list and the commit both find device errors,
  * the bank's sticky word keeps whichever is recorded first. */
@@ -486,7 +488,7 @@ enum {
   RS3_K_ATTN = 6,          /* split-KV attention */
   RS3_K_COMBINE = 7,       /* split merge + W_o + residual + scatter */
   RS3_K_READOUT_F32 = 8,   /* fp32 readout */
-  RS3_K_MERGE_COMMIT = 9,  /* split merge and commit in one launch (rs3_readout_commit) */
+  RS3_K_MERGE_COMMIT = 9,  /* split merge and commit in one launch (rs3_readout_commit, rs3_frame) */
   RS3_K_STACK_GEMM = 10,   /* stack: QKV product, and W_os + LN2 + cross-attention queries */
   RS3_K_STACK_MERGE = 11,  /* stack: split merge of its attentions */
   RS3_K_STACK_MLP = 12,    /* stack: W_vo + LN3 + MLP chunk partials */

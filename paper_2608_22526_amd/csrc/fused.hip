@@ -52,12 +52,23 @@ hipError_t rs3_fused_setup() {
   return e;
 }
 
+// Work-groups of the fused launch beyond which the merge and the commit run
+// as two launches: a fused work-group has the commit's 1,024 threads, whose
+// register count (126) allows one per CU, while the merge's 512-thread
+// blocks fit two per CU on their own (149 us fused against 75 + 34 us
+// separate at 64 objects of 898 selected rows).
+constexpr int FUSE_MAX_WGS = 1024;
+
 hipError_t rs3_launch_merge_commit(const Rs3ReadoutArgs& ra, const Rs3CommitArgs& ca, int d_kv, hipStream_t st) {
   const int rb = cb_rows_for(ra.D, ra.n_obj, ra.max_sel), n_cb = ra.n_obj * ((ra.max_sel + rb - 1) / rb);
   const int mn = ca.m * ca.n;
   Rs3CommitArgs c = ca;
   c.rows_per_wg = commit_rows_per_wg(ca.n_obj, mn);
   const int n_cp = ca.n_obj * (1 + (mn + c.rows_per_wg - 1) / c.rows_per_wg);
+  if (n_cb + n_cp > FUSE_MAX_WGS) {
+    hipError_t e = rs3_launch_combine(ra, st);
+    return e == hipSuccess ? rs3_launch_commit(ca, RS3_BF16, d_kv, 0, 0, 0, st) : e;
+  }
   const size_t lds = merge_commit_lds(ra.D, d_kv);
   if (ra.y_fp32)
     RS3_LAUNCH(RS3_K_MERGE_COMMIT, st, (k_merge_commit<float, true>), dim3(n_cb + n_cp), dim3(CP_THREADS), lds, st,

@@ -1655,6 +1655,10 @@ hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, const Rs3AttnBanks& ab, i
     if (pending) *pending = true;
     return hipSuccess;
   }
+  return rs3_launch_combine(a, st);
+}
+
+hipError_t rs3_launch_combine(const Rs3ReadoutArgs& a, hipStream_t st) {
   const size_t lds = combine_lds_bytes(a.D);
   const int rb = cb_rows_for(a.D, a.n_obj, a.max_sel);
   const dim3 cgrid(a.n_obj, (a.max_sel + rb - 1) / rb);

@@ -313,6 +313,8 @@ hipError_t rs3_launch_readout(const Rs3ReadoutArgs& a, const Rs3AttnBanks& ab, i
                               bool merge = true, bool* pending = nullptr);
 // The readout's split merge and a commit in one launch (bf16 layers).
 hipError_t rs3_launch_merge_commit(const Rs3ReadoutArgs& ra, const Rs3CommitArgs& ca, int d_kv, hipStream_t st);
+// The readout's split merge, output projection and residual scatter alone.
+hipError_t rs3_launch_combine(const Rs3ReadoutArgs& a, hipStream_t st);
 hipError_t rs3_fused_setup();
 // Split-KV attention only; project: the queries are projected from X[sel]
 // inside the kernel (heads of width <= 64), else read from a.Q.

@@ -3,7 +3,8 @@ merge and the commit sharing one launch) through the C ABI against the fp64
 oracle: outputs within 2e-2 (bf16) or 1e-4 (fp32), unselected rows
 bit-identical, banks bit-exact after every fused call, for one object in
 both layer modes, eight objects with per-object lists and out-of-place
-outputs, fp32 outputs, a rotary layer, the fp32 path (no merge launch), a frame
+outputs (past 1,024 work-groups, where the merge and the commit run as two
+launches), fp32 outputs, a rotary layer, the fp32 path (no merge launch), a frame
 with an empty selection, and forced key-split counts from 1 to 100."""
 from dataclasses import replace
 
@@ -70,3 +71,24 @@ def test_fused_forced_splits(absorb, n_splits):
     # than resident tiles (empty splits with l = 0, whose O is never written)
     cfg = replace(CONFIGS["sam2_single"], m=32, n=32, f_max=4, cap_frames=4)
     _fused_run(cfg, 6, 2, rows=64, absorb=absorb, n_splits=n_splits)
+
+
+@pytest.mark.parametrize("n_obj,two", [(1, False), (2, False), (8, True)])
+def test_fused_launch_shape(n_obj, two):
+    # The merge and the commit share one launch while the two parts come to
+    # at most 1,024 work-groups, else run as the readout's merge launch and
+    # the commit launch; both shapes against the oracle, banks bit-exact.
+    # At max_sel 1228 on 64x64 grids: 77 merge blocks (16 rows) and 65 commit
+    # blocks per object, 1,136 at eight objects.
+    import paper_2608_22526_amd as rs3
+    cfg = CONFIGS["sam2_single"] if n_obj == 1 else replace(CONFIGS["multi_obj8"], n_obj=n_obj)
+    rs3.profile_enable(True, 256)
+    rs3.profile_reset()
+    try:
+        _fused_run(cfg, 9, 7, rows=24, max_sel=1228, absorb=True)
+        rep = rs3.profile_report()
+    finally:
+        rs3.profile_enable(False)
+    fused, merge, commit = rep["merge_commit"][1], rep["combine"][1], rep["commit"][1]
+    calls = 2   # frames 7 and 8 in one call each; frames 0-6 by rs3_commit
+    assert (fused, merge, commit) == ((0, calls, 7 + calls) if two else (calls, 0, 7))
