@@ -1225,6 +1225,11 @@ std::vector<uint16_t> product_bits(const void* A, const void* B, int r, int k, i
   return out;
 }
 
+// Hidden units per work-group of the MLP launch: 128 gives F/128 x ceil(M/64)
+// work-groups (240 at 957 kept rows and F = 2048), each with half the
+// weights of a 256-wide chunk, for twice the fp32 partials.
+constexpr int STACK_HC = 128;
+
 // Key splits of the self-attention: a launch of about 256 work-groups
 // (8*n_qt*ceil(H_s*S/8)), at least two key tiles per split.
 int stack_self_splits(int M, int Hs) {
@@ -1254,7 +1259,7 @@ void stack_layout(const rs3_stack* S, int M, int S_c, StackLayout* L) {
   };
   L->z = take((size_t)M * C * 4);
   L->zp = take((size_t)M * C * 4);
-  L->part = take((size_t)(S->F / 256) * M * C * 4);
+  L->part = take((size_t)(S->F / STACK_HC) * M * C * 4);
   L->a1 = take((size_t)M * C * 2);
   L->qs = take((size_t)M * C * 2);
   L->qc = take((size_t)M * S->d_kv * 2);
@@ -1407,7 +1412,7 @@ rs3_status rs3_stack_readout(const rs3_stack* S, const rs3_grid* g, const void* 
   p.Z = (float*)(w + L.z);
   p.Zp = (float*)(w + L.zp);
   p.P = (float*)(w + L.part);
-  p.NC = S->F / 256;
+  p.NC = S->F / STACK_HC;
   p.F = S->F;
   p.A1 = (bf16_t*)(w + L.a1);
   p.Qs = (bf16_t*)(w + L.qs);

@@ -23,7 +23,7 @@
 //   k_stk_post_sa  32 whole rows per work-group: z += O W_os, LN2, queries of
 //                  the cross-attention (x W_q W_k^T)
 //   k_attn         cross-attention; k_stk_merge merges its key splits
-//   k_stk_mlp      64 rows x 256 hidden units per work-group: z' = z + O W_vo
+//   k_stk_mlp      32 rows x 128 hidden units per work-group: z' = z + O W_vo
 //                  (kept by the first hidden chunk), LN3, relu(. W_1[:, chunk])
 //                  W_2[chunk, :] -> an fp32 partial per chunk
 //   k_stk_rows     z = z' + the partials in chunk order, then the next
@@ -390,24 +390,35 @@ __global__ __launch_bounds__(256) void k_stk_post_sa(StkArgs p) {
   }
 }
 
-// grid (ceil(n/64), F/256), block 256, LDS ML_LDS: rows [64 bx, +64) and
-// hidden units [256 by, +256).
+// grid (ceil(n/RM), F/HC), block 256, LDS MlLds<RM>::BYTES: rows [RM bx, +RM)
+// and hidden units [HC by, +HC).
 //   z' = z + O W_vo            (O: the cross-attention's merged output, in Qc;
 //                               the chunk-0 work-group stores z' to Zp)
 //   P[by] = relu(LN3(z') W_1[:, chunk]) W_2[chunk, :]    (fp32)
-// Wave w holds output columns [64w, 64w+64) of every product, both 32-row
-// halves (four 32x32 tiles).  The hidden units reuse the LDS of z'.
+// Wave w holds output columns [64w, 64w+64) of the W_vo and W_2 products and
+// HC/4 hidden units of the W_1 product, for every 32-row half.  The hidden
+// units reuse the LDS of z'.  At 32 rows a work-group takes 54 KB of LDS, so
+// two share a CU and one's memory waits run under the other's work.
 constexpr int ML_OP = 64 + 8;   // LDS pitch of the 64-wide O rows
-constexpr size_t ML_O = 0, ML_A = 64 * ML_OP * 2, ML_Z = ML_A + 64 * SG_PITCH * 2;
-constexpr size_t ML_LDS = ML_Z + 64 * SG_C * 4;
+template <int RM>
+struct MlLds {
+  static constexpr size_t O = 0, A = RM * ML_OP * 2, Z = A + RM * SG_PITCH * 2, BYTES = Z + RM * SG_C * 4;
+};
+constexpr int STACK_MLP_RM = 32;   // rows per work-group of the launch
+template <int HC, int RM>
 __global__ __launch_bounds__(256) void k_stk_mlp(StkArgs p) {
+  static_assert(HC == 256 || HC == 128, "hidden units per work-group");
+  static_assert(RM == 64 || RM == 32, "rows per work-group");
+  constexpr int TW = HC / 128;   // 32-column blocks of the hidden chunk per wave
+  constexpr int NI = RM / 32;    // 32-row halves
+  using LL = MlLds<RM>;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
-  bf16_t* Ob = (bf16_t*)(lds + ML_O);
-  bf16_t* As = (bf16_t*)(lds + ML_A);
-  float* Zs = (float*)(lds + ML_Z);
-  bf16_t* Hs = (bf16_t*)(lds + ML_Z);   // after LN3
+  bf16_t* Ob = (bf16_t*)(lds + LL::O);
+  bf16_t* As = (bf16_t*)(lds + LL::A);
+  float* Zs = (float*)(lds + LL::Z);
+  bf16_t* Hs = (bf16_t*)(lds + LL::Z);   // after LN3
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int row0 = blockIdx.x * 64, chunk = blockIdx.y;
+  const int row0 = blockIdx.x * RM, chunk = blockIdx.y;
   const int cnt = stk_count(p);
   if (row0 >= cnt) return;
   u32x4 bv[2][4];
@@ -415,38 +426,38 @@ __global__ __launch_bounds__(256) void k_stk_mlp(StkArgs p) {
   for (int t = 0; t < 2; ++t)
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) bv[t][ks] = ldb(p.Wvo, 4, 2 * wave + t, ks, lane);
-  u32x4 ov[2];
+  u32x4 ov[NI];
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+  for (int j = 0; j < NI; ++j) {
     const int u = tid + 256 * j, r = u >> 3, c8 = u & 7;
     ov[j] = gload((const u32x4*)(p.Qc + (int64_t)min(row0 + r, cnt - 1) * 64 + 8 * c8));
   }
-  f32x4 zv[16];
+  f32x4 zv[RM / 4];
 #pragma unroll
-  for (int j = 0; j < 16; ++j) {
+  for (int j = 0; j < RM / 4; ++j) {
     const int u = tid + 256 * j, r = u >> 6, c4 = u & 63;
     zv[j] = gload((const f32x4*)(p.Z + (int64_t)min(row0 + r, cnt - 1) * SG_C + 4 * c4));
   }
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+  for (int j = 0; j < NI; ++j) {
     const int u = tid + 256 * j, r = u >> 3, c8 = u & 7;
     *(u32x4*)(Ob + r * ML_OP + 8 * c8) = row0 + r < cnt ? ov[j] : u32x4{0, 0, 0, 0};
   }
 #pragma unroll
-  for (int j = 0; j < 16; ++j) {
+  for (int j = 0; j < RM / 4; ++j) {
     const int u = tid + 256 * j, r = u >> 6, c4 = u & 63;
     *(f32x4*)(Zs + r * SG_C + 4 * c4) = zv[j];
   }
   __syncthreads();
-  f32x16 acc[2][2];
+  f32x16 acc[NI][2];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < NI; ++i)
 #pragma unroll
     for (int t = 0; t < 2; ++t) acc[i][t] = f32x16{};
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < NI; ++i) {
       const u32x4 a = lda(Ob, ML_OP, 32 * i, ks, lane);
 #pragma unroll
       for (int t = 0; t < 2; ++t) acc[i][t] = mfma32(a, bv[t][ks], acc[i][t]);
@@ -454,11 +465,11 @@ __global__ __launch_bounds__(256) void k_stk_mlp(StkArgs p) {
   // W_1 operands of this hidden chunk, in flight over the residual and the norm
   u32x4 bw[2][16];
 #pragma unroll
-  for (int t = 0; t < 2; ++t)
+  for (int t = 0; t < TW; ++t)
 #pragma unroll
-    for (int ks = 0; ks < 16; ++ks) bw[t][ks] = ldb(p.W1, 16, 8 * chunk + 2 * wave + t, ks, lane);
+    for (int ks = 0; ks < 16; ++ks) bw[t][ks] = ldb(p.W1, 16, (HC / 32) * chunk + TW * wave + t, ks, lane);
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < NI; ++i)
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -467,7 +478,7 @@ __global__ __launch_bounds__(256) void k_stk_mlp(StkArgs p) {
   __syncthreads();
   if (chunk == 0) {
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
+    for (int j = 0; j < RM / 4; ++j) {
       const int u = tid + 256 * j, r = u >> 6, c4 = u & 63;
       if (row0 + r < cnt)
         *(f32x4*)(p.Zp + (int64_t)(row0 + r) * SG_C + 4 * c4) = *(const f32x4*)(Zs + r * SG_C + 4 * c4);
@@ -476,58 +487,60 @@ __global__ __launch_bounds__(256) void k_stk_mlp(StkArgs p) {
   {
     const f32x4 g = gload((const f32x4*)(p.ln3_g + 4 * lane));
     const f32x4 b = gload((const f32x4*)(p.ln3_b + 4 * lane));
-    f32x4 zz[16];
+    constexpr int RW = RM / 4;   // rows per wave
+    f32x4 zz[RW];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) zz[i] = *(const f32x4*)(Zs + (16 * wave + i) * SG_C + 4 * lane);
+    for (int i = 0; i < RW; ++i) zz[i] = *(const f32x4*)(Zs + (RW * wave + i) * SG_C + 4 * lane);
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
+    for (int i = 0; i < RW; ++i) {
       u32x2 y = ln_row(zz[i], g, b);
-      if (row0 + 16 * wave + i >= cnt) y = u32x2{0, 0};
-      *(u32x2*)(As + (16 * wave + i) * SG_PITCH + 4 * lane) = y;
+      if (row0 + RW * wave + i >= cnt) y = u32x2{0, 0};
+      *(u32x2*)(As + (RW * wave + i) * SG_PITCH + 4 * lane) = y;
     }
   }
   __syncthreads();   // LN3 rows complete; z' no longer read (its LDS takes the hidden units)
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < NI; ++i)
 #pragma unroll
     for (int t = 0; t < 2; ++t) acc[i][t] = f32x16{};
 #pragma unroll
   for (int ks = 0; ks < 16; ++ks)
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < NI; ++i) {
       const u32x4 a = lda(As, SG_PITCH, 32 * i, ks, lane);
 #pragma unroll
-      for (int t = 0; t < 2; ++t) acc[i][t] = mfma32(a, bw[t][ks], acc[i][t]);
+      for (int t = 0; t < TW; ++t) acc[i][t] = mfma32(a, bw[t][ks], acc[i][t]);
     }
-  // W_2 operands: rows [256 chunk, +256) of W_2 are its steps [16 chunk, +16)
+  // W_2 operands: rows [HC chunk, +HC) of W_2 are its steps [HC/16 chunk, +HC/16)
+  constexpr int KS2 = HC / 16;
 #pragma unroll
   for (int t = 0; t < 2; ++t)
 #pragma unroll
-    for (int ks = 0; ks < 16; ++ks) bw[t][ks] = ldb(p.W2, p.F / 16, 2 * wave + t, 16 * chunk + ks, lane);
+    for (int ks = 0; ks < KS2; ++ks) bw[t][ks] = ldb(p.W2, p.F / 16, 2 * wave + t, KS2 * chunk + ks, lane);
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < NI; ++i)
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int t = 0; t < TW; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r)
-        Hs[(32 * i + c_row(r, lane)) * SG_PITCH + 64 * wave + 32 * t + (lane & 31)] =
+        Hs[(32 * i + c_row(r, lane)) * SG_PITCH + 32 * TW * wave + 32 * t + (lane & 31)] =
             f2bf(fmaxf(acc[i][t][r], 0.f));
   __syncthreads();
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < NI; ++i)
 #pragma unroll
     for (int t = 0; t < 2; ++t) acc[i][t] = f32x16{};
 #pragma unroll
-  for (int ks = 0; ks < 16; ++ks)
+  for (int ks = 0; ks < KS2; ++ks)
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < NI; ++i) {
       const u32x4 a = lda(Hs, SG_PITCH, 32 * i, ks, lane);
 #pragma unroll
       for (int t = 0; t < 2; ++t) acc[i][t] = mfma32(a, bw[t][ks], acc[i][t]);
     }
   float* P = p.P + (int64_t)chunk * p.M * SG_C;
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < NI; ++i)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int row = row0 + 32 * i + c_row(r, lane);
@@ -584,8 +597,13 @@ hipError_t rs3_launch_stack_post_sa(const StkArgs& p, hipStream_t st) {
 
 hipError_t rs3_launch_stack_mlp(const StkArgs& p, hipStream_t st) {
   if (p.M <= 0) return hipSuccess;
-  if (p.F % 256 != 0 || p.NC != p.F / 256) return hipErrorInvalidValue;
-  RS3_LAUNCH(RS3_K_STACK_MLP, st, k_stk_mlp, dim3((unsigned)((p.M + 63) / 64), p.NC), dim3(256), ML_LDS, st, p);
+  if (p.F % 256 != 0 || (p.NC != p.F / 256 && p.NC != p.F / 128)) return hipErrorInvalidValue;
+  constexpr int RM = STACK_MLP_RM;
+  const dim3 grid((unsigned)((p.M + RM - 1) / RM), p.NC);
+  if (p.NC == p.F / 128)
+    RS3_LAUNCH(RS3_K_STACK_MLP, st, (k_stk_mlp<128, RM>), grid, dim3(256), MlLds<RM>::BYTES, st, p);
+  else
+    RS3_LAUNCH(RS3_K_STACK_MLP, st, (k_stk_mlp<256, RM>), grid, dim3(256), MlLds<RM>::BYTES, st, p);
   return hipGetLastError();
 }
 
@@ -609,7 +627,12 @@ hipError_t rs3_launch_stack_copy(const void* X, void* Y, int64_t elems, int y_f3
 }
 
 hipError_t rs3_stack_setup() {
-  hipError_t e = hipFuncSetAttribute((const void*)k_stk_mlp, hipFuncAttributeMaxDynamicSharedMemorySize, (int)ML_LDS);
+  constexpr int RM = STACK_MLP_RM;
+  hipError_t e = hipFuncSetAttribute((const void*)k_stk_mlp<256, RM>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     (int)MlLds<RM>::BYTES);
+  if (e == hipSuccess)
+    e = hipFuncSetAttribute((const void*)k_stk_mlp<128, RM>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)MlLds<RM>::BYTES);
   if (e == hipSuccess)
     e = hipFuncSetAttribute((const void*)k_stk_post_sa, hipFuncAttributeMaxDynamicSharedMemorySize, (int)PS_LDS);
   return e;
