@@ -206,6 +206,10 @@ def gpu_run(args):
     from workloads import CONFIGS, make_frame, make_sequence, make_weights
 
     cfg = CONFIGS[args.workload]
+    if args.objects:
+        # that many objects per call, each on a grid of its own
+        from dataclasses import replace
+        cfg = replace(cfg, n_obj=args.objects, shared_x=False, union_objects=False)
     dev = "cuda"
     n_pre = cfg.f_max
     seq = make_sequence(cfg, n_frames=n_pre + N_DISTINCT)
@@ -977,6 +981,8 @@ def main():
                     help="untimed frames first; the HIP runtime grows its launch-argument pool once "
                          "(a stall of tens of ms) after the first thousand-odd launches of a process")
     ap.add_argument("--workload", default="sam2_single")
+    ap.add_argument("--objects", type=int, default=0,
+                    help="objects per call (at most 64), each on a grid of its own; 0 keeps the workload's")
     ap.add_argument("--splits", type=int, default=0)
     ap.add_argument("--write-dw", type=int, default=-1,
                     help="write every frame at the fixed keep-set K_w of this dilation radius (Eq. 8), built "
@@ -1021,6 +1027,10 @@ def main():
         print("bench.py measures one MI355X: the path runs on a single GPU (objects or bank frames would be "
               "sharded across GPUs with no exchange, which this benchmark does not launch). Use --gpus 1.",
               file=sys.stderr)
+        sys.exit(2)
+    if args.objects and (args.objects > 64 or args.stack or not args.no_cpu_baseline):
+        print("--objects takes 1 to 64 objects per call, without --stack, with --no-cpu-baseline (the oracle "
+              "baseline times the workload's own objects)", file=sys.stderr)
         sys.exit(2)
     if args.post_only:
         for (no, H, W) in ((1, 256, 256), (8, 256, 256), (1, 1024, 1024), (8, 1024, 1024)):
