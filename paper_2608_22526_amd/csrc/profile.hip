@@ -1,6 +1,7 @@
 // Optional per-kernel timing with HIP events.  When enabled, every kernel the
-// library launches is bracketed by a pair of events recorded on the stream it
-// runs on; rs3_profile_report() waits for them and returns per-kernel totals.
+// library launches carries a pair of events that the runtime stamps with the
+// kernel's own start and end (hipExtLaunchKernelGGL);
+// rs3_profile_report() waits for them and returns per-kernel totals.
 // The event pool is created at enable time, so timed calls allocate nothing.
 #include <vector>
 
@@ -18,7 +19,6 @@ struct ProfState {
   std::vector<hipEvent_t> ev;
   std::vector<Rec> recs;
   int next = 0;
-  int open_id = -1;
   double total_ms[RS3_K_COUNT] = {};
   int64_t count[RS3_K_COUNT] = {};
   int64_t dropped = 0;
@@ -43,27 +43,17 @@ hipError_t fold() {
 
 }  // namespace
 
-void rs3_prof_begin(int id, hipStream_t st) {
-  if (!P.on) return;
+bool rs3_prof_events(int id, hipEvent_t* start, hipEvent_t* stop) {
+  if (!P.on) return false;
   if (P.next + 2 > (int)P.ev.size()) {
     ++P.dropped;
-    P.open_id = -1;
-    return;
+    return false;
   }
-  if (hipEventRecord(P.ev[P.next], st) != hipSuccess) {
-    P.open_id = -1;
-    return;
-  }
-  P.open_id = id;
-}
-
-void rs3_prof_end(int id, hipStream_t st) {
-  if (!P.on || P.open_id != id) return;
-  if (hipEventRecord(P.ev[P.next + 1], st) == hipSuccess) {
-    P.recs.push_back(Rec{id, P.next});
-    P.next += 2;
-  }
-  P.open_id = -1;
+  *start = P.ev[P.next];
+  *stop = P.ev[P.next + 1];
+  P.recs.push_back(Rec{id, P.next});
+  P.next += 2;
+  return true;
 }
 
 extern "C" {

@@ -3,6 +3,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 #include <stdint.h>
 
 #include "rs3.h"
@@ -340,15 +341,21 @@ hipError_t rs3_launch_close_masks(int n_obj, int H, int W, const void* logits, i
                                   uint8_t* palette, void* ws, hipStream_t st);
 // Fills the axial rotary table (see rs3_layer_set_rope_axial).
 hipError_t rs3_launch_rope_axial(float* table, int m, int n, int d_h, double theta, hipStream_t st);
-void rs3_prof_begin(int id, hipStream_t st);
-void rs3_prof_end(int id, hipStream_t st);
+// While profiling is on: the next free pair of the event pool for a launch
+// of kernel ID (false when profiling is off or the pool is full).
+bool rs3_prof_events(int id, hipEvent_t* start, hipEvent_t* stop);
 
-// Launch a kernel bracketed by the optional profiling events.
-#define RS3_LAUNCH(ID, ST, ...)  \
-  do {                           \
-    rs3_prof_begin((ID), (ST));  \
-    hipLaunchKernelGGL(__VA_ARGS__); \
-    rs3_prof_end((ID), (ST));    \
+// Launch a kernel; while profiling is on, through hipExtLaunchKernelGGL with
+// a start and a stop event, which the runtime stamps with the kernel's own
+// begin and end (the dispatch gap before it is not counted).  ST is the
+// stream, also passed in the launch arguments.
+#define RS3_LAUNCH(ID, ST, K, G, B, SHM, S, ...)                                   \
+  do {                                                                            \
+    hipEvent_t rs3_e0_, rs3_e1_;                                                  \
+    if (rs3_prof_events((ID), &rs3_e0_, &rs3_e1_))                                \
+      hipExtLaunchKernelGGL(K, G, B, SHM, S, rs3_e0_, rs3_e1_, 0u, __VA_ARGS__);  \
+    else                                                                          \
+      hipLaunchKernelGGL(K, G, B, SHM, S, __VA_ARGS__);                           \
   } while (0)
 // The stack's launches (stack.hip): k_stk_rows (mode 0 gather + LN1,
 // 1 partial sum + LN1, 2 partial sum + scatter), the QKV product, the
