@@ -407,8 +407,9 @@ rs3_status rs3_attend(const void* Qh, const void* Kh, const void* Vh, int32_t n_
 
 /* ---- the L-layer memory-attention stack on the kept queries -----------------
  * Sec. 3.1 ("Sparse memory attention"): the memory attention of the VOS model
- * is a stack of L self-/cross-attention layers, patched at every layer's
- * entry so that each layer runs on the kept queries only.  The paper gives no
+ * is a stack of L self-/cross-attention layers, and the sparse readout
+ * applies at the input of each, so that every layer runs on the kept
+ * queries only.  The paper gives no
  * layer, so the layer is this pre-norm residual one, in the shape of
  * SAM2-class memory attention (z the fp32 residual stream of a kept row):
  *   z += SA(LN1(z))    self-attention among the kept rows: H_s heads of

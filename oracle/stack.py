@@ -2,9 +2,10 @@
 infrastructure; see package doc).
 
 Sec. 3.1 ("Sparse memory attention"): the VOS model's memory attention is a
-stack of L self-/cross-attention layers, and the patch gathers the kept
-queries at every layer's entry, runs the layer on them only, and scatters
-the result with zeros at the dropped positions.  The paper defines no layer
+stack of L self-/cross-attention layers, and the sparse readout applies at
+the input of each of them: the kept queries are gathered, the layer runs on
+them only, and the result is scattered back with zeros at the dropped
+positions.  The paper defines no layer
 and its trained weights are not available, so the stack here is a reading
 with synthetic weights:
 
@@ -25,7 +26,7 @@ with synthetic weights:
   * the linear maps have no bias;
   * the rows are gathered once before the first layer and scattered once
     after the last: a dropped row gets a zero update at every layer (the
-    residual reading U1 of `readout`), so gathering at every layer's entry
+    residual reading U1 of `readout`), so gathering at the input of each layer
     gives the same result; the dropped rows come back bit for bit;
   * no norm follows the last layer (it would change the dropped rows).
 

@@ -1,5 +1,6 @@
 // The L-layer memory-attention stack on the kept queries (Sec. 3.1, "Sparse
-// memory attention": the stack is patched at every layer's entry).  The rows
+// memory attention": the sparse readout applies at the input of each layer
+// of the memory-attention stack, not only the first).  The rows
 // are gathered once before the first layer and scattered once after the
 // last; in between, every layer is
 //     z += SA(LN1(z))  among the kept rows      (one-frame bank of the kept rows)

@@ -1,6 +1,7 @@
 """Pins for the oracle's L-layer memory-attention stack on the kept queries
-(Sec. 3.1, "Sparse memory attention": the stack is patched at every layer's
-entry; the layer itself is the reading stated in oracle/stack.py).
+(Sec. 3.1, "Sparse memory attention": the sparse readout applies at the
+input of each layer; the layer itself is the reading stated in
+oracle/stack.py).
 
 Each pin holds for a reason outside the stack code: a textbook closed form
 (LayerNorm moments, softmax over one key), a reduction to the separately
@@ -151,7 +152,7 @@ def test_self_attention_couples_the_kept_rows_only():
 
 
 def test_layers_compose():
-    # gathering once equals gathering at every layer's entry
+    # gathering once equals gathering at the input of each layer
     X, K, V = _inputs(13, N=25)
     ws = _weights(3, seed=9)
     sel = np.array([0, 5, 6, 7, 14, 21])
