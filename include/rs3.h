@@ -89,8 +89,8 @@ typedef struct rs3_bank rs3_bank;   /* one object's ring memory bank */
 const char* rs3_status_str(rs3_status s);
 
 /* ---- tracker state (Sec. 3.1, streak-counted box fallback, Eq. 5) --------
- * Holds, per object, the last non-empty bounding box in pixel coordinates
- * (inclusive), the count of consecutive empty frames and whether a box was
+ * Holds, per object, the most recent non-empty box (pixel coordinates,
+ * inclusive), the count of consecutive empty frames and whether a box was
  * ever seen.  Created zeroed (no box).  export/import copy
  * int32 [n_obj][RS3_TRACK_WORDS] host arrays and synchronise the device
  * (checkpoint and resume).  import accepts only states the tracker update
@@ -406,10 +406,10 @@ rs3_status rs3_attend(const void* Qh, const void* Kh, const void* Vh, int32_t n_
                       size_t ws_bytes, void* stream);
 
 /* ---- the L-layer memory-attention stack on the kept queries -----------------
- * Sec. 3.1 ("Sparse memory attention"): the memory attention of the VOS model
- * is a stack of L self-/cross-attention layers, and the sparse readout
- * applies at the input of each, so that every layer runs on the kept
- * queries only.  The paper gives no
+ * Sec. 3.1 ("Sparse memory attention"): the memory module of the VOS models
+ * consists of L layers, each with a self-attention and a cross-attention,
+ * and the sparse readout applies at the input of every layer, so that each
+ * runs on the kept queries only.  The paper gives no
  * layer, so the layer is this pre-norm residual one, in the shape of
  * SAM2-class memory attention (z the fp32 residual stream of a kept row):
  *   z += SA(LN1(z))    self-attention among the kept rows: H_s heads of

@@ -2,8 +2,8 @@
 infrastructure; see package doc).
 
 Sec. 3.3 and the end of Algorithm 1: each object's predicted binary mask is
-closed with a k x k square structuring element (k = 9 in the paper), a
-dilation followed by an erosion, at the decoder's output resolution; only
+closed with a k x k square structuring element (k = 9 in the paper): first
+dilated, then eroded, on the full-resolution decoder output; only
 then is the per-pixel argmax over objects taken to give the palette mask.
 The closed masks are what the tracker state of the next frame is updated
 from (bounding box or streak, Eq. 5).

@@ -1,11 +1,11 @@
 """The L-layer memory-attention stack on the kept queries (test
 infrastructure; see package doc).
 
-Sec. 3.1 ("Sparse memory attention"): the VOS model's memory attention is a
-stack of L self-/cross-attention layers, and the sparse readout applies at
-the input of each of them: the kept queries are gathered, the layer runs on
-them only, and the result is scattered back with zeros at the dropped
-positions.  The paper defines no layer
+Sec. 3.1 ("Sparse memory attention"): the memory module of the VOS models
+consists of L layers, each with a self-attention and a cross-attention, and
+the sparse readout applies at the input of every layer: each layer runs on
+the gathered kept queries only, and its update is zero at every dropped
+cell.  The paper defines no layer
 and its trained weights are not available, so the stack here is a reading
 with synthetic weights:
 

@@ -1,8 +1,8 @@
 """The paper's own write keep-set (test infrastructure; see package doc).
 
-Sec. 3.2, Eq. 8: each object's mask at its first-appearance frame tau_o is
-down-sampled to the encoder grid and dilated by D_w cells; the write keep-set
-K_w is the union of these regions over the objects.  It is computed once and
+Sec. 3.2, Eq. 8: for every object, take its mask in the frame tau_o where it
+is first seen, reduce it to the encoder grid by nearest-neighbour sampling
+and grow it by D_w cells; K_w is the union of the grown regions.  It is computed once and
 every later write of the sequence stores the tokens at K_w, so each stored
 frame has the same |K_w| tokens (a constant per-frame stride).  When the
 seed footprint covers more than 95 % or less than 5 % of the grid, the write

@@ -1,6 +1,7 @@
-// The paper's fixed write keep-set (Sec. 3.2, Eq. 8): K_w is the union over
-// objects of the seed masks (each object's mask at its first frame),
-// down-sampled to the encoder grid and dilated by D_w cells (Chebyshev).  It
+// The paper's fixed write keep-set (Sec. 3.2, Eq. 8): every object's seed
+// mask (its mask in the frame where it is first seen) is sampled onto the
+// encoder grid and grown by D_w cells (Chebyshev distance); K_w collects the
+// cells of all objects.  It
 // is computed once per sequence; every later write stores the tokens at K_w,
 // so every stored frame has the same length.  When the undilated footprint
 // count is below fall_min or above fall_max the write falls through to the
