@@ -70,10 +70,10 @@ __device__ __forceinline__ void part_load(const Rs3ReadoutArgs& a, int o, int ro
     const int sp = min(grp + NG * (PART_B * j + i), a.S - 1);
     const int64_t prow = ((int64_t)o * a.S + sp) * rows + rw;
     typedef float f32x2 __attribute__((ext_vector_type(2)));
-    const f32x2 ml = gload((const f32x2*)(a.ML + (prow * a.H + h) * 2));
+    const f32x2 ml = pload((const f32x2*)(a.ML + (prow * a.H + h) * 2));
     pb.m[i] = ml[0];
     pb.l[i] = ml[1];
-    pb.v[i] = gload((const u32x4*)((const bf16_t*)a.Opart + prow * a.D + d0));
+    pb.v[i] = pload((const u32x4*)((const bf16_t*)a.Opart + prow * a.D + d0));
   }
 }
 

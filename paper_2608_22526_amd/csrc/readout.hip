@@ -1299,8 +1299,8 @@ __global__ __launch_bounds__(512) void k_attn_g2(Rs3ReadoutArgs a, int G, Rs3Att
     }
   if (g == 0 && qv) {
     float* ml = a.ML + ((((int64_t)o * S + s) * a.max_sel + qrow) * a.H + h) * 2;
-    ml[0] = m_run;
-    ml[1] = l_tot;
+    pstore(ml, m_run);
+    pstore(ml + 1, l_tot);
   }
   // the staged rows of this wave are written by this wave alone: a wave-local
   // wait for its LDS stores suffices
@@ -1312,7 +1312,7 @@ __global__ __launch_bounds__(512) void k_attn_g2(Rs3ReadoutArgs a, int G, Rs3Att
   for (int q = lane; q < 32 * CH; q += 64) {
     const int rr = q / CH, c = q - rr * CH;
     const int row = row0 + 32 * wave + rr;
-    if (row < cnt) *(u32x4*)(obase + (int64_t)row * a.D + 8 * c) = *(const u32x4*)(ow + rr * OP + 16 * c);
+    if (row < cnt) pstore((u32x4*)(obase + (int64_t)row * a.D + 8 * c), *(const u32x4*)(ow + rr * OP + 16 * c));
   }
 }
 
