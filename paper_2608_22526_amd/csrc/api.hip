@@ -883,6 +883,7 @@ static rs3_status readout_args(const rs3_layer* L, const rs3_grid* g, int32_t n_
   a.n_qt = (max_sel + 127) / 128;
   a.y_fp32 = y_fp32 ? 1 : 0;
   a.rope = ld.rope;
+  a.stream_parts = 1;
   return RS3_OK;
 }
 

@@ -24,16 +24,16 @@ __device__ __forceinline__ void gstore(T* p, const T& v) {
 }
 
 // Non-temporal (streaming) accesses for data that is written once and read
-// once: the split partials.  The merge reads every partial with pload, and
-// k_attn_g2 writes them with pstore.  Measured on the 64x64 one-object
-// frame: the stores gave 1.2-1.4 % more frames/s, the loads another 1.6 %,
-// and the attention of the next frame got faster too (the partials, about
-// 3.7 MB a frame, no longer crowd the bank's key/value tiles out of the
-// L2).  The same marking on stores was slower for the energies and projected
+// once: the readout's split partials.  The merge reads every partial with
+// pload; k_attn_g2, and k_attn when the readout launches it, write them
+// with pstore.  Measured on the 64x64 one-object frame: the stores gave
+// 1.2-1.4 % more frames/s, the loads another 1.6 %, and the attention of the
+// next frame got faster too (the partials, about 3.7 MB a frame, no longer
+// crowd the bank's key/value tiles out of the L2); with k_attn's stores as
+// well the projected 64x64 frame gained 5 %, the other readout workloads
+// 0.2-0.9 %.  The same marking was slower for the energies and projected
 // queries of the energy launch, which the next launch reads back, and for
-// the partials of the stack's attentions; for k_attn's partials in the
-// other readout workloads it made no clear difference, so those keep plain
-// stores.
+// the partials of the stack's attentions, which its own merge reads.
 template <class T>
 __device__ __forceinline__ void pstore(T* p, const T& v) {
   __builtin_nontemporal_store(v, (RS3_GLOBAL T*)p);

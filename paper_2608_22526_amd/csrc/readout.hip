@@ -851,8 +851,13 @@ __global__ __launch_bounds__(256 * NG) void k_attn(Rs3ReadoutArgs a, int G) {
   if (g == 0 && qv) {
     const int64_t prow = ((int64_t)o * a.S + s) * a.max_sel + qrow;
     float* ml = a.ML + (prow * a.H + h) * 2;
-    ml[0] = m_run;
-    ml[1] = l_tot;
+    if (a.stream_parts) {
+      pstore(ml, m_run);
+      pstore(ml + 1, l_tot);
+    } else {
+      ml[0] = m_run;
+      ml[1] = l_tot;
+    }
   }
   __syncthreads();
   constexpr int CH = DH / 8;   // 16-byte chunks per row
@@ -861,7 +866,14 @@ __global__ __launch_bounds__(256 * NG) void k_attn(Rs3ReadoutArgs a, int G) {
   for (int q = lane; q < 32 * CH; q += 64) {
     const int rr = q / CH, c = q - rr * CH;
     const int row = row0 + 32 * wave + rr;
-    if (row < cnt) *(u32x4*)(obase + (int64_t)row * a.D + 8 * c) = *(const u32x4*)(ow + rr * OP + 16 * c);
+    if (row < cnt) {
+      u32x4* dst = (u32x4*)(obase + (int64_t)row * a.D + 8 * c);
+      const u32x4 v = *(const u32x4*)(ow + rr * OP + 16 * c);
+      if (a.stream_parts)
+        pstore(dst, v);
+      else
+        *dst = v;
+    }
   }
 }
 

@@ -216,6 +216,8 @@ struct Rs3ReadoutArgs {
   const float* rope;      // [mn][d_h/2][2] rotary table for the queries, or null
   const void* Qall;       // queries of every cell projected by the energy launch (rs3_frame), or null:
   int64_t qall_stride;    //   [n_x][mn][64] bf16, elements between objects' grids (0 = shared)
+  int stream_parts;       // 1: the split partials are stored non-temporally (the readout's merge
+                          //   reads them once, non-temporally); 0: plain stores (stack, attend)
 };
 
 // The attention-side pointers of every object's bank, handed to the
