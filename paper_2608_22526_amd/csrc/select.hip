@@ -152,6 +152,85 @@ __device__ __forceinline__ void energy_block(const T* __restrict__ X, int64_t x_
   }
 }
 
+// Wide form for large batches (no projection): 256 rows per 256-thread
+// block, one row per thread, read in column slices of EW_CH 16-byte chunks
+// per row with coalesced loads through LDS (row pitch EW_CH + 1 chunks).
+// The next slice's loads are issued before the current slice's sums, so the
+// loads run under the four waves' sums, and every wave sums (the 64-row
+// form sums in one wave while three wait).  Each wave writes the smallest
+// and largest energy bits of its 64 rows to range[xi][64-row block], the
+// layout of the 64-row form.
+constexpr int EW_CH = 8;
+constexpr int EW_ROWS = 256;
+template <typename T>
+__device__ __forceinline__ void energy_block_wide(const T* __restrict__ X, int64_t x_stride, int mn, int C,
+                                                  double* __restrict__ e, unsigned long long* __restrict__ range,
+                                                  int bx, int xi) {
+  __shared__ u32x4 rows[EW_ROWS * (EW_CH + 1)];
+  const int r0 = bx * EW_ROWS, tid = threadIdx.x;
+  const int nrows = min(EW_ROWS, mn - r0);
+  const int cpr = C * (int)sizeof(T) / 16;   // chunks per row
+  const int npass = (cpr + EW_CH - 1) / EW_CH;
+  const u32x4* src = (const u32x4*)(X + (int64_t)xi * x_stride + (int64_t)r0 * C);
+  // slot q = tid + 256 k of the slice at chunk cb: row q / EW_CH, chunk
+  // q % EW_CH (chunks past a short last slice, and rows past the grid,
+  // re-read its last chunk and row)
+  u32x4 v[EW_CH];
+  auto load = [&](int cb) {
+    const int nch = min(EW_CH, cpr - cb);
+#pragma unroll
+    for (int k = 0; k < EW_CH; ++k) {
+      const int q = tid + EW_ROWS * k;
+      const int r = q / EW_CH, c = q % EW_CH;
+      v[k] = src[(int64_t)min(r, nrows - 1) * cpr + cb + min(c, nch - 1)];
+    }
+  };
+  double acc = 0.0;
+  load(0);
+  for (int pass = 0; pass < npass; ++pass) {
+    const int cb = pass * EW_CH, nch = min(EW_CH, cpr - cb);
+    if (pass > 0) __syncthreads();   // every row of the previous slice has been summed
+#pragma unroll
+    for (int k = 0; k < EW_CH; ++k) {
+      const int q = tid + EW_ROWS * k;
+      const int r = q / EW_CH, c = q % EW_CH;
+      if (c < nch) rows[r * (EW_CH + 1) + c] = v[k];
+    }
+    __syncthreads();
+    if (pass + 1 < npass) load(cb + EW_CH);
+    const u32x4* rw = rows + tid * (EW_CH + 1);
+    if (nch == EW_CH) {
+#pragma unroll
+      for (int c = 0; c < EW_CH; ++c) acc = energy_chunk<T>(rw[c], acc);
+    } else {
+      for (int c = 0; c < nch; ++c) acc = energy_chunk<T>(rw[c], acc);
+    }
+  }
+  unsigned long long lo = ~0ull, hi = 0ull;
+  if (tid < nrows) {
+    e[(int64_t)xi * mn + r0 + tid] = acc;
+    lo = hi = (unsigned long long)__double_as_longlong(acc);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const unsigned long long ol = __shfl_xor(lo, off, 64), oh = __shfl_xor(hi, off, 64);
+    lo = ol < lo ? ol : lo;
+    hi = oh > hi ? oh : hi;
+  }
+  const int w = tid >> 6;
+  if ((tid & 63) == 0 && 64 * w < nrows) {
+    unsigned long long* r = range + 2 * ((int64_t)xi * ((mn + 63) >> 6) + (r0 >> 6) + w);
+    r[0] = lo;
+    r[1] = hi;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_energy_wide(const T* __restrict__ X, int64_t x_stride, int mn, int C,
+                                                     double* __restrict__ e, unsigned long long* __restrict__ range) {
+  energy_block_wide<T>(X, x_stride, mn, C, e, range, blockIdx.x, blockIdx.y);
+}
+
 template <typename T, bool QP = false>
 __global__ __launch_bounds__(256) void k_energy(const T* __restrict__ X, int64_t x_stride, int mn,
                                                  int C, double* __restrict__ e,
@@ -1083,13 +1162,16 @@ __global__ __launch_bounds__(SEL_THREADS) void k_select(Rs3SelectArgs a) {
 // the masks and the tracker state, the energies only on X, so the prior
 // blocks (after the energy blocks) run beside them and leave the group's
 // prior rows [m][W] in prior_bits for the selection.
-template <typename T, bool QP = false>
+template <typename T, bool QP = false, bool WIDE = false>
 __global__ __launch_bounds__(256) void k_energy_prior(const T* __restrict__ X, int64_t x_stride, int mn, int C,
                                                       double* __restrict__ e, unsigned long long* __restrict__ range,
                                                       Rs3SelectArgs a, int nbx, int n_e, Rs3QProjArgs qp) {
   const int b = blockIdx.x;
   if (b < n_e) {
-    energy_block<T, QP>(X, x_stride, mn, C, e, range, b % nbx, b / nbx, nbx, &qp);
+    if constexpr (WIDE)
+      energy_block_wide<T>(X, x_stride, mn, C, e, range, b % nbx, b / nbx);
+    else
+      energy_block<T, QP>(X, x_stride, mn, C, e, range, b % nbx, b / nbx, nbx, &qp);
     return;
   }
   const int g = b - n_e, tid = threadIdx.x;
@@ -1118,10 +1200,25 @@ static bool qproj_ok(int C, int dtype, const Rs3QProjArgs* qp) {
   return qp && dtype == RS3_BF16 && C == 8 * EB_CH;
 }
 
+// The wide form when it still gives a launch of at least 256 blocks.
+static bool energy_wide(int n_x, int mn, const Rs3QProjArgs* qp) {
+  return !qp && (int64_t)n_x * ((mn + EW_ROWS - 1) / EW_ROWS) >= 256;
+}
+
 hipError_t rs3_launch_energy(const void* X, int64_t x_stride, int n_x, int mn, int C, int dtype,
                              double* e, unsigned long long* range, hipStream_t st, const Rs3QProjArgs* qp) {
   dim3 grid((mn + 63) / 64, n_x);
   if (qp && !qproj_ok(C, dtype, qp)) return hipErrorInvalidValue;
+  if (energy_wide(n_x, mn, qp)) {
+    const dim3 gw((mn + EW_ROWS - 1) / EW_ROWS, n_x);
+    if (dtype == RS3_BF16)
+      RS3_LAUNCH(RS3_K_ENERGY, st, k_energy_wide<bf16_t>, gw, dim3(256), 0, st, (const bf16_t*)X, x_stride, mn, C, e,
+                 range);
+    else
+      RS3_LAUNCH(RS3_K_ENERGY, st, k_energy_wide<float>, gw, dim3(256), 0, st, (const float*)X, x_stride, mn, C, e,
+                 range);
+    return hipGetLastError();
+  }
   const Rs3QProjArgs q = qp ? *qp : Rs3QProjArgs{};
   if (qp)
     RS3_LAUNCH(RS3_K_ENERGY, st, (k_energy<bf16_t, true>), grid, dim3(256), 0, st, (const bf16_t*)X, x_stride, mn, C,
@@ -1140,10 +1237,21 @@ bool rs3_select_prior_beside(int m, int n, int s) { return m <= 64 && s == 1 && 
 hipError_t rs3_launch_energy_prior(const void* X, int64_t x_stride, int n_x, int mn, int C, int dtype, double* e,
                                    unsigned long long* range, const Rs3SelectArgs& a, int n_groups, hipStream_t st,
                                    const Rs3QProjArgs* qp) {
-  const int nbx = (mn + 63) / 64, n_e = nbx * n_x;
-  const dim3 grid(n_e + n_groups);
   if (qp && !qproj_ok(C, dtype, qp)) return hipErrorInvalidValue;
   const Rs3QProjArgs q = qp ? *qp : Rs3QProjArgs{};
+  if (energy_wide(n_x, mn, qp)) {
+    const int nbw = (mn + EW_ROWS - 1) / EW_ROWS, n_w = nbw * n_x;
+    const dim3 gw(n_w + n_groups);
+    if (dtype == RS3_BF16)
+      RS3_LAUNCH(RS3_K_ENERGY, st, (k_energy_prior<bf16_t, false, true>), gw, dim3(256), 0, st, (const bf16_t*)X,
+                 x_stride, mn, C, e, range, a, nbw, n_w, q);
+    else
+      RS3_LAUNCH(RS3_K_ENERGY, st, (k_energy_prior<float, false, true>), gw, dim3(256), 0, st, (const float*)X,
+                 x_stride, mn, C, e, range, a, nbw, n_w, q);
+    return hipGetLastError();
+  }
+  const int nbx = (mn + 63) / 64, n_e = nbx * n_x;
+  const dim3 grid(n_e + n_groups);
   if (qp)
     RS3_LAUNCH(RS3_K_ENERGY, st, (k_energy_prior<bf16_t, true>), grid, dim3(256), 0, st, (const bf16_t*)X, x_stride,
                mn, C, e, range, a, nbx, n_e, q);

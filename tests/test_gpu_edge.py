@@ -8,7 +8,7 @@ import numpy as np
 import pytest
 
 from harness import OraclePipeline, compare_bank
-from workloads import CONFIGS, make_weights, to_storage
+from workloads import CONFIGS, make_weights, storage_to_f64, to_storage
 import oracle
 
 pytestmark = pytest.mark.gpu
@@ -190,3 +190,49 @@ def test_wide_grid_multiword_rows():
     masks = (rng.random((1, cfg.m, cfg.n)) < 0.004).astype(np.uint8)
     masks[0, 7, 63] = masks[0, 7, 64] = masks[0, 30, 127] = masks[0, 2, 199] = masks[0, 39, 0] = 1
     _check_select(sess, orc, masks, X, [2000])
+
+
+# (grid rows, grid columns, channels, objects, dtype): each call takes the
+# wide energy form (at least 256 blocks of 256 rows): fp32 rows of 72
+# channels (18 chunks: a short last column slice) on 4,100-cell grids (a
+# short last row block) through the energy launch without the prior; 64x64
+# bf16 grids of 64 channels through the launch with the prior beside; and
+# the batch shape of 64 grids of 64x64 x 256 channels (four slices).
+WIDE_ENERGY = {
+    "f32_c72_100x41_obj64": (100, 41, 72, 64, "f32"),
+    "bf16_c64_64x64_obj16": (64, 64, 64, 16, "bf16"),
+    "bf16_c256_64x64_obj64": (64, 64, 256, 64, "bf16"),
+}
+
+
+@pytest.mark.parametrize("case", sorted(WIDE_ENERGY))
+def test_energy_wide_batches(case):
+    """Energies (Eq. 4) of large batches, bit-exact: the fp64 sums and the
+    per-64-cell minimum/maximum words in the selection workspace, the
+    selected lists, priors and tracker states of two frames."""
+    m, n, C, nobj, dt = WIDE_ENERGY[case]
+    cfg = replace(SMALL, m=m, n=n, C=C, d_h=C, n_obj=nobj, shared_x=False, union_objects=False, dtype=dt,
+                  cap_frames=1, f_max=2)
+    W = make_weights(cfg)
+    sess, orc = _session(cfg, W), OraclePipeline(cfg, W)
+    rng = np.random.default_rng(17)
+    mn = cfg.mn
+    nb = (mn + 63) // 64
+    for frame in range(2):
+        X = to_storage(rng.standard_normal((nobj, mn, C)).astype(np.float32), dt)
+        masks = (rng.random((nobj, m, n)) < 0.01).astype(np.uint8)
+        k = [int(x) for x in rng.integers(1, mn // 3, nobj)]
+        _check_select(sess, orc, masks, X, k)
+        ws = _host(sess.ws_sel)
+        e = ws[:nobj * mn * 8].view(np.float64).reshape(nobj, mn)
+        r0 = (nobj * mn * 8 + 255) // 256 * 256
+        rng_words = ws[r0:r0 + nobj * nb * 16].view(np.uint64).reshape(nobj, nb, 2)
+        Xf = storage_to_f64(X, dt)
+        for o in range(nobj):
+            eo = oracle.energy(Xf[o])
+            assert np.array_equal(e[o].view(np.uint64), eo.view(np.uint64)), (case, frame, o)
+            bits = np.zeros(nb * 64, np.uint64)
+            bits[:mn] = eo.view(np.uint64)
+            lo = np.where(np.arange(nb * 64) < mn, bits, np.uint64(~np.uint64(0))).reshape(nb, 64).min(axis=1)
+            hi = bits.reshape(nb, 64).max(axis=1)
+            assert np.array_equal(rng_words[o, :, 0], lo) and np.array_equal(rng_words[o, :, 1], hi), (case, o)
