@@ -430,6 +430,7 @@ def gpu_run(args):
             "hip_graph": graph,
             "fixed_write_keepset": fixed,
             "copy_bandwidth": copy_bandwidth() if args.copy_bw else None,
+            "read_bandwidth": read_bandwidth() if args.copy_bw else None,
         },
     }
     return out
@@ -831,6 +832,33 @@ def run_workload(cfg, *, absorb, steps, warmup, commit=True, prefill=None, split
     }
 
 
+def read_bandwidth(mib: int = 512, reps: int = 10):
+    """Rate of the library's read-only streaming kernel (rs3_stream_read: 16-byte
+    loads, xor-reduced per thread) over `mib` MiB, larger than the 256 MB
+    Infinity Cache: the reference for kernels that mostly read (the energies
+    read every grid row once).  Returns GB/s of bytes read."""
+    import torch
+    import paper_2608_22526_amd as rs3
+    nb = mib << 20
+    src = torch.ones(nb // 4, dtype=torch.int32, device="cuda")
+    out = torch.empty(rs3.RS3_STREAM_READ_THREADS, dtype=torch.int32, device="cuda")
+    rs3.stream_read(src, nb, out)
+    torch.cuda.synchronize()
+    ev = made_events(torch, 2, timing=True)
+    ev[0].record()
+    for _ in range(reps):
+        rs3.stream_read(src, nb, out)
+    ev[1].record()
+    torch.cuda.synchronize()
+    s_per = ev[0].elapsed_time(ev[1]) / 1000.0 / reps
+    # every word is 1: each thread xors an even or odd number of them
+    x = out.cpu().numpy()
+    ok = bool(((x == 0) | (x == 1)).all())
+    return {"GB_s": nb / s_per / 1e9, "bytes_read": float(nb), "us_per_read": s_per * 1e6, "result_ok": ok,
+            "kernel": "rs3_stream_read (16-byte loads, four in flight per thread, %d threads)"
+                      % rs3.RS3_STREAM_READ_THREADS}
+
+
 def copy_bandwidth(mib: int = 512, reps: int = 10):
     """Bandwidth of the library's own grid copy kernel (the out-of-place
     readout's X -> Y copy: a readout with no selected row launches only that
@@ -961,6 +989,8 @@ def report(args):
     # their own, with the library's copy kernel as the bandwidth reference
     out["copy_bandwidth"] = copy_bandwidth()
     print("copy kernel: %.0f GB/s" % out["copy_bandwidth"]["GB_s"], flush=True)
+    out["read_bandwidth"] = read_bandwidth()
+    print("read-only stream: %.0f GB/s" % out["read_bandwidth"]["GB_s"], flush=True)
     for B in (1, 8, 64, 512):
         cfg = replace(base, n_obj=B, shared_x=False, union_objects=False) if B > 1 else CONFIGS["sam2_single"]
         r = run_workload(cfg, absorb=True, steps=max(3, args.steps // 8) if B > 8 else args.steps, warmup=2 if B > 8

@@ -500,6 +500,18 @@ rs3_status rs3_profile_enable(int32_t on, int32_t max_launches);
 rs3_status rs3_profile_report(double* total_ms, int64_t* launches, int64_t* dropped);
 rs3_status rs3_profile_reset(void);
 
+/* ---- read-only streaming rate (measurement) --------------------------------
+ * Not part of the method: the reference that read-bound kernels (the
+ * energies read each grid row once) are measured against, since a copy
+ * kernel's rate counts reads and writes together.  Reads `bytes` bytes of
+ * device memory at `src` once with 16-byte loads over RS3_STREAM_READ_THREADS
+ * threads (grid-stride, four loads in flight per thread) and writes, for
+ * thread i, the xor of every 32-bit word it read to out[i] (device, uint32,
+ * RS3_STREAM_READ_THREADS entries).  src and bytes must be multiples of 16
+ * (RS3_E_INVALID otherwise); nothing is allocated; enqueued on `stream`. */
+#define RS3_STREAM_READ_THREADS (1024 * 256)
+rs3_status rs3_stream_read(const void* src, size_t bytes, uint32_t* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

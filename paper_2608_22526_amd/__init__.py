@@ -12,5 +12,5 @@ from ._binding import (  # noqa: F401
     select_workspace_size, select_queries,
     readout_workspace_size, readout, readout_noalloc, commit, frame_workspace_size, frame, readout_commit, write_keepset, close_workspace_size, close_masks,
     attend_workspace_size, attend,
-    KERNEL_NAMES, profile_enable, profile_reset, profile_report,
+    KERNEL_NAMES, profile_enable, profile_reset, profile_report, RS3_STREAM_READ_THREADS, stream_read,
 )

@@ -99,7 +99,10 @@ _SIGS = {
     "rs3_profile_enable": (c_i32, [c_i32, c_i32]),
     "rs3_profile_report": (c_i32, [c_vp, c_vp, c_vp]),
     "rs3_profile_reset": (c_i32, []),
+    "rs3_stream_read": (c_i32, [c_vp, c_sz, c_vp, c_vp]),
 }
+
+RS3_STREAM_READ_THREADS = 1024 * 256
 
 KERNEL_NAMES = ["energy", "select", "commit", "commit_append", "copy", "qproj", "attn", "combine",
                 "readout_f32", "merge_commit", "stack_gemm", "stack_merge", "stack_mlp", "stack_rows"]
@@ -424,6 +427,12 @@ def profile_enable(on: bool, max_launches: int = 65536):
 
 def profile_reset():
     _check(lib().rs3_profile_reset(), "rs3_profile_reset")
+
+
+def stream_read(src, nbytes: int, out, stream=None):
+    """rs3_stream_read: reads nbytes of device memory at src once; out
+    (RS3_STREAM_READ_THREADS uint32) receives one xor word per thread."""
+    _check(lib().rs3_stream_read(_ptr(src), nbytes, _ptr(out), _stream(stream)), "rs3_stream_read")
 
 
 def profile_report() -> dict:

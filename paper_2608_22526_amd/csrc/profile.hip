@@ -9,6 +9,29 @@
 
 namespace {
 
+using rs3::u32x4;
+
+// Read-only stream: grid-stride 16-byte loads, four in flight per thread,
+// xor-reduced to one word per thread.
+__global__ __launch_bounds__(256) void k_stream_read(const u32x4* __restrict__ src, size_t n16,
+                                                     uint32_t* __restrict__ out) {
+  const size_t tid = (size_t)blockIdx.x * 256 + threadIdx.x, nth = (size_t)gridDim.x * 256;
+  uint32_t x = 0;
+  size_t i = tid;
+  for (; i + 3 * nth < n16; i += 4 * nth) {
+    u32x4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = src[i + u * nth];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) x ^= v[u][0] ^ v[u][1] ^ v[u][2] ^ v[u][3];
+  }
+  for (; i < n16; i += nth) {
+    const u32x4 v = src[i];
+    x ^= v[0] ^ v[1] ^ v[2] ^ v[3];
+  }
+  out[tid] = x;
+}
+
 struct Rec {
   int id;
   int ev;  // index of the start event; ev+1 is the stop event
@@ -82,6 +105,14 @@ rs3_status rs3_profile_report(double* total_ms, int64_t* launches, int64_t* drop
   }
   if (dropped) *dropped = P.dropped;
   return RS3_OK;
+}
+
+rs3_status rs3_stream_read(const void* src, size_t bytes, uint32_t* out, void* stream) {
+  if (!src || !out || ((uintptr_t)src & 15u) || (bytes & 15u)) return RS3_E_INVALID;
+  const hipStream_t st = (hipStream_t)stream;
+  hipLaunchKernelGGL(k_stream_read, dim3(RS3_STREAM_READ_THREADS / 256), dim3(256), 0, st, (const u32x4*)src,
+                     bytes / 16, out);
+  return hipGetLastError() == hipSuccess ? RS3_OK : RS3_E_DEVICE;
 }
 
 rs3_status rs3_profile_reset(void) {
