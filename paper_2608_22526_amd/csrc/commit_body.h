@@ -511,6 +511,9 @@ __device__ __forceinline__ void commit_block(const Rs3CommitArgs& a, int o, int 
   __shared__ int spos[64];
   const int tid = threadIdx.x;
   const BankDev& b = *a.banks[o];
+  // the descriptor words the placement needs, in one batch of loads (each
+  // read behind a branch would otherwise wait for the one before)
+  asm volatile("" ::"s"(b.f_max), "s"(b.frames), "s"(b.hdr), "s"(b.cap), "s"(b.n_pin), "s"(b.pos));
   const int p = (int)((a.parity >> o) & 1);   // current copy of the frame state
   const int m = a.m, n = a.n, s = a.s, mn = m * n, W = n * s;
   const uint8_t* M = a.masks + (int64_t)o * (m * s) * W;

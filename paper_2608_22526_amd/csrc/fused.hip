@@ -15,9 +15,19 @@
 
 namespace rs3 {
 
+// The argument block is memory the host wrote just before the launch: every
+// argument that either kind of block reads before its first data load, and
+// the first entries of the bank tables (the table lines of one-object
+// launches), are loaded in one batch at the start (one memory round trip),
+// so that the later loads behind the block-kind test and the table index
+// find them in the scalar cache.
 template <typename OutT, bool BF16>
 __global__ __launch_bounds__(CP_THREADS) void k_merge_commit(Rs3ReadoutArgs ra, Rs3CommitArgs ca, int n_cb) {
   extern __shared__ __attribute__((aligned(16))) uint8_t dyn[];
+  asm volatile("" ::"s"(n_cb), "s"(ra.n_obj), "s"(ra.D), "s"(ra.max_sel), "s"(ra.sel_idx), "s"(ra.sel_stride),
+               "s"(ra.X), "s"(ra.x_stride), "s"(ra.WoT), "s"(ra.sel_count), "s"(ra.S), "s"(ra.C),
+               "s"(ca.n_obj), "s"(ca.masks), "s"(ca.m), "s"(ca.n), "s"(ca.s), "s"(ca.parity), "s"(ca.t),
+               "s"(ca.fall_min), "s"(ca.fall_max), "s"(ca.banks[0]), "s"(ra.banks[0]));
   const int b = blockIdx.x;
   if (b < n_cb) {
     if (threadIdx.x >= CB_THREADS) return;
@@ -44,12 +54,12 @@ hipError_t rs3_fused_setup() {
     const size_t b = merge_commit_lds(D, 256);
     if (b > max_lds) max_lds = b;
   }
-  hipError_t e = hipFuncSetAttribute((const void*)k_merge_commit<bf16_t, true>,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)max_lds);
-  if (e == hipSuccess)
-    e = hipFuncSetAttribute((const void*)k_merge_commit<float, true>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)max_lds);
-  return e;
+  const void* fs[] = {(const void*)k_merge_commit<bf16_t, true>, (const void*)k_merge_commit<float, true>};
+  for (const void* f : fs) {
+    hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)max_lds);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 // Work-groups of the fused launch beyond which the merge and the commit run
@@ -70,11 +80,10 @@ hipError_t rs3_launch_merge_commit(const Rs3ReadoutArgs& ra, const Rs3CommitArgs
     return e == hipSuccess ? rs3_launch_commit(ca, RS3_BF16, d_kv, 0, 0, 0, st) : e;
   }
   const size_t lds = merge_commit_lds(ra.D, d_kv);
+  const dim3 grid(n_cb + n_cp), blk(CP_THREADS);
   if (ra.y_fp32)
-    RS3_LAUNCH(RS3_K_MERGE_COMMIT, st, (k_merge_commit<float, true>), dim3(n_cb + n_cp), dim3(CP_THREADS), lds, st,
-               ra, c, n_cb);
+    RS3_LAUNCH(RS3_K_MERGE_COMMIT, st, (k_merge_commit<float, true>), grid, blk, lds, st, ra, c, n_cb);
   else
-    RS3_LAUNCH(RS3_K_MERGE_COMMIT, st, (k_merge_commit<bf16_t, true>), dim3(n_cb + n_cp), dim3(CP_THREADS), lds, st,
-               ra, c, n_cb);
+    RS3_LAUNCH(RS3_K_MERGE_COMMIT, st, (k_merge_commit<bf16_t, true>), grid, blk, lds, st, ra, c, n_cb);
   return hipGetLastError();
 }

@@ -922,19 +922,47 @@ static_assert(G2Lds::BYTES <= 160 * 1024, "one CU's LDS");
 
 // QPRE (rs3_frame): the queries of every cell were projected by the energy
 // launch (a.Qall); each lane gathers its query's projected row instead, and
-// the projection steps 2-3 fall away.
-template <bool QPRE>
+// the projection steps 2-3 fall away.  ONE: a one-object launch (o = 0), so
+// the bank table entries are at fixed offsets and join the first batch of
+// argument loads.
+template <bool QPRE, bool ONE>
 __global__ __launch_bounds__(512) void k_attn_g2(Rs3ReadoutArgs a, int G, Rs3AttnBanks ab) {
   constexpr int DH = G2_DH, NT = 512;
   using L = AttnLds<DH>;
   extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];   // G2Lds::BYTES
+  // 0. the arguments of the prologue in one batch of scalar loads: the
+  //    argument block is memory the host wrote just before the launch, so
+  //    each batch that waits on an earlier one (a value tested by a branch,
+  //    an index into a table) costs a memory round trip before the first
+  //    data load
+  int n_qt = a.n_qt, S = a.S, Harg = a.H, Gv = G, max_sel = a.max_sel, sel_stride = a.sel_stride, mn = a.mn;
+  const int32_t* sel_idx = a.sel_idx;
+  const int32_t* sel_count = a.sel_count;
+  const void* Qall = a.Qall;
+  int64_t qall_stride = a.qall_stride;
+  const TileEnt* tiles0 = ab.tiles[0];
+  const int32_t* hdr0 = ab.hdr[0];
+  const void* kh0 = ab.kh[0];
+  const void* vh0 = ab.vh[0];
+  int ntcap0 = ab.ntcap[0];
+  const void* WqT = a.WqT;
+  const void* Xarg = a.X;
+  int64_t x_stride = a.x_stride;
+  int y_fp32 = a.y_fp32;
+  // (one asm statement: each asm is a scheduling barrier, so separate ones
+  // would split the batch; the table entries are read whatever ONE says.
+  // y_fp32 shares a four-dword load with n_qt: held here, its register is
+  // not reused by a later load of the batch, which would wait for the first)
+  asm volatile(""
+               : "+s"(n_qt), "+s"(S), "+s"(Harg), "+s"(Gv), "+s"(max_sel), "+s"(sel_stride), "+s"(mn),
+                 "+s"(sel_idx), "+s"(sel_count), "+s"(Qall), "+s"(qall_stride), "+s"(WqT), "+s"(Xarg),
+                 "+s"(x_stride), "+s"(tiles0), "+s"(hdr0), "+s"(kh0), "+s"(vh0), "+s"(ntcap0), "+s"(y_fp32));
   const int bid = blockIdx.x;
   const int rest = bid >> 3;
-  const int qt = rest % a.n_qt;
-  const int kvg = (rest / a.n_qt) * 8 + (bid & 7);
-  if (kvg >= G) return;
-  const int S = a.S;
-  const int s = kvg % S, oh = kvg / S, h = oh % a.H, o = oh / a.H;
+  const int qt = rest % n_qt;
+  const int kvg = (rest / n_qt) * 8 + (bid & 7);
+  if (kvg >= Gv) return;
+  const int s = kvg % S, oh = kvg / S, h = oh % Harg, o = ONE ? 0 : oh / Harg;
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5;
   const int wave_all = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wave = wave_all & 3;    // the wave's 32 queries: rows 32*wave of the tile
@@ -950,18 +978,18 @@ __global__ __launch_bounds__(512) void k_attn_g2(Rs3ReadoutArgs a, int G, Rs3Att
   const int lt = tid & 255, hchunk = G2_HC * grp + (lt & 15);
   int src[NX];
   u32x4 wreg[NW];
-  const int32_t* sel = a.sel_idx + (int64_t)o * a.sel_stride;
+  const int32_t* sel = sel_idx + (int64_t)o * sel_stride;
   if constexpr (QPRE) {
-    src[0] = gload(sel + min(qrow, a.max_sel - 1));   // this lane's query cell
+    src[0] = gload(sel + min(qrow, max_sel - 1));   // this lane's query cell
   } else {
 #pragma unroll
-    for (int i = 0; i < NX; ++i) src[i] = gload(sel + min(row0 + (lt >> 4) + 16 * i, a.max_sel - 1));
-    const u32x4* wb = (const u32x4*)((const bf16_t*)a.WqT + (int64_t)h * DH * PJ_PC * 8) + hchunk;
+    for (int i = 0; i < NX; ++i) src[i] = gload(sel + min(row0 + (lt >> 4) + 16 * i, max_sel - 1));
+    const u32x4* wb = (const u32x4*)((const bf16_t*)WqT + (int64_t)h * DH * PJ_PC * 8) + hchunk;
 #pragma unroll
     for (int j = 0; j < NW; ++j) wreg[j] = gload(wb + ((lt >> 4) + 16 * j) * PJ_PC);
   }
-  const TileEnt* tiles = ab.tiles[o];
-  const int ntcap = ab.ntcap[o];
+  const TileEnt* tiles = ONE ? tiles0 : ab.tiles[o];
+  const int ntcap = ONE ? ntcap0 : ab.ntcap[o];
   int c_tile;
   uint32_t c_mlo, c_mhi;
   {
@@ -972,9 +1000,9 @@ __global__ __launch_bounds__(512) void k_attn_g2(Rs3ReadoutArgs a, int G, Rs3Att
     c_mlo = (uint32_t)m;
     c_mhi = (uint32_t)(m >> 32);
   }
-  const int ntiles = sload(ab.hdr[o] + HDR_NTILES);
-  int cnt = sload(a.sel_count + (a.sel_stride ? o : 0));   // out of range: reported by the merge
-  cnt = cnt < 0 ? 0 : min(cnt, a.max_sel);
+  const int ntiles = sload((ONE ? hdr0 : ab.hdr[o]) + HDR_NTILES);
+  int cnt = sload(sel_count + (sel_stride ? o : 0));   // out of range: reported by the merge
+  cnt = cnt < 0 ? 0 : min(cnt, max_sel);
   auto keep_loads = [&]() {
 #pragma unroll
     for (int i = 0; i < NX; ++i) keep(src[i]);
@@ -994,10 +1022,10 @@ __global__ __launch_bounds__(512) void k_attn_g2(Rs3ReadoutArgs a, int G, Rs3Att
   //    their rows)
   u32x4 xv[NX];
   if constexpr (!QPRE) {
-    const bf16_t* X = (const bf16_t*)a.X + (int64_t)o * a.x_stride;
+    const bf16_t* X = (const bf16_t*)Xarg + (int64_t)o * x_stride;
 #pragma unroll
     for (int i = 0; i < NX; ++i) {
-      const int r = (src[i] < 0 || src[i] >= a.mn) ? 0 : src[i];
+      const int r = (src[i] < 0 || src[i] >= mn) ? 0 : src[i];
       xv[i] = gload((const u32x4*)(X + (int64_t)r * PJ_PC * 8) + hchunk);
     }
   }
@@ -1010,7 +1038,7 @@ __global__ __launch_bounds__(512) void k_attn_g2(Rs3ReadoutArgs a, int G, Rs3Att
     }
     // the empty partial (m = -inf, l = 0), so that the merge reads every split
     if (g == 0 && grp == 0 && qrow < cnt) {
-      float* ml = a.ML + ((((int64_t)o * S + s) * a.max_sel + qrow) * a.H + h) * 2;
+      float* ml = a.ML + ((((int64_t)o * S + s) * max_sel + qrow) * Harg + h) * 2;
       ml[0] = -INFINITY;
       ml[1] = 0.f;
     }
@@ -1020,9 +1048,9 @@ __global__ __launch_bounds__(512) void k_attn_g2(Rs3ReadoutArgs a, int G, Rs3Att
   const int nh = 2 * nts;   // half tiles, visited from an offset that depends on the query tile
   const int rot = nts <= 64 ? ((qt & 7) * nh) >> 3 : 0;
   auto half_at = [&](int i) { int v = i + rot; return v >= nh ? v - nh : v; };
-  const bf16_t* Kh = (const bf16_t*)ab.kh[o];
-  const bf16_t* Vh = (const bf16_t*)ab.vh[o];
-  const int H = a.H;
+  const bf16_t* Kh = (const bf16_t*)(ONE ? kh0 : ab.kh[o]);
+  const bf16_t* Vh = (const bf16_t*)(ONE ? vh0 : ab.vh[o]);
+  const int H = Harg;
   const AttnDmaOffsets<DH> doff = attn_dma_offsets<DH>(wave, lane);
   int cbase = 0;   // local tile of lane 0's cached entry
   const int npair = nts;   // pairs of half tiles (nh is even)
@@ -1059,8 +1087,8 @@ __global__ __launch_bounds__(512) void k_attn_g2(Rs3ReadoutArgs a, int G, Rs3Att
       const int tl = __builtin_amdgcn_readlane(c_tile, v >> 1);
       attn_issue<DH>(Kh, Vh, tl, v & 1, h, H, lds + (2 * grp + k) * L::STAGE, wave, doff);
     }
-    const int cell = (src[0] < 0 || src[0] >= a.mn) ? 0 : src[0];
-    const bf16_t* qp = (const bf16_t*)a.Qall + (int64_t)o * a.qall_stride + (int64_t)cell * DH + 8 * g;
+    const int cell = (src[0] < 0 || src[0] >= mn) ? 0 : src[0];
+    const bf16_t* qp = (const bf16_t*)Qall + (int64_t)o * qall_stride + (int64_t)cell * DH + 8 * g;
 #pragma unroll
     for (int ks = 0; ks < DH / 16; ++ks) qreg[ks] = gload((const u32x4*)(qp + 16 * ks));
     // both in: the loop's first wait then finds nothing outstanding, and the
@@ -1310,7 +1338,7 @@ __global__ __launch_bounds__(512) void k_attn_g2(Rs3ReadoutArgs a, int G, Rs3Att
       *(u32x2*)(ow + (lane & 31) * OP + d * 2) = w;
     }
   if (g == 0 && qv) {
-    float* ml = a.ML + ((((int64_t)o * S + s) * a.max_sel + qrow) * a.H + h) * 2;
+    float* ml = a.ML + ((((int64_t)o * S + s) * max_sel + qrow) * H + h) * 2;
     pstore(ml, m_run);
     pstore(ml + 1, l_tot);
   }
@@ -1612,10 +1640,15 @@ hipError_t rs3_launch_attn(const Rs3ReadoutArgs& a, const Rs3AttnBanks& ab, hipS
       return deep ? launch_attn_dh<32, false, true>(a, G, nblk, st) : launch_attn_dh<32, false, false>(a, G, nblk, st);
     case 64:
       if (project) {
-        if (a.Qall)
-          RS3_LAUNCH(RS3_K_ATTN, st, k_attn_g2<true>, dim3(nblk), dim3(512), 8 * G2Lds::STAGE, st, a, G, ab);
+        const bool one = a.n_obj == 1;
+        if (a.Qall && one)
+          RS3_LAUNCH(RS3_K_ATTN, st, (k_attn_g2<true, true>), dim3(nblk), dim3(512), 8 * G2Lds::STAGE, st, a, G, ab);
+        else if (a.Qall)
+          RS3_LAUNCH(RS3_K_ATTN, st, (k_attn_g2<true, false>), dim3(nblk), dim3(512), 8 * G2Lds::STAGE, st, a, G, ab);
+        else if (one)
+          RS3_LAUNCH(RS3_K_ATTN, st, (k_attn_g2<false, true>), dim3(nblk), dim3(512), G2Lds::BYTES, st, a, G, ab);
         else
-          RS3_LAUNCH(RS3_K_ATTN, st, k_attn_g2<false>, dim3(nblk), dim3(512), G2Lds::BYTES, st, a, G, ab);
+          RS3_LAUNCH(RS3_K_ATTN, st, (k_attn_g2<false, false>), dim3(nblk), dim3(512), G2Lds::BYTES, st, a, G, ab);
         return hipGetLastError();
       }
       return deep ? launch_attn_dh<64, false, true>(a, G, nblk, st) : launch_attn_dh<64, false, false>(a, G, nblk, st);
@@ -1700,8 +1733,10 @@ hipError_t rs3_readout_setup() {
               {(const void*)k_attn<32, true, true, 2>, std::max(8 * AttnLds<32>::STAGE, AttnProj<32>::BYTES)},
               {(const void*)k_attn<64, false, false>, 4 * AttnLds<64>::STAGE},
               {(const void*)k_attn<64, false, true>, 8 * AttnLds<64>::STAGE},
-              {(const void*)k_attn_g2<false>, G2Lds::BYTES},
-              {(const void*)k_attn_g2<true>, 8 * G2Lds::STAGE},
+              {(const void*)k_attn_g2<false, false>, G2Lds::BYTES},
+              {(const void*)k_attn_g2<false, true>, G2Lds::BYTES},
+              {(const void*)k_attn_g2<true, false>, 8 * G2Lds::STAGE},
+              {(const void*)k_attn_g2<true, true>, 8 * G2Lds::STAGE},
               {(const void*)k_attn<128, false, false>, 4 * AttnLds<128>::STAGE},
               {(const void*)k_attn<256, false, false>, 4 * AttnLds<256>::STAGE}};
   for (const auto& k : attn) {

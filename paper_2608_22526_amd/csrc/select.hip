@@ -1166,6 +1166,12 @@ template <typename T, bool QP = false, bool WIDE = false>
 __global__ __launch_bounds__(256) void k_energy_prior(const T* __restrict__ X, int64_t x_stride, int mn, int C,
                                                       double* __restrict__ e, unsigned long long* __restrict__ range,
                                                       Rs3SelectArgs a, int nbx, int n_e, Rs3QProjArgs qp) {
+  // the arguments of both kinds of block in one batch of loads: the argument
+  // block is memory the host wrote just before the launch, and loads behind
+  // the block-kind test would wait for the test's own load first
+  asm volatile("" ::"s"(n_e), "s"(nbx), "s"(X), "s"(x_stride), "s"(mn), "s"(C), "s"(e), "s"(range),
+               "s"(qp.WqT), "s"(qp.Qall), "s"(a.n), "s"(a.m), "s"(a.union_objects), "s"(a.n_obj), "s"(a.masks),
+               "s"(a.track), "s"(a.prior_bits));
   const int b = blockIdx.x;
   if (b < n_e) {
     if constexpr (WIDE)
